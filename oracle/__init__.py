@@ -1,0 +1,173 @@
+"""CPU oracle for the exact MPT solver -- TEST INFRASTRUCTURE ONLY.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package. The product path (``libmpt.so`` and its
+binding) never imports, links or runs anything here, and nothing here uses
+the product path.
+
+* :mod:`oracle.mpt_oracle` (C, built into ``libmpt_oracle.so``): W table,
+  exact DP, layout read-off, trie cost and hierarchy cost, written from the
+  paper's definitions (Section 2 Eq. 1, Section 3 Thm 1 Eqs. 2-3, Section 3.1).
+* :mod:`oracle.brute` (pure Python, tiny inputs only): brute force over
+  permutations, over hierarchies and over global orders, vertex cover, and the
+  closed forms of Section 5 -- the pins that check the C oracle.
+
+Input instances come from :mod:`paper_2609_13692_amd.workloads`, which only
+draws numbers; any object with ``n_chunks``, ``weights``, ``req_off``,
+``req_chunks`` works.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "mpt_oracle.c")
+_LIB_PATH = os.path.join(_HERE, "libmpt_oracle.so")
+_lib = None
+
+
+def build() -> str:
+    """Compile the C oracle in place (gcc, OpenMP). Returns the library path."""
+    tmp = _LIB_PATH + ".tmp"
+    subprocess.check_call(["gcc", "-O2", "-std=c11", "-fopenmp", "-shared", "-fPIC",
+                           _SRC, "-o", tmp])
+    os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        build()
+    lib = ctypes.CDLL(_LIB_PATH)
+    P = ctypes.c_void_p
+    i32, i64 = ctypes.c_int, ctypes.c_int64
+    lib.oracle_demand_sets.argtypes = [i32, i64, P, P, P]
+    lib.oracle_intersection_weights.argtypes = [i32, i64, P, P, P, P]
+    lib.oracle_exact_dp.argtypes = [i32, P, P, P, i32]
+    lib.oracle_cost_table.argtypes = [i32, P, P, P]
+    lib.oracle_orders.argtypes = [i32, i64, P, P, P, P]
+    lib.oracle_trie_cost.argtypes = [i32, i64, P, P, P]
+    lib.oracle_trie_cost.restype = i64
+    lib.oracle_hierarchy_cost.argtypes = [i32, i64, P, P, P, P]
+    lib.oracle_hierarchy_cost.restype = i64
+    lib.oracle_max_threads.restype = i32
+    _lib = lib
+    return lib
+
+
+def _p(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+class OracleError(RuntimeError):
+    pass
+
+
+def _check(rc: int, what: str) -> None:
+    if rc < 0:
+        raise OracleError(f"{what} failed with status {rc}")
+
+
+def _arrays(inst):
+    w = np.ascontiguousarray(inst.weights, dtype=np.int64)
+    off = np.ascontiguousarray(inst.req_off, dtype=np.int64)
+    ch = np.ascontiguousarray(inst.req_chunks, dtype=np.int32)
+    if ch.size == 0:
+        ch = np.zeros(1, dtype=np.int32)   # valid pointer for an all-empty family
+    return w, off, ch
+
+
+def max_threads() -> int:
+    return int(_load().oracle_max_threads())
+
+
+def demand_sets(inst) -> np.ndarray:
+    """S_x as uint32 masks, one per chunk (Section 3)."""
+    lib = _load()
+    w, off, ch = _arrays(inst)
+    sx = np.zeros(max(1, inst.n_chunks), dtype=np.uint32)
+    _check(lib.oracle_demand_sets(inst.m, inst.n_chunks, _p(off), _p(ch), _p(sx)), "demand_sets")
+    return sx[:inst.n_chunks]
+
+
+def intersection_weights(inst) -> np.ndarray:
+    """W(B) = w(I(B)) for all 2^m subsets B; I(empty) = U."""
+    lib = _load()
+    w, off, ch = _arrays(inst)
+    W = np.empty(1 << inst.m, dtype=np.int64)
+    _check(lib.oracle_intersection_weights(inst.m, inst.n_chunks, _p(w), _p(off), _p(ch), _p(W)),
+           "intersection_weights")
+    return W
+
+
+def exact_dp(m: int, W: np.ndarray, threads: int = 0) -> tuple[np.ndarray, np.ndarray]:
+    """Savings table M and split table of the Section 3.1 recurrence."""
+    lib = _load()
+    W = np.ascontiguousarray(W, dtype=np.int64)
+    M = np.empty(1 << m, dtype=np.int64)
+    split = np.empty(1 << m, dtype=np.uint32)
+    if threads <= 0:
+        threads = max_threads()
+    _check(lib.oracle_exact_dp(m, _p(W), _p(M), _p(split), threads), "exact_dp")
+    return M, split
+
+
+def cost_table(m: int, W: np.ndarray, M: np.ndarray) -> np.ndarray:
+    """C(B) = sum_{i in B} w(R_i) - M(B) (Eq. 3 applied to each sub-instance)."""
+    lib = _load()
+    C = np.empty(1 << m, dtype=np.int64)
+    _check(lib.oracle_cost_table(m, _p(np.ascontiguousarray(W)), _p(np.ascontiguousarray(M)), _p(C)),
+           "cost_table")
+    return C
+
+
+def orders(inst, split: np.ndarray) -> np.ndarray:
+    """pi_i for every request, CSR with the instance's req_off."""
+    lib = _load()
+    w, off, ch = _arrays(inst)
+    out = np.full(max(1, inst.nnz), -1, dtype=np.int32)
+    sp = np.ascontiguousarray(split, dtype=np.uint32)
+    _check(lib.oracle_orders(inst.m, inst.n_chunks, _p(off), _p(ch), _p(sp), _p(out)), "orders")
+    return out[:inst.nnz]
+
+
+def trie_cost(inst, seqs: np.ndarray) -> int:
+    """Eq. (1) for the layout seqs (CSR with the instance's req_off)."""
+    lib = _load()
+    w, off, _ = _arrays(inst)
+    s = np.ascontiguousarray(seqs, dtype=np.int32)
+    if s.size == 0:
+        s = np.zeros(1, dtype=np.int32)
+    c = int(lib.oracle_trie_cost(inst.m, inst.n_chunks, _p(w), _p(off), _p(s)))
+    _check(c, "trie_cost")
+    return c
+
+
+def hierarchy_cost(inst, split: np.ndarray) -> int:
+    """Eq. (2) for the hierarchy encoded by split: sum_x w(x) t_x(H)."""
+    lib = _load()
+    w, off, ch = _arrays(inst)
+    sp = np.ascontiguousarray(split, dtype=np.uint32)
+    c = int(lib.oracle_hierarchy_cost(inst.m, inst.n_chunks, _p(w), _p(off), _p(ch), _p(sp)))
+    _check(c, "hierarchy_cost")
+    return c
+
+
+def solve(inst, threads: int = 0, with_orders: bool = True) -> dict:
+    """Full oracle run: W, M, C, split, OPT, savings and (optionally) orders."""
+    W = intersection_weights(inst)
+    M, split = exact_dp(inst.m, W, threads)
+    C = cost_table(inst.m, W, M)
+    full = (1 << inst.m) - 1
+    res = {"W": W, "M": M, "C": C, "split": split,
+           "opt": int(C[full]), "savings": int(M[full])}
+    if with_orders:
+        res["orders"] = orders(inst, split)
+    return res
