@@ -1,0 +1,151 @@
+/*
+ * mpt.h -- C ABI of libmpt.so, an exact solver for the Minimum Prefix Trie
+ * with Free Permutations (MPT) problem on AMD Instinct MI355X (gfx950).
+ *
+ * Problem (Section 2 of "Prefix Sharing Is a Sorting Problem"): a universe
+ * of n_chunks chunks with weights w(x) > 0 and m requests R_i (sets of chunk
+ * ids). Choose one permutation pi_i of every R_i so that the trie of the m
+ * resulting sequences has the smallest total weight of non-root nodes
+ * (Eq. 1). By the structure theorem (Theorem 1, Eqs. 2-3) the optimum is
+ *     OPT_free = sum_i w(R_i) - max_H sum_{v internal in H} w(I(v)),
+ * a maximum over binary hierarchies H on the requests, with
+ * I(B) = intersection of R_i over i in B. The solver computes it with the
+ * O(3^m) subset DP of Section 3.1, in cost form:
+ *     C({i}) = w(R_i),
+ *     C(S)   = min over A (+) B = S, A holding the lowest request of S,
+ *              both non-empty, of C(A) + C(B)  -  W(S),     W(S) = w(I(S)),
+ * and reads the orders off the optimal hierarchy top-down (proof of
+ * Theorem 1, "<=" half).
+ *
+ * Conventions shared by every entry point
+ *  - Subsets of requests are m-bit masks: bit i set = request i is in the set.
+ *  - Every array argument is DEVICE memory (HBM) owned by the caller; the
+ *    library allocates nothing and keeps no pointer after a call returns.
+ *  - `stream` is a hipStream_t (NULL = the null stream). All device work of a
+ *    call is enqueued on it. Calls that return a host value synchronise it.
+ *  - `workspace` is caller-owned device scratch of at least
+ *    mpt_workspace_bytes(m, nnz) bytes, 256-byte aligned. Calls that share
+ *    one workspace must not run concurrently.
+ *  - Return value: MPT_OK (0) or a negative mpt_status. On error no output is
+ *    guaranteed to be written; mpt_last_error() describes the failure for
+ *    the calling thread. No C++ exception crosses this interface.
+ *  - Integer ranges: 1 <= m <= MPT_MAX_M; 0 <= n_chunks <= MPT_MAX_CHUNKS;
+ *    1 <= w(x) <= MPT_MAX_CHUNK_WEIGHT; sum_i w(R_i) < 2^61. These keep
+ *    every W, C and pair sum inside int64.
+ */
+#ifndef MPT_H
+#define MPT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MPT_MAX_M 28
+#define MPT_MAX_CHUNKS (1LL << 30)
+#define MPT_MAX_CHUNK_WEIGHT (1LL << 32)
+/* C[0] after mpt_solve_exact: the empty set never takes part in a split. */
+#define MPT_COST_SENTINEL (1LL << 62)
+
+enum mpt_status {
+    MPT_OK = 0,
+    MPT_E_INVALID = -1,   /* bad size, null pointer, or req_off not a CSR offset array */
+    MPT_E_RANGE = -2,     /* a chunk id outside [0, n_chunks) */
+    MPT_E_DUP = -3,       /* a chunk repeated inside one request */
+    MPT_E_WEIGHT = -4,    /* a weight <= 0 or > MPT_MAX_CHUNK_WEIGHT */
+    MPT_E_OVERFLOW = -5,  /* sum_i w(R_i) >= 2^61 */
+    MPT_E_WORKSPACE = -6, /* workspace missing, misaligned or too small */
+    MPT_E_DEVICE = -8     /* HIP runtime error (detail in mpt_last_error) */
+};
+
+/* Bytes of device workspace that every entry point below needs for an
+ * instance with m requests and nnz = req_off[m] request slots. */
+size_t mpt_workspace_bytes(int m, int64_t nnz);
+
+/*
+ * Phase 1 -- intersection weights W(B) = w(I(B)) for all 2^m subsets B
+ * (W(B) is the weight of the chunks shared by every request of B; Section 3,
+ * proof of Theorem 1; I(empty) = U, so W(0) is the total weight of all
+ * chunks). Also returns the demand sets S_x = { i : x in R_i } (Section 3).
+ *
+ *   chunk_w    [n_chunks]  int64 weights w(x)
+ *   req_off    [m+1]       int64 CSR offsets, req_off[0] = 0, non-decreasing,
+ *                          req_off[m] = nnz; request i is
+ *                          req_chunks[req_off[i] .. req_off[i+1])
+ *   req_chunks [nnz]       int32 chunk ids, distinct inside each request;
+ *                          requests may be empty or equal to each other
+ *   sig        [n_chunks]  out: uint32 S_x masks
+ *   W          [2^m]       out: int64 table
+ * Validates the device inputs (MPT_E_INVALID / RANGE / DUP / WEIGHT /
+ * OVERFLOW) and synchronises `stream` to report the result.
+ */
+int mpt_build_weights(int m, int64_t n_chunks, int64_t nnz,
+                      const int64_t *chunk_w, const int64_t *req_off,
+                      const int32_t *req_chunks, uint32_t *sig, int64_t *W,
+                      void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Phase 2 -- the exact DP of Section 3.1 over all 2^m subsets, layer by
+ * layer in |S|.
+ *   W      [2^m]  int64 table from mpt_build_weights
+ *   C      [2^m]  out: C(S) = OPT_free of the sub-instance {R_i : i in S};
+ *                 C[0] = MPT_COST_SENTINEL
+ *   split  [2^m]  out: for |S| >= 2 the optimal part A that holds the lowest
+ *                 request of S; among optimal parts the numerically smallest;
+ *                 0 for |S| <= 1. split encodes the optimal hierarchy: the
+ *                 children of S are split[S] and S ^ split[S].
+ *   opt_cost      HOST out, nullable: C(full set) = OPT_free (Theorem 1).
+ *                 When non-null the call synchronises `stream`.
+ */
+int mpt_solve_exact(int m, const int64_t *W, int64_t *C, uint32_t *split,
+                    int64_t *opt_cost, void *workspace, size_t workspace_bytes,
+                    void *stream);
+
+/*
+ * Phase 3 -- the layout read off the hierarchy (proof of Theorem 1): at node
+ * B of the hierarchy each request below B emits I(B) \ I(parent(B)) in
+ * ascending chunk id, with I(parent(root)) = empty. Chunk x of R_i is thus
+ * emitted at the first node on request i's root-to-leaf path that is a
+ * subset of S_x.
+ *   req_off, req_chunks  the instance (as for mpt_build_weights)
+ *   sig, split           outputs of the two calls above
+ *   order_chunks [nnz]   out: pi_i at order_chunks[req_off[i] .. req_off[i+1])
+ */
+int mpt_extract_orders(int m, int64_t n_chunks, int64_t nnz,
+                       const int64_t *req_off, const int32_t *req_chunks,
+                       const uint32_t *sig, const uint32_t *split,
+                       int32_t *order_chunks, void *workspace,
+                       size_t workspace_bytes, void *stream);
+
+/* Static text for a status code. */
+const char *mpt_status_string(int status);
+
+/* Detail of the calling thread's last failed call ("" if none). */
+const char *mpt_last_error(void);
+
+/*
+ * Diagnostics: per-kernel device time with HIP events recorded on the
+ * caller's stream around every launch. mpt_profile_begin() clears and
+ * enables recording (process-wide); mpt_profile_end() waits for the events,
+ * fills up to max_entries rows, disables recording and returns the number of
+ * distinct kernels seen (or a negative status).
+ *   work: the algorithmic units the launches processed -- evaluated
+ *         bipartitions for the DP kernels, bytes written for the W kernel.
+ */
+typedef struct mpt_profile_row {
+    char kernel[48];
+    int64_t launches;
+    double total_ms;
+    double work;
+} mpt_profile_row;
+
+int mpt_profile_begin(void);
+int mpt_profile_end(mpt_profile_row *rows, int max_entries);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MPT_H */

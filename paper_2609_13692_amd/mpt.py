@@ -1,0 +1,227 @@
+"""ctypes binding of libmpt.so (the C ABI in include/mpt.h).
+
+Argument marshalling only: each function checks tensor dtypes, devices and
+sizes, then passes raw device pointers and the current HIP stream to the
+library. Every step of the computation runs in the library's HIP kernels.
+PyTorch only provides device memory and streams. If libmpt.so is missing
+the binding raises; it never falls back to another implementation.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libmpt.so")
+
+MPT_MAX_M = 28
+MPT_COST_SENTINEL = 1 << 62
+
+_STATUS = {
+    0: "MPT_OK", -1: "MPT_E_INVALID", -2: "MPT_E_RANGE", -3: "MPT_E_DUP",
+    -4: "MPT_E_WEIGHT", -5: "MPT_E_OVERFLOW", -6: "MPT_E_WORKSPACE", -8: "MPT_E_DEVICE",
+}
+EXPORTED = ("mpt_workspace_bytes", "mpt_build_weights", "mpt_solve_exact", "mpt_extract_orders",
+            "mpt_status_string", "mpt_last_error", "mpt_profile_begin", "mpt_profile_end")
+
+
+class MptError(RuntimeError):
+    def __init__(self, status: int, where: str, detail: str):
+        self.status = status
+        self.name = _STATUS.get(status, str(status))
+        super().__init__(f"{where}: {self.name}: {detail}")
+
+
+class ProfileRow(ctypes.Structure):
+    _fields_ = [("kernel", ctypes.c_char * 48), ("launches", ctypes.c_int64),
+                ("total_ms", ctypes.c_double), ("work", ctypes.c_double)]
+
+
+_lib = None
+
+
+def load() -> ctypes.CDLL:
+    """Load libmpt.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                           "(hipcc --offload-arch=gfx950); there is no fallback")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, i32, i64, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_size_t
+    lib.mpt_workspace_bytes.argtypes = [i32, i64]
+    lib.mpt_workspace_bytes.restype = sz
+    lib.mpt_build_weights.argtypes = [i32, i64, i64, P, P, P, P, P, P, sz, P]
+    lib.mpt_build_weights.restype = i32
+    lib.mpt_solve_exact.argtypes = [i32, P, P, P, P, P, sz, P]
+    lib.mpt_solve_exact.restype = i32
+    lib.mpt_extract_orders.argtypes = [i32, i64, i64, P, P, P, P, P, P, sz, P]
+    lib.mpt_extract_orders.restype = i32
+    lib.mpt_status_string.argtypes = [i32]
+    lib.mpt_status_string.restype = ctypes.c_char_p
+    lib.mpt_last_error.argtypes = []
+    lib.mpt_last_error.restype = ctypes.c_char_p
+    lib.mpt_profile_begin.argtypes = []
+    lib.mpt_profile_begin.restype = i32
+    lib.mpt_profile_end.argtypes = [ctypes.POINTER(ProfileRow), i32]
+    lib.mpt_profile_end.restype = i32
+    _lib = lib
+    return lib
+
+
+def _check(rc: int, where: str) -> None:
+    if rc != 0:
+        raise MptError(rc, where, load().mpt_last_error().decode())
+
+
+def _ptr(t: torch.Tensor | None, dtype: torch.dtype, n: int, name: str) -> int | None:
+    if t is None:
+        if n > 0:
+            raise ValueError(f"{name} is required")
+        return None
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if t.numel() < n:
+        raise ValueError(f"{name} has {t.numel()} elements, needs {n}")
+    return t.data_ptr() if t.numel() else None
+
+
+def _stream(stream) -> int | None:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream or None
+
+
+def mpt_workspace_bytes(m: int, nnz: int) -> int:
+    return int(load().mpt_workspace_bytes(m, nnz))
+
+
+def alloc_workspace(m: int, nnz: int, device="cuda") -> torch.Tensor:
+    """A uint8 device tensor big enough (and 256-byte aligned) for all calls."""
+    n = mpt_workspace_bytes(m, nnz)
+    if n == 0:
+        raise MptError(-1, "mpt_workspace_bytes", f"invalid m={m} or nnz={nnz}")
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def mpt_build_weights(m, n_chunks, chunk_w, req_off, req_chunks, sig, W, workspace, stream=None):
+    """W(B) = w(I(B)) for all subsets and S_x per chunk (see include/mpt.h)."""
+    nnz = int(req_chunks.numel()) if req_chunks is not None else 0
+    rc = load().mpt_build_weights(
+        m, n_chunks, nnz,
+        _ptr(chunk_w, torch.int64, n_chunks, "chunk_w"),
+        _ptr(req_off, torch.int64, m + 1, "req_off"),
+        _ptr(req_chunks, torch.int32, nnz, "req_chunks") if nnz else None,
+        _ptr(sig, torch.int32, n_chunks, "sig"),
+        _ptr(W, torch.int64, 1 << m, "W"),
+        _ptr(workspace, torch.uint8, 1, "workspace"), workspace.numel(), _stream(stream))
+    _check(rc, "mpt_build_weights")
+
+
+def mpt_solve_exact(m, W, C, split, workspace, stream=None, want_cost=True):
+    """Section 3.1 DP; returns OPT_free (synchronising) or None."""
+    out = ctypes.c_int64(0)
+    rc = load().mpt_solve_exact(
+        m, _ptr(W, torch.int64, 1 << m, "W"), _ptr(C, torch.int64, 1 << m, "C"),
+        _ptr(split, torch.int32, 1 << m, "split"),
+        ctypes.addressof(out) if want_cost else None,
+        _ptr(workspace, torch.uint8, 1, "workspace"), workspace.numel(), _stream(stream))
+    _check(rc, "mpt_solve_exact")
+    return int(out.value) if want_cost else None
+
+
+def mpt_extract_orders(m, n_chunks, req_off, req_chunks, sig, split, order_chunks, workspace, stream=None):
+    """pi_i for every request into order_chunks (CSR with req_off)."""
+    nnz = int(req_chunks.numel()) if req_chunks is not None else 0
+    rc = load().mpt_extract_orders(
+        m, n_chunks, nnz,
+        _ptr(req_off, torch.int64, m + 1, "req_off"),
+        _ptr(req_chunks, torch.int32, nnz, "req_chunks") if nnz else None,
+        _ptr(sig, torch.int32, n_chunks, "sig") if nnz else None,
+        _ptr(split, torch.int32, 1 << m, "split"),
+        _ptr(order_chunks, torch.int32, nnz, "order_chunks") if nnz else None,
+        _ptr(workspace, torch.uint8, 1, "workspace"), workspace.numel(), _stream(stream))
+    _check(rc, "mpt_extract_orders")
+
+
+def profile_begin() -> None:
+    _check(load().mpt_profile_begin(), "mpt_profile_begin")
+
+
+def profile_end(max_rows: int = 64) -> dict:
+    """{kernel: {"launches", "total_ms", "work"}} for the launches since
+    profile_begin()."""
+    rows = (ProfileRow * max_rows)()
+    n = load().mpt_profile_end(rows, max_rows)
+    if n < 0:
+        _check(n, "mpt_profile_end")
+    return {rows[i].kernel.decode(): {"launches": rows[i].launches, "total_ms": rows[i].total_ms,
+                                      "work": rows[i].work} for i in range(min(n, max_rows))}
+
+
+class Problem:
+    """Device-resident instance plus the output tables of one solve.
+
+    Holds the caller-side allocations (torch tensors) that the C ABI expects:
+    inputs uploaded once, W / C / split / orders / sig outputs, workspace.
+    """
+
+    def __init__(self, inst, device="cuda"):
+        self.m = inst.m
+        self.n_chunks = inst.n_chunks
+        self.nnz = inst.nnz
+        dev = torch.device(device)
+        self.chunk_w = torch.as_tensor(inst.weights, dtype=torch.int64).to(dev)
+        self.req_off = torch.as_tensor(inst.req_off, dtype=torch.int64).to(dev)
+        self.req_chunks = torch.as_tensor(inst.req_chunks, dtype=torch.int32).to(dev)
+        n = 1 << self.m
+        self.sig = torch.empty(max(1, self.n_chunks), dtype=torch.int32, device=dev)
+        self.W = torch.empty(n, dtype=torch.int64, device=dev)
+        self.C = torch.empty(n, dtype=torch.int64, device=dev)
+        self.split = torch.empty(n, dtype=torch.int32, device=dev)
+        self.orders = torch.empty(max(1, self.nnz), dtype=torch.int32, device=dev)
+        self.workspace = alloc_workspace(self.m, self.nnz, dev)
+
+    def build(self, stream=None):
+        mpt_build_weights(self.m, self.n_chunks, self.chunk_w, self.req_off, self.req_chunks,
+                          self.sig, self.W, self.workspace, stream)
+
+    def solve(self, stream=None, want_cost=True):
+        return mpt_solve_exact(self.m, self.W, self.C, self.split, self.workspace, stream, want_cost)
+
+    def extract(self, stream=None):
+        mpt_extract_orders(self.m, self.n_chunks, self.req_off, self.req_chunks, self.sig, self.split,
+                           self.orders, self.workspace, stream)
+
+    def run(self, stream=None) -> int:
+        """Whole hot path: W table, DP, orders. Returns OPT_free."""
+        self.build(stream)
+        opt = self.solve(stream)
+        self.extract(stream)
+        return opt
+
+    def host_tables(self) -> dict:
+        """Copies of the device tables as numpy arrays (uint32 views of masks)."""
+        return {
+            "W": self.W.cpu().numpy(),
+            "C": self.C.cpu().numpy(),
+            "split": self.split.cpu().numpy().view("uint32"),
+            "sig": self.sig.cpu().numpy().view("uint32")[:self.n_chunks],
+            "orders": self.orders.cpu().numpy()[:self.nnz],
+        }
+
+
+def solve(inst, device="cuda") -> dict:
+    """One full run on the GPU; returns host copies of every output."""
+    prob = Problem(inst, device)
+    opt = prob.run()
+    out = prob.host_tables()
+    out["opt"] = opt
+    return out

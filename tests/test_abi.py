@@ -1,0 +1,99 @@
+"""The C ABI without a GPU: the library loads, exports every entry point the
+header declares, sizes its workspace, and rejects bad arguments before any
+HIP call."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mpt.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(mpt_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_2609_13692_amd import mpt
+    if not os.path.exists(mpt.LIB_PATH):
+        pytest.fail("libmpt.so is not built (run __graft_entry__.build())")
+    return mpt.load()
+
+
+def test_header_declares_the_three_phases():
+    names = declared_functions()
+    for n in ("mpt_build_weights", "mpt_solve_exact", "mpt_extract_orders", "mpt_workspace_bytes"):
+        assert n in names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    from paper_2609_13692_amd import mpt
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+    assert set(declared_functions()) == set(mpt.EXPORTED)
+
+
+def test_workspace_sizes(lib):
+    from paper_2609_13692_amd import mpt
+    assert mpt.mpt_workspace_bytes(0, 10) == 0
+    assert mpt.mpt_workspace_bytes(29, 10) == 0
+    assert mpt.mpt_workspace_bytes(5, -1) == 0
+    for m in (1, 12, 20, 25, 28):
+        a = mpt.mpt_workspace_bytes(m, 0)
+        b = mpt.mpt_workspace_bytes(m, 10000)
+        assert a >= 256 and b >= a and b % 256 == 0
+        assert b >= 256 + 12 * 10000
+
+
+def test_status_strings(lib):
+    for code in (0, -1, -2, -3, -4, -5, -6, -8):
+        assert lib.mpt_status_string(code)
+    assert lib.mpt_status_string(-77) == b"unknown status"
+
+
+def test_host_side_validation_before_any_device_call(lib):
+    P = ctypes.c_void_p
+    dummy = P(4096)          # never dereferenced: every call below fails its host checks
+    ws = P(256 * 16)
+    # m out of range
+    assert lib.mpt_build_weights(0, 1, 0, dummy, dummy, None, dummy, dummy, ws, 1 << 20, None) == -1
+    assert b"m = 0" in lib.mpt_last_error()
+    assert lib.mpt_solve_exact(29, dummy, dummy, dummy, None, ws, 1 << 20, None) == -1
+    # NULL tables
+    assert lib.mpt_solve_exact(4, None, dummy, dummy, None, ws, 1 << 20, None) == -1
+    # workspace missing, misaligned, too small
+    assert lib.mpt_solve_exact(4, dummy, dummy, dummy, None, None, 1 << 20, None) == -6
+    assert lib.mpt_solve_exact(4, dummy, dummy, dummy, None, P(256 * 16 + 8), 1 << 20, None) == -6
+    assert lib.mpt_solve_exact(4, dummy, dummy, dummy, None, ws, 16, None) == -6
+    assert b"needs" in lib.mpt_last_error()
+    # negative sizes
+    assert lib.mpt_build_weights(3, -1, 0, dummy, dummy, None, dummy, dummy, ws, 1 << 20, None) == -1
+    assert lib.mpt_extract_orders(3, 5, -2, dummy, dummy, dummy, dummy, dummy, ws, 1 << 20, None) == -1
+    # missing request arrays when nnz > 0
+    assert lib.mpt_build_weights(3, 5, 4, dummy, dummy, None, dummy, dummy, ws, 1 << 20, None) == -1
+
+
+def test_binding_refuses_host_tensors(lib):
+    import torch
+    from paper_2609_13692_amd import mpt
+    W = torch.zeros(16, dtype=torch.int64)
+    with pytest.raises(ValueError):
+        mpt._ptr(W, torch.int64, 16, "W")
+    with pytest.raises(TypeError):
+        mpt._ptr(W.to(torch.int32), torch.int64, 16, "W")
+
+
+def test_oracle_is_not_imported_by_the_product():
+    """The product sources never reference the oracle."""
+    pkg = os.path.join(ROOT, "paper_2609_13692_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".h", ".cpp")):
+                text = open(os.path.join(dirpath, f)).read()
+                assert "import oracle" not in text and "from oracle" not in text, f
+                assert "mpt_oracle" not in text, f

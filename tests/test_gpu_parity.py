@@ -1,0 +1,261 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Integer work throughout, so every comparison is bit-exact: the W table, the
+cost table C (entries 1 .. 2^m-1; C[0] is the documented sentinel), the
+tie-broken split table, the demand sets and the read-off orders.
+"""
+import hashlib
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import brute
+from paper_2609_13692_amd import mpt
+from paper_2609_13692_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    mpt.load()
+    yield
+
+
+def say(msg):
+    print(msg, flush=True)
+
+
+def gpu_run(inst):
+    say(f"[gpu] {inst.name} m={inst.m} nnz={inst.nnz}")
+    got = mpt.solve(inst)
+    torch.cuda.synchronize()
+    return got
+
+
+def assert_same(inst, got, ref):
+    assert got["opt"] == ref["opt"]
+    assert np.array_equal(got["W"], ref["W"]), "W table differs"
+    assert got["C"][0] == mpt.MPT_COST_SENTINEL
+    bad = np.nonzero(got["C"][1:] != ref["C"][1:])[0]
+    assert bad.size == 0, f"C differs at {bad[:8] + 1}"
+    bad = np.nonzero(got["split"] != ref["split"])[0]
+    assert bad.size == 0, f"split differs at {bad[:8]}"
+    assert np.array_equal(got["sig"], oracle.demand_sets(inst))
+    assert np.array_equal(got["orders"], ref["orders"]), "orders differ"
+
+
+def digest(a, dtype):
+    return hashlib.sha256(np.ascontiguousarray(a, dtype=dtype).tobytes()).hexdigest()
+
+
+# --- the five benchmark workloads ------------------------------------------------
+
+@pytest.mark.parametrize("idx", [1, 2, 3])
+def test_config_against_live_oracle(idx):
+    inst = wl.config(idx)
+    got = gpu_run(inst)
+    assert_same(inst, got, oracle.solve(inst))
+
+
+@pytest.mark.parametrize("idx", [1, 2, 3, 4, 5])
+def test_config_full_tables_against_golden(idx):
+    """Full tables at the benchmark sizes against digests the oracle wrote."""
+    with open(os.path.join(GOLDEN, f"config_{idx}.json")) as f:
+        g = json.load(f)
+    inst = wl.config(idx)
+    assert inst.sha256() == g["instance_sha256"], "workload generator drifted"
+    got = gpu_run(inst)
+    assert got["opt"] == g["opt"]
+    for s, w, c, sp in g["sample"]:
+        assert (got["W"][s], got["C"][s], got["split"][s]) == (w, c, sp), s
+    assert digest(got["W"], "<i8") == g["W_sha256"]
+    assert digest(got["C"][1:], "<i8") == g["C_sha256_from_1"]
+    assert digest(got["split"], "<u4") == g["split_sha256"]
+    assert got["orders"].tolist() == g["orders"]
+    # Thm 1 sandwich on the GPU's own output: its layout's trie costs OPT
+    assert oracle.trie_cost(inst, got["orders"]) == got["opt"]
+    assert oracle.hierarchy_cost(inst, got["split"]) == got["opt"]
+
+
+def test_config5_sampled_sub_instances():
+    """C(S) at the largest workload equals the oracle's optimum of the
+    sub-instance {R_i : i in S}, for sampled S of up to 14 requests."""
+    inst = wl.config(5)
+    got = gpu_run(inst)
+    sets = inst.requests()
+    rng = np.random.default_rng(3)
+    for trial in range(24):
+        k = int(rng.integers(1, 15))
+        members = sorted(rng.choice(inst.m, size=k, replace=False).tolist())
+        s = sum(1 << i for i in members)
+        sub = wl.from_sets([sets[i] for i in members], inst.weights, inst.n_chunks)
+        assert got["C"][s] == oracle.solve(sub, with_orders=False)["opt"], members
+
+
+# --- sweeps over shapes and seeds ---------------------------------------------------
+
+SWEEP = [
+    # (m, u, kmin, kmax, wmax)
+    (1, 5, 0, 5, 9), (2, 4, 1, 4, 9), (3, 6, 0, 6, 50), (5, 8, 1, 5, 20),
+    (6, 12, 2, 6, 7), (7, 30, 1, 9, 100), (8, 20, 0, 12, 1000), (9, 40, 3, 10, 3),
+    (10, 64, 4, 4, 32), (11, 16, 5, 12, 1), (12, 200, 1, 20, 600), (13, 50, 2, 30, 64),
+    (14, 100, 5, 25, 1 << 20), (15, 300, 10, 40, 600), (16, 64, 8, 32, 5),
+    (17, 500, 5, 15, 600), (18, 2000, 10, 10, 600),
+]
+
+
+@pytest.mark.parametrize("shape", SWEEP, ids=lambda s: f"m{s[0]}")
+def test_random_sweep(shape):
+    m, u, kmin, kmax, wmax = shape
+    for seed in range(3 if m <= 14 else 1):
+        inst = wl.random_small(m, u, kmin, kmax, wmax, seed=1000 * m + seed, allow_empty=True)
+        got = gpu_run(inst)
+        assert_same(inst, got, oracle.solve(inst))
+
+
+@pytest.mark.parametrize("seed", range(1, 11))
+def test_retrieval_shape_seeds(seed):
+    inst = wl.gen_retrieval(m=16, u=2000, topics=50, k=10, seed=seed)
+    got = gpu_run(inst)
+    assert_same(inst, got, oracle.solve(inst))
+
+
+@pytest.mark.parametrize("seed", range(1, 6))
+def test_tiny_shape_seeds(seed):
+    inst = wl.config(1, seed=seed)
+    got = gpu_run(inst)
+    assert_same(inst, got, oracle.solve(inst))
+
+
+# --- the paper's pins through the HIP path -----------------------------------------
+
+def test_k4_3uniform_on_gpu():
+    inst = wl.from_sets([[0, 1, 2], [0, 1, 3], [0, 2, 3], [1, 2, 3]], [1] * 4, 4)
+    got = gpu_run(inst)
+    assert got["opt"] == 8
+    layout = ["".join("abcd"[x] for x in got["orders"][3 * i:3 * i + 3]) for i in range(4)]
+    assert layout == ["abc", "abd", "cda", "cdb"]
+
+
+def test_leave_one_out_closed_form_on_gpu():
+    for n in range(1, 21):
+        got = gpu_run(wl.gen_loo(n))
+        assert got["opt"] == brute.loo_opt_free(n), n
+    n = 16
+    got = gpu_run(wl.gen_loo(n))
+    pc = np.array([bin(s).count("1") for s in range(1 << n)])
+    E = np.array([0] + [brute.loo_opt_free(s) for s in range(1, n + 1)])
+    assert np.array_equal(got["C"][1:], ((n - pc) + E[pc])[1:])
+    assert np.array_equal(got["W"][1:], (n - pc)[1:]) and got["W"][0] == n
+
+
+def test_vertex_cover_on_gpu():
+    for seed in range(6):
+        inst = wl.gen_two_chunk_graph(7, 9, seed)
+        got = gpu_run(inst)
+        assert got["opt"] == brute.vertex_cover_number(7, inst.requests()) + inst.m
+
+
+def test_worst_ratio_and_witness_on_gpu():
+    inst = wl.from_sets([[int(c) for c in s] for s in
+                         ["0145", "0236", "1236", "1245", "1345", "1456", "2346", "2356"]], [1] * 7, 7)
+    assert gpu_run(inst)["opt"] == 14
+    inst = wl.from_sets([[0, 1, 2, 3], [1, 4], [2, 5, 7, 8], [4, 6]], [1] * 9, 9)
+    assert gpu_run(inst)["opt"] == 10
+
+
+# --- edge cases ----------------------------------------------------------------------
+
+def test_single_request():
+    inst = wl.from_sets([[5, 2, 9, 0]], [3] * 10, 10)
+    got = gpu_run(inst)
+    assert got["opt"] == 12
+    assert got["orders"].tolist() == [0, 2, 5, 9]
+    assert_same(inst, got, oracle.solve(inst))
+
+
+def test_empty_and_identical_requests():
+    inst = wl.from_sets([[], [1, 2, 3], [3, 2, 1], [], [1, 2, 3], [4]], [5, 6, 7, 8, 9], 5)
+    got = gpu_run(inst)
+    assert_same(inst, got, oracle.solve(inst))
+    assert got["opt"] == 6 + 7 + 8 + 9
+
+
+def test_all_requests_empty_and_empty_universe():
+    inst = wl.from_sets([[], [], []], [4, 4], 2)
+    got = gpu_run(inst)
+    assert got["opt"] == 0 and got["W"][0] == 8
+    assert_same(inst, got, oracle.solve(inst))
+    inst = wl.from_sets([[], []], [], 0)
+    got = gpu_run(inst)
+    assert got["opt"] == 0 and got["W"].tolist() == [0, 0, 0, 0]
+
+
+def test_large_weights():
+    rng = np.random.default_rng(5)
+    w = rng.integers(1 << 31, (1 << 32) + 1, size=400, dtype=np.int64)
+    sets = [rng.choice(400, size=int(rng.integers(50, 300)), replace=False).tolist() for _ in range(14)]
+    inst = wl.from_sets(sets, w, 400)
+    got = gpu_run(inst)
+    assert_same(inst, got, oracle.solve(inst))
+
+
+def test_max_m_weight_table():
+    """W at MPT_MAX_M = 28 (a 2 GiB table) for L_28: W(S) = 28 - |S|."""
+    n = mpt.MPT_MAX_M
+    inst = wl.gen_loo(n)
+    say(f"[gpu] build only, {inst.name}")
+    prob = mpt.Problem(inst)
+    prob.build()
+    idx = torch.arange(1 << n, device="cuda", dtype=torch.int64)
+    pc = torch.zeros_like(idx)
+    for b in range(n):
+        pc += (idx >> b) & 1
+    expect = n - pc
+    expect[0] = n
+    assert torch.equal(prob.W, expect)
+    del prob, idx, pc, expect
+    torch.cuda.empty_cache()
+
+
+def test_determinism_and_reuse():
+    inst = wl.config(3)
+    prob = mpt.Problem(inst)
+    a = prob.run()
+    t1 = prob.host_tables()
+    b = prob.run()
+    t2 = prob.host_tables()
+    assert a == b
+    for k in t1:
+        assert np.array_equal(t1[k], t2[k]), k
+
+
+@pytest.mark.parametrize("case", ["range", "dup", "weight", "offsets", "workspace"])
+def test_errors_are_reported(case):
+    inst = wl.config(1)
+    prob = mpt.Problem(inst)
+    expect = {"range": "MPT_E_RANGE", "dup": "MPT_E_DUP", "weight": "MPT_E_WEIGHT",
+              "offsets": "MPT_E_INVALID", "workspace": "MPT_E_WORKSPACE"}[case]
+    if case == "range":
+        prob.req_chunks[3] = inst.n_chunks
+    elif case == "dup":
+        prob.req_chunks[1] = prob.req_chunks[0]
+    elif case == "weight":
+        prob.chunk_w[7] = 0
+    elif case == "offsets":
+        prob.req_off[2] = prob.req_off[3] + 1
+    else:
+        prob.workspace = prob.workspace[:128]
+    with pytest.raises(mpt.MptError) as ei:
+        prob.build()
+    assert ei.value.name == expect
+    # the library stays usable after an error
+    prob2 = mpt.Problem(inst)
+    assert prob2.run() == oracle.solve(inst, with_orders=False)["opt"]
