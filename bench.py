@@ -29,7 +29,10 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0
 N_CU, CLOCK_GHZ = 256, 2.4
 VALU_PEAK_TOPS = N_CU * 64 * CLOCK_GHZ / 1000.0      # int32 lane-ops, T/s (39.3)
-DP_OPS_PER_PAIR = 6   # int64 add (2) + int64 compare (1) + select value (2) + select part (1)
+# VALU instructions one evaluated bipartition needs at the least on gfx950:
+# a 64-bit add of two packed keys (v_lshl_add_u64) and a 64-bit unsigned
+# minimum (v_cmp_lt_u64 + two v_cndmask_b32)
+DP_OPS_PER_PAIR = 4
 
 WORKLOADS = {
     1: "tiny random, m=12, u=64, k=4, w~U{1..32}, seed 0",
@@ -130,7 +133,7 @@ def main() -> int:
         with open(gpath) as f:
             golden_opt = json.load(f)["opt"]
 
-    dp_kernels = {k: v for k, v in prof.items() if k.startswith("dp_")}
+    dp_kernels = {k: v for k, v in prof.items() if k.startswith(("dp_", "rb_"))}
     dom = max(dp_kernels, key=lambda k: dp_kernels[k]["total_ms"])
     d = prof[dom]
     achieved_tops = d["work"] * DP_OPS_PER_PAIR / (d["total_ms"] / 1000.0) / 1e12

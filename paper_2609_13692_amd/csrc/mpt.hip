@@ -349,6 +349,345 @@ __global__ __launch_bounds__(256) void k_dp_reduce(int m, int p, uint32_t n_sets
 }
 
 // ---------------------------------------------------------------------------
+// phase 2, row-blocked DP (packed keys).
+//
+// A mask X splits into a high part X_H (bits L..m-1), a middle part X2
+// (bits CB..L-1) and a low part X1 (bits 0..CB-1). Row X_H is the 2^L
+// consecutive table entries that share X_H. Every unordered bipartition
+// {P, Q} of S = S_H|S_L is visited once, from the part holding the lowest
+// request of S_H (or, for S_H = 0, in both orientations):
+//   cross pairs  (A_H, B_H), A_H holding lowbit(S_H), B_H non-empty: the
+//                rows A_H and B_H are complete (lower level), and
+//                C(S_H|S_L) gets min over A_L of rowA[A_L] + rowB[S_L^A_L];
+//   self pair    (S_H, 0): rowA is row S_H itself, filled in order of
+//                |S_L|, rowB is row 0.
+// Levels h = |S_H| run one after the other; within a level every S_H is
+// independent. Inside a pair, a thread takes the block of 2^CB entries for a
+// middle mask and does the CB-bit min-plus subset convolution in registers.
+//
+// Packed keys: during the DP the C table holds C'(X) = C(X) << m, and a
+// candidate is C'(A) + C'(B) + canon(A, B), canon = the part holding
+// lowbit(S) (< 2^m). The smallest key is the smallest cost and, among equal
+// costs, the numerically smallest such part -- the documented tie rule.
+// This needs every cost below 2^(62-m); larger instances take the plain
+// kernels above.
+namespace rb {
+constexpr int L = 12;                 // row bits
+constexpr int CB = 3;                 // register-block bits
+constexpr int R2 = L - CB;            // middle bits
+constexpr int T = 3;                  // log2 of the A2 iterations per work item
+constexpr int NB = 1 << CB;           // entries per block
+constexpr int ROW = 1 << L;           // entries per row
+constexpr int NS2 = 1 << R2;          // blocks per row
+constexpr int THREADS = 256;
+constexpr int WG_TARGET = 2048;       // workgroups aimed at when a level is split
+constexpr int FUSE_MIN_SETS = 512;    // levels with this many S_H keep one workgroup per S_H
+constexpr uint64_t SENT = (uint64_t)1 << 62;
+
+constexpr int cpop(int x) { int c = 0; while (x) { c += x & 1; x >>= 1; } return c; }
+
+// work items of one row pair: (S2, chunk of 2^T submasks A2 of S2), grouped
+// by |S2| from R2 down to 0
+struct Items {
+    uint32_t v[4096];
+    int begin[R2 + 1];
+    int end[R2 + 1];
+    int n;
+};
+constexpr Items make_items() {
+    Items it{};
+    int n = 0;
+    for (int k = R2; k >= 0; --k) {
+        it.begin[k] = n;
+        for (int s = 0; s < NS2; ++s) {
+            if (cpop(s) != k) continue;
+            int chunks = k > T ? 1 << (k - T) : 1;
+            for (int j = 0; j < chunks; ++j) it.v[n++] = (uint32_t)s | ((uint32_t)j << 16);
+        }
+        it.end[k] = n;
+    }
+    it.n = n;
+    return it;
+}
+constexpr Items kItems = make_items();
+static_assert(kItems.n <= 4096, "item table too small");
+__constant__ Items c_items = make_items();
+
+// the middle masks of each popcount, for the one-thread-per-block steps
+struct Blocks { uint16_t v[NS2]; int begin[R2 + 1]; int end[R2 + 1]; };
+constexpr Blocks make_blocks() {
+    Blocks b{};
+    int n = 0;
+    for (int k = 0; k <= R2; ++k) {
+        b.begin[k] = n;
+        for (int s = 0; s < NS2; ++s)
+            if (cpop(s) == k) b.v[n++] = (uint16_t)s;
+        b.end[k] = n;
+    }
+    return b;
+}
+__constant__ Blocks c_blocks = make_blocks();
+
+// LDS position of entry (X2, X1) of a row: 16-byte pieces of each 64-byte
+// block are rotated by bits 1..2 of X2 so that lanes reading different
+// blocks spread over the banks
+__device__ inline int lds_pos(int x2, int x1) {
+    return (x2 << CB) | ((((x1 >> 1) ^ (x2 >> 1)) & 3) << 1) | (x1 & 1);
+}
+
+__device__ inline void load_block(const uint64_t *row, int x2, uint64_t v[NB]) {
+    const ulonglong2 *p = reinterpret_cast<const ulonglong2 *>(row + (x2 << CB));
+    const int s = (x2 >> 1) & 3;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        ulonglong2 t = p[q ^ s];
+        v[2 * q] = t.x;
+        v[2 * q + 1] = t.y;
+    }
+}
+
+// row X_H of the packed table, global -> LDS (swizzled)
+__device__ inline void load_row(uint64_t *row, const uint64_t *C, uint32_t xh) {
+    const ulonglong2 *src = reinterpret_cast<const ulonglong2 *>(C + ((size_t)xh << L));
+    for (int g = threadIdx.x; g < ROW / 2; g += THREADS) {
+        const int x2 = g >> 2, q = g & 3;
+        const ulonglong2 t = src[g];
+        ulonglong2 *dst = reinterpret_cast<ulonglong2 *>(row + (x2 << CB));
+        dst[q ^ ((x2 >> 1) & 3)] = t;
+    }
+}
+
+__device__ inline uint64_t umin64(uint64_t a, uint64_t b) { return b < a ? b : a; }
+
+// deposit the low bits of t into the set bits of mask (in order)
+__device__ inline uint32_t deposit(uint32_t t, uint32_t mask) {
+    uint32_t r = 0;
+    while (t && mask) {
+        const uint32_t bit = mask & (0u - mask);
+        mask ^= bit;
+        if (t & 1u) r |= bit;
+        t >>= 1;
+    }
+    return r;
+}
+
+// CB-bit min-plus subset convolution of one block pair.
+//   best[S1] = min(best[S1], min over A1 in S1 of key(A1, S1 ^ A1))
+// key = a[A1] + b[B1] + canon, canon = A-side mask if the A side holds
+// lowbit(S1) (for S1 = 0: if orient_a), else B-side mask.
+__device__ inline void conv_block(const uint64_t a[NB], const uint64_t b[NB], uint32_t canon_a,
+                                  uint32_t canon_b, bool orient_a, uint64_t best[NB]) {
+    uint64_t aa[NB], bb[NB];
+#pragma unroll
+    for (int x = 0; x < NB; ++x) {
+        aa[x] = a[x] | (uint64_t)(canon_a | (uint32_t)x);
+        bb[x] = b[x] | (uint64_t)(canon_b | (uint32_t)x);
+    }
+    {
+        const uint64_t c = orient_a ? aa[0] + b[0] : a[0] + bb[0];
+        best[0] = umin64(best[0], c);
+    }
+#pragma unroll
+    for (int s1 = 1; s1 < NB; ++s1) {
+        const int low = s1 & -s1;
+#pragma unroll
+        for (int a1 = 0; a1 < NB; ++a1) {
+            if (a1 & ~s1) continue;
+            const int b1 = s1 ^ a1;
+            const uint64_t c = (a1 & low) ? aa[a1] + b[b1] : a[a1] + bb[b1];
+            best[s1] = umin64(best[s1], c);
+        }
+    }
+}
+
+// one work item against the row pair (rowA = A-side rows, rowB = B-side)
+// item A2 range: chunk j of the submasks of S2; skip_full drops A2 == S2,
+// skip_empty drops A2 == 0
+__device__ inline void run_item(uint32_t item, const uint64_t *rowA, const uint64_t *rowB, uint32_t a_hi,
+                                uint32_t b_hi, bool skip_full, bool skip_empty, uint64_t *acc) {
+    const uint32_t s2 = item & 0xffffu;
+    const uint32_t j = item >> 16;
+    const int k = __popc(s2);
+    const int tb = k < T ? k : T;
+    const uint32_t cnt = 1u << tb;
+    const uint32_t low2 = s2 & (0u - s2);
+    uint32_t a2 = deposit(j << tb, s2);
+    uint64_t best[NB];
+#pragma unroll
+    for (int x = 0; x < NB; ++x) best[x] = ~0ull;
+    for (uint32_t i = 0; i < cnt; ++i) {
+        const uint32_t b2 = s2 ^ a2;
+        if (!((skip_full && b2 == 0) || (skip_empty && a2 == 0))) {
+            uint64_t a[NB], b[NB];
+            load_block(rowA, (int)a2, a);
+            load_block(rowB, (int)b2, b);
+            const bool orient_a = (s2 == 0) || (a2 & low2);
+            conv_block(a, b, a_hi | (a2 << CB), b_hi | (b2 << CB), orient_a, best);
+        }
+        a2 = ((a2 | ~s2) + 1u) & s2;
+    }
+#pragma unroll
+    for (int x = 0; x < NB; ++x)
+        if (best[x] != ~0ull) atomicMin((unsigned long long *)&acc[(s2 << CB) | x], (unsigned long long)best[x]);
+}
+
+// Complete row S_H: acc holds the best cross-pair keys (or ~0); rowS is
+// the LDS buffer that receives row S_H; row0 holds row 0 (the same buffer
+// as rowS when S_H = 0). Writes C' and split to global memory.
+__device__ void finalize_row(int m, uint32_t sh, uint64_t *rowS, const uint64_t *row0, uint64_t *acc,
+                             const int64_t *__restrict__ W, uint64_t *__restrict__ Cp,
+                             uint32_t *__restrict__ split) {
+    const uint32_t a_hi = sh << L;
+    const uint64_t mask = ((uint64_t)1 << m) - 1u;
+    uint64_t b0[NB];                         // row 0, block 0 (complete unless S_H = 0)
+    if (sh != 0) load_block(row0, 0, b0);
+    for (int k = 0; k <= R2; ++k) {
+        // A2 a proper submask of S2 (and, for S_H = 0, not empty: those
+        // pairs are the mirrors of the in-block pairs below)
+        for (int it = kItems.begin[k] + threadIdx.x; it < kItems.end[k]; it += THREADS)
+            run_item(c_items.v[it], rowS, row0, a_hi, 0u, true, sh == 0, acc);
+        __syncthreads();
+        // A2 = S2: in-block pairs, one thread per block of this level
+        for (int bi = c_blocks.begin[k] + threadIdx.x; bi < c_blocks.end[k]; bi += THREADS) {
+            const uint32_t s2 = c_blocks.v[bi];
+            const uint32_t base = a_hi | (s2 << CB);
+            uint64_t out[NB];
+            int64_t w[NB];
+            const int64_t *wp = W + base;
+#pragma unroll
+            for (int x = 0; x < NB; ++x) w[x] = wp[x];
+            uint64_t key[NB];
+#pragma unroll
+            for (int x = 0; x < NB; ++x) key[x] = acc[(s2 << CB) | x];
+            uint32_t sp[NB];
+            // S1 in order of popcount so that every A1 < S1 is ready
+#pragma unroll
+            for (int pc = 0; pc <= CB; ++pc) {
+#pragma unroll
+                for (int s1 = 0; s1 < NB; ++s1) {
+                    if (cpop(s1) != pc) continue;
+                    const uint32_t S = base | (uint32_t)s1;
+                    if (S == 0) { out[s1] = SENT; sp[s1] = 0; continue; }
+                    if (__popc(S) == 1) { out[s1] = (uint64_t)w[s1] << m; sp[s1] = 0; continue; }
+                    uint64_t kb = key[s1];
+                    const int low = s1 & -s1;
+#pragma unroll
+                    for (int a1 = 0; a1 < NB; ++a1) {
+                        if ((a1 & ~s1) || a1 == s1) continue;
+                        const int b1 = s1 ^ a1;
+                        const uint64_t av = out[a1];
+                        const uint64_t bv = (sh == 0 && s2 == 0) ? out[b1] : b0[b1];
+                        const uint64_t c = (a1 & low) ? (av | (uint64_t)(base | (uint32_t)a1)) + bv
+                                                      : av + (bv | (uint64_t)(uint32_t)b1);
+                        kb = umin64(kb, c);
+                    }
+                    out[s1] = ((kb >> m) - (uint64_t)w[s1]) << m;
+                    sp[s1] = (uint32_t)(kb & mask);
+                }
+            }
+#pragma unroll
+            for (int x = 0; x < NB; ++x) {
+                rowS[lds_pos((int)s2, x)] = out[x];
+                Cp[base + x] = out[x];
+                split[base + x] = sp[x];
+            }
+        }
+        __syncthreads();
+        if (sh == 0 && k == 0) load_block(row0, 0, b0);   // row 0's block 0 is now complete
+    }
+}
+
+struct Lds {
+    uint64_t rowA[ROW];
+    uint64_t rowB[ROW];
+    uint64_t acc[ROW];
+};
+
+// cross pairs of one (S_H, chunk); fused = finish the row in place
+__global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_pairs, uint32_t chunks,
+                                                      uint32_t per_chunk, int fused, const int64_t *__restrict__ W,
+                                                      uint64_t *__restrict__ Cp, uint32_t *__restrict__ split,
+                                                      uint64_t *__restrict__ partial) {
+    __shared__ Lds s;
+    const uint32_t bid = xcd_block(blockIdx.x, gridDim.x);
+    const uint32_t r = bid / chunks, j = bid % chunks;
+    const int m_hi = m - L;
+    const uint32_t sh = unrank_colex(r, h, m_hi);
+    const uint32_t lowh = sh & (0u - sh);
+    const uint32_t rest = sh ^ lowh;
+    for (int e = threadIdx.x; e < ROW; e += THREADS) s.acc[e] = ~0ull;
+    const uint32_t t0 = j * per_chunk;
+    const uint32_t t1 = min(n_pairs, t0 + per_chunk);
+    uint32_t ah = t0 < t1 ? (lowh | deposit(t0, rest)) : 0u;
+    for (uint32_t t = t0; t < t1; ++t) {
+        const uint32_t bh = sh ^ ah;
+        __syncthreads();
+        load_row(s.rowA, Cp, ah);
+        load_row(s.rowB, Cp, bh);
+        __syncthreads();
+        for (int it = threadIdx.x; it < kItems.n; it += THREADS)
+            run_item(c_items.v[it], s.rowA, s.rowB, ah << L, bh << L, false, false, s.acc);
+        ah = lowh | (((ah | ~rest) + 1u) & rest);    // next A_H holding lowbit(S_H)
+    }
+    __syncthreads();
+    if (fused) {
+        load_row(s.rowB, Cp, 0u);
+        __syncthreads();
+        finalize_row(m, sh, s.rowA, s.rowB, s.acc, W, Cp, split);
+    } else {
+        uint64_t *dst = partial + (size_t)bid * ROW;
+        for (int e = threadIdx.x; e < ROW; e += THREADS) dst[e] = s.acc[e];
+    }
+}
+
+// min over the chunks of one S_H, into chunk 0's slot; 256 entries per block
+__global__ __launch_bounds__(THREADS) void k_rb_reduce(uint32_t chunks, uint64_t *__restrict__ partial) {
+    const uint32_t r = blockIdx.x / (ROW / THREADS);
+    const uint32_t e = (blockIdx.x % (ROW / THREADS)) * THREADS + threadIdx.x;
+    uint64_t *base = partial + (size_t)r * chunks * ROW + e;
+    uint64_t v = base[0];
+    for (uint32_t j = 1; j < chunks; ++j) v = umin64(v, base[(size_t)j * ROW]);
+    base[0] = v;
+}
+
+// finish the rows of one level: acc from the reduced partials (chunks > 0)
+// or empty (levels 0 and 1 have no cross pairs)
+__global__ __launch_bounds__(THREADS) void k_rb_final(int m, int h, uint32_t chunks, const int64_t *__restrict__ W,
+                                                      uint64_t *__restrict__ Cp, uint32_t *__restrict__ split,
+                                                      const uint64_t *__restrict__ partial) {
+    __shared__ Lds s;
+    const uint32_t r = blockIdx.x;
+    const uint32_t sh = unrank_colex(r, h, m - L);
+    const uint64_t *src = partial + (size_t)r * chunks * ROW;
+    for (int e = threadIdx.x; e < ROW; e += THREADS) {
+        s.acc[e] = chunks ? src[e] : ~0ull;
+        s.rowA[e] = 0;
+    }
+    if (sh != 0) load_row(s.rowB, Cp, 0u);
+    __syncthreads();
+    finalize_row(m, sh, s.rowA, sh == 0 ? s.rowA : s.rowB, s.acc, W, Cp, split);
+}
+
+// packed C' -> C (C[0] keeps the documented sentinel)
+__global__ void k_rb_unpack(int m, int64_t *C) {
+    const int64_t n = (int64_t)1 << m;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+        C[i] = i == 0 ? kInf : (int64_t)((uint64_t)C[i] >> m);
+}
+
+// sum_i W({i}), saturated, for the packed-key eligibility test
+__global__ void k_request_total(int m, const int64_t *W, WsHeader *h) {
+    if (threadIdx.x != 0) return;
+    int64_t tot = 0;
+    for (int i = 0; i < m; ++i) {
+        const int64_t v = W[(int64_t)1 << i];
+        tot = (v >= INT64_MAX - tot) ? INT64_MAX : tot + v;
+    }
+    h->pad[0] = tot;
+}
+}  // namespace rb
+
+// ---------------------------------------------------------------------------
 // phase 3: one workgroup per request i. Chunk x of R_i is emitted at the
 // first node of i's root-to-leaf path that lies inside S_x; inside a node
 // chunks go in ascending id. The output slot of x is its rank under the key
@@ -499,8 +838,42 @@ size_t dp_partial_entries(int m) {
     return mx;
 }
 
+// row-blocked DP: one entry per level h = |S_H| of the high part
+struct RbLevel { int h; uint32_t n_sets; uint32_t n_pairs; uint32_t chunks; uint32_t per_chunk; };
+constexpr int kRbMinM = rb::L + 1;
+
+std::vector<RbLevel> rb_plan(int m) {
+    std::vector<RbLevel> v;
+    const int m_hi = m - rb::L;
+    for (int h = 0; h <= m_hi; ++h) {
+        RbLevel L{};
+        L.h = h;
+        L.n_sets = kBinom.v[m_hi][h];
+        L.n_pairs = h >= 2 ? (1u << (h - 1)) - 1u : 0u;
+        if (L.n_pairs == 0) {
+            L.chunks = 0;
+        } else if (L.n_sets >= (uint32_t)rb::FUSE_MIN_SETS) {
+            L.chunks = 1;
+        } else {
+            uint32_t c = (rb::WG_TARGET + L.n_sets - 1) / L.n_sets;
+            L.chunks = std::min(c, L.n_pairs);
+        }
+        L.per_chunk = L.chunks ? (L.n_pairs + L.chunks - 1) / L.chunks : 0;
+        v.push_back(L);
+    }
+    return v;
+}
+
+size_t rb_partial_entries(int m) {
+    if (m < kRbMinM) return 0;
+    size_t mx = 0;
+    for (const RbLevel &L : rb_plan(m))
+        if (L.chunks > 1) mx = std::max(mx, (size_t)L.n_sets * L.chunks * rb::ROW);
+    return mx;
+}
+
 struct WsLayout {
-    size_t list_sig, list_w, part_v, part_a, keys, total;
+    size_t list_sig, list_w, part_v, part_a, keys, rb_part, total;
 };
 
 WsLayout ws_layout(int m, int64_t nnz) {
@@ -518,7 +891,9 @@ WsLayout ws_layout(int m, int64_t nnz) {
     size_t dp_end = L.part_a + align256(P * 4);
     L.keys = off;
     size_t ex_end = L.keys + align256(nz * 8);
-    L.total = std::max(build_end, std::max(dp_end, ex_end));
+    L.rb_part = off;
+    size_t rb_end = L.rb_part + align256(rb_partial_entries(m) * 8);
+    L.total = std::max(std::max(build_end, rb_end), std::max(dp_end, ex_end));
     return L;
 }
 
@@ -546,6 +921,44 @@ int check_common(int m, int64_t n_chunks, int64_t nnz) {
     if (m < 1 || m > MPT_MAX_M) return fail(MPT_E_INVALID, "m = %d outside [1, %d]", m, MPT_MAX_M);
     if (n_chunks < 0 || n_chunks > MPT_MAX_CHUNKS) return fail(MPT_E_INVALID, "n_chunks = %lld out of range", (long long)n_chunks);
     if (nnz < 0 || nnz > (int64_t)INT32_MAX) return fail(MPT_E_INVALID, "nnz = %lld out of range", (long long)nnz);
+    return MPT_OK;
+}
+
+int solve_rb(int m, const int64_t *W, int64_t *C, uint32_t *split, uint64_t *partial, hipStream_t s) {
+    uint64_t *Cp = (uint64_t *)C;
+    double pair_work = 1.0;
+    for (int i = 0; i < rb::L; ++i) pair_work *= 3.0;        // ordered (A_L, S_L) pairs of one row pair
+    for (const RbLevel &P : rb_plan(m)) {
+        if (P.n_pairs == 0) {
+            LaunchScope ls("rb_final", pair_work * P.n_sets, s);
+            rb::k_rb_final<<<P.n_sets, rb::THREADS, 0, s>>>(m, P.h, 0u, W, Cp, split, partial);
+        } else if (P.chunks == 1) {
+            LaunchScope ls("rb_cross", pair_work * (double)P.n_sets * (P.n_pairs + 1), s);
+            rb::k_rb_cross<<<P.n_sets, rb::THREADS, 0, s>>>(m, P.h, P.n_pairs, 1u, P.n_pairs, 1, W, Cp, split,
+                                                            partial);
+        } else {
+            {
+                LaunchScope ls("rb_cross", pair_work * (double)P.n_sets * P.n_pairs, s);
+                rb::k_rb_cross<<<P.n_sets * P.chunks, rb::THREADS, 0, s>>>(m, P.h, P.n_pairs, P.chunks,
+                                                                           P.per_chunk, 0, W, Cp, split, partial);
+            }
+            {
+                LaunchScope ls("rb_reduce", (double)P.n_sets * P.chunks * rb::ROW * 8.0, s);
+                rb::k_rb_reduce<<<P.n_sets * (rb::ROW / rb::THREADS), rb::THREADS, 0, s>>>(P.chunks, partial);
+            }
+            {
+                LaunchScope ls("rb_final", pair_work * P.n_sets, s);
+                rb::k_rb_final<<<P.n_sets, rb::THREADS, 0, s>>>(m, P.h, P.chunks, W, Cp, split, partial);
+            }
+        }
+        HIP_TRY(hipGetLastError());
+    }
+    const int64_t n = (int64_t)1 << m;
+    {
+        LaunchScope ls("rb_unpack", 16.0 * n, s);
+        rb::k_rb_unpack<<<grid_for(n, 256, 16384), 256, 0, s>>>(m, C);
+    }
+    HIP_TRY(hipGetLastError());
     return MPT_OK;
 }
 
@@ -633,6 +1046,23 @@ extern "C" int mpt_solve_exact(int m, const int64_t *W, int64_t *C, uint32_t *sp
     int64_t *part_v = (int64_t *)(ws + L.part_v);
     uint32_t *part_a = (uint32_t *)(ws + L.part_a);
     const int64_t n = (int64_t)1 << m;
+    if (m >= kRbMinM) {
+        // packed keys need every cost below 2^(62-m): check sum_i w(R_i)
+        WsHeader *h = (WsHeader *)ws;
+        rb::k_request_total<<<1, 64, 0, s>>>(m, W, h);
+        int64_t total = 0;
+        HIP_TRY(hipMemcpyAsync(&total, &h->pad[0], sizeof total, hipMemcpyDeviceToHost, s));
+        HIP_TRY(hipStreamSynchronize(s));
+        if (total < ((int64_t)1 << (61 - m))) {
+            rc = solve_rb(m, W, C, split, (uint64_t *)(ws + L.rb_part), s);
+            if (rc) return rc;
+            if (opt_cost) {
+                HIP_TRY(hipMemcpyAsync(opt_cost, C + (n - 1), sizeof(int64_t), hipMemcpyDeviceToHost, s));
+                HIP_TRY(hipStreamSynchronize(s));
+            }
+            return MPT_OK;
+        }
+    }
     {
         LaunchScope ls("dp_init", 8.0 * n, s);
         k_dp_init<<<grid_for(n, 256, 16384), 256, 0, s>>>(m, W, C, split);

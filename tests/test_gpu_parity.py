@@ -207,6 +207,18 @@ def test_large_weights():
     assert_same(inst, got, oracle.solve(inst))
 
 
+def test_costs_too_large_to_pack_take_the_plain_kernels():
+    """With sum_i w(R_i) >= 2^(61-m) the packed-key kernels are not used;
+    the result must not change."""
+    rng = np.random.default_rng(9)
+    w = rng.integers(1 << 31, (1 << 32) + 1, size=3000, dtype=np.int64)
+    sets = [rng.choice(3000, size=60, replace=False).tolist() for _ in range(20)]
+    inst = wl.from_sets(sets, w, 3000)
+    assert int(sum(w[s].sum() for s in sets)) >= 1 << (61 - 20)
+    got = gpu_run(inst)
+    assert_same(inst, got, oracle.solve(inst))
+
+
 def test_max_m_weight_table():
     """W at MPT_MAX_M = 28 (a 2 GiB table) for L_28: W(S) = 28 - |S|."""
     n = mpt.MPT_MAX_M
