@@ -365,31 +365,42 @@ __global__ __launch_bounds__(256) void k_dp_reduce(int m, int p, uint32_t n_sets
 // independent. Inside a pair, a thread takes the block of 2^CB entries for a
 // middle mask and does the CB-bit min-plus subset convolution in registers.
 //
-// Packed keys: during the DP the C table holds C'(X) = C(X) << m, and a
-// candidate is C'(A) + C'(B) + canon(A, B), canon = the part holding
-// lowbit(S) (< 2^m). The smallest key is the smallest cost and, among equal
-// costs, the numerically smallest such part -- the documented tie rule.
-// This needs every cost below 2^(62-m); larger instances take the plain
-// kernels above.
+// Packed keys: during the DP the C table holds C'(X) = C(X) << m. A
+// candidate's key is C'(A) + C'(B) + canon, where canon is the mask of the
+// part holding lowbit(S) (< 2^m). The smallest key is the smallest cost and,
+// among equal costs, the numerically smallest such part -- the documented
+// tie rule. Rows sit in LDS twice: plain (P = C') and tagged with their own
+// mask (T = C' + X), so a key is one add: T(A) + P(B) when A holds
+// lowbit(S), P(A) + T(B) otherwise. P is needed only at even low parts.
+// Keys are exact integers; when every key stays below 2^53 they are held
+// as doubles (one v_add_f64 and one v_min_f64 per candidate), otherwise
+// as uint64 (below 2^62); larger instances take the plain kernels.
 namespace rb {
 constexpr int L = 12;                 // row bits
 constexpr int CB = 3;                 // register-block bits
 constexpr int R2 = L - CB;            // middle bits
-constexpr int T = 3;                  // log2 of the A2 iterations per work item
+#ifndef MPT_RB_ITEM_LOG
+#define MPT_RB_ITEM_LOG 3
+#endif
+#ifndef MPT_RB_THREADS
+#define MPT_RB_THREADS 1024
+#endif
+constexpr int T = MPT_RB_ITEM_LOG;    // log2 of the A2 iterations per work item
 constexpr int NB = 1 << CB;           // entries per block
+constexpr int NE = NB / 2;            // even entries per block
 constexpr int ROW = 1 << L;           // entries per row
 constexpr int NS2 = 1 << R2;          // blocks per row
-constexpr int THREADS = 256;
-constexpr int WG_TARGET = 2048;       // workgroups aimed at when a level is split
-constexpr int FUSE_MIN_SETS = 512;    // levels with this many S_H keep one workgroup per S_H
+constexpr int THREADS = MPT_RB_THREADS;
+constexpr int WG_TARGET = 1024;       // workgroups aimed at when a level is split
+constexpr int FUSE_MIN_SETS = 256;    // levels with this many S_H keep one workgroup per S_H
 constexpr uint64_t SENT = (uint64_t)1 << 62;
 
 constexpr int cpop(int x) { int c = 0; while (x) { c += x & 1; x >>= 1; } return c; }
 
-// work items of one row pair: (S2, chunk of 2^T submasks A2 of S2), grouped
-// by |S2| from R2 down to 0
+// work items of the self pair: (S2, chunk of 2^T submasks A2 of S2),
+// grouped by |S2| from R2 down to 0
 struct Items {
-    uint32_t v[4096];
+    uint32_t v[8192];
     int begin[R2 + 1];
     int end[R2 + 1];
     int n;
@@ -410,7 +421,7 @@ constexpr Items make_items() {
     return it;
 }
 constexpr Items kItems = make_items();
-static_assert(kItems.n <= 4096, "item table too small");
+static_assert(kItems.n <= 8192, "item table too small");
 __constant__ Items c_items = make_items();
 
 // the middle masks of each popcount, for the one-thread-per-block steps
@@ -428,36 +439,100 @@ constexpr Blocks make_blocks() {
 }
 __constant__ Blocks c_blocks = make_blocks();
 
-// LDS position of entry (X2, X1) of a row: 16-byte pieces of each 64-byte
-// block are rotated by bits 1..2 of X2 so that lanes reading different
-// blocks spread over the banks
-__device__ inline int lds_pos(int x2, int x1) {
-    return (x2 << CB) | ((((x1 >> 1) ^ (x2 >> 1)) & 3) << 1) | (x1 & 1);
+// key arithmetic: exact integers as uint64 or as doubles (< 2^53)
+template <class K> struct Key;
+template <> struct Key<uint64_t> {
+    static __device__ inline uint64_t plain(uint64_t c) { return c; }
+    static __device__ inline uint64_t tagged(uint64_t c, uint32_t idx) { return c + idx; }
+    static __device__ inline uint64_t add(uint64_t a, uint64_t b) { return a + b; }
+    static __device__ inline uint64_t min(uint64_t a, uint64_t b) { return b < a ? b : a; }
+    static __device__ inline uint64_t none() { return ~0ull; }
+    static __device__ inline uint64_t bits(uint64_t k) { return k; }
+    static __device__ inline uint64_t value_of_bits(uint64_t b) { return b; }
+};
+template <> struct Key<double> {
+    static __device__ inline double plain(uint64_t c) { return (double)c; }
+    static __device__ inline double tagged(uint64_t c, uint32_t idx) { return (double)(c + idx); }
+    static __device__ inline double add(double a, double b) { return a + b; }
+    static __device__ inline double min(double a, double b) { return fmin(a, b); }
+    static __device__ inline double none() { return __builtin_inf(); }
+    // positive doubles order like their bit patterns
+    static __device__ inline uint64_t bits(double k) { return (uint64_t)__double_as_longlong(k); }
+    static __device__ inline uint64_t value_of_bits(uint64_t b) {
+        return b >= 0x7ff0000000000000ull ? ~0ull : (uint64_t)__longlong_as_double((long long)b);
+    }
+};
+
+template <class K> struct alignas(16) Lds {
+    K pa[NS2 * NE];        // row on the A side, plain, even low parts
+    K ta[ROW];             // row on the A side, tagged
+    K pb[NS2 * NE];        // row on the B side, plain, even low parts
+    K tb[ROW];             // row on the B side, tagged
+    uint64_t acc[ROW];     // best key bits per entry of the output row
+    uint64_t blk0[NB];     // plain C' of row 0, block 0
+};
+
+// LDS positions. Lanes read whole blocks of different middle masks x2, so
+// the 16-byte pieces are spread over the eight 16-byte bank groups of a
+// 128-byte line by g(x2) = (x0^x3^x6, x1^x4^x7, x2^x5^x8): the bank group of
+// piece q of block x2 is a bijective function of g(x2) for every q, for the
+// tagged rows (64-byte blocks) and the plain rows (32-byte blocks) alike.
+// Blocks of a cube of middle masks whose spanning bits fall in different
+// residues mod 3 then never share a bank group.
+__device__ inline int tpos(int x2, int q) {
+    const int slot = x2 ^ (((x2 >> 3) ^ (x2 >> 6)) & 1);
+    const int g12 = (((x2 >> 1) ^ (x2 >> 4) ^ (x2 >> 7)) & 1) | ((((x2 >> 2) ^ (x2 >> 5) ^ (x2 >> 8)) & 1) << 1);
+    return (slot << CB) | ((q ^ g12) << 1);
+}
+__device__ inline int ppos(int x2, int q) {
+    const int slot = x2 ^ (((x2 >> 3) ^ (x2 >> 6)) & 1) ^ ((((x2 >> 4) ^ (x2 >> 7)) & 1) << 1);
+    const int g2 = ((x2 >> 2) ^ (x2 >> 5) ^ (x2 >> 8)) & 1;
+    return (slot << 2) | ((q ^ g2) << 1);
 }
 
-__device__ inline void load_block(const uint64_t *row, int x2, uint64_t v[NB]) {
-    const ulonglong2 *p = reinterpret_cast<const ulonglong2 *>(row + (x2 << CB));
-    const int s = (x2 >> 1) & 3;
+template <class K> struct Vec2;
+template <> struct Vec2<uint64_t> { using type = ulonglong2; };
+template <> struct Vec2<double> { using type = double2; };
+
+template <class K>
+__device__ inline void load_t(const K *row, int x2, K v[NB]) {
+    using V = typename Vec2<K>::type;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-        ulonglong2 t = p[q ^ s];
+        const V t = *reinterpret_cast<const V *>(row + tpos(x2, q));
         v[2 * q] = t.x;
         v[2 * q + 1] = t.y;
     }
 }
 
-// row X_H of the packed table, global -> LDS (swizzled)
-__device__ inline void load_row(uint64_t *row, const uint64_t *C, uint32_t xh) {
-    const ulonglong2 *src = reinterpret_cast<const ulonglong2 *>(C + ((size_t)xh << L));
-    for (int g = threadIdx.x; g < ROW / 2; g += THREADS) {
-        const int x2 = g >> 2, q = g & 3;
-        const ulonglong2 t = src[g];
-        ulonglong2 *dst = reinterpret_cast<ulonglong2 *>(row + (x2 << CB));
-        dst[q ^ ((x2 >> 1) & 3)] = t;
+template <class K>
+__device__ inline void load_p(const K *row, int x2, K v[NE]) {
+    using V = typename Vec2<K>::type;
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+        const V t = *reinterpret_cast<const V *>(row + ppos(x2, q));
+        v[2 * q] = t.x;
+        v[2 * q + 1] = t.y;
     }
 }
 
-__device__ inline uint64_t umin64(uint64_t a, uint64_t b) { return b < a ? b : a; }
+// row X_H of the packed table (global) -> plain and tagged LDS copies
+template <class K>
+__device__ inline void load_row(K *P, K *Tt, const uint64_t *__restrict__ C, uint32_t xh) {
+    const ulonglong2 *src = reinterpret_cast<const ulonglong2 *>(C + ((size_t)xh << L));
+    const uint32_t tag = xh << L;
+    for (int g = threadIdx.x; g < ROW / 2; g += THREADS) {
+        const int x2 = g >> 2, q = g & 3;                  // entries 2q, 2q+1 of block x2
+        const ulonglong2 v = src[g];
+        const uint32_t idx = tag | (uint32_t)(2 * g);
+        using V = typename Vec2<K>::type;
+        V t;
+        t.x = Key<K>::tagged(v.x, idx);
+        t.y = Key<K>::tagged(v.y, idx + 1u);
+        *reinterpret_cast<V *>(Tt + tpos(x2, q)) = t;
+        P[ppos(x2, q >> 1) + (q & 1)] = Key<K>::plain(v.x);
+    }
+}
 
 // deposit the low bits of t into the set bits of mask (in order)
 __device__ inline uint32_t deposit(uint32_t t, uint32_t mask) {
@@ -471,22 +546,15 @@ __device__ inline uint32_t deposit(uint32_t t, uint32_t mask) {
     return r;
 }
 
-// CB-bit min-plus subset convolution of one block pair.
-//   best[S1] = min(best[S1], min over A1 in S1 of key(A1, S1 ^ A1))
-// key = a[A1] + b[B1] + canon, canon = A-side mask if the A side holds
-// lowbit(S1) (for S1 = 0: if orient_a), else B-side mask.
-__device__ inline void conv_block(const uint64_t a[NB], const uint64_t b[NB], uint32_t canon_a,
-                                  uint32_t canon_b, bool orient_a, uint64_t best[NB]) {
-    uint64_t aa[NB], bb[NB];
-#pragma unroll
-    for (int x = 0; x < NB; ++x) {
-        aa[x] = a[x] | (uint64_t)(canon_a | (uint32_t)x);
-        bb[x] = b[x] | (uint64_t)(canon_b | (uint32_t)x);
-    }
-    {
-        const uint64_t c = orient_a ? aa[0] + b[0] : a[0] + bb[0];
-        best[0] = umin64(best[0], c);
-    }
+// CB-bit min-plus subset convolution of one block pair:
+//   best[S1] = min(best[S1], min over A1 in S1 of key(A1, S1 ^ A1)).
+// A side holds lowbit(S1) -> T(A) + P(B); otherwise P(A) + T(B). Either
+// way the plain operand has an even low part. For S1 = 0 the side is
+// orient_a.
+template <class K>
+__device__ inline void conv_block(const K pa[NE], const K ta[NB], const K pb[NE], const K tb[NB], bool orient_a,
+                                  K best[NB]) {
+    best[0] = Key<K>::min(best[0], orient_a ? Key<K>::add(ta[0], pb[0]) : Key<K>::add(pa[0], tb[0]));
 #pragma unroll
     for (int s1 = 1; s1 < NB; ++s1) {
         const int low = s1 & -s1;
@@ -494,17 +562,25 @@ __device__ inline void conv_block(const uint64_t a[NB], const uint64_t b[NB], ui
         for (int a1 = 0; a1 < NB; ++a1) {
             if (a1 & ~s1) continue;
             const int b1 = s1 ^ a1;
-            const uint64_t c = (a1 & low) ? aa[a1] + b[b1] : a[a1] + bb[b1];
-            best[s1] = umin64(best[s1], c);
+            const K c = (a1 & low) ? Key<K>::add(ta[a1], pb[b1 >> 1]) : Key<K>::add(pa[a1 >> 1], tb[b1]);
+            best[s1] = Key<K>::min(best[s1], c);
         }
     }
 }
 
-// one work item against the row pair (rowA = A-side rows, rowB = B-side)
-// item A2 range: chunk j of the submasks of S2; skip_full drops A2 == S2,
-// skip_empty drops A2 == 0
-__device__ inline void run_item(uint32_t item, const uint64_t *rowA, const uint64_t *rowB, uint32_t a_hi,
-                                uint32_t b_hi, bool skip_full, bool skip_empty, uint64_t *acc) {
+template <class K>
+__device__ inline void flush(const K best[NB], uint32_t s2, uint64_t *acc) {
+#pragma unroll
+    for (int x = 0; x < NB; ++x)
+        if (best[x] != Key<K>::none())
+            atomicMin((unsigned long long *)&acc[(s2 << CB) | x], (unsigned long long)Key<K>::bits(best[x]));
+}
+
+// one self-pair work item: chunk j of the submasks A2 of S2 against
+// (rowS, row0); skip A2 == S2, and A2 == 0 when skip_empty
+template <class K>
+__device__ inline void run_item(uint32_t item, const K *pA, const K *tA, const K *pB, const K *tB, uint64_t *acc,
+                                bool skip_empty) {
     const uint32_t s2 = item & 0xffffu;
     const uint32_t j = item >> 16;
     const int k = __popc(s2);
@@ -512,53 +588,46 @@ __device__ inline void run_item(uint32_t item, const uint64_t *rowA, const uint6
     const uint32_t cnt = 1u << tb;
     const uint32_t low2 = s2 & (0u - s2);
     uint32_t a2 = deposit(j << tb, s2);
-    uint64_t best[NB];
+    K best[NB];
 #pragma unroll
-    for (int x = 0; x < NB; ++x) best[x] = ~0ull;
+    for (int x = 0; x < NB; ++x) best[x] = Key<K>::none();
     for (uint32_t i = 0; i < cnt; ++i) {
         const uint32_t b2 = s2 ^ a2;
-        if (!((skip_full && b2 == 0) || (skip_empty && a2 == 0))) {
-            uint64_t a[NB], b[NB];
-            load_block(rowA, (int)a2, a);
-            load_block(rowB, (int)b2, b);
-            const bool orient_a = (s2 == 0) || (a2 & low2);
-            conv_block(a, b, a_hi | (a2 << CB), b_hi | (b2 << CB), orient_a, best);
+        if (b2 != 0 && !(skip_empty && a2 == 0)) {
+            K pa[NE], ta[NB], pb[NE], tb2[NB];
+            load_p(pA, (int)a2, pa);
+            load_t(tA, (int)a2, ta);
+            load_p(pB, (int)b2, pb);
+            load_t(tB, (int)b2, tb2);
+            conv_block<K>(pa, ta, pb, tb2, (s2 == 0) || (a2 & low2), best);
         }
         a2 = ((a2 | ~s2) + 1u) & s2;
     }
-#pragma unroll
-    for (int x = 0; x < NB; ++x)
-        if (best[x] != ~0ull) atomicMin((unsigned long long *)&acc[(s2 << CB) | x], (unsigned long long)best[x]);
+    flush<K>(best, s2, acc);
 }
 
-// Complete row S_H: acc holds the best cross-pair keys (or ~0); rowS is
-// the LDS buffer that receives row S_H; row0 holds row 0 (the same buffer
-// as rowS when S_H = 0). Writes C' and split to global memory.
-__device__ void finalize_row(int m, uint32_t sh, uint64_t *rowS, const uint64_t *row0, uint64_t *acc,
-                             const int64_t *__restrict__ W, uint64_t *__restrict__ Cp,
-                             uint32_t *__restrict__ split) {
+// Complete row S_H. s.acc holds the best cross-pair key bits (or ~0);
+// (pS, tS) receive row S_H, (s.pb, s.tb) hold row 0 -- the same buffers
+// when S_H = 0, in which case they are filled here. Writes C' and split.
+template <class K>
+__device__ void finalize_row(int m, uint32_t sh, Lds<K> &s, K *pS, K *tS, const int64_t *__restrict__ W,
+                             uint64_t *__restrict__ Cp, uint32_t *__restrict__ split) {
     const uint32_t a_hi = sh << L;
     const uint64_t mask = ((uint64_t)1 << m) - 1u;
-    uint64_t b0[NB];                         // row 0, block 0 (complete unless S_H = 0)
-    if (sh != 0) load_block(row0, 0, b0);
     for (int k = 0; k <= R2; ++k) {
-        // A2 a proper submask of S2 (and, for S_H = 0, not empty: those
-        // pairs are the mirrors of the in-block pairs below)
+        // A2 a proper submask of S2 (for S_H = 0 also non-empty: those pairs
+        // mirror the in-block pairs below)
         for (int it = kItems.begin[k] + threadIdx.x; it < kItems.end[k]; it += THREADS)
-            run_item(c_items.v[it], rowS, row0, a_hi, 0u, true, sh == 0, acc);
+            run_item<K>(c_items.v[it], pS, tS, s.pb, s.tb, s.acc, sh == 0);
         __syncthreads();
         // A2 = S2: in-block pairs, one thread per block of this level
         for (int bi = c_blocks.begin[k] + threadIdx.x; bi < c_blocks.end[k]; bi += THREADS) {
             const uint32_t s2 = c_blocks.v[bi];
             const uint32_t base = a_hi | (s2 << CB);
+            uint64_t b0[NB];
+#pragma unroll
+            for (int x = 0; x < NB; ++x) b0[x] = s.blk0[x];
             uint64_t out[NB];
-            int64_t w[NB];
-            const int64_t *wp = W + base;
-#pragma unroll
-            for (int x = 0; x < NB; ++x) w[x] = wp[x];
-            uint64_t key[NB];
-#pragma unroll
-            for (int x = 0; x < NB; ++x) key[x] = acc[(s2 << CB) | x];
             uint32_t sp[NB];
             // S1 in order of popcount so that every A1 < S1 is ready
 #pragma unroll
@@ -567,9 +636,10 @@ __device__ void finalize_row(int m, uint32_t sh, uint64_t *rowS, const uint64_t 
                 for (int s1 = 0; s1 < NB; ++s1) {
                     if (cpop(s1) != pc) continue;
                     const uint32_t S = base | (uint32_t)s1;
+                    const int64_t w = W[S];
                     if (S == 0) { out[s1] = SENT; sp[s1] = 0; continue; }
-                    if (__popc(S) == 1) { out[s1] = (uint64_t)w[s1] << m; sp[s1] = 0; continue; }
-                    uint64_t kb = key[s1];
+                    if (__popc(S) == 1) { out[s1] = (uint64_t)w << m; sp[s1] = 0; continue; }
+                    uint64_t kb = Key<K>::value_of_bits(s.acc[(s2 << CB) | s1]);
                     const int low = s1 & -s1;
 #pragma unroll
                     for (int a1 = 0; a1 < NB; ++a1) {
@@ -577,42 +647,39 @@ __device__ void finalize_row(int m, uint32_t sh, uint64_t *rowS, const uint64_t 
                         const int b1 = s1 ^ a1;
                         const uint64_t av = out[a1];
                         const uint64_t bv = (sh == 0 && s2 == 0) ? out[b1] : b0[b1];
-                        const uint64_t c = (a1 & low) ? (av | (uint64_t)(base | (uint32_t)a1)) + bv
-                                                      : av + (bv | (uint64_t)(uint32_t)b1);
-                        kb = umin64(kb, c);
+                        const uint64_t c = (a1 & low) ? av + bv + (base | (uint32_t)a1) : av + bv + (uint32_t)b1;
+                        kb = c < kb ? c : kb;
                     }
-                    out[s1] = ((kb >> m) - (uint64_t)w[s1]) << m;
+                    out[s1] = ((kb >> m) - (uint64_t)w) << m;
                     sp[s1] = (uint32_t)(kb & mask);
                 }
             }
 #pragma unroll
             for (int x = 0; x < NB; ++x) {
-                rowS[lds_pos((int)s2, x)] = out[x];
+                tS[tpos((int)s2, x >> 1) + (x & 1)] = Key<K>::tagged(out[x], base | (uint32_t)x);
+                if (!(x & 1)) pS[ppos((int)s2, x >> 2) + ((x >> 1) & 1)] = Key<K>::plain(out[x]);
                 Cp[base + x] = out[x];
                 split[base + x] = sp[x];
             }
+            if (sh == 0 && s2 == 0) {
+#pragma unroll
+                for (int x = 0; x < NB; ++x) s.blk0[x] = out[x];
+            }
         }
         __syncthreads();
-        if (sh == 0 && k == 0) load_block(row0, 0, b0);   // row 0's block 0 is now complete
     }
 }
 
-struct Lds {
-    uint64_t rowA[ROW];
-    uint64_t rowB[ROW];
-    uint64_t acc[ROW];
-};
-
 // cross pairs of one (S_H, chunk); fused = finish the row in place
+template <class K>
 __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_pairs, uint32_t chunks,
                                                       uint32_t per_chunk, int fused, const int64_t *__restrict__ W,
                                                       uint64_t *__restrict__ Cp, uint32_t *__restrict__ split,
                                                       uint64_t *__restrict__ partial) {
-    __shared__ Lds s;
+    __shared__ Lds<K> s;
     const uint32_t bid = xcd_block(blockIdx.x, gridDim.x);
     const uint32_t r = bid / chunks, j = bid % chunks;
-    const int m_hi = m - L;
-    const uint32_t sh = unrank_colex(r, h, m_hi);
+    const uint32_t sh = unrank_colex(r, h, m - L);
     const uint32_t lowh = sh & (0u - sh);
     const uint32_t rest = sh ^ lowh;
     for (int e = threadIdx.x; e < ROW; e += THREADS) s.acc[e] = ~0ull;
@@ -622,18 +689,41 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
     for (uint32_t t = t0; t < t1; ++t) {
         const uint32_t bh = sh ^ ah;
         __syncthreads();
-        load_row(s.rowA, Cp, ah);
-        load_row(s.rowB, Cp, bh);
+        load_row<K>(s.pa, s.ta, Cp, ah);
+        load_row<K>(s.pb, s.tb, Cp, bh);
         __syncthreads();
-        for (int it = threadIdx.x; it < kItems.n; it += THREADS)
-            run_item(c_items.v[it], s.rowA, s.rowB, ah << L, bh << L, false, false, s.acc);
+        // items are ordered by |S2| from the top, so the lanes of a wave
+        // run the same number of iterations and flush together
+        for (int it = threadIdx.x; it < kItems.n; it += THREADS) {
+            const uint32_t item = c_items.v[it];
+            const uint32_t s2 = item & 0xffffu;
+            const int k = __popc(s2);
+            const int tb = k < T ? k : T;
+            const uint32_t low2 = s2 & (0u - s2);
+            uint32_t a2 = deposit((item >> 16) << tb, s2);
+            K best[NB];
+#pragma unroll
+            for (int x = 0; x < NB; ++x) best[x] = Key<K>::none();
+            for (uint32_t i = 0; i < (1u << tb); ++i) {
+                const uint32_t b2 = s2 ^ a2;
+                K pa[NE], ta[NB], pb[NE], tb2[NB];
+                load_p(s.pa, (int)a2, pa);
+                load_t(s.ta, (int)a2, ta);
+                load_p(s.pb, (int)b2, pb);
+                load_t(s.tb, (int)b2, tb2);
+                conv_block<K>(pa, ta, pb, tb2, (s2 == 0) || (a2 & low2), best);
+                a2 = ((a2 | ~s2) + 1u) & s2;
+            }
+            flush<K>(best, s2, s.acc);
+        }
         ah = lowh | (((ah | ~rest) + 1u) & rest);    // next A_H holding lowbit(S_H)
     }
     __syncthreads();
     if (fused) {
-        load_row(s.rowB, Cp, 0u);
+        if (threadIdx.x < NB) s.blk0[threadIdx.x] = Cp[threadIdx.x];
+        load_row<K>(s.pb, s.tb, Cp, 0u);
         __syncthreads();
-        finalize_row(m, sh, s.rowA, s.rowB, s.acc, W, Cp, split);
+        finalize_row<K>(m, sh, s, s.pa, s.ta, W, Cp, split);
     } else {
         uint64_t *dst = partial + (size_t)bid * ROW;
         for (int e = threadIdx.x; e < ROW; e += THREADS) dst[e] = s.acc[e];
@@ -641,31 +731,37 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
 }
 
 // min over the chunks of one S_H, into chunk 0's slot; 256 entries per block
-__global__ __launch_bounds__(THREADS) void k_rb_reduce(uint32_t chunks, uint64_t *__restrict__ partial) {
-    const uint32_t r = blockIdx.x / (ROW / THREADS);
-    const uint32_t e = (blockIdx.x % (ROW / THREADS)) * THREADS + threadIdx.x;
+__global__ __launch_bounds__(256) void k_rb_reduce(uint32_t chunks, uint64_t *__restrict__ partial) {
+    const uint32_t r = blockIdx.x / (ROW / 256);
+    const uint32_t e = (blockIdx.x % (ROW / 256)) * 256 + threadIdx.x;
     uint64_t *base = partial + (size_t)r * chunks * ROW + e;
     uint64_t v = base[0];
-    for (uint32_t j = 1; j < chunks; ++j) v = umin64(v, base[(size_t)j * ROW]);
+    for (uint32_t j = 1; j < chunks; ++j) {
+        const uint64_t o = base[(size_t)j * ROW];
+        v = o < v ? o : v;
+    }
     base[0] = v;
 }
 
 // finish the rows of one level: acc from the reduced partials (chunks > 0)
 // or empty (levels 0 and 1 have no cross pairs)
+template <class K>
 __global__ __launch_bounds__(THREADS) void k_rb_final(int m, int h, uint32_t chunks, const int64_t *__restrict__ W,
                                                       uint64_t *__restrict__ Cp, uint32_t *__restrict__ split,
                                                       const uint64_t *__restrict__ partial) {
-    __shared__ Lds s;
+    __shared__ Lds<K> s;
     const uint32_t r = blockIdx.x;
     const uint32_t sh = unrank_colex(r, h, m - L);
     const uint64_t *src = partial + (size_t)r * chunks * ROW;
-    for (int e = threadIdx.x; e < ROW; e += THREADS) {
-        s.acc[e] = chunks ? src[e] : ~0ull;
-        s.rowA[e] = 0;
+    for (int e = threadIdx.x; e < ROW; e += THREADS) s.acc[e] = chunks ? src[e] : ~0ull;
+    if (sh != 0) {
+        if (threadIdx.x < NB) s.blk0[threadIdx.x] = Cp[threadIdx.x];
+        load_row<K>(s.pb, s.tb, Cp, 0u);
     }
-    if (sh != 0) load_row(s.rowB, Cp, 0u);
     __syncthreads();
-    finalize_row(m, sh, s.rowA, sh == 0 ? s.rowA : s.rowB, s.acc, W, Cp, split);
+    // for S_H = 0 the output row is row 0 itself
+    if (sh == 0) finalize_row<K>(m, sh, s, s.pb, s.tb, W, Cp, split);
+    else finalize_row<K>(m, sh, s, s.pa, s.ta, W, Cp, split);
 }
 
 // packed C' -> C (C[0] keeps the documented sentinel)
@@ -924,6 +1020,7 @@ int check_common(int m, int64_t n_chunks, int64_t nnz) {
     return MPT_OK;
 }
 
+template <class K>
 int solve_rb(int m, const int64_t *W, int64_t *C, uint32_t *split, uint64_t *partial, hipStream_t s) {
     uint64_t *Cp = (uint64_t *)C;
     double pair_work = 1.0;
@@ -931,24 +1028,24 @@ int solve_rb(int m, const int64_t *W, int64_t *C, uint32_t *split, uint64_t *par
     for (const RbLevel &P : rb_plan(m)) {
         if (P.n_pairs == 0) {
             LaunchScope ls("rb_final", pair_work * P.n_sets, s);
-            rb::k_rb_final<<<P.n_sets, rb::THREADS, 0, s>>>(m, P.h, 0u, W, Cp, split, partial);
+            rb::k_rb_final<K><<<P.n_sets, rb::THREADS, 0, s>>>(m, P.h, 0u, W, Cp, split, partial);
         } else if (P.chunks == 1) {
             LaunchScope ls("rb_cross", pair_work * (double)P.n_sets * (P.n_pairs + 1), s);
-            rb::k_rb_cross<<<P.n_sets, rb::THREADS, 0, s>>>(m, P.h, P.n_pairs, 1u, P.n_pairs, 1, W, Cp, split,
-                                                            partial);
+            rb::k_rb_cross<K><<<P.n_sets, rb::THREADS, 0, s>>>(m, P.h, P.n_pairs, 1u, P.n_pairs, 1, W, Cp, split,
+                                                               partial);
         } else {
             {
                 LaunchScope ls("rb_cross", pair_work * (double)P.n_sets * P.n_pairs, s);
-                rb::k_rb_cross<<<P.n_sets * P.chunks, rb::THREADS, 0, s>>>(m, P.h, P.n_pairs, P.chunks,
-                                                                           P.per_chunk, 0, W, Cp, split, partial);
+                rb::k_rb_cross<K><<<P.n_sets * P.chunks, rb::THREADS, 0, s>>>(m, P.h, P.n_pairs, P.chunks,
+                                                                              P.per_chunk, 0, W, Cp, split, partial);
             }
             {
                 LaunchScope ls("rb_reduce", (double)P.n_sets * P.chunks * rb::ROW * 8.0, s);
-                rb::k_rb_reduce<<<P.n_sets * (rb::ROW / rb::THREADS), rb::THREADS, 0, s>>>(P.chunks, partial);
+                rb::k_rb_reduce<<<P.n_sets * (rb::ROW / 256), 256, 0, s>>>(P.chunks, partial);
             }
             {
                 LaunchScope ls("rb_final", pair_work * P.n_sets, s);
-                rb::k_rb_final<<<P.n_sets, rb::THREADS, 0, s>>>(m, P.h, P.chunks, W, Cp, split, partial);
+                rb::k_rb_final<K><<<P.n_sets, rb::THREADS, 0, s>>>(m, P.h, P.chunks, W, Cp, split, partial);
             }
         }
         HIP_TRY(hipGetLastError());
@@ -1053,8 +1150,14 @@ extern "C" int mpt_solve_exact(int m, const int64_t *W, int64_t *C, uint32_t *sp
         int64_t total = 0;
         HIP_TRY(hipMemcpyAsync(&total, &h->pad[0], sizeof total, hipMemcpyDeviceToHost, s));
         HIP_TRY(hipStreamSynchronize(s));
+        // keys below 2^53 are exact doubles; below 2^62 they fit uint64
         if (total < ((int64_t)1 << (61 - m))) {
-            rc = solve_rb(m, W, C, split, (uint64_t *)(ws + L.rb_part), s);
+            uint64_t *part = (uint64_t *)(ws + L.rb_part);
+#ifndef MPT_RB_NO_DOUBLE
+#define MPT_RB_NO_DOUBLE 0
+#endif
+            rc = (!MPT_RB_NO_DOUBLE && total < ((int64_t)1 << (52 - m))) ? solve_rb<double>(m, W, C, split, part, s)
+                                                   : solve_rb<uint64_t>(m, W, C, split, part, s);
             if (rc) return rc;
             if (opt_cost) {
                 HIP_TRY(hipMemcpyAsync(opt_cost, C + (n - 1), sizeof(int64_t), hipMemcpyDeviceToHost, s));
