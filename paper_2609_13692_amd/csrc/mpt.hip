@@ -397,8 +397,19 @@ constexpr uint64_t SENT = (uint64_t)1 << 62;
 
 constexpr int cpop(int x) { int c = 0; while (x) { c += x & 1; x >>= 1; } return c; }
 
-// work items of the self pair: (S2, chunk of 2^T submasks A2 of S2),
-// grouped by |S2| from R2 down to 0
+constexpr uint32_t cdeposit(uint32_t t, uint32_t mask) {
+    uint32_t r = 0;
+    while (t && mask) {
+        const uint32_t bit = mask & (0u - mask);
+        mask ^= bit;
+        if (t & 1u) r |= bit;
+        t >>= 1;
+    }
+    return r;
+}
+
+// work items: (S2, first A2 of a chunk of 2^T submasks of S2 in increasing
+// order), grouped by |S2| from R2 down to 0; entry = S2 | first A2 << 16
 struct Items {
     uint32_t v[8192];
     int begin[R2 + 1];
@@ -412,8 +423,9 @@ constexpr Items make_items() {
         it.begin[k] = n;
         for (int s = 0; s < NS2; ++s) {
             if (cpop(s) != k) continue;
-            int chunks = k > T ? 1 << (k - T) : 1;
-            for (int j = 0; j < chunks; ++j) it.v[n++] = (uint32_t)s | ((uint32_t)j << 16);
+            const int tb = k < T ? k : T;
+            const int chunks = 1 << (k - tb);
+            for (int j = 0; j < chunks; ++j) it.v[n++] = (uint32_t)s | (cdeposit((uint32_t)j << tb, (uint32_t)s) << 16);
         }
         it.end[k] = n;
     }
@@ -463,54 +475,47 @@ template <> struct Key<double> {
     }
 };
 
-template <class K> struct alignas(16) Lds {
-    K pa[NS2 * NE];        // row on the A side, plain, even low parts
-    K ta[ROW];             // row on the A side, tagged
-    K pb[NS2 * NE];        // row on the B side, plain, even low parts
-    K tb[ROW];             // row on the B side, tagged
-    uint64_t acc[ROW];     // best key bits per entry of the output row
-    uint64_t blk0[NB];     // plain C' of row 0, block 0
-};
+// LDS rows. Block x2 sits at slot(x2) = x2 ^ (x2 >> 3 & 7) ^ (x2 >> 6 & 7),
+// a GF(2)-linear bijection, so slot(S2 ^ A2) = slot(S2) ^ slot(A2). Blocks
+// are padded to 80 bytes (tagged, 8 entries) and 48 bytes (plain, the 4
+// even entries): piece q of a block then falls in 16-byte bank group
+// (5 slot + q) mod 8 or (3 slot + q) mod 8, a bijection of slot mod 8, and
+// a lane's four (or two) 16-byte reads use immediate offsets.
+constexpr int TSTRIDE = 10;           // K elements per tagged block
+constexpr int PSTRIDE = 6;            // K elements per plain block
+__device__ inline uint32_t slot_of(uint32_t x2) { return x2 ^ ((x2 >> 3) & 7u) ^ ((x2 >> 6) & 7u); }
 
-// LDS positions. Lanes read whole blocks of different middle masks x2, so
-// the 16-byte pieces are spread over the eight 16-byte bank groups of a
-// 128-byte line by g(x2) = (x0^x3^x6, x1^x4^x7, x2^x5^x8): the bank group of
-// piece q of block x2 is a bijective function of g(x2) for every q, for the
-// tagged rows (64-byte blocks) and the plain rows (32-byte blocks) alike.
-// Blocks of a cube of middle masks whose spanning bits fall in different
-// residues mod 3 then never share a bank group.
-__device__ inline int tpos(int x2, int q) {
-    const int slot = x2 ^ (((x2 >> 3) ^ (x2 >> 6)) & 1);
-    const int g12 = (((x2 >> 1) ^ (x2 >> 4) ^ (x2 >> 7)) & 1) | ((((x2 >> 2) ^ (x2 >> 5) ^ (x2 >> 8)) & 1) << 1);
-    return (slot << CB) | ((q ^ g12) << 1);
-}
-__device__ inline int ppos(int x2, int q) {
-    const int slot = x2 ^ (((x2 >> 3) ^ (x2 >> 6)) & 1) ^ ((((x2 >> 4) ^ (x2 >> 7)) & 1) << 1);
-    const int g2 = ((x2 >> 2) ^ (x2 >> 5) ^ (x2 >> 8)) & 1;
-    return (slot << 2) | ((q ^ g2) << 1);
-}
+template <class K> struct alignas(16) Lds {
+    K pa[NS2 * PSTRIDE];   // row on the A side, plain, even low parts
+    K ta[NS2 * TSTRIDE];   // row on the A side, tagged
+    K pb[NS2 * PSTRIDE];   // row on the B side, plain, even low parts
+    K tb[NS2 * TSTRIDE];   // row on the B side, tagged
+    uint64_t acc[ROW];     // best key bits per entry of the output row
+};
 
 template <class K> struct Vec2;
 template <> struct Vec2<uint64_t> { using type = ulonglong2; };
 template <> struct Vec2<double> { using type = double2; };
 
 template <class K>
-__device__ inline void load_t(const K *row, int x2, K v[NB]) {
+__device__ inline void load_t(const K *row, uint32_t slot, K v[NB]) {
     using V = typename Vec2<K>::type;
+    const V *p = reinterpret_cast<const V *>(row + slot * TSTRIDE);
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-        const V t = *reinterpret_cast<const V *>(row + tpos(x2, q));
+        const V t = p[q];
         v[2 * q] = t.x;
         v[2 * q + 1] = t.y;
     }
 }
 
 template <class K>
-__device__ inline void load_p(const K *row, int x2, K v[NE]) {
+__device__ inline void load_p(const K *row, uint32_t slot, K v[NE]) {
     using V = typename Vec2<K>::type;
+    const V *p = reinterpret_cast<const V *>(row + slot * PSTRIDE);
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
-        const V t = *reinterpret_cast<const V *>(row + ppos(x2, q));
+        const V t = p[q];
         v[2 * q] = t.x;
         v[2 * q + 1] = t.y;
     }
@@ -526,11 +531,12 @@ __device__ inline void load_row(K *P, K *Tt, const uint64_t *__restrict__ C, uin
         const ulonglong2 v = src[g];
         const uint32_t idx = tag | (uint32_t)(2 * g);
         using V = typename Vec2<K>::type;
+        const uint32_t sl = slot_of((uint32_t)x2);
         V t;
         t.x = Key<K>::tagged(v.x, idx);
         t.y = Key<K>::tagged(v.y, idx + 1u);
-        *reinterpret_cast<V *>(Tt + tpos(x2, q)) = t;
-        P[ppos(x2, q >> 1) + (q & 1)] = Key<K>::plain(v.x);
+        *reinterpret_cast<V *>(Tt + sl * TSTRIDE + 2 * q) = t;
+        P[sl * PSTRIDE + q] = Key<K>::plain(v.x);
     }
 }
 
@@ -576,34 +582,42 @@ __device__ inline void flush(const K best[NB], uint32_t s2, uint64_t *acc) {
             atomicMin((unsigned long long *)&acc[(s2 << CB) | x], (unsigned long long)Key<K>::bits(best[x]));
 }
 
-// one self-pair work item: chunk j of the submasks A2 of S2 against
-// (rowS, row0); skip A2 == S2, and A2 == 0 when skip_empty
+// one self-pair work item (S2, first A2) against (rowS, row0): 2^min(|S2|,T)
+// submasks A2 of S2 in increasing order, skipping A2 == S2 and, when
+// skip_empty, A2 == 0
 template <class K>
 __device__ inline void run_item(uint32_t item, const K *pA, const K *tA, const K *pB, const K *tB, uint64_t *acc,
                                 bool skip_empty) {
     const uint32_t s2 = item & 0xffffu;
-    const uint32_t j = item >> 16;
     const int k = __popc(s2);
-    const int tb = k < T ? k : T;
-    const uint32_t cnt = 1u << tb;
+    const uint32_t cnt = 1u << (k < T ? k : T);
     const uint32_t low2 = s2 & (0u - s2);
-    uint32_t a2 = deposit(j << tb, s2);
+    const uint32_t slot_s2 = slot_of(s2);
+    uint32_t a2 = item >> 16;
     K best[NB];
 #pragma unroll
     for (int x = 0; x < NB; ++x) best[x] = Key<K>::none();
     for (uint32_t i = 0; i < cnt; ++i) {
         const uint32_t b2 = s2 ^ a2;
         if (b2 != 0 && !(skip_empty && a2 == 0)) {
+            const uint32_t sa = slot_of(a2), sb = slot_s2 ^ sa;
             K pa[NE], ta[NB], pb[NE], tb2[NB];
-            load_p(pA, (int)a2, pa);
-            load_t(tA, (int)a2, ta);
-            load_p(pB, (int)b2, pb);
-            load_t(tB, (int)b2, tb2);
+            load_p(pA, sa, pa);
+            load_t(tA, sa, ta);
+            load_p(pB, sb, pb);
+            load_t(tB, sb, tb2);
             conv_block<K>(pa, ta, pb, tb2, (s2 == 0) || (a2 & low2), best);
         }
         a2 = ((a2 | ~s2) + 1u) & s2;
     }
     flush<K>(best, s2, acc);
+}
+
+// plain C' of an entry of a tagged LDS row whose tag is the entry's own
+// mask (exact: the tag occupies the low m bits that C' leaves zero)
+template <class K>
+__device__ inline uint64_t untag(K t, uint32_t idx) {
+    return Key<K>::value_of_bits(Key<K>::bits(t)) - idx;
 }
 
 // Complete row S_H. s.acc holds the best cross-pair key bits (or ~0);
@@ -624,9 +638,13 @@ __device__ void finalize_row(int m, uint32_t sh, Lds<K> &s, K *pS, K *tS, const 
         for (int bi = c_blocks.begin[k] + threadIdx.x; bi < c_blocks.end[k]; bi += THREADS) {
             const uint32_t s2 = c_blocks.v[bi];
             const uint32_t base = a_hi | (s2 << CB);
+            // row 0, block 0 (complete, except while S_H = 0 builds it: then
+            // it is this very block and out[] is used instead)
             uint64_t b0[NB];
+            if (!(sh == 0 && s2 == 0)) {
 #pragma unroll
-            for (int x = 0; x < NB; ++x) b0[x] = s.blk0[x];
+                for (int x = 0; x < NB; ++x) b0[x] = untag<K>(s.tb[x], (uint32_t)x);
+            }
             uint64_t out[NB];
             uint32_t sp[NB];
             // S1 in order of popcount so that every A1 < S1 is ready
@@ -654,16 +672,13 @@ __device__ void finalize_row(int m, uint32_t sh, Lds<K> &s, K *pS, K *tS, const 
                     sp[s1] = (uint32_t)(kb & mask);
                 }
             }
+            const uint32_t sl = slot_of(s2);
 #pragma unroll
             for (int x = 0; x < NB; ++x) {
-                tS[tpos((int)s2, x >> 1) + (x & 1)] = Key<K>::tagged(out[x], base | (uint32_t)x);
-                if (!(x & 1)) pS[ppos((int)s2, x >> 2) + ((x >> 1) & 1)] = Key<K>::plain(out[x]);
+                tS[sl * TSTRIDE + x] = Key<K>::tagged(out[x], base | (uint32_t)x);
+                if (!(x & 1)) pS[sl * PSTRIDE + (x >> 1)] = Key<K>::plain(out[x]);
                 Cp[base + x] = out[x];
                 split[base + x] = sp[x];
-            }
-            if (sh == 0 && s2 == 0) {
-#pragma unroll
-                for (int x = 0; x < NB; ++x) s.blk0[x] = out[x];
             }
         }
         __syncthreads();
@@ -692,35 +707,35 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
         load_row<K>(s.pa, s.ta, Cp, ah);
         load_row<K>(s.pb, s.tb, Cp, bh);
         __syncthreads();
-        // items are ordered by |S2| from the top, so the lanes of a wave
-        // run the same number of iterations and flush together
+        ah = lowh | (((ah | ~rest) + 1u) & rest);    // next A_H holding lowbit(S_H)
+        // items are ordered by |S2| from the top: the lanes of a wave run
+        // the same number of iterations and flush together
         for (int it = threadIdx.x; it < kItems.n; it += THREADS) {
             const uint32_t item = c_items.v[it];
             const uint32_t s2 = item & 0xffffu;
             const int k = __popc(s2);
-            const int tb = k < T ? k : T;
+            const uint32_t cnt = 1u << (k < T ? k : T);
             const uint32_t low2 = s2 & (0u - s2);
-            uint32_t a2 = deposit((item >> 16) << tb, s2);
+            const uint32_t slot_s2 = slot_of(s2);
+            uint32_t a2 = item >> 16;
             K best[NB];
 #pragma unroll
             for (int x = 0; x < NB; ++x) best[x] = Key<K>::none();
-            for (uint32_t i = 0; i < (1u << tb); ++i) {
-                const uint32_t b2 = s2 ^ a2;
+            for (uint32_t i = 0; i < cnt; ++i) {
+                const uint32_t sa = slot_of(a2), sb = slot_s2 ^ sa;
                 K pa[NE], ta[NB], pb[NE], tb2[NB];
-                load_p(s.pa, (int)a2, pa);
-                load_t(s.ta, (int)a2, ta);
-                load_p(s.pb, (int)b2, pb);
-                load_t(s.tb, (int)b2, tb2);
+                load_p(s.pa, sa, pa);
+                load_t(s.ta, sa, ta);
+                load_p(s.pb, sb, pb);
+                load_t(s.tb, sb, tb2);
                 conv_block<K>(pa, ta, pb, tb2, (s2 == 0) || (a2 & low2), best);
                 a2 = ((a2 | ~s2) + 1u) & s2;
             }
             flush<K>(best, s2, s.acc);
         }
-        ah = lowh | (((ah | ~rest) + 1u) & rest);    // next A_H holding lowbit(S_H)
     }
     __syncthreads();
     if (fused) {
-        if (threadIdx.x < NB) s.blk0[threadIdx.x] = Cp[threadIdx.x];
         load_row<K>(s.pb, s.tb, Cp, 0u);
         __syncthreads();
         finalize_row<K>(m, sh, s, s.pa, s.ta, W, Cp, split);
@@ -754,10 +769,7 @@ __global__ __launch_bounds__(THREADS) void k_rb_final(int m, int h, uint32_t chu
     const uint32_t sh = unrank_colex(r, h, m - L);
     const uint64_t *src = partial + (size_t)r * chunks * ROW;
     for (int e = threadIdx.x; e < ROW; e += THREADS) s.acc[e] = chunks ? src[e] : ~0ull;
-    if (sh != 0) {
-        if (threadIdx.x < NB) s.blk0[threadIdx.x] = Cp[threadIdx.x];
-        load_row<K>(s.pb, s.tb, Cp, 0u);
-    }
+    if (sh != 0) load_row<K>(s.pb, s.tb, Cp, 0u);
     __syncthreads();
     // for S_H = 0 the output row is row 0 itself
     if (sh == 0) finalize_row<K>(m, sh, s, s.pb, s.tb, W, Cp, split);
