@@ -10,8 +10,8 @@ cross-topic slots, log-normal passage lengths clipped to [60, 600] tokens),
 seed 0. The DP evaluates T = (3^m + 1)/2 - 2^m unordered bipartitions.
 
 Prints ONE JSON line. `value` = evaluated bipartitions per second over whole
-steps. `roofline` describes the dominant kernel (the DP wave kernel) against
-the integer VALU peak; `zeta` the W-table kernel against HBM bandwidth;
+steps. `roofline` describes the dominant kernel (the DP cross-pair kernel)
+against the VALU instruction peak; `zeta` the W-table kernel against HBM bandwidth;
 `cpu_baseline` the CPU oracle on a bounded sample of the same workload.
 """
 from __future__ import annotations
@@ -41,6 +41,32 @@ WORKLOADS = {
     4: "retrieval-shaped, m=24, u=5000, T=80 topics, k=20, seed 0",
     5: "retrieval-shaped, m=25, u=10000, T=100 topics, k=50, seed 0",
 }
+
+
+def profiled_traffic(label: str):
+    """HBM bytes per launch of the kernel `label` from the committed
+    rocprofv3 summaries (FETCH_SIZE + WRITE_SIZE, calibrated against a plain
+    copy), or None when no summary was taken from the current kernel source."""
+    import glob
+    import hashlib
+    import re
+    src = os.path.join(ROOT, "paper_2609_13692_amd", "csrc", "mpt.hip")
+    with open(src, "rb") as f:
+        sha = hashlib.sha256(f.read()).hexdigest()
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*.md"))):
+        with open(path) as f:
+            text = f.read()
+        m = re.search(r"```json\n(.*?)\n```", text, re.S)
+        if not m:
+            continue
+        data = json.loads(m.group(1))
+        if data.get("source_sha256") != sha:
+            continue
+        for name, k in data.get("kernels", {}).items():
+            if re.search(r"\bk_" + re.escape(label) + r"\b", name):
+                return {"bytes_per_launch": k["traffic_bytes_per_launch"],
+                        "summary": os.path.relpath(path, ROOT)}
+    return None
 
 
 def t_eval(m: int) -> int:
@@ -158,6 +184,7 @@ def main() -> int:
                 "bytes_per_launch": z["work"] / z["launches"],
                 "dense_zeta_equiv_GBps": round(2 * zgbs, 1)}
 
+    traffic = profiled_traffic(dom)
     line = {
         "metric": "submask transitions/sec (3^m DP) + zeta-transform HBM GB/s, per MI355X",
         "value": T / (ms / 1000.0),
@@ -182,7 +209,10 @@ def main() -> int:
                            for k, v in prof.items()}},
         "roofline": {"kernel": dom, "bound": "alu", "achieved": round(achieved_tops, 3),
                      "peak": round(VALU_PEAK_TOPS, 2), "unit": "TOP/s",
-                     "frac": round(achieved_tops / VALU_PEAK_TOPS, 4), "traffic": None,
+                     "frac": round(achieved_tops / VALU_PEAK_TOPS, 4),
+                     "traffic": round(traffic["bytes_per_launch"]) if traffic else None,
+                     "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
+                     "traffic_source": traffic["summary"] if traffic else None,
                      "avg_launch_ms": round(d["total_ms"] / d["launches"], 4),
                      "ops_per_launch": d["work"] * DP_OPS_PER_PAIR / d["launches"]},
         "zeta": zeta,
