@@ -77,7 +77,7 @@ size_t mpt_workspace_bytes(int m, int64_t nnz);
  *   req_chunks [nnz]       int32 chunk ids, distinct inside each request;
  *                          requests may be empty or equal to each other
  *   sig        [n_chunks]  out: uint32 S_x masks
- *   W          [2^m]       out: int64 table
+ *   W          [2^m]       out: int64 table, 16-byte aligned
  * Validates the device inputs (MPT_E_INVALID / RANGE / DUP / WEIGHT /
  * OVERFLOW) and synchronises `stream` to report the result.
  */

@@ -84,6 +84,15 @@ __device__ inline uint32_t xcd_block(uint32_t bid, uint32_t nblocks) {
     return first + i;
 }
 
+// Workgroup barrier that orders LDS only. Global stores issued before it
+// may still be in flight afterwards: for kernels whose waves exchange data
+// through LDS alone (global results are read by later launches only).
+__device__ inline void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 __device__ inline void lex_min(int64_t &v, uint32_t &a, int64_t ov, uint32_t oa) {
     if (ov < v || (ov == v && oa < a)) { v = ov; a = oa; }
 }
@@ -154,63 +163,116 @@ __global__ void k_compact(int64_t n_chunks, int64_t cap, const int64_t *w, const
     }
 }
 
-// W table, one workgroup per tile of 2^b consecutive subsets that share the
-// high bits H = tile id. A chunk reaches W(H|L) iff H|L is inside S_x, i.e.
-// iff S_x's high part contains H and its low part contains L. So the tile
-// keeps f(L) = sum of w(x) over chunks whose high part contains H and whose
-// low part equals L, and a superset-sum (zeta) over the b low bits turns f
-// into W. The zeta over the high bits is thereby done on the sparse list,
-// and the dense table is written exactly once.
-constexpr int kZetaBits = 13;             // 2^13 int64 = 64 KiB of LDS per tile
+// W table, one workgroup per tile of 2^13 consecutive subsets that share the
+// high bits H = tile id (for m < 13 one tile whose missing request bits no
+// chunk holds). A chunk reaches W(H|L) iff H|L is inside S_x, i.e. iff S_x's
+// high part contains H and its low part contains L. So the tile keeps
+// f(L) = sum of w(x) over chunks whose high part contains H and whose low
+// part equals L, and a superset-sum (zeta) over the 13 low bits turns f into
+// W. The zeta over the high bits is thereby done on the sparse list, and the
+// dense table is written exactly once and never read.
+// The 13-bit zeta runs as three register passes of 4 bits (bits 9-12, 5-8,
+// 0-3, each thread holding 16 elements) plus one lane exchange for bit 4.
+// LDS holds 16 elements per 144 bytes, which keeps every pass free of bank
+// conflicts; the last pass writes 128 contiguous bytes per thread.
+constexpr int kZetaBits = 13;
 constexpr int kZetaThreads = 512;
+constexpr int kZetaN = 1 << kZetaBits;
+__device__ inline int zpos(int e) { return e + 2 * (e >> 4); }
+
+__device__ inline void zeta16(int64_t v[16]) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int k = 0; k < 16; ++k)
+            if (!((k >> j) & 1)) v[k] += v[k | (1 << j)];
+}
+
+// Persistent: each workgroup keeps up to kZetaHeld list entries per thread
+// in registers and walks tiles blockIdx.x, + gridDim.x, ...; a tile's stores
+// drain while the next tile is built.
+constexpr int kZetaHeld = 4;
 
 __global__ __launch_bounds__(kZetaThreads) void k_weights_tile(
-        int m, int b, uint32_t cap, const uint32_t *list_sig, const int64_t *list_w, const WsHeader *h,
+        int m, uint32_t cap, uint32_t n_tiles, const uint32_t *list_sig, const int64_t *list_w, const WsHeader *h,
         int64_t *W) {
-    __shared__ int64_t tile[1 << kZetaBits];
-    const int n = 1 << b;
-    const uint32_t hi = blockIdx.x;                 // high part H of every subset in this tile
-    const uint32_t lowmask = (uint32_t)n - 1u;
-    for (int e = threadIdx.x; e < n; e += blockDim.x) tile[e] = 0;
-    __syncthreads();
+    __shared__ __align__(16) int64_t tile[kZetaN + kZetaN / 8];
+    const int b = kZetaBits;
+    const uint32_t lowmask = (uint32_t)kZetaN - 1u;
+    const int t = threadIdx.x;
     const uint32_t cnt = min(h->n_list, cap);
-    for (uint32_t j = threadIdx.x; j < cnt; j += blockDim.x) {
-        uint32_t s = list_sig[j];
-        uint32_t shi = s >> b;
-        if ((shi & hi) == hi)
-            atomicAdd((unsigned long long *)&tile[s & lowmask], (unsigned long long)list_w[j]);
+    const int64_t zero_weight = h->zero_weight;
+    uint32_t my_sig[kZetaHeld];
+    int64_t my_w[kZetaHeld];
+#pragma unroll
+    for (int i = 0; i < kZetaHeld; ++i) {
+        const uint32_t j = (uint32_t)t + (uint32_t)i * kZetaThreads;
+        my_sig[i] = j < cnt ? list_sig[j] : 0u;
+        my_w[i] = j < cnt ? list_w[j] : 0;
     }
-    if (hi == 0 && threadIdx.x == 0)
-        atomicAdd((unsigned long long *)&tile[0], (unsigned long long)h->zero_weight);
-    __syncthreads();
-    // superset sums over the low bits, three bits per LDS round trip
-    for (int j = 0; j < b; j += 3) {
-        const int r = min(3, b - j);
-        const int g = 1 << r;
-        const int ngroups = n >> r;
-        for (int q = threadIdx.x; q < ngroups; q += blockDim.x) {
-            // group q: the 2^r elements base + k * 2^j, bits j..j+r-1 of base clear
-            const int base = ((q >> j) << (j + r)) | (q & ((1 << j) - 1));
-            int64_t v[8];
+    for (uint32_t hi = blockIdx.x; hi < n_tiles; hi += gridDim.x) {   // hi: high part H of the tile
+    lds_barrier();
+    for (int e = t; e < (kZetaN + kZetaN / 8) / 2; e += kZetaThreads)
+        reinterpret_cast<longlong2 *>(tile)[e] = make_longlong2(0, 0);
+    lds_barrier();
 #pragma unroll
-            for (int k = 0; k < 8; ++k)
-                if (k < g) v[k] = tile[base + (k << j)];
-#pragma unroll
-            for (int t = 0; t < 3; ++t) {
-                if (t < r) {
-#pragma unroll
-                    for (int k = 0; k < 8; ++k)
-                        if (k < g && !((k >> t) & 1)) v[k] += v[k | (1 << t)];
-                }
-            }
-#pragma unroll
-            for (int k = 0; k < 8; ++k)
-                if (k < g) tile[base + (k << j)] = v[k];
-        }
-        __syncthreads();
+    for (int i = 0; i < kZetaHeld; ++i) {
+        const uint32_t s = my_sig[i];
+        if (my_w[i] != 0 && ((s >> b) & hi) == hi)
+            atomicAdd((unsigned long long *)&tile[zpos((int)(s & lowmask))], (unsigned long long)my_w[i]);
     }
+    for (uint32_t j = t + kZetaHeld * kZetaThreads; j < cnt; j += kZetaThreads) {
+        const uint32_t s = list_sig[j];
+        if (((s >> b) & hi) == hi)
+            atomicAdd((unsigned long long *)&tile[zpos((int)(s & lowmask))], (unsigned long long)list_w[j]);
+    }
+    if (hi == 0 && t == 0)
+        atomicAdd((unsigned long long *)&tile[0], (unsigned long long)zero_weight);
+    lds_barrier();
+    int64_t v[16];
+    // bits 0..3: elements 16 t + k, then bit 4 with the neighbouring lane
+    int64_t *row = tile + zpos(t << 4);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+        const longlong2 x = reinterpret_cast<const longlong2 *>(row)[q];
+        v[2 * q] = x.x;
+        v[2 * q + 1] = x.y;
+    }
+    zeta16(v);
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+        // value of the neighbouring lane (t ^ 1): DPP quad permutation [1,0,3,2]
+        const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)v[k], 0xB1, 0xF, 0xF, false);
+        const uint32_t hi32 = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(v[k] >> 32), 0xB1, 0xF, 0xF, false);
+        const int64_t o = (int64_t)(((uint64_t)hi32 << 32) | lo);
+        if (!(t & 1)) v[k] += o;
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q) reinterpret_cast<longlong2 *>(row)[q] = make_longlong2(v[2 * q], v[2 * q + 1]);
+    lds_barrier();
+    // bits 5..8: element (t >> 5) << 9 | k << 5 | (t & 31)
+    const int eb = ((t >> 5) << 9) | (t & 31);
+#pragma unroll
+    for (int k = 0; k < 16; ++k) v[k] = tile[zpos(eb | (k << 5))];
+    zeta16(v);
+#pragma unroll
+    for (int k = 0; k < 16; ++k) tile[zpos(eb | (k << 5))] = v[k];
+    lds_barrier();
+    // bits 9..12: element t + 512 k, stored straight to HBM (each store
+    // instruction covers 512 contiguous bytes)
+#pragma unroll
+    for (int k = 0; k < 16; ++k) v[k] = tile[zpos(t + (k << 9))];
+    zeta16(v);
     int64_t *out = W + ((int64_t)hi << b);
-    for (int e = threadIdx.x; e < n; e += blockDim.x) out[e] = tile[e];
+    if (m >= b) {
+#pragma unroll
+        for (int k = 0; k < 16; ++k) out[t + (k << 9)] = v[k];
+    } else {                        // one partial tile: only the first 2^m subsets exist
+#pragma unroll
+        for (int k = 0; k < 16; ++k)
+            if (t + (k << 9) < (1 << m)) out[t + (k << 9)] = v[k];
+    }
+    }
 }
 
 // every C(S) is at most sum_{i in S} w(R_i) = sum_{i in S} W({i}); the DP
@@ -633,7 +695,7 @@ __device__ void finalize_row(int m, uint32_t sh, Lds<K> &s, K *pS, K *tS, const 
         // mirror the in-block pairs below)
         for (int it = kItems.begin[k] + threadIdx.x; it < kItems.end[k]; it += THREADS)
             run_item<K>(c_items.v[it], pS, tS, s.pb, s.tb, s.acc, sh == 0);
-        __syncthreads();
+        lds_barrier();
         // A2 = S2: in-block pairs, one thread per block of this level
         for (int bi = c_blocks.begin[k] + threadIdx.x; bi < c_blocks.end[k]; bi += THREADS) {
             const uint32_t s2 = c_blocks.v[bi];
@@ -681,7 +743,7 @@ __device__ void finalize_row(int m, uint32_t sh, Lds<K> &s, K *pS, K *tS, const 
                 split[base + x] = sp[x];
             }
         }
-        __syncthreads();
+        lds_barrier();
     }
 }
 
@@ -703,10 +765,10 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
     uint32_t ah = t0 < t1 ? (lowh | deposit(t0, rest)) : 0u;
     for (uint32_t t = t0; t < t1; ++t) {
         const uint32_t bh = sh ^ ah;
-        __syncthreads();
+        lds_barrier();
         load_row<K>(s.pa, s.ta, Cp, ah);
         load_row<K>(s.pb, s.tb, Cp, bh);
-        __syncthreads();
+        lds_barrier();
         ah = lowh | (((ah | ~rest) + 1u) & rest);    // next A_H holding lowbit(S_H)
         // items are ordered by |S2| from the top: the lanes of a wave run
         // the same number of iterations and flush together
@@ -734,10 +796,10 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
             flush<K>(best, s2, s.acc);
         }
     }
-    __syncthreads();
+    lds_barrier();
     if (fused) {
         load_row<K>(s.pb, s.tb, Cp, 0u);
-        __syncthreads();
+        lds_barrier();
         finalize_row<K>(m, sh, s, s.pa, s.ta, W, Cp, split);
     } else {
         uint64_t *dst = partial + (size_t)bid * ROW;
@@ -770,7 +832,7 @@ __global__ __launch_bounds__(THREADS) void k_rb_final(int m, int h, uint32_t chu
     const uint64_t *src = partial + (size_t)r * chunks * ROW;
     for (int e = threadIdx.x; e < ROW; e += THREADS) s.acc[e] = chunks ? src[e] : ~0ull;
     if (sh != 0) load_row<K>(s.pb, s.tb, Cp, 0u);
-    __syncthreads();
+    lds_barrier();
     // for S_H = 0 the output row is row 0 itself
     if (sh == 0) finalize_row<K>(m, sh, s, s.pb, s.tb, W, Cp, split);
     else finalize_row<K>(m, sh, s, s.pa, s.ta, W, Cp, split);
@@ -1104,6 +1166,7 @@ extern "C" int mpt_build_weights(int m, int64_t n_chunks, int64_t nnz, const int
     int rc = check_common(m, n_chunks, nnz);
     if (rc) return rc;
     if (!req_off || !W) return fail(MPT_E_INVALID, "req_off and W must not be NULL");
+    if ((uintptr_t)W & 15u) return fail(MPT_E_INVALID, "W must be 16-byte aligned");
     if (n_chunks > 0 && (!chunk_w || !sig)) return fail(MPT_E_INVALID, "chunk_w and sig must not be NULL");
     if (nnz > 0 && !req_chunks) return fail(MPT_E_INVALID, "req_chunks must not be NULL");
     if ((rc = check_ws(m, nnz, workspace, workspace_bytes))) return rc;
@@ -1131,11 +1194,11 @@ extern "C" int mpt_build_weights(int m, int64_t n_chunks, int64_t nnz, const int
                                                               list_sig, list_w, h);
         }
     }
-    const int b = std::min(m, kZetaBits);
     {
         LaunchScope ls("weights_tile", 8.0 * (double)(1ull << m), s);
-        k_weights_tile<<<1u << (m - b), kZetaThreads, 0, s>>>(m, b, (uint32_t)std::max<int64_t>(nnz, 1), list_sig,
-                                                              list_w, h, W);
+        const uint32_t tiles = m > kZetaBits ? 1u << (m - kZetaBits) : 1u;
+        k_weights_tile<<<std::min(tiles, 512u), kZetaThreads, 0, s>>>(m, (uint32_t)std::max<int64_t>(nnz, 1), tiles,
+                                                                      list_sig, list_w, h, W);
     }
     k_check_total<<<1, 64, 0, s>>>(m, W, h);
     HIP_TRY(hipGetLastError());
