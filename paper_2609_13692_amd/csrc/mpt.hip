@@ -444,6 +444,12 @@ constexpr int R2 = L - CB;            // middle bits
 #ifndef MPT_RB_ITEM_LOG
 #define MPT_RB_ITEM_LOG 3
 #endif
+#ifndef MPT_RB_PIPE
+#define MPT_RB_PIPE 0
+#endif
+#ifndef MPT_RB_LIFT
+#define MPT_RB_LIFT 0
+#endif
 #ifndef MPT_RB_THREADS
 #define MPT_RB_THREADS 1024
 #endif
@@ -471,7 +477,11 @@ constexpr uint32_t cdeposit(uint32_t t, uint32_t mask) {
 }
 
 // work items: (S2, first A2 of a chunk of 2^T submasks of S2 in increasing
-// order), grouped by |S2| from R2 down to 0; entry = S2 | first A2 << 16
+// order), grouped by |S2| from R2 down to 0; entry = S2 | first A2 << 16.
+// Inside a level, up to 8 chunks of one S2 sit in adjacent lanes (so the
+// lanes of a 16-byte LDS read pass share S2 and read structured blocks)
+// and neighbouring groups of 8 lanes hold different S2 (so the accumulator
+// flushes of one wave spread over several blocks).
 struct Items {
     uint32_t v[8192];
     int begin[R2 + 1];
@@ -483,12 +493,15 @@ constexpr Items make_items() {
     int n = 0;
     for (int k = R2; k >= 0; --k) {
         it.begin[k] = n;
-        for (int s = 0; s < NS2; ++s) {
-            if (cpop(s) != k) continue;
-            const int tb = k < T ? k : T;
-            const int chunks = 1 << (k - tb);
-            for (int j = 0; j < chunks; ++j) it.v[n++] = (uint32_t)s | (cdeposit((uint32_t)j << tb, (uint32_t)s) << 16);
-        }
+        const int tb = k < T ? k : T;
+        const int chunks = 1 << (k - tb);
+        const int lo = chunks < 8 ? chunks : 8;          // chunks of one S2 that sit in adjacent lanes
+        for (int jh = 0; jh < chunks / lo; ++jh)
+            for (int s = 0; s < NS2; ++s) {
+                if (cpop(s) != k) continue;
+                for (int jl = 0; jl < lo; ++jl)
+                    it.v[n++] = (uint32_t)s | (cdeposit((uint32_t)(jh * lo + jl) << tb, (uint32_t)s) << 16);
+            }
         it.end[k] = n;
     }
     it.n = n;
@@ -497,6 +510,35 @@ constexpr Items make_items() {
 constexpr Items kItems = make_items();
 static_assert(kItems.n <= 8192, "item table too small");
 __constant__ Items c_items = make_items();
+
+// work items of a cross pair, lifted on the top middle bit E = 1 << (R2-1):
+// a base iteration (S2', A2') over the other R2-1 middle bits also covers
+// (S2'|E, A2') and (S2'|E, A2'|E), which reuse its blocks -- four block
+// loads serve three block convolutions. Entry = S2' | first A2' << 16,
+// 2^min(|S2'|, TL) base iterations each, ordered by |S2'| from the top.
+constexpr int TL = 2;
+constexpr int RL = R2 - 1;
+struct LiftItems { uint32_t v[4096]; int n; };
+constexpr LiftItems make_lift_items() {
+    LiftItems it{};
+    int n = 0;
+    for (int k = RL; k >= 0; --k) {
+        const int tb = k < TL ? k : TL;
+        const int chunks = 1 << (k - tb);
+        const int lo = chunks < 8 ? chunks : 8;
+        for (int jh = 0; jh < chunks / lo; ++jh)
+            for (int s = 0; s < (1 << RL); ++s) {
+                if (cpop(s) != k) continue;
+                for (int jl = 0; jl < lo; ++jl)
+                    it.v[n++] = (uint32_t)s | (cdeposit((uint32_t)(jh * lo + jl) << tb, (uint32_t)s) << 16);
+            }
+    }
+    it.n = n;
+    return it;
+}
+constexpr LiftItems kLift = make_lift_items();
+static_assert(kLift.n <= 4096, "lift item table too small");
+__constant__ LiftItems c_lift = make_lift_items();
 
 // the middle masks of each popcount, for the one-thread-per-block steps
 struct Blocks { uint16_t v[NS2]; int begin[R2 + 1]; int end[R2 + 1]; };
@@ -522,6 +564,7 @@ template <> struct Key<uint64_t> {
     static __device__ inline uint64_t min(uint64_t a, uint64_t b) { return b < a ? b : a; }
     static __device__ inline uint64_t none() { return ~0ull; }
     static __device__ inline uint64_t bits(uint64_t k) { return k; }
+    static __device__ inline uint64_t from_bits(uint64_t b) { return b; }
     static __device__ inline uint64_t value_of_bits(uint64_t b) { return b; }
 };
 template <> struct Key<double> {
@@ -532,6 +575,7 @@ template <> struct Key<double> {
     static __device__ inline double none() { return __builtin_inf(); }
     // positive doubles order like their bit patterns
     static __device__ inline uint64_t bits(double k) { return (uint64_t)__double_as_longlong(k); }
+    static __device__ inline double from_bits(uint64_t b) { return __longlong_as_double((long long)b); }
     static __device__ inline uint64_t value_of_bits(uint64_t b) {
         return b >= 0x7ff0000000000000ull ? ~0ull : (uint64_t)__longlong_as_double((long long)b);
     }
@@ -636,12 +680,44 @@ __device__ inline void conv_block(const K pa[NE], const K ta[NB], const K pb[NE]
     }
 }
 
+// DPP lane exchange of a 64-bit value inside rows of 8 lanes
+template <int CTRL, class K>
+__device__ inline K dpp_get(K v) {
+    const uint64_t b = Key<K>::bits(v);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)b, CTRL, 0xF, 0xF, false);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(b >> 32), CTRL, 0xF, 0xF, false);
+    return Key<K>::from_bits(((uint64_t)hi << 32) | lo);
+}
+
 template <class K>
 __device__ inline void flush(const K best[NB], uint32_t s2, uint64_t *acc) {
 #pragma unroll
     for (int x = 0; x < NB; ++x)
         if (best[x] != Key<K>::none())
             atomicMin((unsigned long long *)&acc[(s2 << CB) | x], (unsigned long long)Key<K>::bits(best[x]));
+}
+
+// Flush of a work item whose adjacent lanes share S2 in aligned groups of
+// seg = 1, 2, 4 or 8 lanes: min inside the group (quad permutations, then
+// the half-row mirror that pairs the two quads of 8 lanes), and one lane
+// per group does the LDS atomics. 64-bit LDS atomics are costly, so this
+// cuts them by the group size.
+template <class K>
+__device__ inline void flush_group(K best[NB], uint32_t s2, uint32_t seg, uint64_t *acc) {
+    const uint32_t lane = threadIdx.x & (kWave - 1);
+    if (seg >= 2) {
+#pragma unroll
+        for (int x = 0; x < NB; ++x) best[x] = Key<K>::min(best[x], dpp_get<0xB1>(best[x]));   // quad_perm [1,0,3,2]
+    }
+    if (seg >= 4) {
+#pragma unroll
+        for (int x = 0; x < NB; ++x) best[x] = Key<K>::min(best[x], dpp_get<0x4E>(best[x]));   // quad_perm [2,3,0,1]
+    }
+    if (seg >= 8) {
+#pragma unroll
+        for (int x = 0; x < NB; ++x) best[x] = Key<K>::min(best[x], dpp_get<0x141>(best[x]));  // row_half_mirror
+    }
+    if ((lane & (seg - 1)) == 0) flush<K>(best, s2, acc);
 }
 
 // one self-pair work item (S2, first A2) against (rowS, row0): 2^min(|S2|,T)
@@ -770,8 +846,46 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
         load_row<K>(s.pb, s.tb, Cp, bh);
         lds_barrier();
         ah = lowh | (((ah | ~rest) + 1u) & rest);    // next A_H holding lowbit(S_H)
-        // items are ordered by |S2| from the top: the lanes of a wave run
-        // the same number of iterations and flush together
+#if MPT_RB_LIFT
+        // lifted items, ordered by |S2'| from the top: the lanes of a wave
+        // run the same number of iterations and flush together
+        constexpr uint32_t E = 1u << RL;
+        const uint32_t slot_e = slot_of(E);
+        for (int it = threadIdx.x; it < kLift.n; it += THREADS) {
+            const uint32_t item = c_lift.v[it];
+            const uint32_t s2 = item & 0xffffu;
+            const int k = __popc(s2);
+            const uint32_t cnt = 1u << (k < TL ? k : TL);
+            const uint32_t low2 = s2 & (0u - s2);
+            const uint32_t slot_s2 = slot_of(s2);
+            uint32_t a2 = item >> 16;
+            K best0[NB], best1[NB];      // outputs S2' and S2'|E
+#pragma unroll
+            for (int x = 0; x < NB; ++x) { best0[x] = Key<K>::none(); best1[x] = Key<K>::none(); }
+            for (uint32_t i = 0; i < cnt; ++i) {
+                const uint32_t sa0 = slot_of(a2), sb0 = slot_s2 ^ sa0;
+                const bool lowin = (a2 & low2) != 0;
+                K pa[NE], ta[NB], pb[NE], tb2[NB];
+                // (S2'|E, A2'): A block A2', B block B2'|E
+                load_p(s.pa, sa0, pa);
+                load_t(s.ta, sa0, ta);
+                load_p(s.pb, sb0 ^ slot_e, pb);
+                load_t(s.tb, sb0 ^ slot_e, tb2);
+                conv_block<K>(pa, ta, pb, tb2, (s2 != 0) && lowin, best1);
+                // (S2', A2'): A block A2', B block B2'
+                load_p(s.pb, sb0, pb);
+                load_t(s.tb, sb0, tb2);
+                conv_block<K>(pa, ta, pb, tb2, (s2 == 0) || lowin, best0);
+                // (S2'|E, A2'|E): A block A2'|E, B block B2'
+                load_p(s.pa, sa0 ^ slot_e, pa);
+                load_t(s.ta, sa0 ^ slot_e, ta);
+                conv_block<K>(pa, ta, pb, tb2, (s2 == 0) || lowin, best1);
+                a2 = ((a2 | ~s2) + 1u) & s2;
+            }
+            flush<K>(best0, s2, s.acc);
+            flush<K>(best1, s2 | E, s.acc);
+        }
+#else
         for (int it = threadIdx.x; it < kItems.n; it += THREADS) {
             const uint32_t item = c_items.v[it];
             const uint32_t s2 = item & 0xffffu;
@@ -783,6 +897,34 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
             K best[NB];
 #pragma unroll
             for (int x = 0; x < NB; ++x) best[x] = Key<K>::none();
+#if MPT_RB_PIPE
+            // the blocks of the next submask are read while this one is combined
+            K pa[NE], ta[NB], pb[NE], tb2[NB];
+            {
+                const uint32_t sa = slot_of(a2), sb = slot_s2 ^ sa;
+                load_p(s.pa, sa, pa);
+                load_t(s.ta, sa, ta);
+                load_p(s.pb, sb, pb);
+                load_t(s.tb, sb, tb2);
+            }
+            for (uint32_t i = 0; i < cnt; ++i) {
+                const bool orient = (s2 == 0) || (a2 & low2);
+                a2 = ((a2 | ~s2) + 1u) & s2;
+                K npa[NE], nta[NB], npb[NE], ntb[NB];
+                if (i + 1 < cnt) {
+                    const uint32_t sa = slot_of(a2), sb = slot_s2 ^ sa;
+                    load_p(s.pa, sa, npa);
+                    load_t(s.ta, sa, nta);
+                    load_p(s.pb, sb, npb);
+                    load_t(s.tb, sb, ntb);
+                }
+                conv_block<K>(pa, ta, pb, tb2, orient, best);
+#pragma unroll
+                for (int x = 0; x < NE; ++x) { pa[x] = npa[x]; pb[x] = npb[x]; }
+#pragma unroll
+                for (int x = 0; x < NB; ++x) { ta[x] = nta[x]; tb2[x] = ntb[x]; }
+            }
+#else
             for (uint32_t i = 0; i < cnt; ++i) {
                 const uint32_t sa = slot_of(a2), sb = slot_s2 ^ sa;
                 K pa[NE], ta[NB], pb[NE], tb2[NB];
@@ -793,8 +935,14 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
                 conv_block<K>(pa, ta, pb, tb2, (s2 == 0) || (a2 & low2), best);
                 a2 = ((a2 | ~s2) + 1u) & s2;
             }
-            flush<K>(best, s2, s.acc);
+#endif
+            {
+                const int tb = k < T ? k : T;
+                const uint32_t chunks = 1u << (k - tb);
+                flush_group<K>(best, s2, chunks < 8u ? chunks : 8u, s.acc);
+            }
         }
+#endif
     }
     lds_barrier();
     if (fused) {
