@@ -29,10 +29,10 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0
 N_CU, CLOCK_GHZ = 256, 2.4
 VALU_PEAK_TOPS = N_CU * 64 * CLOCK_GHZ / 1000.0      # int32 lane-ops, T/s (39.3)
-# VALU instructions one evaluated bipartition needs at the least on gfx950:
-# a 64-bit add of two packed keys (v_lshl_add_u64) and a 64-bit unsigned
-# minimum (v_cmp_lt_u64 + two v_cndmask_b32)
-DP_OPS_PER_PAIR = 4
+# Algorithmic work of one evaluated bipartition: one 64-bit add of two keys
+# and one 64-bit min -- 2 VALU lane-ops, the least gfx950 needs (v_add_f64 +
+# v_min_f64 on exact-integer keys). Peak: 256 CUs x 64 lanes x 2.4 GHz.
+DP_OPS_PER_PAIR = 2
 
 WORKLOADS = {
     1: "tiny random, m=12, u=64, k=4, w~U{1..32}, seed 0",

@@ -448,7 +448,7 @@ constexpr int R2 = L - CB;            // middle bits
 #define MPT_RB_PIPE 0
 #endif
 #ifndef MPT_RB_LIFT
-#define MPT_RB_LIFT 0
+#define MPT_RB_LIFT 1
 #endif
 #ifndef MPT_RB_THREADS
 #define MPT_RB_THREADS 1024
@@ -516,7 +516,10 @@ __constant__ Items c_items = make_items();
 // (S2'|E, A2') and (S2'|E, A2'|E), which reuse its blocks -- four block
 // loads serve three block convolutions. Entry = S2' | first A2' << 16,
 // 2^min(|S2'|, TL) base iterations each, ordered by |S2'| from the top.
-constexpr int TL = 2;
+#ifndef MPT_RB_LIFT_LOG
+#define MPT_RB_LIFT_LOG 2
+#endif
+constexpr int TL = MPT_RB_LIFT_LOG;
 constexpr int RL = R2 - 1;
 struct LiftItems { uint32_t v[4096]; int n; };
 constexpr LiftItems make_lift_items() {
@@ -882,8 +885,13 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
                 conv_block<K>(pa, ta, pb, tb2, (s2 == 0) || lowin, best1);
                 a2 = ((a2 | ~s2) + 1u) & s2;
             }
-            flush<K>(best0, s2, s.acc);
-            flush<K>(best1, s2 | E, s.acc);
+            {
+                const int tb = k < TL ? k : TL;
+                const uint32_t chunks = 1u << (k - tb);
+                const uint32_t seg = chunks < 8u ? chunks : 8u;
+                flush_group<K>(best0, s2, seg, s.acc);
+                flush_group<K>(best1, s2 | E, seg, s.acc);
+            }
         }
 #else
         for (int it = threadIdx.x; it < kItems.n; it += THREADS) {
