@@ -444,12 +444,6 @@ constexpr int R2 = L - CB;            // middle bits
 #ifndef MPT_RB_ITEM_LOG
 #define MPT_RB_ITEM_LOG 3
 #endif
-#ifndef MPT_RB_PIPE
-#define MPT_RB_PIPE 0
-#endif
-#ifndef MPT_RB_LIFT
-#define MPT_RB_LIFT 1
-#endif
 #ifndef MPT_RB_THREADS
 #define MPT_RB_THREADS 1024
 #endif
@@ -511,37 +505,60 @@ constexpr Items kItems = make_items();
 static_assert(kItems.n <= 8192, "item table too small");
 __constant__ Items c_items = make_items();
 
-// work items of a cross pair, lifted on the top middle bit E = 1 << (R2-1):
-// a base iteration (S2', A2') over the other R2-1 middle bits also covers
-// (S2'|E, A2') and (S2'|E, A2'|E), which reuse its blocks -- four block
-// loads serve three block convolutions. Entry = S2' | first A2' << 16,
-// 2^min(|S2'|, TL) base iterations each, ordered by |S2'| from the top.
-#ifndef MPT_RB_LIFT_LOG
-#define MPT_RB_LIFT_LOG 2
-#endif
-constexpr int TL = MPT_RB_LIFT_LOG;
+// Cross-pair work of the threads of a workgroup, lifted on the top middle
+// bit E = 1 << (R2-1): a base iteration (S2', A2') over the other R2-1 middle
+// bits also covers (S2'|E, A2') and (S2'|E, A2'|E), which reuse its blocks,
+// so four block loads serve three block convolutions. Each thread owns
+// exactly one item -- the same for every row pair of its chunk -- and keeps
+// the best keys of its two output blocks in registers across all pairs,
+// flushing them once. Items: chunks of 8 submasks A2' of S2' (|S2'| >= 3),
+// enough of them halved into chunks of 4, and the small S2' whole, so that
+// the items fill THREADS slots; bigger items come first so the lanes of a
+// wave mostly run the same count. Entry: S2' | first A2' << 8 |
+// log2(count) << 16 | 1 << 31 (0 = no item).
 constexpr int RL = R2 - 1;
-struct LiftItems { uint32_t v[4096]; int n; };
-constexpr LiftItems make_lift_items() {
-    LiftItems it{};
-    int n = 0;
-    for (int k = RL; k >= 0; --k) {
-        const int tb = k < TL ? k : TL;
-        const int chunks = 1 << (k - tb);
-        const int lo = chunks < 8 ? chunks : 8;
-        for (int jh = 0; jh < chunks / lo; ++jh)
-            for (int s = 0; s < (1 << RL); ++s) {
-                if (cpop(s) != k) continue;
-                for (int jl = 0; jl < lo; ++jl)
-                    it.v[n++] = (uint32_t)s | (cdeposit((uint32_t)(jh * lo + jl) << tb, (uint32_t)s) << 16);
-            }
-    }
-    it.n = n;
-    return it;
+struct ThreadItems { uint32_t v[THREADS]; int n_big; int n_small; int n_split; };
+constexpr uint32_t titem(int s2, int a2, int lg) {
+    return (uint32_t)s2 | ((uint32_t)a2 << 8) | ((uint32_t)lg << 16) | (1u << 31);
 }
-constexpr LiftItems kLift = make_lift_items();
-static_assert(kLift.n <= 4096, "lift item table too small");
-__constant__ LiftItems c_lift = make_lift_items();
+constexpr ThreadItems make_thread_items() {
+    ThreadItems t{};
+    int n_big = 0, n_small = 0;
+    for (int s = 0; s < (1 << RL); ++s) {
+        if (cpop(s) >= 3) n_big += 1 << (cpop(s) - 3);
+        else ++n_small;
+    }
+    int n_split = THREADS - n_big - n_small;
+    if (n_split < 0) n_split = 0;
+    if (n_split > n_big) n_split = n_big;
+    t.n_big = n_big; t.n_small = n_small; t.n_split = n_split;
+    int whole = 0, halves = n_big - n_split, seen = 0, small = 2 * n_split + n_big - n_split;
+    for (int k = RL; k >= 0; --k)
+        for (int s = 0; s < (1 << RL); ++s) {
+            if (cpop(s) != k) continue;
+            if (k >= 3) {
+                for (int j = 0; j < (1 << (k - 3)); ++j, ++seen) {
+                    const uint32_t a2 = cdeposit((uint32_t)j << 3, (uint32_t)s);
+                    if (seen < n_big - n_split) {
+                        if (whole < THREADS) t.v[whole++] = titem(s, (int)a2, 3);
+                    } else {
+                        const uint32_t a2h = cdeposit(((uint32_t)j << 3) | 4u, (uint32_t)s);
+                        if (halves + 1 < THREADS) {
+                            t.v[halves++] = titem(s, (int)a2, 2);
+                            t.v[halves++] = titem(s, (int)a2h, 2);
+                        }
+                    }
+                }
+            } else if (small < THREADS) {
+                t.v[small++] = titem(s, 0, k);
+            }
+        }
+    return t;
+}
+constexpr ThreadItems kTItems = make_thread_items();
+static_assert(kTItems.n_big + kTItems.n_split + kTItems.n_small <= THREADS,
+              "every cross-pair item needs a thread of its own");
+__constant__ ThreadItems c_titems = make_thread_items();
 
 // the middle masks of each popcount, for the one-thread-per-block steps
 struct Blocks { uint16_t v[NS2]; int begin[R2 + 1]; int end[R2 + 1]; };
@@ -683,44 +700,12 @@ __device__ inline void conv_block(const K pa[NE], const K ta[NB], const K pb[NE]
     }
 }
 
-// DPP lane exchange of a 64-bit value inside rows of 8 lanes
-template <int CTRL, class K>
-__device__ inline K dpp_get(K v) {
-    const uint64_t b = Key<K>::bits(v);
-    const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)b, CTRL, 0xF, 0xF, false);
-    const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(b >> 32), CTRL, 0xF, 0xF, false);
-    return Key<K>::from_bits(((uint64_t)hi << 32) | lo);
-}
-
 template <class K>
 __device__ inline void flush(const K best[NB], uint32_t s2, uint64_t *acc) {
 #pragma unroll
     for (int x = 0; x < NB; ++x)
         if (best[x] != Key<K>::none())
             atomicMin((unsigned long long *)&acc[(s2 << CB) | x], (unsigned long long)Key<K>::bits(best[x]));
-}
-
-// Flush of a work item whose adjacent lanes share S2 in aligned groups of
-// seg = 1, 2, 4 or 8 lanes: min inside the group (quad permutations, then
-// the half-row mirror that pairs the two quads of 8 lanes), and one lane
-// per group does the LDS atomics. 64-bit LDS atomics are costly, so this
-// cuts them by the group size.
-template <class K>
-__device__ inline void flush_group(K best[NB], uint32_t s2, uint32_t seg, uint64_t *acc) {
-    const uint32_t lane = threadIdx.x & (kWave - 1);
-    if (seg >= 2) {
-#pragma unroll
-        for (int x = 0; x < NB; ++x) best[x] = Key<K>::min(best[x], dpp_get<0xB1>(best[x]));   // quad_perm [1,0,3,2]
-    }
-    if (seg >= 4) {
-#pragma unroll
-        for (int x = 0; x < NB; ++x) best[x] = Key<K>::min(best[x], dpp_get<0x4E>(best[x]));   // quad_perm [2,3,0,1]
-    }
-    if (seg >= 8) {
-#pragma unroll
-        for (int x = 0; x < NB; ++x) best[x] = Key<K>::min(best[x], dpp_get<0x141>(best[x]));  // row_half_mirror
-    }
-    if ((lane & (seg - 1)) == 0) flush<K>(best, s2, acc);
 }
 
 // one self-pair work item (S2, first A2) against (rowS, row0): 2^min(|S2|,T)
@@ -842,6 +827,19 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
     const uint32_t t0 = j * per_chunk;
     const uint32_t t1 = min(n_pairs, t0 + per_chunk);
     uint32_t ah = t0 < t1 ? (lowh | deposit(t0, rest)) : 0u;
+    // this thread's item, its best keys for outputs S2' and S2'|E
+    constexpr uint32_t E = 1u << RL;
+    const uint32_t item = c_titems.v[threadIdx.x];
+    const bool has_item = (item >> 31) != 0;
+    const uint32_t s2 = item & 0xffu;
+    const uint32_t a2_first = (item >> 8) & 0xffu;
+    const uint32_t cnt = 1u << ((item >> 16) & 3u);
+    const uint32_t low2 = s2 & (0u - s2);
+    const uint32_t slot_s2 = slot_of(s2);
+    const uint32_t slot_e = slot_of(E);
+    K best0[NB], best1[NB];
+#pragma unroll
+    for (int x = 0; x < NB; ++x) { best0[x] = Key<K>::none(); best1[x] = Key<K>::none(); }
     for (uint32_t t = t0; t < t1; ++t) {
         const uint32_t bh = sh ^ ah;
         lds_barrier();
@@ -849,22 +847,8 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
         load_row<K>(s.pb, s.tb, Cp, bh);
         lds_barrier();
         ah = lowh | (((ah | ~rest) + 1u) & rest);    // next A_H holding lowbit(S_H)
-#if MPT_RB_LIFT
-        // lifted items, ordered by |S2'| from the top: the lanes of a wave
-        // run the same number of iterations and flush together
-        constexpr uint32_t E = 1u << RL;
-        const uint32_t slot_e = slot_of(E);
-        for (int it = threadIdx.x; it < kLift.n; it += THREADS) {
-            const uint32_t item = c_lift.v[it];
-            const uint32_t s2 = item & 0xffffu;
-            const int k = __popc(s2);
-            const uint32_t cnt = 1u << (k < TL ? k : TL);
-            const uint32_t low2 = s2 & (0u - s2);
-            const uint32_t slot_s2 = slot_of(s2);
-            uint32_t a2 = item >> 16;
-            K best0[NB], best1[NB];      // outputs S2' and S2'|E
-#pragma unroll
-            for (int x = 0; x < NB; ++x) { best0[x] = Key<K>::none(); best1[x] = Key<K>::none(); }
+        if (has_item) {
+            uint32_t a2 = a2_first;
             for (uint32_t i = 0; i < cnt; ++i) {
                 const uint32_t sa0 = slot_of(a2), sb0 = slot_s2 ^ sa0;
                 const bool lowin = (a2 & low2) != 0;
@@ -885,72 +869,11 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
                 conv_block<K>(pa, ta, pb, tb2, (s2 == 0) || lowin, best1);
                 a2 = ((a2 | ~s2) + 1u) & s2;
             }
-            {
-                const int tb = k < TL ? k : TL;
-                const uint32_t chunks = 1u << (k - tb);
-                const uint32_t seg = chunks < 8u ? chunks : 8u;
-                flush_group<K>(best0, s2, seg, s.acc);
-                flush_group<K>(best1, s2 | E, seg, s.acc);
-            }
         }
-#else
-        for (int it = threadIdx.x; it < kItems.n; it += THREADS) {
-            const uint32_t item = c_items.v[it];
-            const uint32_t s2 = item & 0xffffu;
-            const int k = __popc(s2);
-            const uint32_t cnt = 1u << (k < T ? k : T);
-            const uint32_t low2 = s2 & (0u - s2);
-            const uint32_t slot_s2 = slot_of(s2);
-            uint32_t a2 = item >> 16;
-            K best[NB];
-#pragma unroll
-            for (int x = 0; x < NB; ++x) best[x] = Key<K>::none();
-#if MPT_RB_PIPE
-            // the blocks of the next submask are read while this one is combined
-            K pa[NE], ta[NB], pb[NE], tb2[NB];
-            {
-                const uint32_t sa = slot_of(a2), sb = slot_s2 ^ sa;
-                load_p(s.pa, sa, pa);
-                load_t(s.ta, sa, ta);
-                load_p(s.pb, sb, pb);
-                load_t(s.tb, sb, tb2);
-            }
-            for (uint32_t i = 0; i < cnt; ++i) {
-                const bool orient = (s2 == 0) || (a2 & low2);
-                a2 = ((a2 | ~s2) + 1u) & s2;
-                K npa[NE], nta[NB], npb[NE], ntb[NB];
-                if (i + 1 < cnt) {
-                    const uint32_t sa = slot_of(a2), sb = slot_s2 ^ sa;
-                    load_p(s.pa, sa, npa);
-                    load_t(s.ta, sa, nta);
-                    load_p(s.pb, sb, npb);
-                    load_t(s.tb, sb, ntb);
-                }
-                conv_block<K>(pa, ta, pb, tb2, orient, best);
-#pragma unroll
-                for (int x = 0; x < NE; ++x) { pa[x] = npa[x]; pb[x] = npb[x]; }
-#pragma unroll
-                for (int x = 0; x < NB; ++x) { ta[x] = nta[x]; tb2[x] = ntb[x]; }
-            }
-#else
-            for (uint32_t i = 0; i < cnt; ++i) {
-                const uint32_t sa = slot_of(a2), sb = slot_s2 ^ sa;
-                K pa[NE], ta[NB], pb[NE], tb2[NB];
-                load_p(s.pa, sa, pa);
-                load_t(s.ta, sa, ta);
-                load_p(s.pb, sb, pb);
-                load_t(s.tb, sb, tb2);
-                conv_block<K>(pa, ta, pb, tb2, (s2 == 0) || (a2 & low2), best);
-                a2 = ((a2 | ~s2) + 1u) & s2;
-            }
-#endif
-            {
-                const int tb = k < T ? k : T;
-                const uint32_t chunks = 1u << (k - tb);
-                flush_group<K>(best, s2, chunks < 8u ? chunks : 8u, s.acc);
-            }
-        }
-#endif
+    }
+    if (has_item) {
+        flush<K>(best0, s2, s.acc);
+        flush<K>(best1, s2 | E, s.acc);
     }
     lds_barrier();
     if (fused) {

@@ -237,6 +237,37 @@ def test_max_m_weight_table():
     torch.cuda.empty_cache()
 
 
+def test_max_m_full_solve():
+    """Whole path at MPT_MAX_M = 28 (2^28-entry tables, 1.1e13 bipartitions)
+    on L_28, where every entry has a closed form: C(S) = (n - |S|) + E(|S|)
+    with E the Eq. (5) free value; the split table encodes a hierarchy whose
+    Eq. (2) cost and read-off trie cost are both OPT."""
+    n = mpt.MPT_MAX_M
+    inst = wl.gen_loo(n)
+    say(f"[gpu] full solve, {inst.name}")
+    prob = mpt.Problem(inst)
+    opt = prob.run()
+    torch.cuda.synchronize()
+    assert opt == brute.loo_opt_free(n) == 136
+    E = torch.tensor([0] + [brute.loo_opt_free(s) for s in range(1, n + 1)], dtype=torch.int64, device="cuda")
+    for lo in range(0, 1 << n, 1 << 26):                 # in slices to bound temporaries
+        idx = torch.arange(lo, lo + (1 << 26), device="cuda", dtype=torch.int64)
+        pc = torch.zeros_like(idx)
+        for b in range(n):
+            pc += (idx >> b) & 1
+        expect = (n - pc) + E[pc]
+        if lo == 0:
+            expect[0] = mpt.MPT_COST_SENTINEL
+        assert torch.equal(prob.C[lo:lo + (1 << 26)], expect), lo
+        del idx, pc, expect
+    split = prob.split.cpu().numpy().view("uint32")
+    assert oracle.hierarchy_cost(inst, split) == opt
+    orders = prob.orders.cpu().numpy()[:inst.nnz]
+    assert oracle.trie_cost(inst, orders) == opt
+    del prob
+    torch.cuda.empty_cache()
+
+
 def test_determinism_and_reuse():
     inst = wl.config(3)
     prob = mpt.Problem(inst)
