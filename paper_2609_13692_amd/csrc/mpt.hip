@@ -13,6 +13,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstdarg>
 #include <cstdint>
 #include <cstdio>
@@ -453,8 +454,7 @@ constexpr int NE = NB / 2;            // even entries per block
 constexpr int ROW = 1 << L;           // entries per row
 constexpr int NS2 = 1 << R2;          // blocks per row
 constexpr int THREADS = MPT_RB_THREADS;
-constexpr int WG_TARGET = 1024;       // workgroups aimed at when a level is split
-constexpr int FUSE_MIN_SETS = 256;    // levels with this many S_H keep one workgroup per S_H
+constexpr int CUS = 256;              // MI355X compute units
 constexpr uint64_t SENT = (uint64_t)1 << 62;
 
 constexpr int cpop(int x) { int c = 0; while (x) { c += x & 1; x >>= 1; } return c; }
@@ -886,17 +886,23 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
     }
 }
 
-// min over the chunks of one S_H, into chunk 0's slot; 256 entries per block
-__global__ __launch_bounds__(256) void k_rb_reduce(uint32_t chunks, uint64_t *__restrict__ partial) {
-    const uint32_t r = blockIdx.x / (ROW / 256);
-    const uint32_t e = (blockIdx.x % (ROW / 256)) * 256 + threadIdx.x;
+// min over the chunks of one S_H, into chunk 0's slot. Block (r, e-range,
+// g) folds chunks 1 + g, 1 + g + G, ... of entries e into chunk 0 with a
+// 64-bit atomic min (unsigned order = key order).
+constexpr int RED_CHUNKS_PER_BLOCK = 32;
+__global__ __launch_bounds__(256) void k_rb_reduce(uint32_t chunks, uint32_t groups, uint64_t *__restrict__ partial) {
+    const uint32_t per_set = (ROW / 256) * groups;
+    const uint32_t r = blockIdx.x / per_set;
+    const uint32_t rem = blockIdx.x % per_set;
+    const uint32_t e = (rem % (ROW / 256)) * 256 + threadIdx.x;
+    const uint32_t g = rem / (ROW / 256);
     uint64_t *base = partial + (size_t)r * chunks * ROW + e;
-    uint64_t v = base[0];
-    for (uint32_t j = 1; j < chunks; ++j) {
+    uint64_t v = ~0ull;
+    for (uint32_t j = 1 + g; j < chunks; j += groups) {
         const uint64_t o = base[(size_t)j * ROW];
         v = o < v ? o : v;
     }
-    base[0] = v;
+    if (v != ~0ull) atomicMin((unsigned long long *)base, (unsigned long long)v);
 }
 
 // finish the rows of one level: acc from the reduced partials (chunks > 0)
@@ -1101,11 +1107,25 @@ std::vector<RbLevel> rb_plan(int m) {
         L.n_pairs = h >= 2 ? (1u << (h - 1)) - 1u : 0u;
         if (L.n_pairs == 0) {
             L.chunks = 0;
-        } else if (L.n_sets >= (uint32_t)rb::FUSE_MIN_SETS) {
-            L.chunks = 1;
         } else {
-            uint32_t c = (rb::WG_TARGET + L.n_sets - 1) / L.n_sets;
-            L.chunks = std::min(c, L.n_pairs);
+            // One workgroup runs per CU at a time (its LDS takes the CU), so a
+            // level of W equal workgroups takes ceil(W / CUs) rounds. Split the
+            // pairs of every S_H into c chunks, c chosen to fill the last round
+            // best; keep c = 1 (the row is finished in the same kernel) unless
+            // splitting wins by a clear margin.
+            const double cus = rb::CUS;
+            auto eff = [&](uint32_t c) {
+                const double w = (double)L.n_sets * c;
+                return w / (cus * std::ceil(w / cus));
+            };
+            uint32_t best = 1;
+            double best_eff = eff(1) + 0.03;
+            for (uint32_t c = 2; c <= std::min<uint32_t>(L.n_pairs, 4096); ++c) {
+                if ((double)L.n_sets * c > 16.0 * cus && c > 1 && eff(best) >= 0.9) break;
+                const double e = eff(c);
+                if (e > best_eff + 1e-9) { best = c; best_eff = e; }
+            }
+            L.chunks = best;
         }
         L.per_chunk = L.chunks ? (L.n_pairs + L.chunks - 1) / L.chunks : 0;
         v.push_back(L);
@@ -1194,7 +1214,8 @@ int solve_rb(int m, const int64_t *W, int64_t *C, uint32_t *split, uint64_t *par
             }
             {
                 LaunchScope ls("rb_reduce", (double)P.n_sets * P.chunks * rb::ROW * 8.0, s);
-                rb::k_rb_reduce<<<P.n_sets * (rb::ROW / 256), 256, 0, s>>>(P.chunks, partial);
+                const uint32_t groups = (P.chunks - 1 + rb::RED_CHUNKS_PER_BLOCK - 1) / rb::RED_CHUNKS_PER_BLOCK;
+                rb::k_rb_reduce<<<P.n_sets * (rb::ROW / 256) * groups, 256, 0, s>>>(P.chunks, groups, partial);
             }
             {
                 LaunchScope ls("rb_final", pair_work * P.n_sets, s);
