@@ -172,13 +172,16 @@ __global__ void k_compact(int64_t n_chunks, int64_t cap, const int64_t *w, const
 // part equals L, and a superset-sum (zeta) over the 13 low bits turns f into
 // W. The zeta over the high bits is thereby done on the sparse list, and the
 // dense table is written exactly once and never read.
-// The 13-bit zeta runs as three register passes of 4 bits (bits 9-12, 5-8,
-// 0-3, each thread holding 16 elements) plus one lane exchange for bit 4.
-// LDS holds 16 elements per 144 bytes, which keeps every pass free of bank
-// conflicts; the last pass writes 128 contiguous bytes per thread.
+// The zeta over the low bits: bits 0..4 are also summed on the sparse list
+// (a chunk with low part L adds w to every L' with L' = L outside bits 0..4
+// and L' a subset of L inside them); bits 5..8 and 9..12 are two register
+// passes with 16 elements per thread. LDS holds 16 elements per 144 bytes,
+// which keeps both passes free of bank conflicts; the last pass holds
+// elements t + 512 k, so each store instruction covers 512 contiguous bytes.
 constexpr int kZetaBits = 13;
 constexpr int kZetaThreads = 512;
 constexpr int kZetaN = 1 << kZetaBits;
+constexpr uint32_t kZetaSparseMask = 31u;     // bits summed on the sparse list
 __device__ inline int zpos(int e) { return e + 2 * (e >> 4); }
 
 __device__ inline void zeta16(int64_t v[16]) {
@@ -187,6 +190,18 @@ __device__ inline void zeta16(int64_t v[16]) {
 #pragma unroll
         for (int k = 0; k < 16; ++k)
             if (!((k >> j) & 1)) v[k] += v[k | (1 << j)];
+}
+
+// w(x) onto every position below low part L inside the sparse bits
+__device__ inline void zeta_scatter(int64_t *tile, uint32_t low, int64_t w) {
+    const uint32_t fixed = low & ~kZetaSparseMask;
+    const uint32_t sm = low & kZetaSparseMask;
+    uint32_t sub = sm;
+    for (;;) {
+        atomicAdd((unsigned long long *)&tile[zpos((int)(fixed | sub))], (unsigned long long)w);
+        if (sub == 0) break;
+        sub = (sub - 1u) & sm;
+    }
 }
 
 // Persistent: each workgroup keeps up to kZetaHeld list entries per thread
@@ -212,67 +227,45 @@ __global__ __launch_bounds__(kZetaThreads) void k_weights_tile(
         my_w[i] = j < cnt ? list_w[j] : 0;
     }
     for (uint32_t hi = blockIdx.x; hi < n_tiles; hi += gridDim.x) {   // hi: high part H of the tile
-    lds_barrier();
-    for (int e = t; e < (kZetaN + kZetaN / 8) / 2; e += kZetaThreads)
-        reinterpret_cast<longlong2 *>(tile)[e] = make_longlong2(0, 0);
-    lds_barrier();
+        lds_barrier();
+        for (int e = t; e < (kZetaN + kZetaN / 8) / 2; e += kZetaThreads)
+            reinterpret_cast<longlong2 *>(tile)[e] = make_longlong2(0, 0);
+        lds_barrier();
 #pragma unroll
-    for (int i = 0; i < kZetaHeld; ++i) {
-        const uint32_t s = my_sig[i];
-        if (my_w[i] != 0 && ((s >> b) & hi) == hi)
-            atomicAdd((unsigned long long *)&tile[zpos((int)(s & lowmask))], (unsigned long long)my_w[i]);
-    }
-    for (uint32_t j = t + kZetaHeld * kZetaThreads; j < cnt; j += kZetaThreads) {
-        const uint32_t s = list_sig[j];
-        if (((s >> b) & hi) == hi)
-            atomicAdd((unsigned long long *)&tile[zpos((int)(s & lowmask))], (unsigned long long)list_w[j]);
-    }
-    if (hi == 0 && t == 0)
-        atomicAdd((unsigned long long *)&tile[0], (unsigned long long)zero_weight);
-    lds_barrier();
-    int64_t v[16];
-    // bits 0..3: elements 16 t + k, then bit 4 with the neighbouring lane
-    int64_t *row = tile + zpos(t << 4);
+        for (int i = 0; i < kZetaHeld; ++i) {
+            const uint32_t sg = my_sig[i];
+            if (my_w[i] != 0 && ((sg >> b) & hi) == hi) zeta_scatter(tile, sg & lowmask, my_w[i]);
+        }
+        for (uint32_t j = t + kZetaHeld * kZetaThreads; j < cnt; j += kZetaThreads) {
+            const uint32_t sg = list_sig[j];
+            if (((sg >> b) & hi) == hi) zeta_scatter(tile, sg & lowmask, list_w[j]);
+        }
+        if (hi == 0 && t == 0)
+            atomicAdd((unsigned long long *)&tile[0], (unsigned long long)zero_weight);
+        lds_barrier();
+        int64_t v[16];
+        // bits 5..8: element (t >> 5) << 9 | k << 5 | (t & 31)
+        const int eb = ((t >> 5) << 9) | (t & 31);
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-        const longlong2 x = reinterpret_cast<const longlong2 *>(row)[q];
-        v[2 * q] = x.x;
-        v[2 * q + 1] = x.y;
-    }
-    zeta16(v);
+        for (int k = 0; k < 16; ++k) v[k] = tile[zpos(eb | (k << 5))];
+        zeta16(v);
 #pragma unroll
-    for (int k = 0; k < 16; ++k) {
-        // value of the neighbouring lane (t ^ 1): DPP quad permutation [1,0,3,2]
-        const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)v[k], 0xB1, 0xF, 0xF, false);
-        const uint32_t hi32 = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(v[k] >> 32), 0xB1, 0xF, 0xF, false);
-        const int64_t o = (int64_t)(((uint64_t)hi32 << 32) | lo);
-        if (!(t & 1)) v[k] += o;
-    }
+        for (int k = 0; k < 16; ++k) tile[zpos(eb | (k << 5))] = v[k];
+        lds_barrier();
+        // bits 9..12: element t + 512 k, stored straight to HBM (each store
+        // instruction covers 512 contiguous bytes)
 #pragma unroll
-    for (int q = 0; q < 8; ++q) reinterpret_cast<longlong2 *>(row)[q] = make_longlong2(v[2 * q], v[2 * q + 1]);
-    lds_barrier();
-    // bits 5..8: element (t >> 5) << 9 | k << 5 | (t & 31)
-    const int eb = ((t >> 5) << 9) | (t & 31);
+        for (int k = 0; k < 16; ++k) v[k] = tile[zpos(t + (k << 9))];
+        zeta16(v);
+        int64_t *out = W + ((int64_t)hi << b);
+        if (m >= b) {
 #pragma unroll
-    for (int k = 0; k < 16; ++k) v[k] = tile[zpos(eb | (k << 5))];
-    zeta16(v);
+            for (int k = 0; k < 16; ++k) out[t + (k << 9)] = v[k];
+        } else {                        // one partial tile: only the first 2^m subsets exist
 #pragma unroll
-    for (int k = 0; k < 16; ++k) tile[zpos(eb | (k << 5))] = v[k];
-    lds_barrier();
-    // bits 9..12: element t + 512 k, stored straight to HBM (each store
-    // instruction covers 512 contiguous bytes)
-#pragma unroll
-    for (int k = 0; k < 16; ++k) v[k] = tile[zpos(t + (k << 9))];
-    zeta16(v);
-    int64_t *out = W + ((int64_t)hi << b);
-    if (m >= b) {
-#pragma unroll
-        for (int k = 0; k < 16; ++k) out[t + (k << 9)] = v[k];
-    } else {                        // one partial tile: only the first 2^m subsets exist
-#pragma unroll
-        for (int k = 0; k < 16; ++k)
-            if (t + (k << 9) < (1 << m)) out[t + (k << 9)] = v[k];
-    }
+            for (int k = 0; k < 16; ++k)
+                if (t + (k << 9) < (1 << m)) out[t + (k << 9)] = v[k];
+        }
     }
 }
 
@@ -708,6 +701,32 @@ __device__ inline void flush(const K best[NB], uint32_t s2, uint64_t *acc) {
             atomicMin((unsigned long long *)&acc[(s2 << CB) | x], (unsigned long long)Key<K>::bits(best[x]));
 }
 
+// DPP lane exchange of a 64-bit value inside rows of 8 lanes
+template <int CTRL>
+__device__ inline uint64_t dpp_get64(uint64_t b) {
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)b, CTRL, 0xF, 0xF, false);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(b >> 32), CTRL, 0xF, 0xF, false);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+// Flush of a self-pair item whose adjacent lanes share S2 in aligned groups
+// of seg = 1, 2, 4 or 8 lanes: min inside the group (quad permutations, then
+// the half-row mirror that pairs the two quads of 8 lanes) and one LDS
+// atomic per group and entry -- 64-bit LDS atomics are slow and contended.
+template <class K>
+__device__ inline void flush_group(const K best[NB], uint32_t s2, uint32_t seg, uint64_t *acc) {
+    const uint32_t lane = threadIdx.x & (kWave - 1);
+#pragma unroll
+    for (int x = 0; x < NB; ++x) {
+        uint64_t b = Key<K>::bits(best[x]);           // unsigned order = key order
+        if (seg >= 2) { const uint64_t o = dpp_get64<0xB1>(b); b = o < b ? o : b; }    // quad_perm [1,0,3,2]
+        if (seg >= 4) { const uint64_t o = dpp_get64<0x4E>(b); b = o < b ? o : b; }    // quad_perm [2,3,0,1]
+        if (seg >= 8) { const uint64_t o = dpp_get64<0x141>(b); b = o < b ? o : b; }   // row_half_mirror
+        if ((lane & (seg - 1)) == 0 && b != Key<K>::bits(Key<K>::none()))
+            atomicMin((unsigned long long *)&acc[(s2 << CB) | x], (unsigned long long)b);
+    }
+}
+
 // one self-pair work item (S2, first A2) against (rowS, row0): 2^min(|S2|,T)
 // submasks A2 of S2 in increasing order, skipping A2 == S2 and, when
 // skip_empty, A2 == 0
@@ -736,7 +755,8 @@ __device__ inline void run_item(uint32_t item, const K *pA, const K *tA, const K
         }
         a2 = ((a2 | ~s2) + 1u) & s2;
     }
-    flush<K>(best, s2, acc);
+    const uint32_t chunks = 1u << (k - (k < T ? k : T));
+    flush_group<K>(best, s2, chunks < 8u ? chunks : 8u, acc);
 }
 
 // plain C' of an entry of a tagged LDS row whose tag is the entry's own
@@ -755,6 +775,14 @@ __device__ void finalize_row(int m, uint32_t sh, Lds<K> &s, K *pS, K *tS, const 
     const uint32_t a_hi = sh << L;
     const uint64_t mask = ((uint64_t)1 << m) - 1u;
     for (int k = 0; k <= R2; ++k) {
+        // W of the block this thread finishes below, read ahead of phase 1
+        int64_t wv[NB];
+        const int bi0 = c_blocks.begin[k] + threadIdx.x;
+        if (bi0 < c_blocks.end[k]) {
+            const int64_t *wp = W + (a_hi | ((uint32_t)c_blocks.v[bi0] << CB));
+#pragma unroll
+            for (int x = 0; x < NB; ++x) wv[x] = wp[x];
+        }
         // A2 a proper submask of S2 (for S_H = 0 also non-empty: those pairs
         // mirror the in-block pairs below)
         for (int it = kItems.begin[k] + threadIdx.x; it < kItems.end[k]; it += THREADS)
@@ -780,7 +808,7 @@ __device__ void finalize_row(int m, uint32_t sh, Lds<K> &s, K *pS, K *tS, const 
                 for (int s1 = 0; s1 < NB; ++s1) {
                     if (cpop(s1) != pc) continue;
                     const uint32_t S = base | (uint32_t)s1;
-                    const int64_t w = W[S];
+                    const int64_t w = bi == bi0 ? wv[s1] : W[S];
                     if (S == 0) { out[s1] = SENT; sp[s1] = 0; continue; }
                     if (__popc(S) == 1) { out[s1] = (uint64_t)w << m; sp[s1] = 0; continue; }
                     uint64_t kb = Key<K>::value_of_bits(s.acc[(s2 << CB) | s1]);
