@@ -579,6 +579,11 @@ template <> struct Key<uint64_t> {
     static __device__ inline uint64_t bits(uint64_t k) { return k; }
     static __device__ inline uint64_t from_bits(uint64_t b) { return b; }
     static __device__ inline uint64_t value_of_bits(uint64_t b) { return b; }
+    // the packed table in HBM holds C' in the key's own representation
+    static __device__ inline uint64_t store(uint64_t c) { return c; }
+    static __device__ inline uint64_t stored_value(uint64_t b) { return b; }
+    static __device__ inline uint64_t load_plain(uint64_t b) { return b; }
+    static __device__ inline uint64_t load_tagged(uint64_t b, uint32_t idx) { return b + idx; }
 };
 template <> struct Key<double> {
     static __device__ inline double plain(uint64_t c) { return (double)c; }
@@ -592,16 +597,20 @@ template <> struct Key<double> {
     static __device__ inline uint64_t value_of_bits(uint64_t b) {
         return b >= 0x7ff0000000000000ull ? ~0ull : (uint64_t)__longlong_as_double((long long)b);
     }
+    static __device__ inline uint64_t store(uint64_t c) { return bits((double)c); }
+    static __device__ inline uint64_t stored_value(uint64_t b) { return (uint64_t)from_bits(b); }
+    static __device__ inline double load_plain(uint64_t b) { return from_bits(b); }
+    static __device__ inline double load_tagged(uint64_t b, uint32_t idx) { return from_bits(b) + (double)idx; }
 };
 
 // LDS rows. Block x2 sits at slot(x2) = x2 ^ (x2 >> 3 & 7) ^ (x2 >> 6 & 7),
 // a GF(2)-linear bijection, so slot(S2 ^ A2) = slot(S2) ^ slot(A2). Blocks
-// are padded to 80 bytes (tagged, 8 entries) and 48 bytes (plain, the 4
-// even entries): piece q of a block then falls in 16-byte bank group
-// (5 slot + q) mod 8 or (3 slot + q) mod 8, a bijection of slot mod 8, and
-// a lane's four (or two) 16-byte reads use immediate offsets.
-constexpr int TSTRIDE = 10;           // K elements per tagged block
-constexpr int PSTRIDE = 6;            // K elements per plain block
+// are padded by 16 bytes (tagged: NB entries, plain: the NE even entries),
+// to an odd number of 16-byte pieces: piece q of a block then falls in
+// 16-byte bank group (odd * slot + q) mod 8, a bijection of slot mod 8, and
+// a lane's 16-byte reads of one block use immediate offsets.
+constexpr int TSTRIDE = NB + 2;       // K elements per tagged block
+constexpr int PSTRIDE = NE + 2;       // K elements per plain block
 __device__ inline uint32_t slot_of(uint32_t x2) { return x2 ^ ((x2 >> 3) & 7u) ^ ((x2 >> 6) & 7u); }
 
 template <class K> struct alignas(16) Lds {
@@ -611,6 +620,7 @@ template <class K> struct alignas(16) Lds {
     K tb[NS2 * TSTRIDE];   // row on the B side, tagged
     uint64_t acc[ROW];     // best key bits per entry of the output row
 };
+static_assert(sizeof(Lds<double>) <= 160 * 1024, "rows and accumulators fit one CU's LDS");
 
 template <class K> struct Vec2;
 template <> struct Vec2<uint64_t> { using type = ulonglong2; };
@@ -621,7 +631,7 @@ __device__ inline void load_t(const K *row, uint32_t slot, K v[NB]) {
     using V = typename Vec2<K>::type;
     const V *p = reinterpret_cast<const V *>(row + slot * TSTRIDE);
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
+    for (int q = 0; q < NB / 2; ++q) {
         const V t = p[q];
         v[2 * q] = t.x;
         v[2 * q + 1] = t.y;
@@ -633,7 +643,7 @@ __device__ inline void load_p(const K *row, uint32_t slot, K v[NE]) {
     using V = typename Vec2<K>::type;
     const V *p = reinterpret_cast<const V *>(row + slot * PSTRIDE);
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
+    for (int q = 0; q < NE / 2; ++q) {
         const V t = p[q];
         v[2 * q] = t.x;
         v[2 * q + 1] = t.y;
@@ -646,16 +656,16 @@ __device__ inline void load_row(K *P, K *Tt, const uint64_t *__restrict__ C, uin
     const ulonglong2 *src = reinterpret_cast<const ulonglong2 *>(C + ((size_t)xh << L));
     const uint32_t tag = xh << L;
     for (int g = threadIdx.x; g < ROW / 2; g += THREADS) {
-        const int x2 = g >> 2, q = g & 3;                  // entries 2q, 2q+1 of block x2
+        const int x2 = g / (NB / 2), q = g % (NB / 2);     // entries 2q, 2q+1 of block x2
         const ulonglong2 v = src[g];
         const uint32_t idx = tag | (uint32_t)(2 * g);
         using V = typename Vec2<K>::type;
         const uint32_t sl = slot_of((uint32_t)x2);
         V t;
-        t.x = Key<K>::tagged(v.x, idx);
-        t.y = Key<K>::tagged(v.y, idx + 1u);
+        t.x = Key<K>::load_tagged(v.x, idx);
+        t.y = Key<K>::load_tagged(v.y, idx + 1u);
         *reinterpret_cast<V *>(Tt + sl * TSTRIDE + 2 * q) = t;
-        P[sl * PSTRIDE + q] = Key<K>::plain(v.x);
+        P[sl * PSTRIDE + q] = Key<K>::load_plain(v.x);
     }
 }
 
@@ -831,7 +841,7 @@ __device__ void finalize_row(int m, uint32_t sh, Lds<K> &s, K *pS, K *tS, const 
             for (int x = 0; x < NB; ++x) {
                 tS[sl * TSTRIDE + x] = Key<K>::tagged(out[x], base | (uint32_t)x);
                 if (!(x & 1)) pS[sl * PSTRIDE + (x >> 1)] = Key<K>::plain(out[x]);
-                Cp[base + x] = out[x];
+                Cp[base + x] = Key<K>::store(out[x]);
                 split[base + x] = sp[x];
             }
         }
@@ -952,10 +962,11 @@ __global__ __launch_bounds__(THREADS) void k_rb_final(int m, int h, uint32_t chu
 }
 
 // packed C' -> C (C[0] keeps the documented sentinel)
+template <class K>
 __global__ void k_rb_unpack(int m, int64_t *C) {
     const int64_t n = (int64_t)1 << m;
     for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
-        C[i] = i == 0 ? kInf : (int64_t)((uint64_t)C[i] >> m);
+        C[i] = i == 0 ? kInf : (int64_t)(Key<K>::stored_value((uint64_t)C[i]) >> m);
 }
 
 // sum_i W({i}), saturated, for the packed-key eligibility test
@@ -1255,7 +1266,7 @@ int solve_rb(int m, const int64_t *W, int64_t *C, uint32_t *split, uint64_t *par
     const int64_t n = (int64_t)1 << m;
     {
         LaunchScope ls("rb_unpack", 16.0 * n, s);
-        rb::k_rb_unpack<<<grid_for(n, 256, 16384), 256, 0, s>>>(m, C);
+        rb::k_rb_unpack<K><<<grid_for(n, 256, 16384), 256, 0, s>>>(m, C);
     }
     HIP_TRY(hipGetLastError());
     return MPT_OK;
