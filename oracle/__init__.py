@@ -7,7 +7,9 @@ the product path.
 
 * :mod:`oracle.mpt_oracle` (C, built into ``libmpt_oracle.so``): W table,
   exact DP, layout read-off, trie cost and hierarchy cost, written from the
-  paper's definitions (Section 2 Eq. 1, Section 3 Thm 1 Eqs. 2-3, Section 3.1).
+  paper's definitions (Section 2 Eq. 1, Section 3 Thm 1 Eqs. 2-3, Section 3.1);
+  pair weights, the agglomerative hierarchy, its layout and savings, and the
+  spanning-tree bound for any m (Sections 6.2-6.3, Theorem 6).
 * :mod:`oracle.brute` (pure Python, tiny inputs only): brute force over
   permutations, over hierarchies and over global orders, vertex cover, and the
   closed forms of Section 5 -- the pins that check the C oracle.
@@ -58,6 +60,14 @@ def _load():
     lib.oracle_hierarchy_cost.argtypes = [i32, i64, P, P, P, P]
     lib.oracle_hierarchy_cost.restype = i64
     lib.oracle_max_threads.restype = i32
+    lib.oracle_pair_weights.argtypes = [i32, i64, P, P, P, P, i32]
+    lib.oracle_greedy.argtypes = [i32, i64, P, P, P, P, P, P, P, i32]
+    lib.oracle_greedy.restype = i64
+    lib.oracle_tree_orders.argtypes = [i32, i64, P, P, i32, P, P]
+    lib.oracle_tree_savings.argtypes = [i32, i64, P, P, P, i32, P]
+    lib.oracle_tree_savings.restype = i64
+    lib.oracle_max_spanning_tree.argtypes = [i32, P]
+    lib.oracle_max_spanning_tree.restype = i64
     _lib = lib
     return lib
 
@@ -170,4 +180,80 @@ def solve(inst, threads: int = 0, with_orders: bool = True) -> dict:
            "opt": int(C[full]), "savings": int(M[full])}
     if with_orders:
         res["orders"] = orders(inst, split)
+    return res
+
+
+# --- Sections 6.2-6.3: agglomerative hierarchy and spanning-tree bound -----
+
+def pair_weights(inst, threads: int = 0) -> np.ndarray:
+    """P[i, j] = w(R_i ∩ R_j) for all requests (diagonal: w(R_i))."""
+    lib = _load()
+    w, off, ch = _arrays(inst)
+    P = np.empty((inst.m, inst.m), dtype=np.int64)
+    _check(lib.oracle_pair_weights(inst.m, inst.n_chunks, _p(w), _p(off), _p(ch), _p(P), threads),
+           "pair_weights")
+    return P
+
+
+def greedy(inst, threads: int = 0) -> dict:
+    """Agglomerative hierarchy H_g (Section 6.2, Theorem 6): merges (a_t, b_t)
+    with gains g_t, node parents (leaf i = node i, step t = node m + t) and
+    SAV(H_g)."""
+    lib = _load()
+    m = inst.m
+    w, off, ch = _arrays(inst)
+    a = np.full(max(1, m - 1), -1, dtype=np.int32)
+    b = np.full(max(1, m - 1), -1, dtype=np.int32)
+    g = np.full(max(1, m - 1), -1, dtype=np.int64)
+    parent = np.full(2 * m - 1, -2, dtype=np.int32)
+    sav = int(lib.oracle_greedy(m, inst.n_chunks, _p(w), _p(off), _p(ch), _p(a), _p(b), _p(g), _p(parent),
+                                threads))
+    _check(sav, "greedy")
+    return {"merge_a": a[:m - 1], "merge_b": b[:m - 1], "gain": g[:m - 1], "parent": parent, "savings": sav}
+
+
+def tree_orders(inst, parent: np.ndarray) -> np.ndarray:
+    """Layout read off an explicit hierarchy (proof of Theorem 1), CSR with
+    the instance's req_off."""
+    lib = _load()
+    w, off, ch = _arrays(inst)
+    par = np.ascontiguousarray(parent, dtype=np.int32)
+    out = np.full(max(1, inst.nnz), -1, dtype=np.int32)
+    _check(lib.oracle_tree_orders(inst.m, inst.n_chunks, _p(off), _p(ch), int(par.size), _p(par), _p(out)),
+           "tree_orders")
+    return out[:inst.nnz]
+
+
+def tree_savings(inst, parent: np.ndarray) -> int:
+    """SAV(H) = sum over internal nodes of w(I(v)) (Eq. 3) for an explicit
+    hierarchy."""
+    lib = _load()
+    w, off, ch = _arrays(inst)
+    par = np.ascontiguousarray(parent, dtype=np.int32)
+    s = int(lib.oracle_tree_savings(inst.m, inst.n_chunks, _p(w), _p(off), _p(ch), int(par.size), _p(par)))
+    _check(s, "tree_savings")
+    return s
+
+
+def max_spanning_tree(P: np.ndarray) -> int:
+    """Weight of a maximum spanning tree of the complete graph with edge
+    weights P (Prim)."""
+    lib = _load()
+    P = np.ascontiguousarray(P, dtype=np.int64)
+    v = int(lib.oracle_max_spanning_tree(int(P.shape[0]), _p(P)))
+    _check(v, "max_spanning_tree")
+    return v
+
+
+def greedy_solve(inst, threads: int = 0) -> dict:
+    """H_g, its layout, and the spanning-tree bound of Sections 6.2-6.3."""
+    P = pair_weights(inst, threads)
+    total = int(np.trace(P))
+    res = greedy(inst, threads)
+    res["orders"] = tree_orders(inst, res["parent"])
+    res["cost"] = total - res["savings"]
+    res["request_total"] = total
+    res["mst"] = max_spanning_tree(P)
+    res["lower_bound"] = total - res["mst"]
+    res["P"] = P
     return res

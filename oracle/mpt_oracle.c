@@ -18,6 +18,10 @@
  *   trie cost        sum over non-root trie nodes of w(chunk)     (Section 2, Eq. 1)
  *   hierarchy cost   sum_x w(x) t_x(H), t_x = number of maximal
  *                    clusters of H inside S_x                     (Thm 1, Eq. 2)
+ *   greedy H_g       merge the two clusters sharing the most
+ *                    weight, signature = intersection         (Section 6.2)
+ *   spanning tree    OPT_free >= sum_i w(R_i) - max spanning tree
+ *                    of w(R_i ∩ R_j)                  (Section 6.3, Thm 6)
  *
  * Readings where the paper is silent (each one is listed with its reason in
  * the design notes of the repository):
@@ -25,7 +29,10 @@
  *   - the part that contains the lowest request of B is called B1, and among
  *     optimal bipartitions the one with the numerically smallest B1 is kept;
  *   - inside a node the newly common chunks are emitted in ascending id;
- *   - I(empty) = U, so W(empty) counts every chunk, even unrequested ones.
+ *   - I(empty) = U, so W(empty) counts every chunk, even unrequested ones;
+ *   - greedy ties: a cluster is named by its smallest request, the
+ *     lexicographically smallest pair of names merges, the merge keeps the
+ *     smaller name.
  *
  * Build: gcc -O2 -fopenmp -shared -fPIC mpt_oracle.c -o libmpt_oracle.so
  */
@@ -302,3 +309,344 @@ done:
 }
 
 int oracle_max_threads(void) { return omp_get_max_threads(); }
+
+/* ===== Sections 6.2-6.3: agglomerative hierarchy, spanning-tree bound =====
+ *
+ * These functions take any m (requests are identified by index, not by a
+ * bit of a mask) and work on sorted chunk lists.
+ */
+
+static int cmp_i32(const void *a, const void *b)
+{
+    int32_t x = *(const int32_t *)a, y = *(const int32_t *)b;
+    return (x > y) - (x < y);
+}
+
+/* Every request as an ascending chunk list at out[req_off[i] ..). Rejects
+ * ids out of range and chunks repeated inside a request. */
+static int sorted_requests(int m, int64_t n_chunks, const int64_t *req_off,
+                           const int32_t *req_chunks, int32_t *out)
+{
+    for (int i = 0; i < m; ++i) {
+        int64_t lo = req_off[i], hi = req_off[i + 1];
+        if (hi < lo) return OR_E_INVALID;
+        for (int64_t j = lo; j < hi; ++j) {
+            if (req_chunks[j] < 0 || req_chunks[j] >= n_chunks) return OR_E_RANGE;
+            out[j] = req_chunks[j];
+        }
+        qsort(out + lo, (size_t)(hi - lo), sizeof(int32_t), cmp_i32);
+        for (int64_t j = lo + 1; j < hi; ++j)
+            if (out[j] == out[j - 1]) return OR_E_DUP;
+    }
+    return OR_OK;
+}
+
+/* w(a ∩ b) of two ascending lists */
+static int64_t inter_weight(const int32_t *a, int64_t na, const int32_t *b, int64_t nb,
+                            const int64_t *w)
+{
+    int64_t i = 0, j = 0, s = 0;
+    while (i < na && j < nb) {
+        if (a[i] < b[j]) ++i;
+        else if (a[i] > b[j]) ++j;
+        else { s += w[a[i]]; ++i; ++j; }
+    }
+    return s;
+}
+
+/* a ∩ b of two ascending lists, written ascending to out; returns its size */
+static int64_t inter_list(const int32_t *a, int64_t na, const int32_t *b, int64_t nb, int32_t *out)
+{
+    int64_t i = 0, j = 0, n = 0;
+    while (i < na && j < nb) {
+        if (a[i] < b[j]) ++i;
+        else if (a[i] > b[j]) ++j;
+        else { out[n++] = a[i]; ++i; ++j; }
+    }
+    return n;
+}
+
+/*
+ * Pair weights P[i*m + j] = w(R_i ∩ R_j) for all requests i, j, so the
+ * diagonal holds w(R_i). These are the edge weights of the spanning-tree
+ * bound and the values of the greedy's first merge (Sections 6.2-6.3).
+ */
+int oracle_pair_weights(int m, int64_t n_chunks, const int64_t *w, const int64_t *req_off,
+                        const int32_t *req_chunks, int64_t *P, int threads)
+{
+    if (m < 1 || n_chunks < 0) return OR_E_INVALID;
+    int32_t *srt = (int32_t *)malloc(sizeof(int32_t) * (size_t)(req_off[m] > 0 ? req_off[m] : 1));
+    if (!srt) return OR_E_NOMEM;
+    int rc = sorted_requests(m, n_chunks, req_off, req_chunks, srt);
+    if (rc == OR_OK) {
+        if (threads > 0) omp_set_num_threads(threads);
+#pragma omp parallel for schedule(dynamic, 4)
+        for (int i = 0; i < m; ++i)
+            for (int j = 0; j < m; ++j)
+                P[(size_t)i * m + j] = inter_weight(srt + req_off[i], req_off[i + 1] - req_off[i],
+                                                    srt + req_off[j], req_off[j + 1] - req_off[j], w);
+    }
+    free(srt);
+    return rc;
+}
+
+/*
+ * Agglomerative common-prefix hierarchy (Section 6.2; H_g of Theorem 6).
+ * Every request starts as a cluster whose signature is R_i. While two or
+ * more clusters remain, the pair whose signatures share the most weight is
+ * merged, and the merged signature is the intersection of the two.
+ *
+ * Reading where the paper is silent (ties): a cluster is named by its
+ * smallest request; among pairs of equal value the lexicographically
+ * smallest pair of names (a, b), a < b, merges, and the merged cluster keeps
+ * the name a.
+ *
+ * Plain: each step scans all active pairs for the maximum and recomputes
+ * the values of the new cluster against every other one from the lists.
+ *
+ * Outputs for step t = 0 .. m-2: merge_a[t] < merge_b[t], gain[t] =
+ * w(I(A) ∩ I(B)). node_parent[v] for the 2m-1 nodes: leaf i is node i, the
+ * merge of step t creates node m + t, the root's parent is -1.
+ * Returns SAV(H_g) = sum of the gains (Theorem 6), or a negative status.
+ */
+int64_t oracle_greedy(int m, int64_t n_chunks, const int64_t *w, const int64_t *req_off,
+                      const int32_t *req_chunks, int32_t *merge_a, int32_t *merge_b,
+                      int64_t *gain, int32_t *node_parent, int threads)
+{
+    if (m < 1 || n_chunks < 0) return OR_E_INVALID;
+    int64_t nnz = req_off[m];
+    int64_t sav = 0;
+    int32_t *srt = (int32_t *)malloc(sizeof(int32_t) * (size_t)(nnz > 0 ? nnz : 1));
+    int32_t *tmp = (int32_t *)malloc(sizeof(int32_t) * (size_t)(nnz > 0 ? nnz : 1));
+    int64_t *len = (int64_t *)malloc(sizeof(int64_t) * (size_t)m);
+    int64_t *V = (int64_t *)malloc(sizeof(int64_t) * (size_t)m * (size_t)m);
+    unsigned char *active = (unsigned char *)malloc((size_t)m);
+    int32_t *node_of = (int32_t *)malloc(sizeof(int32_t) * (size_t)m);
+    int64_t *row_best = (int64_t *)malloc(sizeof(int64_t) * (size_t)m);
+    int32_t *row_arg = (int32_t *)malloc(sizeof(int32_t) * (size_t)m);
+    if (!srt || !tmp || !len || !V || !active || !node_of || !row_best || !row_arg) { sav = OR_E_NOMEM; goto done; }
+    int rc = sorted_requests(m, n_chunks, req_off, req_chunks, srt);
+    if (rc != OR_OK) { sav = rc; goto done; }
+    if (threads > 0) omp_set_num_threads(threads);
+    /* signature of cluster a lives at srt[req_off[a] ..), len[a] entries;
+     * it only ever shrinks, so it stays in place */
+    for (int a = 0; a < m; ++a) {
+        len[a] = req_off[a + 1] - req_off[a];
+        active[a] = 1;
+        node_of[a] = a;
+        node_parent[a] = -1;
+    }
+#pragma omp parallel for schedule(dynamic, 4)
+    for (int a = 0; a < m; ++a)
+        for (int b = 0; b < m; ++b)
+            V[(size_t)a * m + b] = inter_weight(srt + req_off[a], len[a], srt + req_off[b], len[b], w);
+    for (int t = 0; t + 1 < m; ++t) {
+        /* the first maximum in (a, b) order is the lexicographically smallest */
+#pragma omp parallel for schedule(dynamic, 16)
+        for (int a = 0; a < m; ++a) {
+            row_best[a] = -1; row_arg[a] = -1;
+            if (!active[a]) continue;
+            for (int b = a + 1; b < m; ++b)
+                if (active[b] && V[(size_t)a * m + b] > row_best[a]) { row_best[a] = V[(size_t)a * m + b]; row_arg[a] = b; }
+        }
+        int ba = -1, bb = -1;
+        int64_t bv = -1;
+        for (int a = 0; a < m; ++a)
+            if (row_arg[a] >= 0 && row_best[a] > bv) { bv = row_best[a]; ba = a; bb = row_arg[a]; }
+        if (ba < 0) { sav = OR_E_INVALID; goto done; }
+        merge_a[t] = ba; merge_b[t] = bb; gain[t] = bv;
+        sav += bv;
+        int64_t n = inter_list(srt + req_off[ba], len[ba], srt + req_off[bb], len[bb], tmp);
+        memcpy(srt + req_off[ba], tmp, sizeof(int32_t) * (size_t)n);
+        len[ba] = n;
+        active[bb] = 0;
+        node_parent[node_of[ba]] = m + t;
+        node_parent[node_of[bb]] = m + t;
+        node_parent[m + t] = -1;
+        node_of[ba] = m + t;
+#pragma omp parallel for schedule(dynamic, 16)
+        for (int c = 0; c < m; ++c) {
+            if (!active[c] || c == ba) continue;
+            int64_t v = inter_weight(srt + req_off[ba], len[ba], srt + req_off[c], len[c], w);
+            V[(size_t)ba * m + c] = v;
+            V[(size_t)c * m + ba] = v;
+        }
+    }
+done:
+    free(srt); free(tmp); free(len); free(V); free(active); free(node_of); free(row_best); free(row_arg);
+    return sav;
+}
+
+/* Nodes of an explicit hierarchy in an order where every child comes before
+ * its parent; fills child lists. Returns the root or a negative status. */
+static int tree_children(int m, int n_nodes, const int32_t *node_parent, int32_t *kid0, int32_t *kid1,
+                         int32_t *order)
+{
+    int root = -1;
+    for (int v = 0; v < n_nodes; ++v) { kid0[v] = -1; kid1[v] = -1; }
+    for (int v = 0; v < n_nodes; ++v) {
+        int p = node_parent[v];
+        if (p < 0) { if (root >= 0) return OR_E_INVALID; root = v; continue; }
+        if (p < m || p >= n_nodes) return OR_E_INVALID;
+        if (kid0[p] < 0) kid0[p] = v;
+        else if (kid1[p] < 0) kid1[p] = v;
+        else return OR_E_INVALID;
+    }
+    if (root < 0) return OR_E_INVALID;
+    /* post-order by an explicit stack */
+    int32_t *stack = (int32_t *)malloc(sizeof(int32_t) * 2 * (size_t)n_nodes);
+    unsigned char *seen = (unsigned char *)calloc((size_t)n_nodes, 1);
+    if (!stack || !seen) { free(stack); free(seen); return OR_E_NOMEM; }
+    int sp = 0, cnt = 0;
+    stack[sp++] = root;
+    while (sp > 0) {
+        int v = stack[sp - 1];
+        if (v >= m && !seen[v]) {
+            seen[v] = 1;
+            if (kid0[v] < 0 || kid1[v] < 0) { free(stack); free(seen); return OR_E_INVALID; }
+            stack[sp++] = kid0[v];
+            stack[sp++] = kid1[v];
+        } else {
+            --sp;
+            order[cnt++] = v;
+        }
+    }
+    free(stack); free(seen);
+    if (cnt != n_nodes) return OR_E_INVALID;
+    return root;
+}
+
+/* I(v) of every node of an explicit hierarchy, as ascending lists:
+ * I(leaf i) = R_i, I(v) = I(kid0) ∩ I(kid1). list[v] is malloc'd. */
+static int node_intersections(int m, int64_t n_chunks, const int64_t *req_off, const int32_t *req_chunks,
+                              int n_nodes, const int32_t *node_parent, int32_t **list, int64_t *len,
+                              int32_t *parent_out, int *root_out)
+{
+    int32_t *kid0 = (int32_t *)malloc(sizeof(int32_t) * (size_t)n_nodes);
+    int32_t *kid1 = (int32_t *)malloc(sizeof(int32_t) * (size_t)n_nodes);
+    int32_t *order = (int32_t *)malloc(sizeof(int32_t) * (size_t)n_nodes);
+    int64_t nnz = req_off[m];
+    int32_t *srt = (int32_t *)malloc(sizeof(int32_t) * (size_t)(nnz > 0 ? nnz : 1));
+    int rc = OR_OK;
+    if (!kid0 || !kid1 || !order || !srt) { rc = OR_E_NOMEM; goto done; }
+    for (int v = 0; v < n_nodes; ++v) { list[v] = NULL; len[v] = 0; parent_out[v] = node_parent[v]; }
+    rc = sorted_requests(m, n_chunks, req_off, req_chunks, srt);
+    if (rc != OR_OK) goto done;
+    rc = tree_children(m, n_nodes, node_parent, kid0, kid1, order);
+    if (rc < 0) goto done;
+    *root_out = rc;
+    rc = OR_OK;
+    for (int k = 0; k < n_nodes; ++k) {
+        int v = order[k];
+        if (v < m) {
+            len[v] = req_off[v + 1] - req_off[v];
+            list[v] = (int32_t *)malloc(sizeof(int32_t) * (size_t)(len[v] > 0 ? len[v] : 1));
+            if (!list[v]) { rc = OR_E_NOMEM; goto done; }
+            memcpy(list[v], srt + req_off[v], sizeof(int32_t) * (size_t)len[v]);
+        } else {
+            int a = kid0[v], b = kid1[v];
+            int64_t cap = len[a] < len[b] ? len[a] : len[b];
+            list[v] = (int32_t *)malloc(sizeof(int32_t) * (size_t)(cap > 0 ? cap : 1));
+            if (!list[v]) { rc = OR_E_NOMEM; goto done; }
+            len[v] = inter_list(list[a], len[a], list[b], len[b], list[v]);
+        }
+    }
+done:
+    free(kid0); free(kid1); free(order); free(srt);
+    return rc;
+}
+
+/*
+ * Layout read off an explicit hierarchy (proof of Theorem 1, "<=" half), for
+ * any m: leaves 0 .. m-1 are the requests, node_parent[v] is the parent of
+ * node v (-1 at the root) and internal nodes m .. n_nodes-1 have two
+ * children each. Node v emits I(v) \ I(parent(v)) in ascending chunk id,
+ * top-down; pi_i goes to order_chunks[req_off[i] ..).
+ */
+int oracle_tree_orders(int m, int64_t n_chunks, const int64_t *req_off, const int32_t *req_chunks,
+                       int n_nodes, const int32_t *node_parent, int32_t *order_chunks)
+{
+    if (m < 1 || n_nodes != 2 * m - 1) return OR_E_INVALID;
+    int32_t **list = (int32_t **)calloc((size_t)n_nodes, sizeof(int32_t *));
+    int64_t *len = (int64_t *)malloc(sizeof(int64_t) * (size_t)n_nodes);
+    int32_t *par = (int32_t *)malloc(sizeof(int32_t) * (size_t)n_nodes);
+    int32_t *path = (int32_t *)malloc(sizeof(int32_t) * (size_t)n_nodes);
+    int root = -1, rc = OR_OK;
+    if (!list || !len || !par || !path) { rc = OR_E_NOMEM; goto done; }
+    rc = node_intersections(m, n_chunks, req_off, req_chunks, n_nodes, node_parent, list, len, par, &root);
+    if (rc != OR_OK) goto done;
+    for (int i = 0; i < m; ++i) {
+        int d = 0;
+        for (int v = i; v >= 0; v = par[v]) path[d++] = v;     /* leaf .. root */
+        int64_t pos = req_off[i];
+        for (int k = d - 1; k >= 0; --k) {                      /* root .. leaf */
+            int v = path[k], p = par[v];
+            for (int64_t e = 0; e < len[v]; ++e) {
+                int32_t x = list[v][e];
+                int in_parent = 0;
+                if (p >= 0)
+                    for (int64_t f = 0; f < len[p]; ++f)
+                        if (list[p][f] == x) { in_parent = 1; break; }
+                if (in_parent) continue;
+                if (pos >= req_off[i + 1]) { rc = OR_E_INVALID; goto done; }
+                order_chunks[pos++] = x;
+            }
+        }
+        if (pos != req_off[i + 1]) { rc = OR_E_INVALID; goto done; }
+    }
+done:
+    if (list) for (int v = 0; v < n_nodes; ++v) free(list[v]);
+    free(list); free(len); free(par); free(path);
+    return rc;
+}
+
+/* SAV(H) = sum over internal nodes v of w(I(v)) for an explicit hierarchy
+ * (Theorem 1, Eq. 3), computed from the node lists. */
+int64_t oracle_tree_savings(int m, int64_t n_chunks, const int64_t *w, const int64_t *req_off,
+                            const int32_t *req_chunks, int n_nodes, const int32_t *node_parent)
+{
+    if (m < 1 || n_nodes != 2 * m - 1) return OR_E_INVALID;
+    int32_t **list = (int32_t **)calloc((size_t)n_nodes, sizeof(int32_t *));
+    int64_t *len = (int64_t *)malloc(sizeof(int64_t) * (size_t)n_nodes);
+    int32_t *par = (int32_t *)malloc(sizeof(int32_t) * (size_t)n_nodes);
+    int root = -1;
+    int64_t sav = 0;
+    if (!list || !len || !par) { sav = OR_E_NOMEM; goto done; }
+    int rc = node_intersections(m, n_chunks, req_off, req_chunks, n_nodes, node_parent, list, len, par, &root);
+    if (rc != OR_OK) { sav = rc; goto done; }
+    for (int v = m; v < n_nodes; ++v)
+        for (int64_t e = 0; e < len[v]; ++e) sav += w[list[v][e]];
+done:
+    if (list) for (int v = 0; v < n_nodes; ++v) free(list[v]);
+    free(list); free(len); free(par);
+    return sav;
+}
+
+/*
+ * Spanning-tree bound (Section 6.3, after Theorem 6): the savings of any
+ * hierarchy are at most the weight of a maximum spanning tree of the
+ * complete graph on the requests with edge weights P[i][j] = w(R_i ∩ R_j),
+ * so OPT_free >= sum_i w(R_i) - MST. Prim's algorithm, O(m^2). Returns the
+ * weight of a maximum spanning tree.
+ */
+int64_t oracle_max_spanning_tree(int m, const int64_t *P)
+{
+    if (m < 1) return OR_E_INVALID;
+    int64_t *key = (int64_t *)malloc(sizeof(int64_t) * (size_t)m);
+    unsigned char *in = (unsigned char *)calloc((size_t)m, 1);
+    if (!key || !in) { free(key); free(in); return OR_E_NOMEM; }
+    int64_t total = 0;
+    for (int v = 0; v < m; ++v) key[v] = -1;
+    key[0] = 0;
+    for (int it = 0; it < m; ++it) {
+        int u = -1;
+        for (int v = 0; v < m; ++v)
+            if (!in[v] && (u < 0 || key[v] > key[u])) u = v;
+        in[u] = 1;
+        total += key[u];
+        for (int v = 0; v < m; ++v)
+            if (!in[v] && v != u && P[(size_t)u * m + v] > key[v]) key[v] = P[(size_t)u * m + v];
+    }
+    free(key); free(in);
+    return total;
+}
