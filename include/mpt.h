@@ -119,6 +119,72 @@ int mpt_extract_orders(int m, int64_t n_chunks, int64_t nnz,
                        int32_t *order_chunks, void *workspace,
                        size_t workspace_bytes, void *stream);
 
+/*
+ * ---- Sections 6.2-6.3: heuristic and bound for large request counts ----
+ *
+ * These calls take any m in [1, MPT_GREEDY_MAX_M]; requests are identified
+ * by index. Same conventions as above; they share one workspace of
+ * mpt_greedy_workspace_bytes(m, n_chunks, nnz) bytes (about 8 m^2 + 44 nnz
+ * + 8 n_chunks bytes). Instances are validated as for mpt_build_weights.
+ */
+#define MPT_GREEDY_MAX_M 16384
+
+/* Bytes of device workspace for the calls below (0 for sizes out of range). */
+size_t mpt_greedy_workspace_bytes(int m, int64_t n_chunks, int64_t nnz);
+
+/*
+ * Pair weights P[i*m + j] = w(R_i ∩ R_j) for all requests i, j (so
+ * P[i*m + i] = w(R_i)): the edge weights of the spanning-tree bound and the
+ * values of the greedy's first merge (Sections 6.2-6.3).
+ *   P [m*m]         out: int64, row-major, device
+ *   request_total   HOST out, nullable: sum_i w(R_i)
+ * Cost: one scatter per pair of requests sharing a chunk, i.e.
+ * sum_x |S_x|^2 atomic adds -- meant for sparse demand (small |S_x|).
+ * Synchronises `stream` (twice) to report validation errors.
+ */
+int mpt_pair_weights(int m, int64_t n_chunks, int64_t nnz, const int64_t *chunk_w,
+                     const int64_t *req_off, const int32_t *req_chunks, int64_t *P,
+                     int64_t *request_total, void *workspace, size_t workspace_bytes,
+                     void *stream);
+
+/*
+ * Agglomerative common-prefix hierarchy H_g (Section 6.2; Theorem 6 shows
+ * SAV(H_g) >= SAV* / 2). Every request starts as a cluster with signature
+ * R_i; m-1 times, the two clusters whose signatures share the most weight
+ * merge, and the merged signature is their intersection. A cluster is named
+ * by its smallest request; among pairs of equal value the lexicographically
+ * smallest pair of names (a, b), a < b, merges and keeps the name a.
+ *   merge_a, merge_b [m-1]  out: int32 names of step t's pair, a < b
+ *   gain [m-1]              out: int64 w(I(A) ∩ I(B)) of step t
+ *                           (non-increasing, Theorem 6 part i)
+ *   node_parent [2m-1]      out: int32 parent of each node (-1 at the root);
+ *                           leaf i is node i, step t creates node m + t
+ *   order_chunks [nnz]      out, nullable: the layout read off H_g (proof of
+ *                           Theorem 1): top-down, node v emits
+ *                           I(v) \ I(parent(v)) in ascending chunk id;
+ *                           pi_i at order_chunks[req_off[i] ..)
+ *   savings                 HOST out, nullable: SAV(H_g) = sum of the gains;
+ *                           the layout costs at most sum_i w(R_i) - SAV(H_g)
+ * Synchronises `stream` before returning.
+ */
+int mpt_greedy_hierarchy(int m, int64_t n_chunks, int64_t nnz, const int64_t *chunk_w,
+                         const int64_t *req_off, const int32_t *req_chunks,
+                         int32_t *merge_a, int32_t *merge_b, int64_t *gain,
+                         int32_t *node_parent, int32_t *order_chunks, int64_t *savings,
+                         void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Spanning-tree lower bound (Section 6.3): every hierarchy's savings are at
+ * most the weight of a maximum spanning tree of the complete graph on the
+ * requests with edge weights P[i][j] (from mpt_pair_weights), so
+ *     OPT_free >= sum_i P[i][i] - MST.
+ *   P            [m*m] int64 pair weights, device
+ *   mst_weight   HOST out: weight of a maximum spanning tree
+ * Uses the first 256 bytes of the workspace; synchronises `stream`.
+ */
+int mpt_spanning_tree_bound(int m, const int64_t *P, int64_t *mst_weight,
+                            void *workspace, size_t workspace_bytes, void *stream);
+
 /* Static text for a status code. */
 const char *mpt_status_string(int status);
 

@@ -22,9 +22,15 @@
 #include <string>
 #include <vector>
 
+#include "common.h"
 #include "mpt.h"
 
 namespace {
+
+using mptlib::fail;
+using mptlib::grid_for;
+using mptlib::LaunchScope;
+using mptlib::align256;
 
 constexpr int kWave = 64;
 constexpr int64_t kInf = MPT_COST_SENTINEL;   // C[empty]: never part of a minimum
@@ -57,8 +63,6 @@ struct WsHeader {
     int64_t pad[30];
 };
 static_assert(sizeof(WsHeader) == 256, "header is one 256-byte block");
-
-inline size_t align256(size_t b) { return (b + 255) & ~size_t(255); }
 
 // ---------------------------------------------------------------------------
 // small device helpers
@@ -1046,59 +1050,6 @@ __global__ __launch_bounds__(256) void k_extract(int m, int64_t n_chunks, int64_
 // ---------------------------------------------------------------------------
 // host side
 
-thread_local std::string t_last_error;
-
-int fail(int status, const char *fmt, ...) {
-    char buf[512];
-    va_list ap;
-    va_start(ap, fmt);
-    vsnprintf(buf, sizeof buf, fmt, ap);
-    va_end(ap);
-    t_last_error = buf;
-    return status;
-}
-
-#define HIP_TRY(expr)                                                                      \
-    do {                                                                                   \
-        hipError_t e_ = (expr);                                                            \
-        if (e_ != hipSuccess)                                                              \
-            return fail(MPT_E_DEVICE, "%s: %s (%s:%d)", #expr, hipGetErrorString(e_),     \
-                        __FILE__, __LINE__);                                               \
-    } while (0)
-
-// --- event profiler ---------------------------------------------------------
-struct ProfRecord { std::string name; double work; hipEvent_t a, b; };
-struct Profiler {
-    std::mutex mu;
-    bool on = false;
-    std::vector<ProfRecord> recs;
-} g_prof;
-
-struct LaunchScope {
-    hipStream_t s;
-    bool active = false;
-    hipEvent_t a{}, b{};
-    const char *name;
-    double work;
-    LaunchScope(const char *n, double wk, hipStream_t st) : s(st), name(n), work(wk) {
-        std::lock_guard<std::mutex> g(g_prof.mu);
-        if (!g_prof.on) return;
-        if (hipEventCreate(&a) != hipSuccess || hipEventCreate(&b) != hipSuccess) return;
-        active = hipEventRecord(a, s) == hipSuccess;
-    }
-    ~LaunchScope() {
-        if (!active) return;
-        std::lock_guard<std::mutex> g(g_prof.mu);
-        if (hipEventRecord(b, s) == hipSuccess) g_prof.recs.push_back({name, work, a, b});
-    }
-};
-
-inline int grid_for(int64_t n, int threads, int cap = 8192) {
-    int64_t g = (n + threads - 1) / threads;
-    if (g < 1) g = 1;
-    if (g > cap) g = cap;
-    return (int)g;
-}
 
 // layer plan of the DP: which kernel and how many segments per subset
 struct LayerPlan { int p; uint32_t n_sets; int kind; int seg_bits; int seg_log; uint32_t n_tasks; };
@@ -1215,8 +1166,8 @@ int check_ws(int m, int64_t nnz, void *ws, size_t bytes) {
 
 int read_errors(WsHeader *h, hipStream_t s) {
     uint32_t err = 0;
-    HIP_TRY(hipMemcpyAsync(&err, &h->err, sizeof err, hipMemcpyDeviceToHost, s));
-    HIP_TRY(hipStreamSynchronize(s));
+    MPT_HIP_TRY(hipMemcpyAsync(&err, &h->err, sizeof err, hipMemcpyDeviceToHost, s));
+    MPT_HIP_TRY(hipStreamSynchronize(s));
     if (err & ERR_INVALID) return fail(MPT_E_INVALID, "req_off is not a CSR offset array of length m+1 ending at nnz, or split is not a hierarchy");
     if (err & ERR_RANGE) return fail(MPT_E_RANGE, "a chunk id is outside [0, n_chunks)");
     if (err & ERR_DUP) return fail(MPT_E_DUP, "a chunk is repeated inside one request");
@@ -1261,14 +1212,14 @@ int solve_rb(int m, const int64_t *W, int64_t *C, uint32_t *split, uint64_t *par
                 rb::k_rb_final<K><<<P.n_sets, rb::THREADS, 0, s>>>(m, P.h, P.chunks, W, Cp, split, partial);
             }
         }
-        HIP_TRY(hipGetLastError());
+        MPT_HIP_TRY(hipGetLastError());
     }
     const int64_t n = (int64_t)1 << m;
     {
         LaunchScope ls("rb_unpack", 16.0 * n, s);
         rb::k_rb_unpack<K><<<grid_for(n, 256, 16384), 256, 0, s>>>(m, C);
     }
-    HIP_TRY(hipGetLastError());
+    MPT_HIP_TRY(hipGetLastError());
     return MPT_OK;
 }
 
@@ -1296,12 +1247,12 @@ extern "C" const char *mpt_status_string(int status) {
     }
 }
 
-extern "C" const char *mpt_last_error(void) { return t_last_error.c_str(); }
+extern "C" const char *mpt_last_error(void) { return mptlib::error_text(); }
 
 extern "C" int mpt_build_weights(int m, int64_t n_chunks, int64_t nnz, const int64_t *chunk_w,
                                  const int64_t *req_off, const int32_t *req_chunks, uint32_t *sig,
                                  int64_t *W, void *workspace, size_t workspace_bytes, void *stream) {
-    t_last_error.clear();
+    mptlib::clear_error();
     int rc = check_common(m, n_chunks, nnz);
     if (rc) return rc;
     if (!req_off || !W) return fail(MPT_E_INVALID, "req_off and W must not be NULL");
@@ -1340,13 +1291,13 @@ extern "C" int mpt_build_weights(int m, int64_t n_chunks, int64_t nnz, const int
                                                                       list_sig, list_w, h, W);
     }
     k_check_total<<<1, 64, 0, s>>>(m, W, h);
-    HIP_TRY(hipGetLastError());
+    MPT_HIP_TRY(hipGetLastError());
     return read_errors(h, s);
 }
 
 extern "C" int mpt_solve_exact(int m, const int64_t *W, int64_t *C, uint32_t *split, int64_t *opt_cost,
                                void *workspace, size_t workspace_bytes, void *stream) {
-    t_last_error.clear();
+    mptlib::clear_error();
     int rc = check_common(m, 0, 0);
     if (rc) return rc;
     if (!W || !C || !split) return fail(MPT_E_INVALID, "W, C and split must not be NULL");
@@ -1362,8 +1313,8 @@ extern "C" int mpt_solve_exact(int m, const int64_t *W, int64_t *C, uint32_t *sp
         WsHeader *h = (WsHeader *)ws;
         rb::k_request_total<<<1, 64, 0, s>>>(m, W, h);
         int64_t total = 0;
-        HIP_TRY(hipMemcpyAsync(&total, &h->pad[0], sizeof total, hipMemcpyDeviceToHost, s));
-        HIP_TRY(hipStreamSynchronize(s));
+        MPT_HIP_TRY(hipMemcpyAsync(&total, &h->pad[0], sizeof total, hipMemcpyDeviceToHost, s));
+        MPT_HIP_TRY(hipStreamSynchronize(s));
         // keys below 2^53 are exact doubles; below 2^62 they fit uint64
         if (total < ((int64_t)1 << (61 - m))) {
             uint64_t *part = (uint64_t *)(ws + L.rb_part);
@@ -1374,8 +1325,8 @@ extern "C" int mpt_solve_exact(int m, const int64_t *W, int64_t *C, uint32_t *sp
                                                    : solve_rb<uint64_t>(m, W, C, split, part, s);
             if (rc) return rc;
             if (opt_cost) {
-                HIP_TRY(hipMemcpyAsync(opt_cost, C + (n - 1), sizeof(int64_t), hipMemcpyDeviceToHost, s));
-                HIP_TRY(hipStreamSynchronize(s));
+                MPT_HIP_TRY(hipMemcpyAsync(opt_cost, C + (n - 1), sizeof(int64_t), hipMemcpyDeviceToHost, s));
+                MPT_HIP_TRY(hipStreamSynchronize(s));
             }
             return MPT_OK;
         }
@@ -1402,12 +1353,12 @@ extern "C" int mpt_solve_exact(int m, const int64_t *W, int64_t *C, uint32_t *sp
                                                                  part_a);
             }
         }
-        HIP_TRY(hipGetLastError());
+        MPT_HIP_TRY(hipGetLastError());
     }
-    HIP_TRY(hipGetLastError());
+    MPT_HIP_TRY(hipGetLastError());
     if (opt_cost) {
-        HIP_TRY(hipMemcpyAsync(opt_cost, C + (n - 1), sizeof(int64_t), hipMemcpyDeviceToHost, s));
-        HIP_TRY(hipStreamSynchronize(s));
+        MPT_HIP_TRY(hipMemcpyAsync(opt_cost, C + (n - 1), sizeof(int64_t), hipMemcpyDeviceToHost, s));
+        MPT_HIP_TRY(hipStreamSynchronize(s));
     }
     return MPT_OK;
 }
@@ -1415,7 +1366,7 @@ extern "C" int mpt_solve_exact(int m, const int64_t *W, int64_t *C, uint32_t *sp
 extern "C" int mpt_extract_orders(int m, int64_t n_chunks, int64_t nnz, const int64_t *req_off,
                                   const int32_t *req_chunks, const uint32_t *sig, const uint32_t *split,
                                   int32_t *order_chunks, void *workspace, size_t workspace_bytes, void *stream) {
-    t_last_error.clear();
+    mptlib::clear_error();
     int rc = check_common(m, n_chunks, nnz);
     if (rc) return rc;
     if (!req_off || !split) return fail(MPT_E_INVALID, "req_off and split must not be NULL");
@@ -1433,9 +1384,52 @@ extern "C" int mpt_extract_orders(int m, int64_t n_chunks, int64_t nnz, const in
         k_extract<<<m, 256, 0, s>>>(m, n_chunks, nnz, req_off, req_chunks, sig, split, (uint64_t *)(ws + L.keys),
                                     order_chunks, h);
     }
-    HIP_TRY(hipGetLastError());
+    MPT_HIP_TRY(hipGetLastError());
     return read_errors(h, s);
 }
+
+namespace mptlib {
+
+thread_local std::string t_last_error;
+
+int fail(int status, const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    t_last_error = buf;
+    return status;
+}
+
+void clear_error() { t_last_error.clear(); }
+const char *error_text() { return t_last_error.c_str(); }
+
+// --- event profiler ---------------------------------------------------------
+struct ProfRecord { std::string name; double work; hipEvent_t a, b; };
+struct Profiler {
+    std::mutex mu;
+    bool on = false;
+    std::vector<ProfRecord> recs;
+} g_prof;
+
+LaunchScope::LaunchScope(const char *n, double wk, hipStream_t st) : s_(st), name_(n), work_(wk) {
+    std::lock_guard<std::mutex> g(g_prof.mu);
+    if (!g_prof.on) return;
+    if (hipEventCreate(&a_) != hipSuccess || hipEventCreate(&b_) != hipSuccess) return;
+    active_ = hipEventRecord(a_, s_) == hipSuccess;
+}
+
+LaunchScope::~LaunchScope() {
+    if (!active_) return;
+    std::lock_guard<std::mutex> g(g_prof.mu);
+    if (hipEventRecord(b_, s_) == hipSuccess) g_prof.recs.push_back({name_, work_, a_, b_});
+}
+
+}  // namespace mptlib
+
+using mptlib::g_prof;
+using mptlib::ProfRecord;
 
 extern "C" int mpt_profile_begin(void) {
     std::lock_guard<std::mutex> g(g_prof.mu);

@@ -18,13 +18,16 @@ LIB_PATH = os.path.join(_PKG, "libmpt.so")
 
 MPT_MAX_M = 28
 MPT_COST_SENTINEL = 1 << 62
+MPT_GREEDY_MAX_M = 16384
 
 _STATUS = {
     0: "MPT_OK", -1: "MPT_E_INVALID", -2: "MPT_E_RANGE", -3: "MPT_E_DUP",
     -4: "MPT_E_WEIGHT", -5: "MPT_E_OVERFLOW", -6: "MPT_E_WORKSPACE", -8: "MPT_E_DEVICE",
 }
 EXPORTED = ("mpt_workspace_bytes", "mpt_build_weights", "mpt_solve_exact", "mpt_extract_orders",
-            "mpt_status_string", "mpt_last_error", "mpt_profile_begin", "mpt_profile_end")
+            "mpt_status_string", "mpt_last_error", "mpt_profile_begin", "mpt_profile_end",
+            "mpt_greedy_workspace_bytes", "mpt_pair_weights", "mpt_greedy_hierarchy",
+            "mpt_spanning_tree_bound")
 
 
 class MptError(RuntimeError):
@@ -68,6 +71,14 @@ def load() -> ctypes.CDLL:
     lib.mpt_profile_begin.restype = i32
     lib.mpt_profile_end.argtypes = [ctypes.POINTER(ProfileRow), i32]
     lib.mpt_profile_end.restype = i32
+    lib.mpt_greedy_workspace_bytes.argtypes = [i32, i64, i64]
+    lib.mpt_greedy_workspace_bytes.restype = sz
+    lib.mpt_pair_weights.argtypes = [i32, i64, i64, P, P, P, P, P, P, sz, P]
+    lib.mpt_pair_weights.restype = i32
+    lib.mpt_greedy_hierarchy.argtypes = [i32, i64, i64, P, P, P, P, P, P, P, P, P, P, sz, P]
+    lib.mpt_greedy_hierarchy.restype = i32
+    lib.mpt_spanning_tree_bound.argtypes = [i32, P, P, P, sz, P]
+    lib.mpt_spanning_tree_bound.restype = i32
     _lib = lib
     return lib
 
@@ -164,6 +175,112 @@ def profile_end(max_rows: int = 64) -> dict:
         _check(n, "mpt_profile_end")
     return {rows[i].kernel.decode(): {"launches": rows[i].launches, "total_ms": rows[i].total_ms,
                                       "work": rows[i].work} for i in range(min(n, max_rows))}
+
+
+# --- Sections 6.2-6.3: agglomerative hierarchy and spanning-tree bound ------
+
+def mpt_greedy_workspace_bytes(m: int, n_chunks: int, nnz: int) -> int:
+    return int(load().mpt_greedy_workspace_bytes(m, n_chunks, nnz))
+
+
+def alloc_greedy_workspace(m: int, n_chunks: int, nnz: int, device="cuda") -> torch.Tensor:
+    n = mpt_greedy_workspace_bytes(m, n_chunks, nnz)
+    if n == 0:
+        raise MptError(-1, "mpt_greedy_workspace_bytes", f"invalid m={m}, n_chunks={n_chunks} or nnz={nnz}")
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def mpt_pair_weights(m, n_chunks, chunk_w, req_off, req_chunks, P, workspace, stream=None) -> int:
+    """P[i, j] = w(R_i ∩ R_j) (see include/mpt.h); returns sum_i w(R_i)."""
+    nnz = int(req_chunks.numel()) if req_chunks is not None else 0
+    total = ctypes.c_int64(0)
+    rc = load().mpt_pair_weights(
+        m, n_chunks, nnz,
+        _ptr(chunk_w, torch.int64, n_chunks, "chunk_w"),
+        _ptr(req_off, torch.int64, m + 1, "req_off"),
+        _ptr(req_chunks, torch.int32, nnz, "req_chunks") if nnz else None,
+        _ptr(P, torch.int64, m * m, "P"), ctypes.addressof(total),
+        _ptr(workspace, torch.uint8, 1, "workspace"), workspace.numel(), _stream(stream))
+    _check(rc, "mpt_pair_weights")
+    return int(total.value)
+
+
+def mpt_greedy_hierarchy(m, n_chunks, chunk_w, req_off, req_chunks, merge_a, merge_b, gain, node_parent,
+                         order_chunks, workspace, stream=None, want_savings=True):
+    """Agglomerative hierarchy H_g and (if order_chunks is given) its layout;
+    returns SAV(H_g) or None."""
+    nnz = int(req_chunks.numel()) if req_chunks is not None else 0
+    out = ctypes.c_int64(0)
+    rc = load().mpt_greedy_hierarchy(
+        m, n_chunks, nnz,
+        _ptr(chunk_w, torch.int64, n_chunks, "chunk_w"),
+        _ptr(req_off, torch.int64, m + 1, "req_off"),
+        _ptr(req_chunks, torch.int32, nnz, "req_chunks") if nnz else None,
+        _ptr(merge_a, torch.int32, m - 1, "merge_a"), _ptr(merge_b, torch.int32, m - 1, "merge_b"),
+        _ptr(gain, torch.int64, m - 1, "gain"), _ptr(node_parent, torch.int32, 2 * m - 1, "node_parent"),
+        _ptr(order_chunks, torch.int32, nnz, "order_chunks") if (order_chunks is not None and nnz) else None,
+        ctypes.addressof(out) if want_savings else None,
+        _ptr(workspace, torch.uint8, 1, "workspace"), workspace.numel(), _stream(stream))
+    _check(rc, "mpt_greedy_hierarchy")
+    return int(out.value) if want_savings else None
+
+
+def mpt_spanning_tree_bound(m, P, workspace, stream=None) -> int:
+    """Weight of a maximum spanning tree of the pair weights P."""
+    out = ctypes.c_int64(0)
+    rc = load().mpt_spanning_tree_bound(
+        m, _ptr(P, torch.int64, m * m, "P"), ctypes.addressof(out),
+        _ptr(workspace, torch.uint8, 1, "workspace"), workspace.numel(), _stream(stream))
+    _check(rc, "mpt_spanning_tree_bound")
+    return int(out.value)
+
+
+class Greedy:
+    """Device-resident instance plus the outputs of the Section 6.2-6.3 calls."""
+
+    def __init__(self, inst, device="cuda"):
+        self.m = inst.m
+        self.n_chunks = inst.n_chunks
+        self.nnz = inst.nnz
+        dev = torch.device(device)
+        self.chunk_w = torch.as_tensor(inst.weights, dtype=torch.int64).to(dev)
+        self.req_off = torch.as_tensor(inst.req_off, dtype=torch.int64).to(dev)
+        self.req_chunks = torch.as_tensor(inst.req_chunks, dtype=torch.int32).to(dev)
+        m = self.m
+        self.P = torch.empty(m * m, dtype=torch.int64, device=dev)
+        self.merge_a = torch.empty(max(1, m - 1), dtype=torch.int32, device=dev)
+        self.merge_b = torch.empty(max(1, m - 1), dtype=torch.int32, device=dev)
+        self.gain = torch.empty(max(1, m - 1), dtype=torch.int64, device=dev)
+        self.node_parent = torch.empty(2 * m - 1, dtype=torch.int32, device=dev)
+        self.orders = torch.empty(max(1, self.nnz), dtype=torch.int32, device=dev)
+        self.workspace = alloc_greedy_workspace(m, self.n_chunks, self.nnz, dev)
+
+    def pair_weights(self, stream=None) -> int:
+        return mpt_pair_weights(self.m, self.n_chunks, self.chunk_w, self.req_off, self.req_chunks, self.P,
+                                self.workspace, stream)
+
+    def hierarchy(self, stream=None, with_orders=True) -> int:
+        return mpt_greedy_hierarchy(self.m, self.n_chunks, self.chunk_w, self.req_off, self.req_chunks,
+                                    self.merge_a, self.merge_b, self.gain, self.node_parent,
+                                    self.orders if with_orders else None, self.workspace, stream)
+
+    def spanning_tree(self, stream=None) -> int:
+        return mpt_spanning_tree_bound(self.m, self.P, self.workspace, stream)
+
+    def run(self, stream=None) -> dict:
+        """Pair weights, H_g with its layout, and the spanning-tree bound."""
+        total = self.pair_weights(stream)
+        sav = self.hierarchy(stream)
+        mst = self.spanning_tree(stream)
+        return {"savings": sav, "mst": mst, "request_total": total, "cost": total - sav,
+                "lower_bound": total - mst}
+
+    def host(self) -> dict:
+        m = self.m
+        return {"P": self.P.view(m, m).cpu().numpy(),
+                "merge_a": self.merge_a.cpu().numpy()[:m - 1], "merge_b": self.merge_b.cpu().numpy()[:m - 1],
+                "gain": self.gain.cpu().numpy()[:m - 1], "parent": self.node_parent.cpu().numpy(),
+                "orders": self.orders.cpu().numpy()[:self.nnz]}
 
 
 class Problem:

@@ -222,3 +222,21 @@ def config(idx: int, seed: int | None = None) -> Instance:
     if kind == "loo":
         return gen_loo(**c)
     return gen_retrieval(**c)
+
+
+# Request families for the Section 6.2-6.3 heuristic and bound, far past the
+# exact solver's reach: retrieval traces of thousands of queries with a small
+# top-k over a passage pool a few times larger (the shape of the paper's
+# Section 7 traces, e.g. about 3000 queries, k = 8, a few thousand passages).
+TRACE_CONFIGS = {
+    "trace_512": dict(m=512, u=1536, topics=16, k=8, seed=0),
+    "trace_2048": dict(m=2048, u=6144, topics=64, k=8, seed=0),
+    "trace_4096": dict(m=4096, u=12288, topics=128, k=8, seed=0),
+}
+
+
+def trace_config(name: str, seed: int | None = None) -> Instance:
+    c = dict(TRACE_CONFIGS[name])
+    if seed is not None:
+        c["seed"] = seed
+    return gen_retrieval(**c)

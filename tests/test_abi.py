@@ -97,3 +97,29 @@ def test_oracle_is_not_imported_by_the_product():
                 text = open(os.path.join(dirpath, f)).read()
                 assert "import oracle" not in text and "from oracle" not in text, f
                 assert "mpt_oracle" not in text, f
+
+
+def test_greedy_workspace_and_host_validation(lib):
+    from paper_2609_13692_amd import mpt
+    P = ctypes.c_void_p
+    dummy = P(4096)
+    ws = P(256 * 16)
+    assert mpt.mpt_greedy_workspace_bytes(0, 1, 1) == 0
+    assert mpt.mpt_greedy_workspace_bytes(mpt.MPT_GREEDY_MAX_M + 1, 1, 1) == 0
+    assert mpt.mpt_greedy_workspace_bytes(5, -1, 1) == 0
+    for m, u, nnz in ((1, 0, 0), (100, 1000, 800), (4096, 12288, 32768)):
+        a = mpt.mpt_greedy_workspace_bytes(m, u, nnz)
+        assert a >= 8 * m * m + 8 * nnz and a % 256 == 0
+    # m out of range, NULL outputs, workspace missing / misaligned / small
+    assert lib.mpt_pair_weights(0, 1, 0, dummy, dummy, None, dummy, None, ws, 1 << 30, None) == -1
+    assert lib.mpt_pair_weights(3, 5, 0, dummy, dummy, None, None, None, ws, 1 << 30, None) == -1
+    assert lib.mpt_greedy_hierarchy(4, 5, 3, dummy, dummy, dummy, dummy, dummy, dummy, None, None, None,
+                                    ws, 1 << 30, None) == -1
+    assert lib.mpt_greedy_hierarchy(4, 5, 3, dummy, dummy, dummy, dummy, dummy, dummy, dummy, None, None,
+                                    None, 1 << 30, None) == -6
+    assert lib.mpt_greedy_hierarchy(4, 5, 3, dummy, dummy, dummy, dummy, dummy, dummy, dummy, None, None,
+                                    ws, 64, None) == -6
+    assert b"needs" in lib.mpt_last_error()
+    assert lib.mpt_spanning_tree_bound(mpt.MPT_GREEDY_MAX_M + 1, dummy, dummy, ws, 1 << 20, None) == -1
+    assert lib.mpt_spanning_tree_bound(4, dummy, dummy, P(256 * 16 + 8), 1 << 20, None) == -6
+    assert lib.mpt_spanning_tree_bound(4, None, dummy, ws, 1 << 20, None) == -1
