@@ -12,7 +12,8 @@ seed 0. The DP evaluates T = (3^m + 1)/2 - 2^m unordered bipartitions.
 Prints ONE JSON line. `value` = evaluated bipartitions per second over whole
 steps. `roofline` describes the dominant kernel (the DP cross-pair kernel)
 against the VALU instruction peak; `zeta` the W-table kernel against HBM bandwidth;
-`cpu_baseline` the CPU oracle on a bounded sample of the same workload.
+`cpu_baseline` the CPU oracle on a bounded sample of the same workload;
+`greedy` the Section 6.2-6.3 heuristic and bound at m = 4096 requests.
 """
 from __future__ import annotations
 
@@ -109,6 +110,52 @@ def cpu_baseline(inst, budget_s: float) -> dict:
     }
 
 
+GREEDY_WORKLOAD = "trace_4096"
+
+
+def greedy_bench(steps: int, warmup: int, cpu: bool) -> dict:
+    """Sections 6.2-6.3 at thousands of requests: pair weights, the
+    agglomerative hierarchy H_g with its layout, and the spanning-tree bound,
+    on a trace-shaped instance (m = 4096 queries, top-8 over 12288 passages in
+    128 topics), inputs resident in HBM. One step = the three calls."""
+    import torch
+    from paper_2609_13692_amd import mpt
+    from paper_2609_13692_amd import workloads as wl
+
+    inst = wl.trace_config(GREEDY_WORKLOAD)
+    g = mpt.Greedy(inst)
+    for _ in range(warmup):
+        res = g.run()
+    torch.cuda.synchronize()
+    mpt.profile_begin()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        res = g.run()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    prof = mpt.profile_end()
+    ms = (t1 - t0) * 1000.0 / steps
+    out = {
+        "workload": f"{GREEDY_WORKLOAD}: m={inst.m} requests, u={inst.n_chunks}, nnz={inst.nnz}, seed 0",
+        "instance_sha256": inst.sha256()[:16],
+        "ms_per_step": round(ms, 3),
+        "merges_per_s": (inst.m - 1) / (ms / 1000.0),
+        "savings": res["savings"], "cost": res["cost"], "lower_bound": res["lower_bound"],
+        "kernels": {k: {"launches": v["launches"] // steps, "ms_per_step": round(v["total_ms"] / steps, 4)}
+                    for k, v in prof.items() if k.startswith("g_")},
+    }
+    if cpu:
+        import oracle
+        t0 = time.perf_counter()
+        ref = oracle.greedy_solve(inst)
+        t1 = time.perf_counter()
+        out["parity_matches_oracle"] = (ref["savings"] == res["savings"] and ref["mst"] == res["mst"])
+        out["cpu_baseline"] = {"value": t1 - t0, "unit": "s per step", "cores": len(os.sched_getaffinity(0)),
+                               "kind": "oracle", "sample": "the whole instance (pair weights, H_g, layout, "
+                               "spanning tree), OpenMP"}
+    return out
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -117,6 +164,7 @@ def main() -> int:
     ap.add_argument("--config", type=int, default=5, choices=sorted(WORKLOADS))
     ap.add_argument("--cpu-budget", type=float, default=25.0, help="seconds for the CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-greedy", action="store_true", help="skip the Section 6.2-6.3 measurement")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB before the timed steps "
                          "(a known-size kernel that scales rocprofv3 FETCH_SIZE/WRITE_SIZE)")
@@ -217,6 +265,8 @@ def main() -> int:
                      "ops_per_launch": d["work"] * DP_OPS_PER_PAIR / d["launches"]},
         "zeta": zeta,
     }
+    if not args.no_greedy:
+        line["greedy"] = greedy_bench(max(1, args.steps), max(1, args.warmup), not args.no_cpu_baseline)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(inst, args.cpu_budget)
     print(json.dumps(line), flush=True)

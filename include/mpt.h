@@ -180,7 +180,9 @@ int mpt_greedy_hierarchy(int m, int64_t n_chunks, int64_t nnz, const int64_t *ch
  *     OPT_free >= sum_i P[i][i] - MST.
  *   P            [m*m] int64 pair weights, device
  *   mst_weight   HOST out: weight of a maximum spanning tree
- * Uses the first 256 bytes of the workspace; synchronises `stream`.
+ * Boruvka rounds over the whole device (ceil(log2 m) of them); uses
+ * 256 + 32 m bytes of the workspace (rounded up per array); synchronises
+ * `stream`.
  */
 int mpt_spanning_tree_bound(int m, const int64_t *P, int64_t *mst_weight,
                             void *workspace, size_t workspace_bytes, void *stream);

@@ -35,7 +35,7 @@ using mptlib::grid_for;
 using mptlib::LaunchScope;
 
 constexpr int kWave = 64;
-constexpr int kLoopThreads = 1024;           // the one workgroup of the merge loop and of Prim
+constexpr int kLoopThreads = 1024;           // the one workgroup of the merge loop
 constexpr int kLoopWaves = kLoopThreads / kWave;
 constexpr int kSortTile = 4096;              // keys sorted in LDS per workgroup
 constexpr int kSortThreads = 1024;
@@ -83,7 +83,7 @@ GLayout g_layout(int m, int64_t n_chunks, int64_t nnz) {
     L.dbuf = take(4 * (size_t)std::max<int64_t>(nnz, 1));
     L.d_off = take(8 * (2 * mm));
     L.d_len = take(4 * (2 * mm));
-    L.key = take(8 * mm);
+    L.key = take(4 * mm);       // signature starts (int32) when they do not fit on chip
     L.total = o;
     return L;
 }
@@ -290,16 +290,19 @@ __global__ void k_g_fill64(int64_t *p, int64_t n, int64_t v) {
 }
 
 // slot e = (chunk x, request a) adds w(x) to P[a][a] and to P[a][b], P[b][a]
-// for every later request b of S_x
+// for every later request b of S_x; one wave per slot, so a long demand
+// list is spread over 64 lanes
 __global__ void k_g_pairs(int m, int64_t nnz, const uint64_t *keys2, const int32_t *dem, const int64_t *dem_off,
                           const int64_t *w, unsigned long long *P) {
-    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < nnz; e += (int64_t)gridDim.x * blockDim.x) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t waves = (int64_t)gridDim.x * blockDim.x / kWave;
+    for (int64_t e = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / kWave; e < nnz; e += waves) {
         const int64_t x = (int64_t)(keys2[e] >> 32);
         const unsigned long long wx = (unsigned long long)w[x];
         const size_t a = (size_t)dem[e];
-        atomicAdd(&P[a * m + a], wx);
+        if (lane == 0) atomicAdd(&P[a * m + a], wx);
         const int64_t end = dem_off[x + 1];
-        for (int64_t f = e + 1; f < end; ++f) {
+        for (int64_t f = e + 1 + lane; f < end; f += kWave) {
             const size_t b = (size_t)dem[f];
             atomicAdd(&P[a * m + b], wx);
             atomicAdd(&P[b * m + a], wx);
@@ -312,7 +315,7 @@ __global__ void k_g_pairs(int m, int64_t nnz, const uint64_t *keys2, const int32
 
 // best partner of every row: max over d != c of V[c][d], ties to the
 // smallest d; one wave per row
-__global__ void k_g_row_best(int m, const int64_t *V, int64_t *best_v, int32_t *best_p, int32_t *active) {
+__global__ void k_g_row_best(int m, const int64_t *V, int64_t *best_v, int32_t *best_p) {
     const int lane = threadIdx.x & (kWave - 1);
     const int64_t row = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / kWave;
     if (row >= m) return;
@@ -321,7 +324,7 @@ __global__ void k_g_row_best(int m, const int64_t *V, int64_t *best_v, int32_t *
     for (int d = lane; d < m; d += kWave)
         if (d != row && better(V[row * m + d], d, v, p)) { v = V[row * m + d]; p = d; }
     wave_best(v, p);
-    if (lane == 0) { best_v[row] = v; best_p[row] = p; active[row] = 1; }
+    if (lane == 0) { best_v[row] = v; best_p[row] = p; }
 }
 
 struct LoopArgs {
@@ -330,12 +333,10 @@ struct LoopArgs {
     const int64_t *req_off;     // start of cluster a's signature
     int32_t *sig;               // signatures, ascending, shrinking in place
     int32_t *sig_len;
-    const int32_t *dem;
-    const int64_t *dem_off;
+    int32_t *sig_at;            // req_off as int32 (workspace copy, used when m > kMetaCap)
     int64_t *V;                 // V[a][c] = w(I(a) ∩ I(c)) for live a, c
     int64_t *best_v;
     int32_t *best_p;
-    int32_t *active;            // 1 while a is the name of a live cluster
     int32_t *node_of;           // tree node of live cluster a
     int32_t *dbuf;              // D(v) = I(v) \ I(parent(v)), packed
     int64_t dcap;               // entries of dbuf (nnz: the D lists never need more)
@@ -347,135 +348,309 @@ struct LoopArgs {
     GHeader *h;
 };
 
+constexpr int kColsPerThread = MPT_GREEDY_MAX_M / kLoopThreads;   // columns (rows) owned by one thread
+constexpr int kScCap = 2048;                                        // I(C) kept in LDS up to this size
+constexpr int kSigCap = 1024;                                       // I(A), I(B) copied to LDS up to this size
+constexpr int kMetaCap = 8192;                                      // signature starts and lengths in LDS up to this m
+constexpr int kCandCap = 2048;                                      // candidate columns listed in LDS per merge
+constexpr int kRescParts = 4;                                       // waves per rescanned row
+constexpr int kRescRows = kLoopWaves / kRescParts;                  // rows rescanned together
+
+__device__ inline uint64_t lanes_below(int lane) { return (1ull << lane) - 1ull; }
+
+// w(I(C) ∩ list) for an ascending list: I(C) and the weights of its
+// chunks in LDS; the list is read 8 entries at a time so that its loads
+// overlap
+__device__ inline int64_t inter_weight_lds(const int32_t *ic, const int64_t *icw, int64_t n_ic, const int32_t *list,
+                                           int64_t n) {
+    int64_t s = 0;
+    constexpr int U = 8;
+    for (int64_t j0 = 0; j0 < n; j0 += U) {
+        int32_t y[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) y[u] = j0 + u < n ? list[j0 + u] : -1;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (y[u] < 0) continue;
+            const int64_t pos = find_sorted(ic, n_ic, y[u]);
+            if (pos >= 0) s += icw[pos];
+        }
+    }
+    return s;
+}
+
+// the same with I(C) in global memory (too long for the LDS copy)
+__device__ inline int64_t inter_weight_global(const int32_t *ic, int64_t n_ic, const int32_t *list, int64_t n,
+                                              const int64_t *w) {
+    int64_t s = 0;
+    for (int64_t j = 0; j < n; ++j) {
+        const int32_t y = list[j];
+        if (find_sorted(ic, n_ic, y) >= 0) s += w[y];
+    }
+    return s;
+}
+
+// Each step: (1) the pair to merge from the threads' cached row bests;
+// (2) candidate columns c, where both V[a][c] and V[b][c] are positive (the
+// new value is at most their minimum); (3) wave 0 intersects the
+// signatures: I(C) = I(A) ∩ I(B) in place and in LDS, D(A), D(B) to the
+// packed lists; (4) the new row and column of a, from intersections at the
+// candidates; (5) rows whose best partner was a or b are rescanned.
 __global__ __launch_bounds__(kLoopThreads) void k_g_merge_loop(LoopArgs A) {
-    extern __shared__ int64_t newv[];            // m entries: values of the new cluster
+    __shared__ uint8_t act[MPT_GREEDY_MAX_M];    // 1 while r names a live cluster
+    __shared__ int32_t sc[kScCap];               // I(C) of the current merge
+    __shared__ int64_t scw[kScCap];              // w(x) of the chunks of I(C)
+    __shared__ int32_t s_in[2 * kSigCap];        // I(A), I(B) while they are intersected
+    __shared__ uint8_t dirty[kLoopThreads];      // a row owned by this thread changed its best
     __shared__ int64_t red_v[kLoopWaves];
     __shared__ int32_t red_i[kLoopWaves];
     __shared__ int scan_w[kLoopWaves];
     __shared__ int64_t cursor;                   // next free slot of dbuf
+    __shared__ int64_t s_kept;                   // |I(C)|
     __shared__ int n_resc;
     __shared__ int32_t resc[kLoopThreads];       // rows to rescan (overflow: rescan all)
     __shared__ int resc_all;
+    __shared__ int64_t part_v[kRescRows][kRescParts];
+    __shared__ int32_t part_p[kRescRows][kRescParts];
+    __shared__ int32_t m_at[kMetaCap];           // signature start of each cluster (m <= kMetaCap)
+    __shared__ int32_t m_len[kMetaCap];          // signature length of each cluster (m <= kMetaCap)
+    __shared__ int32_t cand_list[kCandCap];
+    __shared__ int n_cand;
     const int m = A.m;
     const int tid = threadIdx.x;
+    const int lane = tid & (kWave - 1), wid = tid / kWave;
+    // signature starts and lengths: on chip when they fit (generic pointers
+    // read either)
+    const bool meta_lds = m <= kMetaCap;
+    int32_t *sat = meta_lds ? m_at : A.sig_at;
+    int32_t *slen = meta_lds ? m_len : A.sig_len;
     if (tid == 0) cursor = 0;
     for (int v = tid; v < 2 * m - 1; v += blockDim.x) { A.node_parent[v] = -1; A.d_off[v] = 0; A.d_len[v] = 0; }
-    for (int a = tid; a < m; a += blockDim.x) A.node_of[a] = a;
+    for (int r = tid; r < m; r += blockDim.x) {
+        A.node_of[r] = r;
+        act[r] = 1;
+        const int32_t at = (int32_t)A.req_off[r], len = (int32_t)(A.req_off[r + 1] - A.req_off[r]);
+        if (meta_lds) { m_at[r] = at; m_len[r] = len; } else { A.sig_at[r] = at; }
+    }
+    dirty[tid] = 1;
+    if (tid == 0) n_cand = 0;
     __syncthreads();
+    int64_t cv = -1;                             // best (value, row) over the rows this thread owns
+    int32_t ci = -1;
     int t = 0;
     for (; t + 1 < m; ++t) {
-        // the pair to merge: the best row value, ties to the smallest row;
-        // that row's best partner is larger than the row (a smaller partner
-        // would be a smaller row with the same value)
-        int64_t g = -1;
-        int32_t a = -1;
-        for (int r = tid; r < m; r += blockDim.x)
-            if (A.active[r] && A.best_p[r] >= 0 && better(A.best_v[r], r, g, a)) { g = A.best_v[r]; a = r; }
+        // (1) the best row value, ties to the smallest row; that row's best
+        // partner is larger than the row (a smaller partner would be a
+        // smaller row with the same value)
+        if (dirty[tid]) {
+            cv = -1; ci = -1;
+            for (int r = tid; r < m; r += blockDim.x)
+                if (act[r] && A.best_p[r] >= 0 && better(A.best_v[r], r, cv, ci)) { cv = A.best_v[r]; ci = r; }
+            dirty[tid] = 0;
+        }
+        int64_t g = cv;
+        int32_t a = ci;
         block_best(g, a, red_v, red_i);
         if (a < 0 || g <= 0) break;              // every remaining value is 0
         const int32_t b = A.best_p[a];
-        if (tid == 0) {
-            A.merge_a[t] = a; A.merge_b[t] = b; A.gain[t] = g;
-            if (b <= a) atomicOr(&A.h->err, GERR_INVALID);
+        // (2) candidate columns of this thread, and which old values of a
+        // are not zero (only changed entries are written back)
+        uint32_t cand = 0, nonzero = 0, flag = 0, listed = 0;
+        for (int k = 0; k < kColsPerThread; ++k) {
+            const int c = tid + k * kLoopThreads;
+            if (c >= m) break;
+            if (!act[c] || c == a) continue;
+            const int64_t va = A.V[(size_t)a * m + c];
+            const int64_t vb = A.V[(size_t)b * m + c];
+            const int32_t p = A.best_p[c];
+            if (va != 0) nonzero |= 1u << k;
+            if (c != b && va > 0 && vb > 0) {
+                cand |= 1u << k;
+                const int i = atomicAdd(&n_cand, 1);       // cleared at the end of the previous step
+                if (i < kCandCap) { cand_list[i] = c; listed |= 1u << k; }
+            }
+            if (p == a || p == b) flag |= 1u << k;
         }
-        // D(B) = I(B) \ I(A), then I(A) <- I(A) ∩ I(B) in place with
-        // D(A) = I(A) \ I(B) on the side
-        int32_t *sa = A.sig + A.req_off[a];
-        const int32_t *sb = A.sig + A.req_off[b];
-        const int64_t na = A.sig_len[a], nb = A.sig_len[b];
-        const int node_a = A.node_of[a], node_b = A.node_of[b];
-        int64_t dcur = cursor;
-        if (dcur + na + nb > A.dcap) {                 // cannot happen for a valid run: stop with an error
+        // (3) signatures, by wave 0 alone
+        const int64_t na = slen[a], nb = slen[b];
+        const int64_t dstart = cursor;
+        if (dstart + na + nb > A.dcap) {         // cannot happen for a valid run: stop with an error
             if (tid == 0) atomicOr(&A.h->err, GERR_INVALID);
             return;
         }
-        const int64_t d_b_at = dcur;
-        for (int64_t base = 0; base < nb; base += blockDim.x) {
-            const int64_t e = base + tid;
-            int32_t x = 0;
-            int keep = 0;
-            if (e < nb) { x = sb[e]; keep = find_sorted(sa, na, x) < 0; }
-            int tot;
-            const int off = block_scan(keep, &tot, scan_w);
-            if (keep) A.dbuf[dcur + off] = x;
-            dcur += tot;
-        }
-        const int64_t d_a_at = dcur;
-        int64_t kept = 0;
-        for (int64_t base = 0; base < na; base += blockDim.x) {
-            const int64_t e = base + tid;
-            int32_t x = 0;
-            int in_b = 0;
-            if (e < na) { x = sa[e]; in_b = find_sorted(sb, nb, x) >= 0; }
-            int tot_in;
-            const int off_in = block_scan(in_b, &tot_in, scan_w);
-            const int off_out = (int)(e - base) - off_in;   // position among this round's dropped entries
-            __syncthreads();                                // every read of this round of sa is done
-            if (e < na) {
-                if (in_b) sa[kept + off_in] = x;
-                else A.dbuf[dcur + off_out] = x;
+        if (wid == 0) {
+            int32_t *sa = A.sig + sat[a];
+            const int32_t *sb_g = A.sig + sat[b];
+            // the two signatures in LDS when they fit (searches stay on chip)
+            const bool in_lds = na <= kSigCap && nb <= kSigCap;
+            const int32_t *sa_r = sa, *sb = sb_g;
+            if (in_lds) {
+                for (int64_t e = lane; e < na; e += kWave) s_in[e] = sa[e];
+                for (int64_t e = lane; e < nb; e += kWave) s_in[kSigCap + e] = sb_g[e];
+                sa_r = s_in;
+                sb = s_in + kSigCap;
             }
-            const int64_t round = std::min<int64_t>((int64_t)blockDim.x, na - base);
-            kept += tot_in;
-            dcur += round - tot_in;
-        }
-        const int node_c = m + t;
-        if (tid == 0) {
-            A.d_off[node_b] = d_b_at; A.d_len[node_b] = (int32_t)(d_a_at - d_b_at);
-            A.d_off[node_a] = d_a_at; A.d_len[node_a] = (int32_t)(dcur - d_a_at);
-            A.node_parent[node_a] = node_c;
-            A.node_parent[node_b] = node_c;
-            A.node_of[a] = node_c;
-            A.sig_len[a] = (int32_t)kept;
-            A.active[b] = 0;
-            cursor = dcur;
-            n_resc = 0;
-            resc_all = 0;
-        }
-        for (int c = tid; c < m; c += blockDim.x) newv[c] = 0;
-        __syncthreads();
-        // values of the new cluster: x in I(C) counts for cluster c iff the
-        // name c (its smallest request) holds x and x is in I(c)
-        for (int64_t e = 0; e < kept; ++e) {
-            const int32_t x = sa[e];
-            const int64_t wx = A.w[x];
-            for (int64_t f = A.dem_off[x] + tid; f < A.dem_off[x + 1]; f += blockDim.x) {
-                const int32_t c = A.dem[f];
-                if (c != a && A.active[c] && find_sorted(A.sig + A.req_off[c], A.sig_len[c], x) >= 0)
-                    atomicAdd((unsigned long long *)&newv[c], (unsigned long long)wx);
+            int64_t dcur = dstart;
+            // D(B) = I(B) \ I(A)
+            for (int64_t base = 0; base < nb; base += kWave) {
+                const int64_t e = base + lane;
+                int32_t x = 0;
+                bool keep = false;
+                if (e < nb) { x = sb[e]; keep = find_sorted(sa_r, na, x) < 0; }
+                const uint64_t mk = __ballot(keep);
+                if (keep) A.dbuf[dcur + __popcll(mk & lanes_below(lane))] = x;
+                dcur += __popcll(mk);
+            }
+            const int64_t d_a_at = dcur;
+            // I(C) = I(A) ∩ I(B) over I(A) in place (and to LDS), D(A) = the rest
+            int64_t kept = 0;
+            for (int64_t base = 0; base < na; base += kWave) {
+                const int64_t e = base + lane;
+                int32_t x = 0;
+                bool in_b = false;
+                if (e < na) { x = sa_r[e]; in_b = find_sorted(sb, nb, x) >= 0; }
+                const uint64_t mi = __ballot(in_b);
+                const uint64_t mo = __ballot(e < na && !in_b);
+                if (in_b) {
+                    const int64_t pos = kept + __popcll(mi & lanes_below(lane));
+                    sa[pos] = x;
+                    if (pos < kScCap) { sc[pos] = x; scw[pos] = A.w[x]; }
+                } else if (e < na) {
+                    A.dbuf[dcur + __popcll(mo & lanes_below(lane))] = x;
+                }
+                kept += __popcll(mi);
+                dcur += __popcll(mo);
+            }
+            if (lane == 0) {
+                const int node_a = A.node_of[a], node_b = A.node_of[b], node_c = m + t;
+                A.merge_a[t] = a; A.merge_b[t] = b; A.gain[t] = g;
+                if (b <= a) atomicOr(&A.h->err, GERR_INVALID);
+                A.d_off[node_b] = dstart; A.d_len[node_b] = (int32_t)(d_a_at - dstart);
+                A.d_off[node_a] = d_a_at; A.d_len[node_a] = (int32_t)(dcur - d_a_at);
+                A.node_parent[node_a] = node_c;
+                A.node_parent[node_b] = node_c;
+                A.node_of[a] = node_c;
+                slen[a] = (int32_t)kept;
+                act[b] = 0;
+                dirty[b % kLoopThreads] = 1;
+                dirty[a % kLoopThreads] = 1;
+                cursor = dcur;
+                s_kept = kept;
+                n_resc = 0;
+                resc_all = 0;
             }
         }
         __syncthreads();
+        // (4) the new values of a against every live c: the listed
+        // candidates are shared out evenly, every other column is 0 (or its
+        // owner computes it when the list overflowed)
+        const int64_t kept = s_kept;
+        const bool ic_lds = kept <= kScCap;
         int64_t bv = -1;
         int32_t bp = -1;
-        for (int c = tid; c < m; c += blockDim.x) {
-            if (!A.active[c] || c == a) continue;
-            const int64_t v = newv[c];
+        const int ncl = min(n_cand, kCandCap);
+        for (int i = tid; i < ncl; i += blockDim.x) {
+            const int c = cand_list[i];
+            int64_t v = 0;
+            if (kept > 0) {
+                const int32_t *list = A.sig + sat[c];
+                const int64_t n = slen[c];       // c != a: unchanged by this merge
+                v = ic_lds ? inter_weight_lds(sc, scw, kept, list, n)
+                           : inter_weight_global(A.sig + sat[a], kept, list, n, A.w);
+            }
             A.V[(size_t)a * m + c] = v;
             A.V[(size_t)c * m + a] = v;
             if (better(v, c, bv, bp)) { bv = v; bp = c; }
-            const int32_t p = A.best_p[c];
-            if (p == a || p == b) {
-                const int k = atomicAdd(&n_resc, 1);
-                if (k < kLoopThreads) resc[k] = c; else resc_all = 1;
+        }
+        for (int k = 0; k < kColsPerThread; ++k) {
+            const int c = tid + k * kLoopThreads;
+            if (c >= m) break;
+            if (!act[c] || c == a) continue;
+            if (!((listed >> k) & 1u)) {
+                const bool is_cand = kept > 0 && ((cand >> k) & 1u);
+                int64_t v = 0;
+                if (is_cand) {
+                    const int32_t *list = A.sig + sat[c];
+                    const int64_t n = slen[c];
+                    v = ic_lds ? inter_weight_lds(sc, scw, kept, list, n)
+                               : inter_weight_global(A.sig + sat[a], kept, list, n, A.w);
+                }
+                if (is_cand || ((nonzero >> k) & 1u)) {  // the old value may differ
+                    A.V[(size_t)a * m + c] = v;
+                    A.V[(size_t)c * m + a] = v;
+                }
+                if (better(v, c, bv, bp)) { bv = v; bp = c; }
+            }
+            if ((flag >> k) & 1u) {
+                const int r = atomicAdd(&n_resc, 1);
+                if (r < kLoopThreads) resc[r] = c; else resc_all = 1;
+                dirty[c % kLoopThreads] = 1;
             }
         }
         block_best(bv, bp, red_v, red_i);        // includes a barrier after the V writes
-        if (tid == 0) { A.best_v[a] = bv; A.best_p[a] = bp; }
-        // rows whose best partner was a or b: rescan, one wave per row
-        const int lane = tid & (kWave - 1), wid = tid / kWave;
+        if (tid == 0) { A.best_v[a] = bv; A.best_p[a] = bp; n_cand = 0; }
+        // (5) rows whose best partner was a or b: rescan. Values never grow,
+        // so the row's old best bounds every entry now: scanning in index
+        // order, the first entry at that bound is the answer (largest value,
+        // smallest index) and the scan can stop there. Rows go four at a
+        // time, each split into four quarters of columns, one wave each.
         const int nr = resc_all ? m : n_resc;
-        for (int k = wid; k < nr; k += kLoopWaves) {
-            const int c = resc_all ? k : resc[k];
-            if (!A.active[c] || c == a || (resc_all && A.best_p[c] != a && A.best_p[c] != b)) continue;
-            int64_t v = -1;
-            int32_t p = -1;
-            for (int d = lane; d < m; d += kWave)
-                if (d != c && A.active[d] && better(A.V[(size_t)c * m + d], d, v, p)) { v = A.V[(size_t)c * m + d]; p = d; }
-            wave_best(v, p);
-            if (lane == 0) { A.best_v[c] = v; A.best_p[c] = p; }
+        for (int r0 = 0; r0 < nr; r0 += kRescRows) {
+            const int slot = wid / kRescParts, part = wid % kRescParts;
+            const int k = r0 + slot;
+            int c = -1;
+            if (k < nr) {
+                c = resc_all ? k : resc[k];
+                if (!act[c] || c == a || (resc_all && A.best_p[c] != a && A.best_p[c] != b)) c = -1;
+            }
+            if (c >= 0) {
+                const int64_t ub = A.best_v[c];
+                const int64_t *row = A.V + (size_t)c * m;
+                const int q = (m + kRescParts - 1) / kRescParts;
+                const int lo = part * q, hi = min(m, lo + q);
+                int64_t v = -1;
+                int32_t p = -1;
+                bool hit = false;
+                constexpr int G = 8;             // chunks of 64 columns loaded together
+                for (int base = lo; base < hi && !hit; base += G * kWave) {
+                    int64_t x[G];
+#pragma unroll
+                    for (int j = 0; j < G; ++j) {
+                        const int d = base + j * kWave + lane;
+                        x[j] = (d < hi && d != c && act[d]) ? row[d] : -1;
+                    }
+#pragma unroll
+                    for (int j = 0; j < G; ++j) {
+                        const int d = base + j * kWave + lane;
+                        const uint64_t at_ub = __ballot(x[j] == ub && x[j] >= 0);
+                        if (!hit && at_ub) {
+                            v = ub;
+                            p = base + j * kWave + __ffsll((long long)at_ub) - 1;
+                            hit = true;
+                        }
+                        if (!hit && better(x[j], d, v, p)) { v = x[j]; p = d; }
+                    }
+                }
+                if (!hit) wave_best(v, p);
+                if (lane == 0) { part_v[slot][part] = v; part_p[slot][part] = p; }
+            }
+            __syncthreads();
+            // quarters in index order: the first that holds a best equal to
+            // the bound decides, otherwise the best of the four
+            if (part == 0 && lane == 0 && c >= 0) {
+                const int64_t ub = A.best_v[c];
+                int64_t v = -1;
+                int32_t p = -1;
+                for (int j = 0; j < kRescParts; ++j) {
+                    if (part_p[slot][j] < 0) continue;
+                    if (part_v[slot][j] == ub) { v = ub; p = part_p[slot][j]; break; }
+                    if (better(part_v[slot][j], part_p[slot][j], v, p)) { v = part_v[slot][j]; p = part_p[slot][j]; }
+                }
+                A.best_v[c] = v;
+                A.best_p[c] = p;
+            }
+            __syncthreads();
         }
-        __syncthreads();
     }
     // Every remaining pair shares nothing: the merges take the two smallest
     // live names in turn (n0, n1), (n0, n2), ... with gain 0, and every
@@ -491,8 +666,8 @@ __global__ __launch_bounds__(kLoopThreads) void k_g_merge_loop(LoopArgs A) {
     int done = 0;                                // live names ranked so far
     for (int base = 0; base < m; base += blockDim.x) {
         const int r = base + tid;
-        const int live = r < m && A.active[r];
-        const int len = live ? A.sig_len[r] : 0;
+        const int live = r < m && act[r];
+        const int len = live ? slen[r] : 0;
         int tot, ltot;
         const int rank = done + block_scan(live, &tot, scan_w);
         const int loff = block_scan(len, &ltot, scan_w);
@@ -502,7 +677,7 @@ __global__ __launch_bounds__(kLoopThreads) void k_g_merge_loop(LoopArgs A) {
         }
         if (live) {
             const int node = A.node_of[r];
-            const int32_t *src = A.sig + A.req_off[r];
+            const int32_t *src = A.sig + sat[r];
             for (int e = 0; e < len; ++e) A.dbuf[dcur + loff + e] = src[e];
             A.d_off[node] = dcur + loff;
             A.d_len[node] = len;
@@ -558,34 +733,85 @@ __global__ void k_g_orders(int m, int64_t nnz, const int64_t *req_off, const int
 }
 
 // ---------------------------------------------------------------------------
-// maximum spanning tree (Prim), one workgroup; key[] in LDS
+// maximum spanning tree (Boruvka). Edges are ordered by (weight desc, then
+// the pair (lo, hi) of their endpoints ascending), a strict total order, so
+// every round's chosen edges form a forest plus mutual pairs and no cycle
+// can close. Every round at least halves the number of components; the
+// complete graph keeps an edge between any two, so ceil(log2 m) rounds
+// leave one. The tree's weight does not depend on which order breaks ties.
 
-__global__ __launch_bounds__(kLoopThreads) void k_g_prim(int m, const int64_t *P, unsigned long long *out) {
-    extern __shared__ int64_t key[];             // -1: in the tree
-    __shared__ int64_t red_v[kLoopWaves];
-    __shared__ int32_t red_i[kLoopWaves];
-    const int tid = threadIdx.x;
-    for (int v = tid; v < m; v += blockDim.x) key[v] = v == 0 ? 0 : INT64_MIN;
-    __syncthreads();
-    unsigned long long total = 0;
-    for (int it = 0; it < m; ++it) {
-        int64_t bv = INT64_MIN;
-        int32_t bu = -1;
-        for (int v = tid; v < m; v += blockDim.x)
-            if (key[v] != -1 && (bu < 0 || better(key[v], v, bv, bu))) { bv = key[v]; bu = v; }
-        block_best(bv, bu, red_v, red_i);
-        if (bu < 0) break;
-        total += (unsigned long long)bv;
-        if (tid == 0) key[bu] = -1;
-        __syncthreads();
-        const int64_t *row = P + (size_t)bu * m;
-        for (int v = tid; v < m; v += blockDim.x) {
-            const int64_t k = key[v];
-            if (k != -1 && row[v] > k) key[v] = row[v];
-        }
-        __syncthreads();
+__device__ inline uint32_t edge_id(int u, int v) {
+    const uint32_t lo = (uint32_t)min(u, v), hi = (uint32_t)max(u, v);
+    return (lo << 14) | hi;                      // m <= 2^14
+}
+
+__global__ void k_bv_init(int m, int32_t *comp, unsigned long long *total) {
+    for (int v = blockIdx.x * blockDim.x + threadIdx.x; v < m; v += gridDim.x * blockDim.x) comp[v] = v;
+    if (blockIdx.x == 0 && threadIdx.x == 0) *total = 0;
+}
+
+__global__ void k_bv_reset(int m, int64_t *cw, uint32_t *ce) {
+    for (int v = blockIdx.x * blockDim.x + threadIdx.x; v < m; v += gridDim.x * blockDim.x) { cw[v] = -1; ce[v] = ~0u; }
+}
+
+// best edge of every vertex to another component (one wave per vertex),
+// folded into its component's best weight
+__global__ void k_bv_vertex(int m, const int64_t *P, const int32_t *comp, int64_t *vw, uint32_t *ve, int64_t *cw) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t u = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / kWave;
+    if (u >= m) return;
+    const int32_t cu = comp[u];
+    int64_t bw = -1;
+    uint32_t be = ~0u;
+    for (int v = lane; v < m; v += kWave) {
+        if (comp[v] == cu) continue;
+        const int64_t x = P[u * m + v];
+        const uint32_t e = edge_id((int)u, v);
+        if (x > bw || (x == bw && e < be)) { bw = x; be = e; }
     }
-    if (tid == 0) *out = total;
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1) {
+        const int64_t ow = __shfl_xor(bw, off, kWave);
+        const uint32_t oe = (uint32_t)__shfl_xor((int)be, off, kWave);
+        if (ow > bw || (ow == bw && oe < be)) { bw = ow; be = oe; }
+    }
+    if (lane == 0) {
+        vw[u] = bw; ve[u] = be;
+        if (bw >= 0) atomicMax((long long *)&cw[cu], (long long)bw);
+    }
+}
+
+// among the vertices that reach their component's best weight, the smallest edge
+__global__ void k_bv_edge(int m, const int32_t *comp, const int64_t *vw, const uint32_t *ve, const int64_t *cw,
+                          uint32_t *ce) {
+    for (int u = blockIdx.x * blockDim.x + threadIdx.x; u < m; u += gridDim.x * blockDim.x) {
+        const int32_t cu = comp[u];
+        if (vw[u] >= 0 && vw[u] == cw[cu]) atomicMin(&ce[cu], ve[u]);
+    }
+}
+
+// every component hooks onto the component across its best edge, except
+// the smaller one of a mutual pair; the hooking side adds the edge weight
+__global__ void k_bv_hook(int m, const int32_t *comp, const int64_t *cw, const uint32_t *ce, int32_t *par,
+                          unsigned long long *total) {
+    for (int c = blockIdx.x * blockDim.x + threadIdx.x; c < m; c += gridDim.x * blockDim.x) {
+        par[c] = c;
+        if (comp[c] != c || ce[c] == ~0u) continue;
+        const int lo = (int)(ce[c] >> 14), hi = (int)(ce[c] & 0x3fffu);
+        const int32_t d = comp[lo] == c ? comp[hi] : comp[lo];
+        if (ce[d] == ce[c] && c < d) continue;           // d hooks onto c
+        par[c] = d;
+        atomicAdd(total, (unsigned long long)cw[c]);
+    }
+}
+
+// new component of every vertex: follow the hooks to a root
+__global__ void k_bv_jump(int m, int32_t *comp, const int32_t *par) {
+    for (int v = blockIdx.x * blockDim.x + threadIdx.x; v < m; v += gridDim.x * blockDim.x) {
+        int32_t r = comp[v];
+        for (int guard = 0; par[r] != r && guard < m; ++guard) r = par[r];
+        comp[v] = r;
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -652,7 +878,8 @@ int g_prepare(int m, int64_t n_chunks, int64_t nnz, const int64_t *chunk_w, cons
         LaunchScope ls("g_pairs", 8.0 * (double)mm, s);
         k_g_fill64<<<grid_for(mm, 256, 16384), 256, 0, s>>>(P, mm, 0);
         if (nnz > 0)
-            k_g_pairs<<<grid_for(nnz, 256), 256, 0, s>>>(m, nnz, keys2, dem, dem_off, chunk_w, (unsigned long long *)P);
+            k_g_pairs<<<grid_for(nnz * kWave, 256, 16384), 256, 0, s>>>(m, nnz, keys2, dem, dem_off, chunk_w,
+                                                                         (unsigned long long *)P);
         MPT_HIP_TRY(hipGetLastError());
     }
     return MPT_OK;
@@ -703,12 +930,10 @@ extern "C" int mpt_greedy_hierarchy(int m, int64_t n_chunks, int64_t nnz, const 
     A.req_off = req_off;
     A.sig = (int32_t *)(ws + L.sig);
     A.sig_len = (int32_t *)(ws + L.sig_len);
-    A.dem = (int32_t *)(ws + L.dem);
-    A.dem_off = (int64_t *)(ws + L.dem_off);
+    A.sig_at = (int32_t *)(ws + L.key);
     A.V = V;
     A.best_v = (int64_t *)(ws + L.best_v);
     A.best_p = (int32_t *)(ws + L.best_p);
-    A.active = (int32_t *)(ws + L.active);
     A.node_of = (int32_t *)(ws + L.node_of);
     A.dbuf = (int32_t *)(ws + L.dbuf);
     A.dcap = std::max<int64_t>(nnz, 1);
@@ -721,13 +946,11 @@ extern "C" int mpt_greedy_hierarchy(int m, int64_t n_chunks, int64_t nnz, const 
     A.h = (GHeader *)ws;
     {
         LaunchScope ls("g_row_best", 8.0 * (double)m * m, s);
-        k_g_row_best<<<(m + 3) / 4, 4 * kWave, 0, s>>>(m, V, A.best_v, A.best_p, A.active);
+        k_g_row_best<<<(m + 3) / 4, 4 * kWave, 0, s>>>(m, V, A.best_v, A.best_p);
     }
     {
-        const size_t lds = sizeof(int64_t) * (size_t)m;
-        MPT_HIP_TRY(hipFuncSetAttribute((const void *)k_g_merge_loop, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
         LaunchScope ls("g_merge_loop", (double)(m - 1), s);
-        k_g_merge_loop<<<1, kLoopThreads, lds, s>>>(A);
+        k_g_merge_loop<<<1, kLoopThreads, 0, s>>>(A);
     }
     MPT_HIP_TRY(hipGetLastError());
     if (order_chunks) {
@@ -759,15 +982,29 @@ extern "C" int mpt_spanning_tree_bound(int m, const int64_t *P, int64_t *mst_wei
     if (!P || !mst_weight) return fail(MPT_E_INVALID, "P and mst_weight must not be NULL");
     if (!workspace) return fail(MPT_E_WORKSPACE, "workspace is NULL");
     if (((uintptr_t)workspace & 255u) != 0) return fail(MPT_E_WORKSPACE, "workspace is not 256-byte aligned");
-    if (workspace_bytes < sizeof(GHeader)) return fail(MPT_E_WORKSPACE, "workspace has %zu bytes, needs %zu",
-                                                       workspace_bytes, sizeof(GHeader));
+    // header, then comp, par, vertex-best and component-best arrays
+    const size_t mm = (size_t)m;
+    const size_t off_comp = align256(sizeof(GHeader)), off_par = off_comp + align256(4 * mm),
+                 off_vw = off_par + align256(4 * mm), off_ve = off_vw + align256(8 * mm),
+                 off_cw = off_ve + align256(4 * mm), off_ce = off_cw + align256(8 * mm), need = off_ce + align256(4 * mm);
+    if (workspace_bytes < need) return fail(MPT_E_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, need);
     hipStream_t s = (hipStream_t)stream;
     GHeader *h = (GHeader *)workspace;
-    {
-        const size_t lds = sizeof(int64_t) * (size_t)m;
-        MPT_HIP_TRY(hipFuncSetAttribute((const void *)k_g_prim, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
-        LaunchScope ls("g_prim", 8.0 * (double)m * m, s);
-        k_g_prim<<<1, kLoopThreads, lds, s>>>(m, P, &h->total);
+    char *ws = (char *)workspace;
+    int32_t *comp = (int32_t *)(ws + off_comp), *par = (int32_t *)(ws + off_par);
+    int64_t *vw = (int64_t *)(ws + off_vw), *cw = (int64_t *)(ws + off_cw);
+    uint32_t *ve = (uint32_t *)(ws + off_ve), *ce = (uint32_t *)(ws + off_ce);
+    int rounds = 0;
+    while ((1 << rounds) < m) ++rounds;
+    const int gv = grid_for(m, 256);
+    k_bv_init<<<gv, 256, 0, s>>>(m, comp, &h->total);
+    for (int r = 0; r < rounds; ++r) {
+        LaunchScope ls("g_boruvka", 8.0 * (double)m * m, s);
+        k_bv_reset<<<gv, 256, 0, s>>>(m, cw, ce);
+        k_bv_vertex<<<(m + 3) / 4, 4 * kWave, 0, s>>>(m, P, comp, vw, ve, cw);
+        k_bv_edge<<<gv, 256, 0, s>>>(m, comp, vw, ve, cw, ce);
+        k_bv_hook<<<gv, 256, 0, s>>>(m, comp, cw, ce, par, &h->total);
+        k_bv_jump<<<gv, 256, 0, s>>>(m, comp, par);
     }
     MPT_HIP_TRY(hipGetLastError());
     unsigned long long total = 0;
