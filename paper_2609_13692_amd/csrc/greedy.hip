@@ -456,6 +456,7 @@ __global__ __launch_bounds__(kLoopThreads) void k_g_merge_loop(LoopArgs A) {
         // (2) candidate columns of this thread, and which old values of a
         // are not zero (only changed entries are written back)
         uint32_t cand = 0, nonzero = 0, flag = 0, listed = 0;
+#pragma unroll 1
         for (int k = 0; k < kColsPerThread; ++k) {
             const int c = tid + k * kLoopThreads;
             if (c >= m) break;
@@ -562,6 +563,7 @@ __global__ __launch_bounds__(kLoopThreads) void k_g_merge_loop(LoopArgs A) {
             A.V[(size_t)c * m + a] = v;
             if (better(v, c, bv, bp)) { bv = v; bp = c; }
         }
+#pragma unroll 1
         for (int k = 0; k < kColsPerThread; ++k) {
             const int c = tid + k * kLoopThreads;
             if (c >= m) break;
