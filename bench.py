@@ -51,9 +51,6 @@ def profiled_traffic(label: str):
     import glob
     import hashlib
     import re
-    src = os.path.join(ROOT, "paper_2609_13692_amd", "csrc", "mpt.hip")
-    with open(src, "rb") as f:
-        sha = hashlib.sha256(f.read()).hexdigest()
     for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*.md"))):
         with open(path) as f:
             text = f.read()
@@ -61,8 +58,12 @@ def profiled_traffic(label: str):
         if not m:
             continue
         data = json.loads(m.group(1))
-        if data.get("source_sha256") != sha:
+        src = os.path.join(ROOT, data.get("source_file", "paper_2609_13692_amd/csrc/mpt.hip"))
+        if not os.path.exists(src):
             continue
+        with open(src, "rb") as f:
+            if data.get("source_sha256") != hashlib.sha256(f.read()).hexdigest():
+                continue
         for name, k in data.get("kernels", {}).items():
             if re.search(r"\bk_" + re.escape(label) + r"\b", name):
                 return {"bytes_per_launch": k["traffic_bytes_per_launch"],
