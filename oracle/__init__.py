@@ -9,7 +9,9 @@ the product path.
   exact DP, layout read-off, trie cost and hierarchy cost, written from the
   paper's definitions (Section 2 Eq. 1, Section 3 Thm 1 Eqs. 2-3, Section 3.1);
   pair weights, the agglomerative hierarchy, its layout and savings, and the
-  spanning-tree bound for any m (Sections 6.2-6.3, Theorem 6).
+  spanning-tree bound for any m (Sections 6.2-6.3, Theorem 6); global-order
+  layouts, DFS and windowed schedules, and the LRU-leaf radix cache
+  (Sections 7-8, Theorem 7).
 * :mod:`oracle.brute` (pure Python, tiny inputs only): brute force over
   permutations, over hierarchies and over global orders, vertex cover, and the
   closed forms of Section 5 -- the pins that check the C oracle.
@@ -68,6 +70,12 @@ def _load():
     lib.oracle_tree_savings.restype = i64
     lib.oracle_max_spanning_tree.argtypes = [i32, P]
     lib.oracle_max_spanning_tree.restype = i64
+    lib.oracle_global_order_layout.argtypes = [i32, i64, P, P, P, P]
+    lib.oracle_popularity_rank.argtypes = [i32, i64, P, P, P]
+    lib.oracle_dfs_schedule.argtypes = [i32, P, P, P]
+    lib.oracle_window_schedule.argtypes = [i32, P, P, i64, P]
+    lib.oracle_lru_cache_cost.argtypes = [i32, i64, P, P, P, P, i64]
+    lib.oracle_lru_cache_cost.restype = i64
     _lib = lib
     return lib
 
@@ -257,3 +265,69 @@ def greedy_solve(inst, threads: int = 0) -> dict:
     res["lower_bound"] = total - res["mst"]
     res["P"] = P
     return res
+
+
+# --- Sections 7-8: layouts, schedules and the radix cache -----------------
+
+def global_order_layout(inst, rank: np.ndarray) -> np.ndarray:
+    """Every request sorted by rank[chunk] ascending (a global order)."""
+    lib = _load()
+    w, off, ch = _arrays(inst)
+    r = np.ascontiguousarray(rank, dtype=np.int32)
+    out = np.full(max(1, inst.nnz), -1, dtype=np.int32)
+    _check(lib.oracle_global_order_layout(inst.m, inst.n_chunks, _p(off), _p(ch), _p(r), _p(out)),
+           "global_order_layout")
+    return out[:inst.nnz]
+
+
+def popularity_rank(inst) -> np.ndarray:
+    """rank[x] of the popularity order: demand descending, id ascending."""
+    lib = _load()
+    w, off, ch = _arrays(inst)
+    r = np.empty(max(1, inst.n_chunks), dtype=np.int32)
+    _check(lib.oracle_popularity_rank(inst.m, inst.n_chunks, _p(off), _p(ch), _p(r)), "popularity_rank")
+    return r[:inst.n_chunks]
+
+
+def id_rank(inst) -> np.ndarray:
+    """rank[x] = x: the chunk-id order."""
+    return np.arange(inst.n_chunks, dtype=np.int32)
+
+
+def _seq_arrays(inst, seqs):
+    off = np.ascontiguousarray(inst.req_off, dtype=np.int64)
+    s = np.ascontiguousarray(seqs, dtype=np.int32)
+    if s.size == 0:
+        s = np.zeros(1, dtype=np.int32)
+    return off, s
+
+
+def dfs_schedule(inst, seqs: np.ndarray) -> np.ndarray:
+    """Requests in the DFS order of the layout's trie (Theorem 7)."""
+    lib = _load()
+    off, s = _seq_arrays(inst, seqs)
+    order = np.empty(inst.m, dtype=np.int32)
+    _check(lib.oracle_dfs_schedule(inst.m, _p(off), _p(s), _p(order)), "dfs_schedule")
+    return order
+
+
+def window_schedule(inst, seqs: np.ndarray, window: int) -> np.ndarray:
+    """Arrival order with every window of `window` requests served in DFS
+    order (window <= 0: the whole stream)."""
+    lib = _load()
+    off, s = _seq_arrays(inst, seqs)
+    order = np.empty(inst.m, dtype=np.int32)
+    _check(lib.oracle_window_schedule(inst.m, _p(off), _p(s), int(window), _p(order)), "window_schedule")
+    return order
+
+
+def lru_cache_cost(inst, seqs: np.ndarray, order: np.ndarray, capacity: int) -> int:
+    """Prefill bill of serving the layout in `order` through a radix cache of
+    weight `capacity` with LRU-leaf eviction (Section 8)."""
+    lib = _load()
+    w, _, _ = _arrays(inst)
+    off, s = _seq_arrays(inst, seqs)
+    o = np.ascontiguousarray(order, dtype=np.int32)
+    c = int(lib.oracle_lru_cache_cost(inst.m, inst.n_chunks, _p(w), _p(off), _p(s), _p(o), int(capacity)))
+    _check(c, "lru_cache_cost")
+    return c

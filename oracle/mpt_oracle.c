@@ -22,6 +22,10 @@
  *                    weight, signature = intersection         (Section 6.2)
  *   spanning tree    OPT_free >= sum_i w(R_i) - max spanning tree
  *                    of w(R_i ∩ R_j)                  (Section 6.3, Thm 6)
+ *   global orders    every request sorted by one chunk order (Section 7)
+ *   DFS schedule     requests in lexicographic order of their sequences,
+ *                    whole stream or per arrival window   (Thm 7, Sec. 8.1)
+ *   radix cache      LRU-leaf eviction under a weight capacity (Section 8)
  *
  * Readings where the paper is silent (each one is listed with its reason in
  * the design notes of the repository):
@@ -649,4 +653,179 @@ int64_t oracle_max_spanning_tree(int m, const int64_t *P)
     }
     free(key); free(in);
     return total;
+}
+
+/* ===== Sections 7-8: layouts, schedules and the radix cache ================
+ *
+ * A layout is a CSR of chunk sequences (seq_off[m+1], seqs[nnz]); request i's
+ * sequence is seqs[seq_off[i] .. seq_off[i+1]).
+ */
+
+/* Global-order layout (Section 3.1, global orders; the popularity and id
+ * orders of the Section 7 comparisons): every request is sorted by
+ * rank[chunk] ascending. */
+static const int32_t *g_rank_for_sort;
+static int cmp_by_rank(const void *a, const void *b)
+{
+    int32_t x = g_rank_for_sort[*(const int32_t *)a], y = g_rank_for_sort[*(const int32_t *)b];
+    return (x > y) - (x < y);
+}
+
+int oracle_global_order_layout(int m, int64_t n_chunks, const int64_t *req_off, const int32_t *req_chunks,
+                               const int32_t *rank, int32_t *seqs)
+{
+    if (m < 1 || n_chunks < 0) return OR_E_INVALID;
+    for (int i = 0; i < m; ++i) {
+        for (int64_t j = req_off[i]; j < req_off[i + 1]; ++j) {
+            if (req_chunks[j] < 0 || req_chunks[j] >= n_chunks) return OR_E_RANGE;
+            seqs[j] = req_chunks[j];
+        }
+        g_rank_for_sort = rank;
+        qsort(seqs + req_off[i], (size_t)(req_off[i + 1] - req_off[i]), sizeof(int32_t), cmp_by_rank);
+    }
+    return OR_OK;
+}
+
+/* Popularity order: chunks by the number of requests that hold them,
+ * descending, ties by id ascending; rank[x] = position of x. */
+int oracle_popularity_rank(int m, int64_t n_chunks, const int64_t *req_off, const int32_t *req_chunks, int32_t *rank)
+{
+    if (m < 1 || n_chunks < 0) return OR_E_INVALID;
+    int64_t *cnt = (int64_t *)calloc((size_t)(n_chunks > 0 ? n_chunks : 1), sizeof(int64_t));
+    if (!cnt) return OR_E_NOMEM;
+    for (int64_t j = 0; j < req_off[m]; ++j) {
+        if (req_chunks[j] < 0 || req_chunks[j] >= n_chunks) { free(cnt); return OR_E_RANGE; }
+        cnt[req_chunks[j]]++;
+    }
+    /* counts from high to low, ids ascending inside each count */
+    int64_t maxc = 0;
+    for (int64_t x = 0; x < n_chunks; ++x) if (cnt[x] > maxc) maxc = cnt[x];
+    int64_t pos = 0;
+    for (int64_t c = maxc; c >= 0; --c)
+        for (int64_t x = 0; x < n_chunks; ++x)
+            if (cnt[x] == c) rank[x] = (int32_t)pos++;
+    free(cnt);
+    return OR_OK;
+}
+
+/* The DFS serving order of the layout's trie (Theorem 7): requests sorted
+ * lexicographically by their sequences (a proper prefix first), equal
+ * sequences by request index. */
+static const int64_t *g_seq_off;
+static const int32_t *g_seqs;
+static int cmp_seq(const void *pa, const void *pb)
+{
+    int a = *(const int *)pa, b = *(const int *)pb;
+    int64_t la = g_seq_off[a + 1] - g_seq_off[a], lb = g_seq_off[b + 1] - g_seq_off[b];
+    const int32_t *sa = g_seqs + g_seq_off[a], *sb = g_seqs + g_seq_off[b];
+    for (int64_t j = 0; j < la && j < lb; ++j)
+        if (sa[j] != sb[j]) return sa[j] < sb[j] ? -1 : 1;
+    if (la != lb) return la < lb ? -1 : 1;
+    return (a > b) - (a < b);
+}
+
+int oracle_dfs_schedule(int m, const int64_t *seq_off, const int32_t *seqs, int32_t *order)
+{
+    if (m < 1) return OR_E_INVALID;
+    for (int i = 0; i < m; ++i) order[i] = i;
+    g_seq_off = seq_off; g_seqs = seqs;
+    qsort(order, (size_t)m, sizeof(int32_t), cmp_seq);
+    return OR_OK;
+}
+
+/* Windowed reordering (Section 8.1): the arrival stream 0, 1, ..., m-1 is cut
+ * into consecutive windows of `window` requests and each window is served
+ * in DFS order; window <= 0 means the whole stream. */
+int oracle_window_schedule(int m, const int64_t *seq_off, const int32_t *seqs, int64_t window, int32_t *order)
+{
+    if (m < 1) return OR_E_INVALID;
+    if (window <= 0 || window > m) window = m;
+    g_seq_off = seq_off; g_seqs = seqs;
+    for (int i = 0; i < m; ++i) order[i] = i;
+    for (int64_t s = 0; s < m; s += window) {
+        int64_t n = (s + window <= m) ? window : m - s;
+        qsort(order + s, (size_t)n, sizeof(int32_t), cmp_seq);
+    }
+    return OR_OK;
+}
+
+/*
+ * Radix cache with least-recently-used leaf eviction (Section 8): the
+ * cached nodes of the layout's trie always include their ancestors. Serving
+ * a request touches every node of its root-to-leaf path (all at the serving
+ * time); the nodes not cached are computed, which costs their weight, and
+ * inserted; then, while the cached weight exceeds `capacity`, the cached
+ * leaf used least recently is evicted. The cache starts empty. Returns the
+ * total computed weight (the prefill bill), or a negative status.
+ * The trie is explicit; each eviction scans every node for the LRU leaf.
+ */
+int64_t oracle_lru_cache_cost(int m, int64_t n_chunks, const int64_t *w, const int64_t *seq_off,
+                              const int32_t *seqs, const int32_t *order, int64_t capacity)
+{
+    if (m < 1 || n_chunks < 0 || capacity < 0) return OR_E_INVALID;
+    int64_t total = seq_off[m];
+    int64_t cap = total + 1;
+    int32_t *chunk = (int32_t *)malloc(sizeof(int32_t) * (size_t)cap);
+    int64_t *parent = (int64_t *)malloc(sizeof(int64_t) * (size_t)cap);
+    int64_t *first_child = (int64_t *)malloc(sizeof(int64_t) * (size_t)cap);
+    int64_t *next_sib = (int64_t *)malloc(sizeof(int64_t) * (size_t)cap);
+    unsigned char *cached = (unsigned char *)calloc((size_t)cap, 1);
+    int64_t *last = (int64_t *)malloc(sizeof(int64_t) * (size_t)cap);
+    int64_t *kids_cached = (int64_t *)calloc((size_t)cap, sizeof(int64_t));
+    int64_t *path = (int64_t *)malloc(sizeof(int64_t) * (size_t)cap);
+    int64_t cost = 0;
+    if (!chunk || !parent || !first_child || !next_sib || !cached || !last || !kids_cached || !path) { cost = OR_E_NOMEM; goto done; }
+    /* the trie of all sequences (node 0 = root, never cached, weight 0) */
+    int64_t nodes = 1;
+    chunk[0] = -1; parent[0] = -1; first_child[0] = -1; next_sib[0] = -1;
+    for (int i = 0; i < m; ++i) {
+        int64_t cur = 0;
+        for (int64_t j = seq_off[i]; j < seq_off[i + 1]; ++j) {
+            int32_t x = seqs[j];
+            if (x < 0 || x >= n_chunks) { cost = OR_E_RANGE; goto done; }
+            int64_t c = first_child[cur];
+            while (c >= 0 && chunk[c] != x) c = next_sib[c];
+            if (c < 0) {
+                c = nodes++;
+                chunk[c] = x; parent[c] = cur; first_child[c] = -1;
+                next_sib[c] = first_child[cur]; first_child[cur] = c;
+            }
+            cur = c;
+        }
+    }
+    int64_t used = 0;
+    for (int t = 0; t < m; ++t) {
+        int i = order[t];
+        if (i < 0 || i >= m) { cost = OR_E_INVALID; goto done; }
+        /* the path of request i */
+        int64_t len = 0, cur = 0;
+        for (int64_t j = seq_off[i]; j < seq_off[i + 1]; ++j) {
+            int64_t c = first_child[cur];
+            while (chunk[c] != seqs[j]) c = next_sib[c];
+            path[len++] = c;
+            cur = c;
+        }
+        for (int64_t d = 0; d < len; ++d) {
+            int64_t v = path[d];
+            last[v] = t;
+            if (!cached[v]) {
+                cached[v] = 1;
+                cost += w[chunk[v]];
+                used += w[chunk[v]];
+                if (parent[v] > 0) kids_cached[parent[v]]++;
+            }
+        }
+        while (used > capacity) {
+            int64_t best = -1;
+            for (int64_t v = 1; v < nodes; ++v)
+                if (cached[v] && kids_cached[v] == 0 && (best < 0 || last[v] < last[best])) best = v;
+            if (best < 0) break;
+            cached[best] = 0;
+            used -= w[chunk[best]];
+            if (parent[best] > 0) kids_cached[parent[best]]--;
+        }
+    }
+done:
+    free(chunk); free(parent); free(first_child); free(next_sib); free(cached); free(last); free(kids_cached); free(path);
+    return cost;
 }
