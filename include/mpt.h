@@ -187,6 +187,72 @@ int mpt_greedy_hierarchy(int m, int64_t n_chunks, int64_t nnz, const int64_t *ch
 int mpt_spanning_tree_bound(int m, const int64_t *P, int64_t *mst_weight,
                             void *workspace, size_t workspace_bytes, void *stream);
 
+/*
+ * ---- Sections 7-8: layouts, serving schedules and the radix cache ----
+ *
+ * A layout is a CSR of chunk sequences: seq_off[m+1] (int64, device) and
+ * seqs[nnz] (int32 chunk ids, device), e.g. the order_chunks output of
+ * mpt_extract_orders or mpt_greedy_hierarchy with the request offsets.
+ * Chunk ids must lie in [0, n_chunks); weights as above. The calls share one
+ * workspace of mpt_layout_workspace_bytes(m, n_chunks, nnz, n_configs) bytes
+ * (n_configs = 0 for the first two calls).
+ */
+#define MPT_LAYOUT_MAX_M (1 << 24)
+#define MPT_CACHE_MAX_CONFIGS 256
+#define MPT_ORDER_ID 0          /* chunk id ascending */
+#define MPT_ORDER_POPULARITY 1  /* number of requests holding the chunk descending, id ascending */
+
+size_t mpt_layout_workspace_bytes(int m, int64_t n_chunks, int64_t nnz, int n_configs);
+
+/*
+ * Global-order layout (Section 3.1's global orders; the id and popularity
+ * baselines of Section 7): every request's chunks sorted by one order of the
+ * chunks.
+ *   req_off, req_chunks  the instance (as for mpt_build_weights)
+ *   order_kind           MPT_ORDER_ID or MPT_ORDER_POPULARITY
+ *   seqs [nnz]           out: the layout, CSR with req_off
+ * Synchronises `stream` once to report validation errors.
+ */
+int mpt_global_order_layout(int m, int64_t n_chunks, int64_t nnz, const int64_t *req_off,
+                            const int32_t *req_chunks, int order_kind, int32_t *seqs,
+                            void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Trie cost of a layout (Eq. 1: the total weight of the non-root nodes of
+ * the trie of the m sequences), and the DFS serving order of that trie
+ * (Theorem 7): requests sorted lexicographically by their sequences, a
+ * proper prefix first, equal sequences by request index.
+ *   dfs_order [m]   out, nullable: request ids in DFS order
+ *   trie_cost       HOST out
+ * Synchronises `stream`.
+ */
+int mpt_layout_cost(int m, int64_t n_chunks, int64_t nnz, const int64_t *chunk_w,
+                    const int64_t *seq_off, const int32_t *seqs, int32_t *dfs_order,
+                    int64_t *trie_cost, void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Radix cache (Section 8): serving a request touches every node of its
+ * root-to-leaf path in the layout's trie; the nodes not cached are computed
+ * (their weight is billed) and inserted; then, while the cached weight
+ * exceeds the capacity, the least-recently-used cached leaf is evicted
+ * (cached nodes always include their ancestors). The cache starts empty.
+ * Configuration c serves the requests in arrival order 0 .. m-1 cut into
+ * windows of windows[c] requests, each window in DFS order (Section 8.1;
+ * windows[c] <= 0 or >= m: the whole stream in DFS order, 1: arrival
+ * order), with capacity capacities[c] (weight units; Theorem 7: in DFS
+ * order max_i w(R_i) already bills exactly the trie cost).
+ *   n_configs              1 .. MPT_CACHE_MAX_CONFIGS
+ *   windows, capacities    HOST arrays [n_configs]
+ *   costs                  HOST out [n_configs]: the billed weight
+ *   trie_cost              HOST out, nullable: the unbounded-cache bill
+ * The configurations run concurrently, one wavefront each. Synchronises
+ * `stream`.
+ */
+int mpt_cache_simulate(int m, int64_t n_chunks, int64_t nnz, const int64_t *chunk_w,
+                       const int64_t *seq_off, const int32_t *seqs, int n_configs,
+                       const int64_t *windows, const int64_t *capacities, int64_t *costs,
+                       int64_t *trie_cost, void *workspace, size_t workspace_bytes, void *stream);
+
 /* Static text for a status code. */
 const char *mpt_status_string(int status);
 

@@ -19,6 +19,10 @@ LIB_PATH = os.path.join(_PKG, "libmpt.so")
 MPT_MAX_M = 28
 MPT_COST_SENTINEL = 1 << 62
 MPT_GREEDY_MAX_M = 16384
+MPT_LAYOUT_MAX_M = 1 << 24
+MPT_CACHE_MAX_CONFIGS = 256
+MPT_ORDER_ID = 0
+MPT_ORDER_POPULARITY = 1
 
 _STATUS = {
     0: "MPT_OK", -1: "MPT_E_INVALID", -2: "MPT_E_RANGE", -3: "MPT_E_DUP",
@@ -27,7 +31,8 @@ _STATUS = {
 EXPORTED = ("mpt_workspace_bytes", "mpt_build_weights", "mpt_solve_exact", "mpt_extract_orders",
             "mpt_status_string", "mpt_last_error", "mpt_profile_begin", "mpt_profile_end",
             "mpt_greedy_workspace_bytes", "mpt_pair_weights", "mpt_greedy_hierarchy",
-            "mpt_spanning_tree_bound")
+            "mpt_spanning_tree_bound", "mpt_layout_workspace_bytes", "mpt_global_order_layout",
+            "mpt_layout_cost", "mpt_cache_simulate")
 
 
 class MptError(RuntimeError):
@@ -79,6 +84,14 @@ def load() -> ctypes.CDLL:
     lib.mpt_greedy_hierarchy.restype = i32
     lib.mpt_spanning_tree_bound.argtypes = [i32, P, P, P, sz, P]
     lib.mpt_spanning_tree_bound.restype = i32
+    lib.mpt_layout_workspace_bytes.argtypes = [i32, i64, i64, i32]
+    lib.mpt_layout_workspace_bytes.restype = sz
+    lib.mpt_global_order_layout.argtypes = [i32, i64, i64, P, P, i32, P, P, sz, P]
+    lib.mpt_global_order_layout.restype = i32
+    lib.mpt_layout_cost.argtypes = [i32, i64, i64, P, P, P, P, P, P, sz, P]
+    lib.mpt_layout_cost.restype = i32
+    lib.mpt_cache_simulate.argtypes = [i32, i64, i64, P, P, P, i32, P, P, P, P, P, sz, P]
+    lib.mpt_cache_simulate.restype = i32
     _lib = lib
     return lib
 
@@ -281,6 +294,94 @@ class Greedy:
                 "merge_a": self.merge_a.cpu().numpy()[:m - 1], "merge_b": self.merge_b.cpu().numpy()[:m - 1],
                 "gain": self.gain.cpu().numpy()[:m - 1], "parent": self.node_parent.cpu().numpy(),
                 "orders": self.orders.cpu().numpy()[:self.nnz]}
+
+
+# --- Sections 7-8: layouts, serving schedules and the radix cache ---------
+
+def mpt_layout_workspace_bytes(m: int, n_chunks: int, nnz: int, n_configs: int = 0) -> int:
+    return int(load().mpt_layout_workspace_bytes(m, n_chunks, nnz, n_configs))
+
+
+def alloc_layout_workspace(m, n_chunks, nnz, n_configs=0, device="cuda") -> torch.Tensor:
+    n = mpt_layout_workspace_bytes(m, n_chunks, nnz, n_configs)
+    if n == 0:
+        raise MptError(-1, "mpt_layout_workspace_bytes", f"invalid sizes m={m} n_chunks={n_chunks} nnz={nnz}")
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def mpt_global_order_layout(m, n_chunks, req_off, req_chunks, order_kind, seqs, workspace, stream=None):
+    nnz = int(req_chunks.numel()) if req_chunks is not None else 0
+    rc = load().mpt_global_order_layout(
+        m, n_chunks, nnz, _ptr(req_off, torch.int64, m + 1, "req_off"),
+        _ptr(req_chunks, torch.int32, nnz, "req_chunks") if nnz else None, int(order_kind),
+        _ptr(seqs, torch.int32, nnz, "seqs") if nnz else None,
+        _ptr(workspace, torch.uint8, 1, "workspace"), workspace.numel(), _stream(stream))
+    _check(rc, "mpt_global_order_layout")
+
+
+def mpt_layout_cost(m, n_chunks, chunk_w, seq_off, seqs, dfs_order, workspace, stream=None) -> int:
+    """Trie cost of the layout; the DFS order into dfs_order if given."""
+    nnz = int(seqs.numel()) if seqs is not None else 0
+    out = ctypes.c_int64(0)
+    rc = load().mpt_layout_cost(
+        m, n_chunks, nnz, _ptr(chunk_w, torch.int64, n_chunks, "chunk_w"),
+        _ptr(seq_off, torch.int64, m + 1, "seq_off"), _ptr(seqs, torch.int32, nnz, "seqs") if nnz else None,
+        _ptr(dfs_order, torch.int32, m, "dfs_order") if dfs_order is not None else None,
+        ctypes.addressof(out), _ptr(workspace, torch.uint8, 1, "workspace"), workspace.numel(), _stream(stream))
+    _check(rc, "mpt_layout_cost")
+    return int(out.value)
+
+
+def mpt_cache_simulate(m, n_chunks, chunk_w, seq_off, seqs, windows, capacities, workspace, stream=None):
+    """Billed weight of every (window, capacity) configuration, and the
+    unbounded-cache bill (the trie cost)."""
+    nnz = int(seqs.numel()) if seqs is not None else 0
+    n = len(windows)
+    if len(capacities) != n:
+        raise ValueError("windows and capacities differ in length")
+    win = (ctypes.c_int64 * n)(*[int(x) for x in windows])
+    cap = (ctypes.c_int64 * n)(*[int(x) for x in capacities])
+    out = (ctypes.c_int64 * n)()
+    tc = ctypes.c_int64(0)
+    rc = load().mpt_cache_simulate(
+        m, n_chunks, nnz, _ptr(chunk_w, torch.int64, n_chunks, "chunk_w"),
+        _ptr(seq_off, torch.int64, m + 1, "seq_off"), _ptr(seqs, torch.int32, nnz, "seqs") if nnz else None,
+        n, win, cap, out, ctypes.addressof(tc),
+        _ptr(workspace, torch.uint8, 1, "workspace"), workspace.numel(), _stream(stream))
+    _check(rc, "mpt_cache_simulate")
+    return [int(x) for x in out], int(tc.value)
+
+
+class Layouts:
+    """Device-resident instance for the Section 7-8 calls: global-order
+    layouts, trie costs, DFS orders and radix-cache simulations of any layout
+    of the instance (a layout = int32 sequences, CSR with the request
+    offsets)."""
+
+    def __init__(self, inst, n_configs=0, device="cuda"):
+        self.m, self.n_chunks, self.nnz = inst.m, inst.n_chunks, inst.nnz
+        dev = torch.device(device)
+        self.chunk_w = torch.as_tensor(inst.weights, dtype=torch.int64).to(dev)
+        self.req_off = torch.as_tensor(inst.req_off, dtype=torch.int64).to(dev)
+        self.req_chunks = torch.as_tensor(inst.req_chunks, dtype=torch.int32).to(dev)
+        self.dfs = torch.empty(self.m, dtype=torch.int32, device=dev)
+        self.workspace = alloc_layout_workspace(self.m, self.n_chunks, self.nnz, n_configs, dev)
+
+    def seqs(self, layout) -> torch.Tensor:
+        return torch.as_tensor(layout, dtype=torch.int32).to(self.req_off.device).contiguous()
+
+    def global_order(self, kind, stream=None) -> torch.Tensor:
+        out = torch.empty(max(1, self.nnz), dtype=torch.int32, device=self.req_off.device)
+        mpt_global_order_layout(self.m, self.n_chunks, self.req_off, self.req_chunks, kind, out, self.workspace, stream)
+        return out[:self.nnz]
+
+    def cost(self, seqs, stream=None) -> int:
+        return mpt_layout_cost(self.m, self.n_chunks, self.chunk_w, self.req_off, seqs, self.dfs, self.workspace,
+                               stream)
+
+    def simulate(self, seqs, windows, capacities, stream=None):
+        return mpt_cache_simulate(self.m, self.n_chunks, self.chunk_w, self.req_off, seqs, windows, capacities,
+                                  self.workspace, stream)
 
 
 class Problem:

@@ -123,3 +123,25 @@ def test_greedy_workspace_and_host_validation(lib):
     assert lib.mpt_spanning_tree_bound(mpt.MPT_GREEDY_MAX_M + 1, dummy, dummy, ws, 1 << 20, None) == -1
     assert lib.mpt_spanning_tree_bound(4, dummy, dummy, P(256 * 16 + 8), 1 << 20, None) == -6
     assert lib.mpt_spanning_tree_bound(4, None, dummy, ws, 1 << 20, None) == -1
+
+
+def test_layout_workspace_and_host_validation(lib):
+    from paper_2609_13692_amd import mpt
+    P = ctypes.c_void_p
+    dummy = P(4096)
+    ws = P(256 * 16)
+    assert mpt.mpt_layout_workspace_bytes(0, 1, 1) == 0
+    assert mpt.mpt_layout_workspace_bytes(4, 5, 3, mpt.MPT_CACHE_MAX_CONFIGS + 1) == 0
+    a = mpt.mpt_layout_workspace_bytes(4096, 12288, 32768, 0)
+    b = mpt.mpt_layout_workspace_bytes(4096, 12288, 32768, 30)
+    assert a % 256 == 0 and b > a + 30 * 4 * 32768
+    # bad order kind, NULL outputs, missing workspace, bad configuration count
+    assert lib.mpt_global_order_layout(3, 5, 0, dummy, None, 7, None, ws, 1 << 30, None) == -1
+    assert lib.mpt_layout_cost(3, 5, 4, dummy, dummy, dummy, None, None, ws, 1 << 30, None) == -1
+    assert lib.mpt_layout_cost(3, 5, 4, dummy, dummy, dummy, None, dummy, None, 1 << 30, None) == -6
+    win = (ctypes.c_int64 * 1)(1)
+    cap = (ctypes.c_int64 * 1)(-5)
+    out = (ctypes.c_int64 * 1)()
+    assert lib.mpt_cache_simulate(3, 5, 4, dummy, dummy, dummy, 0, win, cap, out, None, ws, 1 << 30, None) == -1
+    assert lib.mpt_cache_simulate(3, 5, 4, dummy, dummy, dummy, 1, win, cap, out, None, ws, 1 << 30, None) == -1
+    assert b"negative" in lib.mpt_last_error()

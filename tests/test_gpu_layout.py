@@ -1,0 +1,161 @@
+"""GPU parity of the Section 7-8 calls (global-order layouts, trie cost and
+DFS order, radix-cache simulation) through the C ABI against the CPU
+oracle. Integer work: layouts, orders and billed weights are compared
+exactly.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_13692_amd import mpt
+from paper_2609_13692_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    mpt.load()
+    yield
+
+
+def say(msg):
+    print(msg, flush=True)
+
+
+def max_request(inst):
+    w = inst.weights
+    return max(int(w[np.asarray(r, dtype=np.int64)].sum()) if r else 0 for r in inst.requests())
+
+
+def test_global_orders_match_oracle():
+    for inst in (wl.config(1), wl.gen_loo(9), wl.random_small(m=40, u=70, kmin=0, kmax=12, wmax=9, seed=3),
+                 wl.trace_config("trace_512"), wl.trace_config("trace_4096")):
+        say(f"[gpu layout] global orders {inst.name} m={inst.m}")
+        L = mpt.Layouts(inst)
+        for kind, rank in ((mpt.MPT_ORDER_ID, oracle.id_rank(inst)), (mpt.MPT_ORDER_POPULARITY, oracle.popularity_rank(inst))):
+            got = L.global_order(kind).cpu().numpy()
+            assert np.array_equal(got, oracle.global_order_layout(inst, rank)), kind
+
+
+def layouts(inst):
+    out = {"relevance": np.asarray(inst.req_chunks, dtype=np.int32),
+           "popularity": oracle.global_order_layout(inst, oracle.popularity_rank(inst)),
+           "greedy": oracle.greedy_solve(inst)["orders"]}
+    rng = np.random.default_rng(inst.m + 1)
+    rnd = np.asarray(inst.req_chunks, dtype=np.int32).copy()
+    for i in range(inst.m):
+        a, b = inst.req_off[i], inst.req_off[i + 1]
+        rnd[a:b] = rng.permutation(rnd[a:b])
+    out["random"] = rnd
+    return out
+
+
+@pytest.mark.parametrize("name", ["small", "trace_512", "trace_2048"])
+def test_trie_cost_and_dfs_order(name):
+    inst = wl.random_small(m=30, u=25, kmin=0, kmax=8, wmax=50, seed=5) if name == "small" else wl.trace_config(name)
+    L = mpt.Layouts(inst)
+    for lname, lay in layouts(inst).items():
+        say(f"[gpu layout] cost {inst.name} {lname}")
+        got = L.cost(L.seqs(lay))
+        assert got == oracle.trie_cost(inst, lay), lname
+        assert np.array_equal(L.dfs.cpu().numpy(), oracle.dfs_schedule(inst, lay)), lname
+
+
+def cache_grid(inst):
+    mx = max(1, max_request(inst))
+    windows, caps = [], []
+    for W in (1, 3, 16, 128, 0):
+        for f in (0.0, 0.5, 1.0, 4.0, 64.0):
+            windows.append(W)
+            caps.append(int(f * mx))
+    return windows, caps
+
+
+@pytest.mark.parametrize("name", ["small", "trace_512"])
+def test_cache_simulation_matches_oracle(name):
+    inst = wl.random_small(m=25, u=20, kmin=0, kmax=7, wmax=20, seed=9) if name == "small" else wl.trace_config(name)
+    windows, caps = cache_grid(inst)
+    L = mpt.Layouts(inst, n_configs=len(windows))
+    for lname, lay in layouts(inst).items():
+        say(f"[gpu cache] {inst.name} {lname} {len(windows)} configurations")
+        got, tc = L.simulate(L.seqs(lay), windows, caps)
+        assert tc == oracle.trie_cost(inst, lay)
+        for W, C, g in zip(windows, caps, got):
+            assert g == oracle.lru_cache_cost(inst, lay, oracle.window_schedule(inst, lay, W), C), (lname, W, C)
+
+
+def test_theorem7_on_gpu():
+    """Theorem 7: in DFS order, one request's worth of capacity bills exactly
+    the trie cost, for every layout; arrival order at that capacity does not."""
+    inst = wl.trace_config("trace_2048")
+    mx = max_request(inst)
+    L = mpt.Layouts(inst, n_configs=4)
+    for lname, lay in layouts(inst).items():
+        say(f"[gpu cache] theorem 7 {inst.name} {lname}")
+        got, tc = L.simulate(L.seqs(lay), [0, 0, 0, 1], [mx, 2 * mx, 1 << 60, mx])
+        assert got[0] == got[1] == got[2] == tc, lname
+        assert got[3] >= tc
+
+
+def test_trace_4096_sampled_configurations():
+    """The benchmark family at m = 4096: the greedy layout's bill for a few
+    configurations against the oracle, and the whole grid's invariants
+    (non-increasing in capacity, at least the trie cost, at most the sum of
+    the request weights)."""
+    inst = wl.trace_config("trace_4096")
+    lay = oracle.greedy_solve(inst)["orders"]
+    mx = max_request(inst)
+    total = int(sum(int(inst.weights[np.asarray(r, dtype=np.int64)].sum()) for r in inst.requests()))
+    windows, caps = [], []
+    for W in (1, 128, 512, 2048, 0):
+        for f in (1, 4, 16, 64, 256, 1024):
+            windows.append(W)
+            caps.append(f * mx)
+    L = mpt.Layouts(inst, n_configs=len(windows))
+    got, tc = L.simulate(L.seqs(lay), windows, caps)
+    g = np.array(got).reshape(5, 6)
+    assert np.all(g[:, :-1] >= g[:, 1:]) and np.all(g >= tc) and np.all(g <= total)
+    assert np.all(g[4] == tc)                                   # whole-stream DFS order: Theorem 7
+    for r, c in ((0, 0), (1, 2), (3, 0)):
+        W, C = windows[r * 6 + c], caps[r * 6 + c]
+        assert g[r, c] == oracle.lru_cache_cost(inst, lay, oracle.window_schedule(inst, lay, W), C)
+
+
+def test_degenerate_inputs():
+    cases = [
+        wl.from_sets([[5, 2, 9]], [1] * 10, 10),
+        wl.from_sets([[], []], [], 0),
+        wl.from_sets([[1, 0], [0, 1], [1, 0]], [4, 7], 2),
+        wl.from_sets([[], [3], [], [1, 2]], [1] * 4, 4),
+        wl.from_sets([[0]] * 40, [1 << 32], 1),
+    ]
+    for inst in cases:
+        L = mpt.Layouts(inst, n_configs=3)
+        lay = np.asarray(inst.req_chunks, dtype=np.int32)
+        seqs = L.seqs(lay)
+        assert L.cost(seqs) == oracle.trie_cost(inst, lay)
+        mx = max_request(inst)
+        got, tc = L.simulate(seqs, [1, 0, 2], [0, mx, 1])
+        for W, C, gv in zip([1, 0, 2], [0, mx, 1], got):
+            assert gv == oracle.lru_cache_cost(inst, lay, oracle.window_schedule(inst, lay, W), C)
+
+
+def test_error_codes():
+    inst = wl.from_sets([[0, 1], [1, 2]], [1, 1, 1], 3)
+    L = mpt.Layouts(inst, n_configs=1)
+    bad = L.seqs(np.array([0, 7, 1, 2], dtype=np.int32))
+    with pytest.raises(mpt.MptError) as e:
+        L.cost(bad)
+    assert e.value.status == -2
+    with pytest.raises(mpt.MptError) as e:
+        L.simulate(L.seqs(inst.req_chunks), [1], [-1])
+    assert e.value.status == -1
+    L.chunk_w[1] = 0
+    with pytest.raises(mpt.MptError) as e:
+        L.cost(L.seqs(inst.req_chunks))
+    assert e.value.status == -4
+    L.chunk_w[1] = 1
+    assert L.cost(L.seqs(inst.req_chunks)) == 4
