@@ -13,7 +13,8 @@ Prints ONE JSON line. `value` = evaluated bipartitions per second over whole
 steps. `roofline` describes the dominant kernel (the DP cross-pair kernel)
 against the VALU instruction peak; `zeta` the W-table kernel against HBM bandwidth;
 `cpu_baseline` the CPU oracle on a bounded sample of the same workload;
-`greedy` the Section 6.2-6.3 heuristic and bound at m = 4096 requests.
+`greedy` the Section 6.2-6.3 heuristic and bound at m = 4096 requests;
+`cache` the Section 7-8 layouts and radix-cache grid on the same instance.
 """
 from __future__ import annotations
 
@@ -157,6 +158,76 @@ def greedy_bench(steps: int, warmup: int, cpu: bool) -> dict:
     return out
 
 
+CACHE_WINDOWS = (1, 128, 512, 2048, 0)          # 0: the whole stream
+CACHE_CAPACITIES = (1, 4, 16, 64, 256, 1024)     # multiples of max_i w(R_i)
+
+
+def cache_bench(steps: int, warmup: int, cpu: bool) -> dict:
+    """Sections 7-8 on the same trace-shaped instance: trie costs of the
+    greedy, popularity, chunk-id and relevance (input order) layouts, and the
+    radix cache under every (reorder window, capacity) pair of the Section 8.1
+    grid for the greedy layout. One step = the two global-order layouts, four
+    trie costs and one batched simulation of the 30 configurations."""
+    import numpy as np
+    import torch
+    from paper_2609_13692_amd import mpt
+    from paper_2609_13692_amd import workloads as wl
+
+    inst = wl.trace_config(GREEDY_WORKLOAD)
+    g = mpt.Greedy(inst)
+    g.run()
+    greedy_layout = g.orders[:inst.nnz].clone()
+    w = inst.weights
+    mx = max(int(w[np.asarray(r, dtype=np.int64)].sum()) for r in inst.requests())
+    windows = [W for W in CACHE_WINDOWS for _ in CACHE_CAPACITIES]
+    caps = [c * mx for _ in CACHE_WINDOWS for c in CACHE_CAPACITIES]
+    L = mpt.Layouts(inst, n_configs=len(windows))
+    relevance = L.req_chunks
+
+    def step():
+        pop = L.global_order(mpt.MPT_ORDER_POPULARITY)
+        ids = L.global_order(mpt.MPT_ORDER_ID)
+        costs = {"greedy": L.cost(greedy_layout), "popularity": L.cost(pop), "chunk_id": L.cost(ids),
+                 "relevance": L.cost(relevance)}
+        sims, tc = L.simulate(greedy_layout, windows, caps)
+        return costs, sims, tc
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    mpt.profile_begin()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        costs, sims, tc = step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    prof = mpt.profile_end()
+    ms = (t1 - t0) * 1000.0 / steps
+    excess = {f"W={W or 'all'}": [round(sims[i * len(CACHE_CAPACITIES) + j] / tc - 1.0, 4)
+                                   for j in range(len(CACHE_CAPACITIES))]
+              for i, W in enumerate(CACHE_WINDOWS)}
+    out = {
+        "workload": f"{GREEDY_WORKLOAD}, greedy layout; capacities x max_i w(R_i) = {mx}: {list(CACHE_CAPACITIES)}",
+        "ms_per_step": round(ms, 3),
+        "trie_costs": costs,
+        "unbounded_cache_cost": tc,
+        "excess_over_unbounded": excess,
+        "kernels": {k: {"launches": v["launches"] // steps, "ms_per_step": round(v["total_ms"] / steps, 4)}
+                    for k, v in prof.items() if k.startswith("l_")},
+    }
+    if cpu:
+        import oracle
+        lay = greedy_layout.cpu().numpy()
+        t0 = time.perf_counter()
+        ref = [oracle.lru_cache_cost(inst, lay, oracle.window_schedule(inst, lay, W), C) for W, C in zip(windows, caps)]
+        t1 = time.perf_counter()
+        out["parity_matches_oracle"] = ref == sims
+        out["cpu_baseline"] = {"value": t1 - t0, "unit": "s for the 30 simulations", "cores": 1, "kind": "oracle",
+                               "sample": "the whole grid on the greedy layout, one thread (explicit trie, LRU leaf "
+                                         "found by a scan)"}
+    return out
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -268,6 +339,7 @@ def main() -> int:
     }
     if not args.no_greedy:
         line["greedy"] = greedy_bench(max(1, args.steps), max(1, args.warmup), not args.no_cpu_baseline)
+        line["cache"] = cache_bench(max(1, args.steps), max(1, args.warmup), not args.no_cpu_baseline)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(inst, args.cpu_budget)
     print(json.dumps(line), flush=True)
