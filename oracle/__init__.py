@@ -11,7 +11,8 @@ the product path.
   pair weights, the agglomerative hierarchy, its layout and savings, and the
   spanning-tree bound for any m (Sections 6.2-6.3, Theorem 6); global-order
   layouts, DFS and windowed schedules, and the LRU-leaf radix cache
-  (Sections 7-8, Theorem 7).
+  (Sections 7-8, Theorem 7); the pinned variant (Section 7.1) as a
+  composition of those, in Python.
 * :mod:`oracle.brute` (pure Python, tiny inputs only): brute force over
   permutations, over hierarchies and over global orders, vertex cover, and the
   closed forms of Section 5 -- the pins that check the C oracle.
@@ -331,3 +332,50 @@ def lru_cache_cost(inst, seqs: np.ndarray, order: np.ndarray, capacity: int) -> 
     c = int(lib.oracle_lru_cache_cost(inst.m, inst.n_chunks, _p(w), _p(off), _p(s), _p(o), int(capacity)))
     _check(c, "lru_cache_cost")
     return c
+
+
+# --- Section 7.1: the pinned variant ----------------------------------------
+
+def pinned_split(inst, t: int):
+    """Every request's top-t chunks in relevance (input) order are pinned at
+    the end, most relevant last; the rest is free. Returns the distinct free
+    sets (ascending lists, in order of their first request), each request's
+    distinct-set index, and the pinned suffixes."""
+    t = max(0, int(t))
+    reqs = inst.requests()
+    index = {}
+    sets = []
+    dmap = []
+    suffix = []
+    for r in reqs:
+        tp = min(t, len(r))
+        free = tuple(sorted(r[tp:]))
+        if free not in index:
+            index[free] = len(sets)
+            sets.append(list(free))
+        dmap.append(index[free])
+        suffix.append(list(reversed(r[:tp])))
+    return sets, dmap, suffix
+
+
+def pinned_layout(inst, t: int, method: str = "exact") -> dict:
+    """Section 7.1's constraint: the free parts are laid out by the exact DP
+    (Section 3.1) or the agglomerative greedy (Section 6.2) over the distinct
+    free sets, every request takes its set's free sequence and appends its
+    pinned suffix. Returns the layout (CSR with the request offsets) and its
+    trie cost (Eq. 1)."""
+    from paper_2609_13692_amd import workloads as wl
+    sets, dmap, suffix = pinned_split(inst, t)
+    sub = wl.from_sets(sets, inst.weights, inst.n_chunks)
+    if method == "exact":
+        lay = solve(sub)["orders"]
+    elif method == "greedy":
+        lay = tree_orders(sub, greedy(sub)["parent"])
+    else:
+        raise ValueError(method)
+    free_seq = [lay[sub.req_off[d]:sub.req_off[d + 1]].tolist() for d in range(sub.m)]
+    out = []
+    for i in range(inst.m):
+        out += free_seq[dmap[i]] + suffix[i]
+    seqs = np.asarray(out, dtype=np.int32)
+    return {"orders": seqs, "cost": trie_cost(inst, seqs), "n_distinct": sub.m, "dmap": np.asarray(dmap)}
