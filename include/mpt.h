@@ -253,6 +253,46 @@ int mpt_cache_simulate(int m, int64_t n_chunks, int64_t nnz, const int64_t *chun
                        const int64_t *windows, const int64_t *capacities, int64_t *costs,
                        int64_t *trie_cost, void *workspace, size_t workspace_bytes, void *stream);
 
+/*
+ * ---- Section 7.1: the quality-preserving pinned variant ----
+ *
+ * The first t chunks of every request in its input (relevance) order are
+ * pinned at the end of its sequence, most relevant last; the rest (the free
+ * part) is permuted. The construction: the distinct free sets are laid out
+ * by the exact DP (mpt_build_weights, mpt_solve_exact, mpt_extract_orders)
+ * or the greedy (mpt_greedy_hierarchy), every request takes its set's free
+ * sequence, then its pinned suffix. Requests with equal free sets thereby
+ * share one free sequence, and their suffixes can share trie nodes.
+ */
+size_t mpt_pinned_workspace_bytes(int m, int64_t nnz);
+
+/*
+ * Split into free sets and pinned suffixes.
+ *   t                 pinned chunks per request (0: nothing pinned)
+ *   dmap [m]          out: index of each request's free set among the
+ *                     distinct sets, numbered in order of their first request
+ *   free_off [m+1]    out: CSR offsets of the distinct free sets (the first
+ *                     n_distinct + 1 entries are written)
+ *   free_chunks [nnz] out: the distinct free sets, each in ascending chunk id
+ *   n_distinct        HOST out: number of distinct free sets (>= 1)
+ * Synchronises `stream`.
+ */
+int mpt_pinned_split(int m, int64_t n_chunks, int64_t nnz, const int64_t *req_off,
+                     const int32_t *req_chunks, int t, int32_t *dmap, int64_t *free_off,
+                     int32_t *free_chunks, int *n_distinct, void *workspace,
+                     size_t workspace_bytes, void *stream);
+
+/*
+ * The layout: seqs[req_off[i] ..) = free sequence of set dmap[i] (from
+ * free_layout, CSR with free_off, e.g. the orders of the exact or greedy
+ * call on the distinct sets) followed by request i's pinned suffix.
+ * Uses the first 256 bytes of the workspace; synchronises `stream`.
+ */
+int mpt_pinned_assemble(int m, int64_t nnz, const int64_t *req_off, const int32_t *req_chunks,
+                        int t, const int32_t *dmap, int n_distinct, const int64_t *free_off,
+                        const int32_t *free_layout, int32_t *seqs, void *workspace,
+                        size_t workspace_bytes, void *stream);
+
 /* Static text for a status code. */
 const char *mpt_status_string(int status);
 

@@ -7,7 +7,7 @@ import sys
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
-SRCS = [os.path.join(PKG, "csrc", f) for f in ("mpt.hip", "greedy.hip", "layout.hip")]
+SRCS = [os.path.join(PKG, "csrc", f) for f in ("mpt.hip", "greedy.hip", "layout.hip", "pinned.hip")]
 LIB = os.path.join(PKG, "libmpt.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

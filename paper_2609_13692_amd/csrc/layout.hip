@@ -33,6 +33,7 @@
 #include "bitonic.h"
 #include "common.h"
 #include "mpt.h"
+#include "seqsort.h"
 
 namespace {
 
@@ -42,10 +43,11 @@ using mptlib::grid_for;
 using mptlib::kSortTile;
 using mptlib::LaunchScope;
 using mptlib::sort_keys;
+using mptlib::kSeqSortTile;
+using mptlib::sort_requests;
 
 constexpr int kWave = 64;
 constexpr int kSimNodesLds = 36 * 1024;       // nodes whose latest access fits the LDS of one workgroup
-constexpr int kSeqSortTile = 1024;            // requests sorted in LDS per workgroup (index keys)
 
 enum : uint32_t { LERR_INVALID = 1u, LERR_RANGE = 2u, LERR_WEIGHT = 8u, LERR_OVERFLOW = 16u };
 
@@ -194,88 +196,6 @@ __global__ void k_l_layout_out(int64_t nnz, const uint64_t *keys, const int32_t 
 __global__ void k_l_inverse(int64_t n, const int32_t *rank, int32_t *inv) {
     for (int64_t x = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; x < n; x += (int64_t)gridDim.x * blockDim.x)
         inv[rank[x]] = (int32_t)x;
-}
-
-// ---------------------------------------------------------------------------
-// lexicographic sort of the requests (bitonic over request indices)
-
-// a < b: sequence order, a proper prefix first, equal sequences by index;
-// index -1 is padding and sorts last
-__device__ inline bool seq_less(int a, int b, const int64_t *off, const int32_t *seqs) {
-    if (b < 0) return a >= 0;
-    if (a < 0) return false;
-    const int64_t la = off[a + 1] - off[a], lb = off[b + 1] - off[b];
-    const int32_t *sa = seqs + off[a], *sb = seqs + off[b];
-    const int64_t n = la < lb ? la : lb;
-    for (int64_t j = 0; j < n; ++j)
-        if (sa[j] != sb[j]) return sa[j] < sb[j];
-    if (la != lb) return la < lb;
-    return a < b;
-}
-
-__global__ void k_l_ord_init(int m, int64_t mpad, int32_t *ord) {
-    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < mpad; i += (int64_t)gridDim.x * blockDim.x)
-        ord[i] = i < m ? (int32_t)i : -1;
-}
-
-// all stages with k <= kSeqSortTile inside one tile of request indices
-__global__ __launch_bounds__(256) void k_l_seq_sort_tile(int32_t *ord, const int64_t *off, const int32_t *seqs) {
-    __shared__ int32_t t[kSeqSortTile];
-    const int64_t base = (int64_t)blockIdx.x * kSeqSortTile;
-    for (int e = threadIdx.x; e < kSeqSortTile; e += blockDim.x) t[e] = ord[base + e];
-    __syncthreads();
-    for (int k = 2; k <= kSeqSortTile; k <<= 1)
-        for (int j = k >> 1; j > 0; j >>= 1) {
-            for (int p = threadIdx.x; p < kSeqSortTile / 2; p += blockDim.x) {
-                const int i = ((p / j) * 2 * j) + (p % j), l = i + j;
-                const bool up = ((base + i) & k) == 0;
-                const int a = t[i], b = t[l];
-                if (seq_less(b, a, off, seqs) == up) { t[i] = b; t[l] = a; }
-            }
-            __syncthreads();
-        }
-    for (int e = threadIdx.x; e < kSeqSortTile; e += blockDim.x) ord[base + e] = t[e];
-}
-
-__global__ void k_l_seq_sort_global(int32_t *ord, int64_t n, int64_t k, int64_t j, const int64_t *off,
-                                    const int32_t *seqs) {
-    for (int64_t p = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; p < n / 2; p += (int64_t)gridDim.x * blockDim.x) {
-        const int64_t i = ((p / j) * 2 * j) + (p % j), l = i + j;
-        const bool up = (i & k) == 0;
-        const int a = ord[i], b = ord[l];
-        if (seq_less(b, a, off, seqs) == up) { ord[i] = b; ord[l] = a; }
-    }
-}
-
-__global__ __launch_bounds__(256) void k_l_seq_sort_tile_merge(int32_t *ord, int64_t k, const int64_t *off,
-                                                               const int32_t *seqs) {
-    __shared__ int32_t t[kSeqSortTile];
-    const int64_t base = (int64_t)blockIdx.x * kSeqSortTile;
-    for (int e = threadIdx.x; e < kSeqSortTile; e += blockDim.x) t[e] = ord[base + e];
-    __syncthreads();
-    const bool up = (base & k) == 0;
-    for (int j = kSeqSortTile >> 1; j > 0; j >>= 1) {
-        for (int p = threadIdx.x; p < kSeqSortTile / 2; p += blockDim.x) {
-            const int i = ((p / j) * 2 * j) + (p % j), l = i + j;
-            const int a = t[i], b = t[l];
-            if (seq_less(b, a, off, seqs) == up) { t[i] = b; t[l] = a; }
-        }
-        __syncthreads();
-    }
-    for (int e = threadIdx.x; e < kSeqSortTile; e += blockDim.x) ord[base + e] = t[e];
-}
-
-int sort_requests(int32_t *ord, int m, int64_t n, const int64_t *off, const int32_t *seqs, hipStream_t s) {
-    const int tiles = (int)(n / kSeqSortTile);
-    k_l_ord_init<<<grid_for(n, 256), 256, 0, s>>>(m, n, ord);
-    k_l_seq_sort_tile<<<tiles, 256, 0, s>>>(ord, off, seqs);
-    for (int64_t k = 2 * kSeqSortTile; k <= n; k <<= 1) {
-        for (int64_t j = k >> 1; j >= kSeqSortTile; j >>= 1)
-            k_l_seq_sort_global<<<grid_for(n / 2, 256, 16384), 256, 0, s>>>(ord, n, k, j, off, seqs);
-        k_l_seq_sort_tile_merge<<<tiles, 256, 0, s>>>(ord, k, off, seqs);
-    }
-    MPT_HIP_TRY(hipGetLastError());
-    return MPT_OK;
 }
 
 // ---------------------------------------------------------------------------

@@ -32,7 +32,8 @@ EXPORTED = ("mpt_workspace_bytes", "mpt_build_weights", "mpt_solve_exact", "mpt_
             "mpt_status_string", "mpt_last_error", "mpt_profile_begin", "mpt_profile_end",
             "mpt_greedy_workspace_bytes", "mpt_pair_weights", "mpt_greedy_hierarchy",
             "mpt_spanning_tree_bound", "mpt_layout_workspace_bytes", "mpt_global_order_layout",
-            "mpt_layout_cost", "mpt_cache_simulate")
+            "mpt_layout_cost", "mpt_cache_simulate", "mpt_pinned_workspace_bytes", "mpt_pinned_split",
+            "mpt_pinned_assemble")
 
 
 class MptError(RuntimeError):
@@ -92,6 +93,12 @@ def load() -> ctypes.CDLL:
     lib.mpt_layout_cost.restype = i32
     lib.mpt_cache_simulate.argtypes = [i32, i64, i64, P, P, P, i32, P, P, P, P, P, sz, P]
     lib.mpt_cache_simulate.restype = i32
+    lib.mpt_pinned_workspace_bytes.argtypes = [i32, i64]
+    lib.mpt_pinned_workspace_bytes.restype = sz
+    lib.mpt_pinned_split.argtypes = [i32, i64, i64, P, P, i32, P, P, P, P, P, sz, P]
+    lib.mpt_pinned_split.restype = i32
+    lib.mpt_pinned_assemble.argtypes = [i32, i64, P, P, i32, P, i32, P, P, P, P, sz, P]
+    lib.mpt_pinned_assemble.restype = i32
     _lib = lib
     return lib
 
@@ -252,6 +259,8 @@ class Greedy:
     """Device-resident instance plus the outputs of the Section 6.2-6.3 calls."""
 
     def __init__(self, inst, device="cuda"):
+        if not 1 <= inst.m <= MPT_GREEDY_MAX_M:
+            raise MptError(-1, "Greedy", f"m = {inst.m} outside [1, {MPT_GREEDY_MAX_M}]")
         self.m = inst.m
         self.n_chunks = inst.n_chunks
         self.nnz = inst.nnz
@@ -384,6 +393,56 @@ class Layouts:
                                   self.workspace, stream)
 
 
+# --- Section 7.1: the pinned variant ---------------------------------------
+
+def pinned_layout(inst, t: int, method: str = "exact", device="cuda", stream=None) -> dict:
+    """Top-t of every request pinned at its end (most relevant last), the
+    free parts laid out by the exact DP or the greedy over the distinct free
+    sets (see include/mpt.h). Returns the layout (device tensor, CSR with the
+    request offsets), its trie cost and the distinct-set count."""
+    from types import SimpleNamespace
+    lib = load()
+    dev = torch.device(device)
+    m, nnz = inst.m, inst.nnz
+    chunk_w = torch.as_tensor(inst.weights, dtype=torch.int64).to(dev)
+    req_off = torch.as_tensor(inst.req_off, dtype=torch.int64).to(dev)
+    req_chunks = torch.as_tensor(inst.req_chunks, dtype=torch.int32).to(dev)
+    nbytes = int(lib.mpt_pinned_workspace_bytes(m, nnz))
+    if nbytes == 0:
+        raise MptError(-1, "mpt_pinned_workspace_bytes", f"invalid m={m} or nnz={nnz}")
+    ws = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    dmap = torch.empty(m, dtype=torch.int32, device=dev)
+    free_off = torch.empty(m + 1, dtype=torch.int64, device=dev)
+    free_chunks = torch.empty(max(1, nnz), dtype=torch.int32, device=dev)
+    nd = ctypes.c_int(0)
+    rc = lib.mpt_pinned_split(m, inst.n_chunks, nnz, req_off.data_ptr(), req_chunks.data_ptr() if nnz else None,
+                              int(t), dmap.data_ptr(), free_off.data_ptr(), free_chunks.data_ptr(),
+                              ctypes.addressof(nd), ws.data_ptr(), ws.numel(), _stream(stream))
+    _check(rc, "mpt_pinned_split")
+    n_d = int(nd.value)
+    nnz_f = int(free_off[n_d].item())
+    sub = SimpleNamespace(m=n_d, n_chunks=inst.n_chunks, nnz=nnz_f, weights=chunk_w,
+                          req_off=free_off[:n_d + 1], req_chunks=free_chunks[:nnz_f])
+    if method == "exact":
+        prob = Problem(sub, device)
+        prob.run(stream)
+        free_layout = prob.orders
+    elif method == "greedy":
+        g = Greedy(sub, device)
+        g.hierarchy(stream)
+        free_layout = g.orders
+    else:
+        raise ValueError(method)
+    seqs = torch.empty(max(1, nnz), dtype=torch.int32, device=dev)
+    rc = lib.mpt_pinned_assemble(m, nnz, req_off.data_ptr(), req_chunks.data_ptr() if nnz else None, int(t),
+                                 dmap.data_ptr(), n_d, free_off.data_ptr(), free_layout.data_ptr(),
+                                 seqs.data_ptr(), ws.data_ptr(), ws.numel(), _stream(stream))
+    _check(rc, "mpt_pinned_assemble")
+    L = Layouts(inst, 0, device)
+    cost = L.cost(seqs[:nnz], stream)
+    return {"orders": seqs[:nnz], "cost": cost, "n_distinct": n_d, "dmap": dmap}
+
+
 class Problem:
     """Device-resident instance plus the output tables of one solve.
 
@@ -392,6 +451,8 @@ class Problem:
     """
 
     def __init__(self, inst, device="cuda"):
+        if not 1 <= inst.m <= MPT_MAX_M:
+            raise MptError(-1, "Problem", f"m = {inst.m} outside [1, {MPT_MAX_M}] (the tables hold 2^m entries)")
         self.m = inst.m
         self.n_chunks = inst.n_chunks
         self.nnz = inst.nnz
