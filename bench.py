@@ -14,7 +14,8 @@ steps. `roofline` describes the dominant kernel (the DP cross-pair kernel)
 against the VALU instruction peak; `zeta` the W-table kernel against HBM bandwidth;
 `cpu_baseline` the CPU oracle on a bounded sample of the same workload;
 `greedy` the Section 6.2-6.3 heuristic and bound at m = 4096 requests;
-`cache` the Section 7-8 layouts and radix-cache grid on the same instance.
+`cache` the Section 7-8 layouts and radix-cache grid on the same instance;
+`pinned` the Section 7.1 pinned variant on it.
 """
 from __future__ import annotations
 
@@ -228,6 +229,35 @@ def cache_bench(steps: int, warmup: int, cpu: bool) -> dict:
     return out
 
 
+def pinned_bench(cpu: bool) -> dict:
+    """Section 7.1 on the same trace-shaped instance: the greedy layout with
+    the top-t of every request pinned at its end (t = 0..3), its trie cost and
+    its saving against relevance (input) order, as in the paper's pinned
+    table."""
+    import torch
+    from paper_2609_13692_amd import mpt
+    from paper_2609_13692_amd import workloads as wl
+
+    inst = wl.trace_config(GREEDY_WORKLOAD)
+    base = mpt.Layouts(inst).cost(torch.as_tensor(inst.req_chunks, dtype=torch.int32).cuda())
+    out = {"workload": f"{GREEDY_WORKLOAD}, free parts by the greedy", "relevance_order_cost": base, "t": {}}
+    for t in (0, 1, 2, 3):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        r = mpt.pinned_layout(inst, t, "greedy")
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) * 1000.0
+        out["t"][str(t)] = {"cost": r["cost"], "saving_vs_relevance": round(1.0 - r["cost"] / base, 4),
+                            "distinct_free_sets": r["n_distinct"], "ms": round(ms, 2)}
+    if cpu:
+        import oracle
+        t0 = time.perf_counter()
+        ref = oracle.pinned_layout(inst, 1, "greedy")["cost"]
+        out["parity_matches_oracle_t1"] = ref == out["t"]["1"]["cost"]
+        out["cpu_baseline_t1_s"] = round(time.perf_counter() - t0, 3)
+    return out
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -340,6 +370,7 @@ def main() -> int:
     if not args.no_greedy:
         line["greedy"] = greedy_bench(max(1, args.steps), max(1, args.warmup), not args.no_cpu_baseline)
         line["cache"] = cache_bench(max(1, args.steps), max(1, args.warmup), not args.no_cpu_baseline)
+        line["pinned"] = pinned_bench(not args.no_cpu_baseline)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(inst, args.cpu_budget)
     print(json.dumps(line), flush=True)
