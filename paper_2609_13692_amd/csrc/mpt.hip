@@ -673,6 +673,40 @@ __device__ inline void load_row(K *P, K *Tt, const uint64_t *__restrict__ C, uin
     }
 }
 
+// rows xa and xb into (Pa, Ta) and (Pb, Tb): every thread's global loads
+// of both rows are issued together, then written to LDS
+template <class K>
+__device__ inline void load_rows2(K *Pa, K *Ta, K *Pb, K *Tb, const uint64_t *__restrict__ C, uint32_t xa,
+                                  uint32_t xb) {
+    constexpr int PER = ROW / 2 / THREADS;           // 16-byte pieces per thread and row
+    static_assert(PER * THREADS == ROW / 2, "threads divide the row");
+    const ulonglong2 *srca = reinterpret_cast<const ulonglong2 *>(C + ((size_t)xa << L));
+    const ulonglong2 *srcb = reinterpret_cast<const ulonglong2 *>(C + ((size_t)xb << L));
+    ulonglong2 va[PER], vb[PER];
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+        va[p] = srca[threadIdx.x + p * THREADS];
+        vb[p] = srcb[threadIdx.x + p * THREADS];
+    }
+    using V = typename Vec2<K>::type;
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+        const int g = threadIdx.x + p * THREADS;
+        const int x2 = g / (NB / 2), q = g % (NB / 2);   // entries 2q, 2q+1 of block x2
+        const uint32_t sl = slot_of((uint32_t)x2);
+        const uint32_t ia = (xa << L) | (uint32_t)(2 * g), ib = (xb << L) | (uint32_t)(2 * g);
+        V t;
+        t.x = Key<K>::load_tagged(va[p].x, ia);
+        t.y = Key<K>::load_tagged(va[p].y, ia + 1u);
+        *reinterpret_cast<V *>(Ta + sl * TSTRIDE + 2 * q) = t;
+        Pa[sl * PSTRIDE + q] = Key<K>::load_plain(va[p].x);
+        t.x = Key<K>::load_tagged(vb[p].x, ib);
+        t.y = Key<K>::load_tagged(vb[p].y, ib + 1u);
+        *reinterpret_cast<V *>(Tb + sl * TSTRIDE + 2 * q) = t;
+        Pb[sl * PSTRIDE + q] = Key<K>::load_plain(vb[p].x);
+    }
+}
+
 // deposit the low bits of t into the set bits of mask (in order)
 __device__ inline uint32_t deposit(uint32_t t, uint32_t mask) {
     uint32_t r = 0;
@@ -885,8 +919,7 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
     for (uint32_t t = t0; t < t1; ++t) {
         const uint32_t bh = sh ^ ah;
         lds_barrier();
-        load_row<K>(s.pa, s.ta, Cp, ah);
-        load_row<K>(s.pb, s.tb, Cp, bh);
+        load_rows2<K>(s.pa, s.ta, s.pb, s.tb, Cp, ah, bh);
         lds_barrier();
         ah = lowh | (((ah | ~rest) + 1u) & rest);    // next A_H holding lowbit(S_H)
         if (has_item) {
