@@ -289,7 +289,7 @@ struct LoopArgs {
 constexpr int kColsPerThread = MPT_GREEDY_MAX_M / kLoopThreads;   // columns (rows) owned by one thread
 constexpr int kScCap = 2048;                                        // I(C) kept in LDS up to this size
 constexpr int kSigCap = 1024;                                       // I(A), I(B) copied to LDS up to this size
-constexpr int kMetaCap = 8192;                                      // signature starts and lengths in LDS up to this m
+constexpr int kMetaCap = 4096;                                      // per-cluster state in LDS up to this m
 constexpr int kCandCap = 2048;                                      // candidate columns listed in LDS per merge
 constexpr int kRescParts = 4;                                       // waves per rescanned row
 constexpr int kRescRows = kLoopWaves / kRescParts;                  // rows rescanned together
@@ -352,6 +352,8 @@ __global__ __launch_bounds__(kLoopThreads) void k_g_merge_loop(LoopArgs A) {
     __shared__ int32_t part_p[kRescRows][kRescParts];
     __shared__ int32_t m_at[kMetaCap];           // signature start of each cluster (m <= kMetaCap)
     __shared__ int32_t m_len[kMetaCap];          // signature length of each cluster (m <= kMetaCap)
+    __shared__ int64_t m_bv[kMetaCap];           // best value of each row (m <= kMetaCap)
+    __shared__ int32_t m_bp[kMetaCap];           // best partner of each row (m <= kMetaCap)
     __shared__ int32_t cand_list[kCandCap];
     __shared__ int n_cand;
     const int m = A.m;
@@ -362,13 +364,16 @@ __global__ __launch_bounds__(kLoopThreads) void k_g_merge_loop(LoopArgs A) {
     const bool meta_lds = m <= kMetaCap;
     int32_t *sat = meta_lds ? m_at : A.sig_at;
     int32_t *slen = meta_lds ? m_len : A.sig_len;
+    int64_t *best_v = meta_lds ? m_bv : A.best_v;
+    int32_t *best_p = meta_lds ? m_bp : A.best_p;
     if (tid == 0) cursor = 0;
     for (int v = tid; v < 2 * m - 1; v += blockDim.x) { A.node_parent[v] = -1; A.d_off[v] = 0; A.d_len[v] = 0; }
     for (int r = tid; r < m; r += blockDim.x) {
         A.node_of[r] = r;
         act[r] = 1;
         const int32_t at = (int32_t)A.req_off[r], len = (int32_t)(A.req_off[r + 1] - A.req_off[r]);
-        if (meta_lds) { m_at[r] = at; m_len[r] = len; } else { A.sig_at[r] = at; }
+        if (meta_lds) { m_at[r] = at; m_len[r] = len; m_bv[r] = A.best_v[r]; m_bp[r] = A.best_p[r]; }
+        else { A.sig_at[r] = at; }
     }
     dirty[tid] = 1;
     if (tid == 0) n_cand = 0;
@@ -383,14 +388,14 @@ __global__ __launch_bounds__(kLoopThreads) void k_g_merge_loop(LoopArgs A) {
         if (dirty[tid]) {
             cv = -1; ci = -1;
             for (int r = tid; r < m; r += blockDim.x)
-                if (act[r] && A.best_p[r] >= 0 && better(A.best_v[r], r, cv, ci)) { cv = A.best_v[r]; ci = r; }
+                if (act[r] && best_p[r] >= 0 && better(best_v[r], r, cv, ci)) { cv = best_v[r]; ci = r; }
             dirty[tid] = 0;
         }
         int64_t g = cv;
         int32_t a = ci;
         block_best(g, a, red_v, red_i);
         if (a < 0 || g <= 0) break;              // every remaining value is 0
-        const int32_t b = A.best_p[a];
+        const int32_t b = best_p[a];
         // (2) candidate columns of this thread, and which old values of a
         // are not zero (only changed entries are written back)
         uint32_t cand = 0, nonzero = 0, flag = 0, listed = 0;
@@ -401,7 +406,7 @@ __global__ __launch_bounds__(kLoopThreads) void k_g_merge_loop(LoopArgs A) {
             if (!act[c] || c == a) continue;
             const int64_t va = A.V[(size_t)a * m + c];
             const int64_t vb = A.V[(size_t)b * m + c];
-            const int32_t p = A.best_p[c];
+            const int32_t p = best_p[c];
             if (va != 0) nonzero |= 1u << k;
             if (c != b && va > 0 && vb > 0) {
                 cand |= 1u << k;
@@ -528,7 +533,7 @@ __global__ __launch_bounds__(kLoopThreads) void k_g_merge_loop(LoopArgs A) {
             }
         }
         block_best(bv, bp, red_v, red_i);        // includes a barrier after the V writes
-        if (tid == 0) { A.best_v[a] = bv; A.best_p[a] = bp; n_cand = 0; }
+        if (tid == 0) { best_v[a] = bv; best_p[a] = bp; n_cand = 0; }
         // (5) rows whose best partner was a or b: rescan. Values never grow,
         // so the row's old best bounds every entry now: scanning in index
         // order, the first entry at that bound is the answer (largest value,
@@ -541,10 +546,10 @@ __global__ __launch_bounds__(kLoopThreads) void k_g_merge_loop(LoopArgs A) {
             int c = -1;
             if (k < nr) {
                 c = resc_all ? k : resc[k];
-                if (!act[c] || c == a || (resc_all && A.best_p[c] != a && A.best_p[c] != b)) c = -1;
+                if (!act[c] || c == a || (resc_all && best_p[c] != a && best_p[c] != b)) c = -1;
             }
             if (c >= 0) {
-                const int64_t ub = A.best_v[c];
+                const int64_t ub = best_v[c];
                 const int64_t *row = A.V + (size_t)c * m;
                 const int q = (m + kRescParts - 1) / kRescParts;
                 const int lo = part * q, hi = min(m, lo + q);
@@ -578,7 +583,7 @@ __global__ __launch_bounds__(kLoopThreads) void k_g_merge_loop(LoopArgs A) {
             // quarters in index order: the first that holds a best equal to
             // the bound decides, otherwise the best of the four
             if (part == 0 && lane == 0 && c >= 0) {
-                const int64_t ub = A.best_v[c];
+                const int64_t ub = best_v[c];
                 int64_t v = -1;
                 int32_t p = -1;
                 for (int j = 0; j < kRescParts; ++j) {
@@ -586,8 +591,8 @@ __global__ __launch_bounds__(kLoopThreads) void k_g_merge_loop(LoopArgs A) {
                     if (part_v[slot][j] == ub) { v = ub; p = part_p[slot][j]; break; }
                     if (better(part_v[slot][j], part_p[slot][j], v, p)) { v = part_v[slot][j]; p = part_p[slot][j]; }
                 }
-                A.best_v[c] = v;
-                A.best_p[c] = p;
+                best_v[c] = v;
+                best_p[c] = p;
             }
             __syncthreads();
         }
