@@ -212,6 +212,8 @@ __device__ inline void zeta_scatter(int64_t *tile, uint32_t low, int64_t w) {
 // in registers and walks tiles blockIdx.x, + gridDim.x, ...; a tile's stores
 // drain while the next tile is built.
 constexpr int kZetaHeld = 4;
+// above this many list checks (tiles x slots) the dense route is cheaper
+constexpr double kDenseAbove = 8589934592.0;
 
 __global__ __launch_bounds__(kZetaThreads) void k_weights_tile(
         int m, uint32_t cap, uint32_t n_tiles, const uint32_t *list_sig, const int64_t *list_w, const WsHeader *h,
@@ -269,6 +271,62 @@ __global__ __launch_bounds__(kZetaThreads) void k_weights_tile(
 #pragma unroll
             for (int k = 0; k < 16; ++k)
                 if (t + (k << 9) < (1 << m)) out[t + (k << 9)] = v[k];
+        }
+    }
+}
+
+// Dense route for long chunk lists (the tile kernel scans the whole list
+// once per tile, tiles x entries in all): f(S) = the weight of the chunks
+// with S_x = S, scattered into W, then the superset zeta
+// W(S) = sum_{T superset of S} f(T) in place -- the 13 low bits inside LDS
+// tiles, the high bits two at a time in global passes.
+__global__ void k_dense_zero(int64_t n, int64_t *W) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+        W[i] = 0;
+}
+
+__global__ void k_dense_scatter(uint32_t cap, const uint32_t *list_sig, const int64_t *list_w, const WsHeader *h,
+                                int64_t *W) {
+    const uint32_t cnt = min(h->n_list, cap);
+    for (uint32_t j = blockIdx.x * blockDim.x + threadIdx.x; j < cnt; j += gridDim.x * blockDim.x)
+        atomicAdd((unsigned long long *)&W[list_sig[j]], (unsigned long long)list_w[j]);
+    if (blockIdx.x == 0 && threadIdx.x == 0)
+        atomicAdd((unsigned long long *)&W[0], (unsigned long long)h->zero_weight);
+}
+
+// superset zeta over the low min(m, 13) bits of one tile
+__global__ __launch_bounds__(kZetaThreads) void k_dense_zeta_low(int m, int64_t *W) {
+    __shared__ int64_t tile[kZetaN + kZetaN / 8];
+    const int b = m < kZetaBits ? m : kZetaBits;
+    const int n = 1 << b;
+    int64_t *base = W + ((int64_t)blockIdx.x << kZetaBits);
+    for (int e = threadIdx.x; e < n; e += kZetaThreads) tile[zpos(e)] = base[e];
+    __syncthreads();
+    for (int j = 0; j < b; ++j) {
+        for (int p = threadIdx.x; p < n / 2; p += kZetaThreads) {
+            const int lo = ((p >> j) << (j + 1)) | (p & ((1 << j) - 1));   // bit j clear
+            tile[zpos(lo)] += tile[zpos(lo | (1 << j))];
+        }
+        __syncthreads();
+    }
+    for (int e = threadIdx.x; e < n; e += kZetaThreads) base[e] = tile[zpos(e)];
+}
+
+// superset zeta over bit j (and j + 1 when two is set): every thread owns
+// the subsets that differ only in those bits
+__global__ void k_dense_zeta_high(int m, int j, int two, int64_t *W) {
+    const int64_t groups = (int64_t)1 << (m - 1 - two);
+    for (int64_t g = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; g < groups; g += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t s = ((g >> j) << (j + 1 + two)) | (g & (((int64_t)1 << j) - 1));
+        const int64_t b1 = (int64_t)1 << j;
+        if (two) {
+            const int64_t b2 = b1 << 1;
+            const int64_t d = W[s | b1 | b2], c = W[s | b2] + d, bb = W[s | b1] + d;
+            W[s] += bb + c - d;                  // f(s) + f(s|b1) + f(s|b2) + f(s|b1|b2) sums
+            W[s | b1] = bb;
+            W[s | b2] = c;
+        } else {
+            W[s] += W[s | b1];
         }
     }
 }
@@ -1317,11 +1375,22 @@ extern "C" int mpt_build_weights(int m, int64_t n_chunks, int64_t nnz, const int
                                                               list_sig, list_w, h);
         }
     }
-    {
+    const uint32_t tiles = m > kZetaBits ? 1u << (m - kZetaBits) : 1u;
+    if ((double)tiles * (double)nnz <= kDenseAbove) {
         LaunchScope ls("weights_tile", 8.0 * (double)(1ull << m), s);
-        const uint32_t tiles = m > kZetaBits ? 1u << (m - kZetaBits) : 1u;
         k_weights_tile<<<std::min(tiles, 512u), kZetaThreads, 0, s>>>(m, (uint32_t)std::max<int64_t>(nnz, 1), tiles,
                                                                       list_sig, list_w, h, W);
+    } else {
+        // long list: scatter + zeta over the dense table
+        const int64_t n = (int64_t)1 << m;
+        LaunchScope ls("weights_dense", 8.0 * (double)n, s);
+        k_dense_zero<<<grid_for(n, 256, 16384), 256, 0, s>>>(n, W);
+        k_dense_scatter<<<grid_for(nnz, 256), 256, 0, s>>>((uint32_t)std::max<int64_t>(nnz, 1), list_sig, list_w, h, W);
+        k_dense_zeta_low<<<tiles, kZetaThreads, 0, s>>>(m, W);
+        for (int j = kZetaBits; j < m; j += 2) {
+            const int two = j + 1 < m ? 1 : 0;
+            k_dense_zeta_high<<<grid_for(n >> (1 + two), 256, 16384), 256, 0, s>>>(m, j, two, W);
+        }
     }
     k_check_total<<<1, 64, 0, s>>>(m, W, h);
     MPT_HIP_TRY(hipGetLastError());
