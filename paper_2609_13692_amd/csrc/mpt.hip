@@ -22,6 +22,7 @@
 #include <string>
 #include <vector>
 
+#include "bitonic.h"
 #include "common.h"
 #include "mpt.h"
 
@@ -1079,8 +1080,9 @@ __global__ void k_request_total(int m, const int64_t *W, WsHeader *h) {
 // ---------------------------------------------------------------------------
 // phase 3: one workgroup per request i. Chunk x of R_i is emitted at the
 // first node of i's root-to-leaf path that lies inside S_x; inside a node
-// chunks go in ascending id. The output slot of x is its rank under the key
-// (depth, id); keys are distinct because ids are distinct within R_i.
+// chunks go in ascending id. Every slot gets the key (request, depth, id);
+// one sort of all keys then leaves each request's chunks in its own slot
+// range, in emission order (keys are distinct: ids are distinct within R_i).
 __global__ __launch_bounds__(256) void k_extract(int m, int64_t n_chunks, int64_t nnz, const int64_t *req_off,
                                                  const int32_t *req_chunks, const uint32_t *sig,
                                                  const uint32_t *split, uint64_t *keys, int32_t *order_chunks,
@@ -1125,17 +1127,21 @@ __global__ __launch_bounds__(256) void k_extract(int m, int64_t n_chunks, int64_
             const uint32_t s = sig[x];
             int d = 0;
             while (d < dn - 1 && (path[d] & ~s)) ++d;
-            key = ((uint64_t)d << 32) | (uint32_t)x;
+            key = ((uint64_t)i << 37) | ((uint64_t)d << 32) | (uint32_t)x;   // i < 32, d < 32
         }
         keys[j] = key;
     }
-    __syncthreads();
-    for (int64_t j = lo + threadIdx.x; j < hi; j += blockDim.x) {
-        const uint64_t kj = keys[j];
-        int64_t rank = 0;
-        for (int64_t t = lo; t < hi; ++t) rank += keys[t] < kj;
-        order_chunks[lo + rank] = (int32_t)(kj & 0xffffffffu);
-    }
+    (void)order_chunks;
+}
+
+__global__ void k_fill_u64(uint64_t *p, int64_t from, int64_t to, uint64_t v) {
+    for (int64_t i = from + blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < to; i += (int64_t)gridDim.x * blockDim.x)
+        p[i] = v;
+}
+
+__global__ void k_extract_out(int64_t nnz, const uint64_t *keys, int32_t *order_chunks) {
+    for (int64_t j = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; j < nnz; j += (int64_t)gridDim.x * blockDim.x)
+        order_chunks[j] = (int32_t)(keys[j] & 0xffffffffu);
 }
 
 // ---------------------------------------------------------------------------
@@ -1226,6 +1232,13 @@ struct WsLayout {
     size_t list_sig, list_w, part_v, part_a, keys, rb_part, total;
 };
 
+// keys sorted by the extraction: a power of two, at least one sort tile
+inline size_t extract_keys(int64_t nnz) {
+    size_t n = (size_t)mptlib::kSortTile;
+    while (n < (size_t)nnz) n <<= 1;
+    return n;
+}
+
 WsLayout ws_layout(int m, int64_t nnz) {
     WsLayout L{};
     const size_t nz = (size_t)std::max<int64_t>(nnz, 1);
@@ -1240,7 +1253,7 @@ WsLayout ws_layout(int m, int64_t nnz) {
     L.part_a = off + align256(P * 8);
     size_t dp_end = L.part_a + align256(P * 4);
     L.keys = off;
-    size_t ex_end = L.keys + align256(nz * 8);
+    size_t ex_end = L.keys + align256(extract_keys(nnz) * 8);
     L.rb_part = off;
     size_t rb_end = L.rb_part + align256(rb_partial_entries(m) * 8);
     L.total = std::max(std::max(build_end, rb_end), std::max(dp_end, ex_end));
@@ -1483,11 +1496,20 @@ extern "C" int mpt_extract_orders(int m, int64_t n_chunks, int64_t nnz, const in
     k_check_offsets<<<1, 64, 0, s>>>(m, nnz, req_off, h);
     {
         LaunchScope ls("extract", (double)nnz, s);
-        k_extract<<<m, 256, 0, s>>>(m, n_chunks, nnz, req_off, req_chunks, sig, split, (uint64_t *)(ws + L.keys),
-                                    order_chunks, h);
+        uint64_t *keys = (uint64_t *)(ws + L.keys);
+        const int64_t nk = (int64_t)extract_keys(nnz);
+        k_fill_u64<<<grid_for(nk - nnz, 256), 256, 0, s>>>(keys, nnz, nk, ~0ull);
+        k_extract<<<m, 256, 0, s>>>(m, n_chunks, nnz, req_off, req_chunks, sig, split, keys, order_chunks, h);
+        MPT_HIP_TRY(hipGetLastError());
+        int rc = read_errors(h, s);               // offsets and the hierarchy checked before the sort
+        if (rc) return rc;
+        if (nnz > 0) {
+            if ((rc = mptlib::sort_keys(keys, nk, s))) return rc;
+            k_extract_out<<<grid_for(nnz, 256), 256, 0, s>>>(nnz, keys, order_chunks);
+        }
     }
     MPT_HIP_TRY(hipGetLastError());
-    return read_errors(h, s);
+    return MPT_OK;
 }
 
 namespace mptlib {

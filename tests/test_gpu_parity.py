@@ -321,3 +321,15 @@ def test_weight_table_dense_route_for_long_lists():
     prof = mpt.profile_end()
     assert "weights_dense" in prof and "weights_tile" not in prof
     assert np.array_equal(prob.W.cpu().numpy(), oracle.intersection_weights(inst))
+
+
+def test_long_requests():
+    """Requests of thousands of chunks: every table and the orders against
+    the oracle (the orders come from one sort of (request, depth, id) keys)."""
+    rng = np.random.default_rng(21)
+    u = 30000
+    sets = [rng.choice(u, size=int(rng.integers(6000, 12000)), replace=False).tolist() for _ in range(8)]
+    w = rng.integers(1, 300, size=u, dtype=np.int64)
+    inst = wl.from_sets(sets, w, u)
+    got = gpu_run(inst)
+    assert_same(inst, got, oracle.solve(inst))
