@@ -112,6 +112,9 @@ int mpt_solve_exact(int m, const int64_t *W, int64_t *C, uint32_t *split,
  *   req_off, req_chunks  the instance (as for mpt_build_weights)
  *   sig, split           outputs of the two calls above
  *   order_chunks [nnz]   out: pi_i at order_chunks[req_off[i] .. req_off[i+1])
+ * Fails with MPT_E_INVALID (offsets, or a split table that does not encode
+ * a hierarchy below the full set) or MPT_E_RANGE (a chunk id) before
+ * anything is written; synchronises `stream` once to report those checks.
  */
 int mpt_extract_orders(int m, int64_t n_chunks, int64_t nnz,
                        const int64_t *req_off, const int32_t *req_chunks,

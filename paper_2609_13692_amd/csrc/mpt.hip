@@ -1085,8 +1085,7 @@ __global__ void k_request_total(int m, const int64_t *W, WsHeader *h) {
 // range, in emission order (keys are distinct: ids are distinct within R_i).
 __global__ __launch_bounds__(256) void k_extract(int m, int64_t n_chunks, int64_t nnz, const int64_t *req_off,
                                                  const int32_t *req_chunks, const uint32_t *sig,
-                                                 const uint32_t *split, uint64_t *keys, int32_t *order_chunks,
-                                                 WsHeader *h) {
+                                                 const uint32_t *split, uint64_t *keys, WsHeader *h) {
     __shared__ uint32_t path[32];
     __shared__ int depth_n;
     __shared__ int bad;
@@ -1131,7 +1130,6 @@ __global__ __launch_bounds__(256) void k_extract(int m, int64_t n_chunks, int64_
         }
         keys[j] = key;
     }
-    (void)order_chunks;
 }
 
 __global__ void k_fill_u64(uint64_t *p, int64_t from, int64_t to, uint64_t v) {
@@ -1499,7 +1497,7 @@ extern "C" int mpt_extract_orders(int m, int64_t n_chunks, int64_t nnz, const in
         uint64_t *keys = (uint64_t *)(ws + L.keys);
         const int64_t nk = (int64_t)extract_keys(nnz);
         k_fill_u64<<<grid_for(nk - nnz, 256), 256, 0, s>>>(keys, nnz, nk, ~0ull);
-        k_extract<<<m, 256, 0, s>>>(m, n_chunks, nnz, req_off, req_chunks, sig, split, keys, order_chunks, h);
+        k_extract<<<m, 256, 0, s>>>(m, n_chunks, nnz, req_off, req_chunks, sig, split, keys, h);
         MPT_HIP_TRY(hipGetLastError());
         int rc = read_errors(h, s);               // offsets and the hierarchy checked before the sort
         if (rc) return rc;
