@@ -498,13 +498,9 @@ namespace rb {
 constexpr int L = 12;                 // row bits
 constexpr int CB = 3;                 // register-block bits
 constexpr int R2 = L - CB;            // middle bits
-#ifndef MPT_RB_ITEM_LOG
-#define MPT_RB_ITEM_LOG 3
-#endif
 #ifndef MPT_RB_THREADS
 #define MPT_RB_THREADS 1024
 #endif
-constexpr int T = MPT_RB_ITEM_LOG;    // log2 of the A2 iterations per work item
 constexpr int NB = 1 << CB;           // entries per block
 constexpr int NE = NB / 2;            // even entries per block
 constexpr int ROW = 1 << L;           // entries per row
@@ -526,31 +522,56 @@ constexpr uint32_t cdeposit(uint32_t t, uint32_t mask) {
     return r;
 }
 
-// work items: (S2, first A2 of a chunk of 2^T submasks of S2 in increasing
-// order), grouped by |S2| from R2 down to 0; entry = S2 | first A2 << 16.
-// Inside a level, up to 8 chunks of one S2 sit in adjacent lanes (so the
-// lanes of a 16-byte LDS read pass share S2 and read structured blocks)
-// and neighbouring groups of 8 lanes hold different S2 (so the accumulator
-// flushes of one wave spread over several blocks).
+// the middle masks of each popcount, for the one-thread-per-block steps
+struct Blocks { uint16_t v[NS2]; int begin[R2 + 1]; int end[R2 + 1]; };
+constexpr Blocks make_blocks() {
+    Blocks b{};
+    int n = 0;
+    for (int k = 0; k <= R2; ++k) {
+        b.begin[k] = n;
+        for (int s = 0; s < NS2; ++s)
+            if (cpop(s) == k) b.v[n++] = (uint16_t)s;
+        b.end[k] = n;
+    }
+    return b;
+}
+constexpr Blocks kBlocks = make_blocks();
+__constant__ Blocks c_blocks = kBlocks;
+
+// Self-pair work items of level k = |S2|: chunks of 2^t_k submasks A2 of
+// S2 in increasing order, t_k the least that keeps the level's items within
+// one pass of the workgroup, so a level's critical path is one item.
+// Grouped by level from R2 down to 0; entry = S2 | first A2 << 16 |
+// t_k << 28 | 1 << 31. Inside a level, up to 8 chunks of one S2 sit in
+// adjacent lanes (their flushes combine in registers) and neighbouring
+// groups of 8 lanes hold different S2 (so the accumulator flushes of one
+// wave spread over several blocks).
 struct Items {
     uint32_t v[8192];
     int begin[R2 + 1];
     int end[R2 + 1];
     int n;
 };
+constexpr int self_item_log(const Blocks &b, int k) {
+    for (int t = 0; t < k; ++t)
+        if ((b.end[k] - b.begin[k]) * (1 << (k - t)) <= THREADS) return t;
+    return k;
+}
 constexpr Items make_items() {
     Items it{};
+    const Blocks b = make_blocks();
     int n = 0;
     for (int k = R2; k >= 0; --k) {
         it.begin[k] = n;
-        const int tb = k < T ? k : T;
+        const int tb = self_item_log(b, k);
         const int chunks = 1 << (k - tb);
         const int lo = chunks < 8 ? chunks : 8;          // chunks of one S2 that sit in adjacent lanes
         for (int jh = 0; jh < chunks / lo; ++jh)
-            for (int s = 0; s < NS2; ++s) {
-                if (cpop(s) != k) continue;
+            for (int bi = b.begin[k]; bi < b.end[k]; ++bi) {
+                const int s = b.v[bi];
                 for (int jl = 0; jl < lo; ++jl)
-                    it.v[n++] = (uint32_t)s | (cdeposit((uint32_t)(jh * lo + jl) << tb, (uint32_t)s) << 16);
+                    it.v[n++] = (uint32_t)s | (cdeposit((uint32_t)(jh * lo + jl) << tb, (uint32_t)s) << 16) |
+                                ((uint32_t)tb << 28) | (1u << 31);
             }
         it.end[k] = n;
     }
@@ -559,7 +580,13 @@ constexpr Items make_items() {
 }
 constexpr Items kItems = make_items();
 static_assert(kItems.n <= 8192, "item table too small");
-__constant__ Items c_items = make_items();
+constexpr bool levels_fit(const Items &it, const Blocks &b) {
+    for (int k = 0; k <= R2; ++k)
+        if (it.end[k] - it.begin[k] > THREADS || b.end[k] - b.begin[k] > THREADS) return false;
+    return true;
+}
+static_assert(levels_fit(kItems, kBlocks), "every level of the self pair runs in one pass of the workgroup");
+__constant__ Items c_items = kItems;
 
 // Cross-pair work of the threads of a workgroup, lifted on the top middle
 // bit E = 1 << (R2-1): a base iteration (S2', A2') over the other R2-1 middle
@@ -614,22 +641,21 @@ constexpr ThreadItems make_thread_items() {
 constexpr ThreadItems kTItems = make_thread_items();
 static_assert(kTItems.n_big + kTItems.n_split + kTItems.n_small <= THREADS,
               "every cross-pair item needs a thread of its own");
+// the cross-pair loop steps two submasks at a time: an item of S2' != 0
+// starts at a submask without lowbit(S2') and has an even count; the item
+// of S2' = 0 is its single submask
+constexpr bool items_pair_up(const ThreadItems &t) {
+    for (int i = 0; i < THREADS; ++i) {
+        const uint32_t v = t.v[i];
+        if (!(v >> 31)) continue;
+        const uint32_t s2 = v & 0xffu, a2 = (v >> 8) & 0xffu, lg = (v >> 16) & 3u;
+        if (s2 == 0 ? (lg != 0 || a2 != 0) : (lg == 0 || (a2 & (s2 & (0u - s2))) != 0)) return false;
+    }
+    return true;
+}
+static_assert(items_pair_up(kTItems), "cross-pair items must pair up their submasks");
 __constant__ ThreadItems c_titems = make_thread_items();
 
-// the middle masks of each popcount, for the one-thread-per-block steps
-struct Blocks { uint16_t v[NS2]; int begin[R2 + 1]; int end[R2 + 1]; };
-constexpr Blocks make_blocks() {
-    Blocks b{};
-    int n = 0;
-    for (int k = 0; k <= R2; ++k) {
-        b.begin[k] = n;
-        for (int s = 0; s < NS2; ++s)
-            if (cpop(s) == k) b.v[n++] = (uint16_t)s;
-        b.end[k] = n;
-    }
-    return b;
-}
-__constant__ Blocks c_blocks = make_blocks();
 
 // key arithmetic: exact integers as uint64 or as doubles (< 2^53)
 template <class K> struct Key;
@@ -672,8 +698,13 @@ template <> struct Key<double> {
 // to an odd number of 16-byte pieces: piece q of a block then falls in
 // 16-byte bank group (odd * slot + q) mod 8, a bijection of slot mod 8, and
 // a lane's 16-byte reads of one block use immediate offsets.
+// Inside a tagged block entry x sits at position tpos(x) = (x - 1) mod NB,
+// so entries 1..NB-1 fill whole 16-byte pieces: half of the cross-pair
+// convolutions never read entry 0 of one of their tagged blocks, and those
+// loads then stay three 16-byte reads and one aligned 8-byte read.
 constexpr int TSTRIDE = NB + 2;       // K elements per tagged block
 constexpr int PSTRIDE = NE + 2;       // K elements per plain block
+constexpr int tpos(int x) { return (x + NB - 1) & (NB - 1); }
 __device__ inline uint32_t slot_of(uint32_t x2) { return x2 ^ ((x2 >> 3) & 7u) ^ ((x2 >> 6) & 7u); }
 
 template <class K> struct alignas(16) Lds {
@@ -694,10 +725,10 @@ __device__ inline void load_t(const K *row, uint32_t slot, K v[NB]) {
     using V = typename Vec2<K>::type;
     const V *p = reinterpret_cast<const V *>(row + slot * TSTRIDE);
 #pragma unroll
-    for (int q = 0; q < NB / 2; ++q) {
+    for (int q = 0; q < NB / 2; ++q) {                // positions 2q, 2q+1
         const V t = p[q];
-        v[2 * q] = t.x;
-        v[2 * q + 1] = t.y;
+        v[(2 * q + 1) & (NB - 1)] = t.x;
+        v[(2 * q + 2) & (NB - 1)] = t.y;
     }
 }
 
@@ -722,12 +753,9 @@ __device__ inline void load_row(K *P, K *Tt, const uint64_t *__restrict__ C, uin
         const int x2 = g / (NB / 2), q = g % (NB / 2);     // entries 2q, 2q+1 of block x2
         const ulonglong2 v = src[g];
         const uint32_t idx = tag | (uint32_t)(2 * g);
-        using V = typename Vec2<K>::type;
         const uint32_t sl = slot_of((uint32_t)x2);
-        V t;
-        t.x = Key<K>::load_tagged(v.x, idx);
-        t.y = Key<K>::load_tagged(v.y, idx + 1u);
-        *reinterpret_cast<V *>(Tt + sl * TSTRIDE + 2 * q) = t;
+        Tt[sl * TSTRIDE + tpos(2 * q)] = Key<K>::load_tagged(v.x, idx);
+        Tt[sl * TSTRIDE + tpos(2 * q + 1)] = Key<K>::load_tagged(v.y, idx + 1u);
         P[sl * PSTRIDE + q] = Key<K>::load_plain(v.x);
     }
 }
@@ -747,21 +775,17 @@ __device__ inline void load_rows2(K *Pa, K *Ta, K *Pb, K *Tb, const uint64_t *__
         va[p] = srca[threadIdx.x + p * THREADS];
         vb[p] = srcb[threadIdx.x + p * THREADS];
     }
-    using V = typename Vec2<K>::type;
 #pragma unroll
     for (int p = 0; p < PER; ++p) {
         const int g = threadIdx.x + p * THREADS;
         const int x2 = g / (NB / 2), q = g % (NB / 2);   // entries 2q, 2q+1 of block x2
         const uint32_t sl = slot_of((uint32_t)x2);
         const uint32_t ia = (xa << L) | (uint32_t)(2 * g), ib = (xb << L) | (uint32_t)(2 * g);
-        V t;
-        t.x = Key<K>::load_tagged(va[p].x, ia);
-        t.y = Key<K>::load_tagged(va[p].y, ia + 1u);
-        *reinterpret_cast<V *>(Ta + sl * TSTRIDE + 2 * q) = t;
+        Ta[sl * TSTRIDE + tpos(2 * q)] = Key<K>::load_tagged(va[p].x, ia);
+        Ta[sl * TSTRIDE + tpos(2 * q + 1)] = Key<K>::load_tagged(va[p].y, ia + 1u);
         Pa[sl * PSTRIDE + q] = Key<K>::load_plain(va[p].x);
-        t.x = Key<K>::load_tagged(vb[p].x, ib);
-        t.y = Key<K>::load_tagged(vb[p].y, ib + 1u);
-        *reinterpret_cast<V *>(Tb + sl * TSTRIDE + 2 * q) = t;
+        Tb[sl * TSTRIDE + tpos(2 * q)] = Key<K>::load_tagged(vb[p].x, ib);
+        Tb[sl * TSTRIDE + tpos(2 * q + 1)] = Key<K>::load_tagged(vb[p].y, ib + 1u);
         Pb[sl * PSTRIDE + q] = Key<K>::load_plain(vb[p].x);
     }
 }
@@ -834,7 +858,7 @@ __device__ inline void flush_group(const K best[NB], uint32_t s2, uint32_t seg, 
     }
 }
 
-// one self-pair work item (S2, first A2) against (rowS, row0): 2^min(|S2|,T)
+// one self-pair work item (S2, first A2, t) against (rowS, row0): 2^t
 // submasks A2 of S2 in increasing order, skipping A2 == S2 and, when
 // skip_empty, A2 == 0
 template <class K>
@@ -842,10 +866,11 @@ __device__ inline void run_item(uint32_t item, const K *pA, const K *tA, const K
                                 bool skip_empty) {
     const uint32_t s2 = item & 0xffffu;
     const int k = __popc(s2);
-    const uint32_t cnt = 1u << (k < T ? k : T);
+    const int tb = (int)((item >> 28) & 7u);
+    const uint32_t cnt = 1u << tb;
     const uint32_t low2 = s2 & (0u - s2);
     const uint32_t slot_s2 = slot_of(s2);
-    uint32_t a2 = item >> 16;
+    uint32_t a2 = (item >> 16) & 0xfffu;
     K best[NB];
 #pragma unroll
     for (int x = 0; x < NB; ++x) best[x] = Key<K>::none();
@@ -862,7 +887,7 @@ __device__ inline void run_item(uint32_t item, const K *pA, const K *tA, const K
         }
         a2 = ((a2 | ~s2) + 1u) & s2;
     }
-    const uint32_t chunks = 1u << (k - (k < T ? k : T));
+    const uint32_t chunks = 1u << (k - tb);
     flush_group<K>(best, s2, chunks < 8u ? chunks : 8u, acc);
 }
 
@@ -877,35 +902,48 @@ __device__ inline uint64_t untag(K t, uint32_t idx) {
 // (pS, tS) receive row S_H, (s.pb, s.tb) hold row 0 -- the same buffers
 // when S_H = 0, in which case they are filled here. Writes C' and split.
 template <class K>
-__device__ void finalize_row(int m, uint32_t sh, Lds<K> &s, K *pS, K *tS, const int64_t *__restrict__ W,
-                             uint64_t *__restrict__ Cp, uint32_t *__restrict__ split) {
+__device__ __attribute__((always_inline)) inline void finalize_row(int m, uint32_t sh, Lds<K> &s, K *pS, K *tS,
+                                                                   const int64_t *__restrict__ W,
+                                                                   uint64_t *__restrict__ Cp,
+                                                                   uint32_t *__restrict__ split) {
     const uint32_t a_hi = sh << L;
     const uint64_t mask = ((uint64_t)1 << m) - 1u;
+    // this thread's item and block of a level (0: none), each read one
+    // level ahead so that the table lookups overlap the level before
+    auto level_item = [](int k) -> uint32_t {
+        const int it = c_items.begin[k] + (int)threadIdx.x;
+        return it < c_items.end[k] ? c_items.v[it] : 0u;
+    };
+    auto level_blk = [](int k) -> uint32_t {
+        const int bi = c_blocks.begin[k] + (int)threadIdx.x;
+        return bi < c_blocks.end[k] ? (uint32_t)c_blocks.v[bi] | 0x10000u : 0u;
+    };
+    uint32_t item = level_item(0), blk = level_blk(0);
     for (int k = 0; k <= R2; ++k) {
+        const uint32_t item_next = k < R2 ? level_item(k + 1) : 0u;
+        const uint32_t blk_next = k < R2 ? level_blk(k + 1) : 0u;
         // W of the block this thread finishes below, read ahead of phase 1
         int64_t wv[NB];
-        const int bi0 = c_blocks.begin[k] + threadIdx.x;
-        if (bi0 < c_blocks.end[k]) {
-            const int64_t *wp = W + (a_hi | ((uint32_t)c_blocks.v[bi0] << CB));
+        if (blk) {
+            const int64_t *wp = W + (a_hi | ((blk & 0xffffu) << CB));
 #pragma unroll
             for (int x = 0; x < NB; ++x) wv[x] = wp[x];
         }
         // A2 a proper submask of S2 (for S_H = 0 also non-empty: those pairs
         // mirror the in-block pairs below)
-        for (int it = kItems.begin[k] + threadIdx.x; it < kItems.end[k]; it += THREADS)
-            run_item<K>(c_items.v[it], pS, tS, s.pb, s.tb, s.acc, sh == 0);
+        if (item) run_item<K>(item, pS, tS, s.pb, s.tb, s.acc, sh == 0);
         lds_barrier();
         // A2 = S2: in-block pairs, one thread per block of this level
-        for (int bi = c_blocks.begin[k] + threadIdx.x; bi < c_blocks.end[k]; bi += THREADS) {
-            const uint32_t s2 = c_blocks.v[bi];
+        if (blk) {
+            const uint32_t s2 = blk & 0xffffu;
             const uint32_t base = a_hi | (s2 << CB);
             // row 0, block 0 (complete, except while S_H = 0 builds it: then
-            // it is this very block and out[] is used instead)
+            // it is this very block, whose entries are copied in as they are
+            // finished -- every B1 below is a proper submask of S1)
+            const bool self0 = sh == 0 && s2 == 0;
             uint64_t b0[NB];
-            if (!(sh == 0 && s2 == 0)) {
 #pragma unroll
-                for (int x = 0; x < NB; ++x) b0[x] = untag<K>(s.tb[x], (uint32_t)x);
-            }
+            for (int x = 0; x < NB; ++x) b0[x] = self0 ? 0u : untag<K>(s.tb[tpos(x)], (uint32_t)x);
             uint64_t out[NB];
             uint32_t sp[NB];
             // S1 in order of popcount so that every A1 < S1 is ready
@@ -915,9 +953,14 @@ __device__ void finalize_row(int m, uint32_t sh, Lds<K> &s, K *pS, K *tS, const 
                 for (int s1 = 0; s1 < NB; ++s1) {
                     if (cpop(s1) != pc) continue;
                     const uint32_t S = base | (uint32_t)s1;
-                    const int64_t w = bi == bi0 ? wv[s1] : W[S];
-                    if (S == 0) { out[s1] = SENT; sp[s1] = 0; continue; }
-                    if (__popc(S) == 1) { out[s1] = (uint64_t)w << m; sp[s1] = 0; continue; }
+                    const int64_t w = wv[s1];
+                    if (S == 0) { out[s1] = SENT; sp[s1] = 0; b0[s1] = self0 ? out[s1] : b0[s1]; continue; }
+                    if (__popc(S) == 1) {
+                        out[s1] = (uint64_t)w << m;
+                        sp[s1] = 0;
+                        b0[s1] = self0 ? out[s1] : b0[s1];
+                        continue;
+                    }
                     uint64_t kb = Key<K>::value_of_bits(s.acc[(s2 << CB) | s1]);
                     const int low = s1 & -s1;
 #pragma unroll
@@ -925,25 +968,59 @@ __device__ void finalize_row(int m, uint32_t sh, Lds<K> &s, K *pS, K *tS, const 
                         if ((a1 & ~s1) || a1 == s1) continue;
                         const int b1 = s1 ^ a1;
                         const uint64_t av = out[a1];
-                        const uint64_t bv = (sh == 0 && s2 == 0) ? out[b1] : b0[b1];
+                        const uint64_t bv = b0[b1];
                         const uint64_t c = (a1 & low) ? av + bv + (base | (uint32_t)a1) : av + bv + (uint32_t)b1;
                         kb = c < kb ? c : kb;
                     }
                     out[s1] = ((kb >> m) - (uint64_t)w) << m;
                     sp[s1] = (uint32_t)(kb & mask);
+                    b0[s1] = self0 ? out[s1] : b0[s1];
                 }
             }
             const uint32_t sl = slot_of(s2);
 #pragma unroll
             for (int x = 0; x < NB; ++x) {
-                tS[sl * TSTRIDE + x] = Key<K>::tagged(out[x], base | (uint32_t)x);
+                tS[sl * TSTRIDE + tpos(x)] = Key<K>::tagged(out[x], base | (uint32_t)x);
                 if (!(x & 1)) pS[sl * PSTRIDE + (x >> 1)] = Key<K>::plain(out[x]);
                 Cp[base + x] = Key<K>::store(out[x]);
                 split[base + x] = sp[x];
             }
         }
         lds_barrier();
+        item = item_next;
+        blk = blk_next;
     }
+}
+
+// one base step (S2', A2') of the lifted cross-pair loop: three block
+// convolutions from four block loads. o1 orients S1 = 0 of (S2'|E, A2'),
+// o0 that of (S2', A2') and (S2'|E, A2'|E).
+template <class K>
+__device__ __attribute__((always_inline)) inline void cross_step(const Lds<K> &s, uint32_t a2, uint32_t slot_s2,
+                                                                 uint32_t slot_e, bool o1, bool o0, K best0[NB],
+                                                                 K best1[NB]) {
+    uint32_t sa0 = slot_of(a2), sb0 = slot_s2 ^ sa0;
+    // slots are below NS2; masking values the compiler cannot see through
+    // lets instruction selection use 24-bit multiply-adds for the block
+    // offsets instead of full 32-bit multiplies
+    asm("" : "+v"(sa0), "+v"(sb0));
+    sa0 &= NS2 - 1;
+    sb0 &= NS2 - 1;
+    K pa[NE], ta[NB], pb[NE], tb2[NB];
+    // (S2'|E, A2'): A block A2', B block B2'|E
+    load_p(s.pa, sa0, pa);
+    load_t(s.ta, sa0, ta);
+    load_p(s.pb, sb0 ^ slot_e, pb);
+    load_t(s.tb, sb0 ^ slot_e, tb2);
+    conv_block<K>(pa, ta, pb, tb2, o1, best1);
+    // (S2', A2'): A block A2', B block B2'
+    load_p(s.pb, sb0, pb);
+    load_t(s.tb, sb0, tb2);
+    conv_block<K>(pa, ta, pb, tb2, o0, best0);
+    // (S2'|E, A2'|E): A block A2'|E, B block B2'
+    load_p(s.pa, sa0 ^ slot_e, pa);
+    load_t(s.ta, sa0 ^ slot_e, ta);
+    conv_block<K>(pa, ta, pb, tb2, o0, best1);
 }
 
 // cross pairs of one (S_H, chunk); fused = finish the row in place
@@ -969,7 +1046,6 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
     const uint32_t s2 = item & 0xffu;
     const uint32_t a2_first = (item >> 8) & 0xffu;
     const uint32_t cnt = 1u << ((item >> 16) & 3u);
-    const uint32_t low2 = s2 & (0u - s2);
     const uint32_t slot_s2 = slot_of(s2);
     const uint32_t slot_e = slot_of(E);
     K best0[NB], best1[NB];
@@ -982,26 +1058,19 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
         lds_barrier();
         ah = lowh | (((ah | ~rest) + 1u) & rest);    // next A_H holding lowbit(S_H)
         if (has_item) {
-            uint32_t a2 = a2_first;
-            for (uint32_t i = 0; i < cnt; ++i) {
-                const uint32_t sa0 = slot_of(a2), sb0 = slot_s2 ^ sa0;
-                const bool lowin = (a2 & low2) != 0;
-                K pa[NE], ta[NB], pb[NE], tb2[NB];
-                // (S2'|E, A2'): A block A2', B block B2'|E
-                load_p(s.pa, sa0, pa);
-                load_t(s.ta, sa0, ta);
-                load_p(s.pb, sb0 ^ slot_e, pb);
-                load_t(s.tb, sb0 ^ slot_e, tb2);
-                conv_block<K>(pa, ta, pb, tb2, (s2 != 0) && lowin, best1);
-                // (S2', A2'): A block A2', B block B2'
-                load_p(s.pb, sb0, pb);
-                load_t(s.tb, sb0, tb2);
-                conv_block<K>(pa, ta, pb, tb2, (s2 == 0) || lowin, best0);
-                // (S2'|E, A2'|E): A block A2'|E, B block B2'
-                load_p(s.pa, sa0 ^ slot_e, pa);
-                load_t(s.ta, sa0 ^ slot_e, ta);
-                conv_block<K>(pa, ta, pb, tb2, (s2 == 0) || lowin, best1);
-                a2 = ((a2 | ~s2) + 1u) & s2;
+            if (s2 == 0) {
+                cross_step<K>(s, 0u, slot_s2, slot_e, false, true, best0, best1);
+            } else {
+                // t-th submask of S2' holds lowbit(S2') iff t is odd, and every
+                // item starts at an even t with an even count: the orientation
+                // of each step is fixed at compile time
+                uint32_t a2 = a2_first;
+                for (uint32_t i = 0; i < cnt; i += 2) {
+                    cross_step<K>(s, a2, slot_s2, slot_e, false, false, best0, best1);
+                    a2 = ((a2 | ~s2) + 1u) & s2;
+                    cross_step<K>(s, a2, slot_s2, slot_e, true, true, best0, best1);
+                    a2 = ((a2 | ~s2) + 1u) & s2;
+                }
             }
         }
     }
@@ -1053,8 +1122,7 @@ __global__ __launch_bounds__(THREADS) void k_rb_final(int m, int h, uint32_t chu
     if (sh != 0) load_row<K>(s.pb, s.tb, Cp, 0u);
     lds_barrier();
     // for S_H = 0 the output row is row 0 itself
-    if (sh == 0) finalize_row<K>(m, sh, s, s.pb, s.tb, W, Cp, split);
-    else finalize_row<K>(m, sh, s, s.pa, s.ta, W, Cp, split);
+    finalize_row<K>(m, sh, s, sh == 0 ? s.pb : s.pa, sh == 0 ? s.tb : s.ta, W, Cp, split);
 }
 
 // packed C' -> C (C[0] keeps the documented sentinel)
