@@ -495,7 +495,10 @@ __global__ __launch_bounds__(256) void k_dp_reduce(int m, int p, uint32_t n_sets
 // as doubles (one v_add_f64 and one v_min_f64 per candidate), otherwise
 // as uint64 (below 2^62); larger instances take the plain kernels.
 namespace rb {
-constexpr int L = 12;                 // row bits
+#ifndef MPT_RB_L
+#define MPT_RB_L 12
+#endif
+constexpr int L = MPT_RB_L;           // row bits
 constexpr int CB = 3;                 // register-block bits
 constexpr int R2 = L - CB;            // middle bits
 #ifndef MPT_RB_THREADS
@@ -692,12 +695,16 @@ template <> struct Key<double> {
     static __device__ inline double load_tagged(uint64_t b, uint32_t idx) { return from_bits(b) + (double)idx; }
 };
 
-// LDS rows. Block x2 sits at slot(x2) = x2 ^ (x2 >> 3 & 7) ^ (x2 >> 6 & 7),
-// a GF(2)-linear bijection, so slot(S2 ^ A2) = slot(S2) ^ slot(A2). Blocks
-// are padded by 16 bytes (tagged: NB entries, plain: the NE even entries),
-// to an odd number of 16-byte pieces: piece q of a block then falls in
-// 16-byte bank group (odd * slot + q) mod 8, a bijection of slot mod 8, and
-// a lane's 16-byte reads of one block use immediate offsets.
+// LDS rows. Block x2 sits at slot(x2) = x2 ^ (x2 >> 3 & 7) ^ (x2 >> 6 & 3)
+// (for R2 = 9; the last term takes the bits between 6 and E),
+// a GF(2)-linear bijection, so slot(S2 ^ A2) = slot(S2) ^ slot(A2); it maps
+// the low R2-1 middle bits onto themselves and the top one, E, onto NS2/2,
+// so slot(X | E) = slot(X) + NS2/2 for X below E. Blocks are padded by 16
+// bytes (tagged: NB entries, plain: the NE even entries) to an odd number of
+// 16-byte pieces: piece q of a block falls in the 16-byte bank group
+// (odd * slot + q) mod 16 (gfx950 serves a 16-byte read 16 lanes at a time
+// from 16 such groups), a bijection of slot mod 16, and a lane's 16-byte
+// reads of one block use immediate offsets.
 // Inside a tagged block entry x sits at position tpos(x) = (x - 1) mod NB,
 // so entries 1..NB-1 fill whole 16-byte pieces: half of the cross-pair
 // convolutions never read entry 0 of one of their tagged blocks, and those
@@ -705,7 +712,20 @@ template <> struct Key<double> {
 constexpr int TSTRIDE = NB + 2;       // K elements per tagged block
 constexpr int PSTRIDE = NE + 2;       // K elements per plain block
 constexpr int tpos(int x) { return (x + NB - 1) & (NB - 1); }
-__device__ inline uint32_t slot_of(uint32_t x2) { return x2 ^ ((x2 >> 3) & 7u) ^ ((x2 >> 6) & 7u); }
+__host__ __device__ constexpr uint32_t slot_of(uint32_t x2) {
+    return x2 ^ ((x2 >> 3) & 7u) ^ ((x2 >> 6) & ((1u << (R2 - 7)) - 1u));
+}
+constexpr bool slots_ok() {
+    bool seen[NS2] = {};
+    for (uint32_t x = 0; x < (uint32_t)NS2; ++x) {
+        const uint32_t sl = slot_of(x);
+        if (sl >= (uint32_t)NS2 || seen[sl]) return false;
+        seen[sl] = true;
+        if (x < (uint32_t)NS2 / 2 && (sl >= (uint32_t)NS2 / 2 || slot_of(x | NS2 / 2) != sl + NS2 / 2)) return false;
+    }
+    return true;
+}
+static_assert(R2 >= 7 && slots_ok(), "slot_of is a bijection that puts the E half NS2/2 above the rest");
 
 template <class K> struct alignas(16) Lds {
     K pa[NS2 * PSTRIDE];   // row on the A side, plain, even low parts
@@ -715,6 +735,8 @@ template <class K> struct alignas(16) Lds {
     uint64_t acc[ROW];     // best key bits per entry of the output row
 };
 static_assert(sizeof(Lds<double>) <= 160 * 1024, "rows and accumulators fit one CU's LDS");
+// workgroups that run on one CU at a time (their LDS takes the CU)
+constexpr int WGS_PER_CU = (int)((160 * 1024) / sizeof(Lds<double>));
 
 template <class K> struct Vec2;
 template <> struct Vec2<uint64_t> { using type = ulonglong2; };
@@ -994,32 +1016,33 @@ __device__ __attribute__((always_inline)) inline void finalize_row(int m, uint32
 
 // one base step (S2', A2') of the lifted cross-pair loop: three block
 // convolutions from four block loads. o1 orients S1 = 0 of (S2'|E, A2'),
-// o0 that of (S2', A2') and (S2'|E, A2'|E).
+// o0 that of (S2', A2') and (S2'|E, A2'|E). The blocks with E sit NS2/2
+// slots above those without, a constant offset.
 template <class K>
 __device__ __attribute__((always_inline)) inline void cross_step(const Lds<K> &s, uint32_t a2, uint32_t slot_s2,
-                                                                 uint32_t slot_e, bool o1, bool o0, K best0[NB],
-                                                                 K best1[NB]) {
+                                                                 bool o1, bool o0, K best0[NB], K best1[NB]) {
+    constexpr uint32_t HALF = NS2 / 2;
     uint32_t sa0 = slot_of(a2), sb0 = slot_s2 ^ sa0;
-    // slots are below NS2; masking values the compiler cannot see through
-    // lets instruction selection use 24-bit multiply-adds for the block
-    // offsets instead of full 32-bit multiplies
+    // slots of blocks without E are below HALF; masking values the compiler
+    // cannot see through lets instruction selection use 24-bit multiply-adds
+    // for the block offsets instead of full 32-bit multiplies
     asm("" : "+v"(sa0), "+v"(sb0));
-    sa0 &= NS2 - 1;
-    sb0 &= NS2 - 1;
+    sa0 &= HALF - 1;
+    sb0 &= HALF - 1;
     K pa[NE], ta[NB], pb[NE], tb2[NB];
     // (S2'|E, A2'): A block A2', B block B2'|E
     load_p(s.pa, sa0, pa);
     load_t(s.ta, sa0, ta);
-    load_p(s.pb, sb0 ^ slot_e, pb);
-    load_t(s.tb, sb0 ^ slot_e, tb2);
+    load_p(s.pb + HALF * PSTRIDE, sb0, pb);
+    load_t(s.tb + HALF * TSTRIDE, sb0, tb2);
     conv_block<K>(pa, ta, pb, tb2, o1, best1);
     // (S2', A2'): A block A2', B block B2'
     load_p(s.pb, sb0, pb);
     load_t(s.tb, sb0, tb2);
     conv_block<K>(pa, ta, pb, tb2, o0, best0);
     // (S2'|E, A2'|E): A block A2'|E, B block B2'
-    load_p(s.pa, sa0 ^ slot_e, pa);
-    load_t(s.ta, sa0 ^ slot_e, ta);
+    load_p(s.pa + HALF * PSTRIDE, sa0, pa);
+    load_t(s.ta + HALF * TSTRIDE, sa0, ta);
     conv_block<K>(pa, ta, pb, tb2, o0, best1);
 }
 
@@ -1047,7 +1070,7 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
     const uint32_t a2_first = (item >> 8) & 0xffu;
     const uint32_t cnt = 1u << ((item >> 16) & 3u);
     const uint32_t slot_s2 = slot_of(s2);
-    const uint32_t slot_e = slot_of(E);
+    static_assert(RL == R2 - 1 && (1u << RL) == NS2 / 2, "E is the top middle bit");
     K best0[NB], best1[NB];
 #pragma unroll
     for (int x = 0; x < NB; ++x) { best0[x] = Key<K>::none(); best1[x] = Key<K>::none(); }
@@ -1059,16 +1082,16 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
         ah = lowh | (((ah | ~rest) + 1u) & rest);    // next A_H holding lowbit(S_H)
         if (has_item) {
             if (s2 == 0) {
-                cross_step<K>(s, 0u, slot_s2, slot_e, false, true, best0, best1);
+                cross_step<K>(s, 0u, slot_s2, false, true, best0, best1);
             } else {
                 // t-th submask of S2' holds lowbit(S2') iff t is odd, and every
                 // item starts at an even t with an even count: the orientation
                 // of each step is fixed at compile time
                 uint32_t a2 = a2_first;
                 for (uint32_t i = 0; i < cnt; i += 2) {
-                    cross_step<K>(s, a2, slot_s2, slot_e, false, false, best0, best1);
+                    cross_step<K>(s, a2, slot_s2, false, false, best0, best1);
                     a2 = ((a2 | ~s2) + 1u) & s2;
-                    cross_step<K>(s, a2, slot_s2, slot_e, true, true, best0, best1);
+                    cross_step<K>(s, a2, slot_s2, true, true, best0, best1);
                     a2 = ((a2 | ~s2) + 1u) & s2;
                 }
             }
@@ -1261,12 +1284,13 @@ std::vector<RbLevel> rb_plan(int m) {
         if (L.n_pairs == 0) {
             L.chunks = 0;
         } else {
-            // One workgroup runs per CU at a time (its LDS takes the CU), so a
-            // level of W equal workgroups takes ceil(W / CUs) rounds. Split the
-            // pairs of every S_H into c chunks, c chosen to fill the last round
-            // best; keep c = 1 (the row is finished in the same kernel) unless
-            // splitting wins by a clear margin.
-            const double cus = rb::CUS;
+            // A fixed number of workgroups runs per CU at a time (their LDS
+            // takes the CU), so a level of W equal workgroups takes
+            // ceil(W / slots) rounds. Split the pairs of every S_H into c
+            // chunks, c chosen to fill the last round best; keep c = 1 (the
+            // row is finished in the same kernel) unless splitting wins by a
+            // clear margin.
+            const double cus = rb::CUS * rb::WGS_PER_CU;
             auto eff = [&](uint32_t c) {
                 const double w = (double)L.n_sets * c;
                 return w / (cus * std::ceil(w / cus));
