@@ -167,3 +167,72 @@ def test_determinism():
     b = gpu_greedy(inst)
     for k in ("P", "merge_a", "merge_b", "gain", "parent", "orders"):
         assert np.array_equal(a[k], b[k]), k
+
+
+# --- sizes past the on-chip capacities of the merge loop ------------------
+
+def test_cluster_state_in_global_memory():
+    """m = 6000 requests: the per-cluster signature metadata and row bests no
+    longer fit on chip (4096 clusters) and live in the workspace."""
+    inst = wl.gen_retrieval(m=6000, u=18000, topics=188, k=8, seed=3)
+    got = gpu_greedy(inst)
+    assert_same(inst, got, oracle.greedy_solve(inst))
+
+
+def test_long_intersections():
+    """Requests of 1500-4000 chunks around a shared core of 2500: the
+    intersections I(A), I(B) exceed the on-chip copy (1024 chunks) and I(C)
+    exceeds its on-chip list (2048 chunks)."""
+    rng = np.random.default_rng(11)
+    u = 9000
+    core = rng.choice(u, size=2500, replace=False)
+    rest = np.setdiff1d(np.arange(u), core)
+    sets = []
+    for _ in range(40):
+        keep = core[rng.random(core.size) < rng.uniform(0.85, 1.0)]
+        extra = rng.choice(rest, size=int(rng.integers(0, 1500)), replace=False)
+        sets.append(np.concatenate([keep, extra]).tolist())
+    w = rng.integers(1, 200, size=u)
+    inst = wl.from_sets(sets, w.tolist(), u)
+    got = gpu_greedy(inst)
+    assert_same(inst, got, oracle.greedy_solve(inst))
+
+
+def test_many_candidate_columns():
+    """m = 3000 requests that all hold one common chunk: every merge has
+    positive values against every other cluster, more candidate columns than
+    the on-chip list (2048) holds."""
+    base = wl.gen_retrieval(m=3000, u=9000, topics=94, k=8, seed=4)
+    sets = [r + [9000] for r in base.requests()]
+    w = np.concatenate([base.weights, [5]])
+    inst = wl.from_sets(sets, w.tolist(), 9001)
+    got = gpu_greedy(inst)
+    assert_same(inst, got, oracle.greedy_solve(inst))
+
+
+def test_largest_m_properties():
+    """m = 16384, the largest the calls take. The cubic oracle is out of
+    reach, so: pair weights and spanning-tree bound against the oracle,
+    the first merge against the maximum of P (ties to the smallest pair),
+    merge values non-increasing (Theorem 6 part (i)), the savings equal to
+    the sum of the merge values and to Eq. 3 on the returned hierarchy, and
+    the layout equal to the one read off that hierarchy."""
+    inst = wl.gen_retrieval(m=16384, u=49152, topics=512, k=8, seed=6)
+    got = gpu_greedy(inst)
+    m = inst.m
+    P = oracle.pair_weights(inst)
+    assert np.array_equal(got["P"], P)
+    assert got["mst"] == oracle.max_spanning_tree(P)
+    off = P.copy()
+    np.fill_diagonal(off, -1)
+    best = off.max()
+    i, j = np.argwhere(off == best)[0]                       # row-major: smallest (i, j), i < j
+    assert (got["merge_a"][0], got["merge_b"][0], got["gain"][0]) == (i, j, best)
+    g = got["gain"]
+    assert np.all(g[:-1] >= g[1:]) and g[-1] >= 0
+    assert got["savings"] == int(g.sum()) == oracle.tree_savings(inst, got["parent"])
+    assert got["cost"] == int(np.trace(P)) - got["savings"]
+    assert np.array_equal(got["orders"], oracle.tree_orders(inst, got["parent"]))
+    parent = got["parent"]
+    assert parent.size == 2 * m - 1 and parent[-1] == -1
+    assert np.all(np.bincount(parent[:-1], minlength=2 * m - 1)[m:] == 2)

@@ -159,3 +159,29 @@ def test_error_codes():
     assert e.value.status == -4
     L.chunk_w[1] = 1
     assert L.cost(L.seqs(inst.req_chunks)) == 4
+
+
+def test_cache_simulation_beyond_lds():
+    """m = 8192 requests: the trie has more nodes than the simulator keeps in
+    LDS (36K), so the latest-access table lives in the workspace. Sampled
+    configurations against the oracle, the whole grid against the
+    invariants."""
+    inst = wl.gen_retrieval(m=8192, u=24576, topics=256, k=8, seed=2)
+    lay = np.asarray(inst.req_chunks, dtype=np.int32)
+    unit = wl.from_sets(inst.requests(), [1] * inst.n_chunks, inst.n_chunks)
+    assert oracle.trie_cost(unit, lay) > 36 * 1024                # trie nodes
+    mx = max_request(inst)
+    total = int(sum(int(inst.weights[np.asarray(r, dtype=np.int64)].sum()) for r in inst.requests()))
+    windows = [1, 1, 512, 512, 0, 0]
+    caps = [mx, 16 * mx, mx, 16 * mx, mx, 16 * mx]
+    L = mpt.Layouts(inst, n_configs=len(windows))
+    say(f"[gpu cache] {inst.name} m={inst.m} {len(windows)} configurations")
+    got, tc = L.simulate(L.seqs(lay), windows, caps)
+    assert tc == oracle.trie_cost(inst, lay)
+    assert got[4] == got[5] == tc                                   # Theorem 7
+    for W, C, g in zip(windows, caps, got):
+        assert tc <= g <= total
+    assert got[0] >= got[1] and got[2] >= got[3]
+    for k in (0, 3):
+        W, C = windows[k], caps[k]
+        assert got[k] == oracle.lru_cache_cost(inst, lay, oracle.window_schedule(inst, lay, W), C), (W, C)
