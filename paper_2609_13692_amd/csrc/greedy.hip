@@ -286,7 +286,11 @@ struct LoopArgs {
     GHeader *h;
 };
 
-constexpr int kColsPerThread = MPT_GREEDY_MAX_M / kLoopThreads;   // columns (rows) owned by one thread
+// The columns of the candidate pass and of the new row are owned by the
+// waves other than wave 0, which intersects the signatures meanwhile.
+constexpr int kColThreads = kLoopThreads - kWave;
+constexpr int kColsPerThread = (MPT_GREEDY_MAX_M + kColThreads - 1) / kColThreads;
+static_assert(kColsPerThread <= 32, "the column flags of a thread fit 32 bits");
 constexpr int kScCap = 2048;                                        // I(C) kept in LDS up to this size
 constexpr int kSigCap = 1024;                                       // I(A), I(B) copied to LDS up to this size
 constexpr int kMetaCap = 4096;                                      // per-cluster state in LDS up to this m
@@ -330,10 +334,11 @@ __device__ inline int64_t inter_weight_global(const int32_t *ic, int64_t n_ic, c
 
 // Each step: (1) the pair to merge from the threads' cached row bests;
 // (2) candidate columns c, where both V[a][c] and V[b][c] are positive (the
-// new value is at most their minimum); (3) wave 0 intersects the
-// signatures: I(C) = I(A) ∩ I(B) in place and in LDS, D(A), D(B) to the
-// packed lists; (4) the new row and column of a, from intersections at the
-// candidates; (5) rows whose best partner was a or b are rescanned.
+// new value is at most their minimum), on waves 1 and up; (3) at the same
+// time wave 0 intersects the signatures: I(C) = I(A) ∩ I(B) in place and
+// in LDS, D(A), D(B) to the packed lists; (4) the new row and column of a,
+// from intersections at the candidates; (5) rows whose best partner was a
+// or b are rescanned.
 __global__ __launch_bounds__(kLoopThreads) void k_g_merge_loop(LoopArgs A) {
     __shared__ uint8_t act[MPT_GREEDY_MAX_M];    // 1 while r names a live cluster
     __shared__ int32_t sc[kScCap];               // I(C) of the current merge
@@ -399,9 +404,10 @@ __global__ __launch_bounds__(kLoopThreads) void k_g_merge_loop(LoopArgs A) {
         // (2) candidate columns of this thread, and which old values of a
         // are not zero (only changed entries are written back)
         uint32_t cand = 0, nonzero = 0, flag = 0, listed = 0;
+        const int ct = tid - kWave;              // column owner index (wave 0 owns none)
 #pragma unroll 1
-        for (int k = 0; k < kColsPerThread; ++k) {
-            const int c = tid + k * kLoopThreads;
+        for (int k = 0; k < kColsPerThread && ct >= 0; ++k) {
+            const int c = ct + k * kColThreads;
             if (c >= m) break;
             if (!act[c] || c == a) continue;
             const int64_t va = A.V[(size_t)a * m + c];
@@ -507,8 +513,8 @@ __global__ __launch_bounds__(kLoopThreads) void k_g_merge_loop(LoopArgs A) {
             if (better(v, c, bv, bp)) { bv = v; bp = c; }
         }
 #pragma unroll 1
-        for (int k = 0; k < kColsPerThread; ++k) {
-            const int c = tid + k * kLoopThreads;
+        for (int k = 0; k < kColsPerThread && ct >= 0; ++k) {
+            const int c = ct + k * kColThreads;
             if (c >= m) break;
             if (!act[c] || c == a) continue;
             if (!((listed >> k) & 1u)) {
