@@ -30,6 +30,7 @@
  *    guaranteed to be written; mpt_last_error() describes the failure for
  *    the calling thread. No C++ exception crosses this interface.
  *  - Integer ranges: 1 <= m <= MPT_MAX_M; 0 <= n_chunks <= MPT_MAX_CHUNKS;
+ *    0 <= nnz <= 2^31 - 1 (request slots, the same for every call below);
  *    1 <= w(x) <= MPT_MAX_CHUNK_WEIGHT; sum_i w(R_i) < 2^61. These keep
  *    every W, C and pair sum inside int64.
  */
