@@ -106,8 +106,10 @@ __device__ inline void wave_best(int64_t &v, int32_t &i) {
     }
 }
 
-// best (value, index) over the workgroup; every thread gets the result
-__device__ inline void block_best(int64_t &v, int32_t &i, int64_t *sv, int32_t *si) {
+// best (value, index) over the workgroup, every thread gets the result. No
+// closing barrier: the scratch (sv, si) must not be written again before
+// some other barrier of the workgroup.
+__device__ inline void block_best_once(int64_t &v, int32_t &i, int64_t *sv, int32_t *si) {
     wave_best(v, i);
     const int lane = threadIdx.x & (kWave - 1), wid = threadIdx.x / kWave;
     if (lane == 0) { sv[wid] = v; si[wid] = i; }
@@ -115,8 +117,8 @@ __device__ inline void block_best(int64_t &v, int32_t &i, int64_t *sv, int32_t *
     v = sv[0]; i = si[0];
     for (int k = 1; k < (int)(blockDim.x / kWave); ++k)
         if (better(sv[k], si[k], v, i)) { v = sv[k]; i = si[k]; }
-    __syncthreads();
 }
+
 
 // exclusive prefix sum of one int per thread over the workgroup; returns
 // the thread's offset, *total gets the sum
@@ -345,8 +347,11 @@ __global__ __launch_bounds__(kLoopThreads) void k_g_merge_loop(LoopArgs A) {
     __shared__ int64_t scw[kScCap];              // w(x) of the chunks of I(C)
     __shared__ int32_t s_in[2 * kSigCap];        // I(A), I(B) while they are intersected
     __shared__ uint8_t dirty[kLoopThreads];      // a row owned by this thread changed its best
-    __shared__ int64_t red_v[kLoopWaves];
-    __shared__ int32_t red_i[kLoopWaves];
+    // reduction scratch of steps (1) and (4): each is written again only
+    // after barriers of the other steps, so neither reduction needs a
+    // closing barrier
+    __shared__ int64_t red1_v[kLoopWaves], red4_v[kLoopWaves];
+    __shared__ int32_t red1_i[kLoopWaves], red4_i[kLoopWaves];
     __shared__ int scan_w[kLoopWaves];
     __shared__ int64_t cursor;                   // next free slot of dbuf
     __shared__ int64_t s_kept;                   // |I(C)|
@@ -398,7 +403,7 @@ __global__ __launch_bounds__(kLoopThreads) void k_g_merge_loop(LoopArgs A) {
         }
         int64_t g = cv;
         int32_t a = ci;
-        block_best(g, a, red_v, red_i);
+        block_best_once(g, a, red1_v, red1_i);
         if (a < 0 || g <= 0) break;              // every remaining value is 0
         const int32_t b = best_p[a];
         // (2) candidate columns of this thread, and which old values of a
@@ -538,7 +543,7 @@ __global__ __launch_bounds__(kLoopThreads) void k_g_merge_loop(LoopArgs A) {
                 dirty[c % kLoopThreads] = 1;
             }
         }
-        block_best(bv, bp, red_v, red_i);        // includes a barrier after the V writes
+        block_best_once(bv, bp, red4_v, red4_i);   // its barrier comes after the V writes
         if (tid == 0) { best_v[a] = bv; best_p[a] = bp; n_cand = 0; }
         // (5) rows whose best partner was a or b: rescan. Values never grow,
         // so the row's old best bounds every entry now: scanning in index
