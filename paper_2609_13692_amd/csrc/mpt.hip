@@ -1285,22 +1285,25 @@ std::vector<RbLevel> rb_plan(int m) {
             L.chunks = 0;
         } else {
             // A fixed number of workgroups runs per CU at a time (their LDS
-            // takes the CU), so a level of W equal workgroups takes
-            // ceil(W / slots) rounds. Split the pairs of every S_H into c
-            // chunks, c chosen to fill the last round best; keep c = 1 (the
-            // row is finished in the same kernel) unless splitting wins by a
-            // clear margin.
-            const double cus = rb::CUS * rb::WGS_PER_CU;
-            auto eff = [&](uint32_t c) {
-                const double w = (double)L.n_sets * c;
-                return w / (cus * std::ceil(w / cus));
+            // takes the CU), so W equal workgroups take ceil(W / slots)
+            // rounds. In units of one row pair's time, a workgroup also pays
+            // about one pair of fixed cost (accumulator, flush, partials) and
+            // finishing a row about four; a split level finishes its rows in
+            // a separate pass. Pick the chunk count c with the least
+            // modelled time (ties to fewer chunks).
+            const double slots = rb::CUS * rb::WGS_PER_CU;
+            constexpr double kWgCost = 1.0, kFinishCost = 4.1;
+            auto rounds = [&](double w) { return std::ceil(w / slots); };
+            auto cost = [&](uint32_t c) {
+                const double per = std::ceil((double)L.n_pairs / c);
+                if (c == 1) return rounds(L.n_sets) * (per + kWgCost + kFinishCost);
+                return rounds((double)L.n_sets * c) * (per + kWgCost) + rounds(L.n_sets) * (kFinishCost + 0.3);
             };
             uint32_t best = 1;
-            double best_eff = eff(1) + 0.03;
+            double best_cost = cost(1);
             for (uint32_t c = 2; c <= std::min<uint32_t>(L.n_pairs, 4096); ++c) {
-                if ((double)L.n_sets * c > 16.0 * cus && c > 1 && eff(best) >= 0.9) break;
-                const double e = eff(c);
-                if (e > best_eff + 1e-9) { best = c; best_eff = e; }
+                const double e = cost(c);
+                if (e < best_cost - 1e-9) { best = c; best_cost = e; }
             }
             L.chunks = best;
         }
