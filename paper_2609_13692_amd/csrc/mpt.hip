@@ -488,12 +488,12 @@ __global__ __launch_bounds__(256) void k_dp_reduce(int m, int p, uint32_t n_sets
 // candidate's key is C'(A) + C'(B) + canon, where canon is the mask of the
 // part holding lowbit(S) (< 2^m). The smallest key is the smallest cost and,
 // among equal costs, the numerically smallest such part -- the documented
-// tie rule. Rows sit in LDS twice: plain (P = C') and tagged with their own
-// mask (T = C' + X), so a key is one add: T(A) + P(B) when A holds
-// lowbit(S), P(A) + T(B) otherwise. P is needed only at even low parts.
-// Keys are exact integers; when every key stays below 2^53 they are held
-// as doubles (one v_add_f64 and one v_min_f64 per candidate), otherwise
-// as uint64 (below 2^62); larger instances take the plain kernels.
+// tie rule. An entry is used plain (C') or tagged with its own mask (C' + X,
+// an OR, since C' leaves the low m bits zero), so a key is one add: tagged
+// A + plain B when A holds lowbit(S), plain A + tagged B otherwise. Keys are
+// exact integers held as doubles (one v_add_f64 and one v_min_f64 per
+// candidate) while sum_i w(R_i) < 2^(51-m), otherwise as uint64 (below
+// 2^62); larger instances take the plain kernels.
 namespace rb {
 #ifndef MPT_RB_L
 #define MPT_RB_L 12
@@ -660,58 +660,69 @@ static_assert(items_pair_up(kTItems), "cross-pair items must pair up their subma
 __constant__ ThreadItems c_titems = make_thread_items();
 
 
-// key arithmetic: exact integers as uint64 or as doubles (< 2^53)
+// Key arithmetic. A table entry carries the packed value v = C' or, tagged,
+// C' | X. In both representations tagging is an OR of a 32-bit value into
+// the entry's low 32 bits (m <= 30), so the cross-pair loop can tag an entry
+// it loaded plain with one 32-bit instruction.
+//   uint64: an entry is v itself; a key is the sum of two entries.
+//   double: an entry is the double 2^52 + 2v. Its exponent is fixed, so its
+//   low mantissa bits are the integer 2v and the tag is an OR of 2X. The sum
+//   of two entries is 2^53 + 2(v_A + v_B): even, so exact below 2^54, and
+//   its mantissa is the packed key v_A + v_B. That needs 2v < 2^52 for every
+//   entry, i.e. sum_i w(R_i) < 2^(51-m).
 template <class K> struct Key;
 template <> struct Key<uint64_t> {
-    static __device__ inline uint64_t plain(uint64_t c) { return c; }
-    static __device__ inline uint64_t tagged(uint64_t c, uint32_t idx) { return c + idx; }
+    static constexpr int SH = 0;                            // shift of a tag inside an entry
+    static __device__ inline uint64_t entry(uint64_t v) { return v; }
+    static __device__ inline uint64_t entry_value(uint64_t e) { return e; }
+    static __device__ inline uint64_t tagify(uint64_t e, uint32_t t) { return e | t; }
     static __device__ inline uint64_t add(uint64_t a, uint64_t b) { return a + b; }
     static __device__ inline uint64_t min(uint64_t a, uint64_t b) { return b < a ? b : a; }
     static __device__ inline uint64_t none() { return ~0ull; }
     static __device__ inline uint64_t bits(uint64_t k) { return k; }
     static __device__ inline uint64_t from_bits(uint64_t b) { return b; }
-    static __device__ inline uint64_t value_of_bits(uint64_t b) { return b; }
-    // the packed table in HBM holds C' in the key's own representation
-    static __device__ inline uint64_t store(uint64_t c) { return c; }
+    // key bits (as kept in the accumulators) -> packed key; ~0 for none
+    static __device__ inline uint64_t key_value(uint64_t b) { return b; }
+    // the packed table in HBM holds each entry's bits
+    static __device__ inline uint64_t store(uint64_t v) { return v; }
     static __device__ inline uint64_t stored_value(uint64_t b) { return b; }
-    static __device__ inline uint64_t load_plain(uint64_t b) { return b; }
-    static __device__ inline uint64_t load_tagged(uint64_t b, uint32_t idx) { return b + idx; }
+    static __device__ inline uint64_t load(uint64_t b) { return b; }
 };
 template <> struct Key<double> {
-    static __device__ inline double plain(uint64_t c) { return (double)c; }
-    static __device__ inline double tagged(uint64_t c, uint32_t idx) { return (double)(c + idx); }
+    static constexpr int SH = 1;
+    static constexpr uint64_t E52 = 0x4330000000000000ull;  // bits of 2^52
+    static constexpr uint64_t MANT = (1ull << 52) - 1u;
+    static __device__ inline uint64_t bits(double k) { return (uint64_t)__double_as_longlong(k); }
+    static __device__ inline double from_bits(uint64_t b) { return __longlong_as_double((long long)b); }
+    static __device__ inline double entry(uint64_t v) { return from_bits(E52 | (v << 1)); }
+    static __device__ inline uint64_t entry_value(double e) { return (bits(e) & MANT) >> 1; }
+    static __device__ inline double tagify(double e, uint32_t t) { return from_bits(bits(e) | t); }
     static __device__ inline double add(double a, double b) { return a + b; }
     static __device__ inline double min(double a, double b) { return fmin(a, b); }
     static __device__ inline double none() { return __builtin_inf(); }
-    // positive doubles order like their bit patterns
-    static __device__ inline uint64_t bits(double k) { return (uint64_t)__double_as_longlong(k); }
-    static __device__ inline double from_bits(uint64_t b) { return __longlong_as_double((long long)b); }
-    static __device__ inline uint64_t value_of_bits(uint64_t b) {
-        return b >= 0x7ff0000000000000ull ? ~0ull : (uint64_t)__longlong_as_double((long long)b);
-    }
-    static __device__ inline uint64_t store(uint64_t c) { return bits((double)c); }
-    static __device__ inline uint64_t stored_value(uint64_t b) { return (uint64_t)from_bits(b); }
-    static __device__ inline double load_plain(uint64_t b) { return from_bits(b); }
-    static __device__ inline double load_tagged(uint64_t b, uint32_t idx) { return from_bits(b) + (double)idx; }
+    // keys are positive doubles: they order like their bit patterns
+    static __device__ inline uint64_t key_value(uint64_t b) { return b >= 0x7ff0000000000000ull ? ~0ull : b & MANT; }
+    static __device__ inline uint64_t store(uint64_t v) { return E52 | (v << 1); }
+    static __device__ inline uint64_t stored_value(uint64_t b) { return (b & MANT) >> 1; }
+    static __device__ inline double load(uint64_t b) { return from_bits(b); }
 };
 
 // LDS rows. Block x2 sits at slot(x2) = x2 ^ (x2 >> 3 & 7) ^ (x2 >> 6 & 3)
 // (for R2 = 9; the last term takes the bits between 6 and E),
 // a GF(2)-linear bijection, so slot(S2 ^ A2) = slot(S2) ^ slot(A2); it maps
 // the low R2-1 middle bits onto themselves and the top one, E, onto NS2/2,
-// so slot(X | E) = slot(X) + NS2/2 for X below E. Blocks are padded by 16
-// bytes (tagged: NB entries, plain: the NE even entries) to an odd number of
-// 16-byte pieces: piece q of a block falls in the 16-byte bank group
-// (odd * slot + q) mod 16 (gfx950 serves a 16-byte read 16 lanes at a time
-// from 16 such groups), a bijection of slot mod 16, and a lane's 16-byte
-// reads of one block use immediate offsets.
-// Inside a tagged block entry x sits at position tpos(x) = (x - 1) mod NB,
-// so entries 1..NB-1 fill whole 16-byte pieces: half of the cross-pair
-// convolutions never read entry 0 of one of their tagged blocks, and those
-// loads then stay three 16-byte reads and one aligned 8-byte read.
-constexpr int TSTRIDE = NB + 2;       // K elements per tagged block
-constexpr int PSTRIDE = NE + 2;       // K elements per plain block
-constexpr int tpos(int x) { return (x + NB - 1) & (NB - 1); }
+// so slot(X | E) = slot(X) + NS2/2 for X below E. A block is its NB entries
+// padded by 16 bytes to an odd number of 16-byte pieces: piece q of a block
+// falls in the 16-byte bank group (5 * slot + q) mod 16 (gfx950 serves a
+// 16-byte read 16 lanes at a time from 16 such groups), a bijection of slot
+// mod 16, and a lane's 16-byte reads of one block use immediate offsets.
+// Inside a block the odd entries come first, tagged: an odd entry holds bit
+// 0, so in every candidate it is the part holding lowbit(S1). The even
+// entries follow, plain; where a candidate needs one tagged, the tag is
+// ORed in registers.
+constexpr int BSTRIDE = NB + 2;       // K elements per block
+constexpr int mpos(int x) { return (x & 1) ? (x >> 1) : NE + (x >> 1); }   // position of entry x
+constexpr int ment(int j) { return j < NE ? 2 * j + 1 : 2 * (j - NE); }     // entry at position j
 __host__ __device__ constexpr uint32_t slot_of(uint32_t x2) {
     return x2 ^ ((x2 >> 3) & 7u) ^ ((x2 >> 6) & ((1u << (R2 - 7)) - 1u));
 }
@@ -728,10 +739,8 @@ constexpr bool slots_ok() {
 static_assert(R2 >= 7 && slots_ok(), "slot_of is a bijection that puts the E half NS2/2 above the rest");
 
 template <class K> struct alignas(16) Lds {
-    K pa[NS2 * PSTRIDE];   // row on the A side, plain, even low parts
-    K ta[NS2 * TSTRIDE];   // row on the A side, tagged
-    K pb[NS2 * PSTRIDE];   // row on the B side, plain, even low parts
-    K tb[NS2 * TSTRIDE];   // row on the B side, tagged
+    K ra[NS2 * BSTRIDE];   // row on the A side
+    K rb[NS2 * BSTRIDE];   // row on the B side
     uint64_t acc[ROW];     // best key bits per entry of the output row
 };
 static_assert(sizeof(Lds<double>) <= 160 * 1024, "rows and accumulators fit one CU's LDS");
@@ -742,51 +751,41 @@ template <class K> struct Vec2;
 template <> struct Vec2<uint64_t> { using type = ulonglong2; };
 template <> struct Vec2<double> { using type = double2; };
 
+// block at slot -> v[x] = entry x (odd tagged, even plain)
 template <class K>
-__device__ inline void load_t(const K *row, uint32_t slot, K v[NB]) {
-    using V = typename Vec2<K>::type;
-    const V *p = reinterpret_cast<const V *>(row + slot * TSTRIDE);
+__device__ inline void load_blk(const K *row, uint32_t slot, K v[NB]) {
+    // each 16-byte piece is read as one 128-bit integer: a vector of two
+    // keys whose lanes are used apart gets split into 8-byte reads
+    const __uint128_t *p = reinterpret_cast<const __uint128_t *>(row + slot * BSTRIDE);
 #pragma unroll
-    for (int q = 0; q < NB / 2; ++q) {                // positions 2q, 2q+1
-        const V t = p[q];
-        v[(2 * q + 1) & (NB - 1)] = t.x;
-        v[(2 * q + 2) & (NB - 1)] = t.y;
+    for (int q = 0; q < NB / 2; ++q) {
+        const __uint128_t t = p[q];
+        v[ment(2 * q)] = Key<K>::from_bits((uint64_t)t);
+        v[ment(2 * q + 1)] = Key<K>::from_bits((uint64_t)(t >> 64));
     }
 }
 
+// global 16-byte piece g of row xh (entries 2g, 2g+1 of the row) -> LDS row
 template <class K>
-__device__ inline void load_p(const K *row, uint32_t slot, K v[NE]) {
-    using V = typename Vec2<K>::type;
-    const V *p = reinterpret_cast<const V *>(row + slot * PSTRIDE);
-#pragma unroll
-    for (int q = 0; q < NE / 2; ++q) {
-        const V t = p[q];
-        v[2 * q] = t.x;
-        v[2 * q + 1] = t.y;
-    }
+__device__ inline void put_piece(K *R, uint32_t xh, int g, ulonglong2 v) {
+    const int x2 = g / (NB / 2), q = g % (NB / 2);       // entries 2q, 2q+1 of block x2
+    const uint32_t idx = (xh << L) | (uint32_t)(2 * g + 1);
+    K *blk = R + slot_of((uint32_t)x2) * BSTRIDE;
+    blk[mpos(2 * q)] = Key<K>::load(v.x);
+    blk[mpos(2 * q + 1)] = Key<K>::tagify(Key<K>::load(v.y), idx << Key<K>::SH);
 }
 
-// row X_H of the packed table (global) -> plain and tagged LDS copies
+// row X_H of the packed table (global) -> LDS row
 template <class K>
-__device__ inline void load_row(K *P, K *Tt, const uint64_t *__restrict__ C, uint32_t xh) {
+__device__ inline void load_row(K *R, const uint64_t *__restrict__ C, uint32_t xh) {
     const ulonglong2 *src = reinterpret_cast<const ulonglong2 *>(C + ((size_t)xh << L));
-    const uint32_t tag = xh << L;
-    for (int g = threadIdx.x; g < ROW / 2; g += THREADS) {
-        const int x2 = g / (NB / 2), q = g % (NB / 2);     // entries 2q, 2q+1 of block x2
-        const ulonglong2 v = src[g];
-        const uint32_t idx = tag | (uint32_t)(2 * g);
-        const uint32_t sl = slot_of((uint32_t)x2);
-        Tt[sl * TSTRIDE + tpos(2 * q)] = Key<K>::load_tagged(v.x, idx);
-        Tt[sl * TSTRIDE + tpos(2 * q + 1)] = Key<K>::load_tagged(v.y, idx + 1u);
-        P[sl * PSTRIDE + q] = Key<K>::load_plain(v.x);
-    }
+    for (int g = threadIdx.x; g < ROW / 2; g += THREADS) put_piece<K>(R, xh, g, src[g]);
 }
 
-// rows xa and xb into (Pa, Ta) and (Pb, Tb): every thread's global loads
-// of both rows are issued together, then written to LDS
+// rows xa and xb into Ra and Rb: every thread's global loads of both rows
+// are issued together, then written to LDS
 template <class K>
-__device__ inline void load_rows2(K *Pa, K *Ta, K *Pb, K *Tb, const uint64_t *__restrict__ C, uint32_t xa,
-                                  uint32_t xb) {
+__device__ inline void load_rows2(K *Ra, K *Rb, const uint64_t *__restrict__ C, uint32_t xa, uint32_t xb) {
     constexpr int PER = ROW / 2 / THREADS;           // 16-byte pieces per thread and row
     static_assert(PER * THREADS == ROW / 2, "threads divide the row");
     const ulonglong2 *srca = reinterpret_cast<const ulonglong2 *>(C + ((size_t)xa << L));
@@ -799,16 +798,8 @@ __device__ inline void load_rows2(K *Pa, K *Ta, K *Pb, K *Tb, const uint64_t *__
     }
 #pragma unroll
     for (int p = 0; p < PER; ++p) {
-        const int g = threadIdx.x + p * THREADS;
-        const int x2 = g / (NB / 2), q = g % (NB / 2);   // entries 2q, 2q+1 of block x2
-        const uint32_t sl = slot_of((uint32_t)x2);
-        const uint32_t ia = (xa << L) | (uint32_t)(2 * g), ib = (xb << L) | (uint32_t)(2 * g);
-        Ta[sl * TSTRIDE + tpos(2 * q)] = Key<K>::load_tagged(va[p].x, ia);
-        Ta[sl * TSTRIDE + tpos(2 * q + 1)] = Key<K>::load_tagged(va[p].y, ia + 1u);
-        Pa[sl * PSTRIDE + q] = Key<K>::load_plain(va[p].x);
-        Tb[sl * TSTRIDE + tpos(2 * q)] = Key<K>::load_tagged(vb[p].x, ib);
-        Tb[sl * TSTRIDE + tpos(2 * q + 1)] = Key<K>::load_tagged(vb[p].y, ib + 1u);
-        Pb[sl * PSTRIDE + q] = Key<K>::load_plain(vb[p].x);
+        put_piece<K>(Ra, xa, threadIdx.x + p * THREADS, va[p]);
+        put_piece<K>(Rb, xb, threadIdx.x + p * THREADS, vb[p]);
     }
 }
 
@@ -824,15 +815,19 @@ __device__ inline uint32_t deposit(uint32_t t, uint32_t mask) {
     return r;
 }
 
-// CB-bit min-plus subset convolution of one block pair:
-//   best[S1] = min(best[S1], min over A1 in S1 of key(A1, S1 ^ A1)).
-// A side holds lowbit(S1) -> T(A) + P(B); otherwise P(A) + T(B). Either
-// way the plain operand has an even low part. For S1 = 0 the side is
-// orient_a.
-template <class K>
-__device__ inline void conv_block(const K pa[NE], const K ta[NB], const K pb[NE], const K tb[NB], bool orient_a,
-                                  K best[NB]) {
-    best[0] = Key<K>::min(best[0], orient_a ? Key<K>::add(ta[0], pb[0]) : Key<K>::add(pa[0], tb[0]));
+// CB-bit min-plus subset convolution of one block pair, entries a[] (A
+// side) and b[] (B side):
+//   best[S1] = min(best[S1], min over A1 in S1 of a[A1] + b[S1 ^ A1]),
+// where the operand holding lowbit(S1) must be tagged and the other plain.
+// Odd entries are loaded tagged and always play the tagged part. An even
+// entry x > 0 plays the plain part only in candidates whose tagged operand
+// is odd or, for x = 4, entry 2; so the candidates run in classes by their
+// tagged operand -- odd, 2, 4, 6 -- and the caller tags entry x of its
+// blocks in place just before class x. S1 = 0 (its tagged side set by the
+// orientation) comes last.
+static_assert(CB == 3, "the class order below is worked out for 3-bit blocks");
+template <class K, int CLS>
+__device__ inline void conv_class(const K a[NB], const K b[NB], K best[NB]) {
 #pragma unroll
     for (int s1 = 1; s1 < NB; ++s1) {
         const int low = s1 & -s1;
@@ -840,10 +835,33 @@ __device__ inline void conv_block(const K pa[NE], const K ta[NB], const K pb[NE]
         for (int a1 = 0; a1 < NB; ++a1) {
             if (a1 & ~s1) continue;
             const int b1 = s1 ^ a1;
-            const K c = (a1 & low) ? Key<K>::add(ta[a1], pb[b1 >> 1]) : Key<K>::add(pa[a1 >> 1], tb[b1]);
-            best[s1] = Key<K>::min(best[s1], c);
+            const int t = (a1 & low) ? a1 : b1;          // the tagged operand
+            if (((t & 1) ? 1 : t) != CLS) continue;
+            best[s1] = Key<K>::min(best[s1], Key<K>::add(a[a1], b[b1]));
         }
     }
+}
+
+// tag entry X of a block whose entry 0 has mask tag0 (tags pre-shifted)
+template <class K, int X>
+__device__ inline void tag_entry(K v[NB], uint32_t tag0) {
+    v[X] = Key<K>::tagify(v[X], tag0 | ((uint32_t)X << Key<K>::SH));
+}
+
+// the whole convolution of one block pair; ta, tb: shifted masks of entry 0
+// of the two blocks; orient_a: the A side holds lowbit(S) for S1 = 0
+template <class K>
+__device__ inline void conv_pair(K a[NB], K b[NB], uint32_t ta, uint32_t tb, bool orient_a, K best[NB]) {
+    conv_class<K, 1>(a, b, best);
+    tag_entry<K, 2>(a, ta); tag_entry<K, 2>(b, tb);
+    conv_class<K, 2>(a, b, best);
+    tag_entry<K, 4>(a, ta); tag_entry<K, 4>(b, tb);
+    conv_class<K, 4>(a, b, best);
+    tag_entry<K, 6>(a, ta); tag_entry<K, 6>(b, tb);
+    conv_class<K, 6>(a, b, best);
+    const K a0 = orient_a ? Key<K>::tagify(a[0], ta) : a[0];
+    const K b0 = orient_a ? b[0] : Key<K>::tagify(b[0], tb);
+    best[0] = Key<K>::min(best[0], Key<K>::add(a0, b0));
 }
 
 template <class K>
@@ -882,10 +900,11 @@ __device__ inline void flush_group(const K best[NB], uint32_t s2, uint32_t seg, 
 
 // one self-pair work item (S2, first A2, t) against (rowS, row0): 2^t
 // submasks A2 of S2 in increasing order, skipping A2 == S2 and, when
-// skip_empty, A2 == 0
+// skip_empty, A2 == 0. tag_h: the shifted mask of row S_H's entry 0.
 template <class K>
-__device__ inline void run_item(uint32_t item, const K *pA, const K *tA, const K *pB, const K *tB, uint64_t *acc,
+__device__ inline void run_item(uint32_t item, const K *rA, const K *rB, uint32_t tag_h, uint64_t *acc,
                                 bool skip_empty) {
+    constexpr int SH = Key<K>::SH;
     const uint32_t s2 = item & 0xffffu;
     const int k = __popc(s2);
     const int tb = (int)((item >> 28) & 7u);
@@ -900,12 +919,10 @@ __device__ inline void run_item(uint32_t item, const K *pA, const K *tA, const K
         const uint32_t b2 = s2 ^ a2;
         if (b2 != 0 && !(skip_empty && a2 == 0)) {
             const uint32_t sa = slot_of(a2), sb = slot_s2 ^ sa;
-            K pa[NE], ta[NB], pb[NE], tb2[NB];
-            load_p(pA, sa, pa);
-            load_t(tA, sa, ta);
-            load_p(pB, sb, pb);
-            load_t(tB, sb, tb2);
-            conv_block<K>(pa, ta, pb, tb2, (s2 == 0) || (a2 & low2), best);
+            K a[NB], b[NB];
+            load_blk(rA, sa, a);
+            load_blk(rB, sb, b);
+            conv_pair<K>(a, b, tag_h | (a2 << (CB + SH)), b2 << (CB + SH), (s2 == 0) || (a2 & low2), best);
         }
         a2 = ((a2 | ~s2) + 1u) & s2;
     }
@@ -913,18 +930,11 @@ __device__ inline void run_item(uint32_t item, const K *pA, const K *tA, const K
     flush_group<K>(best, s2, chunks < 8u ? chunks : 8u, acc);
 }
 
-// plain C' of an entry of a tagged LDS row whose tag is the entry's own
-// mask (exact: the tag occupies the low m bits that C' leaves zero)
-template <class K>
-__device__ inline uint64_t untag(K t, uint32_t idx) {
-    return Key<K>::value_of_bits(Key<K>::bits(t)) - idx;
-}
-
 // Complete row S_H. s.acc holds the best cross-pair key bits (or ~0);
-// (pS, tS) receive row S_H, (s.pb, s.tb) hold row 0 -- the same buffers
-// when S_H = 0, in which case they are filled here. Writes C' and split.
+// rS receives row S_H, s.rb holds row 0 -- the same buffer when S_H = 0, in
+// which case it is filled here. Writes C' and split.
 template <class K>
-__device__ __attribute__((always_inline)) inline void finalize_row(int m, uint32_t sh, Lds<K> &s, K *pS, K *tS,
+__device__ __attribute__((always_inline)) inline void finalize_row(int m, uint32_t sh, Lds<K> &s, K *rS,
                                                                    const int64_t *__restrict__ W,
                                                                    uint64_t *__restrict__ Cp,
                                                                    uint32_t *__restrict__ split) {
@@ -953,7 +963,7 @@ __device__ __attribute__((always_inline)) inline void finalize_row(int m, uint32
         }
         // A2 a proper submask of S2 (for S_H = 0 also non-empty: those pairs
         // mirror the in-block pairs below)
-        if (item) run_item<K>(item, pS, tS, s.pb, s.tb, s.acc, sh == 0);
+        if (item) run_item<K>(item, rS, s.rb, a_hi << Key<K>::SH, s.acc, sh == 0);
         lds_barrier();
         // A2 = S2: in-block pairs, one thread per block of this level
         if (blk) {
@@ -965,7 +975,8 @@ __device__ __attribute__((always_inline)) inline void finalize_row(int m, uint32
             const bool self0 = sh == 0 && s2 == 0;
             uint64_t b0[NB];
 #pragma unroll
-            for (int x = 0; x < NB; ++x) b0[x] = self0 ? 0u : untag<K>(s.tb[tpos(x)], (uint32_t)x);
+            for (int x = 0; x < NB; ++x)
+                b0[x] = self0 ? 0u : Key<K>::entry_value(s.rb[mpos(x)]) - (uint64_t)(x & 1 ? x : 0);
             uint64_t out[NB];
             uint32_t sp[NB];
             // S1 in order of popcount so that every A1 < S1 is ready
@@ -983,7 +994,7 @@ __device__ __attribute__((always_inline)) inline void finalize_row(int m, uint32
                         b0[s1] = self0 ? out[s1] : b0[s1];
                         continue;
                     }
-                    uint64_t kb = Key<K>::value_of_bits(s.acc[(s2 << CB) | s1]);
+                    uint64_t kb = Key<K>::key_value(s.acc[(s2 << CB) | s1]);
                     const int low = s1 & -s1;
 #pragma unroll
                     for (int a1 = 0; a1 < NB; ++a1) {
@@ -1002,9 +1013,10 @@ __device__ __attribute__((always_inline)) inline void finalize_row(int m, uint32
             const uint32_t sl = slot_of(s2);
 #pragma unroll
             for (int x = 0; x < NB; ++x) {
-                tS[sl * TSTRIDE + tpos(x)] = Key<K>::tagged(out[x], base | (uint32_t)x);
-                if (!(x & 1)) pS[sl * PSTRIDE + (x >> 1)] = Key<K>::plain(out[x]);
-                Cp[base + x] = Key<K>::store(out[x]);
+                // C'(empty set) = 0 in the table (the unpacked C[0] is the sentinel)
+                const uint64_t v = (base | (uint32_t)x) == 0 ? 0u : out[x];
+                rS[sl * BSTRIDE + mpos(x)] = Key<K>::entry(x & 1 ? v | base | (uint32_t)x : v);
+                Cp[base + x] = Key<K>::store(v);
                 split[base + x] = sp[x];
             }
         }
@@ -1015,13 +1027,20 @@ __device__ __attribute__((always_inline)) inline void finalize_row(int m, uint32
 }
 
 // one base step (S2', A2') of the lifted cross-pair loop: three block
-// convolutions from four block loads. o1 orients S1 = 0 of (S2'|E, A2'),
-// o0 that of (S2', A2') and (S2'|E, A2'|E). The blocks with E sit NS2/2
-// slots above those without, a constant offset.
-template <class K>
+// convolutions from four block loads. O1 orients S1 = 0 of (S2'|E, A2'),
+// O0 that of (S2', A2') and (S2'|E, A2'|E). The blocks with E sit NS2/2
+// slots above those without, a constant offset. tag_a, tag_bs: shifted
+// masks of entry 0 of block 0 of row A_H and of block S2' of row B_H. Each
+// even entry is tagged in place once, for all three convolutions, before
+// the class that first needs it tagged.
+template <class K, bool O1, bool O0>
 __device__ __attribute__((always_inline)) inline void cross_step(const Lds<K> &s, uint32_t a2, uint32_t slot_s2,
-                                                                 bool o1, bool o0, K best0[NB], K best1[NB]) {
+                                                                 uint32_t tag_a, uint32_t tag_bs, K best0[NB],
+                                                                 K best1[NB]) {
+    static_assert(O0 || !O1, "block A2' is used plain for S1 = 0 after it is tagged");
     constexpr uint32_t HALF = NS2 / 2;
+    constexpr int SH = Key<K>::SH;
+    constexpr uint32_t TE = HALF << (CB + SH);            // shifted mask of E
     uint32_t sa0 = slot_of(a2), sb0 = slot_s2 ^ sa0;
     // slots of blocks without E are below HALF; masking values the compiler
     // cannot see through lets instruction selection use 24-bit multiply-adds
@@ -1029,21 +1048,42 @@ __device__ __attribute__((always_inline)) inline void cross_step(const Lds<K> &s
     asm("" : "+v"(sa0), "+v"(sb0));
     sa0 &= HALF - 1;
     sb0 &= HALF - 1;
-    K pa[NE], ta[NB], pb[NE], tb2[NB];
-    // (S2'|E, A2'): A block A2', B block B2'|E
-    load_p(s.pa, sa0, pa);
-    load_t(s.ta, sa0, ta);
-    load_p(s.pb + HALF * PSTRIDE, sb0, pb);
-    load_t(s.tb + HALF * TSTRIDE, sb0, tb2);
-    conv_block<K>(pa, ta, pb, tb2, o1, best1);
-    // (S2', A2'): A block A2', B block B2'
-    load_p(s.pb, sb0, pb);
-    load_t(s.tb, sb0, tb2);
-    conv_block<K>(pa, ta, pb, tb2, o0, best0);
-    // (S2'|E, A2'|E): A block A2'|E, B block B2'
-    load_p(s.pa + HALF * PSTRIDE, sa0, pa);
-    load_t(s.ta + HALF * TSTRIDE, sa0, ta);
-    conv_block<K>(pa, ta, pb, tb2, o0, best1);
+    const uint32_t ta = tag_a | (a2 << (CB + SH));        // block A2'
+    const uint32_t tb = tag_bs - (a2 << (CB + SH));       // block B2' = S2' ^ A2'
+    K a0[NB], a1[NB], b0[NB], b1[NB];
+    load_blk(s.ra, sa0, a0);                              // A2'
+    load_blk(s.rb + HALF * BSTRIDE, sb0, b1);             // B2'|E
+    load_blk(s.rb, sb0, b0);                              // B2'
+    load_blk(s.ra + HALF * BSTRIDE, sa0, a1);             // A2'|E
+    // (S2'|E, A2') -> best1, (S2', A2') -> best0, (S2'|E, A2'|E) -> best1
+    conv_class<K, 1>(a0, b1, best1);
+    conv_class<K, 1>(a0, b0, best0);
+    conv_class<K, 1>(a1, b0, best1);
+    tag_entry<K, 2>(a0, ta); tag_entry<K, 2>(a1, ta | TE); tag_entry<K, 2>(b0, tb); tag_entry<K, 2>(b1, tb | TE);
+    conv_class<K, 2>(a0, b1, best1);
+    conv_class<K, 2>(a0, b0, best0);
+    conv_class<K, 2>(a1, b0, best1);
+    tag_entry<K, 4>(a0, ta); tag_entry<K, 4>(a1, ta | TE); tag_entry<K, 4>(b0, tb); tag_entry<K, 4>(b1, tb | TE);
+    conv_class<K, 4>(a0, b1, best1);
+    conv_class<K, 4>(a0, b0, best0);
+    conv_class<K, 4>(a1, b0, best1);
+    tag_entry<K, 6>(a0, ta); tag_entry<K, 6>(a1, ta | TE); tag_entry<K, 6>(b0, tb); tag_entry<K, 6>(b1, tb | TE);
+    conv_class<K, 6>(a0, b1, best1);
+    conv_class<K, 6>(a0, b0, best0);
+    conv_class<K, 6>(a1, b0, best1);
+    // S1 = 0
+    if (O1) tag_entry<K, 0>(a0, ta);
+    else tag_entry<K, 0>(b1, tb | TE);
+    best1[0] = Key<K>::min(best1[0], Key<K>::add(a0[0], b1[0]));
+    if (O0) {
+        if (!O1) tag_entry<K, 0>(a0, ta);
+        tag_entry<K, 0>(a1, ta | TE);
+    } else {
+        tag_entry<K, 0>(b0, tb);
+    }
+    best0[0] = Key<K>::min(best0[0], Key<K>::add(a0[0], b0[0]));
+    best1[0] = Key<K>::min(best1[0], Key<K>::add(a1[0], b0[0]));
+    __builtin_amdgcn_sched_barrier(0);
 }
 
 // cross pairs of one (S_H, chunk); fused = finish the row in place
@@ -1077,21 +1117,23 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
     for (uint32_t t = t0; t < t1; ++t) {
         const uint32_t bh = sh ^ ah;
         lds_barrier();
-        load_rows2<K>(s.pa, s.ta, s.pb, s.tb, Cp, ah, bh);
+        load_rows2<K>(s.ra, s.rb, Cp, ah, bh);
         lds_barrier();
+        const uint32_t tag_a = ah << (L + Key<K>::SH);
+        const uint32_t tag_bs = ((bh << L) | (s2 << CB)) << Key<K>::SH;
         ah = lowh | (((ah | ~rest) + 1u) & rest);    // next A_H holding lowbit(S_H)
         if (has_item) {
             if (s2 == 0) {
-                cross_step<K>(s, 0u, slot_s2, false, true, best0, best1);
+                cross_step<K, false, true>(s, 0u, slot_s2, tag_a, tag_bs, best0, best1);
             } else {
                 // t-th submask of S2' holds lowbit(S2') iff t is odd, and every
                 // item starts at an even t with an even count: the orientation
                 // of each step is fixed at compile time
                 uint32_t a2 = a2_first;
                 for (uint32_t i = 0; i < cnt; i += 2) {
-                    cross_step<K>(s, a2, slot_s2, false, false, best0, best1);
+                    cross_step<K, false, false>(s, a2, slot_s2, tag_a, tag_bs, best0, best1);
                     a2 = ((a2 | ~s2) + 1u) & s2;
-                    cross_step<K>(s, a2, slot_s2, true, true, best0, best1);
+                    cross_step<K, true, true>(s, a2, slot_s2, tag_a, tag_bs, best0, best1);
                     a2 = ((a2 | ~s2) + 1u) & s2;
                 }
             }
@@ -1103,9 +1145,9 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
     }
     lds_barrier();
     if (fused) {
-        load_row<K>(s.pb, s.tb, Cp, 0u);
+        load_row<K>(s.rb, Cp, 0u);
         lds_barrier();
-        finalize_row<K>(m, sh, s, s.pa, s.ta, W, Cp, split);
+        finalize_row<K>(m, sh, s, s.ra, W, Cp, split);
     } else {
         uint64_t *dst = partial + (size_t)bid * ROW;
         for (int e = threadIdx.x; e < ROW; e += THREADS) dst[e] = s.acc[e];
@@ -1142,10 +1184,10 @@ __global__ __launch_bounds__(THREADS) void k_rb_final(int m, int h, uint32_t chu
     const uint32_t sh = unrank_colex(r, h, m - L);
     const uint64_t *src = partial + (size_t)r * chunks * ROW;
     for (int e = threadIdx.x; e < ROW; e += THREADS) s.acc[e] = chunks ? src[e] : ~0ull;
-    if (sh != 0) load_row<K>(s.pb, s.tb, Cp, 0u);
+    if (sh != 0) load_row<K>(s.rb, Cp, 0u);
     lds_barrier();
     // for S_H = 0 the output row is row 0 itself
-    finalize_row<K>(m, sh, s, sh == 0 ? s.pb : s.pa, sh == 0 ? s.tb : s.ta, W, Cp, split);
+    finalize_row<K>(m, sh, s, sh == 0 ? s.rb : s.ra, W, Cp, split);
 }
 
 // packed C' -> C (C[0] keeps the documented sentinel)
@@ -1523,13 +1565,13 @@ extern "C" int mpt_solve_exact(int m, const int64_t *W, int64_t *C, uint32_t *sp
         int64_t total = 0;
         MPT_HIP_TRY(hipMemcpyAsync(&total, &h->pad[0], sizeof total, hipMemcpyDeviceToHost, s));
         MPT_HIP_TRY(hipStreamSynchronize(s));
-        // keys below 2^53 are exact doubles; below 2^62 they fit uint64
+        // doubles while 2 C' < 2^52 (Key<double>); below 2^62 keys fit uint64
         if (total < ((int64_t)1 << (61 - m))) {
             uint64_t *part = (uint64_t *)(ws + L.rb_part);
 #ifndef MPT_RB_NO_DOUBLE
 #define MPT_RB_NO_DOUBLE 0
 #endif
-            rc = (!MPT_RB_NO_DOUBLE && total < ((int64_t)1 << (52 - m))) ? solve_rb<double>(m, W, C, split, part, s)
+            rc = (!MPT_RB_NO_DOUBLE && total < ((int64_t)1 << (51 - m))) ? solve_rb<double>(m, W, C, split, part, s)
                                                    : solve_rb<uint64_t>(m, W, C, split, part, s);
             if (rc) return rc;
             if (opt_cost) {

@@ -207,6 +207,34 @@ def test_large_weights():
     assert_same(inst, got, oracle.solve(inst))
 
 
+@pytest.mark.parametrize("excess", [-1, 0])
+def test_double_keys_at_their_limit(excess):
+    """Costs are packed into doubles while sum_i w(R_i) < 2^(51-m) and into
+    uint64 from there on. Private chunks (weights <= 2^32, spread over the
+    requests) set the total to 2^(51-m) + excess, so the largest keys either
+    path ever holds are exercised (m = 14, row-blocked kernels)."""
+    m = 14
+    rng = np.random.default_rng(31 + excess)
+    n = 300
+    target = (1 << (51 - m)) + excess
+    w = list(rng.integers(1 << 26, 1 << 28, size=n, dtype=np.int64))
+    sets = [rng.choice(n, size=int(rng.integers(10, 40)), replace=False).tolist() for _ in range(m)]
+    left = target - int(sum(sum(w[x] for x in s) for s in sets))
+    assert left > 0
+    i = 0
+    while left > 0:
+        piece = min(left, (1 << 32) - int(rng.integers(0, 1 << 20)))
+        w.append(piece)
+        sets[i % m].append(len(w) - 1)
+        left -= piece
+        i += 1
+    w = np.array(w, dtype=np.int64)
+    inst = wl.from_sets(sets, w, len(w))
+    assert int(sum(w[s].sum() for s in sets)) == target
+    got = gpu_run(inst)
+    assert_same(inst, got, oracle.solve(inst))
+
+
 def test_costs_too_large_to_pack_take_the_plain_kernels():
     """With sum_i w(R_i) >= 2^(61-m) the packed-key kernels are not used;
     the result must not change."""
