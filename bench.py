@@ -49,7 +49,9 @@ WORKLOADS = {
 def profiled_traffic(label: str):
     """HBM bytes per launch of the kernel `label` from the committed
     rocprofv3 summaries (FETCH_SIZE + WRITE_SIZE, calibrated against a plain
-    copy), or None when no summary was taken from the current kernel source."""
+    copy), with the L2 hit rate and VALU issue fraction the same summary
+    records, or None when no summary was taken from the current kernel
+    source."""
     import glob
     import hashlib
     import re
@@ -69,6 +71,7 @@ def profiled_traffic(label: str):
         for name, k in data.get("kernels", {}).items():
             if re.search(r"\bk_" + re.escape(label) + r"\b", name):
                 return {"bytes_per_launch": k["traffic_bytes_per_launch"],
+                        "l2_hit_rate": k.get("l2_hit_rate"), "valu_issue_frac": k.get("valu_issue_frac"),
                         "summary": os.path.relpath(path, ROOT)}
     return None
 
@@ -363,6 +366,11 @@ def main() -> int:
                      "traffic": round(traffic["bytes_per_launch"]) if traffic else None,
                      "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
                      "traffic_source": traffic["summary"] if traffic else None,
+                     # from the same summary: TCC_HIT / (TCC_HIT + TCC_MISS), and the share of
+                     # the SIMDs' VALU issue cycles at 2.4 GHz that the kernel's instructions use
+                     "l2_hit_rate": round(traffic["l2_hit_rate"], 4) if traffic and traffic["l2_hit_rate"] else None,
+                     "valu_issue_frac": (round(traffic["valu_issue_frac"], 4)
+                                         if traffic and traffic["valu_issue_frac"] else None),
                      "avg_launch_ms": round(d["total_ms"] / d["launches"], 4),
                      "ops_per_launch": d["work"] * DP_OPS_PER_PAIR / d["launches"]},
         "zeta": zeta,
