@@ -353,6 +353,7 @@ def main() -> int:
         "data": "synthetic",
         "config": {"workload": WORKLOADS[args.config], "m": m, "n_chunks": inst.n_chunks, "nnz": inst.nnz,
                    "instance_sha256": inst.sha256()[:16]},
+        "instance_stats": {k: (round(v, 4) if isinstance(v, float) else v) for k, v in inst.stats().items()},
         "opt": opt,
         "parity_opt_matches_oracle_golden": (opt == golden_opt) if golden_opt is not None else None,
         "transitions_3m_equiv_per_s": 3 ** m / (ms / 1000.0),
