@@ -20,6 +20,7 @@
 #include <cstring>
 #include <mutex>
 #include <string>
+#include <type_traits>
 #include <vector>
 
 #include "bitonic.h"
@@ -707,22 +708,30 @@ template <> struct Key<double> {
     static __device__ inline double load(uint64_t b) { return from_bits(b); }
 };
 
-// LDS rows. Block x2 sits at slot(x2) = x2 ^ (x2 >> 3 & 7) ^ (x2 >> 6 & 3)
-// (for R2 = 9; the last term takes the bits between 6 and E),
-// a GF(2)-linear bijection, so slot(S2 ^ A2) = slot(S2) ^ slot(A2); it maps
-// the low R2-1 middle bits onto themselves and the top one, E, onto NS2/2,
-// so slot(X | E) = slot(X) + NS2/2 for X below E. A block is its NB entries
-// padded by 16 bytes to an odd number of 16-byte pieces: piece q of a block
-// falls in the 16-byte bank group (5 * slot + q) mod 16 (gfx950 serves a
-// 16-byte read 16 lanes at a time from 16 such groups), a bijection of slot
-// mod 16, and a lane's 16-byte reads of one block use immediate offsets.
+// Rows, in HBM and in LDS alike. Block x2 (the NB entries sharing the
+// middle mask x2) sits at slot(x2) = x2 ^ (x2 >> 3 & 7) ^ (x2 >> 6 & 3)
+// (for R2 = 9; the last term takes the bits between 6 and E), a GF(2)-linear
+// involution, so slot(S2 ^ A2) = slot(S2) ^ slot(A2); it maps the low R2-1
+// middle bits onto themselves and the top one, E, onto NS2/2, so
+// slot(X | E) = slot(X) + NS2/2 for X below E.
 // Inside a block the odd entries come first, tagged: an odd entry holds bit
 // 0, so in every candidate it is the part holding lowbit(S1). The even
 // entries follow, plain; where a candidate needs one tagged, the tag is
-// ORed in registers.
-constexpr int BSTRIDE = NB + 2;       // K elements per block
+// ORed in registers. A row is stored as NB/2 planes of 16-byte pieces:
+// plane q holds positions 2q and 2q+1 of every block, block at slot s in
+// piece s. A lane's four reads of one block are then 8 KiB apart
+// (immediate offsets), and a 16-lane pass of reads is free of bank
+// conflicts when its lanes' slots differ mod 16 (gfx950 serves a 16-byte
+// read 16 lanes at a time from 16 groups of 16 bytes; a plane is a
+// multiple of 256 bytes). Because HBM holds the rows in this same layout,
+// a row reaches LDS as a plain copy, straight from global memory.
+constexpr int PLANE = 2 * NS2;        // K elements per plane
 constexpr int mpos(int x) { return (x & 1) ? (x >> 1) : NE + (x >> 1); }   // position of entry x
 constexpr int ment(int j) { return j < NE ? 2 * j + 1 : 2 * (j - NE); }     // entry at position j
+// element index inside a row of the entry at position pos of the block at slot
+__host__ __device__ constexpr uint32_t lpos(uint32_t slot, int pos) {
+    return (uint32_t)(pos >> 1) * PLANE + slot * 2u + (uint32_t)(pos & 1);
+}
 __host__ __device__ constexpr uint32_t slot_of(uint32_t x2) {
     return x2 ^ ((x2 >> 3) & 7u) ^ ((x2 >> 6) & ((1u << (R2 - 7)) - 1u));
 }
@@ -730,78 +739,56 @@ constexpr bool slots_ok() {
     bool seen[NS2] = {};
     for (uint32_t x = 0; x < (uint32_t)NS2; ++x) {
         const uint32_t sl = slot_of(x);
-        if (sl >= (uint32_t)NS2 || seen[sl]) return false;
+        if (sl >= (uint32_t)NS2 || seen[sl] || slot_of(sl) != x) return false;
         seen[sl] = true;
         if (x < (uint32_t)NS2 / 2 && (sl >= (uint32_t)NS2 / 2 || slot_of(x | NS2 / 2) != sl + NS2 / 2)) return false;
     }
     return true;
 }
-static_assert(R2 >= 7 && slots_ok(), "slot_of is a bijection that puts the E half NS2/2 above the rest");
+static_assert(R2 >= 7 && slots_ok(), "slot_of is an involution that puts the E half NS2/2 above the rest");
+static_assert(NB == 8 && (PLANE * 8) % 256 == 0, "four planes of 16-byte pieces, each a multiple of 256 bytes");
 
+// two buffers of the (A, B) row pair: the next pair's rows are copied in
+// while the current pair runs
 template <class K> struct alignas(16) Lds {
-    K ra[NS2 * BSTRIDE];   // row on the A side
-    K rb[NS2 * BSTRIDE];   // row on the B side
+    K r[2][2][ROW];        // [buffer][A side, B side]
     uint64_t acc[ROW];     // best key bits per entry of the output row
 };
 static_assert(sizeof(Lds<double>) <= 160 * 1024, "rows and accumulators fit one CU's LDS");
 // workgroups that run on one CU at a time (their LDS takes the CU)
 constexpr int WGS_PER_CU = (int)((160 * 1024) / sizeof(Lds<double>));
 
-template <class K> struct Vec2;
-template <> struct Vec2<uint64_t> { using type = ulonglong2; };
-template <> struct Vec2<double> { using type = double2; };
-
 // block at slot -> v[x] = entry x (odd tagged, even plain)
 template <class K>
 __device__ inline void load_blk(const K *row, uint32_t slot, K v[NB]) {
     // each 16-byte piece is read as one 128-bit integer: a vector of two
     // keys whose lanes are used apart gets split into 8-byte reads
-    const __uint128_t *p = reinterpret_cast<const __uint128_t *>(row + slot * BSTRIDE);
+    const __uint128_t *p = reinterpret_cast<const __uint128_t *>(row + slot * 2u);
 #pragma unroll
     for (int q = 0; q < NB / 2; ++q) {
-        const __uint128_t t = p[q];
+        const __uint128_t t = p[q * (PLANE / 2)];
         v[ment(2 * q)] = Key<K>::from_bits((uint64_t)t);
         v[ment(2 * q + 1)] = Key<K>::from_bits((uint64_t)(t >> 64));
     }
 }
 
-// global 16-byte piece g of row xh (entries 2g, 2g+1 of the row) -> LDS row
-template <class K>
-__device__ inline void put_piece(K *R, uint32_t xh, int g, ulonglong2 v) {
-    const int x2 = g / (NB / 2), q = g % (NB / 2);       // entries 2q, 2q+1 of block x2
-    const uint32_t idx = (xh << L) | (uint32_t)(2 * g + 1);
-    K *blk = R + slot_of((uint32_t)x2) * BSTRIDE;
-    blk[mpos(2 * q)] = Key<K>::load(v.x);
-    blk[mpos(2 * q + 1)] = Key<K>::tagify(Key<K>::load(v.y), idx << Key<K>::SH);
-}
-
-// row X_H of the packed table (global) -> LDS row
-template <class K>
-__device__ inline void load_row(K *R, const uint64_t *__restrict__ C, uint32_t xh) {
-    const ulonglong2 *src = reinterpret_cast<const ulonglong2 *>(C + ((size_t)xh << L));
-    for (int g = threadIdx.x; g < ROW / 2; g += THREADS) put_piece<K>(R, xh, g, src[g]);
-}
-
-// rows xa and xb into Ra and Rb: every thread's global loads of both rows
-// are issued together, then written to LDS
-template <class K>
-__device__ inline void load_rows2(K *Ra, K *Rb, const uint64_t *__restrict__ C, uint32_t xa, uint32_t xb) {
-    constexpr int PER = ROW / 2 / THREADS;           // 16-byte pieces per thread and row
-    static_assert(PER * THREADS == ROW / 2, "threads divide the row");
-    const ulonglong2 *srca = reinterpret_cast<const ulonglong2 *>(C + ((size_t)xa << L));
-    const ulonglong2 *srcb = reinterpret_cast<const ulonglong2 *>(C + ((size_t)xb << L));
-    ulonglong2 va[PER], vb[PER];
+// row xh of the table -> LDS dst, as direct global-to-LDS copies of 16 bytes
+// per lane (no registers held). Completion: this thread's vmcnt, then a
+// workgroup barrier.
+typedef __attribute__((address_space(3))) void lds_void;
+__device__ inline void copy_row(void *dst, const uint64_t *__restrict__ C, uint32_t xh) {
+    constexpr int PIECES = ROW / 2;                      // 16-byte pieces per row
+    constexpr int PER_WAVE = PIECES / (THREADS / kWave);
+    static_assert(PER_WAVE % kWave == 0, "whole wave copies");
+    const int w = (int)(threadIdx.x / kWave), lane = (int)(threadIdx.x & (kWave - 1));
+    const uint4 *src = reinterpret_cast<const uint4 *>(C + ((size_t)xh << L));
 #pragma unroll
-    for (int p = 0; p < PER; ++p) {
-        va[p] = srca[threadIdx.x + p * THREADS];
-        vb[p] = srcb[threadIdx.x + p * THREADS];
-    }
-#pragma unroll
-    for (int p = 0; p < PER; ++p) {
-        put_piece<K>(Ra, xa, threadIdx.x + p * THREADS, va[p]);
-        put_piece<K>(Rb, xb, threadIdx.x + p * THREADS, vb[p]);
+    for (int i = 0; i < PER_WAVE / kWave; ++i) {
+        const int p0 = w * PER_WAVE + i * kWave;         // first piece of this wave copy (uniform)
+        __builtin_amdgcn_global_load_lds(src + p0 + lane, (lds_void *)((char *)dst + p0 * 16), 16, 0, 0);
     }
 }
+__device__ inline void copies_done() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 // deposit the low bits of t into the set bits of mask (in order)
 __device__ inline uint32_t deposit(uint32_t t, uint32_t mask) {
@@ -931,10 +918,10 @@ __device__ inline void run_item(uint32_t item, const K *rA, const K *rB, uint32_
 }
 
 // Complete row S_H. s.acc holds the best cross-pair key bits (or ~0);
-// rS receives row S_H, s.rb holds row 0 -- the same buffer when S_H = 0, in
-// which case it is filled here. Writes C' and split.
+// rS receives row S_H, r0 holds row 0 -- the same buffer when S_H = 0, in
+// which case it is filled here. Writes the row to the table, and split.
 template <class K>
-__device__ __attribute__((always_inline)) inline void finalize_row(int m, uint32_t sh, Lds<K> &s, K *rS,
+__device__ __attribute__((always_inline)) inline void finalize_row(int m, uint32_t sh, Lds<K> &s, K *rS, K *r0,
                                                                    const int64_t *__restrict__ W,
                                                                    uint64_t *__restrict__ Cp,
                                                                    uint32_t *__restrict__ split) {
@@ -963,7 +950,7 @@ __device__ __attribute__((always_inline)) inline void finalize_row(int m, uint32
         }
         // A2 a proper submask of S2 (for S_H = 0 also non-empty: those pairs
         // mirror the in-block pairs below)
-        if (item) run_item<K>(item, rS, s.rb, a_hi << Key<K>::SH, s.acc, sh == 0);
+        if (item) run_item<K>(item, rS, r0, a_hi << Key<K>::SH, s.acc, sh == 0);
         lds_barrier();
         // A2 = S2: in-block pairs, one thread per block of this level
         if (blk) {
@@ -976,7 +963,7 @@ __device__ __attribute__((always_inline)) inline void finalize_row(int m, uint32
             uint64_t b0[NB];
 #pragma unroll
             for (int x = 0; x < NB; ++x)
-                b0[x] = self0 ? 0u : Key<K>::entry_value(s.rb[mpos(x)]) - (uint64_t)(x & 1 ? x : 0);
+                b0[x] = self0 ? 0u : Key<K>::entry_value(r0[lpos(0u, mpos(x))]) - (uint64_t)(x & 1 ? x : 0);
             uint64_t out[NB];
             uint32_t sp[NB];
             // S1 in order of popcount so that every A1 < S1 is ready
@@ -1015,8 +1002,9 @@ __device__ __attribute__((always_inline)) inline void finalize_row(int m, uint32
             for (int x = 0; x < NB; ++x) {
                 // C'(empty set) = 0 in the table (the unpacked C[0] is the sentinel)
                 const uint64_t v = (base | (uint32_t)x) == 0 ? 0u : out[x];
-                rS[sl * BSTRIDE + mpos(x)] = Key<K>::entry(x & 1 ? v | base | (uint32_t)x : v);
-                Cp[base + x] = Key<K>::store(v);
+                const uint64_t e = x & 1 ? v | base | (uint32_t)x : v;     // odd entries tagged
+                rS[lpos(sl, mpos(x))] = Key<K>::entry(e);
+                Cp[a_hi + lpos(sl, mpos(x))] = Key<K>::store(e);
                 split[base + x] = sp[x];
             }
         }
@@ -1034,27 +1022,24 @@ __device__ __attribute__((always_inline)) inline void finalize_row(int m, uint32
 // even entry is tagged in place once, for all three convolutions, before
 // the class that first needs it tagged.
 template <class K, bool O1, bool O0>
-__device__ __attribute__((always_inline)) inline void cross_step(const Lds<K> &s, uint32_t a2, uint32_t slot_s2,
-                                                                 uint32_t tag_a, uint32_t tag_bs, K best0[NB],
-                                                                 K best1[NB]) {
+__device__ __attribute__((always_inline)) inline void cross_step(const K *ra, const K *rb, uint32_t a2,
+                                                                 uint32_t slot_s2, uint32_t tag_a, uint32_t tag_bs,
+                                                                 K best0[NB], K best1[NB]) {
     static_assert(O0 || !O1, "block A2' is used plain for S1 = 0 after it is tagged");
     constexpr uint32_t HALF = NS2 / 2;
     constexpr int SH = Key<K>::SH;
     constexpr uint32_t TE = HALF << (CB + SH);            // shifted mask of E
     uint32_t sa0 = slot_of(a2), sb0 = slot_s2 ^ sa0;
-    // slots of blocks without E are below HALF; masking values the compiler
-    // cannot see through lets instruction selection use 24-bit multiply-adds
-    // for the block offsets instead of full 32-bit multiplies
-    asm("" : "+v"(sa0), "+v"(sb0));
+    // slots of blocks without E are below HALF (known bits for the compiler)
     sa0 &= HALF - 1;
     sb0 &= HALF - 1;
     const uint32_t ta = tag_a | (a2 << (CB + SH));        // block A2'
     const uint32_t tb = tag_bs - (a2 << (CB + SH));       // block B2' = S2' ^ A2'
     K a0[NB], a1[NB], b0[NB], b1[NB];
-    load_blk(s.ra, sa0, a0);                              // A2'
-    load_blk(s.rb + HALF * BSTRIDE, sb0, b1);             // B2'|E
-    load_blk(s.rb, sb0, b0);                              // B2'
-    load_blk(s.ra + HALF * BSTRIDE, sa0, a1);             // A2'|E
+    load_blk(ra, sa0, a0);                                // A2'
+    load_blk(rb + HALF * 2, sb0, b1);                     // B2'|E
+    load_blk(rb, sb0, b0);                                // B2'
+    load_blk(ra + HALF * 2, sa0, a1);                     // A2'|E
     // (S2'|E, A2') -> best1, (S2', A2') -> best0, (S2'|E, A2'|E) -> best1
     conv_class<K, 1>(a0, b1, best1);
     conv_class<K, 1>(a0, b0, best0);
@@ -1114,30 +1099,53 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
     K best0[NB], best1[NB];
 #pragma unroll
     for (int x = 0; x < NB; ++x) { best0[x] = Key<K>::none(); best1[x] = Key<K>::none(); }
-    for (uint32_t t = t0; t < t1; ++t) {
+    // pair t of the chunk runs on buffer (t - t0) & 1 while the rows of
+    // pair t + 1 are copied into the other one
+    auto pair = [&](auto cur_c, uint32_t t) {
+        constexpr int CUR = decltype(cur_c)::value;
         const uint32_t bh = sh ^ ah;
-        lds_barrier();
-        load_rows2<K>(s.ra, s.rb, Cp, ah, bh);
-        lds_barrier();
+        copies_done();
+        lds_barrier();     // rows of pair t in place; pair t - 1 done with the other buffer
+        const uint32_t an = lowh | (((ah | ~rest) + 1u) & rest);    // next A_H holding lowbit(S_H)
+        if (t + 1 < t1) {
+            copy_row(s.r[CUR ^ 1][0], Cp, an);
+            copy_row(s.r[CUR ^ 1][1], Cp, sh ^ an);
+        }
+        // the buffers' LDS offsets, opaque to the compiler: buffer 1 lies
+        // beyond the 16-bit immediate offsets of LDS reads, and a known base
+        // would be folded into every read's address instead of added once
+        typedef __attribute__((address_space(3))) const K lds_k;
+        uint32_t oa = (uint32_t)(uintptr_t)(lds_k *)s.r[CUR][0];
+        uint32_t ob = (uint32_t)(uintptr_t)(lds_k *)s.r[CUR][1];
+        asm("" : "+s"(oa), "+s"(ob));
+        const K *ra = (const K *)(lds_k *)(uintptr_t)oa, *rb = (const K *)(lds_k *)(uintptr_t)ob;
         const uint32_t tag_a = ah << (L + Key<K>::SH);
         const uint32_t tag_bs = ((bh << L) | (s2 << CB)) << Key<K>::SH;
-        ah = lowh | (((ah | ~rest) + 1u) & rest);    // next A_H holding lowbit(S_H)
+        ah = an;
         if (has_item) {
             if (s2 == 0) {
-                cross_step<K, false, true>(s, 0u, slot_s2, tag_a, tag_bs, best0, best1);
+                cross_step<K, false, true>(ra, rb, 0u, slot_s2, tag_a, tag_bs, best0, best1);
             } else {
                 // t-th submask of S2' holds lowbit(S2') iff t is odd, and every
                 // item starts at an even t with an even count: the orientation
                 // of each step is fixed at compile time
                 uint32_t a2 = a2_first;
                 for (uint32_t i = 0; i < cnt; i += 2) {
-                    cross_step<K, false, false>(s, a2, slot_s2, tag_a, tag_bs, best0, best1);
+                    cross_step<K, false, false>(ra, rb, a2, slot_s2, tag_a, tag_bs, best0, best1);
                     a2 = ((a2 | ~s2) + 1u) & s2;
-                    cross_step<K, true, true>(s, a2, slot_s2, tag_a, tag_bs, best0, best1);
+                    cross_step<K, true, true>(ra, rb, a2, slot_s2, tag_a, tag_bs, best0, best1);
                     a2 = ((a2 | ~s2) + 1u) & s2;
                 }
             }
         }
+    };
+    if (t0 < t1) {
+        copy_row(s.r[0][0], Cp, ah);
+        copy_row(s.r[0][1], Cp, sh ^ ah);
+    }
+    for (uint32_t t = t0; t < t1; t += 2) {
+        pair(std::integral_constant<int, 0>{}, t);
+        if (t + 1 < t1) pair(std::integral_constant<int, 1>{}, t + 1);
     }
     if (has_item) {
         flush<K>(best0, s2, s.acc);
@@ -1145,9 +1153,10 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
     }
     lds_barrier();
     if (fused) {
-        load_row<K>(s.rb, Cp, 0u);
+        copy_row(s.r[0][1], Cp, 0u);
+        copies_done();
         lds_barrier();
-        finalize_row<K>(m, sh, s, s.ra, W, Cp, split);
+        finalize_row<K>(m, sh, s, s.r[0][0], s.r[0][1], W, Cp, split);
     } else {
         uint64_t *dst = partial + (size_t)bid * ROW;
         for (int e = threadIdx.x; e < ROW; e += THREADS) dst[e] = s.acc[e];
@@ -1184,18 +1193,34 @@ __global__ __launch_bounds__(THREADS) void k_rb_final(int m, int h, uint32_t chu
     const uint32_t sh = unrank_colex(r, h, m - L);
     const uint64_t *src = partial + (size_t)r * chunks * ROW;
     for (int e = threadIdx.x; e < ROW; e += THREADS) s.acc[e] = chunks ? src[e] : ~0ull;
-    if (sh != 0) load_row<K>(s.rb, Cp, 0u);
+    if (sh != 0) copy_row(s.r[0][1], Cp, 0u);
+    copies_done();
     lds_barrier();
     // for S_H = 0 the output row is row 0 itself
-    finalize_row<K>(m, sh, s, sh == 0 ? s.rb : s.ra, W, Cp, split);
+    finalize_row<K>(m, sh, s, sh == 0 ? s.r[0][1] : s.r[0][0], s.r[0][1], W, Cp, split);
 }
 
-// packed C' -> C (C[0] keeps the documented sentinel)
+// packed table -> C, one workgroup per row, in place: the whole row is
+// read before any of it is written (C[0] keeps the documented sentinel).
+// The low m bits of a stored value (a tag, or zero) drop out of C' >> m.
 template <class K>
-__global__ void k_rb_unpack(int m, int64_t *C) {
-    const int64_t n = (int64_t)1 << m;
-    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
-        C[i] = i == 0 ? kInf : (int64_t)(Key<K>::stored_value((uint64_t)C[i]) >> m);
+__global__ __launch_bounds__(THREADS) void k_rb_unpack(int m, int64_t *C) {
+    constexpr int PER = ROW / THREADS;
+    const uint32_t xh = blockIdx.x;
+    int64_t *row = C + ((size_t)xh << L);
+    int64_t v[PER];
+    uint32_t at[PER];
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+        const uint32_t e = threadIdx.x + (uint32_t)k * THREADS;      // element of the stored row
+        const uint32_t q = e / PLANE, o = e % PLANE;
+        const int pos = (int)(2 * q + (o & 1u));
+        at[k] = (slot_of(o >> 1) << CB) | (uint32_t)ment(pos);     // slot_of is an involution
+        v[k] = (int64_t)(Key<K>::stored_value((uint64_t)row[e]) >> m);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < PER; ++k) row[at[k]] = (xh == 0 && at[k] == 0) ? kInf : v[k];
 }
 
 // sum_i W({i}), saturated, for the packed-key eligibility test
@@ -1456,7 +1481,7 @@ int solve_rb(int m, const int64_t *W, int64_t *C, uint32_t *split, uint64_t *par
     const int64_t n = (int64_t)1 << m;
     {
         LaunchScope ls("rb_unpack", 16.0 * n, s);
-        rb::k_rb_unpack<K><<<grid_for(n, 256, 16384), 256, 0, s>>>(m, C);
+        rb::k_rb_unpack<K><<<(unsigned)(n >> rb::L), rb::THREADS, 0, s>>>(m, C);
     }
     MPT_HIP_TRY(hipGetLastError());
     return MPT_OK;
