@@ -1014,32 +1014,31 @@ __device__ __attribute__((always_inline)) inline void finalize_row(int m, uint32
     }
 }
 
+template <class K>
+__device__ inline const K *lds_at(uint32_t off) {
+    return (const K *)(__attribute__((address_space(3))) const K *)(uintptr_t)off;
+}
+
 // one base step (S2', A2') of the lifted cross-pair loop: three block
 // convolutions from four block loads. O1 orients S1 = 0 of (S2'|E, A2'),
-// O0 that of (S2', A2') and (S2'|E, A2'|E). The blocks with E sit NS2/2
-// slots above those without, a constant offset. tag_a, tag_bs: shifted
-// masks of entry 0 of block 0 of row A_H and of block S2' of row B_H. Each
-// even entry is tagged in place once, for all three convolutions, before
-// the class that first needs it tagged.
+// O0 that of (S2', A2') and (S2'|E, A2'|E). off_a, off_b: LDS byte offsets
+// of blocks A2' and B2' = S2' ^ A2' in their rows; the blocks with E sit
+// NS2/2 slots above those without, a constant offset. ta, tb: shifted masks
+// of entry 0 of those two blocks. Each even entry is tagged in place once,
+// for all three convolutions, before the class that first needs it tagged.
 template <class K, bool O1, bool O0>
-__device__ __attribute__((always_inline)) inline void cross_step(const K *ra, const K *rb, uint32_t a2,
-                                                                 uint32_t slot_s2, uint32_t tag_a, uint32_t tag_bs,
-                                                                 K best0[NB], K best1[NB]) {
+__device__ __attribute__((always_inline)) inline void cross_step(uint32_t off_a, uint32_t off_b, uint32_t ta,
+                                                                 uint32_t tb, K best0[NB], K best1[NB]) {
     static_assert(O0 || !O1, "block A2' is used plain for S1 = 0 after it is tagged");
     constexpr uint32_t HALF = NS2 / 2;
     constexpr int SH = Key<K>::SH;
     constexpr uint32_t TE = HALF << (CB + SH);            // shifted mask of E
-    uint32_t sa0 = slot_of(a2), sb0 = slot_s2 ^ sa0;
-    // slots of blocks without E are below HALF (known bits for the compiler)
-    sa0 &= HALF - 1;
-    sb0 &= HALF - 1;
-    const uint32_t ta = tag_a | (a2 << (CB + SH));        // block A2'
-    const uint32_t tb = tag_bs - (a2 << (CB + SH));       // block B2' = S2' ^ A2'
+    const K *pa = lds_at<K>(off_a), *pb = lds_at<K>(off_b);
     K a0[NB], a1[NB], b0[NB], b1[NB];
-    load_blk(ra, sa0, a0);                                // A2'
-    load_blk(rb + HALF * 2, sb0, b1);                     // B2'|E
-    load_blk(rb, sb0, b0);                                // B2'
-    load_blk(ra + HALF * 2, sa0, a1);                     // A2'|E
+    load_blk(pa, 0u, a0);                                 // A2'
+    load_blk(pb, HALF, b1);                               // B2'|E
+    load_blk(pb, 0u, b0);                                 // B2'
+    load_blk(pa, HALF, a1);                               // A2'|E
     // (S2'|E, A2') -> best1, (S2', A2') -> best0, (S2'|E, A2'|E) -> best1
     conv_class<K, 1>(a0, b1, best1);
     conv_class<K, 1>(a0, b0, best0);
@@ -1095,7 +1094,11 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
     const uint32_t a2_first = (item >> 8) & 0xffu;
     const uint32_t cnt = 1u << ((item >> 16) & 3u);
     const uint32_t slot_s2 = slot_of(s2);
+    const uint32_t low2 = s2 & (0u - s2);
+    const uint32_t low_off = slot_of(low2) * 16u;                    // block offset of lowbit(S2')
+    const uint32_t low_tag = low2 << (CB + Key<K>::SH);
     static_assert(RL == R2 - 1 && (1u << RL) == NS2 / 2, "E is the top middle bit");
+    static_assert(NS2 / 2 * 16 <= 32 * 1024, "slot offsets stay below the row size");
     K best0[NB], best1[NB];
 #pragma unroll
     for (int x = 0; x < NB; ++x) { best0[x] = Key<K>::none(); best1[x] = Key<K>::none(); }
@@ -1111,30 +1114,39 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
             copy_row(s.r[CUR ^ 1][0], Cp, an);
             copy_row(s.r[CUR ^ 1][1], Cp, sh ^ an);
         }
-        // the buffers' LDS offsets, opaque to the compiler: buffer 1 lies
-        // beyond the 16-bit immediate offsets of LDS reads, and a known base
-        // would be folded into every read's address instead of added once
+        // the buffers' LDS offsets (multiples of the 32 KiB row size), opaque
+        // to the compiler: buffer 1 lies beyond the 16-bit immediate offsets
+        // of LDS reads, and a known base would be folded into every read's
+        // address instead of added once
         typedef __attribute__((address_space(3))) const K lds_k;
         uint32_t oa = (uint32_t)(uintptr_t)(lds_k *)s.r[CUR][0];
         uint32_t ob = (uint32_t)(uintptr_t)(lds_k *)s.r[CUR][1];
         asm("" : "+s"(oa), "+s"(ob));
-        const K *ra = (const K *)(lds_k *)(uintptr_t)oa, *rb = (const K *)(lds_k *)(uintptr_t)ob;
-        const uint32_t tag_a = ah << (L + Key<K>::SH);
-        const uint32_t tag_bs = ((bh << L) | (s2 << CB)) << Key<K>::SH;
+        constexpr int SH = Key<K>::SH;
+        const uint32_t tag_a = ah << (L + SH);
+        const uint32_t tag_bs = ((bh << L) | (s2 << CB)) << SH;
         ah = an;
         if (has_item) {
             if (s2 == 0) {
-                cross_step<K, false, true>(ra, rb, 0u, slot_s2, tag_a, tag_bs, best0, best1);
+                cross_step<K, false, true>(oa, ob, tag_a, tag_bs, best0, best1);
             } else {
                 // t-th submask of S2' holds lowbit(S2') iff t is odd, and every
                 // item starts at an even t with an even count: the orientation
-                // of each step is fixed at compile time
+                // of each step is fixed at compile time. The odd submask is
+                // the even one plus lowbit(S2'); slot_of is GF(2)-linear and
+                // the slot offsets (below 4 KiB) sit under the row offsets'
+                // zero bits, so its block offsets are the even step's XOR a
+                // constant of the item.
                 uint32_t a2 = a2_first;
                 for (uint32_t i = 0; i < cnt; i += 2) {
-                    cross_step<K, false, false>(ra, rb, a2, slot_s2, tag_a, tag_bs, best0, best1);
-                    a2 = ((a2 | ~s2) + 1u) & s2;
-                    cross_step<K, true, true>(ra, rb, a2, slot_s2, tag_a, tag_bs, best0, best1);
-                    a2 = ((a2 | ~s2) + 1u) & s2;
+                    const uint32_t sa = slot_of(a2) & (NS2 / 2 - 1u);
+                    const uint32_t sb = (slot_s2 ^ sa) & (NS2 / 2 - 1u);
+                    const uint32_t off_a = oa + sa * 16u, off_b = ob + sb * 16u;
+                    const uint32_t ta = tag_a | (a2 << (CB + SH)), tb = tag_bs - (a2 << (CB + SH));
+                    cross_step<K, false, false>(off_a, off_b, ta, tb, best0, best1);
+                    cross_step<K, true, true>(off_a ^ low_off, off_b ^ low_off, ta | low_tag, tb - low_tag, best0,
+                                              best1);
+                    a2 = ((a2 | low2 | ~s2) + 1u) & s2;            // two submasks on
                 }
             }
         }
