@@ -180,21 +180,27 @@ __global__ void k_compact(int64_t n_chunks, int64_t cap, const int64_t *w, const
 // dense table is written exactly once and never read.
 // The zeta over the low bits: bits 0..4 are also summed on the sparse list
 // (a chunk with low part L adds w to every L' with L' = L outside bits 0..4
-// and L' a subset of L inside them); bits 5..8 and 9..12 are two register
-// passes with 16 elements per thread. LDS holds 16 elements per 144 bytes,
-// which keeps both passes free of bank conflicts; the last pass holds
-// elements t + 512 k, so each store instruction covers 512 contiguous bytes.
-constexpr int kZetaBits = 13;
-constexpr int kZetaThreads = 512;
+// and L' a subset of L inside them); bits 5..8 and 9..11 are two register
+// passes, with 16 elements per thread and with two groups of 8. LDS holds
+// 16 elements per 144 bytes, which keeps both passes free of bank
+// conflicts; the last pass holds elements g + 512 k for g = t and t + 256,
+// so each store instruction covers 2 KiB of contiguous bytes. A tile takes
+// 36 KiB of LDS, so four workgroups share a CU: the stores of one tile
+// drain while others are built, and each workgroup's first tile, built
+// before any of its stores start, is short.
+constexpr int kZetaBits = 12;
+constexpr int kZetaThreads = 256;
 constexpr int kZetaN = 1 << kZetaBits;
 constexpr uint32_t kZetaSparseMask = 31u;     // bits summed on the sparse list
 __device__ inline int zpos(int e) { return e + 2 * (e >> 4); }
 
-__device__ inline void zeta16(int64_t v[16]) {
+// superset zeta over the index bits of N = 2^J register elements
+template <int N>
+__device__ inline void zeta_regs(int64_t v[N]) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; (1 << j) < N; ++j)
 #pragma unroll
-        for (int k = 0; k < 16; ++k)
+        for (int k = 0; k < N; ++k)
             if (!((k >> j) & 1)) v[k] += v[k | (1 << j)];
 }
 
@@ -251,28 +257,34 @@ __global__ __launch_bounds__(kZetaThreads) void k_weights_tile(
         if (hi == 0 && t == 0)
             atomicAdd((unsigned long long *)&tile[0], (unsigned long long)zero_weight);
         lds_barrier();
+        static_assert(kZetaBits == 12 && kZetaThreads == 256, "pass shapes below");
         int64_t v[16];
         // bits 5..8: element (t >> 5) << 9 | k << 5 | (t & 31)
         const int eb = ((t >> 5) << 9) | (t & 31);
 #pragma unroll
         for (int k = 0; k < 16; ++k) v[k] = tile[zpos(eb | (k << 5))];
-        zeta16(v);
+        zeta_regs<16>(v);
 #pragma unroll
         for (int k = 0; k < 16; ++k) tile[zpos(eb | (k << 5))] = v[k];
         lds_barrier();
-        // bits 9..12: element t + 512 k, stored straight to HBM (each store
-        // instruction covers 512 contiguous bytes)
-#pragma unroll
-        for (int k = 0; k < 16; ++k) v[k] = tile[zpos(t + (k << 9))];
-        zeta16(v);
+        // bits 9..11: elements g + 512 k for the groups g = t and t + 256,
+        // stored straight to HBM (each store instruction covers 2 KiB)
         int64_t *out = W + ((int64_t)hi << b);
-        if (m >= b) {
 #pragma unroll
-            for (int k = 0; k < 16; ++k) out[t + (k << 9)] = v[k];
-        } else {                        // one partial tile: only the first 2^m subsets exist
+        for (int half = 0; half < 2; ++half) {
+            const int g = t + half * kZetaThreads;
+            int64_t u[8];
 #pragma unroll
-            for (int k = 0; k < 16; ++k)
-                if (t + (k << 9) < (1 << m)) out[t + (k << 9)] = v[k];
+            for (int k = 0; k < 8; ++k) u[k] = tile[zpos(g + (k << 9))];
+            zeta_regs<8>(u);
+            if (m >= b) {
+#pragma unroll
+                for (int k = 0; k < 8; ++k) out[g + (k << 9)] = u[k];
+            } else {                    // one partial tile: only the first 2^m subsets exist
+#pragma unroll
+                for (int k = 0; k < 8; ++k)
+                    if (g + (k << 9) < (1 << m)) out[g + (k << 9)] = u[k];
+            }
         }
     }
 }
@@ -1563,7 +1575,7 @@ extern "C" int mpt_build_weights(int m, int64_t n_chunks, int64_t nnz, const int
     const uint32_t tiles = m > kZetaBits ? 1u << (m - kZetaBits) : 1u;
     if ((double)tiles * (double)nnz <= kDenseAbove) {
         LaunchScope ls("weights_tile", 8.0 * (double)(1ull << m), s);
-        k_weights_tile<<<std::min(tiles, 512u), kZetaThreads, 0, s>>>(m, (uint32_t)std::max<int64_t>(nnz, 1), tiles,
+        k_weights_tile<<<std::min(tiles, 1024u), kZetaThreads, 0, s>>>(m, (uint32_t)std::max<int64_t>(nnz, 1), tiles,
                                                                       list_sig, list_w, h, W);
     } else {
         // long list: scatter + zeta over the dense table
