@@ -483,30 +483,33 @@ __global__ __launch_bounds__(256) void k_dp_reduce(int m, int p, uint32_t n_sets
 // ---------------------------------------------------------------------------
 // phase 2, row-blocked DP (packed keys).
 //
-// A mask X splits into a high part X_H (bits L..m-1), a middle part X2
-// (bits CB..L-1) and a low part X1 (bits 0..CB-1). Row X_H is the 2^L
-// consecutive table entries that share X_H. Every unordered bipartition
-// {P, Q} of S = S_H|S_L is visited once, from the part holding the lowest
-// request of S_H (or, for S_H = 0, in both orientations):
-//   cross pairs  (A_H, B_H), A_H holding lowbit(S_H), B_H non-empty: the
-//                rows A_H and B_H are complete (lower level), and
-//                C(S_H|S_L) gets min over A_L of rowA[A_L] + rowB[S_L^A_L];
-//   self pair    (S_H, 0): rowA is row S_H itself, filled in order of
-//                |S_L|, rowB is row 0.
-// Levels h = |S_H| run one after the other; within a level every S_H is
-// independent. Inside a pair, a thread takes the block of 2^CB entries for a
-// middle mask and does the CB-bit min-plus subset convolution in registers.
+// A mask X splits into a row part X_H, its low H = m - L bits, and an
+// in-row part X_L, its high L bits: X = X_H | X_L << H, with X_L made of a
+// middle part X2 (its high L - CB bits) and a low part X1 (its low CB bits).
+// Row X_H is the 2^L table entries that share X_H, stored together. Every
+// unordered bipartition of S = S_H | S_L << H with S_H non-empty is visited
+// once, from the part A holding lowbit(S_H) -- which is lowbit(S), since
+// S_H holds the low bits:
+//   cross pairs  (A_H, B_H), A_H holding lowbit(S_H), B_H non-empty: rows
+//                A_H and B_H are complete (lower level), and C(S) gets
+//                min over A_L of rowA[A_L] + rowB[S_L ^ A_L];
+//   self pair    (S_H, 0): rowA is row S_H itself, filled in order of |S_L|,
+//                rowB is row 0.
+// Row 0 (S_H = 0) is the DP over the L in-row requests alone, done first by
+// one workgroup. Levels h = |S_H| run one after the other; within a level
+// every S_H is independent. Inside a pair, a thread takes the block of 2^CB
+// entries for a middle mask and does the CB-bit min-plus subset convolution
+// in registers.
 //
-// Packed keys: during the DP the C table holds C'(X) = C(X) << m. A
-// candidate's key is C'(A) + C'(B) + canon, where canon is the mask of the
-// part holding lowbit(S) (< 2^m). The smallest key is the smallest cost and,
-// among equal costs, the numerically smallest such part -- the documented
-// tie rule. An entry is used plain (C') or tagged with its own mask (C' + X,
-// an OR, since C' leaves the low m bits zero), so a key is one add: tagged
-// A + plain B when A holds lowbit(S), plain A + tagged B otherwise. Keys are
-// exact integers held as doubles (one v_add_f64 and one v_min_f64 per
-// candidate) while sum_i w(R_i) < 2^(51-m), otherwise as uint64 (below
-// 2^62); larger instances take the plain kernels.
+// Packed keys: C'(X) = C(X) << m. A candidate's key is C'(A) + C'(B) + A,
+// with A the mask of the part holding lowbit(S), below 2^m. The smallest key
+// is the smallest cost and, among equal costs, the numerically smallest such
+// part -- the documented tie rule. That part is always the one from the A
+// row, so the table is kept twice: tagged (C'(X) + X, an OR, since C' leaves
+// the low m bits zero) for rows on the A side and plain (C') for rows on the
+// B side, and a key is one add. Keys are exact integers held as doubles (one
+// v_add_f64 and one v_min_f64 per candidate) while sum_i w(R_i) < 2^(51-m),
+// otherwise as uint64 (below 2^62); larger instances take the plain kernels.
 namespace rb {
 #ifndef MPT_RB_L
 #define MPT_RB_L 12
@@ -518,12 +521,10 @@ constexpr int R2 = L - CB;            // middle bits
 #define MPT_RB_THREADS 1024
 #endif
 constexpr int NB = 1 << CB;           // entries per block
-constexpr int NE = NB / 2;            // even entries per block
 constexpr int ROW = 1 << L;           // entries per row
 constexpr int NS2 = 1 << R2;          // blocks per row
 constexpr int THREADS = MPT_RB_THREADS;
 constexpr int CUS = 256;              // MI355X compute units
-constexpr uint64_t SENT = (uint64_t)1 << 62;
 
 constexpr int cpop(int x) { int c = 0; while (x) { c += x & 1; x >>= 1; } return c; }
 
@@ -674,21 +675,17 @@ __constant__ ThreadItems c_titems = make_thread_items();
 
 
 // Key arithmetic. A table entry carries the packed value v = C' or, tagged,
-// C' | X. In both representations tagging is an OR of a 32-bit value into
-// the entry's low 32 bits (m <= 30), so the cross-pair loop can tag an entry
-// it loaded plain with one 32-bit instruction.
+// C' | X.
 //   uint64: an entry is v itself; a key is the sum of two entries.
 //   double: an entry is the double 2^52 + 2v. Its exponent is fixed, so its
-//   low mantissa bits are the integer 2v and the tag is an OR of 2X. The sum
-//   of two entries is 2^53 + 2(v_A + v_B): even, so exact below 2^54, and
-//   its mantissa is the packed key v_A + v_B. That needs 2v < 2^52 for every
-//   entry, i.e. sum_i w(R_i) < 2^(51-m).
+//   low mantissa bits are the integer 2v. The sum of two entries is
+//   2^53 + 2(v_A + v_B): even, so exact below 2^54, and its mantissa is the
+//   packed key v_A + v_B. That needs 2v < 2^52 for every entry, i.e.
+//   sum_i w(R_i) < 2^(51-m).
 template <class K> struct Key;
 template <> struct Key<uint64_t> {
-    static constexpr int SH = 0;                            // shift of a tag inside an entry
     static __device__ inline uint64_t entry(uint64_t v) { return v; }
     static __device__ inline uint64_t entry_value(uint64_t e) { return e; }
-    static __device__ inline uint64_t tagify(uint64_t e, uint32_t t) { return e | t; }
     static __device__ inline uint64_t add(uint64_t a, uint64_t b) { return a + b; }
     static __device__ inline uint64_t min(uint64_t a, uint64_t b) { return b < a ? b : a; }
     static __device__ inline uint64_t none() { return ~0ull; }
@@ -702,14 +699,12 @@ template <> struct Key<uint64_t> {
     static __device__ inline uint64_t load(uint64_t b) { return b; }
 };
 template <> struct Key<double> {
-    static constexpr int SH = 1;
     static constexpr uint64_t E52 = 0x4330000000000000ull;  // bits of 2^52
     static constexpr uint64_t MANT = (1ull << 52) - 1u;
     static __device__ inline uint64_t bits(double k) { return (uint64_t)__double_as_longlong(k); }
     static __device__ inline double from_bits(uint64_t b) { return __longlong_as_double((long long)b); }
     static __device__ inline double entry(uint64_t v) { return from_bits(E52 | (v << 1)); }
     static __device__ inline uint64_t entry_value(double e) { return (bits(e) & MANT) >> 1; }
-    static __device__ inline double tagify(double e, uint32_t t) { return from_bits(bits(e) | t); }
     static __device__ inline double add(double a, double b) { return a + b; }
     static __device__ inline double min(double a, double b) { return fmin(a, b); }
     static __device__ inline double none() { return __builtin_inf(); }
@@ -725,24 +720,18 @@ template <> struct Key<double> {
 // (for R2 = 9; the last term takes the bits between 6 and E), a GF(2)-linear
 // involution, so slot(S2 ^ A2) = slot(S2) ^ slot(A2); it maps the low R2-1
 // middle bits onto themselves and the top one, E, onto NS2/2, so
-// slot(X | E) = slot(X) + NS2/2 for X below E.
-// Inside a block the odd entries come first, tagged: an odd entry holds bit
-// 0, so in every candidate it is the part holding lowbit(S1). The even
-// entries follow, plain; where a candidate needs one tagged, the tag is
-// ORed in registers. A row is stored as NB/2 planes of 16-byte pieces:
-// plane q holds positions 2q and 2q+1 of every block, block at slot s in
-// piece s. A lane's four reads of one block are then 8 KiB apart
-// (immediate offsets), and a 16-lane pass of reads is free of bank
-// conflicts when its lanes' slots differ mod 16 (gfx950 serves a 16-byte
-// read 16 lanes at a time from 16 groups of 16 bytes; a plane is a
-// multiple of 256 bytes). Because HBM holds the rows in this same layout,
-// a row reaches LDS as a plain copy, straight from global memory.
+// slot(X | E) = slot(X) + NS2/2 for X below E. A row is stored as NB/2
+// planes of 16-byte pieces: plane q holds entries 2q and 2q+1 of every
+// block, block at slot s in piece s. A lane's four reads of one block are
+// then 8 KiB apart (immediate offsets), and a 16-lane pass of reads is free
+// of bank conflicts when its lanes' slots differ mod 16 (gfx950 serves a
+// 16-byte read 16 lanes at a time from 16 groups of 16 bytes; a plane is a
+// multiple of 256 bytes). Because HBM holds the rows in this same layout, a
+// row reaches LDS as a plain copy, straight from global memory.
 constexpr int PLANE = 2 * NS2;        // K elements per plane
-constexpr int mpos(int x) { return (x & 1) ? (x >> 1) : NE + (x >> 1); }   // position of entry x
-constexpr int ment(int j) { return j < NE ? 2 * j + 1 : 2 * (j - NE); }     // entry at position j
-// element index inside a row of the entry at position pos of the block at slot
-__host__ __device__ constexpr uint32_t lpos(uint32_t slot, int pos) {
-    return (uint32_t)(pos >> 1) * PLANE + slot * 2u + (uint32_t)(pos & 1);
+// element index inside a row of entry x of the block at slot
+__host__ __device__ constexpr uint32_t lpos(uint32_t slot, int x) {
+    return (uint32_t)(x >> 1) * PLANE + slot * 2u + (uint32_t)(x & 1);
 }
 __host__ __device__ constexpr uint32_t slot_of(uint32_t x2) {
     return x2 ^ ((x2 >> 3) & 7u) ^ ((x2 >> 6) & ((1u << (R2 - 7)) - 1u));
@@ -763,14 +752,14 @@ static_assert(NB == 8 && (PLANE * 8) % 256 == 0, "four planes of 16-byte pieces,
 // two buffers of the (A, B) row pair: the next pair's rows are copied in
 // while the current pair runs
 template <class K> struct alignas(16) Lds {
-    K r[2][2][ROW];        // [buffer][A side, B side]
+    K r[2][2][ROW];        // [buffer][A side (tagged), B side (plain)]
     uint64_t acc[ROW];     // best key bits per entry of the output row
 };
 static_assert(sizeof(Lds<double>) <= 160 * 1024, "rows and accumulators fit one CU's LDS");
 // workgroups that run on one CU at a time (their LDS takes the CU)
 constexpr int WGS_PER_CU = (int)((160 * 1024) / sizeof(Lds<double>));
 
-// block at slot -> v[x] = entry x (odd tagged, even plain)
+// block at slot -> v[x] = entry x
 template <class K>
 __device__ inline void load_blk(const K *row, uint32_t slot, K v[NB]) {
     // each 16-byte piece is read as one 128-bit integer: a vector of two
@@ -779,21 +768,21 @@ __device__ inline void load_blk(const K *row, uint32_t slot, K v[NB]) {
 #pragma unroll
     for (int q = 0; q < NB / 2; ++q) {
         const __uint128_t t = p[q * (PLANE / 2)];
-        v[ment(2 * q)] = Key<K>::from_bits((uint64_t)t);
-        v[ment(2 * q + 1)] = Key<K>::from_bits((uint64_t)(t >> 64));
+        v[2 * q] = Key<K>::from_bits((uint64_t)t);
+        v[2 * q + 1] = Key<K>::from_bits((uint64_t)(t >> 64));
     }
 }
 
-// row xh of the table -> LDS dst, as direct global-to-LDS copies of 16 bytes
+// row xh of a table -> LDS dst, as direct global-to-LDS copies of 16 bytes
 // per lane (no registers held). Completion: this thread's vmcnt, then a
 // workgroup barrier.
 typedef __attribute__((address_space(3))) void lds_void;
-__device__ inline void copy_row(void *dst, const uint64_t *__restrict__ C, uint32_t xh) {
+__device__ inline void copy_row(void *dst, const uint64_t *__restrict__ tab, uint32_t xh) {
     constexpr int PIECES = ROW / 2;                      // 16-byte pieces per row
     constexpr int PER_WAVE = PIECES / (THREADS / kWave);
     static_assert(PER_WAVE % kWave == 0, "whole wave copies");
     const int w = (int)(threadIdx.x / kWave), lane = (int)(threadIdx.x & (kWave - 1));
-    const uint4 *src = reinterpret_cast<const uint4 *>(C + ((size_t)xh << L));
+    const uint4 *src = reinterpret_cast<const uint4 *>(tab + ((size_t)xh << L));
 #pragma unroll
     for (int i = 0; i < PER_WAVE / kWave; ++i) {
         const int p0 = w * PER_WAVE + i * kWave;         // first piece of this wave copy (uniform)
@@ -814,53 +803,16 @@ __device__ inline uint32_t deposit(uint32_t t, uint32_t mask) {
     return r;
 }
 
-// CB-bit min-plus subset convolution of one block pair, entries a[] (A
-// side) and b[] (B side):
-//   best[S1] = min(best[S1], min over A1 in S1 of a[A1] + b[S1 ^ A1]),
-// where the operand holding lowbit(S1) must be tagged and the other plain.
-// Odd entries are loaded tagged and always play the tagged part. An even
-// entry x > 0 plays the plain part only in candidates whose tagged operand
-// is odd or, for x = 4, entry 2; so the candidates run in classes by their
-// tagged operand -- odd, 2, 4, 6 -- and the caller tags entry x of its
-// blocks in place just before class x. S1 = 0 (its tagged side set by the
-// orientation) comes last.
-static_assert(CB == 3, "the class order below is worked out for 3-bit blocks");
-template <class K, int CLS>
-__device__ inline void conv_class(const K a[NB], const K b[NB], K best[NB]) {
-#pragma unroll
-    for (int s1 = 1; s1 < NB; ++s1) {
-        const int low = s1 & -s1;
-#pragma unroll
-        for (int a1 = 0; a1 < NB; ++a1) {
-            if (a1 & ~s1) continue;
-            const int b1 = s1 ^ a1;
-            const int t = (a1 & low) ? a1 : b1;          // the tagged operand
-            if (((t & 1) ? 1 : t) != CLS) continue;
-            best[s1] = Key<K>::min(best[s1], Key<K>::add(a[a1], b[b1]));
-        }
-    }
-}
-
-// tag entry X of a block whose entry 0 has mask tag0 (tags pre-shifted)
-template <class K, int X>
-__device__ inline void tag_entry(K v[NB], uint32_t tag0) {
-    v[X] = Key<K>::tagify(v[X], tag0 | ((uint32_t)X << Key<K>::SH));
-}
-
-// the whole convolution of one block pair; ta, tb: shifted masks of entry 0
-// of the two blocks; orient_a: the A side holds lowbit(S) for S1 = 0
+// CB-bit min-plus subset convolution of one block pair, a[] from the A row
+// (tagged) and b[] from the B row (plain):
+//   best[S1] = min(best[S1], min over A1 in S1 of a[A1] + b[S1 ^ A1]).
 template <class K>
-__device__ inline void conv_pair(K a[NB], K b[NB], uint32_t ta, uint32_t tb, bool orient_a, K best[NB]) {
-    conv_class<K, 1>(a, b, best);
-    tag_entry<K, 2>(a, ta); tag_entry<K, 2>(b, tb);
-    conv_class<K, 2>(a, b, best);
-    tag_entry<K, 4>(a, ta); tag_entry<K, 4>(b, tb);
-    conv_class<K, 4>(a, b, best);
-    tag_entry<K, 6>(a, ta); tag_entry<K, 6>(b, tb);
-    conv_class<K, 6>(a, b, best);
-    const K a0 = orient_a ? Key<K>::tagify(a[0], ta) : a[0];
-    const K b0 = orient_a ? b[0] : Key<K>::tagify(b[0], tb);
-    best[0] = Key<K>::min(best[0], Key<K>::add(a0, b0));
+__device__ inline void conv_full(const K a[NB], const K b[NB], K best[NB]) {
+#pragma unroll
+    for (int s1 = 0; s1 < NB; ++s1)
+#pragma unroll
+        for (int a1 = 0; a1 < NB; ++a1)
+            if (!(a1 & ~s1)) best[s1] = Key<K>::min(best[s1], Key<K>::add(a[a1], b[s1 ^ a1]));
 }
 
 template <class K>
@@ -897,31 +849,27 @@ __device__ inline void flush_group(const K best[NB], uint32_t s2, uint32_t seg, 
     }
 }
 
-// one self-pair work item (S2, first A2, t) against (rowS, row0): 2^t
-// submasks A2 of S2 in increasing order, skipping A2 == S2 and, when
-// skip_empty, A2 == 0. tag_h: the shifted mask of row S_H's entry 0.
+// one self-pair work item (S2, first A2, t) of row S_H against row 0: 2^t
+// submasks A2 of S2 in increasing order, skipping A2 == S2 (B2 would be
+// empty); rA is row S_H (tagged), rB row 0 (plain)
 template <class K>
-__device__ inline void run_item(uint32_t item, const K *rA, const K *rB, uint32_t tag_h, uint64_t *acc,
-                                bool skip_empty) {
-    constexpr int SH = Key<K>::SH;
+__device__ inline void run_item(uint32_t item, const K *rA, const K *rB, uint64_t *acc) {
     const uint32_t s2 = item & 0xffffu;
     const int k = __popc(s2);
     const int tb = (int)((item >> 28) & 7u);
     const uint32_t cnt = 1u << tb;
-    const uint32_t low2 = s2 & (0u - s2);
     const uint32_t slot_s2 = slot_of(s2);
     uint32_t a2 = (item >> 16) & 0xfffu;
     K best[NB];
 #pragma unroll
     for (int x = 0; x < NB; ++x) best[x] = Key<K>::none();
     for (uint32_t i = 0; i < cnt; ++i) {
-        const uint32_t b2 = s2 ^ a2;
-        if (b2 != 0 && !(skip_empty && a2 == 0)) {
+        if (a2 != s2) {
             const uint32_t sa = slot_of(a2), sb = slot_s2 ^ sa;
             K a[NB], b[NB];
             load_blk(rA, sa, a);
             load_blk(rB, sb, b);
-            conv_pair<K>(a, b, tag_h | (a2 << (CB + SH)), b2 << (CB + SH), (s2 == 0) || (a2 & low2), best);
+            conv_full<K>(a, b, best);
         }
         a2 = ((a2 | ~s2) + 1u) & s2;
     }
@@ -929,15 +877,17 @@ __device__ inline void run_item(uint32_t item, const K *rA, const K *rB, uint32_
     flush_group<K>(best, s2, chunks < 8u ? chunks : 8u, acc);
 }
 
-// Complete row S_H. s.acc holds the best cross-pair key bits (or ~0);
-// rS receives row S_H, r0 holds row 0 -- the same buffer when S_H = 0, in
-// which case it is filled here. Writes the row to the table, and split.
+// Complete row S_H (non-empty). s.acc holds the best cross-pair key bits (or
+// ~0); rS receives row S_H (tagged), r0 holds row 0 (plain). Writes the row
+// to both tables and its splits to Sr (row-major, mask order inside a row).
 template <class K>
-__device__ __attribute__((always_inline)) inline void finalize_row(int m, uint32_t sh, Lds<K> &s, K *rS, K *r0,
-                                                                   const int64_t *__restrict__ W,
-                                                                   uint64_t *__restrict__ Cp,
-                                                                   uint32_t *__restrict__ split) {
-    const uint32_t a_hi = sh << L;
+__device__ __attribute__((always_inline)) inline void finalize_row(int m, uint32_t sh, Lds<K> &s, K *rS, const K *r0,
+                                                                   const int64_t *__restrict__ Wr,
+                                                                   uint64_t *__restrict__ Tt,
+                                                                   uint64_t *__restrict__ Pt,
+                                                                   uint32_t *__restrict__ Sr) {
+    const int H = m - L;
+    const uint32_t row = sh << L;
     const uint64_t mask = ((uint64_t)1 << m) - 1u;
     // this thread's item and block of a level (0: none), each read one
     // level ahead so that the table lookups overlap the level before
@@ -950,32 +900,29 @@ __device__ __attribute__((always_inline)) inline void finalize_row(int m, uint32
         return bi < c_blocks.end[k] ? (uint32_t)c_blocks.v[bi] | 0x10000u : 0u;
     };
     uint32_t item = level_item(0), blk = level_blk(0);
+    // block 0 of row 0, plain: C'(X1 << H) for every low part X1
+    uint64_t b0[NB];
+#pragma unroll
+    for (int x = 0; x < NB; ++x) b0[x] = Key<K>::entry_value(r0[lpos(0u, x)]);
     for (int k = 0; k <= R2; ++k) {
         const uint32_t item_next = k < R2 ? level_item(k + 1) : 0u;
         const uint32_t blk_next = k < R2 ? level_blk(k + 1) : 0u;
         // W of the block this thread finishes below, read ahead of phase 1
         int64_t wv[NB];
         if (blk) {
-            const int64_t *wp = W + (a_hi | ((blk & 0xffffu) << CB));
+            const int64_t *wp = Wr + (row | ((blk & 0xffffu) << CB));
 #pragma unroll
             for (int x = 0; x < NB; ++x) wv[x] = wp[x];
         }
-        // A2 a proper submask of S2 (for S_H = 0 also non-empty: those pairs
-        // mirror the in-block pairs below)
-        if (item) run_item<K>(item, rS, r0, a_hi << Key<K>::SH, s.acc, sh == 0);
+        // A2 a proper submask of S2
+        if (item) run_item<K>(item, rS, r0, s.acc);
         lds_barrier();
-        // A2 = S2: in-block pairs, one thread per block of this level
+        // A2 = S2: in-block pairs, one thread per block of this level; A =
+        // (S_H, S2, A1) holds lowbit(S), B = (0, 0, S1 ^ A1) is in block 0
+        // of row 0
         if (blk) {
             const uint32_t s2 = blk & 0xffffu;
-            const uint32_t base = a_hi | (s2 << CB);
-            // row 0, block 0 (complete, except while S_H = 0 builds it: then
-            // it is this very block, whose entries are copied in as they are
-            // finished -- every B1 below is a proper submask of S1)
-            const bool self0 = sh == 0 && s2 == 0;
-            uint64_t b0[NB];
-#pragma unroll
-            for (int x = 0; x < NB; ++x)
-                b0[x] = self0 ? 0u : Key<K>::entry_value(r0[lpos(0u, mpos(x))]) - (uint64_t)(x & 1 ? x : 0);
+            const uint32_t base = sh | ((s2 << CB) << H);        // mask of (S_H, S2, X1 = 0)
             uint64_t out[NB];
             uint32_t sp[NB];
             // S1 in order of popcount so that every A1 < S1 is ready
@@ -984,40 +931,28 @@ __device__ __attribute__((always_inline)) inline void finalize_row(int m, uint32
 #pragma unroll
                 for (int s1 = 0; s1 < NB; ++s1) {
                     if (cpop(s1) != pc) continue;
-                    const uint32_t S = base | (uint32_t)s1;
+                    const uint32_t S = base | ((uint32_t)s1 << H);
                     const int64_t w = wv[s1];
-                    if (S == 0) { out[s1] = SENT; sp[s1] = 0; b0[s1] = self0 ? out[s1] : b0[s1]; continue; }
-                    if (__popc(S) == 1) {
-                        out[s1] = (uint64_t)w << m;
-                        sp[s1] = 0;
-                        b0[s1] = self0 ? out[s1] : b0[s1];
-                        continue;
-                    }
+                    if (__popc(S) == 1) { out[s1] = (uint64_t)w << m; sp[s1] = 0; continue; }
                     uint64_t kb = Key<K>::key_value(s.acc[(s2 << CB) | s1]);
-                    const int low = s1 & -s1;
 #pragma unroll
                     for (int a1 = 0; a1 < NB; ++a1) {
                         if ((a1 & ~s1) || a1 == s1) continue;
-                        const int b1 = s1 ^ a1;
-                        const uint64_t av = out[a1];
-                        const uint64_t bv = b0[b1];
-                        const uint64_t c = (a1 & low) ? av + bv + (base | (uint32_t)a1) : av + bv + (uint32_t)b1;
+                        const uint64_t c = out[a1] + b0[s1 ^ a1] + (base | ((uint32_t)a1 << H));
                         kb = c < kb ? c : kb;
                     }
                     out[s1] = ((kb >> m) - (uint64_t)w) << m;
                     sp[s1] = (uint32_t)(kb & mask);
-                    b0[s1] = self0 ? out[s1] : b0[s1];
                 }
             }
             const uint32_t sl = slot_of(s2);
 #pragma unroll
             for (int x = 0; x < NB; ++x) {
-                // C'(empty set) = 0 in the table (the unpacked C[0] is the sentinel)
-                const uint64_t v = (base | (uint32_t)x) == 0 ? 0u : out[x];
-                const uint64_t e = x & 1 ? v | base | (uint32_t)x : v;     // odd entries tagged
-                rS[lpos(sl, mpos(x))] = Key<K>::entry(e);
-                Cp[a_hi + lpos(sl, mpos(x))] = Key<K>::store(e);
-                split[base + x] = sp[x];
+                const uint64_t tagged = out[x] | base | ((uint32_t)x << H);
+                rS[lpos(sl, x)] = Key<K>::entry(tagged);
+                Tt[row + lpos(sl, x)] = Key<K>::store(tagged);
+                Pt[row + lpos(sl, x)] = Key<K>::store(out[x]);
+                Sr[row | (s2 << CB) | (uint32_t)x] = sp[x];
             }
         }
         lds_barrier();
@@ -1032,62 +967,31 @@ __device__ inline const K *lds_at(uint32_t off) {
 }
 
 // one base step (S2', A2') of the lifted cross-pair loop: three block
-// convolutions from four block loads. O1 orients S1 = 0 of (S2'|E, A2'),
-// O0 that of (S2', A2') and (S2'|E, A2'|E). off_a, off_b: LDS byte offsets
-// of blocks A2' and B2' = S2' ^ A2' in their rows; the blocks with E sit
-// NS2/2 slots above those without, a constant offset. ta, tb: shifted masks
-// of entry 0 of those two blocks. Each even entry is tagged in place once,
-// for all three convolutions, before the class that first needs it tagged.
-template <class K, bool O1, bool O0>
-__device__ __attribute__((always_inline)) inline void cross_step(uint32_t off_a, uint32_t off_b, uint32_t ta,
-                                                                 uint32_t tb, K best0[NB], K best1[NB]) {
-    static_assert(O0 || !O1, "block A2' is used plain for S1 = 0 after it is tagged");
+// convolutions from four block loads. off_a, off_b: LDS byte offsets of
+// blocks A2' (tagged row) and B2' = S2' ^ A2' (plain row); the blocks with
+// E sit NS2/2 slots above those without, a constant offset.
+template <class K>
+__device__ __attribute__((always_inline)) inline void cross_step(uint32_t off_a, uint32_t off_b, K best0[NB],
+                                                                 K best1[NB]) {
     constexpr uint32_t HALF = NS2 / 2;
-    constexpr int SH = Key<K>::SH;
-    constexpr uint32_t TE = HALF << (CB + SH);            // shifted mask of E
     const K *pa = lds_at<K>(off_a), *pb = lds_at<K>(off_b);
     K a0[NB], a1[NB], b0[NB], b1[NB];
     load_blk(pa, 0u, a0);                                 // A2'
     load_blk(pb, HALF, b1);                               // B2'|E
     load_blk(pb, 0u, b0);                                 // B2'
     load_blk(pa, HALF, a1);                               // A2'|E
-    // (S2'|E, A2') -> best1, (S2', A2') -> best0, (S2'|E, A2'|E) -> best1
-    conv_class<K, 1>(a0, b1, best1);
-    conv_class<K, 1>(a0, b0, best0);
-    conv_class<K, 1>(a1, b0, best1);
-    tag_entry<K, 2>(a0, ta); tag_entry<K, 2>(a1, ta | TE); tag_entry<K, 2>(b0, tb); tag_entry<K, 2>(b1, tb | TE);
-    conv_class<K, 2>(a0, b1, best1);
-    conv_class<K, 2>(a0, b0, best0);
-    conv_class<K, 2>(a1, b0, best1);
-    tag_entry<K, 4>(a0, ta); tag_entry<K, 4>(a1, ta | TE); tag_entry<K, 4>(b0, tb); tag_entry<K, 4>(b1, tb | TE);
-    conv_class<K, 4>(a0, b1, best1);
-    conv_class<K, 4>(a0, b0, best0);
-    conv_class<K, 4>(a1, b0, best1);
-    tag_entry<K, 6>(a0, ta); tag_entry<K, 6>(a1, ta | TE); tag_entry<K, 6>(b0, tb); tag_entry<K, 6>(b1, tb | TE);
-    conv_class<K, 6>(a0, b1, best1);
-    conv_class<K, 6>(a0, b0, best0);
-    conv_class<K, 6>(a1, b0, best1);
-    // S1 = 0
-    if (O1) tag_entry<K, 0>(a0, ta);
-    else tag_entry<K, 0>(b1, tb | TE);
-    best1[0] = Key<K>::min(best1[0], Key<K>::add(a0[0], b1[0]));
-    if (O0) {
-        if (!O1) tag_entry<K, 0>(a0, ta);
-        tag_entry<K, 0>(a1, ta | TE);
-    } else {
-        tag_entry<K, 0>(b0, tb);
-    }
-    best0[0] = Key<K>::min(best0[0], Key<K>::add(a0[0], b0[0]));
-    best1[0] = Key<K>::min(best1[0], Key<K>::add(a1[0], b0[0]));
+    conv_full<K>(a0, b1, best1);                          // (S2'|E, A2')
+    conv_full<K>(a0, b0, best0);                          // (S2', A2')
+    conv_full<K>(a1, b0, best1);                          // (S2'|E, A2'|E)
     __builtin_amdgcn_sched_barrier(0);
 }
 
 // cross pairs of one (S_H, chunk); fused = finish the row in place
 template <class K>
 __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_pairs, uint32_t chunks,
-                                                      uint32_t per_chunk, int fused, const int64_t *__restrict__ W,
-                                                      uint64_t *__restrict__ Cp, uint32_t *__restrict__ split,
-                                                      uint64_t *__restrict__ partial) {
+                                                      uint32_t per_chunk, int fused, const int64_t *__restrict__ Wr,
+                                                      uint64_t *__restrict__ Tt, uint64_t *__restrict__ Pt,
+                                                      uint32_t *__restrict__ Sr, uint64_t *__restrict__ partial) {
     __shared__ Lds<K> s;
     const uint32_t bid = xcd_block(blockIdx.x, gridDim.x);
     const uint32_t r = bid / chunks, j = bid % chunks;
@@ -1108,7 +1012,6 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
     const uint32_t slot_s2 = slot_of(s2);
     const uint32_t low2 = s2 & (0u - s2);
     const uint32_t low_off = slot_of(low2) * 16u;                    // block offset of lowbit(S2')
-    const uint32_t low_tag = low2 << (CB + Key<K>::SH);
     static_assert(RL == R2 - 1 && (1u << RL) == NS2 / 2, "E is the top middle bit");
     static_assert(NS2 / 2 * 16 <= 32 * 1024, "slot offsets stay below the row size");
     K best0[NB], best1[NB];
@@ -1118,14 +1021,14 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
     // pair t + 1 are copied into the other one
     auto pair = [&](auto cur_c, uint32_t t) {
         constexpr int CUR = decltype(cur_c)::value;
-        const uint32_t bh = sh ^ ah;
         copies_done();
         lds_barrier();     // rows of pair t in place; pair t - 1 done with the other buffer
         const uint32_t an = lowh | (((ah | ~rest) + 1u) & rest);    // next A_H holding lowbit(S_H)
         if (t + 1 < t1) {
-            copy_row(s.r[CUR ^ 1][0], Cp, an);
-            copy_row(s.r[CUR ^ 1][1], Cp, sh ^ an);
+            copy_row(s.r[CUR ^ 1][0], Tt, an);
+            copy_row(s.r[CUR ^ 1][1], Pt, sh ^ an);
         }
+        ah = an;
         // the buffers' LDS offsets (multiples of the 32 KiB row size), opaque
         // to the compiler: buffer 1 lies beyond the 16-bit immediate offsets
         // of LDS reads, and a known base would be folded into every read's
@@ -1134,38 +1037,30 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
         uint32_t oa = (uint32_t)(uintptr_t)(lds_k *)s.r[CUR][0];
         uint32_t ob = (uint32_t)(uintptr_t)(lds_k *)s.r[CUR][1];
         asm("" : "+s"(oa), "+s"(ob));
-        constexpr int SH = Key<K>::SH;
-        const uint32_t tag_a = ah << (L + SH);
-        const uint32_t tag_bs = ((bh << L) | (s2 << CB)) << SH;
-        ah = an;
         if (has_item) {
             if (s2 == 0) {
-                cross_step<K, false, true>(oa, ob, tag_a, tag_bs, best0, best1);
+                cross_step<K>(oa, ob, best0, best1);
             } else {
-                // t-th submask of S2' holds lowbit(S2') iff t is odd, and every
-                // item starts at an even t with an even count: the orientation
-                // of each step is fixed at compile time. The odd submask is
-                // the even one plus lowbit(S2'); slot_of is GF(2)-linear and
-                // the slot offsets (below 4 KiB) sit under the row offsets'
-                // zero bits, so its block offsets are the even step's XOR a
-                // constant of the item.
+                // every item starts at a submask without lowbit(S2') and has an
+                // even count; the odd submask is the even one plus lowbit(S2').
+                // slot_of is GF(2)-linear and the slot offsets (below 4 KiB) sit
+                // under the row offsets' zero bits, so its block offsets are the
+                // even step's XOR a constant of the item.
                 uint32_t a2 = a2_first;
                 for (uint32_t i = 0; i < cnt; i += 2) {
                     const uint32_t sa = slot_of(a2) & (NS2 / 2 - 1u);
                     const uint32_t sb = (slot_s2 ^ sa) & (NS2 / 2 - 1u);
                     const uint32_t off_a = oa + sa * 16u, off_b = ob + sb * 16u;
-                    const uint32_t ta = tag_a | (a2 << (CB + SH)), tb = tag_bs - (a2 << (CB + SH));
-                    cross_step<K, false, false>(off_a, off_b, ta, tb, best0, best1);
-                    cross_step<K, true, true>(off_a ^ low_off, off_b ^ low_off, ta | low_tag, tb - low_tag, best0,
-                                              best1);
+                    cross_step<K>(off_a, off_b, best0, best1);
+                    cross_step<K>(off_a ^ low_off, off_b ^ low_off, best0, best1);
                     a2 = ((a2 | low2 | ~s2) + 1u) & s2;            // two submasks on
                 }
             }
         }
     };
     if (t0 < t1) {
-        copy_row(s.r[0][0], Cp, ah);
-        copy_row(s.r[0][1], Cp, sh ^ ah);
+        copy_row(s.r[0][0], Tt, ah);
+        copy_row(s.r[0][1], Pt, sh ^ ah);
     }
     for (uint32_t t = t0; t < t1; t += 2) {
         pair(std::integral_constant<int, 0>{}, t);
@@ -1177,10 +1072,10 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
     }
     lds_barrier();
     if (fused) {
-        copy_row(s.r[0][1], Cp, 0u);
+        copy_row(s.r[0][1], Pt, 0u);
         copies_done();
         lds_barrier();
-        finalize_row<K>(m, sh, s, s.r[0][0], s.r[0][1], W, Cp, split);
+        finalize_row<K>(m, sh, s, s.r[0][0], s.r[0][1], Wr, Tt, Pt, Sr);
     } else {
         uint64_t *dst = partial + (size_t)bid * ROW;
         for (int e = threadIdx.x; e < ROW; e += THREADS) dst[e] = s.acc[e];
@@ -1207,44 +1102,137 @@ __global__ __launch_bounds__(256) void k_rb_reduce(uint32_t chunks, uint32_t gro
 }
 
 // finish the rows of one level: acc from the reduced partials (chunks > 0)
-// or empty (levels 0 and 1 have no cross pairs)
+// or empty (level 1 has no cross pairs)
 template <class K>
-__global__ __launch_bounds__(THREADS) void k_rb_final(int m, int h, uint32_t chunks, const int64_t *__restrict__ W,
-                                                      uint64_t *__restrict__ Cp, uint32_t *__restrict__ split,
-                                                      const uint64_t *__restrict__ partial) {
+__global__ __launch_bounds__(THREADS) void k_rb_final(int m, int h, uint32_t chunks, const int64_t *__restrict__ Wr,
+                                                      uint64_t *__restrict__ Tt, uint64_t *__restrict__ Pt,
+                                                      uint32_t *__restrict__ Sr, const uint64_t *__restrict__ partial) {
     __shared__ Lds<K> s;
     const uint32_t r = blockIdx.x;
     const uint32_t sh = unrank_colex(r, h, m - L);
     const uint64_t *src = partial + (size_t)r * chunks * ROW;
     for (int e = threadIdx.x; e < ROW; e += THREADS) s.acc[e] = chunks ? src[e] : ~0ull;
-    if (sh != 0) copy_row(s.r[0][1], Cp, 0u);
+    copy_row(s.r[0][1], Pt, 0u);
     copies_done();
     lds_barrier();
-    // for S_H = 0 the output row is row 0 itself
-    finalize_row<K>(m, sh, s, sh == 0 ? s.r[0][1] : s.r[0][0], s.r[0][1], W, Cp, split);
+    finalize_row<K>(m, sh, s, s.r[0][0], s.r[0][1], Wr, Tt, Pt, Sr);
 }
 
-// packed table -> C, one workgroup per row, in place: the whole row is
-// read before any of it is written (C[0] keeps the documented sentinel).
-// The low m bits of a stored value (a tag, or zero) drop out of C' >> m.
+// the in-row masks grouped by popcount, for the row-0 DP
+struct Subsets { uint16_t v[ROW]; int begin[L + 2]; };
+constexpr Subsets make_subsets() {
+    Subsets t{};
+    int count[L + 1] = {};
+    for (int e = 0; e < ROW; ++e) ++count[cpop(e)];
+    t.begin[0] = 0;
+    for (int k = 0; k <= L; ++k) t.begin[k + 1] = t.begin[k] + count[k];
+    int at[L + 1] = {};
+    for (int k = 0; k <= L; ++k) at[k] = t.begin[k];
+    for (int e = 0; e < ROW; ++e) t.v[at[cpop(e)]++] = (uint16_t)e;
+    return t;
+}
+__constant__ Subsets c_subsets = make_subsets();
+
+// Row 0: the DP over the L requests of the in-row part alone (S_H empty),
+// level by level in |S_L|, a group of lanes per subset; the key of a candidate is
+// C'(A) + C'(S ^ A) + A's mask, with A holding lowbit(S). Writes row 0 to the
+// plain table (it is only ever a B row) and its splits.
 template <class K>
-__global__ __launch_bounds__(THREADS) void k_rb_unpack(int m, int64_t *C) {
-    constexpr int PER = ROW / THREADS;
-    const uint32_t xh = blockIdx.x;
-    int64_t *row = C + ((size_t)xh << L);
-    int64_t v[PER];
-    uint32_t at[PER];
-#pragma unroll
-    for (int k = 0; k < PER; ++k) {
-        const uint32_t e = threadIdx.x + (uint32_t)k * THREADS;      // element of the stored row
-        const uint32_t q = e / PLANE, o = e % PLANE;
-        const int pos = (int)(2 * q + (o & 1u));
-        at[k] = (slot_of(o >> 1) << CB) | (uint32_t)ment(pos);     // slot_of is an involution
-        v[k] = (int64_t)(Key<K>::stored_value((uint64_t)row[e]) >> m);
+__global__ __launch_bounds__(THREADS) void k_rb_row0(int m, const int64_t *__restrict__ Wr,
+                                                     uint64_t *__restrict__ Pt, uint32_t *__restrict__ Sr) {
+    __shared__ uint64_t c[ROW];
+    __shared__ uint32_t spl[ROW];
+    const int H = m - L;
+    const uint64_t mask = ((uint64_t)1 << m) - 1u;
+    for (int e = threadIdx.x; e < ROW; e += THREADS) {
+        c[e] = __popc((uint32_t)e) == 1 ? (uint64_t)Wr[e] << m : 0u;     // C(empty) = 0 is never a part
+        spl[e] = 0u;
     }
     __syncthreads();
-#pragma unroll
-    for (int k = 0; k < PER; ++k) row[at[k]] = (xh == 0 && at[k] == 0) ? kInf : v[k];
+    const int wv = (int)(threadIdx.x / kWave), lane = (int)(threadIdx.x & (kWave - 1));
+    for (int p = 2; p <= L; ++p) {
+        // one thread per subset while a subset has at most 127 candidates
+        // (each level is then one round of the workgroup), a wave per subset
+        // above; lane li of a group takes candidates li, li + G, ..., its A'
+        // stepping by a masked add of G
+        const int G = p <= 8 ? 1 : kWave;
+        const uint32_t n_sub = (uint32_t)(c_subsets.begin[p + 1] - c_subsets.begin[p]);
+        const uint32_t per_wave = (uint32_t)(kWave / G);
+        const uint32_t gl = (uint32_t)(lane / G), li = (uint32_t)(lane % G);
+        for (uint32_t r0 = (uint32_t)wv * per_wave; r0 < n_sub; r0 += (uint32_t)(THREADS / kWave) * per_wave) {
+            const uint32_t r = r0 + gl;
+            uint64_t kb = ~0ull;
+            uint32_t S = 0;
+            if (r < n_sub) {
+                S = c_subsets.v[c_subsets.begin[p] + (int)r];
+                const uint32_t lb = S & (0u - S), rest = S ^ lb;
+                const uint32_t n_a = (1u << (p - 1)) - 1u;   // A = lb | A', A' a proper subset of rest
+                const uint32_t step = deposit((uint32_t)G, rest);
+                uint32_t ap = deposit(li, rest);
+                for (uint32_t t = li; t < n_a; t += (uint32_t)G) {
+                    const uint32_t A = lb | ap;
+                    const uint64_t key = c[A] + c[S ^ A] + ((uint64_t)A << H);
+                    kb = key < kb ? key : kb;
+                    ap = ((ap | ~rest) + step) & rest;
+                }
+            }
+            for (int off = G / 2; off > 0; off >>= 1) {
+                const uint64_t o = __shfl_xor(kb, off, kWave);
+                kb = o < kb ? o : kb;
+            }
+            if (r < n_sub && li == 0) {
+                c[S] = ((kb >> m) - (uint64_t)Wr[S]) << m;
+                spl[S] = (uint32_t)(kb & mask);
+            }
+        }
+        __syncthreads();
+    }
+    for (int e = threadIdx.x; e < ROW; e += THREADS) {
+        Pt[lpos(slot_of((uint32_t)e >> CB), e & (NB - 1))] = Key<K>::store(c[e]);
+        Sr[e] = spl[e];
+    }
+}
+
+// plain table -> C in mask order: C[S_H | S_L << H] = C'(S) >> m (C[0]
+// keeps the documented sentinel). Tiles of 64 rows x 64 stored elements go
+// through LDS, so reads run along rows and writes along S_H.
+template <class K>
+__global__ __launch_bounds__(256) void k_rb_unpack(int m, const uint64_t *__restrict__ Pt, int64_t *__restrict__ C) {
+    __shared__ int64_t tile[64][65];
+    const int H = m - L;
+    const uint32_t R = 1u << H;
+    const uint32_t r0 = blockIdx.x * 64u, e0 = blockIdx.y * 64u;
+    const int tx = (int)(threadIdx.x & 63u), ty = (int)(threadIdx.x >> 6);
+    for (int i = ty; i < 64; i += 4) {
+        const uint32_t r = r0 + (uint32_t)i;
+        if (r < R) tile[i][tx] = (int64_t)(Key<K>::stored_value(Pt[((size_t)r << L) + e0 + (uint32_t)tx]) >> m);
+    }
+    __syncthreads();
+    for (int jj = ty; jj < 64; jj += 4) {
+        const uint32_t e = e0 + (uint32_t)jj;                  // stored element of every row in the tile
+        const uint32_t q = e / PLANE, o = e % PLANE;
+        const uint32_t sl = (slot_of(o >> 1) << CB) | (2u * q + (o & 1u));   // its in-row mask
+        const uint32_t r = r0 + (uint32_t)tx;
+        if (r < R) C[(size_t)r | ((size_t)sl << H)] = (r == 0 && sl == 0) ? kInf : tile[tx][jj];
+    }
+}
+
+// out[c][r] = in[r][c] for a row-major R x Cn matrix, tiles of 64 x 64
+template <class T>
+__global__ __launch_bounds__(256) void k_transpose(const T *__restrict__ in, T *__restrict__ out, uint32_t R,
+                                                   uint32_t Cn) {
+    __shared__ T tile[64][65];
+    const uint32_t r0 = blockIdx.y * 64u, c0 = blockIdx.x * 64u;
+    const int tx = (int)(threadIdx.x & 63u), ty = (int)(threadIdx.x >> 6);
+    for (int i = ty; i < 64; i += 4) {
+        const uint32_t r = r0 + (uint32_t)i, c = c0 + (uint32_t)tx;
+        if (r < R && c < Cn) tile[i][tx] = in[(size_t)r * Cn + c];
+    }
+    __syncthreads();
+    for (int jj = ty; jj < 64; jj += 4) {
+        const uint32_t c = c0 + (uint32_t)jj, r = r0 + (uint32_t)tx;
+        if (r < R && c < Cn) out[(size_t)c * R + r] = tile[tx][jj];
+    }
 }
 
 // sum_i W({i}), saturated, for the packed-key eligibility test
@@ -1413,7 +1401,7 @@ size_t rb_partial_entries(int m) {
 }
 
 struct WsLayout {
-    size_t list_sig, list_w, part_v, part_a, keys, rb_part, total;
+    size_t list_sig, list_w, part_v, part_a, keys, rb_part, rb_plain, rb_wrow, rb_srow, total;
 };
 
 // keys sorted by the extraction: a power of two, at least one sort tile
@@ -1440,6 +1428,16 @@ WsLayout ws_layout(int m, int64_t nnz) {
     size_t ex_end = L.keys + align256(extract_keys(nnz) * 8);
     L.rb_part = off;
     size_t rb_end = L.rb_part + align256(rb_partial_entries(m) * 8);
+    if (m >= kRbMinM) {
+        // the packed DP's plain table, W and split in row order (the tagged
+        // table lives in the C buffer until the unpack)
+        L.rb_plain = rb_end;
+        rb_end += align256((size_t)8 << m);
+        L.rb_wrow = rb_end;
+        rb_end += align256((size_t)8 << m);
+        L.rb_srow = rb_end;
+        rb_end += align256((size_t)4 << m);
+    }
     L.total = std::max(std::max(build_end, rb_end), std::max(dp_end, ex_end));
     return L;
 }
@@ -1472,23 +1470,41 @@ int check_common(int m, int64_t n_chunks, int64_t nnz) {
 }
 
 template <class K>
-int solve_rb(int m, const int64_t *W, int64_t *C, uint32_t *split, uint64_t *partial, hipStream_t s) {
-    uint64_t *Cp = (uint64_t *)C;
+int solve_rb(int m, const int64_t *W, int64_t *C, uint32_t *split, char *ws, const WsLayout &Lw, hipStream_t s) {
+    uint64_t *Tt = (uint64_t *)C;                            // tagged table, until the unpack
+    uint64_t *Pt = (uint64_t *)(ws + Lw.rb_plain);
+    int64_t *Wr = (int64_t *)(ws + Lw.rb_wrow);
+    uint32_t *Sr = (uint32_t *)(ws + Lw.rb_srow);
+    uint64_t *partial = (uint64_t *)(ws + Lw.rb_part);
+    const int H = m - rb::L;
+    const uint32_t R = 1u << H;
+    const int64_t n = (int64_t)1 << m;
     double pair_work = 1.0;
     for (int i = 0; i < rb::L; ++i) pair_work *= 3.0;        // ordered (A_L, S_L) pairs of one row pair
+    {
+        // W in mask order is a 2^L x 2^H matrix (S_L, S_H); rows need it transposed
+        LaunchScope ls("rb_wrows", 16.0 * n, s);
+        rb::k_transpose<int64_t><<<dim3((R + 63) / 64, rb::ROW / 64), 256, 0, s>>>(W, Wr, (uint32_t)rb::ROW, R);
+    }
+    {
+        LaunchScope ls("rb_row0", pair_work / 2, s);
+        rb::k_rb_row0<K><<<1, rb::THREADS, 0, s>>>(m, Wr, Pt, Sr);
+    }
     for (const RbLevel &P : rb_plan(m)) {
+        if (P.h == 0) continue;                               // row 0: done above
         if (P.n_pairs == 0) {
             LaunchScope ls("rb_final", pair_work * P.n_sets, s);
-            rb::k_rb_final<K><<<P.n_sets, rb::THREADS, 0, s>>>(m, P.h, 0u, W, Cp, split, partial);
+            rb::k_rb_final<K><<<P.n_sets, rb::THREADS, 0, s>>>(m, P.h, 0u, Wr, Tt, Pt, Sr, partial);
         } else if (P.chunks == 1) {
             LaunchScope ls("rb_cross", pair_work * (double)P.n_sets * (P.n_pairs + 1), s);
-            rb::k_rb_cross<K><<<P.n_sets, rb::THREADS, 0, s>>>(m, P.h, P.n_pairs, 1u, P.n_pairs, 1, W, Cp, split,
+            rb::k_rb_cross<K><<<P.n_sets, rb::THREADS, 0, s>>>(m, P.h, P.n_pairs, 1u, P.n_pairs, 1, Wr, Tt, Pt, Sr,
                                                                partial);
         } else {
             {
                 LaunchScope ls("rb_cross", pair_work * (double)P.n_sets * P.n_pairs, s);
                 rb::k_rb_cross<K><<<P.n_sets * P.chunks, rb::THREADS, 0, s>>>(m, P.h, P.n_pairs, P.chunks,
-                                                                              P.per_chunk, 0, W, Cp, split, partial);
+                                                                              P.per_chunk, 0, Wr, Tt, Pt, Sr,
+                                                                              partial);
             }
             {
                 LaunchScope ls("rb_reduce", (double)P.n_sets * P.chunks * rb::ROW * 8.0, s);
@@ -1497,15 +1513,18 @@ int solve_rb(int m, const int64_t *W, int64_t *C, uint32_t *split, uint64_t *par
             }
             {
                 LaunchScope ls("rb_final", pair_work * P.n_sets, s);
-                rb::k_rb_final<K><<<P.n_sets, rb::THREADS, 0, s>>>(m, P.h, P.chunks, W, Cp, split, partial);
+                rb::k_rb_final<K><<<P.n_sets, rb::THREADS, 0, s>>>(m, P.h, P.chunks, Wr, Tt, Pt, Sr, partial);
             }
         }
         MPT_HIP_TRY(hipGetLastError());
     }
-    const int64_t n = (int64_t)1 << m;
     {
         LaunchScope ls("rb_unpack", 16.0 * n, s);
-        rb::k_rb_unpack<K><<<(unsigned)(n >> rb::L), rb::THREADS, 0, s>>>(m, C);
+        rb::k_rb_unpack<K><<<dim3((R + 63) / 64, rb::ROW / 64), 256, 0, s>>>(m, Pt, C);
+    }
+    {
+        LaunchScope ls("rb_split", 8.0 * n, s);
+        rb::k_transpose<uint32_t><<<dim3(rb::ROW / 64, (R + 63) / 64), 256, 0, s>>>(Sr, split, R, (uint32_t)rb::ROW);
     }
     MPT_HIP_TRY(hipGetLastError());
     return MPT_OK;
@@ -1616,12 +1635,11 @@ extern "C" int mpt_solve_exact(int m, const int64_t *W, int64_t *C, uint32_t *sp
         MPT_HIP_TRY(hipStreamSynchronize(s));
         // doubles while 2 C' < 2^52 (Key<double>); below 2^62 keys fit uint64
         if (total < ((int64_t)1 << (61 - m))) {
-            uint64_t *part = (uint64_t *)(ws + L.rb_part);
 #ifndef MPT_RB_NO_DOUBLE
 #define MPT_RB_NO_DOUBLE 0
 #endif
-            rc = (!MPT_RB_NO_DOUBLE && total < ((int64_t)1 << (51 - m))) ? solve_rb<double>(m, W, C, split, part, s)
-                                                   : solve_rb<uint64_t>(m, W, C, split, part, s);
+            rc = (!MPT_RB_NO_DOUBLE && total < ((int64_t)1 << (51 - m))) ? solve_rb<double>(m, W, C, split, ws, L, s)
+                                                   : solve_rb<uint64_t>(m, W, C, split, ws, L, s);
             if (rc) return rc;
             if (opt_cost) {
                 MPT_HIP_TRY(hipMemcpyAsync(opt_cost, C + (n - 1), sizeof(int64_t), hipMemcpyDeviceToHost, s));
