@@ -1200,38 +1200,63 @@ template <class K>
 __global__ __launch_bounds__(256) void k_rb_unpack(int m, const uint64_t *__restrict__ Pt, int64_t *__restrict__ C) {
     __shared__ int64_t tile[64][65];
     const int H = m - L;
-    const uint32_t R = 1u << H;
+    const uint32_t R = 1u << H;                                // rows, a power of two >= 2
     const uint32_t r0 = blockIdx.x * 64u, e0 = blockIdx.y * 64u;
-    const int tx = (int)(threadIdx.x & 63u), ty = (int)(threadIdx.x >> 6);
-    for (int i = ty; i < 64; i += 4) {
+    const int tx = (int)(threadIdx.x & 31u), ty = (int)(threadIdx.x >> 5);
+    // reads: 16 bytes (two stored elements) per lane along a row
+    for (int i = ty; i < 64; i += 8) {
         const uint32_t r = r0 + (uint32_t)i;
-        if (r < R) tile[i][tx] = (int64_t)(Key<K>::stored_value(Pt[((size_t)r << L) + e0 + (uint32_t)tx]) >> m);
+        if (r < R) {
+            const ulonglong2 v = *reinterpret_cast<const ulonglong2 *>(Pt + ((size_t)r << L) + e0 + 2u * (uint32_t)tx);
+            tile[i][2 * tx] = (int64_t)(Key<K>::stored_value(v.x) >> m);
+            tile[i][2 * tx + 1] = (int64_t)(Key<K>::stored_value(v.y) >> m);
+        }
     }
     __syncthreads();
-    for (int jj = ty; jj < 64; jj += 4) {
+    // writes: 16 bytes (two consecutive S_H) per lane along mask order
+    for (int jj = ty; jj < 64; jj += 8) {
         const uint32_t e = e0 + (uint32_t)jj;                  // stored element of every row in the tile
         const uint32_t q = e / PLANE, o = e % PLANE;
         const uint32_t sl = (slot_of(o >> 1) << CB) | (2u * q + (o & 1u));   // its in-row mask
-        const uint32_t r = r0 + (uint32_t)tx;
-        if (r < R) C[(size_t)r | ((size_t)sl << H)] = (r == 0 && sl == 0) ? kInf : tile[tx][jj];
+        const uint32_t r = r0 + 2u * (uint32_t)tx;
+        if (r < R) {
+            longlong2 v;
+            v.x = (r == 0 && sl == 0) ? kInf : tile[2 * tx][jj];
+            v.y = tile[2 * tx + 1][jj];
+            *reinterpret_cast<longlong2 *>(C + ((size_t)r | ((size_t)sl << H))) = v;
+        }
     }
 }
 
-// out[c][r] = in[r][c] for a row-major R x Cn matrix, tiles of 64 x 64
-template <class T>
+// out[c][r] = in[r][c] for a row-major R x Cn matrix, tiles of 64 x 64.
+// Each lane moves V consecutive elements per global access (R and Cn are
+// multiples of V).
+template <class T, int V>
 __global__ __launch_bounds__(256) void k_transpose(const T *__restrict__ in, T *__restrict__ out, uint32_t R,
                                                    uint32_t Cn) {
+    constexpr int TW = 64 / V;                 // lanes across 64 elements
+    constexpr int TH = 256 / TW;               // tile rows per pass
+    typedef T Vec __attribute__((ext_vector_type(V)));
     __shared__ T tile[64][65];
     const uint32_t r0 = blockIdx.y * 64u, c0 = blockIdx.x * 64u;
-    const int tx = (int)(threadIdx.x & 63u), ty = (int)(threadIdx.x >> 6);
-    for (int i = ty; i < 64; i += 4) {
-        const uint32_t r = r0 + (uint32_t)i, c = c0 + (uint32_t)tx;
-        if (r < R && c < Cn) tile[i][tx] = in[(size_t)r * Cn + c];
+    const int tx = (int)(threadIdx.x % TW), ty = (int)(threadIdx.x / TW);
+    for (int i = ty; i < 64; i += TH) {
+        const uint32_t r = r0 + (uint32_t)i, c = c0 + (uint32_t)(tx * V);
+        if (r < R && c < Cn) {
+            const Vec v = *reinterpret_cast<const Vec *>(in + (size_t)r * Cn + c);
+#pragma unroll
+            for (int k = 0; k < V; ++k) tile[i][tx * V + k] = v[k];
+        }
     }
     __syncthreads();
-    for (int jj = ty; jj < 64; jj += 4) {
-        const uint32_t c = c0 + (uint32_t)jj, r = r0 + (uint32_t)tx;
-        if (r < R && c < Cn) out[(size_t)c * R + r] = tile[tx][jj];
+    for (int jj = ty; jj < 64; jj += TH) {
+        const uint32_t c = c0 + (uint32_t)jj, r = r0 + (uint32_t)(tx * V);
+        if (r < R && c < Cn) {
+            Vec v;
+#pragma unroll
+            for (int k = 0; k < V; ++k) v[k] = tile[tx * V + k][jj];
+            *reinterpret_cast<Vec *>(out + (size_t)c * R + r) = v;
+        }
     }
 }
 
@@ -1484,7 +1509,7 @@ int solve_rb(int m, const int64_t *W, int64_t *C, uint32_t *split, char *ws, con
     {
         // W in mask order is a 2^L x 2^H matrix (S_L, S_H); rows need it transposed
         LaunchScope ls("rb_wrows", 16.0 * n, s);
-        rb::k_transpose<int64_t><<<dim3((R + 63) / 64, rb::ROW / 64), 256, 0, s>>>(W, Wr, (uint32_t)rb::ROW, R);
+        rb::k_transpose<int64_t, 2><<<dim3((R + 63) / 64, rb::ROW / 64), 256, 0, s>>>(W, Wr, (uint32_t)rb::ROW, R);
     }
     {
         LaunchScope ls("rb_row0", pair_work / 2, s);
@@ -1524,7 +1549,13 @@ int solve_rb(int m, const int64_t *W, int64_t *C, uint32_t *split, char *ws, con
     }
     {
         LaunchScope ls("rb_split", 8.0 * n, s);
-        rb::k_transpose<uint32_t><<<dim3(rb::ROW / 64, (R + 63) / 64), 256, 0, s>>>(Sr, split, R, (uint32_t)rb::ROW);
+        // 16-byte accesses need R (2^(m-12) rows) to be a multiple of 4
+        if (R >= 4)
+            rb::k_transpose<uint32_t, 4><<<dim3(rb::ROW / 64, (R + 63) / 64), 256, 0, s>>>(Sr, split, R,
+                                                                                       (uint32_t)rb::ROW);
+        else
+            rb::k_transpose<uint32_t, 1><<<dim3(rb::ROW / 64, (R + 63) / 64), 256, 0, s>>>(Sr, split, R,
+                                                                                       (uint32_t)rb::ROW);
     }
     MPT_HIP_TRY(hipGetLastError());
     return MPT_OK;
