@@ -99,6 +99,7 @@ int mpt_build_weights(int m, int64_t n_chunks, int64_t nnz,
  *                 children of S are split[S] and S ^ split[S].
  *   opt_cost      HOST out, nullable: C(full set) = OPT_free (Theorem 1).
  *                 When non-null the call synchronises `stream`.
+ * W, C and split need only the alignment of their element types.
  * For m >= 13 the call also synchronises `stream` once before its kernels,
  * to read sum_i W({i}) back: that total picks the key representation of the
  * packed kernels (exact doubles, uint64, or the plain kernels).

@@ -1195,8 +1195,9 @@ __global__ __launch_bounds__(THREADS) void k_rb_row0(int m, const int64_t *__res
 
 // plain table -> C in mask order: C[S_H | S_L << H] = C'(S) >> m (C[0]
 // keeps the documented sentinel). Tiles of 64 rows x 64 stored elements go
-// through LDS, so reads run along rows and writes along S_H.
-template <class K>
+// through LDS, so reads run along rows and writes along S_H; VEC writes two
+// entries per 16-byte store (C 16-byte aligned).
+template <class K, bool VEC>
 __global__ __launch_bounds__(256) void k_rb_unpack(int m, const uint64_t *__restrict__ Pt, int64_t *__restrict__ C) {
     __shared__ int64_t tile[64][65];
     const int H = m - L;
@@ -1220,10 +1221,14 @@ __global__ __launch_bounds__(256) void k_rb_unpack(int m, const uint64_t *__rest
         const uint32_t sl = (slot_of(o >> 1) << CB) | (2u * q + (o & 1u));   // its in-row mask
         const uint32_t r = r0 + 2u * (uint32_t)tx;
         if (r < R) {
-            longlong2 v;
-            v.x = (r == 0 && sl == 0) ? kInf : tile[2 * tx][jj];
-            v.y = tile[2 * tx + 1][jj];
-            *reinterpret_cast<longlong2 *>(C + ((size_t)r | ((size_t)sl << H))) = v;
+            const int64_t x = (r == 0 && sl == 0) ? kInf : tile[2 * tx][jj], y = tile[2 * tx + 1][jj];
+            int64_t *dst = C + ((size_t)r | ((size_t)sl << H));
+            if (VEC) {
+                *reinterpret_cast<longlong2 *>(dst) = make_longlong2(x, y);
+            } else {
+                dst[0] = x;
+                dst[1] = y;
+            }
         }
     }
 }
@@ -1426,7 +1431,7 @@ size_t rb_partial_entries(int m) {
 }
 
 struct WsLayout {
-    size_t list_sig, list_w, part_v, part_a, keys, rb_part, rb_plain, rb_wrow, rb_srow, total;
+    size_t list_sig, list_w, part_v, part_a, keys, rb_part, rb_tagged, rb_plain, rb_wrow, rb_srow, total;
 };
 
 // keys sorted by the extraction: a power of two, at least one sort tile
@@ -1454,8 +1459,9 @@ WsLayout ws_layout(int m, int64_t nnz) {
     L.rb_part = off;
     size_t rb_end = L.rb_part + align256(rb_partial_entries(m) * 8);
     if (m >= kRbMinM) {
-        // the packed DP's plain table, W and split in row order (the tagged
-        // table lives in the C buffer until the unpack)
+        // the packed DP's tagged and plain tables, W and split in row order
+        L.rb_tagged = rb_end;
+        rb_end += align256((size_t)8 << m);
         L.rb_plain = rb_end;
         rb_end += align256((size_t)8 << m);
         L.rb_wrow = rb_end;
@@ -1496,7 +1502,7 @@ int check_common(int m, int64_t n_chunks, int64_t nnz) {
 
 template <class K>
 int solve_rb(int m, const int64_t *W, int64_t *C, uint32_t *split, char *ws, const WsLayout &Lw, hipStream_t s) {
-    uint64_t *Tt = (uint64_t *)C;                            // tagged table, until the unpack
+    uint64_t *Tt = (uint64_t *)(ws + Lw.rb_tagged);
     uint64_t *Pt = (uint64_t *)(ws + Lw.rb_plain);
     int64_t *Wr = (int64_t *)(ws + Lw.rb_wrow);
     uint32_t *Sr = (uint32_t *)(ws + Lw.rb_srow);
@@ -1506,10 +1512,17 @@ int solve_rb(int m, const int64_t *W, int64_t *C, uint32_t *split, char *ws, con
     const int64_t n = (int64_t)1 << m;
     double pair_work = 1.0;
     for (int i = 0; i < rb::L; ++i) pair_work *= 3.0;        // ordered (A_L, S_L) pairs of one row pair
+    // the caller's W, C and split need not be 16-byte aligned: 16-byte
+    // accesses only where they are
+    auto aligned16 = [](const void *p) { return ((uintptr_t)p & 15u) == 0; };
     {
         // W in mask order is a 2^L x 2^H matrix (S_L, S_H); rows need it transposed
         LaunchScope ls("rb_wrows", 16.0 * n, s);
-        rb::k_transpose<int64_t, 2><<<dim3((R + 63) / 64, rb::ROW / 64), 256, 0, s>>>(W, Wr, (uint32_t)rb::ROW, R);
+        const dim3 grid((R + 63) / 64, rb::ROW / 64);
+        if (aligned16(W))
+            rb::k_transpose<int64_t, 2><<<grid, 256, 0, s>>>(W, Wr, (uint32_t)rb::ROW, R);
+        else
+            rb::k_transpose<int64_t, 1><<<grid, 256, 0, s>>>(W, Wr, (uint32_t)rb::ROW, R);
     }
     {
         LaunchScope ls("rb_row0", pair_work / 2, s);
@@ -1545,12 +1558,16 @@ int solve_rb(int m, const int64_t *W, int64_t *C, uint32_t *split, char *ws, con
     }
     {
         LaunchScope ls("rb_unpack", 16.0 * n, s);
-        rb::k_rb_unpack<K><<<dim3((R + 63) / 64, rb::ROW / 64), 256, 0, s>>>(m, Pt, C);
+        const dim3 grid((R + 63) / 64, rb::ROW / 64);
+        if (aligned16(C))
+            rb::k_rb_unpack<K, true><<<grid, 256, 0, s>>>(m, Pt, C);
+        else
+            rb::k_rb_unpack<K, false><<<grid, 256, 0, s>>>(m, Pt, C);
     }
     {
         LaunchScope ls("rb_split", 8.0 * n, s);
         // 16-byte accesses need R (2^(m-12) rows) to be a multiple of 4
-        if (R >= 4)
+        if (R >= 4 && aligned16(split))
             rb::k_transpose<uint32_t, 4><<<dim3(rb::ROW / 64, (R + 63) / 64), 256, 0, s>>>(Sr, split, R,
                                                                                        (uint32_t)rb::ROW);
         else

@@ -296,6 +296,36 @@ def test_max_m_full_solve():
     torch.cuda.empty_cache()
 
 
+@pytest.mark.parametrize("m", [13, 17])
+def test_unaligned_tables(m):
+    """The solve's W, C and split may start anywhere a whole element does
+    (the build's W output must be 16-byte aligned): offset views, 8- and
+    4-byte aligned but not 16, give the same tables as the oracle."""
+    inst = wl.gen_retrieval(m=m, u=600, topics=20, k=6, seed=41 + m)
+    say(f"[gpu] unaligned tables m={m}")
+    dev = torch.device("cuda")
+    n = 1 << m
+    t = lambda a, dt: torch.as_tensor(a, dtype=dt, device=dev)
+    W_built = torch.empty(n, dtype=torch.int64, device=dev)
+    W = torch.empty(n + 1, dtype=torch.int64, device=dev)[1:]
+    C = torch.empty(n + 1, dtype=torch.int64, device=dev)[1:]
+    split = torch.empty(n + 3, dtype=torch.int32, device=dev)[3:]
+    sig = torch.empty(max(1, inst.n_chunks), dtype=torch.int32, device=dev)
+    ws = mpt.alloc_workspace(m, inst.nnz, dev)
+    assert W.data_ptr() % 16 and C.data_ptr() % 16 and split.data_ptr() % 16
+    mpt.mpt_build_weights(m, inst.n_chunks, t(inst.weights, torch.int64), t(inst.req_off, torch.int64),
+                          t(inst.req_chunks, torch.int32), sig, W_built, ws)
+    W.copy_(W_built)
+    opt = mpt.mpt_solve_exact(m, W, C, split, ws)
+    torch.cuda.synchronize()
+    ref = oracle.solve(inst)
+    assert opt == ref["opt"]
+    assert np.array_equal(W.cpu().numpy(), ref["W"])
+    Cg = C.cpu().numpy()
+    assert Cg[0] == mpt.MPT_COST_SENTINEL and np.array_equal(Cg[1:], ref["C"][1:])
+    assert np.array_equal(split.cpu().numpy().view(np.uint32), ref["split"].astype(np.uint32))
+
+
 def test_determinism_and_reuse():
     inst = wl.config(3)
     prob = mpt.Problem(inst)
