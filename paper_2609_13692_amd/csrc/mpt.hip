@@ -789,7 +789,11 @@ __device__ inline void copy_row(void *dst, const uint64_t *__restrict__ tab, uin
         __builtin_amdgcn_global_load_lds(src + p0 + lane, (lds_void *)((char *)dst + p0 * 16), 16, 0, 0);
     }
 }
-__device__ inline void copies_done() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+// vmcnt(0), expcnt and lgkmcnt untouched (gfx9 encoding). The builtin, not
+// inline asm, so that the compiler's wait insertion sees the copies retire:
+// a pending direct-to-LDS copy (a flat-encoded instruction) makes it treat
+// the LDS counter as out of order and wait for every outstanding LDS read.
+__device__ inline void copies_done() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
 // deposit the low bits of t into the set bits of mask (in order)
 __device__ inline uint32_t deposit(uint32_t t, uint32_t mask) {
@@ -1040,6 +1044,7 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
         if (has_item) {
             if (s2 == 0) {
                 cross_step<K>(oa, ob, best0, best1);
+                copies_done();
             } else {
                 // every item starts at a submask without lowbit(S2') and has an
                 // even count; the odd submask is the even one plus lowbit(S2').
@@ -1047,14 +1052,20 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
                 // under the row offsets' zero bits, so its block offsets are the
                 // even step's XOR a constant of the item.
                 uint32_t a2 = a2_first;
-                for (uint32_t i = 0; i < cnt; i += 2) {
+                auto two = [&]() {
                     const uint32_t sa = slot_of(a2) & (NS2 / 2 - 1u);
                     const uint32_t sb = (slot_s2 ^ sa) & (NS2 / 2 - 1u);
                     const uint32_t off_a = oa + sa * 16u, off_b = ob + sb * 16u;
                     cross_step<K>(off_a, off_b, best0, best1);
                     cross_step<K>(off_a ^ low_off, off_b ^ low_off, best0, best1);
                     a2 = ((a2 | low2 | ~s2) + 1u) & s2;            // two submasks on
-                }
+                };
+                // the next pair's copies land while the first two steps run;
+                // retired before the loop on every path, they leave the loop's
+                // LDS reads free to wait only for what each use needs
+                two();
+                copies_done();
+                for (uint32_t i = 2; i < cnt; i += 2) two();
             }
         }
     };
