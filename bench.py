@@ -31,11 +31,14 @@ sys.path.insert(0, ROOT)
 # MI355X published figures used as peaks
 HBM_PEAK_GBS = 8000.0
 N_CU, CLOCK_GHZ = 256, 2.4
-VALU_PEAK_TOPS = N_CU * 64 * CLOCK_GHZ / 1000.0      # int32 lane-ops, T/s (39.3)
-# Algorithmic work of one evaluated bipartition: one 64-bit add of two keys
-# and one 64-bit min -- 2 VALU lane-ops, the least gfx950 needs (v_add_f64 +
-# v_min_f64 on exact-integer keys). Peak: 256 CUs x 64 lanes x 2.4 GHz.
-DP_OPS_PER_PAIR = 2
+VALU_PEAK_TOPS = N_CU * 64 * CLOCK_GHZ / 1000.0      # VALU lane-instructions, T/s (39.3)
+# VALU lane-instructions one evaluated bipartition needs at least, by the key
+# width the cross-pair kernel runs on. While sum_i w(R_i) < 2^20 - 1 the
+# library packs a key into 32 bits (cost << 12 | in-row part of A): one
+# v_add_u32 per candidate and one v_min3_u32 per two candidates, 1.5. Above
+# that, 64-bit keys held as exact-integer doubles: v_add_f64 + v_min_f64, 2.
+NARROW_TOTAL = (1 << 20) - 1
+DP_OPS_NARROW, DP_OPS_WIDE = 1.5, 2.0
 
 WORKLOADS = {
     1: "tiny random, m=12, u=64, k=4, w~U{1..32}, seed 0",
@@ -334,7 +337,10 @@ def main() -> int:
     dp_kernels = {k: v for k, v in prof.items() if k.startswith(("dp_", "rb_"))}
     dom = max(dp_kernels, key=lambda k: dp_kernels[k]["total_ms"])
     d = prof[dom]
-    achieved_tops = d["work"] * DP_OPS_PER_PAIR / (d["total_ms"] / 1000.0) / 1e12
+    total_w = int(inst.weights[inst.req_chunks].sum())              # sum_i w(R_i)
+    narrow = total_w < NARROW_TOTAL
+    ops_per_pair = DP_OPS_NARROW if narrow else DP_OPS_WIDE
+    achieved_tops = d["work"] * ops_per_pair / (d["total_ms"] / 1000.0) / 1e12
     dp_ms = sum(v["total_ms"] for v in dp_kernels.values()) / args.steps
     z = prof.get("weights_tile")
     zeta = None
@@ -382,7 +388,9 @@ def main() -> int:
                      "valu_issue_frac": (round(traffic["valu_issue_frac"], 4)
                                          if traffic and traffic["valu_issue_frac"] else None),
                      "avg_launch_ms": round(d["total_ms"] / d["launches"], 4),
-                     "ops_per_launch": d["work"] * DP_OPS_PER_PAIR / d["launches"]},
+                     "keys": "u32 (v_add_u32 + v_min3_u32)" if narrow else "f64 (v_add_f64 + v_min_f64)",
+                     "ops_per_pair": ops_per_pair,
+                     "ops_per_launch": d["work"] * ops_per_pair / d["launches"]},
         "zeta": zeta,
     }
     if not args.no_greedy:

@@ -697,6 +697,8 @@ template <> struct Key<uint64_t> {
     static __device__ inline uint64_t store(uint64_t v) { return v; }
     static __device__ inline uint64_t stored_value(uint64_t b) { return b; }
     static __device__ inline uint64_t load(uint64_t b) { return b; }
+    // packed key -> the bits the accumulators hold
+    static __device__ inline uint64_t key_bits(uint64_t k) { return k; }
 };
 template <> struct Key<double> {
     static constexpr uint64_t E52 = 0x4330000000000000ull;  // bits of 2^52
@@ -713,7 +715,27 @@ template <> struct Key<double> {
     static __device__ inline uint64_t store(uint64_t v) { return E52 | (v << 1); }
     static __device__ inline uint64_t stored_value(uint64_t b) { return (b & MANT) >> 1; }
     static __device__ inline double load(uint64_t b) { return from_bits(b); }
+    // packed key -> the bits of the sum that carries it: 2^53 + 2k
+    static __device__ inline uint64_t key_bits(uint64_t k) { return 0x4340000000000000ull | k; }
 };
+
+// Narrow keys, for the cross pairs while sum_i w(R_i) < 2^20 - 1. Every
+// C(A) + C(B) is then below 2^20 - 1 (a sub-instance costs at most the sum
+// of its request weights), and a candidate's key fits 32 bits:
+// (C(A) + C(B)) << L | A_L, A_L the in-row part of the part holding
+// lowbit(S). Inside one row pair A_H is fixed, so the order of these keys is
+// the order of (cost, A). The entries are C(X) << L | X_L (tagged) and
+// C(X) << L (plain), so a key is again one add, and the minimum over a
+// candidate chain becomes v_min3_u32 (two candidates per instruction).
+// Across the pairs of a chunk, taken in increasing A_H, each output entry
+// keeps beside its best key the A_H of the first pair that reached it.
+template <> struct Key<uint32_t> {
+    static __device__ inline uint32_t add(uint32_t a, uint32_t b) { return a + b; }
+    static __device__ inline uint32_t min(uint32_t a, uint32_t b) { return b < a ? b : a; }
+    static __device__ inline uint32_t none() { return 0xffffffffu; }
+};
+constexpr int64_t kNarrowTotal = (int64_t)1 << (32 - L);   // sum_i w(R_i) must stay below this - 1
+static_assert(32 - L >= 20, "narrow keys leave 20 bits for the cost");
 
 // Rows, in HBM and in LDS alike. Block x2 (the NB entries sharing the
 // middle mask x2) sits at slot(x2) = x2 ^ (x2 >> 3 & 7) ^ (x2 >> 6 & 3)
@@ -748,6 +770,13 @@ constexpr bool slots_ok() {
 }
 static_assert(R2 >= 7 && slots_ok(), "slot_of is an involution that puts the E half NS2/2 above the rest");
 static_assert(NB == 8 && (PLANE * 8) % 256 == 0, "four planes of 16-byte pieces, each a multiple of 256 bytes");
+// Narrow tables use the same slots with 4-byte elements: NB/4 planes of
+// 16-byte pieces, plane q holding entries 4q..4q+3 of every block, block at
+// slot s in piece s (a plane is 8 KiB, a row 16 KiB).
+constexpr int NPLANE = 4 * NS2;       // uint32 elements per narrow plane
+__host__ __device__ constexpr uint32_t npos(uint32_t slot, int x) {
+    return (uint32_t)(x >> 2) * NPLANE + slot * 4u + (uint32_t)(x & 3);
+}
 
 // two buffers of the (A, B) row pair: the next pair's rows are copied in
 // while the current pair runs
@@ -773,12 +802,26 @@ __device__ inline void load_blk(const K *row, uint32_t slot, K v[NB]) {
     }
 }
 
-// row xh of a table -> LDS dst, as direct global-to-LDS copies of 16 bytes
-// per lane (no registers held). Completion: this thread's vmcnt, then a
-// workgroup barrier.
+// narrow block at slot -> v[x] = entry x (two 16-byte reads)
+__device__ inline void load_blk(const uint32_t *row, uint32_t slot, uint32_t v[NB]) {
+    const uint4 *p = reinterpret_cast<const uint4 *>(row + slot * 4u);
+#pragma unroll
+    for (int q = 0; q < NB / 4; ++q) {
+        const uint4 t = p[q * (NPLANE / 4)];
+        v[4 * q] = t.x;
+        v[4 * q + 1] = t.y;
+        v[4 * q + 2] = t.z;
+        v[4 * q + 3] = t.w;
+    }
+}
+
+// row xh of a table of E-byte elements -> LDS dst, as direct global-to-LDS
+// copies of 16 bytes per lane (no registers held). Completion: this
+// thread's vmcnt, then a workgroup barrier.
 typedef __attribute__((address_space(3))) void lds_void;
-__device__ inline void copy_row(void *dst, const uint64_t *__restrict__ tab, uint32_t xh) {
-    constexpr int PIECES = ROW / 2;                      // 16-byte pieces per row
+template <class E>
+__device__ inline void copy_row(void *dst, const E *__restrict__ tab, uint32_t xh) {
+    constexpr int PIECES = ROW * (int)sizeof(E) / 16;    // 16-byte pieces per row
     constexpr int PER_WAVE = PIECES / (THREADS / kWave);
     static_assert(PER_WAVE % kWave == 0, "whole wave copies");
     const int w = (int)(threadIdx.x / kWave), lane = (int)(threadIdx.x & (kWave - 1));
@@ -825,6 +868,20 @@ __device__ inline void flush(const K best[NB], uint32_t s2, uint64_t *acc) {
     for (int x = 0; x < NB; ++x)
         if (best[x] != Key<K>::none())
             atomicMin((unsigned long long *)&acc[(s2 << CB) | x], (unsigned long long)Key<K>::bits(best[x]));
+}
+
+// narrow best keys of one output block, with the A_H of the pair that gave
+// each, as packed keys (cost << m | A_L << H | A_H) into the accumulator row
+template <class K>
+__device__ inline void flush_narrow(const uint32_t best[NB], const uint32_t bh[NB], uint32_t s2, int m,
+                                    uint64_t *acc) {
+    const int H = m - L;
+#pragma unroll
+    for (int x = 0; x < NB; ++x)
+        if (best[x] != Key<uint32_t>::none()) {
+            const uint64_t key = ((uint64_t)(best[x] >> L) << m) | ((uint64_t)(best[x] & (ROW - 1u)) << H) | bh[x];
+            atomicMin((unsigned long long *)&acc[(s2 << CB) | x], (unsigned long long)Key<K>::key_bits(key));
+        }
 }
 
 // DPP lane exchange of a 64-bit value inside rows of 8 lanes
@@ -883,12 +940,15 @@ __device__ inline void run_item(uint32_t item, const K *rA, const K *rB, uint64_
 
 // Complete row S_H (non-empty). s.acc holds the best cross-pair key bits (or
 // ~0); rS receives row S_H (tagged), r0 holds row 0 (plain). Writes the row
-// to both tables and its splits to Sr (row-major, mask order inside a row).
-template <class K>
+// to the plain table, to the tagged one (NARROW: to the two narrow tables
+// instead) and its splits to Sr (row-major, mask order inside a row).
+template <class K, bool NARROW>
 __device__ __attribute__((always_inline)) inline void finalize_row(int m, uint32_t sh, Lds<K> &s, K *rS, const K *r0,
                                                                    const int64_t *__restrict__ Wr,
                                                                    uint64_t *__restrict__ Tt,
                                                                    uint64_t *__restrict__ Pt,
+                                                                   uint32_t *__restrict__ Tn,
+                                                                   uint32_t *__restrict__ Pn,
                                                                    uint32_t *__restrict__ Sr) {
     const int H = m - L;
     const uint32_t row = sh << L;
@@ -954,9 +1014,24 @@ __device__ __attribute__((always_inline)) inline void finalize_row(int m, uint32
             for (int x = 0; x < NB; ++x) {
                 const uint64_t tagged = out[x] | base | ((uint32_t)x << H);
                 rS[lpos(sl, x)] = Key<K>::entry(tagged);
-                Tt[row + lpos(sl, x)] = Key<K>::store(tagged);
+                if (!NARROW) Tt[row + lpos(sl, x)] = Key<K>::store(tagged);
                 Pt[row + lpos(sl, x)] = Key<K>::store(out[x]);
                 Sr[row | (s2 << CB) | (uint32_t)x] = sp[x];
+            }
+            if (NARROW) {
+                // C(X) << L, and tagged with X_L = S2 << CB | X1
+                uint32_t pn[NB];
+#pragma unroll
+                for (int x = 0; x < NB; ++x) pn[x] = (uint32_t)(out[x] >> m) << L;
+                const uint32_t tag = s2 << CB;
+#pragma unroll
+                for (int q = 0; q < NB / 4; ++q) {
+                    const uint32_t at = row + npos(sl, 4 * q);
+                    *reinterpret_cast<uint4 *>(Pn + at) = make_uint4(pn[4 * q], pn[4 * q + 1], pn[4 * q + 2], pn[4 * q + 3]);
+                    *reinterpret_cast<uint4 *>(Tn + at) =
+                        make_uint4(pn[4 * q] | tag | (4u * q), pn[4 * q + 1] | tag | (4u * q + 1u),
+                                   pn[4 * q + 2] | tag | (4u * q + 2u), pn[4 * q + 3] | tag | (4u * q + 3u));
+                }
             }
         }
         lds_barrier();
@@ -973,29 +1048,34 @@ __device__ inline const K *lds_at(uint32_t off) {
 // one base step (S2', A2') of the lifted cross-pair loop: three block
 // convolutions from four block loads. off_a, off_b: LDS byte offsets of
 // blocks A2' (tagged row) and B2' = S2' ^ A2' (plain row); the blocks with
-// E sit NS2/2 slots above those without, a constant offset.
-template <class K>
-__device__ __attribute__((always_inline)) inline void cross_step(uint32_t off_a, uint32_t off_b, K best0[NB],
-                                                                 K best1[NB]) {
+// E sit NS2/2 slots above those without, a constant offset. KI is the key
+// type in LDS: a wide K, or uint32_t for narrow rows.
+template <class KI>
+__device__ __attribute__((always_inline)) inline void cross_step(uint32_t off_a, uint32_t off_b, KI best0[NB],
+                                                                 KI best1[NB]) {
     constexpr uint32_t HALF = NS2 / 2;
-    const K *pa = lds_at<K>(off_a), *pb = lds_at<K>(off_b);
-    K a0[NB], a1[NB], b0[NB], b1[NB];
+    const KI *pa = lds_at<KI>(off_a), *pb = lds_at<KI>(off_b);
+    KI a0[NB], a1[NB], b0[NB], b1[NB];
     load_blk(pa, 0u, a0);                                 // A2'
     load_blk(pb, HALF, b1);                               // B2'|E
     load_blk(pb, 0u, b0);                                 // B2'
     load_blk(pa, HALF, a1);                               // A2'|E
-    conv_full<K>(a0, b1, best1);                          // (S2'|E, A2')
-    conv_full<K>(a0, b0, best0);                          // (S2', A2')
-    conv_full<K>(a1, b0, best1);                          // (S2'|E, A2'|E)
+    conv_full<KI>(a0, b1, best1);                         // (S2'|E, A2')
+    conv_full<KI>(a0, b0, best0);                         // (S2', A2')
+    conv_full<KI>(a1, b0, best1);                         // (S2'|E, A2'|E)
     __builtin_amdgcn_sched_barrier(0);
 }
 
-// cross pairs of one (S_H, chunk); fused = finish the row in place
-template <class K>
+// cross pairs of one (S_H, chunk); fused = finish the row in place. NARROW:
+// the pairs run on the narrow tables (Tn tagged, Pn plain), two buffers of
+// 16 KiB rows at the start of the wide rows' space.
+template <class K, bool NARROW>
 __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_pairs, uint32_t chunks,
                                                       uint32_t per_chunk, int fused, const int64_t *__restrict__ Wr,
                                                       uint64_t *__restrict__ Tt, uint64_t *__restrict__ Pt,
+                                                      uint32_t *__restrict__ Tn, uint32_t *__restrict__ Pn,
                                                       uint32_t *__restrict__ Sr, uint64_t *__restrict__ partial) {
+    typedef typename std::conditional<NARROW, uint32_t, K>::type KI;
     __shared__ Lds<K> s;
     const uint32_t bid = xcd_block(blockIdx.x, gridDim.x);
     const uint32_t r = bid / chunks, j = bid % chunks;
@@ -1017,33 +1097,56 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
     const uint32_t low2 = s2 & (0u - s2);
     const uint32_t low_off = slot_of(low2) * 16u;                    // block offset of lowbit(S2')
     static_assert(RL == R2 - 1 && (1u << RL) == NS2 / 2, "E is the top middle bit");
-    static_assert(NS2 / 2 * 16 <= 32 * 1024, "slot offsets stay below the row size");
-    K best0[NB], best1[NB];
+    static_assert(NS2 / 2 * 16 <= 16 * 1024, "slot offsets stay below the row size");
+    KI best0[NB], best1[NB];
+    uint32_t bh0[NB], bh1[NB];                                       // NARROW: A_H of each best key
 #pragma unroll
-    for (int x = 0; x < NB; ++x) { best0[x] = Key<K>::none(); best1[x] = Key<K>::none(); }
+    for (int x = 0; x < NB; ++x) {
+        best0[x] = Key<KI>::none();
+        best1[x] = Key<KI>::none();
+        bh0[x] = 0u;
+        bh1[x] = 0u;
+    }
+    // row buffer [buf][side] of this kernel's key type
+    auto buf = [&](int b, int side) -> KI * {
+        if constexpr (NARROW) return reinterpret_cast<uint32_t *>(&s.r[0][0][0]) + (b * 2 + side) * ROW;
+        else return s.r[b][side];
+    };
+    auto copy_pair = [&](int b, uint32_t a_h) {
+        if constexpr (NARROW) {
+            copy_row(buf(b, 0), Tn, a_h);
+            copy_row(buf(b, 1), Pn, sh ^ a_h);
+        } else {
+            copy_row(buf(b, 0), Tt, a_h);
+            copy_row(buf(b, 1), Pt, sh ^ a_h);
+        }
+    };
     // pair t of the chunk runs on buffer (t - t0) & 1 while the rows of
     // pair t + 1 are copied into the other one
     auto pair = [&](auto cur_c, uint32_t t) {
         constexpr int CUR = decltype(cur_c)::value;
         copies_done();
         lds_barrier();     // rows of pair t in place; pair t - 1 done with the other buffer
+        const uint32_t ah_cur = ah;
         const uint32_t an = lowh | (((ah | ~rest) + 1u) & rest);    // next A_H holding lowbit(S_H)
-        if (t + 1 < t1) {
-            copy_row(s.r[CUR ^ 1][0], Tt, an);
-            copy_row(s.r[CUR ^ 1][1], Pt, sh ^ an);
-        }
+        if (t + 1 < t1) copy_pair(CUR ^ 1, an);
         ah = an;
-        // the buffers' LDS offsets (multiples of the 32 KiB row size), opaque
-        // to the compiler: buffer 1 lies beyond the 16-bit immediate offsets
-        // of LDS reads, and a known base would be folded into every read's
-        // address instead of added once
-        typedef __attribute__((address_space(3))) const K lds_k;
-        uint32_t oa = (uint32_t)(uintptr_t)(lds_k *)s.r[CUR][0];
-        uint32_t ob = (uint32_t)(uintptr_t)(lds_k *)s.r[CUR][1];
+        // the buffers' LDS offsets (multiples of the row size), opaque to the
+        // compiler: a known base would be folded into every read's address
+        // instead of added once (and wide buffer 1 lies beyond the 16-bit
+        // immediate offsets of LDS reads)
+        typedef __attribute__((address_space(3))) const KI lds_k;
+        uint32_t oa = (uint32_t)(uintptr_t)(lds_k *)buf(CUR, 0);
+        uint32_t ob = (uint32_t)(uintptr_t)(lds_k *)buf(CUR, 1);
         asm("" : "+s"(oa), "+s"(ob));
         if (has_item) {
+            KI old0[NB], old1[NB];
+            if constexpr (NARROW) {
+#pragma unroll
+                for (int x = 0; x < NB; ++x) { old0[x] = best0[x]; old1[x] = best1[x]; }
+            }
             if (s2 == 0) {
-                cross_step<K>(oa, ob, best0, best1);
+                cross_step<KI>(oa, ob, best0, best1);
                 copies_done();
             } else {
                 // every item starts at a submask without lowbit(S2') and has an
@@ -1056,8 +1159,8 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
                     const uint32_t sa = slot_of(a2) & (NS2 / 2 - 1u);
                     const uint32_t sb = (slot_s2 ^ sa) & (NS2 / 2 - 1u);
                     const uint32_t off_a = oa + sa * 16u, off_b = ob + sb * 16u;
-                    cross_step<K>(off_a, off_b, best0, best1);
-                    cross_step<K>(off_a ^ low_off, off_b ^ low_off, best0, best1);
+                    cross_step<KI>(off_a, off_b, best0, best1);
+                    cross_step<KI>(off_a ^ low_off, off_b ^ low_off, best0, best1);
                     a2 = ((a2 | low2 | ~s2) + 1u) & s2;            // two submasks on
                 };
                 // the next pair's copies land while the first two steps run;
@@ -1067,26 +1170,37 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
                 copies_done();
                 for (uint32_t i = 2; i < cnt; i += 2) two();
             }
+            if constexpr (NARROW) {
+                // a key this pair lowered came from this pair; an equal key
+                // keeps the earlier, smaller A_H
+#pragma unroll
+                for (int x = 0; x < NB; ++x) {
+                    bh0[x] = best0[x] < old0[x] ? ah_cur : bh0[x];
+                    bh1[x] = best1[x] < old1[x] ? ah_cur : bh1[x];
+                }
+            }
         }
     };
-    if (t0 < t1) {
-        copy_row(s.r[0][0], Tt, ah);
-        copy_row(s.r[0][1], Pt, sh ^ ah);
-    }
+    if (t0 < t1) copy_pair(0, ah);
     for (uint32_t t = t0; t < t1; t += 2) {
         pair(std::integral_constant<int, 0>{}, t);
         if (t + 1 < t1) pair(std::integral_constant<int, 1>{}, t + 1);
     }
     if (has_item) {
-        flush<K>(best0, s2, s.acc);
-        flush<K>(best1, s2 | E, s.acc);
+        if constexpr (NARROW) {
+            flush_narrow<K>(best0, bh0, s2, m, s.acc);
+            flush_narrow<K>(best1, bh1, s2 | E, m, s.acc);
+        } else {
+            flush<K>(best0, s2, s.acc);
+            flush<K>(best1, s2 | E, s.acc);
+        }
     }
     lds_barrier();
     if (fused) {
         copy_row(s.r[0][1], Pt, 0u);
         copies_done();
         lds_barrier();
-        finalize_row<K>(m, sh, s, s.r[0][0], s.r[0][1], Wr, Tt, Pt, Sr);
+        finalize_row<K, NARROW>(m, sh, s, s.r[0][0], s.r[0][1], Wr, Tt, Pt, Tn, Pn, Sr);
     } else {
         uint64_t *dst = partial + (size_t)bid * ROW;
         for (int e = threadIdx.x; e < ROW; e += THREADS) dst[e] = s.acc[e];
@@ -1114,9 +1228,10 @@ __global__ __launch_bounds__(256) void k_rb_reduce(uint32_t chunks, uint32_t gro
 
 // finish the rows of one level: acc from the reduced partials (chunks > 0)
 // or empty (level 1 has no cross pairs)
-template <class K>
+template <class K, bool NARROW>
 __global__ __launch_bounds__(THREADS) void k_rb_final(int m, int h, uint32_t chunks, const int64_t *__restrict__ Wr,
                                                       uint64_t *__restrict__ Tt, uint64_t *__restrict__ Pt,
+                                                      uint32_t *__restrict__ Tn, uint32_t *__restrict__ Pn,
                                                       uint32_t *__restrict__ Sr, const uint64_t *__restrict__ partial) {
     __shared__ Lds<K> s;
     const uint32_t r = blockIdx.x;
@@ -1126,7 +1241,7 @@ __global__ __launch_bounds__(THREADS) void k_rb_final(int m, int h, uint32_t chu
     copy_row(s.r[0][1], Pt, 0u);
     copies_done();
     lds_barrier();
-    finalize_row<K>(m, sh, s, s.r[0][0], s.r[0][1], Wr, Tt, Pt, Sr);
+    finalize_row<K, NARROW>(m, sh, s, s.r[0][0], s.r[0][1], Wr, Tt, Pt, Tn, Pn, Sr);
 }
 
 // the in-row masks grouped by popcount, for the row-0 DP
@@ -1511,9 +1626,12 @@ int check_common(int m, int64_t n_chunks, int64_t nnz) {
     return MPT_OK;
 }
 
-template <class K>
+template <class K, bool NARROW>
 int solve_rb(int m, const int64_t *W, int64_t *C, uint32_t *split, char *ws, const WsLayout &Lw, hipStream_t s) {
-    uint64_t *Tt = (uint64_t *)(ws + Lw.rb_tagged);
+    // NARROW: the two narrow tables take the wide tagged table's space
+    uint64_t *Tt = NARROW ? nullptr : (uint64_t *)(ws + Lw.rb_tagged);
+    uint32_t *Tn = NARROW ? (uint32_t *)(ws + Lw.rb_tagged) : nullptr;
+    uint32_t *Pn = NARROW ? Tn + ((size_t)1 << m) : nullptr;
     uint64_t *Pt = (uint64_t *)(ws + Lw.rb_plain);
     int64_t *Wr = (int64_t *)(ws + Lw.rb_wrow);
     uint32_t *Sr = (uint32_t *)(ws + Lw.rb_srow);
@@ -1543,17 +1661,16 @@ int solve_rb(int m, const int64_t *W, int64_t *C, uint32_t *split, char *ws, con
         if (P.h == 0) continue;                               // row 0: done above
         if (P.n_pairs == 0) {
             LaunchScope ls("rb_final", pair_work * P.n_sets, s);
-            rb::k_rb_final<K><<<P.n_sets, rb::THREADS, 0, s>>>(m, P.h, 0u, Wr, Tt, Pt, Sr, partial);
+            rb::k_rb_final<K, NARROW><<<P.n_sets, rb::THREADS, 0, s>>>(m, P.h, 0u, Wr, Tt, Pt, Tn, Pn, Sr, partial);
         } else if (P.chunks == 1) {
             LaunchScope ls("rb_cross", pair_work * (double)P.n_sets * (P.n_pairs + 1), s);
-            rb::k_rb_cross<K><<<P.n_sets, rb::THREADS, 0, s>>>(m, P.h, P.n_pairs, 1u, P.n_pairs, 1, Wr, Tt, Pt, Sr,
-                                                               partial);
+            rb::k_rb_cross<K, NARROW><<<P.n_sets, rb::THREADS, 0, s>>>(m, P.h, P.n_pairs, 1u, P.n_pairs, 1, Wr, Tt,
+                                                                       Pt, Tn, Pn, Sr, partial);
         } else {
             {
                 LaunchScope ls("rb_cross", pair_work * (double)P.n_sets * P.n_pairs, s);
-                rb::k_rb_cross<K><<<P.n_sets * P.chunks, rb::THREADS, 0, s>>>(m, P.h, P.n_pairs, P.chunks,
-                                                                              P.per_chunk, 0, Wr, Tt, Pt, Sr,
-                                                                              partial);
+                rb::k_rb_cross<K, NARROW><<<P.n_sets * P.chunks, rb::THREADS, 0, s>>>(
+                    m, P.h, P.n_pairs, P.chunks, P.per_chunk, 0, Wr, Tt, Pt, Tn, Pn, Sr, partial);
             }
             {
                 LaunchScope ls("rb_reduce", (double)P.n_sets * P.chunks * rb::ROW * 8.0, s);
@@ -1562,7 +1679,8 @@ int solve_rb(int m, const int64_t *W, int64_t *C, uint32_t *split, char *ws, con
             }
             {
                 LaunchScope ls("rb_final", pair_work * P.n_sets, s);
-                rb::k_rb_final<K><<<P.n_sets, rb::THREADS, 0, s>>>(m, P.h, P.chunks, Wr, Tt, Pt, Sr, partial);
+                rb::k_rb_final<K, NARROW><<<P.n_sets, rb::THREADS, 0, s>>>(m, P.h, P.chunks, Wr, Tt, Pt, Tn, Pn, Sr,
+                                                                        partial);
             }
         }
         MPT_HIP_TRY(hipGetLastError());
@@ -1697,8 +1815,18 @@ extern "C" int mpt_solve_exact(int m, const int64_t *W, int64_t *C, uint32_t *sp
 #ifndef MPT_RB_NO_DOUBLE
 #define MPT_RB_NO_DOUBLE 0
 #endif
-            rc = (!MPT_RB_NO_DOUBLE && total < ((int64_t)1 << (51 - m))) ? solve_rb<double>(m, W, C, split, ws, L, s)
-                                                   : solve_rb<uint64_t>(m, W, C, split, ws, L, s);
+#ifndef MPT_RB_NO_NARROW
+#define MPT_RB_NO_NARROW 0
+#endif
+            // narrow cross-pair keys while every C(A) + C(B) stays below 2^20 - 1
+            // (then 2 C' < 2^52 too, for any m up to 30)
+            static_assert(rb::kNarrowTotal <= ((int64_t)1 << (51 - MPT_MAX_M)), "narrow keys imply double keys");
+            if (!MPT_RB_NO_DOUBLE && !MPT_RB_NO_NARROW && total < rb::kNarrowTotal - 1)
+                rc = solve_rb<double, true>(m, W, C, split, ws, L, s);
+            else if (!MPT_RB_NO_DOUBLE && total < ((int64_t)1 << (51 - m)))
+                rc = solve_rb<double, false>(m, W, C, split, ws, L, s);
+            else
+                rc = solve_rb<uint64_t, false>(m, W, C, split, ws, L, s);
             if (rc) return rc;
             if (opt_cost) {
                 MPT_HIP_TRY(hipMemcpyAsync(opt_cost, C + (n - 1), sizeof(int64_t), hipMemcpyDeviceToHost, s));

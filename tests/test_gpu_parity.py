@@ -235,6 +235,46 @@ def test_double_keys_at_their_limit(excess):
     assert_same(inst, got, oracle.solve(inst))
 
 
+@pytest.mark.parametrize("excess", [-1, 0])
+def test_narrow_keys_at_their_limit(excess):
+    """Cross pairs run on 32-bit keys (cost << 12 | in-row part of A) while
+    sum_i w(R_i) < 2^20 - 1, and on doubles from there on. The total is set
+    to 2^20 - 1 + excess with mostly private chunks, so the top-level
+    candidates reach the largest narrow keys (m = 16: levels of up to 7
+    cross pairs per row)."""
+    m = 16
+    rng = np.random.default_rng(41 + excess)
+    n = 120
+    target = (1 << 20) - 1 + excess
+    w = list(rng.integers(1, 64, size=n, dtype=np.int64))
+    sets = [rng.choice(n, size=int(rng.integers(4, 12)), replace=False).tolist() for _ in range(m)]
+    left = target - int(sum(sum(w[x] for x in s) for s in sets))
+    assert left > 0
+    for i in range(m):
+        piece = left // (m - i)
+        w.append(piece)
+        sets[i].append(len(w) - 1)
+        left -= piece
+    w = np.array(w, dtype=np.int64)
+    inst = wl.from_sets(sets, w, len(w))
+    assert int(sum(w[s].sum() for s in sets)) == target
+    got = gpu_run(inst)
+    assert_same(inst, got, oracle.solve(inst))
+
+
+@pytest.mark.parametrize("seed", [1, 2])
+def test_narrow_keys_with_many_ties(seed):
+    """Unit weights over a small universe: many bipartitions tie on cost and
+    on the in-row part of A, differing only in the row part A_H, which the
+    narrow path keeps beside each best key (m = 18, up to 31 cross pairs per
+    row, split over chunks)."""
+    rng = np.random.default_rng(700 + seed)
+    sets = [rng.choice(10, size=int(rng.integers(2, 6)), replace=False).tolist() for _ in range(18)]
+    inst = wl.from_sets(sets, np.ones(10, dtype=np.int64), 10)
+    got = gpu_run(inst)
+    assert_same(inst, got, oracle.solve(inst))
+
+
 def test_costs_too_large_to_pack_take_the_plain_kernels():
     """With sum_i w(R_i) >= 2^(61-m) the packed-key kernels are not used;
     the result must not change."""
