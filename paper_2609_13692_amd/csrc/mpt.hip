@@ -611,66 +611,70 @@ __constant__ Items c_items = kItems;
 // so four block loads serve three block convolutions. Each thread owns
 // exactly one item -- the same for every row pair of its chunk -- and keeps
 // the best keys of its two output blocks in registers across all pairs,
-// flushing them once. Items: chunks of 8 submasks A2' of S2' (|S2'| >= 3),
-// enough of them halved into chunks of 4, and the small S2' whole, so that
-// the items fill THREADS slots; bigger items come first so the lanes of a
-// wave mostly run the same count. Entry: S2' | first A2' << 8 |
-// log2(count) << 16 | 1 << 31 (0 = no item).
+// flushing them once. An item is a run of consecutive submasks A2' of one
+// S2' (in increasing order), starting at an even index with an even count
+// (the S2' = 0 item is its single submask).
+//
+// The waves of a workgroup go to the four SIMDs in turn, and every pair ends
+// at a workgroup barrier, so the SIMD with the most steps sets the pace. The
+// runs are cut to step capacities by wave: the first half of the waves take
+// runs of 8, the next quarter runs of up to 6, the last quarter runs of up to
+// 4, so that each SIMD gets two waves of 8, one of 6 and one of 4 steps
+// (26, against 3^(R2-1) / 64 / 4 = 25.6 at least). The S2' are taken by
+// decreasing popcount; a run never leaves a remainder of 2 that would need
+// a lane of its own. Entry: S2' | first A2' << 8 | count << 16 | 1 << 31
+// (0 = no item).
 constexpr int RL = R2 - 1;
-struct ThreadItems { uint32_t v[THREADS]; int n_big; int n_small; int n_split; };
-constexpr uint32_t titem(int s2, int a2, int lg) {
-    return (uint32_t)s2 | ((uint32_t)a2 << 8) | ((uint32_t)lg << 16) | (1u << 31);
+struct ThreadItems { uint32_t v[THREADS]; bool ok; };
+constexpr uint32_t titem(int s2, int a2, int cnt) {
+    return (uint32_t)s2 | ((uint32_t)a2 << 8) | ((uint32_t)cnt << 16) | (1u << 31);
 }
 constexpr ThreadItems make_thread_items() {
     ThreadItems t{};
-    int n_big = 0, n_small = 0;
-    for (int s = 0; s < (1 << RL); ++s) {
-        if (cpop(s) >= 3) n_big += 1 << (cpop(s) - 3);
-        else ++n_small;
-    }
-    int n_split = THREADS - n_big - n_small;
-    if (n_split < 0) n_split = 0;
-    if (n_split > n_big) n_split = n_big;
-    t.n_big = n_big; t.n_small = n_small; t.n_split = n_split;
-    int whole = 0, halves = n_big - n_split, seen = 0, small = 2 * n_split + n_big - n_split;
+    constexpr int WAVES = THREADS / kWave;
+    // lane classes: [0, nA) capacity 8, [nA, nA + nB) 6, the rest 4
+    const int nA = WAVES / 2 * kWave, nB = WAVES / 4 * kWave;
+    int at[3] = {0, nA, nA + nB};
+    const int end[3] = {nA, nA + nB, THREADS};
+    t.ok = true;
     for (int k = RL; k >= 0; --k)
         for (int s = 0; s < (1 << RL); ++s) {
             if (cpop(s) != k) continue;
-            if (k >= 3) {
-                for (int j = 0; j < (1 << (k - 3)); ++j, ++seen) {
-                    const uint32_t a2 = cdeposit((uint32_t)j << 3, (uint32_t)s);
-                    if (seen < n_big - n_split) {
-                        if (whole < THREADS) t.v[whole++] = titem(s, (int)a2, 3);
-                    } else {
-                        const uint32_t a2h = cdeposit(((uint32_t)j << 3) | 4u, (uint32_t)s);
-                        if (halves + 1 < THREADS) {
-                            t.v[halves++] = titem(s, (int)a2, 2);
-                            t.v[halves++] = titem(s, (int)a2h, 2);
-                        }
-                    }
-                }
-            } else if (small < THREADS) {
-                t.v[small++] = titem(s, 0, k);
+            int n = 1 << k, first = 0;
+            while (n > 0) {
+                int cls = -1, take = 0;
+                if (n >= 8 && at[0] < end[0]) { cls = 0; take = 8; }
+                else if (n >= 6 && at[1] < end[1] && (n == 6 || n >= 10)) { cls = 1; take = 6; }
+                else if (n >= 4 && at[2] < end[2]) { cls = 2; take = 4; }
+                else if (at[1] < end[1]) { cls = 1; take = n < 4 ? n : 4; }
+                else if (at[2] < end[2] && n < 4) { cls = 2; take = n; }
+                if (cls < 0) { t.ok = false; return t; }
+                t.v[at[cls]++] = titem(s, (int)cdeposit((uint32_t)first, (uint32_t)s), take);
+                first += take;
+                n -= take;
             }
         }
     return t;
 }
 constexpr ThreadItems kTItems = make_thread_items();
-static_assert(kTItems.n_big + kTItems.n_split + kTItems.n_small <= THREADS,
-              "every cross-pair item needs a thread of its own");
+static_assert(kTItems.ok, "every cross-pair run needs a thread of its own");
 // the cross-pair loop steps two submasks at a time: an item of S2' != 0
 // starts at a submask without lowbit(S2') and has an even count; the item
-// of S2' = 0 is its single submask
+// of S2' = 0 is its single submask; every submask of every S2' is covered once
 constexpr bool items_pair_up(const ThreadItems &t) {
+    int steps[1 << RL] = {};
     for (int i = 0; i < THREADS; ++i) {
         const uint32_t v = t.v[i];
         if (!(v >> 31)) continue;
-        const uint32_t s2 = v & 0xffu, a2 = (v >> 8) & 0xffu, lg = (v >> 16) & 3u;
-        if (s2 == 0 ? (lg != 0 || a2 != 0) : (lg == 0 || (a2 & (s2 & (0u - s2))) != 0)) return false;
+        const uint32_t s2 = v & 0xffu, a2 = (v >> 8) & 0xffu, cnt = (v >> 16) & 15u;
+        if (s2 == 0 ? (cnt != 1 || a2 != 0) : (cnt == 0 || (cnt & 1u) || (a2 & (s2 & (0u - s2))) != 0)) return false;
+        steps[s2] += (int)cnt;
     }
+    for (int s = 0; s < (1 << RL); ++s)
+        if (steps[s] != (1 << cpop(s))) return false;
     return true;
 }
-static_assert(items_pair_up(kTItems), "cross-pair items must pair up their submasks");
+static_assert(items_pair_up(kTItems), "cross-pair items must pair up their submasks and cover each once");
 __constant__ ThreadItems c_titems = make_thread_items();
 
 
@@ -1092,7 +1096,7 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
     const bool has_item = (item >> 31) != 0;
     const uint32_t s2 = item & 0xffu;
     const uint32_t a2_first = (item >> 8) & 0xffu;
-    const uint32_t cnt = 1u << ((item >> 16) & 3u);
+    const uint32_t cnt = (item >> 16) & 15u;
     const uint32_t slot_s2 = slot_of(s2);
     const uint32_t low2 = s2 & (0u - s2);
     const uint32_t low_off = slot_of(low2) * 16u;                    // block offset of lowbit(S2')
