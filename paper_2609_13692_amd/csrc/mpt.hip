@@ -1067,7 +1067,10 @@ __device__ __attribute__((always_inline)) inline void cross_step(uint32_t off_a,
     conv_full<KI>(a0, b1, best1);                         // (S2'|E, A2')
     conv_full<KI>(a0, b0, best0);                         // (S2', A2')
     conv_full<KI>(a1, b0, best1);                         // (S2'|E, A2'|E)
-    __builtin_amdgcn_sched_barrier(0);
+    // 64-bit keys: steps kept apart (measured faster). Narrow keys leave
+    // registers for the compiler to start a step's reads during the
+    // previous step's arithmetic (measured faster there).
+    if (!std::is_same<KI, uint32_t>::value) __builtin_amdgcn_sched_barrier(0);
 }
 
 // cross pairs of one (S_H, chunk); fused = finish the row in place. NARROW:
