@@ -33,11 +33,10 @@ HBM_PEAK_GBS = 8000.0
 N_CU, CLOCK_GHZ = 256, 2.4
 VALU_PEAK_TOPS = N_CU * 64 * CLOCK_GHZ / 1000.0      # VALU lane-instructions, T/s (39.3)
 # VALU lane-instructions one evaluated bipartition needs at least, by the key
-# width the cross-pair kernel runs on. While sum_i w(R_i) < 2^20 - 1 the
-# library packs a key into 32 bits (cost << 12 | in-row part of A): one
-# v_add_u32 per candidate and one v_min3_u32 per two candidates, 1.5. Above
-# that, 64-bit keys held as exact-integer doubles: v_add_f64 + v_min_f64, 2.
-NARROW_TOTAL = (1 << 20) - 1
+# width the cross-pair kernel ran on, which the library names in its launch
+# label: "rb_cross_u32" for 32-bit keys (cost << 12 | in-row part of A; one
+# v_add_u32 per candidate and one v_min3_u32 per two candidates, 1.5),
+# "rb_cross" for 64-bit keys (exact-integer doubles: v_add_f64 + v_min_f64, 2).
 DP_OPS_NARROW, DP_OPS_WIDE = 1.5, 2.0
 
 WORKLOADS = {
@@ -337,8 +336,7 @@ def main() -> int:
     dp_kernels = {k: v for k, v in prof.items() if k.startswith(("dp_", "rb_"))}
     dom = max(dp_kernels, key=lambda k: dp_kernels[k]["total_ms"])
     d = prof[dom]
-    total_w = int(inst.weights[inst.req_chunks].sum())              # sum_i w(R_i)
-    narrow = total_w < NARROW_TOTAL
+    narrow = dom.endswith("_u32")
     ops_per_pair = DP_OPS_NARROW if narrow else DP_OPS_WIDE
     achieved_tops = d["work"] * ops_per_pair / (d["total_ms"] / 1000.0) / 1e12
     dp_ms = sum(v["total_ms"] for v in dp_kernels.values()) / args.steps
@@ -352,7 +350,7 @@ def main() -> int:
                 "bytes_per_launch": z["work"] / z["launches"],
                 "dense_zeta_equiv_GBps": round(2 * zgbs, 1)}
 
-    traffic = profiled_traffic(dom)
+    traffic = profiled_traffic(dom[:-4] if narrow else dom)
     line = {
         "metric": "submask transitions/sec (3^m DP) + zeta-transform HBM GB/s, per MI355X",
         "value": T / (ms / 1000.0),

@@ -1704,6 +1704,8 @@ int solve_rb(int m, const int64_t *W, int64_t *C, uint32_t *split, char *ws, con
     uint32_t *Tn = NARROW ? (uint32_t *)(ws + Lw.rb_tagged) : nullptr;
     uint32_t *Pn = NARROW ? Tn + ((size_t)1 << m) : nullptr;
     uint64_t *Pt = (uint64_t *)(ws + Lw.rb_plain);
+    // profiling label of the cross-pair launches: names the key width
+    const char *kCrossLabel = NARROW ? "rb_cross_u32" : "rb_cross";
     int64_t *Wr = (int64_t *)(ws + Lw.rb_wrow);
     uint32_t *Sr = (uint32_t *)(ws + Lw.rb_srow);
     uint64_t *partial = (uint64_t *)(ws + Lw.rb_part);
@@ -1734,12 +1736,12 @@ int solve_rb(int m, const int64_t *W, int64_t *C, uint32_t *split, char *ws, con
             LaunchScope ls("rb_final", pair_work * P.n_sets, s);
             rb::k_rb_final<K, NARROW><<<P.n_sets, rb::THREADS, 0, s>>>(m, P.h, 0u, Wr, Tt, Pt, Tn, Pn, Sr, partial);
         } else if (P.chunks == 1) {
-            LaunchScope ls("rb_cross", pair_work * (double)P.n_sets * (P.n_pairs + 1), s);
+            LaunchScope ls(kCrossLabel, pair_work * (double)P.n_sets * (P.n_pairs + 1), s);
             rb::k_rb_cross<K, NARROW><<<P.n_sets, rb::THREADS, 0, s>>>(m, P.h, P.n_pairs, 1u, P.n_pairs, 1, Wr, Tt,
                                                                        Pt, Tn, Pn, Sr, partial);
         } else {
             {
-                LaunchScope ls("rb_cross", pair_work * (double)P.n_sets * P.n_pairs, s);
+                LaunchScope ls(kCrossLabel, pair_work * (double)P.n_sets * P.n_pairs, s);
                 rb::k_rb_cross<K, NARROW><<<P.n_sets * P.chunks, rb::THREADS, 0, s>>>(
                     m, P.h, P.n_pairs, P.chunks, P.per_chunk, 0, Wr, Tt, Pt, Tn, Pn, Sr, partial);
             }
