@@ -102,7 +102,9 @@ int mpt_build_weights(int m, int64_t n_chunks, int64_t nnz,
  * W, C and split need only the alignment of their element types.
  * For m >= 13 the call also synchronises `stream` once before its kernels,
  * to read sum_i W({i}) back: that total picks the key representation of the
- * packed kernels (exact doubles, uint64, or the plain kernels).
+ * packed kernels (32-bit keys for the cross and self pairs while it is below
+ * 2^20 - 1, else exact doubles, uint64, or the plain kernels). Every
+ * representation gives the same C and split.
  */
 int mpt_solve_exact(int m, const int64_t *W, int64_t *C, uint32_t *split,
                     int64_t *opt_cost, void *workspace, size_t workspace_bytes,

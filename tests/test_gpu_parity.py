@@ -262,6 +262,25 @@ def test_narrow_keys_at_their_limit(excess):
     assert_same(inst, got, oracle.solve(inst))
 
 
+def test_wide_keys_on_the_retrieval_shape():
+    """The retrieval-shaped m = 20 workload with every weight times 64:
+    sum_i w(R_i) passes 2^20 - 1, so the 64-bit kernels run (levels split
+    into up to 127 chunks, reduce and finishing passes). Against the oracle,
+    and against the narrow path on the unscaled instance: scaling every
+    weight by 64 scales every cost by 64 and keeps every tie, so C is 64
+    times the narrow C and split is the same."""
+    import dataclasses
+    base = wl.config(3)
+    inst = dataclasses.replace(base, weights=base.weights * 64, name=base.name + " x64")
+    assert int(inst.weights[inst.req_chunks].sum()) >= (1 << 20) - 1
+    got = gpu_run(inst)
+    assert_same(inst, got, oracle.solve(inst))
+    narrow = gpu_run(base)
+    assert np.array_equal(got["C"][1:], 64 * narrow["C"][1:])
+    assert np.array_equal(got["split"], narrow["split"])
+    assert np.array_equal(got["orders"], narrow["orders"])
+
+
 @pytest.mark.parametrize("seed", [1, 2])
 def test_narrow_keys_with_many_ties(seed):
     """Unit weights over a small universe: many bipartitions tie on cost and
