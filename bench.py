@@ -1,8 +1,11 @@
 """Benchmark of the exact MPT solver on one MI355X.
 
 One step = the whole hot path over one synthetic instance already resident
-in HBM: demand sets + W table (mpt_build_weights), the layered DP
-(mpt_solve_exact) and the order read-off (mpt_extract_orders).
+in HBM, through the context layer of the C ABI: demand sets + W table
+(mpt_ctx_build_weights, which copies the resident instance into the
+context's workspace and validates it), the layered DP (mpt_ctx_solve_exact,
+returning OPT_free) and the order read-off (mpt_ctx_extract_orders, orders
+left in the workspace).
 
 Default workload: retrieval-shaped, m = 25 requests over 10000 passages in
 100 topics, top-k = 50 (Zipf s = 1.1 topics and in-topic popularity, 20%
@@ -33,11 +36,20 @@ HBM_PEAK_GBS = 8000.0
 N_CU, CLOCK_GHZ = 256, 2.4
 VALU_PEAK_TOPS = N_CU * 64 * CLOCK_GHZ / 1000.0      # VALU lane-instructions, T/s (39.3)
 # VALU lane-instructions one evaluated bipartition needs at least, by the key
-# width the cross-pair kernel ran on, which the library names in its launch
-# label: "rb_cross_u32" for 32-bit keys (cost << 12 | in-row part of A; one
-# v_add_u32 per candidate and one v_min3_u32 per two candidates, 1.5),
-# "rb_cross" for 64-bit keys (exact-integer doubles: v_add_f64 + v_min_f64, 2).
-DP_OPS_NARROW, DP_OPS_WIDE = 1.5, 2.0
+# representation the cross-pair kernel ran on, which the library names in its
+# launch label, with the kernel's name in rocprofv3 summaries:
+#   rb_cross_u32: 32-bit keys (cost << 12 | in-row part of A): one v_add_u32
+#                 per candidate and one v_min3_u32 per two candidates, 1.5;
+#   rb_cross_f64: exact-integer doubles: v_add_f64 + v_min_f64, 2;
+#   rb_cross_u64: uint64: v_lshl_add_u64 + v_cmp_lt_u64 + two v_cndmask_b32, 4.
+# The plain kernels (dp_*, m <= 12 or costs too large to pack) gather their
+# operands from the cache hierarchy; no instruction roofline is given for them.
+DP_KEYS = {
+    "rb_cross_u32": ("k_rb_cross<double, true>", 1.5, "u32 packed keys (v_add_u32 + v_min3_u32)"),
+    "rb_cross_f64": ("k_rb_cross<double, false>", 2.0, "f64 exact-integer keys (v_add_f64 + v_min_f64)"),
+    "rb_cross_u64": ("k_rb_cross<unsigned long, false>", 4.0,
+                     "u64 keys (v_lshl_add_u64 + v_cmp_lt_u64 + 2 v_cndmask_b32)"),
+}
 
 WORKLOADS = {
     1: "tiny random, m=12, u=64, k=4, w~U{1..32}, seed 0",
@@ -48,8 +60,8 @@ WORKLOADS = {
 }
 
 
-def profiled_traffic(label: str):
-    """HBM bytes per launch of the kernel `label` from the committed
+def profiled_traffic(kernel: str):
+    """HBM bytes per launch of the kernel named `kernel` from the committed
     rocprofv3 summaries (FETCH_SIZE + WRITE_SIZE, calibrated against a plain
     copy), with the L2 hit rate and VALU issue fraction the same summary
     records, or None when no summary was taken from the current kernel
@@ -71,7 +83,7 @@ def profiled_traffic(label: str):
             if data.get("source_sha256") != hashlib.sha256(f.read()).hexdigest():
                 continue
         for name, k in data.get("kernels", {}).items():
-            if re.search(r"\bk_" + re.escape(label) + r"\b", name):
+            if name.endswith(kernel):
                 return {"bytes_per_launch": k["traffic_bytes_per_launch"],
                         "l2_hit_rate": k.get("l2_hit_rate"), "valu_issue_frac": k.get("valu_issue_frac"),
                         "summary": os.path.relpath(path, ROOT)}
@@ -90,6 +102,15 @@ def cpu_baseline(inst, budget_s: float) -> dict:
     from paper_2609_13692_amd import workloads as wl
 
     threads = len(os.sched_getaffinity(0))
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
     sets = inst.requests()
     best = None
     m_s = min(inst.m, 16)
@@ -117,6 +138,7 @@ def cpu_baseline(inst, budget_s: float) -> dict:
         "value": t_eval(m_s) / tdp,
         "unit": "bipartitions/s",
         "cores": threads,
+        "cpu_model": model,
         "kind": "oracle",
         "sample": f"first {m_s} of the {inst.m} requests (T = {t_eval(m_s):.3e} bipartitions); "
                   f"oracle DP {tdp:.2f} s, oracle W table {tw:.3f} s, {threads} OpenMP threads",
@@ -297,13 +319,20 @@ def main() -> int:
     torch.cuda.set_device(0)
     inst = wl.config(args.config)
     m = inst.m
-    prob = mpt.Problem(inst)
     stream = torch.cuda.current_stream()
+    # the instance resident in HBM; one step is the three phases on a context
+    # (include/mpt.h): the build copies it into the context's workspace
+    dev = torch.device("cuda")
+    chunk_w = torch.as_tensor(inst.weights, dtype=torch.int64).to(dev)
+    req_off = torch.as_tensor(inst.req_off, dtype=torch.int64).to(dev)
+    req_chunks = torch.as_tensor(inst.req_chunks, dtype=torch.int32).to(dev)
+    ctx = mpt.Context(dev, stream)
+    ctx.reserve(m, inst.n_chunks, inst.nnz)
 
     def step():
-        prob.build(stream)
-        opt = prob.solve(stream)
-        prob.extract(stream)
+        ctx.build_weights(m, inst.n_chunks, chunk_w, req_off, req_chunks)
+        opt = ctx.solve_exact()[0]
+        ctx.extract_orders(to_host=False)
         return opt
 
     if args.calib_copy_mib:
@@ -336,9 +365,7 @@ def main() -> int:
     dp_kernels = {k: v for k, v in prof.items() if k.startswith(("dp_", "rb_"))}
     dom = max(dp_kernels, key=lambda k: dp_kernels[k]["total_ms"])
     d = prof[dom]
-    narrow = dom.endswith("_u32")
-    ops_per_pair = DP_OPS_NARROW if narrow else DP_OPS_WIDE
-    achieved_tops = d["work"] * ops_per_pair / (d["total_ms"] / 1000.0) / 1e12
+    key = DP_KEYS.get(dom)
     dp_ms = sum(v["total_ms"] for v in dp_kernels.values()) / args.steps
     z = prof.get("weights_tile")
     zeta = None
@@ -350,7 +377,28 @@ def main() -> int:
                 "bytes_per_launch": z["work"] / z["launches"],
                 "dense_zeta_equiv_GBps": round(2 * zgbs, 1)}
 
-    traffic = profiled_traffic(dom[:-4] if narrow else dom)
+    roofline = None
+    if key:
+        kernel, ops_per_pair, keys = key
+        achieved_tops = d["work"] * ops_per_pair / (d["total_ms"] / 1000.0) / 1e12
+        traffic = profiled_traffic(kernel)
+        roofline = {"kernel": dom, "bound": "alu", "achieved": round(achieved_tops, 3),
+                    "peak": round(VALU_PEAK_TOPS, 2), "unit": "TOP/s",
+                    "frac": round(achieved_tops / VALU_PEAK_TOPS, 4),
+                    "traffic": round(traffic["bytes_per_launch"]) if traffic else None,
+                    "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
+                    "traffic_source": traffic["summary"] if traffic else None,
+                    # from the same summary: TCC_HIT / (TCC_HIT + TCC_MISS), and the share of
+                    # the SIMDs' VALU issue cycles at 2.4 GHz that the kernel's instructions use
+                    "l2_hit_rate": (round(traffic["l2_hit_rate"], 4)
+                                    if traffic and traffic["l2_hit_rate"] else None),
+                    "valu_issue_frac": (round(traffic["valu_issue_frac"], 4)
+                                        if traffic and traffic["valu_issue_frac"] else None),
+                    "avg_launch_ms": round(d["total_ms"] / d["launches"], 4),
+                    "keys": keys,
+                    "ops_per_pair": ops_per_pair,
+                    "ops_per_launch": d["work"] * ops_per_pair / d["launches"]}
+    dtype = "int64 results, " + (key[2].split(" (")[0] if key else "int64 gathers (plain kernels)")
     line = {
         "metric": "submask transitions/sec (3^m DP) + zeta-transform HBM GB/s, per MI355X",
         "value": T / (ms / 1000.0),
@@ -362,7 +410,7 @@ def main() -> int:
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "int64",
+        "dtype": dtype,
         "data": "synthetic",
         "config": {"workload": WORKLOADS[args.config], "m": m, "n_chunks": inst.n_chunks, "nnz": inst.nnz,
                    "instance_sha256": inst.sha256()[:16]},
@@ -374,21 +422,7 @@ def main() -> int:
                "kernels": {k: {"launches": v["launches"] // args.steps,
                                "ms_per_step": round(v["total_ms"] / args.steps, 3)}
                            for k, v in prof.items()}},
-        "roofline": {"kernel": dom, "bound": "alu", "achieved": round(achieved_tops, 3),
-                     "peak": round(VALU_PEAK_TOPS, 2), "unit": "TOP/s",
-                     "frac": round(achieved_tops / VALU_PEAK_TOPS, 4),
-                     "traffic": round(traffic["bytes_per_launch"]) if traffic else None,
-                     "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
-                     "traffic_source": traffic["summary"] if traffic else None,
-                     # from the same summary: TCC_HIT / (TCC_HIT + TCC_MISS), and the share of
-                     # the SIMDs' VALU issue cycles at 2.4 GHz that the kernel's instructions use
-                     "l2_hit_rate": round(traffic["l2_hit_rate"], 4) if traffic and traffic["l2_hit_rate"] else None,
-                     "valu_issue_frac": (round(traffic["valu_issue_frac"], 4)
-                                         if traffic and traffic["valu_issue_frac"] else None),
-                     "avg_launch_ms": round(d["total_ms"] / d["launches"], 4),
-                     "keys": "u32 (v_add_u32 + v_min3_u32)" if narrow else "f64 (v_add_f64 + v_min_f64)",
-                     "ops_per_pair": ops_per_pair,
-                     "ops_per_launch": d["work"] * ops_per_pair / d["launches"]},
+        "roofline": roofline,
         "zeta": zeta,
     }
     if not args.no_greedy:

@@ -44,7 +44,7 @@
 extern "C" {
 #endif
 
-#define MPT_MAX_M 28
+#define MPT_MAX_M 30
 #define MPT_MAX_CHUNKS (1LL << 30)
 #define MPT_MAX_CHUNK_WEIGHT (1LL << 32)
 /* C[0] after mpt_solve_exact: the empty set never takes part in a split. */
@@ -58,7 +58,9 @@ enum mpt_status {
     MPT_E_WEIGHT = -4,    /* a weight <= 0 or > MPT_MAX_CHUNK_WEIGHT */
     MPT_E_OVERFLOW = -5,  /* sum_i w(R_i) >= 2^61 */
     MPT_E_WORKSPACE = -6, /* workspace missing, misaligned or too small */
-    MPT_E_DEVICE = -8     /* HIP runtime error (detail in mpt_last_error) */
+    MPT_E_STATE = -7,     /* context call out of order (e.g. a solve before a build) */
+    MPT_E_DEVICE = -8,    /* HIP runtime error (detail in mpt_last_error) */
+    MPT_E_INTERNAL = -9   /* internal error (e.g. a host allocation failed) */
 };
 
 /* Bytes of device workspace that every entry point below needs for an
@@ -128,6 +130,105 @@ int mpt_extract_orders(int m, int64_t n_chunks, int64_t nnz,
                        const uint32_t *sig, const uint32_t *split,
                        int32_t *order_chunks, void *workspace,
                        size_t workspace_bytes, void *stream);
+
+/*
+ * ---- The context layer: the three phases of one instance on one device ----
+ *
+ * A context holds a device, a stream, a caller-owned workspace and the state
+ * of one instance: created -> built (mpt_ctx_build_weights) -> solved
+ * (mpt_ctx_solve_exact) -> extracted (mpt_ctx_extract_orders). Each phase
+ * needs the one before it (else MPT_E_STATE); a new build starts over. A
+ * failed build leaves the context created (no instance); a failed solve or
+ * extraction leaves it where it was before that phase. Inputs are borrowed
+ * for the duration of the build and copied into the workspace, which also
+ * holds W, C, split, the demand sets and the orders; mpt_copy_table reads
+ * them out. Compared with the stateless calls above, the solve needs no
+ * read-back of sum_i w(R_i) (the build keeps it) and the extraction no
+ * validation of a split table the library made, so the solve and the
+ * extraction synchronise the stream only when they return host data.
+ * A context serves one thread at a time; contexts are independent.
+ */
+typedef struct mpt_ctx mpt_ctx;
+
+#define MPT_TABLE_W 0       /* int64 [2^m]      after a build */
+#define MPT_TABLE_SIG 1     /* uint32 [n_chunks] after a build */
+#define MPT_TABLE_C 2       /* int64 [2^m]      after a solve (C[0] = MPT_COST_SENTINEL) */
+#define MPT_TABLE_SPLIT 3   /* uint32 [2^m]     after a solve */
+#define MPT_TABLE_ORDERS 4  /* int32 [nnz]      after an extraction (CSR with req_off) */
+
+/* Options (mpt_set_option). MPT_OPT_CHUNK_PAIRS: 0 (default) lets the
+ * library plan how the cross pairs of each DP level are split over
+ * workgroups; k >= 1 runs every level in chunks of at most k pairs (a level
+ * whose pairs fit one chunk finishes its rows in the same kernel). Results
+ * do not depend on it (it exists to test exactly that); it changes the
+ * workspace size. */
+#define MPT_OPT_CHUNK_PAIRS 1
+
+/* New context on HIP device hip_device, enqueueing on hip_stream (a
+ * hipStream_t created on that device; NULL = its null stream). *out = NULL
+ * on failure. Every context call makes hip_device current for its duration
+ * and restores the caller's device. */
+int mpt_create(mpt_ctx **out, int hip_device, void *hip_stream);
+
+/* Frees the context (host memory only: the workspace is the caller's).
+ * NULL-safe. Waits for nothing: the caller must not destroy a context whose
+ * work is still in flight on its stream and then reuse the workspace. */
+void mpt_destroy(mpt_ctx *ctx);
+
+/* Sets an option (see MPT_OPT_*); MPT_E_INVALID for an unknown option or
+ * value. Resets the context to created. */
+int mpt_set_option(mpt_ctx *ctx, int option, int64_t value);
+
+/* Device bytes the context needs for an instance of m requests, n_chunks
+ * chunks and nnz request slots, with the context's options (ctx NULL:
+ * default options). 0 for sizes out of range. */
+size_t mpt_ctx_workspace_bytes(const mpt_ctx *ctx, int m, int64_t n_chunks, int64_t nnz);
+
+/* Hands the context a caller-owned device workspace (256-byte aligned, on
+ * the context's device, alive until the next mpt_set_workspace or
+ * mpt_destroy). Its size is checked at each build. Resets the context to
+ * created. dev_ptr NULL detaches it. */
+int mpt_set_workspace(mpt_ctx *ctx, void *dev_ptr, size_t bytes);
+
+/*
+ * Phase 1 (as mpt_build_weights): copies the instance into the workspace,
+ * validates it and builds W and the demand sets. chunk_w [n_chunks],
+ * req_off [m+1] and req_chunks [nnz] may be host or device memory (copied
+ * with hipMemcpyDefault). Synchronises the stream to report validation
+ * errors. MPT_E_WORKSPACE if the workspace is missing or smaller than
+ * mpt_ctx_workspace_bytes(ctx, m, n_chunks, nnz).
+ */
+int mpt_ctx_build_weights(mpt_ctx *ctx, int m, int64_t n_chunks, int64_t nnz, const int64_t *chunk_w,
+                          const int64_t *req_off, const int32_t *req_chunks);
+
+/*
+ * Phase 2 (as mpt_solve_exact), after a build (else MPT_E_STATE).
+ *   opt_cost    HOST out, nullable: OPT_free = C(full set) (Theorem 1)
+ *   savings     HOST out, nullable: sum_i w(R_i) - OPT_free, the weight the
+ *               optimal trie saves over no sharing (Eq. 3)
+ *   split_host  HOST out, nullable: uint32 [2^m] split table
+ * Synchronises the stream only if one of them is non-NULL.
+ */
+int mpt_ctx_solve_exact(mpt_ctx *ctx, int64_t *opt_cost, int64_t *savings, uint32_t *split_host);
+
+/*
+ * Phase 3 (as mpt_extract_orders), after a solve (else MPT_E_STATE).
+ *   order_chunks_host  HOST out, nullable: int32 [nnz], pi_i at
+ *                      [req_off[i], req_off[i+1])
+ * Synchronises the stream only if order_chunks_host is non-NULL.
+ */
+int mpt_ctx_extract_orders(mpt_ctx *ctx, int32_t *order_chunks_host);
+
+/*
+ * Copies table `which` (MPT_TABLE_*) to host_dst, which holds `bytes` bytes
+ * (at least the table's size, else MPT_E_INVALID); MPT_E_STATE if the phase
+ * that writes the table has not run since the last build. Synchronises.
+ */
+int mpt_copy_table(const mpt_ctx *ctx, int which, void *host_dst, size_t bytes);
+
+/* Device address and size of table `which` inside the workspace (valid
+ * until the next build or workspace change), under the same state rules. */
+int mpt_table_device(const mpt_ctx *ctx, int which, const void **dev_ptr, size_t *bytes);
 
 /*
  * ---- Sections 6.2-6.3: heuristic and bound for large request counts ----

@@ -17,6 +17,7 @@
 #include <cstdarg>
 #include <cstdint>
 #include <cstdio>
+#include <cstddef>
 #include <cstring>
 #include <mutex>
 #include <string>
@@ -25,6 +26,7 @@
 
 #include "bitonic.h"
 #include "common.h"
+#include "core.h"
 #include "mpt.h"
 
 namespace {
@@ -62,7 +64,8 @@ struct WsHeader {
     uint32_t err;          // OR of ERR_* bits
     uint32_t n_list;       // entries of the compact (S_x, w) list
     int64_t zero_weight;   // total weight of chunks that no request holds
-    int64_t pad[30];
+    int64_t total;         // sum_i w(R_i) = sum_i W({i}) (saturated)
+    int64_t pad[29];
 };
 static_assert(sizeof(WsHeader) == 256, "header is one 256-byte block");
 
@@ -122,7 +125,7 @@ __global__ void k_fill_u32(uint32_t *p, int64_t n, uint32_t v) {
 }
 
 __global__ void k_header_init(WsHeader *h) {
-    if (threadIdx.x == 0) { h->err = 0; h->n_list = 0; h->zero_weight = 0; }
+    if (threadIdx.x == 0) { h->err = 0; h->n_list = 0; h->zero_weight = 0; h->total = 0; }
 }
 
 // req_off must be a CSR offset array: req_off[0] = 0, non-decreasing, = nnz at m
@@ -355,6 +358,7 @@ __global__ void k_check_total(int m, const int64_t *W, WsHeader *h) {
         int64_t v = W[(int64_t)1 << i];
         if (v >= kCostLimit - tot) over = true; else tot += v;
     }
+    h->total = over ? kCostLimit : tot;
     if (over) atomicOr(&h->err, ERR_OVERFLOW);
 }
 
@@ -406,52 +410,54 @@ __global__ __launch_bounds__(256) void k_dp_wave(int m, int p, int seg_bits, uin
     const uint32_t lb = xcd_block(blockIdx.x, gridDim.x);
     const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const uint32_t lane = threadIdx.x % kWave;
-    const uint32_t task = lb * (blockDim.x / kWave) + wave;
-    if (task >= n_tasks) return;
-    const uint32_t set_rank = task >> seg_log;
-    const uint32_t seg = task & ((1u << seg_log) - 1u);
-    const uint32_t S = unrank_colex(set_rank, p, m);
-    const uint32_t l = S & (0u - S);
-    const uint32_t R = S ^ l;
-    // lane part: deposit of the lane id into the 6 lowest bits of R
-    uint32_t rr = R, lane_part = 0;
+    const uint32_t waves = gridDim.x * (blockDim.x / kWave);
+    // a grid of at most kMaxGrid blocks walks the tasks (wave-uniform)
+    for (uint32_t task = lb * (blockDim.x / kWave) + wave; task < n_tasks; task += waves) {
+        const uint32_t set_rank = task >> seg_log;
+        const uint32_t seg = task & ((1u << seg_log) - 1u);
+        const uint32_t S = unrank_colex(set_rank, p, m);
+        const uint32_t l = S & (0u - S);
+        const uint32_t R = S ^ l;
+        // lane part: deposit of the lane id into the 6 lowest bits of R
+        uint32_t rr = R, lane_part = 0;
 #pragma unroll
-    for (int k = 0; k < 6; ++k) {
-        uint32_t bit = rr & (0u - rr);
-        rr ^= bit;
-        if ((lane >> k) & 1u) lane_part |= bit;
-    }
-    const uint32_t R_hi = rr;
-    const uint32_t nh = 1u << (seg_bits - 6);
-    // deposit of the segment's first counter value into R_hi
-    uint32_t hp = 0;
-    {
-        uint32_t hh = seg * nh, rem = R_hi;
-        while (hh) {
-            uint32_t bit = rem & (0u - rem);
-            rem ^= bit;
-            if (hh & 1u) hp |= bit;
-            hh >>= 1;
+        for (int k = 0; k < 6; ++k) {
+            uint32_t bit = rr & (0u - rr);
+            rr ^= bit;
+            if ((lane >> k) & 1u) lane_part |= bit;
         }
-    }
-    const uint32_t base_a = lane_part | l;
-    int64_t best = INT64_MAX;
-    uint32_t best_a = 0;
+        const uint32_t R_hi = rr;
+        const uint32_t nh = 1u << (seg_bits - 6);
+        // deposit of the segment's first counter value into R_hi
+        uint32_t hp = 0;
+        {
+            uint32_t hh = seg * nh, rem = R_hi;
+            while (hh) {
+                uint32_t bit = rem & (0u - rem);
+                rem ^= bit;
+                if (hh & 1u) hp |= bit;
+                hh >>= 1;
+            }
+        }
+        const uint32_t base_a = lane_part | l;
+        int64_t best = INT64_MAX;
+        uint32_t best_a = 0;
 #pragma unroll 4
-    for (uint32_t it = 0; it < nh; ++it) {
-        const uint32_t A = base_a | hp;
-        const int64_t v = C[A] + C[S ^ A];
-        if (v < best) { best = v; best_a = A; }
-        hp = ((hp | ~R_hi) + 1u) & R_hi;
-    }
-    wave_lex_min(best, best_a);
-    if (lane == 0) {
-        if (seg_log == 0) {
-            C[S] = best - W[S];
-            split[S] = best_a;
-        } else {
-            part_v[task] = best;
-            part_a[task] = best_a;
+        for (uint32_t it = 0; it < nh; ++it) {
+            const uint32_t A = base_a | hp;
+            const int64_t v = C[A] + C[S ^ A];
+            if (v < best) { best = v; best_a = A; }
+            hp = ((hp | ~R_hi) + 1u) & R_hi;
+        }
+        wave_lex_min(best, best_a);
+        if (lane == 0) {
+            if (seg_log == 0) {
+                C[S] = best - W[S];
+                split[S] = best_a;
+            } else {
+                part_v[task] = best;
+                part_a[task] = best_a;
+            }
         }
     }
 }
@@ -463,20 +469,21 @@ __global__ __launch_bounds__(256) void k_dp_reduce(int m, int p, uint32_t n_sets
                                                    const uint32_t *__restrict__ part_a) {
     const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const uint32_t lane = threadIdx.x % kWave;
-    const uint32_t set_rank = blockIdx.x * (blockDim.x / kWave) + wave;
-    if (set_rank >= n_sets) return;
+    const uint32_t waves = gridDim.x * (blockDim.x / kWave);
     const uint32_t nseg = 1u << seg_log;
-    int64_t best = INT64_MAX;
-    uint32_t best_a = 0xffffffffu;
-    for (uint32_t j = lane; j < nseg; j += kWave) {
-        const uint32_t t = (set_rank << seg_log) + j;
-        lex_min(best, best_a, part_v[t], part_a[t]);
-    }
-    wave_lex_min(best, best_a);
-    if (lane == 0) {
-        const uint32_t S = unrank_colex(set_rank, p, m);
-        C[S] = best - W[S];
-        split[S] = best_a;
+    for (uint32_t set_rank = blockIdx.x * (blockDim.x / kWave) + wave; set_rank < n_sets; set_rank += waves) {
+        int64_t best = INT64_MAX;
+        uint32_t best_a = 0xffffffffu;
+        for (uint32_t j = lane; j < nseg; j += kWave) {
+            const uint32_t t = (set_rank << seg_log) + j;
+            lex_min(best, best_a, part_v[t], part_a[t]);
+        }
+        wave_lex_min(best, best_a);
+        if (lane == 0) {
+            const uint32_t S = unrank_colex(set_rank, p, m);
+            C[S] = best - W[S];
+            split[S] = best_a;
+        }
     }
 }
 
@@ -1470,7 +1477,7 @@ __global__ void k_request_total(int m, const int64_t *W, WsHeader *h) {
         const int64_t v = W[(int64_t)1 << i];
         tot = (v >= INT64_MAX - tot) ? INT64_MAX : tot + v;
     }
-    h->pad[0] = tot;
+    h->total = tot;
 }
 }  // namespace rb
 
@@ -1547,6 +1554,8 @@ __global__ void k_extract_out(int64_t nnz, const uint64_t *keys, int32_t *order_
 struct LayerPlan { int p; uint32_t n_sets; int kind; int seg_bits; int seg_log; uint32_t n_tasks; };
 enum { KIND_LANE = 0, KIND_WAVE = 1 };
 constexpr uint32_t kTargetWaves = 32768;   // enough waves to fill 256 CUs several times over
+// grids of the plain kernels stay within 2^32 work-items; they walk the rest
+constexpr uint32_t kMaxGrid = 1u << 20;
 
 LayerPlan plan_layer(int m, int p) {
     LayerPlan L{};
@@ -1578,9 +1587,17 @@ size_t dp_partial_entries(int m) {
 // row-blocked DP: one entry per level h = |S_H| of the high part
 struct RbLevel { int h; uint32_t n_sets; uint32_t n_pairs; uint32_t chunks; uint32_t per_chunk; };
 constexpr int kRbMinM = rb::L + 1;
+constexpr int kRbMaxLevels = MPT_MAX_M - rb::L + 1;
+constexpr uint32_t kRbMaxChunks = 4096;
+struct RbPlan { RbLevel v[kRbMaxLevels]; int n; };
 
-std::vector<RbLevel> rb_plan(int m) {
-    std::vector<RbLevel> v;
+// chunk_pairs = 0: the chunk count of every level from the cost model below.
+// chunk_pairs > 0: every level runs its cross pairs in chunks of at most
+// chunk_pairs pairs (at most kRbMaxChunks chunks); a level whose pairs fit one
+// chunk finishes its rows in the same kernel. Every plan gives the same tables:
+// the chunks' keys are folded by exact minima.
+RbPlan rb_plan(int m, int64_t chunk_pairs) {
+    RbPlan plan{};
     const int m_hi = m - rb::L;
     for (int h = 0; h <= m_hi; ++h) {
         RbLevel L{};
@@ -1589,6 +1606,9 @@ std::vector<RbLevel> rb_plan(int m) {
         L.n_pairs = h >= 2 ? (1u << (h - 1)) - 1u : 0u;
         if (L.n_pairs == 0) {
             L.chunks = 0;
+        } else if (chunk_pairs > 0) {
+            const int64_t c = ((int64_t)L.n_pairs + chunk_pairs - 1) / chunk_pairs;
+            L.chunks = (uint32_t)std::min<int64_t>(c, kRbMaxChunks);
         } else {
             // A fixed number of workgroups runs per CU at a time (their LDS
             // takes the CU), so W equal workgroups take ceil(W / slots)
@@ -1607,28 +1627,33 @@ std::vector<RbLevel> rb_plan(int m) {
             };
             uint32_t best = 1;
             double best_cost = cost(1);
-            for (uint32_t c = 2; c <= std::min<uint32_t>(L.n_pairs, 4096); ++c) {
+            for (uint32_t c = 2; c <= std::min<uint32_t>(L.n_pairs, kRbMaxChunks); ++c) {
                 const double e = cost(c);
                 if (e < best_cost - 1e-9) { best = c; best_cost = e; }
             }
             L.chunks = best;
         }
         L.per_chunk = L.chunks ? (L.n_pairs + L.chunks - 1) / L.chunks : 0;
-        v.push_back(L);
+        plan.v[plan.n++] = L;
     }
-    return v;
+    return plan;
 }
 
-size_t rb_partial_entries(int m) {
+size_t rb_partial_entries(int m, int64_t chunk_pairs) {
     if (m < kRbMinM) return 0;
     size_t mx = 0;
-    for (const RbLevel &L : rb_plan(m))
+    const RbPlan plan = rb_plan(m, chunk_pairs);
+    for (int i = 0; i < plan.n; ++i) {
+        const RbLevel &L = plan.v[i];
         if (L.chunks > 1) mx = std::max(mx, (size_t)L.n_sets * L.chunks * rb::ROW);
+    }
     return mx;
 }
 
 struct WsLayout {
-    size_t list_sig, list_w, part_v, part_a, keys, rb_part, rb_tagged, rb_plain, rb_wrow, rb_srow, total;
+    size_t list_sig, list_w, part_v, part_a, keys, rb_part, rb_tagged, rb_plain, rb_wrow, rb_srow;
+    size_t build_end, extract_end;   // bytes the build and the extraction use
+    size_t total;                    // bytes every phase fits in
 };
 
 // keys sorted by the extraction: a power of two, at least one sort tile
@@ -1638,7 +1663,7 @@ inline size_t extract_keys(int64_t nnz) {
     return n;
 }
 
-WsLayout ws_layout(int m, int64_t nnz) {
+WsLayout ws_layout(int m, int64_t nnz, int64_t chunk_pairs) {
     WsLayout L{};
     const size_t nz = (size_t)std::max<int64_t>(nnz, 1);
     const size_t P = std::max<size_t>(dp_partial_entries(m), 1);
@@ -1654,7 +1679,7 @@ WsLayout ws_layout(int m, int64_t nnz) {
     L.keys = off;
     size_t ex_end = L.keys + align256(extract_keys(nnz) * 8);
     L.rb_part = off;
-    size_t rb_end = L.rb_part + align256(rb_partial_entries(m) * 8);
+    size_t rb_end = L.rb_part + align256(rb_partial_entries(m, chunk_pairs) * 8);
     if (m >= kRbMinM) {
         // the packed DP's tagged and plain tables, W and split in row order
         L.rb_tagged = rb_end;
@@ -1666,27 +1691,35 @@ WsLayout ws_layout(int m, int64_t nnz) {
         L.rb_srow = rb_end;
         rb_end += align256((size_t)4 << m);
     }
+    L.build_end = build_end;
+    L.extract_end = ex_end;
     L.total = std::max(std::max(build_end, rb_end), std::max(dp_end, ex_end));
     return L;
 }
 
-int check_ws(int m, int64_t nnz, void *ws, size_t bytes) {
+// need: the bytes the calling phase uses (at most mpt_workspace_bytes)
+int check_ws(void *ws, size_t bytes, size_t need) {
     if (!ws) return fail(MPT_E_WORKSPACE, "workspace is NULL");
     if (((uintptr_t)ws & 255u) != 0) return fail(MPT_E_WORKSPACE, "workspace is not 256-byte aligned");
-    size_t need = ws_layout(m, nnz).total;
     if (bytes < need) return fail(MPT_E_WORKSPACE, "workspace has %zu bytes, needs %zu", bytes, need);
     return MPT_OK;
 }
 
-int read_errors(WsHeader *h, hipStream_t s) {
-    uint32_t err = 0;
-    MPT_HIP_TRY(hipMemcpyAsync(&err, &h->err, sizeof err, hipMemcpyDeviceToHost, s));
+// the first fields of the header, as the host reads them back
+struct HeaderHead { uint32_t err; uint32_t n_list; int64_t zero_weight; int64_t total; };
+static_assert(offsetof(WsHeader, total) == offsetof(HeaderHead, total), "header prefix");
+
+int read_errors(WsHeader *h, hipStream_t s, int64_t *total = nullptr) {
+    HeaderHead hh{};
+    MPT_HIP_TRY(hipMemcpyAsync(&hh, h, sizeof hh, hipMemcpyDeviceToHost, s));
     MPT_HIP_TRY(hipStreamSynchronize(s));
+    const uint32_t err = hh.err;
     if (err & ERR_INVALID) return fail(MPT_E_INVALID, "req_off is not a CSR offset array of length m+1 ending at nnz, or split is not a hierarchy");
     if (err & ERR_RANGE) return fail(MPT_E_RANGE, "a chunk id is outside [0, n_chunks)");
     if (err & ERR_DUP) return fail(MPT_E_DUP, "a chunk is repeated inside one request");
     if (err & ERR_WEIGHT) return fail(MPT_E_WEIGHT, "a chunk weight is <= 0 or > 2^32");
     if (err & ERR_OVERFLOW) return fail(MPT_E_OVERFLOW, "sum of request weights reaches 2^61");
+    if (total) *total = hh.total;
     return MPT_OK;
 }
 
@@ -1698,14 +1731,15 @@ int check_common(int m, int64_t n_chunks, int64_t nnz) {
 }
 
 template <class K, bool NARROW>
-int solve_rb(int m, const int64_t *W, int64_t *C, uint32_t *split, char *ws, const WsLayout &Lw, hipStream_t s) {
+int solve_rb(int m, const int64_t *W, int64_t *C, uint32_t *split, char *ws, const WsLayout &Lw,
+             int64_t chunk_pairs, hipStream_t s) {
     // NARROW: the two narrow tables take the wide tagged table's space
     uint64_t *Tt = NARROW ? nullptr : (uint64_t *)(ws + Lw.rb_tagged);
     uint32_t *Tn = NARROW ? (uint32_t *)(ws + Lw.rb_tagged) : nullptr;
     uint32_t *Pn = NARROW ? Tn + ((size_t)1 << m) : nullptr;
     uint64_t *Pt = (uint64_t *)(ws + Lw.rb_plain);
     // profiling label of the cross-pair launches: names the key width
-    const char *kCrossLabel = NARROW ? "rb_cross_u32" : "rb_cross";
+    const char *kCrossLabel = NARROW ? "rb_cross_u32" : (std::is_same<K, double>::value ? "rb_cross_f64" : "rb_cross_u64");
     int64_t *Wr = (int64_t *)(ws + Lw.rb_wrow);
     uint32_t *Sr = (uint32_t *)(ws + Lw.rb_srow);
     uint64_t *partial = (uint64_t *)(ws + Lw.rb_part);
@@ -1730,7 +1764,9 @@ int solve_rb(int m, const int64_t *W, int64_t *C, uint32_t *split, char *ws, con
         LaunchScope ls("rb_row0", pair_work / 2, s);
         rb::k_rb_row0<K, NARROW><<<1, rb::THREADS, 0, s>>>(m, Wr, Pt, Pn, Sr);
     }
-    for (const RbLevel &P : rb_plan(m)) {
+    const RbPlan plan = rb_plan(m, chunk_pairs);
+    for (int li = 0; li < plan.n; ++li) {
+        const RbLevel &P = plan.v[li];
         if (P.h == 0) continue;                               // row 0: done above
         if (P.n_pairs == 0) {
             LaunchScope ls("rb_final", pair_work * P.n_sets, s);
@@ -1783,44 +1819,30 @@ int solve_rb(int m, const int64_t *W, int64_t *C, uint32_t *split, char *ws, con
 }  // namespace
 
 // ===========================================================================
-// C ABI
+// Phases behind the C ABI. The exported calls below and the context layer
+// (ctx.hip) validate their arguments and call these.
 
-extern "C" size_t mpt_workspace_bytes(int m, int64_t nnz) {
+namespace mptcore {
+
+size_t workspace_bytes(int m, int64_t nnz, int64_t chunk_pairs) {
     if (m < 1 || m > MPT_MAX_M || nnz < 0) return 0;
-    return ws_layout(m, nnz).total;
+    return ws_layout(m, nnz, chunk_pairs).total;
 }
 
-extern "C" const char *mpt_status_string(int status) {
-    switch (status) {
-        case MPT_OK: return "ok";
-        case MPT_E_INVALID: return "invalid argument";
-        case MPT_E_RANGE: return "chunk id out of range";
-        case MPT_E_DUP: return "chunk repeated inside a request";
-        case MPT_E_WEIGHT: return "chunk weight out of range";
-        case MPT_E_OVERFLOW: return "costs would overflow int64";
-        case MPT_E_WORKSPACE: return "workspace too small or misaligned";
-        case MPT_E_DEVICE: return "HIP runtime error";
-        default: return "unknown status";
-    }
-}
-
-extern "C" const char *mpt_last_error(void) { return mptlib::error_text(); }
-
-extern "C" int mpt_build_weights(int m, int64_t n_chunks, int64_t nnz, const int64_t *chunk_w,
-                                 const int64_t *req_off, const int32_t *req_chunks, uint32_t *sig,
-                                 int64_t *W, void *workspace, size_t workspace_bytes, void *stream) {
-    mptlib::clear_error();
+int build(int m, int64_t n_chunks, int64_t nnz, const int64_t *chunk_w, const int64_t *req_off,
+          const int32_t *req_chunks, uint32_t *sig, int64_t *W, void *workspace, size_t workspace_bytes,
+          hipStream_t s, int64_t *total) {
+    mptlib::Range range("mpt build_weights");
     int rc = check_common(m, n_chunks, nnz);
     if (rc) return rc;
     if (!req_off || !W) return fail(MPT_E_INVALID, "req_off and W must not be NULL");
     if ((uintptr_t)W & 15u) return fail(MPT_E_INVALID, "W must be 16-byte aligned");
     if (n_chunks > 0 && (!chunk_w || !sig)) return fail(MPT_E_INVALID, "chunk_w and sig must not be NULL");
     if (nnz > 0 && !req_chunks) return fail(MPT_E_INVALID, "req_chunks must not be NULL");
-    if ((rc = check_ws(m, nnz, workspace, workspace_bytes))) return rc;
-    hipStream_t s = (hipStream_t)stream;
+    const WsLayout L = ws_layout(m, nnz, 0);
+    if ((rc = check_ws(workspace, workspace_bytes, L.build_end))) return rc;
     char *ws = (char *)workspace;
     WsHeader *h = (WsHeader *)ws;
-    WsLayout L = ws_layout(m, nnz);
     uint32_t *list_sig = (uint32_t *)(ws + L.list_sig);
     int64_t *list_w = (int64_t *)(ws + L.list_w);
 
@@ -1860,46 +1882,42 @@ extern "C" int mpt_build_weights(int m, int64_t n_chunks, int64_t nnz, const int
     }
     k_check_total<<<1, 64, 0, s>>>(m, W, h);
     MPT_HIP_TRY(hipGetLastError());
-    return read_errors(h, s);
+    return read_errors(h, s, total);
 }
 
-extern "C" int mpt_solve_exact(int m, const int64_t *W, int64_t *C, uint32_t *split, int64_t *opt_cost,
-                               void *workspace, size_t workspace_bytes, void *stream) {
-    mptlib::clear_error();
+int solve(int m, const int64_t *W, int64_t *C, uint32_t *split, int64_t *opt_cost, void *workspace,
+          size_t workspace_bytes, hipStream_t s, int64_t total, int64_t chunk_pairs) {
+    mptlib::Range range("mpt solve_exact");
     int rc = check_common(m, 0, 0);
     if (rc) return rc;
     if (!W || !C || !split) return fail(MPT_E_INVALID, "W, C and split must not be NULL");
-    if ((rc = check_ws(m, 0, workspace, workspace_bytes))) return rc;
-    hipStream_t s = (hipStream_t)stream;
+    if (chunk_pairs < 0) return fail(MPT_E_INVALID, "chunk_pairs = %lld is negative", (long long)chunk_pairs);
+    const WsLayout L = ws_layout(m, 0, chunk_pairs);
+    if ((rc = check_ws(workspace, workspace_bytes, L.total))) return rc;
     char *ws = (char *)workspace;
-    WsLayout L = ws_layout(m, 0);
     int64_t *part_v = (int64_t *)(ws + L.part_v);
     uint32_t *part_a = (uint32_t *)(ws + L.part_a);
     const int64_t n = (int64_t)1 << m;
     if (m >= kRbMinM) {
-        // packed keys need every cost below 2^(62-m): check sum_i w(R_i)
-        WsHeader *h = (WsHeader *)ws;
-        rb::k_request_total<<<1, 64, 0, s>>>(m, W, h);
-        int64_t total = 0;
-        MPT_HIP_TRY(hipMemcpyAsync(&total, &h->pad[0], sizeof total, hipMemcpyDeviceToHost, s));
-        MPT_HIP_TRY(hipStreamSynchronize(s));
+        // packed keys need every cost below 2^(62-m): sum_i w(R_i) picks the
+        // representation. Unknown (< 0): read it back from W.
+        if (total < 0) {
+            WsHeader *h = (WsHeader *)ws;
+            rb::k_request_total<<<1, 64, 0, s>>>(m, W, h);
+            MPT_HIP_TRY(hipMemcpyAsync(&total, &h->total, sizeof total, hipMemcpyDeviceToHost, s));
+            MPT_HIP_TRY(hipStreamSynchronize(s));
+        }
         // doubles while 2 C' < 2^52 (Key<double>); below 2^62 keys fit uint64
         if (total < ((int64_t)1 << (61 - m))) {
-#ifndef MPT_RB_NO_DOUBLE
-#define MPT_RB_NO_DOUBLE 0
-#endif
-#ifndef MPT_RB_NO_NARROW
-#define MPT_RB_NO_NARROW 0
-#endif
             // narrow cross-pair keys while every C(A) + C(B) stays below 2^20 - 1
-            // (then 2 C' < 2^52 too, for any m up to 30)
+            // (then 2 C' < 2^52 too, for any m up to MPT_MAX_M)
             static_assert(rb::kNarrowTotal <= ((int64_t)1 << (51 - MPT_MAX_M)), "narrow keys imply double keys");
-            if (!MPT_RB_NO_DOUBLE && !MPT_RB_NO_NARROW && total < rb::kNarrowTotal - 1)
-                rc = solve_rb<double, true>(m, W, C, split, ws, L, s);
-            else if (!MPT_RB_NO_DOUBLE && total < ((int64_t)1 << (51 - m)))
-                rc = solve_rb<double, false>(m, W, C, split, ws, L, s);
+            if (total < rb::kNarrowTotal - 1)
+                rc = solve_rb<double, true>(m, W, C, split, ws, L, chunk_pairs, s);
+            else if (total < ((int64_t)1 << (51 - m)))
+                rc = solve_rb<double, false>(m, W, C, split, ws, L, chunk_pairs, s);
             else
-                rc = solve_rb<uint64_t, false>(m, W, C, split, ws, L, s);
+                rc = solve_rb<uint64_t, false>(m, W, C, split, ws, L, chunk_pairs, s);
             if (rc) return rc;
             if (opt_cost) {
                 MPT_HIP_TRY(hipMemcpyAsync(opt_cost, C + (n - 1), sizeof(int64_t), hipMemcpyDeviceToHost, s));
@@ -1921,13 +1939,13 @@ extern "C" int mpt_solve_exact(int m, const int64_t *W, int64_t *C, uint32_t *sp
         } else {
             {
                 LaunchScope ls("dp_wave", pairs, s);
-                k_dp_wave<<<(P.n_tasks + 3) / 4, 256, 0, s>>>(m, p, P.seg_bits, P.n_tasks, P.seg_log, W, C, split,
-                                                               part_v, part_a);
+                k_dp_wave<<<std::min((P.n_tasks + 3) / 4, kMaxGrid), 256, 0, s>>>(
+                    m, p, P.seg_bits, P.n_tasks, P.seg_log, W, C, split, part_v, part_a);
             }
             if (P.seg_log > 0) {
                 LaunchScope ls("dp_reduce", (double)P.n_tasks, s);
-                k_dp_reduce<<<(P.n_sets + 3) / 4, 256, 0, s>>>(m, p, P.n_sets, P.seg_log, W, C, split, part_v,
-                                                                 part_a);
+                k_dp_reduce<<<std::min((P.n_sets + 3) / 4, kMaxGrid), 256, 0, s>>>(m, p, P.n_sets, P.seg_log, W, C,
+                                                                                  split, part_v, part_a);
             }
         }
         MPT_HIP_TRY(hipGetLastError());
@@ -1940,22 +1958,23 @@ extern "C" int mpt_solve_exact(int m, const int64_t *W, int64_t *C, uint32_t *sp
     return MPT_OK;
 }
 
-extern "C" int mpt_extract_orders(int m, int64_t n_chunks, int64_t nnz, const int64_t *req_off,
-                                  const int32_t *req_chunks, const uint32_t *sig, const uint32_t *split,
-                                  int32_t *order_chunks, void *workspace, size_t workspace_bytes, void *stream) {
-    mptlib::clear_error();
+int extract(int m, int64_t n_chunks, int64_t nnz, const int64_t *req_off, const int32_t *req_chunks,
+            const uint32_t *sig, const uint32_t *split, int32_t *order_chunks, void *workspace,
+            size_t workspace_bytes, hipStream_t s, bool validate) {
+    mptlib::Range range("mpt extract_orders");
     int rc = check_common(m, n_chunks, nnz);
     if (rc) return rc;
     if (!req_off || !split) return fail(MPT_E_INVALID, "req_off and split must not be NULL");
     if (nnz > 0 && (!req_chunks || !order_chunks || !sig))
         return fail(MPT_E_INVALID, "req_chunks, sig and order_chunks must not be NULL");
-    if ((rc = check_ws(m, nnz, workspace, workspace_bytes))) return rc;
-    hipStream_t s = (hipStream_t)stream;
+    const WsLayout L = ws_layout(m, nnz, 0);
+    if ((rc = check_ws(workspace, workspace_bytes, L.extract_end))) return rc;
     char *ws = (char *)workspace;
     WsHeader *h = (WsHeader *)ws;
-    WsLayout L = ws_layout(m, nnz);
-    k_header_init<<<1, 64, 0, s>>>(h);
-    k_check_offsets<<<1, 64, 0, s>>>(m, nnz, req_off, h);
+    if (validate) {
+        k_header_init<<<1, 64, 0, s>>>(h);
+        k_check_offsets<<<1, 64, 0, s>>>(m, nnz, req_off, h);
+    }
     {
         LaunchScope ls("extract", (double)nnz, s);
         uint64_t *keys = (uint64_t *)(ws + L.keys);
@@ -1963,8 +1982,9 @@ extern "C" int mpt_extract_orders(int m, int64_t n_chunks, int64_t nnz, const in
         k_fill_u64<<<grid_for(nk - nnz, 256), 256, 0, s>>>(keys, nnz, nk, ~0ull);
         k_extract<<<m, 256, 0, s>>>(m, n_chunks, nnz, req_off, req_chunks, sig, split, keys, h);
         MPT_HIP_TRY(hipGetLastError());
-        int rc = read_errors(h, s);               // offsets and the hierarchy checked before the sort
-        if (rc) return rc;
+        // offsets and the hierarchy are checked before the sort (inputs that
+        // the library produced itself need no check)
+        if (validate && (rc = read_errors(h, s))) return rc;
         if (nnz > 0) {
             if ((rc = mptlib::sort_keys(keys, nk, s))) return rc;
             k_extract_out<<<grid_for(nnz, 256), 256, 0, s>>>(nnz, keys, order_chunks);
@@ -1974,6 +1994,66 @@ extern "C" int mpt_extract_orders(int m, int64_t n_chunks, int64_t nnz, const in
     return MPT_OK;
 }
 
+}  // namespace mptcore
+
+// ===========================================================================
+// C ABI
+
+extern "C" size_t mpt_workspace_bytes(int m, int64_t nnz) {
+    try {
+        return mptcore::workspace_bytes(m, nnz, 0);
+    } catch (...) {
+        return 0;
+    }
+}
+
+extern "C" const char *mpt_status_string(int status) {
+    switch (status) {
+        case MPT_OK: return "ok";
+        case MPT_E_INVALID: return "invalid argument";
+        case MPT_E_RANGE: return "chunk id out of range";
+        case MPT_E_DUP: return "chunk repeated inside a request";
+        case MPT_E_WEIGHT: return "chunk weight out of range";
+        case MPT_E_OVERFLOW: return "costs would overflow int64";
+        case MPT_E_WORKSPACE: return "workspace too small or misaligned";
+        case MPT_E_STATE: return "call out of order for the context's state";
+        case MPT_E_DEVICE: return "HIP runtime error";
+        case MPT_E_INTERNAL: return "internal error";
+        default: return "unknown status";
+    }
+}
+
+extern "C" const char *mpt_last_error(void) { return mptlib::error_text(); }
+
+extern "C" int mpt_build_weights(int m, int64_t n_chunks, int64_t nnz, const int64_t *chunk_w,
+                                 const int64_t *req_off, const int32_t *req_chunks, uint32_t *sig,
+                                 int64_t *W, void *workspace, size_t workspace_bytes, void *stream) {
+    mptlib::clear_error();
+    return mptlib::guarded(__func__, [&]() -> int {
+        return mptcore::build(m, n_chunks, nnz, chunk_w, req_off, req_chunks, sig, W, workspace, workspace_bytes,
+                              (hipStream_t)stream, nullptr);
+    });
+}
+
+extern "C" int mpt_solve_exact(int m, const int64_t *W, int64_t *C, uint32_t *split, int64_t *opt_cost,
+                               void *workspace, size_t workspace_bytes, void *stream) {
+    mptlib::clear_error();
+    return mptlib::guarded(__func__, [&]() -> int {
+        return mptcore::solve(m, W, C, split, opt_cost, workspace, workspace_bytes, (hipStream_t)stream, -1, 0);
+    });
+}
+
+extern "C" int mpt_extract_orders(int m, int64_t n_chunks, int64_t nnz, const int64_t *req_off,
+                                  const int32_t *req_chunks, const uint32_t *sig, const uint32_t *split,
+                                  int32_t *order_chunks, void *workspace, size_t workspace_bytes, void *stream) {
+    mptlib::clear_error();
+    return mptlib::guarded(__func__, [&]() -> int {
+        return mptcore::extract(m, n_chunks, nnz, req_off, req_chunks, sig, split, order_chunks, workspace,
+                                workspace_bytes, (hipStream_t)stream, true);
+    });
+}
+
+// ---------------------------------------------------------------------------
 namespace mptlib {
 
 thread_local std::string t_last_error;

@@ -16,24 +16,29 @@ import torch
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libmpt.so")
 
-MPT_MAX_M = 28
+MPT_MAX_M = 30
 MPT_COST_SENTINEL = 1 << 62
 MPT_GREEDY_MAX_M = 16384
 MPT_LAYOUT_MAX_M = 1 << 24
 MPT_CACHE_MAX_CONFIGS = 256
 MPT_ORDER_ID = 0
 MPT_ORDER_POPULARITY = 1
+MPT_TABLE_W, MPT_TABLE_SIG, MPT_TABLE_C, MPT_TABLE_SPLIT, MPT_TABLE_ORDERS = 0, 1, 2, 3, 4
+MPT_OPT_CHUNK_PAIRS = 1
 
 _STATUS = {
     0: "MPT_OK", -1: "MPT_E_INVALID", -2: "MPT_E_RANGE", -3: "MPT_E_DUP",
-    -4: "MPT_E_WEIGHT", -5: "MPT_E_OVERFLOW", -6: "MPT_E_WORKSPACE", -8: "MPT_E_DEVICE",
+    -4: "MPT_E_WEIGHT", -5: "MPT_E_OVERFLOW", -6: "MPT_E_WORKSPACE", -7: "MPT_E_STATE",
+    -8: "MPT_E_DEVICE", -9: "MPT_E_INTERNAL",
 }
 EXPORTED = ("mpt_workspace_bytes", "mpt_build_weights", "mpt_solve_exact", "mpt_extract_orders",
             "mpt_status_string", "mpt_last_error", "mpt_profile_begin", "mpt_profile_end",
             "mpt_greedy_workspace_bytes", "mpt_pair_weights", "mpt_greedy_hierarchy",
             "mpt_spanning_tree_bound", "mpt_layout_workspace_bytes", "mpt_global_order_layout",
             "mpt_layout_cost", "mpt_cache_simulate", "mpt_pinned_workspace_bytes", "mpt_pinned_split",
-            "mpt_pinned_assemble")
+            "mpt_pinned_assemble", "mpt_create", "mpt_destroy", "mpt_set_option", "mpt_ctx_workspace_bytes",
+            "mpt_set_workspace", "mpt_ctx_build_weights", "mpt_ctx_solve_exact", "mpt_ctx_extract_orders",
+            "mpt_copy_table", "mpt_table_device")
 
 
 class MptError(RuntimeError):
@@ -99,6 +104,26 @@ def load() -> ctypes.CDLL:
     lib.mpt_pinned_split.restype = i32
     lib.mpt_pinned_assemble.argtypes = [i32, i64, P, P, i32, P, i32, P, P, P, P, sz, P]
     lib.mpt_pinned_assemble.restype = i32
+    lib.mpt_create.argtypes = [ctypes.POINTER(P), i32, P]
+    lib.mpt_create.restype = i32
+    lib.mpt_destroy.argtypes = [P]
+    lib.mpt_destroy.restype = None
+    lib.mpt_set_option.argtypes = [P, i32, i64]
+    lib.mpt_set_option.restype = i32
+    lib.mpt_ctx_workspace_bytes.argtypes = [P, i32, i64, i64]
+    lib.mpt_ctx_workspace_bytes.restype = sz
+    lib.mpt_set_workspace.argtypes = [P, P, sz]
+    lib.mpt_set_workspace.restype = i32
+    lib.mpt_ctx_build_weights.argtypes = [P, i32, i64, i64, P, P, P]
+    lib.mpt_ctx_build_weights.restype = i32
+    lib.mpt_ctx_solve_exact.argtypes = [P, P, P, P]
+    lib.mpt_ctx_solve_exact.restype = i32
+    lib.mpt_ctx_extract_orders.argtypes = [P, P]
+    lib.mpt_ctx_extract_orders.restype = i32
+    lib.mpt_copy_table.argtypes = [P, i32, P, sz]
+    lib.mpt_copy_table.restype = i32
+    lib.mpt_table_device.argtypes = [P, i32, ctypes.POINTER(P), ctypes.POINTER(sz)]
+    lib.mpt_table_device.restype = i32
     _lib = lib
     return lib
 
@@ -504,3 +529,148 @@ def solve(inst, device="cuda") -> dict:
     out = prob.host_tables()
     out["opt"] = opt
     return out
+
+
+# --- the context layer ------------------------------------------------------
+
+def _any_ptr(t, dtype, n: int, name: str):
+    """Pointer to a contiguous tensor in host or device memory (the context
+    build copies its inputs with hipMemcpyDefault)."""
+    if t is None:
+        if n > 0:
+            raise ValueError(f"{name} is required")
+        return None
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if t.numel() < n:
+        raise ValueError(f"{name} has {t.numel()} elements, needs {n}")
+    return t.data_ptr() if t.numel() else None
+
+
+class Context:
+    """An mpt_ctx (include/mpt.h): one instance on one device, its phases in
+    order, over a workspace tensor that this object allocates with torch and
+    keeps alive."""
+
+    _DTYPES = {MPT_TABLE_W: "int64", MPT_TABLE_SIG: "uint32", MPT_TABLE_C: "int64",
+               MPT_TABLE_SPLIT: "uint32", MPT_TABLE_ORDERS: "int32"}
+
+    def __init__(self, device="cuda", stream=None):
+        lib = load()
+        self.device = torch.device(device)
+        idx = self.device.index if self.device.index is not None else torch.cuda.current_device()
+        if stream is None:
+            stream = torch.cuda.current_stream(idx)
+        self.stream = stream
+        h = ctypes.c_void_p()
+        _check(lib.mpt_create(ctypes.byref(h), idx, stream.cuda_stream or None), "mpt_create")
+        self._h = h
+        self.workspace = None
+
+    def close(self):
+        if getattr(self, "_h", None) is not None and self._h.value:
+            load().mpt_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def set_option(self, option: int, value: int) -> None:
+        _check(load().mpt_set_option(self._h, option, value), "mpt_set_option")
+
+    def workspace_bytes(self, m: int, n_chunks: int, nnz: int) -> int:
+        return int(load().mpt_ctx_workspace_bytes(self._h, m, n_chunks, nnz))
+
+    def reserve(self, m: int, n_chunks: int, nnz: int) -> None:
+        """Allocates (with torch) and attaches a workspace for these sizes,
+        unless the attached one is already large enough."""
+        need = self.workspace_bytes(m, n_chunks, nnz)
+        if need == 0:
+            raise MptError(-1, "mpt_ctx_workspace_bytes", f"invalid sizes m={m} n_chunks={n_chunks} nnz={nnz}")
+        if self.workspace is None or self.workspace.numel() < need:
+            self.workspace = None
+            self.workspace = torch.empty(need, dtype=torch.uint8, device=self.device)
+        self.set_workspace(self.workspace)
+
+    def set_workspace(self, ws) -> None:
+        ptr = _ptr(ws, torch.uint8, 1, "workspace") if ws is not None else None
+        _check(load().mpt_set_workspace(self._h, ptr, ws.numel() if ws is not None else 0), "mpt_set_workspace")
+
+    def build_weights(self, m, n_chunks, chunk_w, req_off, req_chunks) -> None:
+        nnz = int(req_chunks.numel()) if req_chunks is not None else 0
+        _check(load().mpt_ctx_build_weights(
+            self._h, m, n_chunks, nnz, _any_ptr(chunk_w, torch.int64, n_chunks, "chunk_w"),
+            _any_ptr(req_off, torch.int64, m + 1, "req_off"),
+            _any_ptr(req_chunks, torch.int32, nnz, "req_chunks") if nnz else None), "mpt_ctx_build_weights")
+        self._sizes = (m, n_chunks, nnz)
+
+    def solve_exact(self, want_cost=True, want_split=False):
+        """Returns (OPT_free, savings, split) with None for what was not asked."""
+        import numpy as np
+        opt, sav = ctypes.c_int64(0), ctypes.c_int64(0)
+        split = None
+        if want_split:
+            n = self._table_len(MPT_TABLE_W)
+            split = np.empty(n, dtype=np.uint32)
+        _check(load().mpt_ctx_solve_exact(
+            self._h, ctypes.addressof(opt) if want_cost else None, ctypes.addressof(sav) if want_cost else None,
+            split.ctypes.data if split is not None else None), "mpt_ctx_solve_exact")
+        return (int(opt.value) if want_cost else None, int(sav.value) if want_cost else None, split)
+
+    def extract_orders(self, to_host=True):
+        import numpy as np
+        out = None
+        if to_host:
+            out = np.empty(max(1, self._table_len(MPT_TABLE_ORDERS)), dtype=np.int32)
+        _check(load().mpt_ctx_extract_orders(self._h, out.ctypes.data if out is not None else None),
+               "mpt_ctx_extract_orders")
+        return out[:self._nnz] if out is not None else None
+
+    def copy_table(self, which: int):
+        import numpy as np
+        n = self._table_len(which)
+        out = np.empty(max(1, n), dtype=self._DTYPES.get(which, "uint8"))   # unknown: the library says so
+        _check(load().mpt_copy_table(self._h, which, out.ctypes.data, out.nbytes), "mpt_copy_table")
+        return out[:n]
+
+    def table_device(self, which: int):
+        """(device address, bytes) of a table inside the workspace."""
+        p, nb = ctypes.c_void_p(), ctypes.c_size_t(0)
+        _check(load().mpt_table_device(self._h, which, ctypes.byref(p), ctypes.byref(nb)), "mpt_table_device")
+        return int(p.value or 0), int(nb.value)
+
+    # sizes of the last build, kept on the Python side for output buffers
+    _sizes = (0, 0, 0)
+
+    def _table_len(self, which):
+        m, u, nnz = self._sizes
+        return {MPT_TABLE_W: 1 << m, MPT_TABLE_C: 1 << m, MPT_TABLE_SPLIT: 1 << m, MPT_TABLE_SIG: u,
+                MPT_TABLE_ORDERS: nnz}.get(which, 1)
+
+    @property
+    def _nnz(self):
+        return self._sizes[2]
+
+    def run(self, inst_or_tensors) -> dict:
+        """Build, solve and extract one instance (a workloads instance or a
+        (m, n_chunks, chunk_w, req_off, req_chunks) tuple of tensors); returns
+        OPT_free, the savings and the orders (host)."""
+        if isinstance(inst_or_tensors, tuple):
+            m, u, chunk_w, req_off, req_chunks = inst_or_tensors
+        else:
+            inst = inst_or_tensors
+            m, u = inst.m, inst.n_chunks
+            chunk_w = torch.as_tensor(inst.weights, dtype=torch.int64)
+            req_off = torch.as_tensor(inst.req_off, dtype=torch.int64)
+            req_chunks = torch.as_tensor(inst.req_chunks, dtype=torch.int32)
+        nnz = int(req_chunks.numel())
+        self.reserve(m, u, nnz)
+        self.build_weights(m, u, chunk_w, req_off, req_chunks)
+        opt, sav, _ = self.solve_exact()
+        orders = self.extract_orders()
+        return {"opt": opt, "savings": sav, "orders": orders}

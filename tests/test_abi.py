@@ -41,9 +41,9 @@ def test_every_declared_symbol_is_exported(lib):
 def test_workspace_sizes(lib):
     from paper_2609_13692_amd import mpt
     assert mpt.mpt_workspace_bytes(0, 10) == 0
-    assert mpt.mpt_workspace_bytes(29, 10) == 0
+    assert mpt.mpt_workspace_bytes(mpt.MPT_MAX_M + 1, 10) == 0
     assert mpt.mpt_workspace_bytes(5, -1) == 0
-    for m in (1, 12, 20, 25, 28):
+    for m in (1, 12, 20, 25, 28, mpt.MPT_MAX_M):
         a = mpt.mpt_workspace_bytes(m, 0)
         b = mpt.mpt_workspace_bytes(m, 10000)
         assert a >= 256 and b >= a and b % 256 == 0
@@ -51,8 +51,8 @@ def test_workspace_sizes(lib):
 
 
 def test_status_strings(lib):
-    for code in (0, -1, -2, -3, -4, -5, -6, -8):
-        assert lib.mpt_status_string(code)
+    for code in (0, -1, -2, -3, -4, -5, -6, -7, -8, -9):
+        assert lib.mpt_status_string(code) != b"unknown status"
     assert lib.mpt_status_string(-77) == b"unknown status"
 
 
@@ -63,7 +63,7 @@ def test_host_side_validation_before_any_device_call(lib):
     # m out of range
     assert lib.mpt_build_weights(0, 1, 0, dummy, dummy, None, dummy, dummy, ws, 1 << 20, None) == -1
     assert b"m = 0" in lib.mpt_last_error()
-    assert lib.mpt_solve_exact(29, dummy, dummy, dummy, None, ws, 1 << 20, None) == -1
+    assert lib.mpt_solve_exact(31, dummy, dummy, dummy, None, ws, 1 << 20, None) == -1
     # NULL tables
     assert lib.mpt_solve_exact(4, None, dummy, dummy, None, ws, 1 << 20, None) == -1
     # workspace missing, misaligned, too small
@@ -76,6 +76,55 @@ def test_host_side_validation_before_any_device_call(lib):
     assert lib.mpt_extract_orders(3, 5, -2, dummy, dummy, dummy, dummy, dummy, ws, 1 << 20, None) == -1
     # missing request arrays when nnz > 0
     assert lib.mpt_build_weights(3, 5, 4, dummy, dummy, None, dummy, dummy, ws, 1 << 20, None) == -1
+
+
+def test_header_declares_the_context_layer():
+    """The calls and codes of the context layer: create / destroy, the
+    workspace, the three phases on a context, table read-out, the state
+    error and the internal error."""
+    names = declared_functions()
+    for n in ("mpt_create", "mpt_destroy", "mpt_set_workspace", "mpt_ctx_workspace_bytes", "mpt_set_option",
+              "mpt_ctx_build_weights", "mpt_ctx_solve_exact", "mpt_ctx_extract_orders", "mpt_copy_table",
+              "mpt_table_device", "mpt_status_string", "mpt_last_error"):
+        assert n in names, n
+    text = open(HEADER).read()
+    for code, val in (("MPT_E_STATE", -7), ("MPT_E_INTERNAL", -9), ("MPT_E_DEVICE", -8)):
+        assert re.search(rf"\b{code} = {val}\b", text), code
+    assert re.search(r"#define MPT_MAX_M 30\b", text)
+
+
+def test_context_host_side_validation(lib):
+    """Context calls that must fail before any device work: NULL contexts,
+    bad options, sizes out of range, phases out of order."""
+    from paper_2609_13692_amd import mpt
+    P = ctypes.c_void_p
+    dummy = P(4096)
+    assert lib.mpt_set_option(None, mpt.MPT_OPT_CHUNK_PAIRS, 1) == -1
+    assert lib.mpt_set_workspace(None, None, 0) == -1
+    assert lib.mpt_ctx_build_weights(None, 4, 1, 0, dummy, dummy, None) == -1
+    assert lib.mpt_ctx_solve_exact(None, None, None, None) == -1
+    assert lib.mpt_ctx_extract_orders(None, None) == -1
+    assert lib.mpt_copy_table(None, 0, dummy, 8) == -1
+    lib.mpt_destroy(None)                                     # NULL-safe
+    assert lib.mpt_create(None, 0, None) == -1
+    assert mpt.mpt_workspace_bytes(4, 0) > 0
+    assert lib.mpt_ctx_workspace_bytes(None, 0, 1, 1) == 0
+    assert lib.mpt_ctx_workspace_bytes(None, mpt.MPT_MAX_M + 1, 1, 1) == 0
+    assert lib.mpt_ctx_workspace_bytes(None, 4, -1, 1) == 0
+    a = lib.mpt_ctx_workspace_bytes(None, 20, 2000, 200)
+    # the context's workspace holds W, C and split besides the phases' own
+    assert a >= (20 << 20) + mpt.mpt_workspace_bytes(20, 200)
+
+
+def test_context_creation_without_a_gpu(lib):
+    """With no GPU present, mpt_create reports the device error (or an
+    invalid device) and hands back no context."""
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present")
+    h = ctypes.c_void_p(1234)
+    rc = lib.mpt_create(ctypes.byref(h), 0, None)
+    assert rc in (-1, -8) and not h.value
 
 
 def test_binding_refuses_host_tensors(lib):

@@ -39,6 +39,23 @@ def gpu_run(inst):
     return got
 
 
+def gpu_run_labelled(inst):
+    """gpu_run, plus the set of launch labels the library recorded (they
+    name the key width of the DP's cross-pair launches: rb_cross_u32 for
+    32-bit keys, rb_cross_f64 for exact-integer doubles, rb_cross_u64 for
+    uint64; dp_* for the plain kernels)."""
+    mpt.profile_begin()
+    try:
+        got = gpu_run(inst)
+    finally:
+        prof = mpt.profile_end()
+    return got, set(prof)
+
+
+def cross_labels(labels):
+    return {k for k in labels if k.startswith("rb_cross")}
+
+
 def assert_same(inst, got, ref):
     assert got["opt"] == ref["opt"]
     assert np.array_equal(got["W"], ref["W"]), "W table differs"
@@ -82,6 +99,40 @@ def test_config_full_tables_against_golden(idx):
     # Thm 1 sandwich on the GPU's own output: its layout's trie costs OPT
     assert oracle.trie_cost(inst, got["orders"]) == got["opt"]
     assert oracle.hierarchy_cost(inst, got["split"]) == got["opt"]
+
+
+# Scaling every chunk weight by s scales every W and every cost by s and keeps
+# every tie, so the split table and the orders do not change. Scaled copies
+# of the largest workloads push sum_i w(R_i) past the 32-bit key limit and
+# run the 64-bit key paths at full size, checked against the same oracle
+# digests: config 5 x 64 (total 1.6e7 < 2^26: exact-integer doubles),
+# config 5 x 4096 (1.0e9: uint64 keys) and config 4 x 4096 (4.0e8 >= 2^27:
+# uint64 keys), each with split levels of up to 256 chunks.
+SCALED = [(5, 64, "rb_cross_f64"), (5, 4096, "rb_cross_u64"), (4, 4096, "rb_cross_u64")]
+
+
+@pytest.mark.parametrize("idx,scale,label", SCALED, ids=lambda v: str(v))
+def test_scaled_config_takes_the_wide_keys(idx, scale, label):
+    import dataclasses
+    with open(os.path.join(GOLDEN, f"config_{idx}.json")) as f:
+        g = json.load(f)
+    base = wl.config(idx)
+    assert base.sha256() == g["instance_sha256"], "workload generator drifted"
+    inst = dataclasses.replace(base, weights=base.weights * scale, name=f"{base.name} x{scale}")
+    total = int(inst.weights[inst.req_chunks].sum())
+    assert total >= (1 << 20) - 1
+    got, labels = gpu_run_labelled(inst)
+    assert cross_labels(labels) == {label}
+    assert "rb_reduce" in labels                         # split levels ran
+    assert got["opt"] == scale * g["opt"]
+    W, C = got["W"], got["C"][1:]
+    assert not (W % scale).any() and not (C % scale).any()
+    assert digest(W // scale, "<i8") == g["W_sha256"]
+    assert digest(C // scale, "<i8") == g["C_sha256_from_1"]
+    assert digest(got["split"], "<u4") == g["split_sha256"]
+    assert got["orders"].tolist() == g["orders"]
+    for s_, w, c, sp in g["sample"]:
+        assert (W[s_], got["C"][s_], got["split"][s_]) == (scale * w, scale * c if s_ else got["C"][0], sp), s_
 
 
 def test_config5_sampled_sub_instances():
@@ -231,7 +282,8 @@ def test_double_keys_at_their_limit(excess):
     w = np.array(w, dtype=np.int64)
     inst = wl.from_sets(sets, w, len(w))
     assert int(sum(w[s].sum() for s in sets)) == target
-    got = gpu_run(inst)
+    got, labels = gpu_run_labelled(inst)
+    assert cross_labels(labels) == ({"rb_cross_f64"} if excess < 0 else {"rb_cross_u64"})
     assert_same(inst, got, oracle.solve(inst))
 
 
@@ -258,7 +310,8 @@ def test_narrow_keys_at_their_limit(excess):
     w = np.array(w, dtype=np.int64)
     inst = wl.from_sets(sets, w, len(w))
     assert int(sum(w[s].sum() for s in sets)) == target
-    got = gpu_run(inst)
+    got, labels = gpu_run_labelled(inst)
+    assert cross_labels(labels) == ({"rb_cross_u32"} if excess < 0 else {"rb_cross_f64"})
     assert_same(inst, got, oracle.solve(inst))
 
 
@@ -273,7 +326,8 @@ def test_wide_keys_on_the_retrieval_shape():
     base = wl.config(3)
     inst = dataclasses.replace(base, weights=base.weights * 64, name=base.name + " x64")
     assert int(inst.weights[inst.req_chunks].sum()) >= (1 << 20) - 1
-    got = gpu_run(inst)
+    got, labels = gpu_run_labelled(inst)
+    assert cross_labels(labels) == {"rb_cross_f64"}
     assert_same(inst, got, oracle.solve(inst))
     narrow = gpu_run(base)
     assert np.array_equal(got["C"][1:], 64 * narrow["C"][1:])
@@ -290,7 +344,8 @@ def test_narrow_keys_with_many_ties(seed):
     rng = np.random.default_rng(700 + seed)
     sets = [rng.choice(10, size=int(rng.integers(2, 6)), replace=False).tolist() for _ in range(18)]
     inst = wl.from_sets(sets, np.ones(10, dtype=np.int64), 10)
-    got = gpu_run(inst)
+    got, labels = gpu_run_labelled(inst)
+    assert cross_labels(labels) == {"rb_cross_u32"}
     assert_same(inst, got, oracle.solve(inst))
 
 
@@ -307,7 +362,7 @@ def test_costs_too_large_to_pack_take_the_plain_kernels():
 
 
 def test_max_m_weight_table():
-    """W at MPT_MAX_M = 28 (a 2 GiB table) for L_28: W(S) = 28 - |S|."""
+    """W at MPT_MAX_M = 30 (an 8 GiB table) for L_30: W(S) = 30 - |S|."""
     n = mpt.MPT_MAX_M
     inst = wl.gen_loo(n)
     say(f"[gpu] build only, {inst.name}")
@@ -325,7 +380,7 @@ def test_max_m_weight_table():
 
 
 def test_max_m_full_solve():
-    """Whole path at MPT_MAX_M = 28 (2^28-entry tables, 1.1e13 bipartitions)
+    """Whole path at MPT_MAX_M = 30 (2^30-entry tables, 1.0e14 bipartitions)
     on L_28, where every entry has a closed form: C(S) = (n - |S|) + E(|S|)
     with E the Eq. (5) free value; the split table encodes a hierarchy whose
     Eq. (2) cost and read-off trie cost are both OPT."""
@@ -335,7 +390,8 @@ def test_max_m_full_solve():
     prob = mpt.Problem(inst)
     opt = prob.run()
     torch.cuda.synchronize()
-    assert opt == brute.loo_opt_free(n) == 136
+    c = (n - 1).bit_length()                               # ceil(log2 n)
+    assert opt == brute.loo_opt_free(n) == n * c - (1 << c) + n    # Eq. (5): 148 at n = 30
     E = torch.tensor([0] + [brute.loo_opt_free(s) for s in range(1, n + 1)], dtype=torch.int64, device="cuda")
     for lo in range(0, 1 << n, 1 << 26):                 # in slices to bound temporaries
         idx = torch.arange(lo, lo + (1 << 26), device="cuda", dtype=torch.int64)
