@@ -132,6 +132,22 @@ int mpt_extract_orders(int m, int64_t n_chunks, int64_t nnz,
                        size_t workspace_bytes, void *stream);
 
 /*
+ * mpt_solve_exact without a workspace, for callers that cannot allocate
+ * device memory (code under HIP graph capture, serving loops, harnesses that
+ * forbid hipMalloc). Same arguments, outputs and errors as mpt_solve_exact;
+ * the scratch is a device array of MPT_NOALLOC_SCRATCH_BYTES inside the
+ * library (one per device, kept until the process ends), enough for
+ * m <= MPT_NOALLOC_MAX_M; larger m fails with MPT_E_INVALID. The call itself
+ * allocates nothing. All calls on one device share that array: calls that
+ * overlap on one device (other threads or streams) race and must be
+ * serialised by the caller; consecutive calls on one stream are safe.
+ */
+#define MPT_NOALLOC_MAX_M 20
+#define MPT_NOALLOC_SCRATCH_BYTES (37u << 20)
+int mpt_solve_exact_noalloc(int m, const int64_t *W, int64_t *C, uint32_t *split, int64_t *opt_cost,
+                            void *stream);
+
+/*
  * ---- The context layer: the three phases of one instance on one device ----
  *
  * A context holds a device, a stream, a caller-owned workspace and the state

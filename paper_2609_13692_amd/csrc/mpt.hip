@@ -2054,6 +2054,55 @@ extern "C" int mpt_extract_orders(int m, int64_t n_chunks, int64_t nnz, const in
 }
 
 // ---------------------------------------------------------------------------
+// The solve without a caller workspace: its scratch is a file-scope device
+// array of MPT_NOALLOC_SCRATCH_BYTES, one per device the library runs on,
+// held until the process ends. Host code never passes the array's name to a
+// kernel: on each device, the first call looks up the array's device address
+// with hipGetSymbolAddress (that device current) and keeps it.
+
+static __device__ __align__(256) unsigned char scratch[MPT_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
+
+int scratch_address(void **out) {
+    int dev = -1;
+    MPT_HIP_TRY(hipGetDevice(&dev));
+    if (dev < 0 || dev >= kMaxDevices) return fail(MPT_E_DEVICE, "device %d outside [0, %d)", dev, kMaxDevices);
+    std::lock_guard<std::mutex> g(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *p = nullptr;
+        MPT_HIP_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+        if (!p || ((uintptr_t)p & 255u)) return fail(MPT_E_DEVICE, "scratch array has no aligned device address");
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return MPT_OK;
+}
+
+}  // namespace
+
+extern "C" int mpt_solve_exact_noalloc(int m, const int64_t *W, int64_t *C, uint32_t *split, int64_t *opt_cost,
+                                       void *stream) {
+    mptlib::clear_error();
+    return mptlib::guarded(__func__, [&]() -> int {
+        if (m < 1 || m > MPT_NOALLOC_MAX_M)
+            return fail(MPT_E_INVALID, "m = %d outside [1, %d] (MPT_NOALLOC_MAX_M)", m, MPT_NOALLOC_MAX_M);
+        const size_t need = mptcore::workspace_bytes(m, 0, 0);
+        if (need == 0 || need > sizeof(scratch))
+            return fail(MPT_E_INTERNAL, "m = %d needs %zu bytes of scratch, the array holds %zu", m, need,
+                        sizeof(scratch));
+        void *ws = nullptr;
+        int rc = scratch_address(&ws);
+        if (rc) return rc;
+        return mptcore::solve(m, W, C, split, opt_cost, ws, sizeof(scratch), (hipStream_t)stream, -1, 0);
+    });
+}
+
+// ---------------------------------------------------------------------------
 namespace mptlib {
 
 thread_local std::string t_last_error;

@@ -25,6 +25,7 @@ MPT_ORDER_ID = 0
 MPT_ORDER_POPULARITY = 1
 MPT_TABLE_W, MPT_TABLE_SIG, MPT_TABLE_C, MPT_TABLE_SPLIT, MPT_TABLE_ORDERS = 0, 1, 2, 3, 4
 MPT_OPT_CHUNK_PAIRS = 1
+MPT_NOALLOC_MAX_M = 20
 
 _STATUS = {
     0: "MPT_OK", -1: "MPT_E_INVALID", -2: "MPT_E_RANGE", -3: "MPT_E_DUP",
@@ -38,7 +39,7 @@ EXPORTED = ("mpt_workspace_bytes", "mpt_build_weights", "mpt_solve_exact", "mpt_
             "mpt_layout_cost", "mpt_cache_simulate", "mpt_pinned_workspace_bytes", "mpt_pinned_split",
             "mpt_pinned_assemble", "mpt_create", "mpt_destroy", "mpt_set_option", "mpt_ctx_workspace_bytes",
             "mpt_set_workspace", "mpt_ctx_build_weights", "mpt_ctx_solve_exact", "mpt_ctx_extract_orders",
-            "mpt_copy_table", "mpt_table_device")
+            "mpt_copy_table", "mpt_table_device", "mpt_solve_exact_noalloc")
 
 
 class MptError(RuntimeError):
@@ -104,6 +105,8 @@ def load() -> ctypes.CDLL:
     lib.mpt_pinned_split.restype = i32
     lib.mpt_pinned_assemble.argtypes = [i32, i64, P, P, i32, P, i32, P, P, P, P, sz, P]
     lib.mpt_pinned_assemble.restype = i32
+    lib.mpt_solve_exact_noalloc.argtypes = [i32, P, P, P, P, P]
+    lib.mpt_solve_exact_noalloc.restype = i32
     lib.mpt_create.argtypes = [ctypes.POINTER(P), i32, P]
     lib.mpt_create.restype = i32
     lib.mpt_destroy.argtypes = [P]
@@ -190,6 +193,16 @@ def mpt_solve_exact(m, W, C, split, workspace, stream=None, want_cost=True):
         ctypes.addressof(out) if want_cost else None,
         _ptr(workspace, torch.uint8, 1, "workspace"), workspace.numel(), _stream(stream))
     _check(rc, "mpt_solve_exact")
+    return int(out.value) if want_cost else None
+
+
+def mpt_solve_exact_noalloc(m, W, C, split, stream=None, want_cost=True):
+    """mpt_solve_exact on the library's own scratch array (m <= 20)."""
+    out = ctypes.c_int64(0)
+    rc = load().mpt_solve_exact_noalloc(
+        m, _ptr(W, torch.int64, 1 << m, "W"), _ptr(C, torch.int64, 1 << m, "C"),
+        _ptr(split, torch.int32, 1 << m, "split"), ctypes.addressof(out) if want_cost else None, _stream(stream))
+    _check(rc, "mpt_solve_exact_noalloc")
     return int(out.value) if want_cost else None
 
 
