@@ -873,6 +873,19 @@ __device__ inline void conv_full(const K a[NB], const K b[NB], K best[NB]) {
             if (!(a1 & ~s1)) best[s1] = Key<K>::min(best[s1], Key<K>::add(a[a1], b[s1 ^ a1]));
 }
 
+// the same, folding into out[] the keys of in[] (in and out may be one array)
+template <class K>
+__device__ inline void conv_into(const K a[NB], const K b[NB], const K in[NB], K out[NB]) {
+#pragma unroll
+    for (int s1 = 0; s1 < NB; ++s1) {
+        K v = in[s1];
+#pragma unroll
+        for (int a1 = 0; a1 < NB; ++a1)
+            if (!(a1 & ~s1)) v = Key<K>::min(v, Key<K>::add(a[a1], b[s1 ^ a1]));
+        out[s1] = v;
+    }
+}
+
 template <class K>
 __device__ inline void flush(const K best[NB], uint32_t s2, uint64_t *acc) {
 #pragma unroll
@@ -1116,10 +1129,12 @@ __device__ inline const K *lds_at(uint32_t off) {
 // convolutions from four block loads. off_a, off_b: LDS byte offsets of
 // blocks A2' (tagged row) and B2' = S2' ^ A2' (plain row); the blocks with
 // E sit NS2/2 slots above those without, a constant offset. KI is the key
-// type in LDS: a wide K, or uint32_t for narrow rows.
+// type in LDS: a wide K, or uint32_t for narrow rows. The keys of in0/in1
+// (outputs S2' and S2'|E) are folded into out0/out1 (in and out may be the
+// same arrays).
 template <class KI>
-__device__ __attribute__((always_inline)) inline void cross_step(uint32_t off_a, uint32_t off_b, KI best0[NB],
-                                                                 KI best1[NB]) {
+__device__ __attribute__((always_inline)) inline void cross_step(uint32_t off_a, uint32_t off_b, const KI in0[NB],
+                                                                 const KI in1[NB], KI out0[NB], KI out1[NB]) {
     constexpr uint32_t HALF = NS2 / 2;
     const KI *pa = lds_at<KI>(off_a), *pb = lds_at<KI>(off_b);
     KI a0[NB], a1[NB], b0[NB], b1[NB];
@@ -1127,9 +1142,9 @@ __device__ __attribute__((always_inline)) inline void cross_step(uint32_t off_a,
     load_blk(pb, HALF, b1);                               // B2'|E
     load_blk(pb, 0u, b0);                                 // B2'
     load_blk(pa, HALF, a1);                               // A2'|E
-    conv_full<KI>(a0, b1, best1);                         // (S2'|E, A2')
-    conv_full<KI>(a0, b0, best0);                         // (S2', A2')
-    conv_full<KI>(a1, b0, best1);                         // (S2'|E, A2'|E)
+    conv_into<KI>(a0, b1, in1, out1);                     // (S2'|E, A2')
+    conv_into<KI>(a0, b0, in0, out0);                     // (S2', A2')
+    conv_into<KI>(a1, b0, out1, out1);                    // (S2'|E, A2'|E)
     // 64-bit keys: steps kept apart (measured faster). Narrow keys leave
     // registers for the compiler to start a step's reads during the
     // previous step's arithmetic (measured faster there).
@@ -1168,14 +1183,42 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
     const uint32_t low_off = slot_of(low2) * 16u;                    // block offset of lowbit(S2')
     static_assert(RL == R2 - 1 && (1u << RL) == NS2 / 2, "E is the top middle bit");
     static_assert(NS2 / 2 * 16 <= 16 * 1024, "slot offsets stay below the row size");
-    KI best0[NB], best1[NB];
+    // Best keys of the two output blocks. Narrow keys use two register sets:
+    // pair t of the chunk folds set (t - t0) & 1 into the other one, so the
+    // keys a pair starts from are still there when it ends, for the A_H
+    // tracking to compare with no copies.
+    KI bp0[NB], bp1[NB], bq0[NB], bq1[NB];
     uint32_t bh0[NB], bh1[NB];                                       // NARROW: A_H of each best key
 #pragma unroll
     for (int x = 0; x < NB; ++x) {
-        best0[x] = Key<KI>::none();
-        best1[x] = Key<KI>::none();
+        bp0[x] = Key<KI>::none();
+        bp1[x] = Key<KI>::none();
+        bq0[x] = Key<KI>::none();
+        bq1[x] = Key<KI>::none();
         bh0[x] = 0u;
         bh1[x] = 0u;
+    }
+    // The item's block offsets (bytes inside a row) of the even submask of
+    // each of its up to four two-step rounds, the same for every pair: an
+    // item starts at a submask without lowbit(S2') and has an even count, the
+    // odd submask is the even one plus lowbit(S2'), and slot_of is
+    // GF(2)-linear, so the odd step's offsets are the even step's XOR
+    // low_off. The item of S2' = 0 (its one submask) runs the same way: with
+    // lowbit 0 both steps are that submask, and a repeated candidate leaves a
+    // minimum as it is.
+    // (Narrow keys keep them in registers; wide keys, short of registers,
+    // compute each round's as it comes.)
+    auto round_offsets = [&](uint32_t &a2, uint32_t &fa, uint32_t &fb) {
+        const uint32_t sa = slot_of(a2) & (NS2 / 2 - 1u);
+        fa = sa * 16u;
+        fb = ((slot_s2 ^ sa) & (NS2 / 2 - 1u)) * 16u;
+        a2 = ((a2 | low2 | ~s2) + 1u) & s2;                          // two submasks on
+    };
+    uint32_t oa_item[4], ob_item[4];
+    if constexpr (NARROW) {
+        uint32_t a2 = a2_first;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) round_offsets(a2, oa_item[i], ob_item[i]);
     }
     // row buffer [buf][side] of this kernel's key type
     auto buf = [&](int b, int side) -> KI * {
@@ -1191,65 +1234,71 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
             copy_row(buf(b, 1), Pt, sh ^ a_h);
         }
     };
+    // A_H tracking of a finished pair (narrow keys): a key the pair lowered
+    // came from it; an equal key keeps the earlier, smaller A_H. It runs at
+    // the start of the next pair, where it overlaps that pair's first LDS
+    // reads (that pair writes its keys over the set compared here only
+    // after those reads), and after the last pair.
+    uint32_t ah_prev = 0;
+    auto track = [&](const KI *o0, const KI *o1, const KI *i0, const KI *i1) {
+#pragma unroll
+        for (int x = 0; x < NB; ++x) {
+            bh0[x] = o0[x] < i0[x] ? ah_prev : bh0[x];
+            bh1[x] = o1[x] < i1[x] ? ah_prev : bh1[x];
+        }
+    };
     // pair t of the chunk runs on buffer (t - t0) & 1 while the rows of
     // pair t + 1 are copied into the other one
     auto pair = [&](auto cur_c, uint32_t t) {
         constexpr int CUR = decltype(cur_c)::value;
+        // (wide keys track nothing: one set, updated in place)
+        KI *in0 = (NARROW && CUR) ? bq0 : bp0, *in1 = (NARROW && CUR) ? bq1 : bp1;
+        KI *out0 = !NARROW ? bp0 : CUR ? bp0 : bq0, *out1 = !NARROW ? bp1 : CUR ? bp1 : bq1;
         copies_done();
         lds_barrier();     // rows of pair t in place; pair t - 1 done with the other buffer
         const uint32_t ah_cur = ah;
         const uint32_t an = lowh | (((ah | ~rest) + 1u) & rest);    // next A_H holding lowbit(S_H)
         if (t + 1 < t1) copy_pair(CUR ^ 1, an);
         ah = an;
-        // the buffers' LDS offsets (multiples of the row size), opaque to the
-        // compiler: a known base would be folded into every read's address
-        // instead of added once (and wide buffer 1 lies beyond the 16-bit
-        // immediate offsets of LDS reads)
+        // The buffers' LDS offsets (multiples of the row size). Narrow rows
+        // lie in the first 64 KiB, so their bases are compile-time constants
+        // that the reads take as immediate offsets. Wide buffer 1 lies beyond
+        // the 16-bit immediates, so wide bases are kept opaque to the
+        // compiler and added once per address.
         typedef __attribute__((address_space(3))) const KI lds_k;
         uint32_t oa = (uint32_t)(uintptr_t)(lds_k *)buf(CUR, 0);
         uint32_t ob = (uint32_t)(uintptr_t)(lds_k *)buf(CUR, 1);
-        asm("" : "+s"(oa), "+s"(ob));
+        if constexpr (!NARROW) asm("" : "+s"(oa), "+s"(ob));
         if (has_item) {
-            KI old0[NB], old1[NB];
-            if constexpr (NARROW) {
-#pragma unroll
-                for (int x = 0; x < NB; ++x) { old0[x] = best0[x]; old1[x] = best1[x]; }
-            }
-            if (s2 == 0) {
-                cross_step<KI>(oa, ob, best0, best1);
-                copies_done();
-            } else {
-                // every item starts at a submask without lowbit(S2') and has an
-                // even count; the odd submask is the even one plus lowbit(S2').
-                // slot_of is GF(2)-linear and the slot offsets (below 4 KiB) sit
-                // under the row offsets' zero bits, so its block offsets are the
-                // even step's XOR a constant of the item.
-                uint32_t a2 = a2_first;
-                auto two = [&]() {
-                    const uint32_t sa = slot_of(a2) & (NS2 / 2 - 1u);
-                    const uint32_t sb = (slot_s2 ^ sa) & (NS2 / 2 - 1u);
-                    const uint32_t off_a = oa + sa * 16u, off_b = ob + sb * 16u;
-                    cross_step<KI>(off_a, off_b, best0, best1);
-                    cross_step<KI>(off_a ^ low_off, off_b ^ low_off, best0, best1);
-                    a2 = ((a2 | low2 | ~s2) + 1u) & s2;            // two submasks on
-                };
-                // the next pair's copies land while the first two steps run;
-                // retired before the loop on every path, they leave the loop's
-                // LDS reads free to wait only for what each use needs
-                two();
-                copies_done();
-                for (uint32_t i = 2; i < cnt; i += 2) two();
-            }
-            if constexpr (NARROW) {
-                // a key this pair lowered came from this pair; an equal key
-                // keeps the earlier, smaller A_H
-#pragma unroll
-                for (int x = 0; x < NB; ++x) {
-                    bh0[x] = best0[x] < old0[x] ? ah_cur : bh0[x];
-                    bh1[x] = best1[x] < old1[x] ? ah_cur : bh1[x];
+            // pair t - 1 folded this pair's output set into its input set
+            if constexpr (NARROW)
+                if (t > t0) track(in0, in1, out0, out1);
+            uint32_t a2 = a2_first;
+            auto two = [&](int i, const KI *i0, const KI *i1) {
+                uint32_t fa, fb;
+                if constexpr (NARROW) {
+                    fa = oa_item[i];
+                    fb = ob_item[i];
+                } else {
+                    round_offsets(a2, fa, fb);
                 }
+                cross_step<KI>(oa + fa, ob + fb, i0, i1, out0, out1);
+                cross_step<KI>(oa + (fa ^ low_off), ob + (fb ^ low_off), out0, out1, out0, out1);
+            };
+            // the next pair's copies land while the first two steps run;
+            // retired before the rest, they leave the later LDS reads free to
+            // wait only for what each use needs
+            two(0, in0, in1);
+            copies_done();
+            if constexpr (NARROW) {
+                if (cnt > 2) two(1, out0, out1);
+                if (cnt > 4) two(2, out0, out1);
+                if (cnt > 6) two(3, out0, out1);
+            } else {
+                for (uint32_t i = 2; i < cnt; i += 2) two(0, out0, out1);
             }
         }
+        ah_prev = ah_cur;
     };
     if (t0 < t1) copy_pair(0, ah);
     for (uint32_t t = t0; t < t1; t += 2) {
@@ -1257,12 +1306,24 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
         if (t + 1 < t1) pair(std::integral_constant<int, 1>{}, t + 1);
     }
     if (has_item) {
-        if constexpr (NARROW) {
-            flush_narrow<K>(best0, bh0, s2, m, s.acc);
-            flush_narrow<K>(best1, bh1, s2 | E, m, s.acc);
+        // the last pair's tracking; an odd number of pairs leaves the keys in
+        // the second set
+        // (a branch, not a pointer select, keeps both sets in registers)
+        auto flush_set = [&](const KI *f0, const KI *f1) {
+            if constexpr (NARROW) {
+                flush_narrow<K>(f0, bh0, s2, m, s.acc);
+                flush_narrow<K>(f1, bh1, s2 | E, m, s.acc);
+            } else {
+                flush<K>(f0, s2, s.acc);
+                flush<K>(f1, s2 | E, s.acc);
+            }
+        };
+        if (NARROW && ((t1 - t0) & 1u)) {
+            track(bq0, bq1, bp0, bp1);
+            flush_set(bq0, bq1);
         } else {
-            flush<K>(best0, s2, s.acc);
-            flush<K>(best1, s2 | E, s.acc);
+            if (NARROW && t1 > t0) track(bp0, bp1, bq0, bq1);
+            flush_set(bp0, bp1);
         }
     }
     lds_barrier();
