@@ -228,6 +228,14 @@ int mpt_ctx_build_weights(mpt_ctx *ctx, int m, int64_t n_chunks, int64_t nnz, co
 int mpt_ctx_solve_exact(mpt_ctx *ctx, int64_t *opt_cost, int64_t *savings, uint32_t *split_host);
 
 /*
+ * OPT_free and the savings of the last solve (HOST outs, nullable), after a
+ * solve (else MPT_E_STATE): reads C(full set) back, synchronising the stream.
+ * With this call a solve that returns no host data, the extraction and the
+ * read-back run as one stream of work with a single synchronisation.
+ */
+int mpt_ctx_optimum(const mpt_ctx *ctx, int64_t *opt_cost, int64_t *savings);
+
+/*
  * Phase 3 (as mpt_extract_orders), after a solve (else MPT_E_STATE).
  *   order_chunks_host  HOST out, nullable: int32 [nnz], pi_i at
  *                      [req_off[i], req_off[i+1])
@@ -429,7 +437,10 @@ const char *mpt_last_error(void);
 /*
  * Diagnostics: per-kernel device time with HIP events recorded on the
  * caller's stream around every launch. mpt_profile_begin() clears and
- * enables recording (process-wide); mpt_profile_end() waits for the events,
+ * enables recording (process-wide); mpt_profile_begin_prefix(p) does the
+ * same for the launches whose label starts with p only (the events add a few
+ * microseconds between launches, so a timing run records only the kernels it
+ * needs); mpt_profile_end() waits for the events,
  * fills up to max_entries rows, disables recording and returns the number of
  * distinct kernels seen (or a negative status).
  *   work: the algorithmic units the launches processed -- evaluated
@@ -443,6 +454,7 @@ typedef struct mpt_profile_row {
 } mpt_profile_row;
 
 int mpt_profile_begin(void);
+int mpt_profile_begin_prefix(const char *prefix);
 int mpt_profile_end(mpt_profile_row *rows, int max_entries);
 
 #ifdef __cplusplus

@@ -229,6 +229,25 @@ extern "C" int mpt_ctx_solve_exact(mpt_ctx *ctx, int64_t *opt_cost, int64_t *sav
     });
 }
 
+extern "C" int mpt_ctx_optimum(const mpt_ctx *ctx, int64_t *opt_cost, int64_t *savings) {
+    mptlib::clear_error();
+    if (!ctx) return fail(MPT_E_INVALID, "ctx must not be NULL");
+    if (ctx->state < SOLVED) return fail(MPT_E_STATE, "mpt_ctx_optimum needs a solved instance (mpt_ctx_solve_exact)");
+    return mptlib::guarded(__func__, [&]() -> int {
+        if (!opt_cost && !savings) return MPT_OK;
+        DeviceScope dev(ctx->device);
+        if (!dev.ok()) return fail(MPT_E_DEVICE, "cannot make device %d current", ctx->device);
+        int64_t opt = 0;
+        const int64_t *C = ctx->at<int64_t>(ctx->lay.C);
+        MPT_HIP_TRY(hipMemcpyAsync(&opt, C + (((int64_t)1 << ctx->m) - 1), sizeof opt, hipMemcpyDeviceToHost,
+                                   ctx->stream));
+        MPT_HIP_TRY(hipStreamSynchronize(ctx->stream));
+        if (opt_cost) *opt_cost = opt;
+        if (savings) *savings = ctx->total - opt;
+        return MPT_OK;
+    });
+}
+
 extern "C" int mpt_ctx_extract_orders(mpt_ctx *ctx, int32_t *order_chunks_host) {
     mptlib::clear_error();
     if (!ctx) return fail(MPT_E_INVALID, "ctx must not be NULL");

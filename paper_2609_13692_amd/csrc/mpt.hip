@@ -2186,12 +2186,13 @@ struct ProfRecord { std::string name; double work; hipEvent_t a, b; };
 struct Profiler {
     std::mutex mu;
     bool on = false;
+    std::string prefix;      // record only launches whose label starts with it
     std::vector<ProfRecord> recs;
 } g_prof;
 
 LaunchScope::LaunchScope(const char *n, double wk, hipStream_t st) : s_(st), name_(n), work_(wk) {
     std::lock_guard<std::mutex> g(g_prof.mu);
-    if (!g_prof.on) return;
+    if (!g_prof.on || std::strncmp(n, g_prof.prefix.c_str(), g_prof.prefix.size()) != 0) return;
     if (hipEventCreate(&a_) != hipSuccess || hipEventCreate(&b_) != hipSuccess) return;
     active_ = hipEventRecord(a_, s_) == hipSuccess;
 }
@@ -2207,10 +2208,13 @@ LaunchScope::~LaunchScope() {
 using mptlib::g_prof;
 using mptlib::ProfRecord;
 
-extern "C" int mpt_profile_begin(void) {
+extern "C" int mpt_profile_begin(void) { return mpt_profile_begin_prefix(""); }
+
+extern "C" int mpt_profile_begin_prefix(const char *prefix) {
     std::lock_guard<std::mutex> g(g_prof.mu);
     for (auto &r : g_prof.recs) { (void)hipEventDestroy(r.a); (void)hipEventDestroy(r.b); }
     g_prof.recs.clear();
+    g_prof.prefix = prefix ? prefix : "";
     g_prof.on = true;
     return MPT_OK;
 }

@@ -39,7 +39,8 @@ EXPORTED = ("mpt_workspace_bytes", "mpt_build_weights", "mpt_solve_exact", "mpt_
             "mpt_layout_cost", "mpt_cache_simulate", "mpt_pinned_workspace_bytes", "mpt_pinned_split",
             "mpt_pinned_assemble", "mpt_create", "mpt_destroy", "mpt_set_option", "mpt_ctx_workspace_bytes",
             "mpt_set_workspace", "mpt_ctx_build_weights", "mpt_ctx_solve_exact", "mpt_ctx_extract_orders",
-            "mpt_copy_table", "mpt_table_device", "mpt_solve_exact_noalloc")
+            "mpt_copy_table", "mpt_table_device", "mpt_solve_exact_noalloc", "mpt_ctx_optimum",
+            "mpt_profile_begin_prefix")
 
 
 class MptError(RuntimeError):
@@ -81,6 +82,8 @@ def load() -> ctypes.CDLL:
     lib.mpt_last_error.restype = ctypes.c_char_p
     lib.mpt_profile_begin.argtypes = []
     lib.mpt_profile_begin.restype = i32
+    lib.mpt_profile_begin_prefix.argtypes = [ctypes.c_char_p]
+    lib.mpt_profile_begin_prefix.restype = i32
     lib.mpt_profile_end.argtypes = [ctypes.POINTER(ProfileRow), i32]
     lib.mpt_profile_end.restype = i32
     lib.mpt_greedy_workspace_bytes.argtypes = [i32, i64, i64]
@@ -121,6 +124,8 @@ def load() -> ctypes.CDLL:
     lib.mpt_ctx_build_weights.restype = i32
     lib.mpt_ctx_solve_exact.argtypes = [P, P, P, P]
     lib.mpt_ctx_solve_exact.restype = i32
+    lib.mpt_ctx_optimum.argtypes = [P, P, P]
+    lib.mpt_ctx_optimum.restype = i32
     lib.mpt_ctx_extract_orders.argtypes = [P, P]
     lib.mpt_ctx_extract_orders.restype = i32
     lib.mpt_copy_table.argtypes = [P, i32, P, sz]
@@ -220,8 +225,9 @@ def mpt_extract_orders(m, n_chunks, req_off, req_chunks, sig, split, order_chunk
     _check(rc, "mpt_extract_orders")
 
 
-def profile_begin() -> None:
-    _check(load().mpt_profile_begin(), "mpt_profile_begin")
+def profile_begin(prefix: str = "") -> None:
+    """Start recording launch times (only labels starting with prefix)."""
+    _check(load().mpt_profile_begin_prefix(prefix.encode()), "mpt_profile_begin_prefix")
 
 
 def profile_end(max_rows: int = 64) -> dict:
@@ -634,6 +640,12 @@ class Context:
             self._h, ctypes.addressof(opt) if want_cost else None, ctypes.addressof(sav) if want_cost else None,
             split.ctypes.data if split is not None else None), "mpt_ctx_solve_exact")
         return (int(opt.value) if want_cost else None, int(sav.value) if want_cost else None, split)
+
+    def optimum(self):
+        """(OPT_free, savings) of the last solve (one synchronisation)."""
+        opt, sav = ctypes.c_int64(0), ctypes.c_int64(0)
+        _check(load().mpt_ctx_optimum(self._h, ctypes.addressof(opt), ctypes.addressof(sav)), "mpt_ctx_optimum")
+        return int(opt.value), int(sav.value)
 
     def extract_orders(self, to_host=True):
         import numpy as np

@@ -147,9 +147,11 @@ def test_state_machine():
     expect("MPT_E_STATE", ctx.extract_orders)
     ctx.build_weights(inst.m, inst.n_chunks, w, off, ch)
     expect("MPT_E_STATE", ctx.extract_orders)
+    expect("MPT_E_STATE", ctx.optimum)
     expect("MPT_E_STATE", ctx.copy_table, mpt.MPT_TABLE_C)
     assert np.array_equal(ctx.copy_table(mpt.MPT_TABLE_W), oracle.intersection_weights(inst))
     opt, sav, _ = ctx.solve_exact()
+    assert ctx.optimum() == (opt, sav)
     expect("MPT_E_STATE", ctx.copy_table, mpt.MPT_TABLE_ORDERS)
     orders = ctx.extract_orders()
     ref = oracle.solve(inst)
@@ -177,6 +179,22 @@ def test_state_machine():
     ptr, nb = ctx.table_device(mpt.MPT_TABLE_W)
     base = ctx.workspace.data_ptr()
     assert nb == 8 << inst.m and base <= ptr and ptr + nb <= base + ctx.workspace.numel()
+    ctx.close()
+
+
+def test_solve_and_extract_without_host_data():
+    """A solve that returns nothing to the host and the extraction queue
+    their work back to back; mpt_ctx_optimum then reads OPT_free."""
+    inst = wl.config(3)
+    ref = oracle.solve(inst)
+    ctx = mpt.Context("cuda")
+    w, off, ch = tensors(inst, "cuda")
+    ctx.reserve(inst.m, inst.n_chunks, inst.nnz)
+    ctx.build_weights(inst.m, inst.n_chunks, w, off, ch)
+    assert ctx.solve_exact(want_cost=False) == (None, None, None)
+    assert ctx.extract_orders(to_host=False) is None
+    assert ctx.optimum() == (ref["opt"], int(inst.weights[inst.req_chunks].sum()) - ref["opt"])
+    assert np.array_equal(ctx.copy_table(mpt.MPT_TABLE_ORDERS), ref["orders"])
     ctx.close()
 
 
