@@ -1066,24 +1066,31 @@ __device__ __attribute__((always_inline)) inline void finalize_row(int m, uint32
             const uint32_t base = sh | ((s2 << CB) << H);        // mask of (S_H, S2, X1 = 0)
             uint64_t out[NB];
             uint32_t sp[NB];
-            // S1 in order of popcount so that every A1 < S1 is ready
+            // the block's accumulated keys (cross pairs and this level's
+            // items), read together before the dependent chain below
+            uint64_t kacc[NB];
+#pragma unroll
+            for (int x = 0; x < NB; ++x) kacc[x] = Key<K>::key_value(s.acc[(s2 << CB) | x]);
+            // S = (S_H, 0, 0) with one request in S_H is a leaf: C = W
+            const bool leaf0 = s2 == 0 && (sh & (sh - 1u)) == 0;
+            // S1 in order of popcount so that every A1 < S1 is ready; no
+            // branches, so the reads above stay ahead of the chain
 #pragma unroll
             for (int pc = 0; pc <= CB; ++pc) {
 #pragma unroll
                 for (int s1 = 0; s1 < NB; ++s1) {
                     if (cpop(s1) != pc) continue;
-                    const uint32_t S = base | ((uint32_t)s1 << H);
                     const int64_t w = wv[s1];
-                    if (__popc(S) == 1) { out[s1] = (uint64_t)w << m; sp[s1] = 0; continue; }
-                    uint64_t kb = Key<K>::key_value(s.acc[(s2 << CB) | s1]);
+                    uint64_t kb = kacc[s1];
 #pragma unroll
                     for (int a1 = 0; a1 < NB; ++a1) {
                         if ((a1 & ~s1) || a1 == s1) continue;
                         const uint64_t c = out[a1] + b0[s1 ^ a1] + (base | ((uint32_t)a1 << H));
                         kb = c < kb ? c : kb;
                     }
-                    out[s1] = ((kb >> m) - (uint64_t)w) << m;
-                    sp[s1] = (uint32_t)(kb & mask);
+                    const bool leaf = s1 == 0 && leaf0;
+                    out[s1] = leaf ? (uint64_t)w << m : ((kb >> m) - (uint64_t)w) << m;
+                    sp[s1] = leaf ? 0u : (uint32_t)(kb & mask);
                 }
             }
             const uint32_t sl = slot_of(s2);
@@ -1112,6 +1119,159 @@ __device__ __attribute__((always_inline)) inline void finalize_row(int m, uint32
                     *reinterpret_cast<uint4 *>(Tn + at) = tv;
                     *reinterpret_cast<uint4 *>(rSn + npos(sl, 4 * q)) = tv;
                 }
+            }
+        }
+        lds_barrier();
+        item = item_next;
+        blk = blk_next;
+    }
+}
+
+// One self-pair item (as run_item_narrow) whose group minimum goes to the
+// narrow self-pair minima sacc (32-bit LDS atomics): every candidate of the
+// self pair has A_H = S_H, so the 32-bit key order is the (cost, A) order.
+__device__ inline void run_item_self(uint32_t item, const uint32_t *rA, const uint32_t *rB, uint32_t *sacc) {
+    const uint32_t s2 = item & 0xffffu;
+    const int k = __popc(s2);
+    const int tb = (int)((item >> 28) & 7u);
+    const uint32_t cnt = 1u << tb;
+    const uint32_t slot_s2 = slot_of(s2);
+    uint32_t a2 = (item >> 16) & 0xfffu;
+    uint32_t best[NB];
+#pragma unroll
+    for (int x = 0; x < NB; ++x) best[x] = Key<uint32_t>::none();
+    for (uint32_t i = 0; i < cnt; ++i) {
+        if (a2 != s2) {
+            const uint32_t sa = slot_of(a2), sb = slot_s2 ^ sa;
+            uint32_t a[NB], b[NB];
+            load_blk(rA, sa, a);
+            load_blk(rB, sb, b);
+            conv_full<uint32_t>(a, b, best);
+        }
+        a2 = ((a2 | ~s2) + 1u) & s2;
+    }
+    const uint32_t chunks = 1u << (k - tb);
+    const uint32_t seg = chunks < 8u ? chunks : 8u;
+    const uint32_t lane = threadIdx.x & (kWave - 1);
+#pragma unroll
+    for (int x = 0; x < NB; ++x) {
+        uint32_t b = best[x];
+        if (seg >= 2) { const uint32_t o = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)b, 0xB1, 0xF, 0xF, false); b = o < b ? o : b; }
+        if (seg >= 4) { const uint32_t o = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)b, 0x4E, 0xF, 0xF, false); b = o < b ? o : b; }
+        if (seg >= 8) { const uint32_t o = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)b, 0x141, 0xF, 0xF, false); b = o < b ? o : b; }
+        best[x] = b;
+    }
+    if ((lane & (seg - 1)) == 0) {
+#pragma unroll
+        for (int x = 0; x < NB; ++x)
+            if (best[x] != Key<uint32_t>::none()) atomicMin(&sacc[(s2 << CB) | x], best[x]);
+    }
+}
+
+// Completes row S_H (non-empty) on narrow keys. In LDS: acc, the 64-bit
+// cross-pair keys of the row; rSn, row S_H (tagged, filled here); r0n, row 0
+// (plain); sacc, the narrow self-pair minima (4096 entries set to all ones
+// before the caller's barrier). Writes the row to the plain 64-bit table, to
+// both narrow tables and its splits to Sr (row-major, mask order inside a
+// row). The self pair's candidates (A_H = S_H) are kept as 32-bit keys up
+// to the comparison with the cross pairs' key of each entry.
+template <class K>
+__device__ __attribute__((always_inline)) inline void finalize_row_narrow(
+        int m, uint32_t sh, const uint64_t *acc, uint32_t *rSn, const uint32_t *r0n, uint32_t *sacc,
+        const int64_t *__restrict__ Wr, uint64_t *__restrict__ Pt, uint32_t *__restrict__ Tn,
+        uint32_t *__restrict__ Pn, uint32_t *__restrict__ Sr) {
+    const int H = m - L;
+    const uint32_t row = sh << L;
+    const uint64_t mask = ((uint64_t)1 << m) - 1u;
+    auto level_item = [](int k) -> uint32_t {
+        const int it = c_items.begin[k] + (int)threadIdx.x;
+        return it < c_items.end[k] ? c_items.v[it] : 0u;
+    };
+    auto level_blk = [](int k) -> uint32_t {
+        const int bi = c_blocks.begin[k] + (int)threadIdx.x;
+        return bi < c_blocks.end[k] ? (uint32_t)c_blocks.v[bi] | 0x10000u : 0u;
+    };
+    uint32_t item = level_item(0), blk = level_blk(0);
+    // block 0 of row 0, plain narrow: C(X1 << H) << L for every low part X1
+    uint32_t b0n[NB];
+#pragma unroll
+    for (int x = 0; x < NB; ++x) b0n[x] = r0n[npos(0u, x)];
+    // S = (S_H, 0, 0) with one request in S_H is a leaf: C = W
+    const bool single = (sh & (sh - 1u)) == 0;
+    for (int k = 0; k <= R2; ++k) {
+        const uint32_t item_next = k < R2 ? level_item(k + 1) : 0u;
+        const uint32_t blk_next = k < R2 ? level_blk(k + 1) : 0u;
+        int64_t wv[NB];
+        if (blk) {
+            const int64_t *wp = Wr + (row | ((blk & 0xffffu) << CB));
+#pragma unroll
+            for (int x = 0; x < NB; ++x) wv[x] = wp[x];
+        }
+        // A2 a proper submask of S2
+        if (item) run_item_self(item, rSn, r0n, sacc);
+        lds_barrier();
+        // A2 = S2: in-block pairs, one thread per block of this level; A =
+        // (S_H, S2, A1) holds lowbit(S), B = (0, 0, S1 ^ A1) is in block 0
+        // of row 0
+        if (blk) {
+            const uint32_t s2 = blk & 0xffffu;
+            const uint32_t tag = s2 << CB;                       // in-row part of (S2, X1 = 0)
+            // the block's self-pair minima and cross-pair keys, read together
+            uint32_t sself[NB];
+            {
+                const uint4 *sp4 = reinterpret_cast<const uint4 *>(sacc + tag);
+                const uint4 u0 = sp4[0], u1 = sp4[1];
+                sself[0] = u0.x; sself[1] = u0.y; sself[2] = u0.z; sself[3] = u0.w;
+                sself[4] = u1.x; sself[5] = u1.y; sself[6] = u1.z; sself[7] = u1.w;
+            }
+            uint64_t kacc[NB];
+#pragma unroll
+            for (int x = 0; x < NB; ++x) kacc[x] = Key<K>::key_value(acc[tag | x]);
+            const bool leaf0 = s2 == 0 && single;
+            uint32_t on[NB], sp[NB];
+            uint64_t cm[NB];
+            // S1 in order of popcount so that every A1 < S1 is ready
+#pragma unroll
+            for (int pc = 0; pc <= CB; ++pc) {
+#pragma unroll
+                for (int s1 = 0; s1 < NB; ++s1) {
+                    if (cpop(s1) != pc) continue;
+                    uint32_t nk = sself[s1];
+#pragma unroll
+                    for (int a1 = 0; a1 < NB; ++a1) {
+                        if ((a1 & ~s1) || a1 == s1) continue;
+                        const uint32_t c = on[a1] + b0n[s1 ^ a1];
+                        nk = c < nk ? c : nk;
+                    }
+                    // as a 64-bit key: cost << m | A_L << H | A_H, A_H = S_H
+                    const uint64_t ks = nk == Key<uint32_t>::none()
+                                            ? ~0ull
+                                            : ((uint64_t)(nk >> L) << m) | ((uint64_t)(nk & (ROW - 1u)) << H) | sh;
+                    const uint64_t kb = kacc[s1] < ks ? kacc[s1] : ks;
+                    const int64_t w = wv[s1];
+                    const bool leaf = s1 == 0 && leaf0;
+                    const uint64_t c = leaf ? (uint64_t)w : (kb >> m) - (uint64_t)w;
+                    sp[s1] = leaf ? 0u : (uint32_t)(kb & mask);
+                    cm[s1] = c << m;
+                    on[s1] = ((uint32_t)c << L) | tag | (uint32_t)s1;
+                }
+            }
+            const uint32_t sl = slot_of(s2);
+#pragma unroll
+            for (int x = 0; x < NB; ++x) {
+                Pt[row + lpos(sl, x)] = Key<K>::store(cm[x]);
+                Sr[row | tag | (uint32_t)x] = sp[x];
+            }
+            // C(X) << L, and tagged with X_L = S2 << CB | X1
+#pragma unroll
+            for (int q = 0; q < NB / 4; ++q) {
+                const uint32_t at = row + npos(sl, 4 * q);
+                const uint32_t lo = ~(ROW - 1u);
+                *reinterpret_cast<uint4 *>(Pn + at) =
+                    make_uint4(on[4 * q] & lo, on[4 * q + 1] & lo, on[4 * q + 2] & lo, on[4 * q + 3] & lo);
+                const uint4 tv = make_uint4(on[4 * q], on[4 * q + 1], on[4 * q + 2], on[4 * q + 3]);
+                *reinterpret_cast<uint4 *>(Tn + at) = tv;
+                *reinterpret_cast<uint4 *>(rSn + npos(sl, 4 * q)) = tv;
             }
         }
         lds_barrier();
@@ -1328,11 +1488,17 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
     }
     lds_barrier();
     if (fused) {
-        if constexpr (NARROW) copy_row(buf(0, 1), Pn, 0u);
-        else copy_row(s.r[0][1], Pt, 0u);
+        if constexpr (NARROW) {
+            copy_row(buf(0, 1), Pn, 0u);
+            uint32_t *sacc = buf(1, 0);
+            for (int e = threadIdx.x; e < ROW; e += THREADS) sacc[e] = Key<uint32_t>::none();
+        } else {
+            copy_row(s.r[0][1], Pt, 0u);
+        }
         copies_done();
         lds_barrier();
-        finalize_row<K, NARROW>(m, sh, s, buf(0, 0), buf(0, 1), Wr, Tt, Pt, Tn, Pn, Sr);
+        if constexpr (NARROW) finalize_row_narrow<K>(m, sh, s.acc, buf(0, 0), buf(0, 1), buf(1, 0), Wr, Pt, Tn, Pn, Sr);
+        else finalize_row<K, NARROW>(m, sh, s, buf(0, 0), buf(0, 1), Wr, Tt, Pt, Tn, Pn, Sr);
     } else {
         uint64_t *dst = partial + (size_t)bid * ROW;
         for (int e = threadIdx.x; e < ROW; e += THREADS) dst[e] = s.acc[e];
@@ -1372,11 +1538,15 @@ __global__ __launch_bounds__(THREADS) void k_rb_final(int m, int h, uint32_t chu
     for (int e = threadIdx.x; e < ROW; e += THREADS) s.acc[e] = chunks ? src[e] : ~0ull;
     // NARROW: the two narrow rows (16 KiB each) at the start of the row space
     uint32_t *nr = reinterpret_cast<uint32_t *>(&s.r[0][0][0]);
-    if constexpr (NARROW) copy_row(nr + ROW, Pn, 0u);
-    else copy_row(s.r[0][1], Pt, 0u);
+    if constexpr (NARROW) {
+        copy_row(nr + ROW, Pn, 0u);
+        for (int e = threadIdx.x; e < ROW; e += THREADS) nr[2 * ROW + e] = Key<uint32_t>::none();
+    } else {
+        copy_row(s.r[0][1], Pt, 0u);
+    }
     copies_done();
     lds_barrier();
-    if constexpr (NARROW) finalize_row<K, NARROW>(m, sh, s, nr, nr + ROW, Wr, Tt, Pt, Tn, Pn, Sr);
+    if constexpr (NARROW) finalize_row_narrow<K>(m, sh, s.acc, nr, nr + ROW, nr + 2 * ROW, Wr, Pt, Tn, Pn, Sr);
     else finalize_row<K, NARROW>(m, sh, s, s.r[0][0], s.r[0][1], Wr, Tt, Pt, Tn, Pn, Sr);
 }
 
