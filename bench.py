@@ -18,7 +18,8 @@ against the VALU instruction peak; `zeta` the W-table kernel against HBM bandwid
 `cpu_baseline` the CPU oracle on a bounded sample of the same workload;
 `greedy` the Section 6.2-6.3 heuristic and bound at m = 4096 requests;
 `cache` the Section 7-8 layouts and radix-cache grid on the same instance;
-`pinned` the Section 7.1 pinned variant on it.
+`pinned` the Section 7.1 pinned variant on it; `dense_w` the W table's
+dense route on an instance with long requests.
 """
 from __future__ import annotations
 
@@ -195,6 +196,59 @@ def greedy_bench(steps: int, warmup: int, cpu: bool) -> dict:
     return out
 
 
+def dense_w_bench(steps: int, warmup: int) -> dict:
+    """The W table's dense route (scatter into a zeroed table, then the
+    superset zeta in read-write passes of up to 11 and 5 bits) on the long-
+    list instance (m = 25 requests of 90000 chunks over 2^20), inputs
+    resident in HBM. One step = one mpt_ctx_build_weights (demand sets,
+    compaction, W). `roofline` prices the route's own table traffic (the
+    zeroing write plus a read and a write per pass) against HBM; the
+    algorithmic minimum is one write of the table."""
+    import torch
+    from paper_2609_13692_amd import mpt
+    from paper_2609_13692_amd import workloads as wl
+
+    inst = wl.gen_long_lists()
+    m = inst.m
+    dev = torch.device("cuda")
+    w = torch.as_tensor(inst.weights, dtype=torch.int64).to(dev)
+    off = torch.as_tensor(inst.req_off, dtype=torch.int64).to(dev)
+    ch = torch.as_tensor(inst.req_chunks, dtype=torch.int32).to(dev)
+    ctx = mpt.Context(dev)
+    ctx.reserve(m, inst.n_chunks, inst.nnz)
+    for _ in range(warmup):
+        ctx.build_weights(m, inst.n_chunks, w, off, ch)
+    torch.cuda.synchronize()
+    mpt.profile_begin()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        ctx.build_weights(m, inst.n_chunks, w, off, ch)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    prof = mpt.profile_end()
+    ctx.close()
+    dense = prof.get("weights_dense")
+    passes = 1 + max(0, -(-(m - 11) // 5))
+    route_bytes = 8 * (1 << m) * (1 + 2 * passes)
+    out = {
+        "workload": f"long lists: m={m} requests of 90000 chunks drawn uniformly from u={inst.n_chunks}, "
+                    f"w~U{{1..999}}, seed 12, nnz={inst.nnz}",
+        "instance_sha256": inst.sha256()[:16],
+        "ms_per_build": round((t1 - t0) * 1000.0 / steps, 3),
+        "phases_ms": {k: round(v["total_ms"] / steps, 4) for k, v in prof.items()},
+        "route": "dense" if dense else "list",
+    }
+    if dense:
+        ms = dense["total_ms"] / dense["launches"]
+        gbs = route_bytes / (ms / 1000.0) / 1e9
+        out["roofline"] = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                           "frac": round(gbs / HBM_PEAK_GBS, 4), "route_bytes": route_bytes,
+                           "passes": passes, "ms": round(ms, 4),
+                           "algorithmic_bytes": 8 * (1 << m),
+                           "algorithmic_GBps": round(8 * (1 << m) / (ms / 1000.0) / 1e9, 1)}
+    return out
+
+
 CACHE_WINDOWS = (1, 128, 512, 2048, 0)          # 0: the whole stream
 CACHE_CAPACITIES = (1, 4, 16, 64, 256, 1024)     # multiples of max_i w(R_i)
 
@@ -303,6 +357,7 @@ def main() -> int:
     ap.add_argument("--cpu-budget", type=float, default=25.0, help="seconds for the CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-greedy", action="store_true", help="skip the Section 6.2-6.3 measurement")
+    ap.add_argument("--no-dense", action="store_true", help="skip the dense W route measurement")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB before the timed steps "
                          "(a known-size kernel that scales rocprofv3 FETCH_SIZE/WRITE_SIZE)")
@@ -436,6 +491,8 @@ def main() -> int:
         "roofline": roofline,
         "zeta": zeta,
     }
+    if not args.no_dense:
+        line["dense_w"] = dense_w_bench(max(1, args.steps), max(1, args.warmup))
     if not args.no_greedy:
         line["greedy"] = greedy_bench(max(1, args.steps), max(1, args.warmup), not args.no_cpu_baseline)
         line["cache"] = cache_bench(max(1, args.steps), max(1, args.warmup), not args.no_cpu_baseline)

@@ -180,6 +180,17 @@ typedef struct mpt_ctx mpt_ctx;
  * workspace size. */
 #define MPT_OPT_CHUNK_PAIRS 1
 
+/* MPT_OPT_WEIGHT_ROUTE: how a build computes W (Section 3.1's superset
+ * sums). 0 (default) picks by size; MPT_ROUTE_LIST makes each 2^12-subset
+ * tile scan the list of (S_x, w(x)) and write its part of W once (cost grows
+ * with tiles x list length); MPT_ROUTE_DENSE scatters the list into W and
+ * runs the superset zeta in place over the whole table (cost grows with
+ * 2^m). The tables are the same on either route. */
+#define MPT_OPT_WEIGHT_ROUTE 2
+#define MPT_ROUTE_AUTO 0
+#define MPT_ROUTE_LIST 1
+#define MPT_ROUTE_DENSE 2
+
 /* New context on HIP device hip_device, enqueueing on hip_stream (a
  * hipStream_t created on that device; NULL = its null stream). *out = NULL
  * on failure. Every context call makes hip_device current for its duration

@@ -14,10 +14,11 @@ namespace mptcore {
 // library's level plan). 0 for sizes out of range.
 size_t workspace_bytes(int m, int64_t nnz, int64_t chunk_pairs);
 
-// W table and demand sets; *total (nullable) receives sum_i w(R_i).
+// W table and demand sets; *total (nullable) receives sum_i w(R_i). route:
+// MPT_ROUTE_AUTO, MPT_ROUTE_LIST or MPT_ROUTE_DENSE.
 int build(int m, int64_t n_chunks, int64_t nnz, const int64_t *chunk_w, const int64_t *req_off,
           const int32_t *req_chunks, uint32_t *sig, int64_t *W, void *workspace, size_t workspace_bytes,
-          hipStream_t s, int64_t *total);
+          hipStream_t s, int64_t *total, int route);
 
 // The Section 3.1 DP. total: sum_i w(R_i) of the instance that W belongs to,
 // or < 0 to read it back from W (one stream synchronisation). chunk_pairs > 0

@@ -80,6 +80,7 @@ struct mpt_ctx {
     char *ws = nullptr;
     size_t ws_bytes = 0;
     int64_t chunk_pairs = 0;
+    int route = MPT_ROUTE_AUTO;
     State state = CREATED;
     int m = 0;
     int64_t n_chunks = 0, nnz = 0, total = 0;
@@ -137,9 +138,16 @@ extern "C" void mpt_destroy(mpt_ctx *ctx) { delete ctx; }
 extern "C" int mpt_set_option(mpt_ctx *ctx, int option, int64_t value) {
     mptlib::clear_error();
     if (!ctx) return fail(MPT_E_INVALID, "ctx must not be NULL");
-    if (option != MPT_OPT_CHUNK_PAIRS) return fail(MPT_E_INVALID, "unknown option %d", option);
-    if (value < 0) return fail(MPT_E_INVALID, "MPT_OPT_CHUNK_PAIRS = %lld is negative", (long long)value);
-    ctx->chunk_pairs = value;
+    if (option == MPT_OPT_CHUNK_PAIRS) {
+        if (value < 0) return fail(MPT_E_INVALID, "MPT_OPT_CHUNK_PAIRS = %lld is negative", (long long)value);
+        ctx->chunk_pairs = value;
+    } else if (option == MPT_OPT_WEIGHT_ROUTE) {
+        if (value != MPT_ROUTE_AUTO && value != MPT_ROUTE_LIST && value != MPT_ROUTE_DENSE)
+            return fail(MPT_E_INVALID, "MPT_OPT_WEIGHT_ROUTE = %lld is not a route", (long long)value);
+        ctx->route = (int)value;
+    } else {
+        return fail(MPT_E_INVALID, "unknown option %d", option);
+    }
     ctx->state = CREATED;
     return MPT_OK;
 }
@@ -194,7 +202,7 @@ extern "C" int mpt_ctx_build_weights(mpt_ctx *ctx, int m, int64_t n_chunks, int6
         int64_t total = 0;
         const int rc = mptcore::build(m, n_chunks, nnz, ctx->at<int64_t>(L.chunk_w), ctx->at<int64_t>(L.req_off),
                                       ctx->at<int32_t>(L.req_chunks), ctx->at<uint32_t>(L.sig), ctx->at<int64_t>(L.W),
-                                      ctx->ws + L.core, L.core_bytes, s, &total);
+                                      ctx->ws + L.core, L.core_bytes, s, &total, ctx->route);
         if (rc) return rc;
         ctx->total = total;
         ctx->state = BUILT;

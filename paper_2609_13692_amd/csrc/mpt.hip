@@ -156,21 +156,125 @@ __global__ void k_demand_sets(int m, int64_t n_chunks, int64_t nnz, const int64_
 }
 
 // weight check and compaction of the chunks that some request holds into a
-// (S_x, w(x)) list; the others only reach W(empty) and are summed apart.
-__global__ void k_compact(int64_t n_chunks, int64_t cap, const int64_t *w, const uint32_t *sig,
-                          uint32_t *list_sig, int64_t *list_w, WsHeader *h) {
-    for (int64_t x = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; x < n_chunks; x += (int64_t)gridDim.x * blockDim.x) {
-        int64_t wx = w[x];
-        if (wx <= 0 || wx > MPT_MAX_CHUNK_WEIGHT) { atomicOr(&h->err, ERR_WEIGHT); continue; }
-        uint32_t s = sig[x];
-        if (s == 0) {
-            atomicAdd((unsigned long long *)&h->zero_weight, (unsigned long long)wx);
-        } else {
-            uint32_t idx = atomicAdd(&h->n_list, 1u);
-            if ((int64_t)idx < cap) { list_sig[idx] = s; list_w[idx] = wx; }
-            else atomicOr(&h->err, ERR_INVALID);
-        }
+// (S_x, w(x)) list, in chunk order; the others only reach W(empty) and are
+// summed apart. Three passes without contended atomics: each block counts
+// its contiguous range, one workgroup scans the counts (and sums the
+// unrequested weight), each block writes its range at its offset.
+constexpr int kCompactThreads = 256;
+constexpr int kCompactMaxBlocks = 4096;
+
+struct CompactPlan {
+    int64_t per;     // chunks per block (a multiple of the block size)
+    uint32_t blocks;
+};
+
+inline CompactPlan compact_plan(int64_t n_chunks) {
+    const int64_t want = (n_chunks + 4095) / 4096;
+    const uint32_t blocks = (uint32_t)std::max<int64_t>(1, std::min<int64_t>(want, kCompactMaxBlocks));
+    int64_t per = (n_chunks + blocks - 1) / blocks;
+    per = (per + kCompactThreads - 1) / kCompactThreads * kCompactThreads;
+    return {std::max<int64_t>(per, kCompactThreads), blocks};
+}
+
+__device__ inline int64_t block_sum_i64(int64_t v, int64_t *red) {
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1) v += __shfl_xor(v, off, kWave);
+    if ((threadIdx.x & (kWave - 1)) == 0) red[threadIdx.x / kWave] = v;
+    __syncthreads();
+    int64_t s = 0;
+    for (int i = 0; i < kCompactThreads / kWave; ++i) s += red[i];
+    return s;
+}
+
+__global__ __launch_bounds__(kCompactThreads) void k_compact_count(int64_t n_chunks, int64_t per, const int64_t *w,
+                                                                    const uint32_t *sig, uint32_t *bcount,
+                                                                    int64_t *bzero, WsHeader *h) {
+    __shared__ int64_t red[2][kCompactThreads / kWave];
+    const int64_t lo = blockIdx.x * per, hi = min(n_chunks, lo + per);
+    int64_t taken = 0, zw = 0;
+    bool bad = false;
+    for (int64_t x = lo + threadIdx.x; x < hi; x += kCompactThreads) {
+        const int64_t wx = w[x];
+        const uint32_t sx = sig[x];
+        if (wx <= 0 || wx > MPT_MAX_CHUNK_WEIGHT) { bad = true; continue; }
+        if (sx) ++taken; else zw += wx;
     }
+    if (bad) atomicOr(&h->err, ERR_WEIGHT);
+    taken = block_sum_i64(taken, red[0]);
+    zw = block_sum_i64(zw, red[1]);
+    if (threadIdx.x == 0) { bcount[blockIdx.x] = (uint32_t)taken; bzero[blockIdx.x] = zw; }
+}
+
+// exclusive scan of the block counts, the list length and the unrequested
+// weight into the header; one workgroup
+constexpr int kScanThreads = 1024;
+__global__ __launch_bounds__(kScanThreads) void k_compact_scan(uint32_t blocks, const uint32_t *bcount,
+                                                               const int64_t *bzero, uint32_t *boff, WsHeader *h) {
+    __shared__ uint64_t part[kScanThreads];
+    __shared__ int64_t zpart[kScanThreads];
+    const uint32_t t = threadIdx.x;
+    const uint32_t per = (blocks + kScanThreads - 1) / kScanThreads;
+    const uint32_t lo = min(blocks, t * per), hi = min(blocks, lo + per);
+    uint64_t sum = 0;
+    int64_t zs = 0;
+    for (uint32_t i = lo; i < hi; ++i) { sum += bcount[i]; zs += bzero[i]; }
+    part[t] = sum;
+    zpart[t] = zs;
+    __syncthreads();
+    for (uint32_t off = 1; off < kScanThreads; off <<= 1) {
+        const uint64_t v = t >= off ? part[t - off] : 0u;
+        const int64_t z = t >= off ? zpart[t - off] : 0;
+        __syncthreads();
+        part[t] += v;
+        zpart[t] += z;
+        __syncthreads();
+    }
+    uint64_t run = t ? part[t - 1] : 0u;
+    for (uint32_t i = lo; i < hi; ++i) {
+        boff[i] = (uint32_t)run;
+        run += bcount[i];
+    }
+    if (t == kScanThreads - 1) {
+        h->n_list = (uint32_t)part[t];
+        h->zero_weight = zpart[t];
+    }
+}
+
+__global__ __launch_bounds__(kCompactThreads) void k_compact_write(int64_t n_chunks, int64_t per, int64_t cap,
+                                                                    const int64_t *w, const uint32_t *sig,
+                                                                    const uint32_t *boff, uint32_t *list_sig,
+                                                                    int64_t *list_w, WsHeader *h) {
+    constexpr int kWaves = kCompactThreads / kWave;
+    __shared__ uint32_t wcount[kWaves];
+    const int lane = (int)(threadIdx.x & (kWave - 1)), wv = (int)(threadIdx.x / kWave);
+    const uint64_t below = lane ? (~0ull >> (kWave - lane)) : 0ull;     // lanes under this one
+    const int64_t lo = blockIdx.x * per, hi = min(n_chunks, lo + per);
+    uint32_t base = boff[blockIdx.x];
+    bool over = false;
+    // every thread of the block runs the same iterations (out-of-range lanes idle)
+    for (int64_t x0 = lo; x0 < hi; x0 += kCompactThreads) {
+        const int64_t x = x0 + threadIdx.x;
+        const int64_t wx = x < hi ? w[x] : 0;
+        const uint32_t sx = x < hi ? sig[x] : 0u;
+        const bool take = sx != 0 && wx > 0 && wx <= MPT_MAX_CHUNK_WEIGHT;
+        const uint64_t mask = __ballot(take);
+        if (lane == 0) wcount[wv] = (uint32_t)__popcll(mask);
+        __syncthreads();
+        uint32_t before = 0, all = 0;
+#pragma unroll
+        for (int i = 0; i < kWaves; ++i) {
+            before += i < wv ? wcount[i] : 0u;
+            all += wcount[i];
+        }
+        if (take) {
+            const uint32_t idx = base + before + (uint32_t)__popcll(mask & below);
+            if ((int64_t)idx < cap) { list_sig[idx] = sx; list_w[idx] = wx; }
+            else over = true;
+        }
+        base += all;
+        __syncthreads();
+    }
+    if (over) atomicOr(&h->err, ERR_INVALID);
 }
 
 // W table, one workgroup per tile of 2^13 consecutive subsets that share the
@@ -223,8 +327,13 @@ __device__ inline void zeta_scatter(int64_t *tile, uint32_t low, int64_t w) {
 // in registers and walks tiles blockIdx.x, + gridDim.x, ...; a tile's stores
 // drain while the next tile is built.
 constexpr int kZetaHeld = 4;
-// above this many list checks (tiles x slots) the dense route is cheaper
-constexpr double kDenseAbove = 8589934592.0;
+// the dense route pays once the tiles' list checks (tiles x slots, about
+// 1 ps each) cost more than its passes over the table (about 10 ps per
+// subset at m = 25) plus its launches (about 30 us)
+inline bool dense_route_pays(int m, int64_t nnz) {
+    const double tiles = m > 12 ? std::ldexp(1.0, m - 12) : 1.0;
+    return tiles * (double)nnz > 10.0 * std::ldexp(1.0, m) + 3.0e7;
+}
 
 __global__ __launch_bounds__(kZetaThreads) void k_weights_tile(
         int m, uint32_t cap, uint32_t n_tiles, const uint32_t *list_sig, const int64_t *list_w, const WsHeader *h,
@@ -294,57 +403,131 @@ __global__ __launch_bounds__(kZetaThreads) void k_weights_tile(
 
 // Dense route for long chunk lists (the tile kernel scans the whole list
 // once per tile, tiles x entries in all): f(S) = the weight of the chunks
-// with S_x = S, scattered into W, then the superset zeta
-// W(S) = sum_{T superset of S} f(T) in place -- the 13 low bits inside LDS
-// tiles, the high bits two at a time in global passes.
+// with S_x = S, scattered into a zeroed W, then the superset zeta
+// W(S) = sum_{T superset of S} f(T) in place, in read-write passes of up to
+// 11 bits (low bits) and 5 bits (the others) that keep every subset a
+// thread touches in registers: at m = 25, the zeroing plus four passes.
 __global__ void k_dense_zero(int64_t n, int64_t *W) {
     for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
         W[i] = 0;
 }
 
-__global__ void k_dense_scatter(uint32_t cap, const uint32_t *list_sig, const int64_t *list_w, const WsHeader *h,
-                                int64_t *W) {
-    const uint32_t cnt = min(h->n_list, cap);
-    for (uint32_t j = blockIdx.x * blockDim.x + threadIdx.x; j < cnt; j += gridDim.x * blockDim.x)
-        atomicAdd((unsigned long long *)&W[list_sig[j]], (unsigned long long)list_w[j]);
+// The scatter adds each workgroup's slice of the list into an LDS hash table
+// first: demand sets repeat (chunks held by the same few requests share
+// S_x), and device-wide atomics on one address serialize, so each distinct
+// set of a slice costs one global atomic. Entries that find no slot within
+// the probe limit go to W directly. Integer sums: the result does not depend
+// on the order.
+constexpr int kScatterThreads = 1024;
+constexpr int kScatterSlice = 8192;          // list entries per workgroup pass
+constexpr int kHashBits = 13;
+constexpr int kHashSlots = 1 << kHashBits;
+constexpr int kHashProbes = 16;
+
+__global__ __launch_bounds__(kScatterThreads) void k_dense_scatter(uint32_t cap, const uint32_t *list_sig,
+                                                                    const int64_t *list_w, const WsHeader *h,
+                                                                    int64_t *W) {
+    __shared__ uint32_t key[kHashSlots];              // 0 = empty (no listed chunk has S_x = 0)
+    __shared__ unsigned long long sum[kHashSlots];
+    const uint64_t cnt = min(h->n_list, cap);
+    for (uint64_t lo = (uint64_t)blockIdx.x * kScatterSlice; lo < cnt; lo += (uint64_t)gridDim.x * kScatterSlice) {
+        for (int i = threadIdx.x; i < kHashSlots; i += kScatterThreads) { key[i] = 0u; sum[i] = 0ull; }
+        __syncthreads();
+        const uint64_t hi = min(cnt, lo + kScatterSlice);
+        for (uint64_t j = lo + threadIdx.x; j < hi; j += kScatterThreads) {
+            const uint32_t sx = list_sig[j];
+            const unsigned long long wx = (unsigned long long)list_w[j];
+            uint32_t slot = (sx * 2654435761u) >> (32 - kHashBits);
+            bool done = false;
+            for (int p = 0; p < kHashProbes && !done; ++p) {
+                const uint32_t k = atomicCAS(&key[slot], 0u, sx);
+                if (k == 0u || k == sx) {
+                    atomicAdd(&sum[slot], wx);
+                    done = true;
+                }
+                slot = (slot + 1u) & (kHashSlots - 1u);
+            }
+            if (!done) atomicAdd((unsigned long long *)&W[sx], wx);
+        }
+        __syncthreads();
+        for (int i = threadIdx.x; i < kHashSlots; i += kScatterThreads)
+            if (key[i]) atomicAdd((unsigned long long *)&W[key[i]], sum[i]);
+        __syncthreads();
+    }
     if (blockIdx.x == 0 && threadIdx.x == 0)
         atomicAdd((unsigned long long *)&W[0], (unsigned long long)h->zero_weight);
 }
 
-// superset zeta over the low min(m, 13) bits of one tile
-__global__ __launch_bounds__(kZetaThreads) void k_dense_zeta_low(int m, int64_t *W) {
-    __shared__ int64_t tile[kZetaN + kZetaN / 8];
-    const int b = m < kZetaBits ? m : kZetaBits;
-    const int n = 1 << b;
-    int64_t *base = W + ((int64_t)blockIdx.x << kZetaBits);
-    for (int e = threadIdx.x; e < n; e += kZetaThreads) tile[zpos(e)] = base[e];
-    __syncthreads();
-    for (int j = 0; j < b; ++j) {
-        for (int p = threadIdx.x; p < n / 2; p += kZetaThreads) {
-            const int lo = ((p >> j) << (j + 1)) | (p & ((1 << j) - 1));   // bit j clear
-            tile[zpos(lo)] += tile[zpos(lo | (1 << j))];
-        }
-        __syncthreads();
-    }
-    for (int e = threadIdx.x; e < n; e += kZetaThreads) base[e] = tile[zpos(e)];
+// superset zeta over 2^K values in registers: v[r] += v[r | 2^b], bit by bit
+template <int K>
+__device__ inline void zeta_reg_bits(int64_t (&v)[1 << K]) {
+#pragma unroll
+    for (int b = 0; b < K; ++b)
+#pragma unroll
+        for (int r = 0; r < (1 << K); ++r)
+            if (!(r & (1 << b))) v[r] += v[r | (1 << b)];
 }
 
-// superset zeta over bit j (and j + 1 when two is set): every thread owns
-// the subsets that differ only in those bits
-__global__ void k_dense_zeta_high(int m, int j, int two, int64_t *W) {
-    const int64_t groups = (int64_t)1 << (m - 1 - two);
-    for (int64_t g = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; g < groups; g += (int64_t)gridDim.x * blockDim.x) {
-        const int64_t s = ((g >> j) << (j + 1 + two)) | (g & (((int64_t)1 << j) - 1));
-        const int64_t b1 = (int64_t)1 << j;
-        if (two) {
-            const int64_t b2 = b1 << 1;
-            const int64_t d = W[s | b1 | b2], c = W[s | b2] + d, bb = W[s | b1] + d;
-            W[s] += bb + c - d;                  // f(s) + f(s|b1) + f(s|b2) + f(s|b1|b2) sums
-            W[s | b1] = bb;
-            W[s | b2] = c;
-        } else {
-            W[s] += W[s | b1];
+// the low min(m, 11) bits: a wave owns 2^11 consecutive subsets, lane l
+// holds subsets l + 64 r (r < 32), so every load and store is 64
+// consecutive values; bits 6..10 are register bits, bits 0..5 lane bits
+// (lane l adds lane l + 2^b when its bit b is clear). Subsets past 2^m read
+// as 0 and are not stored: adding them changes nothing.
+constexpr int kLaneRegBits = 5;
+constexpr int kLowPassBits = 6 + kLaneRegBits;
+constexpr int kDenseThreads = 256;
+__global__ __launch_bounds__(kDenseThreads) void k_dense_zeta_low(int64_t n, int64_t *W) {
+    constexpr int R = 1 << kLaneRegBits;
+    const int lane = (int)(threadIdx.x & (kWave - 1));
+    const int64_t base = ((blockIdx.x * (int64_t)kDenseThreads + threadIdx.x) >> 6) << kLowPassBits;
+    if (base >= n) return;                            // whole waves
+    int64_t v[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const int64_t i = base + lane + ((int64_t)r << 6);
+        v[r] = i < n ? W[i] : 0;
+    }
+    zeta_reg_bits<kLaneRegBits>(v);
+#pragma unroll
+    for (int b = 0; b < 6; ++b) {
+        const bool add = !(lane & (1 << b));
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const int64_t up = __shfl_down(v[r], 1u << b, kWave);
+            if (add) v[r] += up;
         }
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const int64_t i = base + lane + ((int64_t)r << 6);
+        if (i < n) W[i] = v[r];
+    }
+}
+
+// bits j .. j + K - 1 (j >= 11, j + K <= m): a thread owns the 2^K subsets
+// that differ only in those bits; consecutive threads take consecutive low
+// subsets, so each of its loads and stores is coalesced across the wave
+template <int K>
+__global__ __launch_bounds__(kDenseThreads) void k_dense_zeta_high(int m, int j, int64_t *W) {
+    const int64_t g = blockIdx.x * (int64_t)kDenseThreads + threadIdx.x;
+    if (g >= ((int64_t)1 << (m - K))) return;
+    const int64_t s = ((g >> j) << (j + K)) | (g & (((int64_t)1 << j) - 1));
+    int64_t v[1 << K];
+#pragma unroll
+    for (int r = 0; r < (1 << K); ++r) v[r] = W[s + ((int64_t)r << j)];
+    zeta_reg_bits<K>(v);
+#pragma unroll
+    for (int r = 0; r + 1 < (1 << K); ++r) W[s + ((int64_t)r << j)] = v[r];   // the full-set value is unchanged
+}
+
+void dense_zeta_high(int m, int j, int K, int64_t *W, hipStream_t s) {
+    const uint32_t blocks = (uint32_t)((((int64_t)1 << (m - K)) + kDenseThreads - 1) / kDenseThreads);
+    switch (K) {
+    case 1: k_dense_zeta_high<1><<<blocks, kDenseThreads, 0, s>>>(m, j, W); break;
+    case 2: k_dense_zeta_high<2><<<blocks, kDenseThreads, 0, s>>>(m, j, W); break;
+    case 3: k_dense_zeta_high<3><<<blocks, kDenseThreads, 0, s>>>(m, j, W); break;
+    case 4: k_dense_zeta_high<4><<<blocks, kDenseThreads, 0, s>>>(m, j, W); break;
+    default: k_dense_zeta_high<5><<<blocks, kDenseThreads, 0, s>>>(m, j, W); break;
     }
 }
 
@@ -1883,6 +2066,7 @@ size_t rb_partial_entries(int m, int64_t chunk_pairs) {
 
 struct WsLayout {
     size_t list_sig, list_w, part_v, part_a, keys, rb_part, rb_tagged, rb_plain, rb_wrow, rb_srow;
+    size_t compact_count, compact_zero, compact_off;
     size_t build_end, extract_end;   // bytes the build and the extraction use
     size_t total;                    // bytes every phase fits in
 };
@@ -1904,6 +2088,11 @@ WsLayout ws_layout(int m, int64_t nnz, int64_t chunk_pairs) {
     L.list_sig = off;
     L.list_w = off + align256(nz * 4);
     size_t build_end = L.list_w + align256(nz * 8);
+    // the compaction's per-block counts, unrequested weights and offsets
+    L.compact_count = build_end;
+    L.compact_zero = L.compact_count + align256((size_t)kCompactMaxBlocks * 4);
+    L.compact_off = L.compact_zero + align256((size_t)kCompactMaxBlocks * 8);
+    build_end = L.compact_off + align256((size_t)kCompactMaxBlocks * 4);
     L.part_v = off;
     L.part_a = off + align256(P * 8);
     size_t dp_end = L.part_a + align256(P * 4);
@@ -2062,7 +2251,7 @@ size_t workspace_bytes(int m, int64_t nnz, int64_t chunk_pairs) {
 
 int build(int m, int64_t n_chunks, int64_t nnz, const int64_t *chunk_w, const int64_t *req_off,
           const int32_t *req_chunks, uint32_t *sig, int64_t *W, void *workspace, size_t workspace_bytes,
-          hipStream_t s, int64_t *total) {
+          hipStream_t s, int64_t *total, int route) {
     mptlib::Range range("mpt build_weights");
     int rc = check_common(m, n_chunks, nnz);
     if (rc) return rc;
@@ -2090,26 +2279,32 @@ int build(int m, int64_t n_chunks, int64_t nnz, const int64_t *chunk_w, const in
         }
         {
             LaunchScope ls("compact", (double)n_chunks, s);
-            k_compact<<<grid_for(n_chunks, 256), 256, 0, s>>>(n_chunks, std::max<int64_t>(nnz, 1), chunk_w, sig,
-                                                              list_sig, list_w, h);
+            const CompactPlan cp = compact_plan(n_chunks);
+            uint32_t *bcount = (uint32_t *)(ws + L.compact_count), *boff = (uint32_t *)(ws + L.compact_off);
+            int64_t *bzero = (int64_t *)(ws + L.compact_zero);
+            k_compact_count<<<cp.blocks, kCompactThreads, 0, s>>>(n_chunks, cp.per, chunk_w, sig, bcount, bzero, h);
+            k_compact_scan<<<1, kScanThreads, 0, s>>>(cp.blocks, bcount, bzero, boff, h);
+            k_compact_write<<<cp.blocks, kCompactThreads, 0, s>>>(n_chunks, cp.per, std::max<int64_t>(nnz, 1), chunk_w,
+                                                                 sig, boff, list_sig, list_w, h);
         }
     }
     const uint32_t tiles = m > kZetaBits ? 1u << (m - kZetaBits) : 1u;
-    if ((double)tiles * (double)nnz <= kDenseAbove) {
+    const bool dense = route == MPT_ROUTE_DENSE || (route == MPT_ROUTE_AUTO && dense_route_pays(m, nnz));
+    if (!dense) {
         LaunchScope ls("weights_tile", 8.0 * (double)(1ull << m), s);
         k_weights_tile<<<std::min(tiles, 1024u), kZetaThreads, 0, s>>>(m, (uint32_t)std::max<int64_t>(nnz, 1), tiles,
                                                                       list_sig, list_w, h, W);
     } else {
-        // long list: scatter + zeta over the dense table
+        // long list: scatter into a zeroed table, then the zeta passes
         const int64_t n = (int64_t)1 << m;
+        const uint32_t cap = (uint32_t)std::max<int64_t>(nnz, 1);
         LaunchScope ls("weights_dense", 8.0 * (double)n, s);
         k_dense_zero<<<grid_for(n, 256, 16384), 256, 0, s>>>(n, W);
-        k_dense_scatter<<<grid_for(nnz, 256), 256, 0, s>>>((uint32_t)std::max<int64_t>(nnz, 1), list_sig, list_w, h, W);
-        k_dense_zeta_low<<<tiles, kZetaThreads, 0, s>>>(m, W);
-        for (int j = kZetaBits; j < m; j += 2) {
-            const int two = j + 1 < m ? 1 : 0;
-            k_dense_zeta_high<<<grid_for(n >> (1 + two), 256, 16384), 256, 0, s>>>(m, j, two, W);
-        }
+        k_dense_scatter<<<(uint32_t)std::min<int64_t>((cap + kScatterSlice - 1) / kScatterSlice, 1024),
+                          kScatterThreads, 0, s>>>(cap, list_sig, list_w, h, W);
+        const int64_t waves = (n + (1 << kLowPassBits) - 1) >> kLowPassBits;
+        k_dense_zeta_low<<<(uint32_t)((waves * kWave + kDenseThreads - 1) / kDenseThreads), kDenseThreads, 0, s>>>(n, W);
+        for (int j = kLowPassBits; j < m; j += kLaneRegBits) dense_zeta_high(m, j, std::min(kLaneRegBits, m - j), W, s);
     }
     k_check_total<<<1, 64, 0, s>>>(m, W, h);
     MPT_HIP_TRY(hipGetLastError());
@@ -2262,7 +2457,7 @@ extern "C" int mpt_build_weights(int m, int64_t n_chunks, int64_t nnz, const int
     mptlib::clear_error();
     return mptlib::guarded(__func__, [&]() -> int {
         return mptcore::build(m, n_chunks, nnz, chunk_w, req_off, req_chunks, sig, W, workspace, workspace_bytes,
-                              (hipStream_t)stream, nullptr);
+                              (hipStream_t)stream, nullptr, MPT_ROUTE_AUTO);
     });
 }
 

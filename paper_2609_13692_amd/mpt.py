@@ -25,6 +25,8 @@ MPT_ORDER_ID = 0
 MPT_ORDER_POPULARITY = 1
 MPT_TABLE_W, MPT_TABLE_SIG, MPT_TABLE_C, MPT_TABLE_SPLIT, MPT_TABLE_ORDERS = 0, 1, 2, 3, 4
 MPT_OPT_CHUNK_PAIRS = 1
+MPT_OPT_WEIGHT_ROUTE = 2
+MPT_ROUTE_AUTO, MPT_ROUTE_LIST, MPT_ROUTE_DENSE = 0, 1, 2
 MPT_NOALLOC_MAX_M = 20
 
 _STATUS = {

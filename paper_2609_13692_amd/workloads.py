@@ -235,6 +235,18 @@ TRACE_CONFIGS = {
 }
 
 
+def gen_long_lists(m: int = 25, u: int = 1 << 20, k: int = 90000, wmax: int = 999, seed: int = 12) -> Instance:
+    """Long requests over a large pool: each of the m requests holds k
+    distinct chunks drawn uniformly from u, weights U{1..wmax} drawn after
+    the sets. At the defaults most chunks are held by one to three requests
+    (the same few demand sets over and over) and the list of held chunks is
+    about 0.9 u long: the shape for which W is built by the dense route."""
+    rng = np.random.default_rng(seed)
+    sets = [rng.choice(u, size=k, replace=False).tolist() for _ in range(m)]
+    w = rng.integers(1, wmax + 1, size=u, dtype=np.int64)
+    return from_sets(sets, w, u, f"long_lists(m={m},u={u},k={k},seed={seed})")
+
+
 def trace_config(name: str, seed: int | None = None) -> Instance:
     c = dict(TRACE_CONFIGS[name])
     if seed is not None:

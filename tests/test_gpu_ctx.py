@@ -129,6 +129,60 @@ def test_wide_keys_do_not_depend_on_the_level_plan():
             assert digest(got["split"], "<u4") == g["split_sha256"], (scale, cp)
 
 
+def routed_W(inst, route):
+    ctx = mpt.Context("cuda")
+    ctx.set_option(mpt.MPT_OPT_WEIGHT_ROUTE, route)
+    w, off, ch = tensors(inst, "cuda")
+    ctx.reserve(inst.m, inst.n_chunks, inst.nnz)
+    ctx.build_weights(inst.m, inst.n_chunks, w, off, ch)
+    W = ctx.copy_table(mpt.MPT_TABLE_W)
+    ctx.close()
+    return W
+
+
+# m below the 11-bit low pass, at it, one past it, and the high passes of
+# 1 .. 5 bits (the last pass is m - 11 mod 5 bits wide)
+ROUTE_MS = [1, 4, 10, 11, 12, 13, 14, 15, 16, 17, 21, 22]
+
+
+@pytest.mark.parametrize("m", ROUTE_MS)
+def test_both_weight_routes_give_the_oracle_table(m):
+    """The list route and the dense route (scatter, then the zeta passes)
+    on the same instances: requests of random sizes, chunks of random
+    weights, some chunks held by no request, and a slice of chunks held by
+    every request (S_x = all requests)."""
+    rng = np.random.default_rng(100 + m)
+    u = int(rng.integers(50, 4000))
+    sets = []
+    for i in range(m):
+        k = int(rng.integers(0, u // 2 + 1))
+        sets.append(sorted(set(rng.choice(u, size=k, replace=False).tolist()) | {0, 1}))
+    w = rng.integers(1, 1 << 20, size=u + 7, dtype=np.int64)
+    inst = wl.from_sets(sets, w, u + 7, name=f"routes m={m}")
+    say(f"[gpu ctx] weight routes m={m} u={inst.n_chunks} nnz={inst.nnz}")
+    ref = oracle.intersection_weights(inst)
+    for route in (mpt.MPT_ROUTE_LIST, mpt.MPT_ROUTE_DENSE):
+        assert np.array_equal(routed_W(inst, route), ref), route
+
+
+def test_dense_route_with_repeated_demand_sets():
+    """Many chunks with the same few S_x (hash slots shared within a
+    workgroup) after a first stretch of chunks with nearly all-distinct S_x:
+    the list keeps chunk order, so those slices fill the LDS table past its
+    probe limit and the overflow goes to W directly."""
+    rng = np.random.default_rng(7)
+    m, u = 18, 300000
+    # the first 40% of chunks in 3 .. m random requests, the others in 1 or 2
+    k = np.where(np.arange(u) < 2 * u // 5, rng.integers(3, m + 1, size=u), rng.integers(1, 3, size=u))
+    rank = rng.random((u, m)).argsort(1).argsort(1)
+    held = rank < k[:, None]
+    memb = [np.nonzero(held[:, i])[0].tolist() for i in range(m)]
+    w = rng.integers(1, 1000, size=u, dtype=np.int64)
+    inst = wl.from_sets(memb, w, u, name="repeated demand sets")
+    say(f"[gpu ctx] dense route, repeated sets m={m} nnz={inst.nnz}")
+    assert np.array_equal(routed_W(inst, mpt.MPT_ROUTE_DENSE), oracle.intersection_weights(inst))
+
+
 def test_state_machine():
     """created -> built -> solved -> extracted, MPT_E_STATE out of order; a
     new build, a failed build, a new workspace or an option reset it."""
@@ -173,6 +227,8 @@ def test_state_machine():
     ctx.set_option(mpt.MPT_OPT_CHUNK_PAIRS, 2)
     expect("MPT_E_STATE", ctx.solve_exact)
     expect("MPT_E_INVALID", ctx.set_option, 99, 1)
+    expect("MPT_E_INVALID", ctx.set_option, mpt.MPT_OPT_WEIGHT_ROUTE, 3)
+    expect("MPT_E_INVALID", ctx.set_option, mpt.MPT_OPT_CHUNK_PAIRS, -1)
     expect("MPT_E_INVALID", ctx.copy_table, 17)
     # table_device gives the table's address inside the workspace
     ctx.build_weights(inst.m, inst.n_chunks, w, off, ch)

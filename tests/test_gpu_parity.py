@@ -478,14 +478,10 @@ def test_errors_are_reported(case):
 
 
 def test_weight_table_dense_route_for_long_lists():
-    """25 requests of 90000 chunks over 2^20: 4096 tiles x 2.25M slots is
+    """25 requests of 90000 chunks over 2^20: 8192 tiles x 2.25M slots is
     past the tile kernel's list scan, so W is built by scatter plus a dense
     superset zeta; it must equal the oracle's table."""
-    rng = np.random.default_rng(12)
-    u = 1 << 20
-    sets = [rng.choice(u, size=90000, replace=False).tolist() for _ in range(25)]
-    w = rng.integers(1, 1000, size=u, dtype=np.int64)
-    inst = wl.from_sets(sets, w, u)
+    inst = wl.gen_long_lists()
     say(f"[gpu] dense W route m={inst.m} nnz={inst.nnz}")
     prob = mpt.Problem(inst)
     mpt.profile_begin()
