@@ -271,7 +271,8 @@ int mpt_table_device(const mpt_ctx *ctx, int which, const void **dev_ptr, size_t
  * These calls take any m in [1, MPT_GREEDY_MAX_M]; requests are identified
  * by index. Same conventions as above; they share one workspace of
  * mpt_greedy_workspace_bytes(m, n_chunks, nnz) bytes (about 8 m^2 + 44 nnz
- * + 8 n_chunks bytes). Instances are validated as for mpt_build_weights.
+ * + 8 n_chunks + 110 m bytes). Instances are validated as for
+ * mpt_build_weights.
  */
 #define MPT_GREEDY_MAX_M 16384
 
@@ -311,7 +312,10 @@ int mpt_pair_weights(int m, int64_t n_chunks, int64_t nnz, const int64_t *chunk_
  *                           pi_i at order_chunks[req_off[i] ..)
  *   savings                 HOST out, nullable: SAV(H_g) = sum of the gains;
  *                           the layout costs at most sum_i w(R_i) - SAV(H_g)
- * Synchronises `stream` before returning.
+ * The merges are found in parallel rounds (every mutually best pair of
+ * clusters at once) and put in the sequence above afterwards; the outputs
+ * are those of the one-merge-at-a-time procedure. Synchronises `stream`
+ * once per eight rounds and before returning.
  */
 int mpt_greedy_hierarchy(int m, int64_t n_chunks, int64_t nnz, const int64_t *chunk_w,
                          const int64_t *req_off, const int32_t *req_chunks,

@@ -12,12 +12,12 @@
 // families of retrieval shape have small |S_x|, so this touches
 // sum_x |S_x|^2 entries instead of a dense m x m x u contraction.
 //
-// The greedy's m-1 merges depend on each other, so one workgroup runs them
-// all. Per merge it reduces the per-row best pairs to the global one,
-// intersects the two signatures, scatters the new cluster's values through
-// the demand lists of its signature (an LDS accumulator), and rescans only
-// the rows whose best partner was one of the merged clusters (merge values
-// never grow, Theorem 6 part i, so no other row's best can change).
+// The greedy's merges run in rounds over the whole chip: every round merges
+// all pairs of clusters that are each other's best partner (merge values
+// never grow, Theorem 6 part i, so each such pair is one of the greedy's
+// merges), intersects their signatures, recomputes the new rows and only
+// the best partners that can have changed. A sort of the merges by the
+// lowest priority in their subtrees then gives the greedy's sequence.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -38,8 +38,6 @@ using mptlib::kSortTile;
 using mptlib::sort_keys;
 
 constexpr int kWave = 64;
-constexpr int kLoopThreads = 1024;           // the one workgroup of the merge loop
-constexpr int kLoopWaves = kLoopThreads / kWave;
 
 enum : uint32_t { GERR_INVALID = 1u, GERR_RANGE = 2u, GERR_DUP = 4u, GERR_WEIGHT = 8u, GERR_OVERFLOW = 16u };
 
@@ -48,7 +46,13 @@ struct GHeader {
     uint32_t err;
     uint32_t pad0;
     unsigned long long total;    // sum_i w(R_i), unsigned so it cannot wrap before the check
-    int64_t pad[30];
+    int32_t n_rec;               // merge records so far
+    int32_t lo;                  // first record of the current round
+    int32_t n_resc[2];           // rows marked for a rescan, by round parity
+    int32_t last_pairs;          // merges of the last finished round
+    int32_t pad1;
+    unsigned long long dcursor;  // next free slot of the packed D lists
+    int64_t pad[26];
 };
 static_assert(sizeof(GHeader) == 256, "header is one 256-byte block");
 
@@ -59,10 +63,12 @@ inline int64_t pow2_at_least(int64_t n) {
 }
 
 struct GLayout {
-    size_t keys1, keys2, sig, sig_len, dem, dem_off, V, best_v, best_p, active, node_of, dbuf, d_off, d_len,
-        key, total;
+    size_t keys1, keys2, sig, sig_len, dem, dem_off, V, best_v, best_p, active, last, touched, resc, dbuf, d_off,
+        d_len, rec32, rec64, total;
     int64_t npad;
 };
+constexpr int kRec32 = 7;    // int32 arrays of the merge records
+constexpr int kRec64 = 3;    // int64 arrays of the merge records
 
 GLayout g_layout(int m, int64_t n_chunks, int64_t nnz) {
     GLayout L{};
@@ -80,11 +86,14 @@ GLayout g_layout(int m, int64_t n_chunks, int64_t nnz) {
     L.best_v = take(8 * mm);
     L.best_p = take(4 * mm);
     L.active = take(4 * mm);
-    L.node_of = take(4 * mm);
+    L.last = take(4 * mm);
+    L.touched = take(4 * mm);
+    L.resc = take(4 * mm);
     L.dbuf = take(4 * (size_t)std::max<int64_t>(nnz, 1));
     L.d_off = take(8 * (2 * mm));
     L.d_len = take(4 * (2 * mm));
-    L.key = take(4 * mm);       // signature starts (int32) when they do not fit on chip
+    L.rec32 = take(4 * mm * kRec32);
+    L.rec64 = take(8 * mm * kRec64);
     L.total = o;
     return L;
 }
@@ -105,20 +114,6 @@ __device__ inline void wave_best(int64_t &v, int32_t &i) {
         if (better(ov, oi, v, i)) { v = ov; i = oi; }
     }
 }
-
-// best (value, index) over the workgroup, every thread gets the result. No
-// closing barrier: the scratch (sv, si) must not be written again before
-// some other barrier of the workgroup.
-__device__ inline void block_best_once(int64_t &v, int32_t &i, int64_t *sv, int32_t *si) {
-    wave_best(v, i);
-    const int lane = threadIdx.x & (kWave - 1), wid = threadIdx.x / kWave;
-    if (lane == 0) { sv[wid] = v; si[wid] = i; }
-    __syncthreads();
-    v = sv[0]; i = si[0];
-    for (int k = 1; k < (int)(blockDim.x / kWave); ++k)
-        if (better(sv[k], si[k], v, i)) { v = sv[k]; i = si[k]; }
-}
-
 
 // exclusive prefix sum of one int per thread over the workgroup; returns
 // the thread's offset, *total gets the sum
@@ -267,17 +262,36 @@ __global__ void k_g_row_best(int m, const int64_t *V, int64_t *best_v, int32_t *
     if (lane == 0) { best_v[row] = v; best_p[row] = p; }
 }
 
-struct LoopArgs {
+// The greedy's merges in rounds. Merge values never grow (Theorem 6 part
+// i): a cluster formed from A and B shares with any C at most what A and B
+// each share with C. Order pairs by (value desc, smaller name asc, larger
+// name asc), where a cluster's name is its smallest request; the sequential
+// greedy merges the first pair in this order every time. A pair (a, b) in
+// which each is the other's best partner stays so under every other merge,
+// so the sequential greedy merges it at some point: every round merges all
+// such mutual-best pairs of positive value at once (the first pair overall
+// is always one), until no positive value is left. The rounds produce the
+// greedy's merges, not its sequence; the sequence is the pair order itself.
+// A merge X that forms a cluster taking part in a later merge Y of names
+// p < q comes first: X's value is at least Y's, and if equal, the parts
+// named p and q already shared that value when X was chosen (their
+// signatures contain those of Y's clusters), so X's pair preceded (p, q).
+struct Rac {
     int m;
     const int64_t *w;
-    const int64_t *req_off;     // start of cluster a's signature
+    const int64_t *req_off;     // start of each cluster's signature in sig
     int32_t *sig;               // signatures, ascending, shrinking in place
     int32_t *sig_len;
-    int32_t *sig_at;            // req_off as int32 (workspace copy, used when m > kMetaCap)
     int64_t *V;                 // V[a][c] = w(I(a) ∩ I(c)) for live a, c
     int64_t *best_v;
     int32_t *best_p;
-    int32_t *node_of;           // tree node of live cluster a
+    int32_t *act;               // 1 while the name is a live cluster
+    int32_t *last;              // last merge record into each name (-1: a leaf)
+    int32_t *touched;           // round in which the name last merged
+    int32_t *resc;              // rows whose best partner is recomputed this round
+    // merge records, in the order the rounds produce them
+    int32_t *ra, *rb, *rca, *rcb, *rpos, *rdal, *rdbl;
+    int64_t *rgain, *rdao, *rdbo;
     int32_t *dbuf;              // D(v) = I(v) \ I(parent(v)), packed
     int64_t dcap;               // entries of dbuf (nnz: the D lists never need more)
     int64_t *d_off;
@@ -288,362 +302,293 @@ struct LoopArgs {
     GHeader *h;
 };
 
-// The columns of the candidate pass and of the new row are owned by the
-// waves other than wave 0, which intersects the signatures meanwhile.
-constexpr int kColThreads = kLoopThreads - kWave;
-constexpr int kColsPerThread = (MPT_GREEDY_MAX_M + kColThreads - 1) / kColThreads;
-static_assert(kColsPerThread <= 32, "the column flags of a thread fit 32 bits");
-constexpr int kScCap = 2048;                                        // I(C) kept in LDS up to this size
-constexpr int kSigCap = 1024;                                       // I(A), I(B) copied to LDS up to this size
-constexpr int kMetaCap = 4096;                                      // per-cluster state in LDS up to this m
-constexpr int kCandCap = 2048;                                      // candidate columns listed in LDS per merge
-constexpr int kRescParts = 4;                                       // waves per rescanned row
-constexpr int kRescRows = kLoopWaves / kRescParts;                  // rows rescanned together
-
 __device__ inline uint64_t lanes_below(int lane) { return (1ull << lane) - 1ull; }
 
-// w(I(C) ∩ list) for an ascending list: I(C) and the weights of its
-// chunks in LDS; the list is read 8 entries at a time so that its loads
-// overlap
-__device__ inline int64_t inter_weight_lds(const int32_t *ic, const int64_t *icw, int64_t n_ic, const int32_t *list,
-                                           int64_t n) {
+// w(p ∩ q) for ascending lists: the shorter searched in the longer
+__device__ inline int64_t inter_weight(const int32_t *p, int64_t np, const int32_t *q, int64_t nq, const int64_t *w) {
+    if (np > nq) { const int32_t *t = p; p = q; q = t; const int64_t n = np; np = nq; nq = n; }
     int64_t s = 0;
+    for (int64_t j = 0; j < np; ++j) {
+        const int32_t y = p[j];
+        if (find_sorted(q, nq, y) >= 0) s += w[y];
+    }
+    return s;
+}
+
+// pair order (gain, a, b): true when x comes after y in the greedy's order
+// (smaller gain; equal gains, larger names)
+__device__ inline bool after(int64_t xg, int32_t xa, int32_t xb, int64_t yg, int32_t ya, int32_t yb) {
+    return xg < yg || (xg == yg && (xa > ya || (xa == ya && xb > yb)));
+}
+
+__global__ void k_rac_init(Rac R) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    const int64_t t0 = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    for (int64_t r = t0; r < R.m; r += stride) { R.act[r] = 1; R.last[r] = -1; R.touched[r] = -1; R.rpos[r] = 0; }
+    for (int64_t v = t0; v < 2 * (int64_t)R.m - 1; v += stride) { R.node_parent[v] = -1; R.d_off[v] = 0; R.d_len[v] = 0; }
+    if (t0 == 0) {
+        R.h->n_rec = 0;
+        R.h->lo = 0;
+        R.h->n_resc[0] = 0;
+        R.h->n_resc[1] = 0;
+        R.h->last_pairs = -1;
+        R.h->dcursor = 0;
+    }
+}
+
+// mutual-best pairs of positive value
+__global__ void k_rac_pairs(Rac R) {
+    for (int a = blockIdx.x * blockDim.x + threadIdx.x; a < R.m; a += gridDim.x * blockDim.x) {
+        if (!R.act[a] || R.best_v[a] <= 0) continue;
+        const int32_t b = R.best_p[a];
+        if (b <= a || R.best_p[b] != a) continue;
+        const int i = atomicAdd(&R.h->n_rec, 1);
+        if (i >= R.m - 1) { atomicOr(&R.h->err, GERR_INVALID); continue; }   // cannot happen
+        R.ra[i] = a;
+        R.rb[i] = b;
+        R.rgain[i] = R.best_v[a];
+    }
+}
+
+// one wave per merge of the round: I(C) = I(A) ∩ I(B) in place of I(A),
+// D(B) = I(B) \ I(A) and D(A) = I(A) \ I(B) to the packed lists, and the
+// merges that formed A and B
+__global__ void k_rac_merge(Rac R, int round) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int lo = R.h->lo, hi = min(R.h->n_rec, R.m - 1);
+    const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) / kWave;
+    for (int64_t i = lo + (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) / kWave; i < hi; i += nwaves) {
+        const int32_t a = R.ra[i], b = R.rb[i];
+        int32_t *sa = R.sig + R.req_off[a];
+        const int32_t *sb = R.sig + R.req_off[b];
+        const int64_t na = R.sig_len[a], nb = R.sig_len[b];
+        int64_t kept = 0;
+        for (int64_t base = 0; base < na; base += kWave) {
+            const int64_t e = base + lane;
+            kept += __popcll(__ballot(e < na && find_sorted(sb, nb, sa[e]) >= 0));
+        }
+        const int64_t dlen = na + nb - 2 * kept;
+        unsigned long long dstart = 0;
+        if (lane == 0) dstart = atomicAdd(&R.h->dcursor, (unsigned long long)dlen);
+        dstart = __shfl(dstart, 0, kWave);
+        if ((int64_t)dstart + dlen > R.dcap) {   // cannot happen for a valid run
+            if (lane == 0) atomicOr(&R.h->err, GERR_INVALID);
+            continue;
+        }
+        int64_t dcur = (int64_t)dstart;
+        for (int64_t base = 0; base < nb; base += kWave) {
+            const int64_t e = base + lane;
+            int32_t x = 0;
+            bool keep = false;
+            if (e < nb) { x = sb[e]; keep = find_sorted(sa, na, x) < 0; }
+            const uint64_t mk = __ballot(keep);
+            if (keep) R.dbuf[dcur + __popcll(mk & lanes_below(lane))] = x;
+            dcur += __popcll(mk);
+        }
+        const int64_t d_a_at = dcur;
+        // in place: a lane writes at or below the entry it read, and the
+        // entries above the current 64 are not written yet
+        int64_t k = 0;
+        for (int64_t base = 0; base < na; base += kWave) {
+            const int64_t e = base + lane;
+            int32_t x = 0;
+            bool in_b = false;
+            if (e < na) { x = sa[e]; in_b = find_sorted(sb, nb, x) >= 0; }
+            const uint64_t mi = __ballot(in_b);
+            const uint64_t mo = __ballot(e < na && !in_b);
+            if (in_b) sa[k + __popcll(mi & lanes_below(lane))] = x;
+            else if (e < na) R.dbuf[dcur + __popcll(mo & lanes_below(lane))] = x;
+            k += __popcll(mi);
+            dcur += __popcll(mo);
+        }
+        if (lane == 0) {
+            R.sig_len[a] = (int32_t)kept;
+            R.act[b] = 0;
+            R.touched[a] = round;
+            R.touched[b] = round;
+            const int32_t ca = R.last[a], cb = R.last[b];
+            R.rca[i] = ca;
+            R.rcb[i] = cb;
+            R.last[a] = (int32_t)i;
+            R.rdbo[i] = (int64_t)dstart;
+            R.rdbl[i] = (int32_t)(d_a_at - (int64_t)dstart);
+            R.rdao[i] = d_a_at;
+            R.rdal[i] = (int32_t)(dcur - d_a_at);
+        }
+    }
+}
+
+// the new clusters' rows against every live column. A value is positive
+// only where both old values are; the row of a is written by its own merge
+// (columns of clusters merged in the same round included: both sides
+// compute the same value), the column entry of every other row here.
+// The same launch marks the rows whose best partner may have changed: the
+// new clusters and the rows whose best partner merged (no other row's best
+// can change: values fall).
+__global__ void k_rac_rows(Rac R, int round) {
+    const int lo = R.h->lo, hi = min(R.h->n_rec, R.m - 1);
+    const int64_t m = R.m;
+    const int64_t total = (int64_t)(hi - lo) * m;
+    const int64_t t0 = blockIdx.x * (int64_t)blockDim.x + threadIdx.x, stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t f = t0; f < total; f += stride) {
+        const int64_t i = lo + f / m;
+        const int32_t x = (int32_t)(f % m);
+        const int32_t a = R.ra[i], b = R.rb[i];
+        if (x == a || !R.act[x]) continue;
+        const int64_t va = R.V[a * m + x], vb = R.V[b * m + x];
+        const int64_t kept = R.sig_len[a];
+        int64_t v = 0;
+        if (va > 0 && vb > 0 && kept > 0)
+            v = inter_weight(R.sig + R.req_off[a], kept, R.sig + R.req_off[x], R.sig_len[x], R.w);
+        if (v != va) {
+            R.V[a * m + x] = v;
+            if (R.touched[x] != round) R.V[(int64_t)x * m + a] = v;
+        }
+    }
+    if (hi <= lo) return;                        // nothing merged, nothing to rescan
+    for (int64_t x = t0; x < m; x += stride) {
+        if (!R.act[x]) continue;
+        const int32_t p = R.best_p[x];
+        if (R.touched[x] == round || (p >= 0 && R.touched[p] == round))
+            R.resc[atomicAdd(&R.h->n_resc[round & 1], 1)] = (int32_t)x;
+    }
+}
+
+// one workgroup per marked row: best partner, ties to the smallest index;
+// each thread loads 8 columns before comparing them. Block 0 also closes
+// the round: the next round's records start at the current count, and its
+// rescan counter starts at 0.
+constexpr int kRescThreads = 256;
+__global__ __launch_bounds__(kRescThreads) void k_rac_rescan(Rac R, int round) {
+    __shared__ int64_t sv[kRescThreads / kWave];
+    __shared__ int32_t si[kRescThreads / kWave];
+    const int n = R.h->n_resc[round & 1];
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        R.h->last_pairs = R.h->n_rec - R.h->lo;
+        R.h->lo = R.h->n_rec;
+        R.h->n_resc[(round + 1) & 1] = 0;
+    }
+    const int64_t m = R.m;
+    const int lane = threadIdx.x & (kWave - 1), wid = threadIdx.x / kWave;
     constexpr int U = 8;
-    for (int64_t j0 = 0; j0 < n; j0 += U) {
-        int32_t y[U];
+    for (int j = blockIdx.x; j < n; j += gridDim.x) {
+        const int32_t x = R.resc[j];
+        const int64_t *row = R.V + x * m;
+        int64_t v = -1;
+        int32_t p = -1;
+        for (int64_t d0 = threadIdx.x; d0 < m; d0 += (int64_t)kRescThreads * U) {
+            int64_t val[U];
+            int32_t live[U];
 #pragma unroll
-        for (int u = 0; u < U; ++u) y[u] = j0 + u < n ? list[j0 + u] : -1;
+            for (int u = 0; u < U; ++u) {
+                const int64_t d = d0 + (int64_t)u * kRescThreads;
+                val[u] = d < m ? row[d] : -1;
+                live[u] = d < m ? R.act[d] : 0;
+            }
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            if (y[u] < 0) continue;
-            const int64_t pos = find_sorted(ic, n_ic, y[u]);
-            if (pos >= 0) s += icw[pos];
+            for (int u = 0; u < U; ++u) {
+                const int32_t d = (int32_t)(d0 + (int64_t)u * kRescThreads);
+                if (live[u] && d != x && better(val[u], d, v, p)) { v = val[u]; p = d; }
+            }
         }
-    }
-    return s;
-}
-
-// the same with I(C) in global memory (too long for the LDS copy)
-__device__ inline int64_t inter_weight_global(const int32_t *ic, int64_t n_ic, const int32_t *list, int64_t n,
-                                              const int64_t *w) {
-    int64_t s = 0;
-    for (int64_t j = 0; j < n; ++j) {
-        const int32_t y = list[j];
-        if (find_sorted(ic, n_ic, y) >= 0) s += w[y];
-    }
-    return s;
-}
-
-// Each step: (1) the pair to merge from the threads' cached row bests;
-// (2) candidate columns c, where both V[a][c] and V[b][c] are positive (the
-// new value is at most their minimum), on waves 1 and up; (3) at the same
-// time wave 0 intersects the signatures: I(C) = I(A) ∩ I(B) in place and
-// in LDS, D(A), D(B) to the packed lists; (4) the new row and column of a,
-// from intersections at the candidates; (5) rows whose best partner was a
-// or b are rescanned.
-__global__ __launch_bounds__(kLoopThreads) void k_g_merge_loop(LoopArgs A) {
-    __shared__ uint8_t act[MPT_GREEDY_MAX_M];    // 1 while r names a live cluster
-    __shared__ int32_t sc[kScCap];               // I(C) of the current merge
-    __shared__ int64_t scw[kScCap];              // w(x) of the chunks of I(C)
-    __shared__ int32_t s_in[2 * kSigCap];        // I(A), I(B) while they are intersected
-    __shared__ uint8_t dirty[kLoopThreads];      // a row owned by this thread changed its best
-    // reduction scratch of steps (1) and (4): each is written again only
-    // after barriers of the other steps, so neither reduction needs a
-    // closing barrier
-    __shared__ int64_t red1_v[kLoopWaves], red4_v[kLoopWaves];
-    __shared__ int32_t red1_i[kLoopWaves], red4_i[kLoopWaves];
-    __shared__ int scan_w[kLoopWaves];
-    __shared__ int64_t cursor;                   // next free slot of dbuf
-    __shared__ int64_t s_kept;                   // |I(C)|
-    __shared__ int n_resc;
-    __shared__ int32_t resc[kLoopThreads];       // rows to rescan (overflow: rescan all)
-    __shared__ int resc_all;
-    __shared__ int64_t part_v[kRescRows][kRescParts];
-    __shared__ int32_t part_p[kRescRows][kRescParts];
-    __shared__ int32_t m_at[kMetaCap];           // signature start of each cluster (m <= kMetaCap)
-    __shared__ int32_t m_len[kMetaCap];          // signature length of each cluster (m <= kMetaCap)
-    __shared__ int64_t m_bv[kMetaCap];           // best value of each row (m <= kMetaCap)
-    __shared__ int32_t m_bp[kMetaCap];           // best partner of each row (m <= kMetaCap)
-    __shared__ int32_t cand_list[kCandCap];
-    __shared__ int n_cand;
-    const int m = A.m;
-    const int tid = threadIdx.x;
-    const int lane = tid & (kWave - 1), wid = tid / kWave;
-    // signature starts and lengths: on chip when they fit (generic pointers
-    // read either)
-    const bool meta_lds = m <= kMetaCap;
-    int32_t *sat = meta_lds ? m_at : A.sig_at;
-    int32_t *slen = meta_lds ? m_len : A.sig_len;
-    int64_t *best_v = meta_lds ? m_bv : A.best_v;
-    int32_t *best_p = meta_lds ? m_bp : A.best_p;
-    if (tid == 0) cursor = 0;
-    for (int v = tid; v < 2 * m - 1; v += blockDim.x) { A.node_parent[v] = -1; A.d_off[v] = 0; A.d_len[v] = 0; }
-    for (int r = tid; r < m; r += blockDim.x) {
-        A.node_of[r] = r;
-        act[r] = 1;
-        const int32_t at = (int32_t)A.req_off[r], len = (int32_t)(A.req_off[r + 1] - A.req_off[r]);
-        if (meta_lds) { m_at[r] = at; m_len[r] = len; m_bv[r] = A.best_v[r]; m_bp[r] = A.best_p[r]; }
-        else { A.sig_at[r] = at; }
-    }
-    dirty[tid] = 1;
-    if (tid == 0) n_cand = 0;
-    __syncthreads();
-    int64_t cv = -1;                             // best (value, row) over the rows this thread owns
-    int32_t ci = -1;
-    int t = 0;
-    for (; t + 1 < m; ++t) {
-        // (1) the best row value, ties to the smallest row; that row's best
-        // partner is larger than the row (a smaller partner would be a
-        // smaller row with the same value)
-        if (dirty[tid]) {
-            cv = -1; ci = -1;
-            for (int r = tid; r < m; r += blockDim.x)
-                if (act[r] && best_p[r] >= 0 && better(best_v[r], r, cv, ci)) { cv = best_v[r]; ci = r; }
-            dirty[tid] = 0;
-        }
-        int64_t g = cv;
-        int32_t a = ci;
-        block_best_once(g, a, red1_v, red1_i);
-        if (a < 0 || g <= 0) break;              // every remaining value is 0
-        const int32_t b = best_p[a];
-        // (2) candidate columns of this thread, and which old values of a
-        // are not zero (only changed entries are written back)
-        uint32_t cand = 0, nonzero = 0, flag = 0, listed = 0;
-        const int ct = tid - kWave;              // column owner index (wave 0 owns none)
-#pragma unroll 1
-        for (int k = 0; k < kColsPerThread && ct >= 0; ++k) {
-            const int c = ct + k * kColThreads;
-            if (c >= m) break;
-            if (!act[c] || c == a) continue;
-            const int64_t va = A.V[(size_t)a * m + c];
-            const int64_t vb = A.V[(size_t)b * m + c];
-            const int32_t p = best_p[c];
-            if (va != 0) nonzero |= 1u << k;
-            if (c != b && va > 0 && vb > 0) {
-                cand |= 1u << k;
-                const int i = atomicAdd(&n_cand, 1);       // cleared at the end of the previous step
-                if (i < kCandCap) { cand_list[i] = c; listed |= 1u << k; }
-            }
-            if (p == a || p == b) flag |= 1u << k;
-        }
-        // (3) signatures, by wave 0 alone
-        const int64_t na = slen[a], nb = slen[b];
-        const int64_t dstart = cursor;
-        if (dstart + na + nb > A.dcap) {         // cannot happen for a valid run: stop with an error
-            if (tid == 0) atomicOr(&A.h->err, GERR_INVALID);
-            return;
-        }
-        if (wid == 0) {
-            int32_t *sa = A.sig + sat[a];
-            const int32_t *sb_g = A.sig + sat[b];
-            // the two signatures in LDS when they fit (searches stay on chip)
-            const bool in_lds = na <= kSigCap && nb <= kSigCap;
-            const int32_t *sa_r = sa, *sb = sb_g;
-            if (in_lds) {
-                for (int64_t e = lane; e < na; e += kWave) s_in[e] = sa[e];
-                for (int64_t e = lane; e < nb; e += kWave) s_in[kSigCap + e] = sb_g[e];
-                sa_r = s_in;
-                sb = s_in + kSigCap;
-            }
-            int64_t dcur = dstart;
-            // D(B) = I(B) \ I(A)
-            for (int64_t base = 0; base < nb; base += kWave) {
-                const int64_t e = base + lane;
-                int32_t x = 0;
-                bool keep = false;
-                if (e < nb) { x = sb[e]; keep = find_sorted(sa_r, na, x) < 0; }
-                const uint64_t mk = __ballot(keep);
-                if (keep) A.dbuf[dcur + __popcll(mk & lanes_below(lane))] = x;
-                dcur += __popcll(mk);
-            }
-            const int64_t d_a_at = dcur;
-            // I(C) = I(A) ∩ I(B) over I(A) in place (and to LDS), D(A) = the rest
-            int64_t kept = 0;
-            for (int64_t base = 0; base < na; base += kWave) {
-                const int64_t e = base + lane;
-                int32_t x = 0;
-                bool in_b = false;
-                if (e < na) { x = sa_r[e]; in_b = find_sorted(sb, nb, x) >= 0; }
-                const uint64_t mi = __ballot(in_b);
-                const uint64_t mo = __ballot(e < na && !in_b);
-                if (in_b) {
-                    const int64_t pos = kept + __popcll(mi & lanes_below(lane));
-                    sa[pos] = x;
-                    if (pos < kScCap) { sc[pos] = x; scw[pos] = A.w[x]; }
-                } else if (e < na) {
-                    A.dbuf[dcur + __popcll(mo & lanes_below(lane))] = x;
-                }
-                kept += __popcll(mi);
-                dcur += __popcll(mo);
-            }
-            if (lane == 0) {
-                const int node_a = A.node_of[a], node_b = A.node_of[b], node_c = m + t;
-                A.merge_a[t] = a; A.merge_b[t] = b; A.gain[t] = g;
-                if (b <= a) atomicOr(&A.h->err, GERR_INVALID);
-                A.d_off[node_b] = dstart; A.d_len[node_b] = (int32_t)(d_a_at - dstart);
-                A.d_off[node_a] = d_a_at; A.d_len[node_a] = (int32_t)(dcur - d_a_at);
-                A.node_parent[node_a] = node_c;
-                A.node_parent[node_b] = node_c;
-                A.node_of[a] = node_c;
-                slen[a] = (int32_t)kept;
-                act[b] = 0;
-                dirty[b % kLoopThreads] = 1;
-                dirty[a % kLoopThreads] = 1;
-                cursor = dcur;
-                s_kept = kept;
-                n_resc = 0;
-                resc_all = 0;
-            }
+        wave_best(v, p);
+        if (lane == 0) { sv[wid] = v; si[wid] = p; }
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            for (int k = 1; k < kRescThreads / kWave; ++k)
+                if (better(sv[k], si[k], v, p)) { v = sv[k]; p = si[k]; }
+            R.best_v[x] = v;
+            R.best_p[x] = p;
         }
         __syncthreads();
-        // (4) the new values of a against every live c: the listed
-        // candidates are shared out evenly, every other column is 0 (or its
-        // owner computes it when the list overflowed)
-        const int64_t kept = s_kept;
-        const bool ic_lds = kept <= kScCap;
-        int64_t bv = -1;
-        int32_t bp = -1;
-        const int ncl = min(n_cand, kCandCap);
-        for (int i = tid; i < ncl; i += blockDim.x) {
-            const int c = cand_list[i];
-            int64_t v = 0;
-            if (kept > 0) {
-                const int32_t *list = A.sig + sat[c];
-                const int64_t n = slen[c];       // c != a: unchanged by this merge
-                v = ic_lds ? inter_weight_lds(sc, scw, kept, list, n)
-                           : inter_weight_global(A.sig + sat[a], kept, list, n, A.w);
-            }
-            A.V[(size_t)a * m + c] = v;
-            A.V[(size_t)c * m + a] = v;
-            if (better(v, c, bv, bp)) { bv = v; bp = c; }
-        }
-#pragma unroll 1
-        for (int k = 0; k < kColsPerThread && ct >= 0; ++k) {
-            const int c = ct + k * kColThreads;
-            if (c >= m) break;
-            if (!act[c] || c == a) continue;
-            if (!((listed >> k) & 1u)) {
-                const bool is_cand = kept > 0 && ((cand >> k) & 1u);
-                int64_t v = 0;
-                if (is_cand) {
-                    const int32_t *list = A.sig + sat[c];
-                    const int64_t n = slen[c];
-                    v = ic_lds ? inter_weight_lds(sc, scw, kept, list, n)
-                               : inter_weight_global(A.sig + sat[a], kept, list, n, A.w);
-                }
-                if (is_cand || ((nonzero >> k) & 1u)) {  // the old value may differ
-                    A.V[(size_t)a * m + c] = v;
-                    A.V[(size_t)c * m + a] = v;
-                }
-                if (better(v, c, bv, bp)) { bv = v; bp = c; }
-            }
-            if ((flag >> k) & 1u) {
-                const int r = atomicAdd(&n_resc, 1);
-                if (r < kLoopThreads) resc[r] = c; else resc_all = 1;
-                dirty[c % kLoopThreads] = 1;
-            }
-        }
-        block_best_once(bv, bp, red4_v, red4_i);   // its barrier comes after the V writes
-        if (tid == 0) { best_v[a] = bv; best_p[a] = bp; n_cand = 0; }
-        // (5) rows whose best partner was a or b: rescan. Values never grow,
-        // so the row's old best bounds every entry now: scanning in index
-        // order, the first entry at that bound is the answer (largest value,
-        // smallest index) and the scan can stop there. Rows go four at a
-        // time, each split into four quarters of columns, one wave each.
-        const int nr = resc_all ? m : n_resc;
-        for (int r0 = 0; r0 < nr; r0 += kRescRows) {
-            const int slot = wid / kRescParts, part = wid % kRescParts;
-            const int k = r0 + slot;
-            int c = -1;
-            if (k < nr) {
-                c = resc_all ? k : resc[k];
-                if (!act[c] || c == a || (resc_all && best_p[c] != a && best_p[c] != b)) c = -1;
-            }
-            if (c >= 0) {
-                const int64_t ub = best_v[c];
-                const int64_t *row = A.V + (size_t)c * m;
-                const int q = (m + kRescParts - 1) / kRescParts;
-                const int lo = part * q, hi = min(m, lo + q);
-                int64_t v = -1;
-                int32_t p = -1;
-                bool hit = false;
-                constexpr int G = 8;             // chunks of 64 columns loaded together
-                for (int base = lo; base < hi && !hit; base += G * kWave) {
-                    int64_t x[G];
-#pragma unroll
-                    for (int j = 0; j < G; ++j) {
-                        const int d = base + j * kWave + lane;
-                        x[j] = (d < hi && d != c && act[d]) ? row[d] : -1;
-                    }
-#pragma unroll
-                    for (int j = 0; j < G; ++j) {
-                        const int d = base + j * kWave + lane;
-                        const uint64_t at_ub = __ballot(x[j] == ub && x[j] >= 0);
-                        if (!hit && at_ub) {
-                            v = ub;
-                            p = base + j * kWave + __ffsll((long long)at_ub) - 1;
-                            hit = true;
-                        }
-                        if (!hit && better(x[j], d, v, p)) { v = x[j]; p = d; }
-                    }
-                }
-                if (!hit) wave_best(v, p);
-                if (lane == 0) { part_v[slot][part] = v; part_p[slot][part] = p; }
-            }
-            __syncthreads();
-            // quarters in index order: the first that holds a best equal to
-            // the bound decides, otherwise the best of the four
-            if (part == 0 && lane == 0 && c >= 0) {
-                const int64_t ub = best_v[c];
-                int64_t v = -1;
-                int32_t p = -1;
-                for (int j = 0; j < kRescParts; ++j) {
-                    if (part_p[slot][j] < 0) continue;
-                    if (part_v[slot][j] == ub) { v = ub; p = part_p[slot][j]; break; }
-                    if (better(part_v[slot][j], part_p[slot][j], v, p)) { v = part_v[slot][j]; p = part_p[slot][j]; }
-                }
-                best_v[c] = v;
-                best_p[c] = p;
-            }
-            __syncthreads();
-        }
     }
-    // Every remaining pair shares nothing: the merges take the two smallest
-    // live names in turn (n0, n1), (n0, n2), ... with gain 0, and every
-    // merged signature is empty, so D(child) is the child's whole signature
-    // (the root's whole signature if only one cluster is left) and the
-    // chain's own nodes emit nothing. Live names in ascending order, one
-    // round of the workgroup at a time.
+}
+
+// position of every record in the greedy's sequence: the records before it
+// in the pair order. Blocks take a tile of records (x) against a tile of
+// others (y), held in LDS, and add their counts (positions start at 0).
+constexpr int kRankThreads = 256;
+__global__ __launch_bounds__(kRankThreads) void k_rac_rank(Rac R, int n) {
+    __shared__ int64_t tg[kRankThreads];
+    __shared__ int32_t ta[kRankThreads], tb[kRankThreads];
+    const int i = blockIdx.x * kRankThreads + threadIdx.x;
+    const int j0 = blockIdx.y * kRankThreads;
+    const int j = j0 + threadIdx.x;
+    if (j < n) { tg[threadIdx.x] = R.rgain[j]; ta[threadIdx.x] = R.ra[j]; tb[threadIdx.x] = R.rb[j]; }
+    __syncthreads();
+    if (i >= n) return;
+    const int64_t g = R.rgain[i];
+    const int32_t a = R.ra[i], b = R.rb[i];
+    const int cnt = min(kRankThreads, n - j0);
+    int pos = 0;
+    for (int k = 0; k < cnt; ++k) pos += after(g, a, b, tg[k], ta[k], tb[k]) ? 1 : 0;
+    if (pos) atomicAdd(&R.rpos[i], pos);
+}
+
+// tree node of merge record i is m + its position; leaves are 0 .. m - 1
+__device__ inline int32_t rec_node(const Rac &R, int32_t rec, int32_t leaf) {
+    return rec >= 0 ? R.m + R.rpos[rec] : leaf;
+}
+
+__global__ void k_rac_emit(Rac R, int n) {
+    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) {
+        const int t = R.rpos[i];
+        const int32_t a = R.ra[i], b = R.rb[i];
+        R.merge_a[t] = a;
+        R.merge_b[t] = b;
+        R.gain[t] = R.rgain[i];
+        const int32_t node = R.m + t;
+        const int32_t na = rec_node(R, R.rca[i], a), nb = rec_node(R, R.rcb[i], b);
+        R.node_parent[na] = node;
+        R.node_parent[nb] = node;
+        R.d_off[na] = R.rdao[i];
+        R.d_len[na] = R.rdal[i];
+        R.d_off[nb] = R.rdbo[i];
+        R.d_len[nb] = R.rdbl[i];
+    }
+}
+
+// Every remaining pair shares nothing: the merges take the two smallest
+// live names in turn (n0, n1), (n0, n2), ... with gain 0, and every
+// merged signature is empty, so D(child) is the child's whole signature
+// (the root's whole signature if only one cluster is left) and the
+// chain's own nodes emit nothing. Live names in ascending order, one
+// round of the workgroup at a time.
+constexpr int kChainThreads = 1024;
+__global__ __launch_bounds__(kChainThreads) void k_rac_chain(Rac R, int t0) {
+    __shared__ int scan_w[kChainThreads / kWave];
     __shared__ int32_t first_name;
+    const int m = R.m, tid = threadIdx.x;
     if (tid == 0) first_name = -1;
     __syncthreads();
-    const int t0 = t;
-    int64_t dcur = cursor;
+    int64_t dcur = (int64_t)R.h->dcursor;
     int done = 0;                                // live names ranked so far
-    for (int base = 0; base < m; base += blockDim.x) {
+    for (int base = 0; base < m; base += kChainThreads) {
         const int r = base + tid;
-        const int live = r < m && act[r];
-        const int len = live ? slen[r] : 0;
+        const int live = r < m && R.act[r];
+        const int len = live ? R.sig_len[r] : 0;
         int tot, ltot;
         const int rank = done + block_scan(live, &tot, scan_w);
         const int loff = block_scan(len, &ltot, scan_w);
-        if (dcur + ltot > A.dcap) {              // cannot happen for a valid run
-            if (tid == 0) atomicOr(&A.h->err, GERR_INVALID);
+        if (dcur + ltot > R.dcap) {              // cannot happen for a valid run
+            if (tid == 0) atomicOr(&R.h->err, GERR_INVALID);
             return;
         }
         if (live) {
-            const int node = A.node_of[r];
-            const int32_t *src = A.sig + sat[r];
-            for (int e = 0; e < len; ++e) A.dbuf[dcur + loff + e] = src[e];
-            A.d_off[node] = dcur + loff;
-            A.d_len[node] = len;
+            const int32_t node = rec_node(R, R.last[r], r);
+            const int32_t *src = R.sig + R.req_off[r];
+            for (int e = 0; e < len; ++e) R.dbuf[dcur + loff + e] = src[e];
+            R.d_off[node] = dcur + loff;
+            R.d_len[node] = len;
             if (rank == 0) {
                 first_name = r;
             } else {
                 const int tt = t0 + rank - 1;    // the merge that takes r
-                A.merge_b[tt] = r;
-                A.gain[tt] = 0;
-                A.node_parent[node] = m + tt;
+                if (tt < m - 1) {
+                    R.merge_b[tt] = r;
+                    R.gain[tt] = 0;
+                    R.node_parent[node] = m + tt;
+                }
             }
         }
         done += tot;
@@ -653,14 +598,14 @@ __global__ __launch_bounds__(kLoopThreads) void k_g_merge_loop(LoopArgs A) {
     const int n_live = done;
     // the chain: node m+t0 holds the first two names, node m+t0+k holds
     // node m+t0+k-1 and the name of rank k+1
-    for (int k = tid; k + 1 < n_live; k += blockDim.x) {
-        A.merge_a[t0 + k] = first_name;
-        A.d_off[m + t0 + k] = dcur;
-        A.d_len[m + t0 + k] = 0;
-        if (k > 0) A.node_parent[m + t0 + k - 1] = m + t0 + k;
+    for (int k = tid; k + 1 < n_live && t0 + k < m - 1; k += kChainThreads) {
+        R.merge_a[t0 + k] = first_name;
+        R.d_off[m + t0 + k] = dcur;
+        R.d_len[m + t0 + k] = 0;
+        if (k > 0) R.node_parent[m + t0 + k - 1] = m + t0 + k;
     }
-    if (tid == 0 && n_live >= 2) A.node_parent[A.node_of[first_name]] = m + t0;
-    if (tid == 0 && t0 + n_live - 1 != m - 1) atomicOr(&A.h->err, GERR_INVALID);
+    if (tid == 0 && n_live >= 2) R.node_parent[rec_node(R, R.last[first_name], first_name)] = m + t0;
+    if (tid == 0 && t0 + n_live - 1 != m - 1) atomicOr(&R.h->err, GERR_INVALID);
 }
 
 // pi_i: walk from leaf i to the root, placing D(v) of every node on the
@@ -880,42 +825,84 @@ extern "C" int mpt_greedy_hierarchy(int m, int64_t n_chunks, int64_t nnz, const 
     char *ws = (char *)workspace;
     int64_t *V = (int64_t *)(ws + L.V);
     if ((rc = g_prepare(m, n_chunks, nnz, chunk_w, req_off, req_chunks, V, L, ws, s))) return rc;
-    LoopArgs A{};
-    A.m = m;
-    A.w = chunk_w;
-    A.req_off = req_off;
-    A.sig = (int32_t *)(ws + L.sig);
-    A.sig_len = (int32_t *)(ws + L.sig_len);
-    A.sig_at = (int32_t *)(ws + L.key);
-    A.V = V;
-    A.best_v = (int64_t *)(ws + L.best_v);
-    A.best_p = (int32_t *)(ws + L.best_p);
-    A.node_of = (int32_t *)(ws + L.node_of);
-    A.dbuf = (int32_t *)(ws + L.dbuf);
-    A.dcap = std::max<int64_t>(nnz, 1);
-    A.d_off = (int64_t *)(ws + L.d_off);
-    A.d_len = (int32_t *)(ws + L.d_len);
-    A.merge_a = merge_a;
-    A.merge_b = merge_b;
-    A.gain = gain;
-    A.node_parent = node_parent;
-    A.h = (GHeader *)ws;
+    Rac R{};
+    R.m = m;
+    R.w = chunk_w;
+    R.req_off = req_off;
+    R.sig = (int32_t *)(ws + L.sig);
+    R.sig_len = (int32_t *)(ws + L.sig_len);
+    R.V = V;
+    R.best_v = (int64_t *)(ws + L.best_v);
+    R.best_p = (int32_t *)(ws + L.best_p);
+    R.act = (int32_t *)(ws + L.active);
+    R.last = (int32_t *)(ws + L.last);
+    R.touched = (int32_t *)(ws + L.touched);
+    R.resc = (int32_t *)(ws + L.resc);
+    int32_t *r32 = (int32_t *)(ws + L.rec32);
+    int32_t **f32[kRec32] = {&R.ra, &R.rb, &R.rca, &R.rcb, &R.rpos, &R.rdal, &R.rdbl};
+    for (int k = 0; k < kRec32; ++k) *f32[k] = r32 + (size_t)k * m;
+    int64_t *r64 = (int64_t *)(ws + L.rec64);
+    int64_t **f64[kRec64] = {&R.rgain, &R.rdao, &R.rdbo};
+    for (int k = 0; k < kRec64; ++k) *f64[k] = r64 + (size_t)k * m;
+    R.dbuf = (int32_t *)(ws + L.dbuf);
+    R.dcap = std::max<int64_t>(nnz, 1);
+    R.d_off = (int64_t *)(ws + L.d_off);
+    R.d_len = (int32_t *)(ws + L.d_len);
+    R.merge_a = merge_a;
+    R.merge_b = merge_b;
+    R.gain = gain;
+    R.node_parent = node_parent;
+    R.h = (GHeader *)ws;
     {
         LaunchScope ls("g_row_best", 8.0 * (double)m * m, s);
-        k_g_row_best<<<(m + 3) / 4, 4 * kWave, 0, s>>>(m, V, A.best_v, A.best_p);
+        k_g_row_best<<<(m + 3) / 4, 4 * kWave, 0, s>>>(m, V, R.best_v, R.best_p);
+        k_rac_init<<<grid_for(2 * (int64_t)m, 256), 256, 0, s>>>(R);
+    }
+    // rounds in batches without host synchronisation; a round that finds
+    // no pair changes nothing, so the batch's last round tells whether the
+    // rounds are over
+    int n_rec = 0;
+    {
+        LaunchScope ls("g_rounds", (double)(m - 1), s);
+        const int g_rows = grid_for((int64_t)m, 256);
+        const int g_rec = std::max(1, std::min(4096, (m + 3) / 4));        // waves: one per record
+        const int g_cols = grid_for((int64_t)m * std::max(1, m / 2), 256, 2048);
+        const int g_resc = std::max(1, std::min(m, 2048));                  // workgroups: one per marked row
+        constexpr int kBatch = 8;
+        for (int round = 0;;) {
+            for (int k = 0; k < kBatch; ++k, ++round) {
+                k_rac_pairs<<<g_rows, 256, 0, s>>>(R);
+                k_rac_merge<<<g_rec, 4 * kWave, 0, s>>>(R, round);
+                k_rac_rows<<<g_cols, 256, 0, s>>>(R, round);
+                k_rac_rescan<<<g_resc, kRescThreads, 0, s>>>(R, round);
+            }
+            MPT_HIP_TRY(hipGetLastError());
+            GHeader hh;
+            MPT_HIP_TRY(hipMemcpyAsync(&hh, R.h, sizeof hh, hipMemcpyDeviceToHost, s));
+            MPT_HIP_TRY(hipStreamSynchronize(s));
+            if (hh.err) return fail(MPT_E_INTERNAL, "greedy rounds left an inconsistent state");   // cannot happen
+            n_rec = std::min(hh.n_rec, m - 1);
+            if (hh.last_pairs == 0) break;
+            if (round > m + kBatch) return fail(MPT_E_INTERNAL, "greedy rounds do not end");   // cannot happen
+        }
     }
     {
-        LaunchScope ls("g_merge_loop", (double)(m - 1), s);
-        k_g_merge_loop<<<1, kLoopThreads, 0, s>>>(A);
+        LaunchScope ls("g_sequence", (double)m, s);
+        if (n_rec > 0) {
+            const unsigned tiles = (unsigned)((n_rec + kRankThreads - 1) / kRankThreads);
+            k_rac_rank<<<dim3(tiles, tiles), kRankThreads, 0, s>>>(R, n_rec);
+            k_rac_emit<<<grid_for(n_rec, 256), 256, 0, s>>>(R, n_rec);
+        }
+        k_rac_chain<<<1, kChainThreads, 0, s>>>(R, n_rec);
     }
     MPT_HIP_TRY(hipGetLastError());
     if (order_chunks) {
         LaunchScope ls("g_orders", 4.0 * (double)nnz, s);
-        k_g_orders<<<(m + 3) / 4, 4 * kWave, 0, s>>>(m, nnz, req_off, node_parent, A.dbuf, A.d_off, A.d_len,
-                                                     order_chunks, A.h);
+        k_g_orders<<<(m + 3) / 4, 4 * kWave, 0, s>>>(m, nnz, req_off, node_parent, R.dbuf, R.d_off, R.d_len,
+                                                     order_chunks, R.h);
         MPT_HIP_TRY(hipGetLastError());
     }
-    if ((rc = g_read_errors(A.h, s))) return rc;
+    if ((rc = g_read_errors(R.h, s))) return rc;
     if (savings) {
         *savings = 0;
         if (m > 1) {

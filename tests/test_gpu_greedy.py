@@ -169,20 +169,34 @@ def test_determinism():
         assert np.array_equal(a[k], b[k]), k
 
 
-# --- sizes past the on-chip capacities of the merge loop ------------------
+# --- shapes that stress the merge rounds -----------------------------------
+
+@pytest.mark.parametrize("seed", range(24))
+def test_rounds_give_the_sequential_merges(seed):
+    """Unit or small weights over a small pool: many equal merge values
+    within a round and across rounds, so the sequence differs from the
+    order the rounds find the merges in and rests on the pair order alone."""
+    rng = np.random.default_rng(500 + seed)
+    m = int(rng.integers(5, 160))
+    u = int(rng.integers(4, 40))
+    sets = [rng.choice(u, size=int(rng.integers(0, u // 2 + 1)), replace=False).tolist() for _ in range(m)]
+    w = rng.integers(1, 1 + int(rng.choice([1, 2, 6])), size=u)
+    inst = wl.from_sets(sets, w.tolist(), u, name=f"ties seed {seed}")
+    got = gpu_greedy(inst)
+    assert_same(inst, got, oracle.greedy_solve(inst))
+
 
 def test_cluster_state_in_global_memory():
-    """m = 6000 requests: the per-cluster signature metadata and row bests no
-    longer fit on chip (4096 clusters) and live in the workspace."""
+    """m = 6000 requests: more clusters than one workgroup could hold state
+    for; rounds of thousands of merges and rescans."""
     inst = wl.gen_retrieval(m=6000, u=18000, topics=188, k=8, seed=3)
     got = gpu_greedy(inst)
     assert_same(inst, got, oracle.greedy_solve(inst))
 
 
 def test_long_intersections():
-    """Requests of 1500-4000 chunks around a shared core of 2500: the
-    intersections I(A), I(B) exceed the on-chip copy (1024 chunks) and I(C)
-    exceeds its on-chip list (2048 chunks)."""
+    """Requests of 1500-4000 chunks around a shared core of 2500: long
+    signature intersections in the merges and in the new rows."""
     rng = np.random.default_rng(11)
     u = 9000
     core = rng.choice(u, size=2500, replace=False)
@@ -200,8 +214,8 @@ def test_long_intersections():
 
 def test_many_candidate_columns():
     """m = 3000 requests that all hold one common chunk: every merge has
-    positive values against every other cluster, more candidate columns than
-    the on-chip list (2048) holds."""
+    positive values against every other cluster, so every new row is
+    recomputed in full."""
     base = wl.gen_retrieval(m=3000, u=9000, topics=94, k=8, seed=4)
     sets = [r + [9000] for r in base.requests()]
     w = np.concatenate([base.weights, [5]])
