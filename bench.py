@@ -19,7 +19,8 @@ against the VALU instruction peak; `zeta` the W-table kernel against HBM bandwid
 `greedy` the Section 6.2-6.3 heuristic and bound at m = 4096 requests;
 `cache` the Section 7-8 layouts and radix-cache grid on the same instance;
 `pinned` the Section 7.1 pinned variant on it; `dense_w` the W table's
-dense route on an instance with long requests.
+dense route on an instance with long requests; `wide_keys` the step on the
+same instance with weights scaled past the 32-bit keys (doubles, uint64).
 """
 from __future__ import annotations
 
@@ -249,6 +250,64 @@ def dense_w_bench(steps: int, warmup: int) -> dict:
     return out
 
 
+def wide_keys_bench(inst, steps: int, golden_opt) -> dict:
+    """The same step on the same instance with every chunk weight scaled, so
+    that sum_i w(R_i) passes the 32-bit key range: x64 runs the DP on
+    exact-integer doubles, x4096 on uint64 keys. Per scale: ms per step, the
+    cross-pair kernel's share and its fraction of the VALU roofline at that
+    representation's instruction count, and OPT_free against the golden
+    optimum times the scale."""
+    import dataclasses
+    import torch
+    from paper_2609_13692_amd import mpt
+
+    out = {}
+    dev = torch.device("cuda")
+    for scale in (64, 4096):
+        sc = dataclasses.replace(inst, weights=inst.weights * scale)
+        w = torch.as_tensor(sc.weights, dtype=torch.int64).to(dev)
+        off = torch.as_tensor(sc.req_off, dtype=torch.int64).to(dev)
+        ch = torch.as_tensor(sc.req_chunks, dtype=torch.int32).to(dev)
+        ctx = mpt.Context(dev)
+        ctx.reserve(sc.m, sc.n_chunks, sc.nnz)
+
+        def step():
+            ctx.build_weights(sc.m, sc.n_chunks, w, off, ch)
+            ctx.solve_exact(want_cost=False)
+            ctx.extract_orders(to_host=False)
+            return ctx.optimum()[0]
+
+        step()
+        torch.cuda.synchronize()
+        mpt.profile_begin()
+        step()
+        torch.cuda.synchronize()
+        prof = mpt.profile_end()
+        dom = max((k for k in prof if k.startswith("rb_cross")), key=lambda k: prof[k]["total_ms"])
+        mpt.profile_begin(dom)
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            opt = step()
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        d = mpt.profile_end()[dom]
+        ctx.close()
+        ms = (t1 - t0) * 1000.0 / steps
+        kernel, ops, keys = DP_KEYS[dom]
+        tops = d["work"] * ops / (d["total_ms"] / 1000.0) / 1e12
+        out[f"x{scale}"] = {
+            "request_total": int(sc.weights[sc.req_chunks].sum()),
+            "keys": keys, "kernel": dom, "ms_per_step": round(ms, 3),
+            "bipartitions_per_s": t_eval(sc.m) / (ms / 1000.0),
+            "dominant_ms_per_step": round(d["total_ms"] / steps, 3),
+            "roofline": {"bound": "alu", "achieved": round(tops, 3), "peak": round(VALU_PEAK_TOPS, 2),
+                         "unit": "TOP/s", "frac": round(tops / VALU_PEAK_TOPS, 4), "ops_per_pair": ops},
+            "opt": opt,
+            "opt_matches_scaled_golden": (opt == scale * golden_opt) if golden_opt is not None else None,
+        }
+    return out
+
+
 CACHE_WINDOWS = (1, 128, 512, 2048, 0)          # 0: the whole stream
 CACHE_CAPACITIES = (1, 4, 16, 64, 256, 1024)     # multiples of max_i w(R_i)
 
@@ -358,6 +417,7 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-greedy", action="store_true", help="skip the Section 6.2-6.3 measurement")
     ap.add_argument("--no-dense", action="store_true", help="skip the dense W route measurement")
+    ap.add_argument("--no-wide", action="store_true", help="skip the 64-bit key measurement")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB before the timed steps "
                          "(a known-size kernel that scales rocprofv3 FETCH_SIZE/WRITE_SIZE)")
@@ -491,6 +551,8 @@ def main() -> int:
         "roofline": roofline,
         "zeta": zeta,
     }
+    if not args.no_wide:
+        line["wide_keys"] = wide_keys_bench(inst, max(1, min(args.steps, 3)), golden_opt)
     if not args.no_dense:
         line["dense_w"] = dense_w_bench(max(1, args.steps), max(1, args.warmup))
     if not args.no_greedy:
