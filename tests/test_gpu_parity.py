@@ -381,7 +381,7 @@ def test_max_m_weight_table():
 
 def test_max_m_full_solve():
     """Whole path at MPT_MAX_M = 30 (2^30-entry tables, 1.0e14 bipartitions)
-    on L_28, where every entry has a closed form: C(S) = (n - |S|) + E(|S|)
+    on L_30, where every entry has a closed form: C(S) = (n - |S|) + E(|S|)
     with E the Eq. (5) free value; the split table encodes a hierarchy whose
     Eq. (2) cost and read-off trie cost are both OPT."""
     n = mpt.MPT_MAX_M
