@@ -395,8 +395,11 @@ int mpt_layout_cost(int m, int64_t n_chunks, int64_t nnz, const int64_t *chunk_w
  *   windows, capacities    HOST arrays [n_configs]
  *   costs                  HOST out [n_configs]: the billed weight
  *   trie_cost              HOST out, nullable: the unbounded-cache bill
- * The configurations run concurrently, one wavefront each. Synchronises
- * `stream`.
+ * Such a cache always holds the longest prefix of its recency stack that
+ * fits (the stack property of LRU), so an access hits iff the distinct
+ * weight accessed since its node's previous access, plus its own, fits.
+ * Configurations with equal windows share one schedule and one pass that
+ * prices all their capacities. Synchronises `stream`.
  */
 int mpt_cache_simulate(int m, int64_t n_chunks, int64_t nnz, const int64_t *chunk_w,
                        const int64_t *seq_off, const int32_t *seqs, int n_configs,

@@ -18,12 +18,13 @@
 // Radix cache. Serving a request touches its whole path, so an ancestor is
 // never older than a descendant, and the least-recently-used leaf is the
 // deepest of the least-recently-used nodes: the policy is plain LRU over
-// nodes, with each request's path touched from the leaf up. An LRU cache of
-// weighted items always holds the longest suffix of its access log whose
-// distinct items fit the capacity, so eviction walks the log from its tail,
-// dropping entries that are still the latest access of their node. One
-// wave runs one (window, capacity) pair, 64 log entries per step, with the
-// latest access of every node in LDS.
+// nodes, with each request's path touched from the leaf up. Such a cache
+// always holds the longest prefix of its recency stack that fits, so an
+// access hits iff the distinct weight accessed since its node's previous
+// access, plus its own, fits the capacity. That stack distance does not
+// depend on the capacity: configurations with the same window share one
+// schedule, one access log and one pass that prices all their capacities,
+// every log entry on its own thread.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -47,7 +48,6 @@ using mptlib::kSeqSortTile;
 using mptlib::sort_requests;
 
 constexpr int kWave = 64;
-constexpr int kSimNodesLds = 36 * 1024;       // nodes whose latest access fits the LDS of one workgroup
 
 enum : uint32_t { LERR_INVALID = 1u, LERR_RANGE = 2u, LERR_WEIGHT = 8u, LERR_OVERFLOW = 16u };
 
@@ -67,8 +67,8 @@ inline int64_t pow2_at_least(int64_t n) {
 }
 
 struct LLayout {
-    size_t ord, rank, lcp, base, pn, nw, cur, crank, cinv, keys, sched, log_off, logs, state, cfg_win, cfg_cap,
-        costs, total;
+    size_t ord, rank, lcp, base, pn, nw, cur, crank, cinv, keys, sched, log_off, logs, acc_start, prev, next, accw,
+        bnext, bsum, cfg_win, cfg_cap, cfg_off, cfg_list, costs, total;
     int64_t mpad, kpad;
 };
 
@@ -77,8 +77,9 @@ LLayout l_layout(int m, int64_t n_chunks, int64_t nnz, int n_cfg) {
     LLayout L{};
     const size_t mm = (size_t)m, nz = (size_t)std::max<int64_t>(nnz, 1), nc = (size_t)std::max(n_cfg, 0);
     L.mpad = std::max<int64_t>(pow2_at_least(m), kSeqSortTile);
-    L.kpad = std::max<int64_t>(pow2_at_least(std::max<int64_t>(std::max<int64_t>(nnz, n_chunks), (int64_t)nc * m)),
-                               kSortTile);
+    L.kpad = std::max<int64_t>(
+        pow2_at_least(std::max(std::max<int64_t>(nnz, n_chunks), (int64_t)nc * std::max<int64_t>(m, nnz))), kSortTile);
+    const size_t nblk = (nz + 255) / 256;       // sorted blocks of the access logs (kStackBlock entries)
     size_t o = align256(sizeof(LHeader));
     auto take = [&](size_t bytes) { size_t at = o; o = align256(o + std::max<size_t>(bytes, 1)); return at; };
     L.ord = take(4 * (size_t)L.mpad);
@@ -94,9 +95,16 @@ LLayout l_layout(int m, int64_t n_chunks, int64_t nnz, int n_cfg) {
     L.sched = take(4 * nc * mm);
     L.log_off = take(8 * nc * mm);
     L.logs = take(4 * nc * nz);
-    L.state = take(nz > (size_t)kSimNodesLds ? 4 * nc * nz : 0);
+    L.acc_start = take(4 * nc * nz);
+    L.prev = take(4 * nc * nz);
+    L.next = take(4 * nc * nz);
+    L.accw = take(8 * nc * nz);
+    L.bnext = take(4 * nc * nblk * 256);
+    L.bsum = take(8 * nc * nblk * 256);
     L.cfg_win = take(8 * nc);
     L.cfg_cap = take(8 * nc);
+    L.cfg_off = take(4 * (nc + 1));
+    L.cfg_list = take(4 * nc);
     L.costs = take(8 * nc);
     L.total = o;
     return L;
@@ -371,91 +379,172 @@ __global__ __launch_bounds__(1024) void k_l_log_scan(int m, int64_t *log_off) {
 // the access log of every configuration: served requests in order, each
 // path from its leaf up to the root
 __global__ void k_l_logs(int m, int n_cfg, int64_t nnz, const int32_t *sched, const int64_t *log_off,
-                         const int64_t *off, const int32_t *pn, int32_t *logs) {
+                         const int64_t *off, const int32_t *pn, int32_t *logs, int32_t *acc_start) {
     for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < (int64_t)n_cfg * m;
          e += (int64_t)gridDim.x * blockDim.x) {
         const int c = (int)(e / m);
         const int i = sched[e];
         const int64_t li = off[i + 1] - off[i], at = log_off[e];
         int32_t *dst = logs + (int64_t)c * nnz + at;
+        int32_t *st = acc_start + (int64_t)c * nnz + at;
         const int32_t *path = pn + off[i];
-        for (int64_t j = 0; j < li; ++j) dst[j] = path[li - 1 - j];
+        for (int64_t j = 0; j < li; ++j) {
+            dst[j] = path[li - 1 - j];
+            st[j] = (int32_t)at;                 // where the request's accesses start
+        }
     }
 }
 
 // ---------------------------------------------------------------------------
-// the radix cache, one wave per configuration
+// the radix cache by stack distances
+//
+// Serving a request touches its whole path, each node of it more recently
+// than its descendants, and every miss is inserted before the cache evicts
+// (least-recently-used leaf first, which is the least-recently-used node,
+// since an ancestor is never older than its descendants). By induction over
+// the requests, the cache after each request holds exactly the longest
+// prefix of the recency stack (nodes by latest access, most recent first)
+// whose weight fits the capacity: the stack property of LRU (Mattson et al.,
+// 1970), here with weights. So node v of the request whose accesses start at
+// log position s is a hit iff it was accessed before and the nodes above it
+// in the stack together with v fit: D + w(v) <= capacity, where D is the
+// weight of the distinct nodes accessed between v's previous access p and s,
+// i.e. the sum of w_j over log entries p < j < s whose node is not accessed
+// again before s (next_j >= s). D does not depend on the capacity: one pass
+// over a schedule's log bills all its capacities.
 
-template <bool kLds>
-__global__ __launch_bounds__(kWave) void k_l_simulate(int m, int64_t nnz, int64_t n_nodes, const int64_t *capacities,
-                                                      const int32_t *sched, const int64_t *off, const int32_t *pn,
-                                                      const int64_t *nw, const int32_t *logs, int32_t *state_g,
-                                                      int64_t *costs) {
-    extern __shared__ int32_t state_s[];
-    const int c = blockIdx.x;
-    const int lane = threadIdx.x;
-    int32_t *last = kLds ? state_s : state_g + (int64_t)c * nnz;   // latest log position of a cached node, -1 if not cached
-    const int32_t *log = logs + (int64_t)c * nnz;
-    const int32_t *sc = sched + (int64_t)c * m;
-    const int64_t cap = capacities[c];
-    for (int64_t v = lane; v < n_nodes; v += kWave) last[v] = -1;
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    int64_t used = 0, cost = 0, head = 0, tail = 0;
-    for (int t = 0; t < m; ++t) {
-        const int i = sc[t];
-        const int64_t li = off[i + 1] - off[i];
-        const int32_t *path = pn + off[i];
-        // misses: the nodes not cached (the cached ones are the top of the
-        // path); then every node of the path becomes the latest access
-        int64_t miss = 0;
-        for (int64_t j0 = 0; j0 < li; j0 += kWave) {
-            const int64_t j = j0 + lane;
-            if (j < li) {
-                const int32_t v = path[j];
-                if (last[v] < 0) miss += nw[v];
-                last[v] = (int32_t)(head + (li - 1 - j));
-            }
-        }
-#pragma unroll
-        for (int o = kWave / 2; o > 0; o >>= 1) miss += __shfl_xor(miss, o, kWave);
-        cost += miss;
-        used += miss;
-        head += li;
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-        // evict from the log tail: an entry that is still its node's latest
-        // access is a cached node, the oldest one left
-        while (used > cap && tail < head) {
-            const int64_t e = tail + lane;
-            int64_t wl = 0;
-            int32_t v = -1;
-            if (e < head) {
-                v = log[e];
-                if (last[v] == (int32_t)e) wl = nw[v];
-            }
-            int64_t incl = wl;
-#pragma unroll
-            for (int o = 1; o < kWave; o <<= 1) {
-                const int64_t y = __shfl_up(incl, o, kWave);
-                if (lane >= o) incl += y;
-            }
-            // first lane after which the cache fits; all 64 if none
-            const uint64_t fits = __ballot(e < head && used - incl <= cap);
-            const int cut = fits ? __ffsll((long long)fits) - 1 : kWave - 1;
-            if (lane <= cut && wl > 0) last[v] = -1;
-            const int64_t dropped = __shfl(incl, cut, kWave);
-            used -= dropped;
-            tail += cut + 1;
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-            __builtin_amdgcn_wave_barrier();
-            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-        }
-        if (tail > head) tail = head;
+constexpr int kStackBlock = 256;               // log entries per sorted block
+
+// sort keys of the access logs of schedules d0 .. d0 + nd - 1: (schedule,
+// node, log position); the padding sorts last
+__global__ void k_l_acc_keys(int64_t nnz, int d0, int nd, int be, int bn, int64_t npad, const int32_t *logs,
+                             uint64_t *keys) {
+    for (int64_t k = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; k < npad; k += (int64_t)gridDim.x * blockDim.x) {
+        if (k >= (int64_t)nd * nnz) { keys[k] = ~0ull; continue; }
+        const int64_t dl = k / nnz, e = k % nnz;
+        const uint64_t v = (uint64_t)logs[(d0 + dl) * nnz + e];
+        keys[k] = ((uint64_t)dl << (bn + be)) | (v << be) | (uint64_t)e;
     }
-    if (lane == 0) costs[c] = cost;
+}
+
+// previous and next access of the same node (-1 / nnz when there is none);
+// schedule d0 + dl holds sorted positions [dl nnz, (dl + 1) nnz)
+__global__ void k_l_prev_next(int64_t nnz, int d0, int nd, int be, const uint64_t *keys, int32_t *prev,
+                              int32_t *next) {
+    const uint64_t emask = (1ull << be) - 1ull;
+    const int64_t n = (int64_t)nd * nnz;
+    for (int64_t k = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; k < n; k += (int64_t)gridDim.x * blockDim.x) {
+        const uint64_t key = keys[k], grp = key >> be;
+        const int64_t at = (d0 + k / nnz) * nnz + (int64_t)(key & emask);
+        const bool has_prev = (k % nnz) > 0 && (keys[k - 1] >> be) == grp;
+        const bool has_next = (k + 1) % nnz != 0 && (keys[k + 1] >> be) == grp;
+        prev[at] = has_prev ? (int32_t)(keys[k - 1] & emask) : -1;
+        next[at] = has_next ? (int32_t)(keys[k + 1] & emask) : (int32_t)nnz;
+    }
+}
+
+// one workgroup per block of 256 log entries of one schedule: the entries'
+// weights, and the block sorted by next access descending with the running
+// weight sum, so that the weight of the entries with next >= s is a prefix
+__global__ __launch_bounds__(kStackBlock) void k_l_stack_blocks(int64_t nnz, int64_t nblk, const int32_t *logs,
+                                                                const int64_t *nw, const int32_t *next,
+                                                                int64_t *accw, int32_t *bnext, int64_t *bsum) {
+    __shared__ uint64_t t[kStackBlock];
+    __shared__ int64_t ws[kStackBlock];
+    const int64_t d = blockIdx.x / nblk, b = blockIdx.x % nblk;
+    const int64_t j = b * kStackBlock + threadIdx.x;
+    const int64_t at = d * nnz + j;
+    int64_t w = 0;
+    int32_t nx = -1;                                     // padding: never counted
+    if (j < nnz) {
+        w = nw[logs[at]];
+        nx = next[at];
+        accw[at] = w;
+    }
+    ws[threadIdx.x] = w;
+    // key: next access in the high half (biased so that -1 sorts lowest),
+    // entry index in the low half; sorted descending
+    t[threadIdx.x] = ((uint64_t)(uint32_t)(nx + 1) << 32) | (uint64_t)threadIdx.x;
+    __syncthreads();
+    for (int k = 2; k <= kStackBlock; k <<= 1)
+        for (int s = k >> 1; s > 0; s >>= 1) {
+            const int i = threadIdx.x, pj = i ^ s;
+            if (pj > i) {
+                const bool desc = (i & k) == 0;
+                const uint64_t a = t[i], c = t[pj];
+                if (desc ? (a < c) : (a > c)) { t[i] = c; t[pj] = a; }
+            }
+            __syncthreads();
+        }
+    const uint64_t key = t[threadIdx.x];
+    int64_t x = ws[key & 0xffffffffull];
+    // inclusive scan of the weights in sorted order
+    __shared__ int64_t sw[kStackBlock / kWave];
+    const int lane = threadIdx.x & (kWave - 1), wid = threadIdx.x / kWave;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        const int64_t y = __shfl_up(x, o, kWave);
+        if (lane >= o) x += y;
+    }
+    if (lane == kWave - 1) sw[wid] = x;
+    __syncthreads();
+    for (int k = 0; k < wid; ++k) x += sw[k];
+    const int64_t out = d * nblk * kStackBlock + j;
+    bnext[out] = (int32_t)(key >> 32) - 1;
+    bsum[out] = x;
+}
+
+// one thread per log entry of one schedule: its stack distance, then its
+// bill under every capacity of the schedule, summed per workgroup in LDS
+// and added to the configurations' costs
+constexpr int kBillThreads = 256;
+__global__ __launch_bounds__(kBillThreads) void k_l_bill(int64_t nnz, int64_t nblk, const int32_t *prev,
+                                                         const int32_t *next, const int32_t *acc_start,
+                                                         const int64_t *accw, const int32_t *bnext,
+                                                         const int64_t *bsum, const int32_t *cfg_off,
+                                                         const int32_t *cfg_list, const int64_t *caps,
+                                                         unsigned long long *costs) {
+    __shared__ unsigned long long acc[MPT_CACHE_MAX_CONFIGS];
+    const int d = blockIdx.y;
+    const int c0 = cfg_off[d], nc = cfg_off[d + 1] - c0;
+    for (int k = threadIdx.x; k < nc; k += kBillThreads) acc[k] = 0ull;
+    __syncthreads();
+    const int64_t e = blockIdx.x * (int64_t)kBillThreads + threadIdx.x;
+    if (e < nnz) {
+        const int64_t base = (int64_t)d * nnz;
+        const int64_t w = accw[base + e];
+        const int64_t p = prev[base + e];
+        int64_t dist = -1;                               // -1: first access, a miss everywhere
+        if (p >= 0) {
+            const int64_t s = acc_start[base + e];
+            dist = 0;
+            int64_t j = p + 1;
+            // entries up to the end of p's block, one by one
+            const int64_t first_full = (j + kStackBlock - 1) / kStackBlock * kStackBlock;
+            for (; j < min(s, first_full); ++j)
+                if (next[base + j] >= s) dist += accw[base + j];
+            // whole blocks: the prefix of the block with next >= s
+            for (; j + kStackBlock <= s; j += kStackBlock) {
+                const int64_t bo = (int64_t)d * nblk * kStackBlock + j;
+                int lo = 0, hi = kStackBlock;              // first sorted entry with next < s
+                while (lo < hi) {
+                    const int mid = (lo + hi) >> 1;
+                    if (bnext[bo + mid] >= s) lo = mid + 1; else hi = mid;
+                }
+                if (lo > 0) dist += bsum[bo + lo - 1];
+            }
+            // the rest, one by one
+            for (; j < s; ++j)
+                if (next[base + j] >= s) dist += accw[base + j];
+        }
+        for (int k = 0; k < nc; ++k) {
+            const bool miss = dist < 0 || dist + w > caps[cfg_list[c0 + k]];
+            if (miss) atomicAdd(&acc[k], (unsigned long long)w);
+        }
+    }
+    __syncthreads();
+    for (int k = threadIdx.x; k < nc; k += kBillThreads)
+        if (acc[k]) atomicAdd(&costs[cfg_list[c0 + k]], acc[k]);
 }
 
 // ---------------------------------------------------------------------------
@@ -603,43 +692,79 @@ extern "C" int mpt_cache_simulate(int m, int64_t n_chunks, int64_t nnz, const in
     int64_t tc = 0, n_nodes = 0;
     if ((rc = l_prepare(m, n_chunks, nnz, chunk_w, seq_off, seqs, L, ws, s, true, &tc, &n_nodes))) return rc;
     if (trie_cost) *trie_cost = tc;
-    // configurations: window <= 0 or > m means the whole stream
-    std::vector<int64_t> win(n_configs), capv(capacities, capacities + n_configs);
-    for (int c = 0; c < n_configs; ++c) win[c] = (windows[c] <= 0 || windows[c] > m) ? m : windows[c];
-    int64_t *dev_cfg = (int64_t *)(ws + L.cfg_win), *dev_capacity = (int64_t *)(ws + L.cfg_cap);
-    MPT_HIP_TRY(hipMemcpyAsync(dev_cfg, win.data(), sizeof(int64_t) * n_configs, hipMemcpyHostToDevice, s));
+    // configurations: window <= 0 or > m means the whole stream. Equal
+    // windows share one schedule (and log); cfg_off / cfg_list list the
+    // configurations of every schedule.
+    std::vector<int64_t> win;
+    std::vector<int> sched_of(n_configs);
+    for (int c = 0; c < n_configs; ++c) {
+        const int64_t wc = (windows[c] <= 0 || windows[c] > m) ? m : windows[c];
+        int d = 0;
+        while (d < (int)win.size() && win[d] != wc) ++d;
+        if (d == (int)win.size()) win.push_back(wc);
+        sched_of[c] = d;
+    }
+    const int n_sched = (int)win.size();
+    std::vector<int32_t> cfg_off(n_sched + 1, 0), cfg_list;
+    for (int d = 0; d < n_sched; ++d) {
+        for (int c = 0; c < n_configs; ++c)
+            if (sched_of[c] == d) cfg_list.push_back(c);
+        cfg_off[d + 1] = (int32_t)cfg_list.size();
+    }
+    std::vector<int64_t> capv(capacities, capacities + n_configs);
+    int64_t *dev_win = (int64_t *)(ws + L.cfg_win), *dev_capacity = (int64_t *)(ws + L.cfg_cap);
+    int32_t *dev_cfg_off = (int32_t *)(ws + L.cfg_off), *dev_cfg_list = (int32_t *)(ws + L.cfg_list);
+    MPT_HIP_TRY(hipMemcpyAsync(dev_win, win.data(), sizeof(int64_t) * n_sched, hipMemcpyHostToDevice, s));
     MPT_HIP_TRY(hipMemcpyAsync(dev_capacity, capv.data(), sizeof(int64_t) * n_configs, hipMemcpyHostToDevice, s));
+    MPT_HIP_TRY(hipMemcpyAsync(dev_cfg_off, cfg_off.data(), sizeof(int32_t) * (n_sched + 1), hipMemcpyHostToDevice, s));
+    MPT_HIP_TRY(hipMemcpyAsync(dev_cfg_list, cfg_list.data(), sizeof(int32_t) * n_configs, hipMemcpyHostToDevice, s));
     uint64_t *keys = (uint64_t *)(ws + L.keys);
     int32_t *sched = (int32_t *)(ws + L.sched), *logs = (int32_t *)(ws + L.logs);
-    int64_t *log_off = (int64_t *)(ws + L.log_off);
+    int32_t *acc_start = (int32_t *)(ws + L.acc_start), *prev = (int32_t *)(ws + L.prev), *next = (int32_t *)(ws + L.next);
+    int64_t *log_off = (int64_t *)(ws + L.log_off), *accw = (int64_t *)(ws + L.accw);
     const int32_t *ord = (const int32_t *)(ws + L.ord), *rank = (const int32_t *)(ws + L.rank);
     {
-        LaunchScope ls("l_schedules", (double)n_configs * m, s);
-        k_l_sched_keys<<<grid_for(L.kpad, 256), 256, 0, s>>>(m, n_configs, L.kpad, dev_cfg, rank, keys);
-        if ((rc = sort_keys(keys, L.kpad, s))) return rc;
-        k_l_sched_out<<<grid_for((int64_t)n_configs * m, 256), 256, 0, s>>>(m, n_configs, keys, ord, seq_off, sched,
-                                                                           log_off);
-        k_l_log_scan<<<n_configs, 1024, 0, s>>>(m, log_off);
+        LaunchScope ls("l_schedules", (double)n_sched * m, s);
+        const int64_t spad = std::max<int64_t>(pow2_at_least((int64_t)n_sched * m), kSortTile);
+        k_l_sched_keys<<<grid_for(spad, 256), 256, 0, s>>>(m, n_sched, spad, dev_win, rank, keys);
+        if ((rc = sort_keys(keys, spad, s))) return rc;
+        k_l_sched_out<<<grid_for((int64_t)n_sched * m, 256), 256, 0, s>>>(m, n_sched, keys, ord, seq_off, sched,
+                                                                          log_off);
+        k_l_log_scan<<<n_sched, 1024, 0, s>>>(m, log_off);
         if (nnz > 0)
-            k_l_logs<<<grid_for((int64_t)n_configs * m, 256), 256, 0, s>>>(m, n_configs, nnz, sched, log_off, seq_off,
-                                                                          (const int32_t *)(ws + L.pn), logs);
+            k_l_logs<<<grid_for((int64_t)n_sched * m, 256), 256, 0, s>>>(m, n_sched, nnz, sched, log_off, seq_off,
+                                                                         (const int32_t *)(ws + L.pn), logs, acc_start);
     }
     MPT_HIP_TRY(hipGetLastError());
     int64_t *dev_costs = (int64_t *)(ws + L.costs);
-    {
-        LaunchScope ls("l_simulate", (double)n_configs * nnz, s);
-        if (n_nodes <= kSimNodesLds) {
-            const size_t lds = sizeof(int32_t) * (size_t)std::max<int64_t>(n_nodes, 1);
-            MPT_HIP_TRY(hipFuncSetAttribute((const void *)k_l_simulate<true>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                            (int)lds));
-            k_l_simulate<true><<<n_configs, kWave, lds, s>>>(m, nnz, n_nodes, dev_capacity, sched, seq_off,
-                                                             (const int32_t *)(ws + L.pn), (const int64_t *)(ws + L.nw),
-                                                             logs, nullptr, dev_costs);
-        } else {
-            k_l_simulate<false><<<n_configs, kWave, 0, s>>>(m, nnz, n_nodes, dev_capacity, sched, seq_off,
-                                                            (const int32_t *)(ws + L.pn), (const int64_t *)(ws + L.nw),
-                                                            logs, (int32_t *)(ws + L.state), dev_costs);
+    k_l_fill_u64<<<1, 256, 0, s>>>((uint64_t *)dev_costs, n_configs, 0ull);
+    if (nnz > 0) {
+        {
+            // previous and next access of every log entry: a sort of
+            // (schedule, node, position) keys, as many schedules per sort as
+            // the 63 key bits hold
+            LaunchScope ls("l_reuse", (double)n_sched * nnz, s);
+            auto bits = [](int64_t n) { int b = 1; while (b < 62 && ((int64_t)1 << b) < n) ++b; return b; };
+            const int be = bits(nnz), bn = bits(std::max<int64_t>(n_nodes, 1));
+            const int gb = 63 - be - bn;                  // >= 1: nnz and the node count stay below 2^31
+            const int group = gb >= 8 ? n_sched : std::min(n_sched, 1 << gb);
+            for (int d0 = 0; d0 < n_sched; d0 += group) {
+                const int nd = std::min(group, n_sched - d0);
+                const int64_t npad = std::max<int64_t>(pow2_at_least((int64_t)nd * nnz), kSortTile);
+                k_l_acc_keys<<<grid_for(npad, 256), 256, 0, s>>>(nnz, d0, nd, be, bn, npad, logs, keys);
+                if ((rc = sort_keys(keys, npad, s))) return rc;
+                k_l_prev_next<<<grid_for((int64_t)nd * nnz, 256), 256, 0, s>>>(nnz, d0, nd, be, keys, prev, next);
+            }
         }
+        LaunchScope ls("l_simulate", (double)n_configs * nnz, s);
+        const int64_t nblk = (nnz + kStackBlock - 1) / kStackBlock;
+        int32_t *bnext = (int32_t *)(ws + L.bnext);
+        int64_t *bsum = (int64_t *)(ws + L.bsum);
+        k_l_stack_blocks<<<(unsigned)(n_sched * nblk), kStackBlock, 0, s>>>(nnz, nblk, logs, (const int64_t *)(ws + L.nw),
+                                                                            next, accw, bnext, bsum);
+        k_l_bill<<<dim3((unsigned)((nnz + kBillThreads - 1) / kBillThreads), (unsigned)n_sched), kBillThreads, 0, s>>>(
+            nnz, nblk, prev, next, acc_start, accw, bnext, bsum, dev_cfg_off, dev_cfg_list, dev_capacity,
+            (unsigned long long *)dev_costs);
     }
     MPT_HIP_TRY(hipGetLastError());
     MPT_HIP_TRY(hipMemcpyAsync(costs, dev_costs, sizeof(int64_t) * n_configs, hipMemcpyDeviceToHost, s));
