@@ -67,7 +67,7 @@ inline int64_t pow2_at_least(int64_t n) {
 }
 
 struct LLayout {
-    size_t ord, rank, lcp, base, pn, nw, cur, crank, cinv, keys, sched, log_off, logs, acc_start, prev, next, accw,
+    size_t ord, rank, lcp, base, pn, nw, mtree, crank, cinv, keys, sched, log_off, logs, acc_start, prev, next, accw,
         bnext, bsum, cfg_win, cfg_cap, cfg_off, cfg_list, costs, total;
     int64_t mpad, kpad;
 };
@@ -88,7 +88,7 @@ LLayout l_layout(int m, int64_t n_chunks, int64_t nnz, int n_cfg) {
     L.base = take(8 * (mm + 1));
     L.pn = take(4 * nz);
     L.nw = take(8 * nz);
-    L.cur = take(4 * nz);
+    L.mtree = take(8 * (size_t)L.mpad);          // min segment tree over the LCPs
     L.crank = take(4 * (size_t)n_chunks);
     L.cinv = take(4 * (size_t)n_chunks);
     L.keys = take(8 * (size_t)L.kpad);
@@ -272,49 +272,74 @@ __global__ void k_l_node_weights(int m, const int32_t *ord, const int64_t *off, 
     }
 }
 
-// node ids of every request's path: depth j < LCP takes the node of the
-// same depth of the previous request in sorted order, deeper ones are the
-// request's own new nodes. One wave walks the sorted requests, 64 at a time
-// (their offsets, lengths, LCPs and bases loaded together); lane l owns the
-// depths l, l + 64, ..., the first kRegDepth of them in registers and the
-// rest in `cur` (only ever read back by the same lane).
-constexpr int kRegDepth = 4;
-__global__ __launch_bounds__(kWave) void k_l_paths(int m, const int32_t *ord, const int64_t *off, const int32_t *lcp,
-                                                   const int64_t *base, int32_t *pn, int32_t *cur) {
-    const int lane = threadIdx.x;
-    int32_t reg[kRegDepth];
-#pragma unroll
-    for (int r = 0; r < kRegDepth; ++r) reg[r] = -1;
-    for (int s0 = 0; s0 < m; s0 += kWave) {
-        const int s = s0 + lane;
-        int64_t my_off = 0, my_len = 0, my_b = 0;
-        int my_l = 0;
-        if (s < m) {
-            const int i = ord[s];
-            my_off = off[i];
-            my_len = off[i + 1] - my_off;
-            my_l = lcp[s];
-            my_b = base[s];
+// node ids of every request's path. Request s (in sorted order) creates the
+// nodes of depths LCP(s) .. len-1, with ids base[s] + (j - LCP(s)); a
+// shallower depth j < LCP(s) holds the node of the previous request, and so
+// on back to the last request t <= s with LCP(t) <= j, which created it. A
+// min segment tree over the LCPs finds t in O(log m), so every slot of the
+// layout is one independent thread.
+constexpr int kTreeBlock = 2048;               // leaves of the subtree one workgroup builds in LDS
+
+// leaves mtree[mpad + t] = LCP(t) (padding: INT32_MAX) and the levels of each
+// workgroup's subtree of kTreeBlock leaves (heap order: node n has children
+// 2n, 2n + 1; the root is 1)
+__global__ __launch_bounds__(1024) void k_l_mtree_low(int m, int64_t mpad, const int32_t *lcp, int32_t *mtree) {
+    __shared__ int32_t t[kTreeBlock];
+    const int64_t S = min<int64_t>(kTreeBlock, mpad);
+    const int64_t first = (int64_t)blockIdx.x * S;
+    for (int64_t e = threadIdx.x; e < S; e += blockDim.x) {
+        const int64_t leaf = first + e;
+        const int32_t v = leaf < m ? lcp[leaf] : INT32_MAX;
+        t[e] = v;
+        mtree[mpad + leaf] = v;
+    }
+    __syncthreads();
+    for (int64_t len = S >> 1, k = 1; len >= 1; len >>= 1, ++k) {
+        int32_t v = 0;
+        const int64_t e = threadIdx.x;
+        if (e < len) v = min(t[2 * e], t[2 * e + 1]);
+        __syncthreads();
+        if (e < len) {
+            t[e] = v;
+            mtree[(mpad >> k) + (first >> k) + e] = v;
         }
-        const int cnt = min(kWave, m - s0);
-        for (int q = 0; q < cnt; ++q) {
-            const int64_t io = __shfl(my_off, q, kWave), len = __shfl(my_len, q, kWave), b = __shfl(my_b, q, kWave);
-            const int l = __shfl(my_l, q, kWave);
-#pragma unroll
-            for (int r = 0; r < kRegDepth; ++r) {
-                const int64_t j = lane + (int64_t)r * kWave;
-                if (j < len) {
-                    if (j >= l) reg[r] = (int32_t)(b + (j - l));
-                    pn[io + j] = reg[r];
-                }
-            }
-            for (int64_t j = lane + (int64_t)kRegDepth * kWave; j < len; j += kWave) {
-                int32_t v;
-                if (j >= l) { v = (int32_t)(b + (j - l)); cur[j] = v; }
-                else v = cur[j];
-                pn[io + j] = v;
-            }
+        __syncthreads();
+    }
+}
+
+// the levels above the subtrees, one workgroup
+__global__ __launch_bounds__(1024) void k_l_mtree_top(int64_t top, int32_t *mtree) {
+    for (int64_t len = top >> 1; len >= 1; len >>= 1) {
+        for (int64_t n = len + threadIdx.x; n < 2 * len; n += blockDim.x) mtree[n] = min(mtree[2 * n], mtree[2 * n + 1]);
+        __syncthreads();
+    }
+}
+
+// last position t <= r whose LCP is at most j (exists: LCP(0) = 0)
+__device__ inline int64_t last_at_most(const int32_t *mtree, int64_t mpad, int64_t r, int32_t j) {
+    int64_t n = mpad + r;
+    if (mtree[n] <= j) return r;
+    while (n > 1) {
+        if ((n & 1) && mtree[n - 1] <= j) { n -= 1; break; }   // the left neighbour's subtree holds one
+        n >>= 1;
+    }
+    while (n < mpad) n = mtree[2 * n + 1] <= j ? 2 * n + 1 : 2 * n;
+    return n - mpad;
+}
+
+__global__ void k_l_paths(int m, int64_t nnz, int64_t mpad, const int64_t *off, const int32_t *rank, const int32_t *lcp,
+                          const int64_t *base, const int32_t *mtree, int32_t *pn) {
+    for (int64_t k = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; k < nnz; k += (int64_t)gridDim.x * blockDim.x) {
+        // the request holding slot k: the last i with off[i] <= k
+        int lo = 0, hi = m - 1;
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (off[mid] <= k) lo = mid; else hi = mid - 1;
         }
+        const int64_t j = k - off[lo];
+        const int64_t s = rank[lo];
+        const int64_t t = j < lcp[s] ? last_at_most(mtree, mpad, s - 1, (int32_t)j) : s;
+        pn[k] = (int32_t)(base[t] + (j - lcp[t]));
     }
 }
 
@@ -587,11 +612,15 @@ int l_prepare(int m, int64_t n_chunks, int64_t nnz, const int64_t *w, const int6
     }
     MPT_HIP_TRY(hipGetLastError());
     if (paths) {
-        int32_t *pn = (int32_t *)(ws + L.pn), *cur = (int32_t *)(ws + L.cur);
+        int32_t *pn = (int32_t *)(ws + L.pn), *mtree = (int32_t *)(ws + L.mtree);
         int64_t *nw = (int64_t *)(ws + L.nw);
         LaunchScope ls("l_paths", (double)nnz, s);
         k_l_node_weights<<<grid_for(m, 256), 256, 0, s>>>(m, ord, off, seqs, w, lcp, base, nw);
-        k_l_paths<<<1, kWave, 0, s>>>(m, ord, off, lcp, base, pn, cur);
+        const int64_t sub = std::min<int64_t>(kTreeBlock, L.mpad);
+        k_l_mtree_low<<<(unsigned)(L.mpad / sub), 1024, 0, s>>>(m, L.mpad, lcp, mtree);
+        if (L.mpad > sub) k_l_mtree_top<<<1, 1024, 0, s>>>(L.mpad / sub, mtree);
+        if (nnz > 0)
+            k_l_paths<<<grid_for(nnz, 256), 256, 0, s>>>(m, nnz, L.mpad, off, rank, lcp, base, mtree, pn);
         MPT_HIP_TRY(hipGetLastError());
     }
     int64_t hv[2] = {0, 0};
