@@ -178,9 +178,20 @@ def test_retrieval_shape_seeds(seed):
     assert_same(inst, got, oracle.solve(inst))
 
 
-@pytest.mark.parametrize("seed", range(1, 6))
+@pytest.mark.parametrize("seed", range(1, 51))
 def test_tiny_shape_seeds(seed):
+    """Config 1's shape (m = 12, k = 4 of 64 chunks, w ~ U{1..32}), seeds
+    1..50: the plain path, whole tables and orders."""
     inst = wl.config(1, seed=seed)
+    got = gpu_run(inst)
+    assert_same(inst, got, oracle.solve(inst))
+
+
+@pytest.mark.parametrize("seed", range(1, 51))
+def test_config3_shape_seeds(seed):
+    """Config 3's shape (m = 20 retrieval requests, k = 10 of 2000 passages in
+    50 topics), seeds 1..50: the row-blocked path, whole tables and orders."""
+    inst = wl.config(3, seed=seed)
     got = gpu_run(inst)
     assert_same(inst, got, oracle.solve(inst))
 
