@@ -87,6 +87,23 @@ def test_cache_simulation_matches_oracle(name):
             assert g == oracle.lru_cache_cost(inst, lay, oracle.window_schedule(inst, lay, W), C), (lname, W, C)
 
 
+def test_cache_configurations_in_any_order():
+    """Configurations whose windows name the same schedule (0, -1, m and
+    past m are all the whole stream) interleaved with others and with
+    capacities in no order: every bill against the oracle's simulator."""
+    inst = wl.random_small(m=40, u=30, kmin=1, kmax=9, wmax=50, seed=17)
+    lay = oracle.greedy_solve(inst)["orders"]
+    mx = max_request(inst)
+    m = inst.m
+    windows = [5, -1, 0, m + 5, m, 5, 1, 7, 1, 0, 13, -7]
+    caps = [mx, 3 * mx, 0, mx // 2, 1 << 40, 2 * mx, mx, 5 * mx, 0, mx, 7, 4 * mx]
+    L = mpt.Layouts(inst, n_configs=len(windows))
+    got, tc = L.simulate(L.seqs(lay), windows, caps)
+    assert tc == oracle.trie_cost(inst, lay)
+    for W, C, g in zip(windows, caps, got):
+        assert g == oracle.lru_cache_cost(inst, lay, oracle.window_schedule(inst, lay, W), C), (W, C)
+
+
 def test_theorem7_on_gpu():
     """Theorem 7: in DFS order, one request's worth of capacity bills exactly
     the trie cost, for every layout; arrival order at that capacity does not."""
@@ -161,11 +178,11 @@ def test_error_codes():
     assert L.cost(L.seqs(inst.req_chunks)) == 4
 
 
-def test_cache_simulation_beyond_lds():
-    """m = 8192 requests: the trie has more nodes than the simulator keeps in
-    LDS (36K), so the latest-access table lives in the workspace. Sampled
-    configurations against the oracle, the whole grid against the
-    invariants."""
+def test_cache_simulation_at_m_8192():
+    """m = 8192 requests: a trie of more than 36K nodes and access logs of
+    65K entries (256 sorted blocks per schedule, reuse distances across
+    many of them). Sampled configurations against the oracle, the whole
+    grid against the invariants."""
     inst = wl.gen_retrieval(m=8192, u=24576, topics=256, k=8, seed=2)
     lay = np.asarray(inst.req_chunks, dtype=np.int32)
     unit = wl.from_sets(inst.requests(), [1] * inst.n_chunks, inst.n_chunks)
