@@ -609,10 +609,12 @@ __global__ __launch_bounds__(kChainThreads) void k_rac_chain(Rac R, int t0) {
 }
 
 // pi_i: walk from leaf i to the root, placing D(v) of every node on the
-// path right to left (the root's list comes first); one wave per request
+// path right to left (the root's list comes first); one wave per request.
+// The zero-gain merges (nodes m + chain_from and up) emit nothing and
+// every node above one of them is one of them, so a walk ends there.
 __global__ void k_g_orders(int m, int64_t nnz, const int64_t *req_off, const int32_t *node_parent,
                            const int32_t *dbuf, const int64_t *d_off, const int32_t *d_len, int32_t *order_chunks,
-                           GHeader *h) {
+                           int chain_from, GHeader *h) {
     const int lane = threadIdx.x & (kWave - 1);
     const int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / kWave;
     if (i >= m) return;
@@ -621,6 +623,7 @@ __global__ void k_g_orders(int m, int64_t nnz, const int64_t *req_off, const int
     int steps = 0;
     for (int v = (int)i; v >= 0 && steps < 2 * m; v = node_parent[v], ++steps) {
         if (v >= 2 * m - 1) { if (lane == 0) atomicOr(&h->err, GERR_INVALID); return; }
+        if (v >= m + chain_from) break;
         const int64_t len = d_len[v];
         if (len < 0 || end - len < begin || d_off[v] < 0 || d_off[v] + len > nnz) {
             if (lane == 0) atomicOr(&h->err, GERR_INVALID);
@@ -899,7 +902,7 @@ extern "C" int mpt_greedy_hierarchy(int m, int64_t n_chunks, int64_t nnz, const 
     if (order_chunks) {
         LaunchScope ls("g_orders", 4.0 * (double)nnz, s);
         k_g_orders<<<(m + 3) / 4, 4 * kWave, 0, s>>>(m, nnz, req_off, node_parent, R.dbuf, R.d_off, R.d_len,
-                                                     order_chunks, R.h);
+                                                     order_chunks, n_rec, R.h);
         MPT_HIP_TRY(hipGetLastError());
     }
     if ((rc = g_read_errors(R.h, s))) return rc;
