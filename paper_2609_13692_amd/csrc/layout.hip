@@ -439,6 +439,7 @@ __global__ void k_l_logs(int m, int n_cfg, int64_t nnz, const int32_t *sched, co
 // over a schedule's log bills all its capacities.
 
 constexpr int kStackBlock = 256;               // log entries per sorted block
+static_assert(kStackBlock == 256, "the lockstep searches of k_l_bill take 9 halvings");
 
 // sort keys of the access logs of schedules d0 .. d0 + nd - 1: (schedule,
 // node, log position); the padding sorts last
@@ -543,24 +544,61 @@ __global__ __launch_bounds__(kBillThreads) void k_l_bill(int64_t nnz, int64_t nb
         if (p >= 0) {
             const int64_t s = acc_start[base + e];
             dist = 0;
-            int64_t j = p + 1;
-            // entries up to the end of p's block, one by one
-            const int64_t first_full = (j + kStackBlock - 1) / kStackBlock * kStackBlock;
-            for (; j < min(s, first_full); ++j)
-                if (next[base + j] >= s) dist += accw[base + j];
-            // whole blocks: the prefix of the block with next >= s
-            for (; j + kStackBlock <= s; j += kStackBlock) {
-                const int64_t bo = (int64_t)d * nblk * kStackBlock + j;
-                int lo = 0, hi = kStackBlock;              // first sorted entry with next < s
-                while (lo < hi) {
-                    const int mid = (lo + hi) >> 1;
-                    if (bnext[bo + mid] >= s) lo = mid + 1; else hi = mid;
+            // a range of single entries, 8 loads in flight at a time
+            auto singles = [&](int64_t from, int64_t to) {
+                for (int64_t q = from; q < to; q += 8) {
+                    int32_t nx[8];
+                    int64_t wq[8];
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) {
+                        nx[u] = q + u < to ? next[base + q + u] : -1;
+                        wq[u] = q + u < to ? accw[base + q + u] : 0;
+                    }
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) dist += nx[u] >= s ? wq[u] : 0;
                 }
-                if (lo > 0) dist += bsum[bo + lo - 1];
+            };
+            const int64_t j0 = p + 1;
+            const int64_t first_full = (j0 + kStackBlock - 1) / kStackBlock * kStackBlock;
+            const int64_t end_full = s / kStackBlock * kStackBlock;
+            if (first_full >= end_full) {
+                singles(j0, s);                          // no whole block in between
+            } else {
+                singles(j0, first_full);
+                singles(end_full, s);
+                // whole blocks: the prefix of each block with next >= s, four
+                // binary searches in lockstep
+                const int64_t bbase = (int64_t)d * nblk * kStackBlock;
+                int64_t j = first_full;
+                for (; j + 4 * kStackBlock <= end_full; j += 4 * kStackBlock) {
+                    int lo[4] = {0, 0, 0, 0}, hi[4] = {kStackBlock, kStackBlock, kStackBlock, kStackBlock};
+                    for (int it = 0; it <= 8; ++it) {           // log2(kStackBlock) + 1 halvings
+                        int32_t v[4];
+#pragma unroll
+                        for (int u = 0; u < 4; ++u) {
+                            const int mid = (lo[u] + hi[u]) >> 1;
+                            v[u] = lo[u] < hi[u] ? bnext[bbase + j + u * kStackBlock + mid] : 0;
+                        }
+#pragma unroll
+                        for (int u = 0; u < 4; ++u) {
+                            if (lo[u] >= hi[u]) continue;
+                            const int mid = (lo[u] + hi[u]) >> 1;
+                            if (v[u] >= s) lo[u] = mid + 1; else hi[u] = mid;
+                        }
+                    }
+#pragma unroll
+                    for (int u = 0; u < 4; ++u)
+                        if (lo[u] > 0) dist += bsum[bbase + j + u * kStackBlock + lo[u] - 1];
+                }
+                for (; j < end_full; j += kStackBlock) {
+                    int lo = 0, hi = kStackBlock;              // first sorted entry with next < s
+                    while (lo < hi) {
+                        const int mid = (lo + hi) >> 1;
+                        if (bnext[bbase + j + mid] >= s) lo = mid + 1; else hi = mid;
+                    }
+                    if (lo > 0) dist += bsum[bbase + j + lo - 1];
+                }
             }
-            // the rest, one by one
-            for (; j < s; ++j)
-                if (next[base + j] >= s) dist += accw[base + j];
         }
         for (int k = 0; k < nc; ++k) {
             const bool miss = dist < 0 || dist + w > caps[cfg_list[c0 + k]];
