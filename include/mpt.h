@@ -285,8 +285,9 @@ size_t mpt_greedy_workspace_bytes(int m, int64_t n_chunks, int64_t nnz);
  * values of the greedy's first merge (Sections 6.2-6.3).
  *   P [m*m]         out: int64, row-major, device
  *   request_total   HOST out, nullable: sum_i w(R_i)
- * Cost: one scatter per pair of requests sharing a chunk, i.e.
- * sum_x |S_x|^2 atomic adds -- meant for sparse demand (small |S_x|).
+ * Cost: one write of P plus sum_x |S_x|^2 additions, in on-chip memory,
+ * one per pair of requests sharing a chunk -- meant for sparse demand
+ * (small |S_x|).
  * Synchronises `stream` (twice) to report validation errors.
  */
 int mpt_pair_weights(int m, int64_t n_chunks, int64_t nnz, const int64_t *chunk_w,

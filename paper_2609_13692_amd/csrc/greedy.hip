@@ -220,29 +220,35 @@ __global__ void k_g_dem_off(int64_t n_chunks, int64_t nnz, const uint64_t *keys2
     }
 }
 
-__global__ void k_g_fill64(int64_t *p, int64_t n, int64_t v) {
-    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) p[i] = v;
-}
-
-// slot e = (chunk x, request a) adds w(x) to P[a][a] and to P[a][b], P[b][a]
-// for every later request b of S_x; one wave per slot, so a long demand
-// list is spread over 64 lanes
-__global__ void k_g_pairs(int m, int64_t nnz, const uint64_t *keys2, const int32_t *dem, const int64_t *dem_off,
-                          const int64_t *w, unsigned long long *P) {
-    const int lane = threadIdx.x & (kWave - 1);
-    const int64_t waves = (int64_t)gridDim.x * blockDim.x / kWave;
-    for (int64_t e = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / kWave; e < nnz; e += waves) {
-        const int64_t x = (int64_t)(keys2[e] >> 32);
+// row a of P, a tile of kPairTile columns per workgroup: every chunk x of
+// R_a adds w(x) to the columns of the requests in its demand list S_x (one
+// wave per chunk, lanes along S_x), summed in LDS and written once. The
+// row's tiles cover every column, so P needs no zeroing.
+constexpr int kPairTile = 4096;
+constexpr int kPairThreads = 256;
+__global__ __launch_bounds__(kPairThreads) void k_g_pair_rows(int m, const int32_t *sig, const int64_t *req_off,
+                                                              const int32_t *dem, const int64_t *dem_off,
+                                                              const int64_t *w, int64_t *P) {
+    __shared__ unsigned long long row[kPairTile];
+    const int tiles = (m + kPairTile - 1) / kPairTile;
+    const int64_t a = blockIdx.x / tiles;
+    const int c0 = (int)(blockIdx.x % tiles) * kPairTile;
+    const int width = min(kPairTile, m - c0);
+    for (int j = threadIdx.x; j < width; j += kPairThreads) row[j] = 0ull;
+    __syncthreads();
+    const int lane = threadIdx.x & (kWave - 1), wid = threadIdx.x / kWave;
+    const int64_t s0 = req_off[a], s1 = req_off[a + 1];
+    for (int64_t q = s0 + wid; q < s1; q += kPairThreads / kWave) {
+        const int32_t x = sig[q];
         const unsigned long long wx = (unsigned long long)w[x];
-        const size_t a = (size_t)dem[e];
-        if (lane == 0) atomicAdd(&P[a * m + a], wx);
-        const int64_t end = dem_off[x + 1];
-        for (int64_t f = e + 1 + lane; f < end; f += kWave) {
-            const size_t b = (size_t)dem[f];
-            atomicAdd(&P[a * m + b], wx);
-            atomicAdd(&P[b * m + a], wx);
+        for (int64_t f = dem_off[x] + lane; f < dem_off[x + 1]; f += kWave) {
+            const int b = dem[f] - c0;
+            if (b >= 0 && b < width) atomicAdd(&row[b], wx);
         }
     }
+    __syncthreads();
+    int64_t *out = P + a * (int64_t)m + c0;
+    for (int j = threadIdx.x; j < width; j += kPairThreads) out[j] = (int64_t)row[j];
 }
 
 // ---------------------------------------------------------------------------
@@ -780,10 +786,8 @@ int g_prepare(int m, int64_t n_chunks, int64_t nnz, const int64_t *chunk_w, cons
     if (P) {
         const int64_t mm = (int64_t)m * m;
         LaunchScope ls("g_pairs", 8.0 * (double)mm, s);
-        k_g_fill64<<<grid_for(mm, 256, 16384), 256, 0, s>>>(P, mm, 0);
-        if (nnz > 0)
-            k_g_pairs<<<grid_for(nnz * kWave, 256, 16384), 256, 0, s>>>(m, nnz, keys2, dem, dem_off, chunk_w,
-                                                                         (unsigned long long *)P);
+        const int64_t blocks = (int64_t)m * ((m + kPairTile - 1) / kPairTile);
+        k_g_pair_rows<<<(unsigned)blocks, kPairThreads, 0, s>>>(m, sig, req_off, dem, dem_off, chunk_w, P);
         MPT_HIP_TRY(hipGetLastError());
     }
     return MPT_OK;
