@@ -1590,8 +1590,8 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
             bh1[x] = o1[x] < i1[x] ? ah_prev : bh1[x];
         }
     };
-    // pair t of the chunk runs on buffer (t - t0) & 1 while the rows of
-    // pair t + 1 are copied into the other one
+    // (wide keys) pair t of the chunk runs on buffer (t - t0) & 1 while the
+    // rows of pair t + 1 are copied into the other one
     auto pair = [&](auto cur_c, uint32_t t) {
         constexpr int CUR = decltype(cur_c)::value;
         // (wide keys track nothing: one set, updated in place)
@@ -1603,11 +1603,9 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
         const uint32_t an = lowh | (((ah | ~rest) + 1u) & rest);    // next A_H holding lowbit(S_H)
         if (t + 1 < t1) copy_pair(CUR ^ 1, an);
         ah = an;
-        // The buffers' LDS offsets (multiples of the row size). Narrow rows
-        // lie in the first 64 KiB, so their bases are compile-time constants
-        // that the reads take as immediate offsets. Wide buffer 1 lies beyond
-        // the 16-bit immediates, so wide bases are kept opaque to the
-        // compiler and added once per address.
+        // The buffers' LDS offsets (multiples of the row size). Wide buffer 1
+        // lies beyond the 16-bit immediates, so wide bases are kept opaque to
+        // the compiler and added once per address.
         typedef __attribute__((address_space(3))) const KI lds_k;
         uint32_t oa = (uint32_t)(uintptr_t)(lds_k *)buf(CUR, 0);
         uint32_t ob = (uint32_t)(uintptr_t)(lds_k *)buf(CUR, 1);
@@ -1643,10 +1641,75 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
         }
         ah_prev = ah_cur;
     };
-    if (t0 < t1) copy_pair(0, ah);
-    for (uint32_t t = t0; t < t1; t += 2) {
-        pair(std::integral_constant<int, 0>{}, t);
-        if (t + 1 < t1) pair(std::integral_constant<int, 1>{}, t + 1);
+    if constexpr (NARROW) {
+        // Narrow keys run the pairs in sets of two: the four narrow row pairs
+        // fill the 128 KiB of row buffers (set 0 in slots 0, 1, set 1 in
+        // slots 2, 3), so one barrier and one batch of copies serve two
+        // pairs; the copies of the next set are awaited after the first two
+        // steps of the set's first pair, and the rest runs with none in
+        // flight. Set 1 lies 64 KiB up, past the reads' 16-bit immediate
+        // offsets: its pairs add 64 KiB to the items' offset registers and
+        // take set 0's immediates.
+        auto adv = [&](uint32_t x) __attribute__((always_inline)) { return lowh | (((x | ~rest) + 1u) & rest); };
+        uint32_t ah_copy = ah, ah_run = ah;
+        auto copy_set = [&](int S, uint32_t t) __attribute__((always_inline)) {
+            if (t < t1) { copy_pair(2 * S, ah_copy); ah_copy = adv(ah_copy); }
+            if (t + 1 < t1) { copy_pair(2 * S + 1, ah_copy); ah_copy = adv(ah_copy); }
+        };
+        auto pair_n = [&](auto cur_c, uint32_t t) __attribute__((always_inline)) {
+            constexpr int CUR = decltype(cur_c)::value;
+            KI *in0 = CUR ? bq0 : bp0, *in1 = CUR ? bq1 : bp1;
+            KI *out0 = CUR ? bp0 : bq0, *out1 = CUR ? bp1 : bq1;
+            const uint32_t ah_cur = ah_run;
+            ah_run = adv(ah_run);
+            typedef __attribute__((address_space(3))) const KI lds_k;
+            const uint32_t oa = (uint32_t)(uintptr_t)(lds_k *)buf(CUR, 0);
+            const uint32_t ob = (uint32_t)(uintptr_t)(lds_k *)buf(CUR, 1);
+            if (has_item) {
+                if (t > t0) track(in0, in1, out0, out1);
+                auto two = [&](int i, const KI *i0, const KI *i1) __attribute__((always_inline)) {
+                    const uint32_t fa = oa_item[i], fb = ob_item[i];
+                    cross_step<KI>(oa + fa, ob + fb, i0, i1, out0, out1);
+                    cross_step<KI>(oa + (fa ^ low_off), ob + (fb ^ low_off), out0, out1, out0, out1);
+                };
+                two(0, in0, in1);
+                if constexpr (CUR == 0) copies_done();
+                if (cnt > 2) two(1, out0, out1);
+                if (cnt > 4) two(2, out0, out1);
+                if (cnt > 6) two(3, out0, out1);
+            }
+            ah_prev = ah_cur;
+        };
+        auto shift = [&](uint32_t d) __attribute__((always_inline)) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                oa_item[i] += d;
+                ob_item[i] += d;
+                // opaque: the old values die here instead of being kept for after set 1
+                asm volatile("" : "+v"(oa_item[i]), "+v"(ob_item[i]));
+            }
+        };
+        auto set_run = [&](auto s_c, uint32_t t) __attribute__((always_inline)) {
+            constexpr int S = decltype(s_c)::value;
+            copies_done();
+            lds_barrier();     // rows of this set in place; the previous set done with the other one
+            copy_set(S ^ 1, t + 2);
+            if constexpr (S == 1) shift(0x10000u);
+            pair_n(std::integral_constant<int, 0>{}, t);
+            if (t + 1 < t1) pair_n(std::integral_constant<int, 1>{}, t + 1);
+            if constexpr (S == 1) shift(0u - 0x10000u);
+        };
+        if (t0 < t1) copy_set(0, t0);
+        for (uint32_t t = t0; t < t1; t += 4) {
+            set_run(std::integral_constant<int, 0>{}, t);
+            if (t + 2 < t1) set_run(std::integral_constant<int, 1>{}, t + 2);
+        }
+    } else {
+        if (t0 < t1) copy_pair(0, ah);
+        for (uint32_t t = t0; t < t1; t += 2) {
+            pair(std::integral_constant<int, 0>{}, t);
+            if (t + 1 < t1) pair(std::integral_constant<int, 1>{}, t + 1);
+        }
     }
     if (has_item) {
         // the last pair's tracking; an odd number of pairs leaves the keys in

@@ -92,10 +92,13 @@ def test_context_on_the_largest_workload():
     assert got["orders"].tolist() == g["orders"]
 
 
-# chunk sizes: 1 pair per workgroup (every level split to the limit), 3 and
-# 7 (chunk boundaries that cut the A_H order at odd places) and 1 << 20 (every
-# level in one chunk, rows finished in the cross-pair kernel)
-PLANS = [1, 3, 7, 1 << 20]
+# chunk sizes: 1 pair per workgroup (every level split to the limit), 2, 3, 5
+# and 7 (chunk boundaries that cut the A_H order at odd places; narrow keys run
+# pairs in sets of two on alternating buffers, so these end a chunk on a full
+# set, after one pair of the second set, after one pair of a reused first set
+# and after one pair of a reused second set) and 1 << 20 (every level in one
+# chunk, rows finished in the cross-pair kernel)
+PLANS = [1, 2, 3, 5, 7, 1 << 20]
 
 
 @pytest.mark.parametrize("idx", [3, 4])
