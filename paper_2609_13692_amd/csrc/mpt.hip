@@ -865,7 +865,123 @@ constexpr bool items_pair_up(const ThreadItems &t) {
     return true;
 }
 static_assert(items_pair_up(kTItems), "cross-pair items must pair up their submasks and cover each once");
-__constant__ ThreadItems c_titems = make_thread_items();
+__constant__ ThreadItems c_titems = kTItems;
+
+// The lanes whose items have one S2', for combining their best keys after
+// the pairs: the items of an S2' are handed out in one go, class by class,
+// so they sit in runs of adjacent lanes, at most two with this table.
+// Entry: first lane | count << 16 (count 0: no run).
+constexpr int kRuns = 2;
+struct ItemRuns { uint32_t r[1 << RL][kRuns]; bool ok; };
+constexpr ItemRuns make_item_runs(const ThreadItems &t) {
+    ItemRuns g{};
+    g.ok = true;
+    int n[1 << RL] = {};
+    for (int i = 0; i < THREADS; ++i) {
+        if (!(t.v[i] >> 31)) continue;
+        const int sp = (int)(t.v[i] & 0xffu);
+        if (n[sp] > 0) {
+            uint32_t &last = g.r[sp][n[sp] - 1];
+            if ((int)(last & 0xffffu) + (int)(last >> 16) == i) {
+                last += 1u << 16;
+                continue;
+            }
+        }
+        if (n[sp] == kRuns) {
+            g.ok = false;
+            return g;
+        }
+        g.r[sp][n[sp]++] = (uint32_t)i | (1u << 16);
+    }
+    return g;
+}
+constexpr ItemRuns kItemRuns = make_item_runs(kTItems);
+static_assert(kItemRuns.ok, "the lanes of one S2' form at most two runs");
+// the runs cover exactly the lanes with items, each S2' with at least one
+constexpr bool runs_cover(const ThreadItems &t, const ItemRuns &g) {
+    int owner[THREADS] = {};
+    for (int i = 0; i < THREADS; ++i) owner[i] = -1;
+    for (int sp = 0; sp < (1 << RL); ++sp) {
+        int lanes = 0;
+        for (int q = 0; q < kRuns; ++q)
+            for (int i = 0; i < (int)(g.r[sp][q] >> 16); ++i) {
+                const int l = (int)(g.r[sp][q] & 0xffffu) + i;
+                if (l >= THREADS || owner[l] != -1 || !(t.v[l] >> 31) || (int)(t.v[l] & 0xffu) != sp) return false;
+                owner[l] = sp;
+                ++lanes;
+            }
+        if (lanes == 0) return false;
+    }
+    for (int i = 0; i < THREADS; ++i)
+        if ((t.v[i] >> 31) && owner[i] == -1) return false;
+    return true;
+}
+static_assert(runs_cover(kTItems, kItemRuns), "every lane with an item is in one run of its S2'");
+__constant__ ItemRuns c_item_runs = kItemRuns;
+
+// The combining plan. Each 16-lane quarter of a wave takes four S2' in
+// turn, lane q the entry q of each (q < 8: entry q of block S2', else entry
+// q - 8 of block S2'|E), and reads the staged keys of the S2''s lanes. The
+// quarters of a wave step together, so a step costs its costliest S2' (one
+// read per lane of it): the S2' are grouped four to a step by decreasing
+// cost, and the groups go to the waves, four each, costliest first onto the
+// least loaded wave. Entry [wave][quarter]: the four S2' (8 bits each, step
+// j in bits 8j..8j+7) and, per step, their runs as first lane | count << 10
+// in 16 bits each.
+constexpr int kWaves = THREADS / kWave;
+static_assert((1 << RL) == kWaves * 4 * 4, "four steps of four quarters per wave cover every S2'");
+struct alignas(16) GatherSlot { uint32_t runs[4]; uint32_t s2; uint32_t pad[3]; };
+struct GatherPlan { GatherSlot s[kWaves][4]; bool ok; };
+constexpr GatherPlan make_gather_plan(const ItemRuns &g) {
+    GatherPlan plan{};
+    plan.ok = true;
+    int cost[1 << RL] = {};
+    int maxc = 0;
+    for (int sp = 0; sp < (1 << RL); ++sp) {
+        for (int q = 0; q < kRuns; ++q) cost[sp] += (int)(g.r[sp][q] >> 16);
+        maxc = cost[sp] > maxc ? cost[sp] : maxc;
+    }
+    int order[1 << RL] = {};
+    int n = 0;
+    for (int c = maxc; c >= 0; --c)
+        for (int sp = 0; sp < (1 << RL); ++sp)
+            if (cost[sp] == c) order[n++] = sp;
+    int load[kWaves] = {}, used[kWaves] = {};
+    for (int gi = 0; gi < (1 << RL) / 4; ++gi) {
+        int w = -1;
+        for (int x = 0; x < kWaves; ++x)
+            if (used[x] < 4 && (w < 0 || load[x] < load[w])) w = x;
+        for (int u = 0; u < 4; ++u) {
+            const int sp = order[4 * gi + u];
+            uint32_t word = 0;
+            for (int q = 0; q < kRuns; ++q) {
+                const uint32_t first = g.r[sp][q] & 0xffffu, cnt = g.r[sp][q] >> 16;
+                if (first >= 1024u || cnt >= 64u) plan.ok = false;
+                word |= (first | cnt << 10) << (16 * q);
+            }
+            plan.s[w][u].runs[used[w]] = word;
+            plan.s[w][u].s2 |= (uint32_t)sp << (8 * used[w]);
+        }
+        load[w] += cost[order[4 * gi]];
+        ++used[w];
+    }
+    return plan;
+}
+constexpr GatherPlan kGatherPlan = make_gather_plan(kItemRuns);
+static_assert(kRuns == 2 && THREADS <= 1024 && kGatherPlan.ok, "runs fit 16 bits each");
+constexpr bool gather_covers(const GatherPlan &plan) {
+    bool seen[1 << RL] = {};
+    for (int w = 0; w < kWaves; ++w)
+        for (int u = 0; u < 4; ++u)
+            for (int j = 0; j < 4; ++j) {
+                const int sp = (int)((plan.s[w][u].s2 >> (8 * j)) & 0xffu);
+                if (seen[sp]) return false;
+                seen[sp] = true;
+            }
+    return true;
+}
+static_assert(gather_covers(kGatherPlan), "every S2' is combined by one quarter of one wave");
+__constant__ GatherPlan c_gather = kGatherPlan;
 
 
 // Key arithmetic. A table entry carries the packed value v = C' or, tagged,
@@ -1069,51 +1185,36 @@ __device__ inline void conv_into(const K a[NB], const K b[NB], const K in[NB], K
     }
 }
 
-template <class K>
-__device__ inline void flush(const K best[NB], uint32_t s2, uint64_t *acc) {
-#pragma unroll
-    for (int x = 0; x < NB; ++x)
-        if (best[x] != Key<K>::none())
-            atomicMin((unsigned long long *)&acc[(s2 << CB) | x], (unsigned long long)Key<K>::bits(best[x]));
+// minimum of v over an aligned group of seg = 1, 2, 4, 8 or 16 lanes (every
+// lane of the group gets it): quad permutations, then the half-row mirror
+// that pairs the two quads of 8 lanes, then the row mirror that pairs the
+// two halves of 16
+__device__ inline uint32_t group_min32(uint32_t v, uint32_t seg) {
+    auto take = [&](uint32_t o) { v = o < v ? o : v; };
+    if (seg >= 2) take((uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false));    // quad_perm [1,0,3,2]
+    if (seg >= 4) take((uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false));    // quad_perm [2,3,0,1]
+    if (seg >= 8) take((uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x141, 0xF, 0xF, false));   // row_half_mirror
+    if (seg >= 16) take((uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x140, 0xF, 0xF, false));  // row_mirror
+    return v;
 }
 
-// narrow best keys of one output block, with the A_H of the pair that gave
-// each, as packed keys (cost << m | A_L << H | A_H) into the accumulator row
-template <class K>
-__device__ inline void flush_narrow(const uint32_t best[NB], const uint32_t bh[NB], uint32_t s2, int m,
-                                    uint64_t *acc) {
-    const int H = m - L;
-#pragma unroll
-    for (int x = 0; x < NB; ++x)
-        if (best[x] != Key<uint32_t>::none()) {
-            const uint64_t key = ((uint64_t)(best[x] >> L) << m) | ((uint64_t)(best[x] & (ROW - 1u)) << H) | bh[x];
-            atomicMin((unsigned long long *)&acc[(s2 << CB) | x], (unsigned long long)Key<K>::key_bits(key));
-        }
-}
-
-// DPP lane exchange of a 64-bit value inside rows of 8 lanes
-template <int CTRL>
-__device__ inline uint64_t dpp_get64(uint64_t b) {
-    const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)b, CTRL, 0xF, 0xF, false);
-    const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(b >> 32), CTRL, 0xF, 0xF, false);
-    return ((uint64_t)hi << 32) | lo;
-}
-
-// Flush of a self-pair item whose adjacent lanes share S2 in aligned groups
-// of seg = 1, 2, 4 or 8 lanes: min inside the group (quad permutations, then
-// the half-row mirror that pairs the two quads of 8 lanes) and one LDS
-// atomic per group and entry -- 64-bit LDS atomics are slow and contended.
+// Flush of best keys (one block of the output row) from lanes that share S2
+// in aligned groups of seg lanes: the group minimum of each entry's key bits
+// (the high words, then the low words among the lanes holding the least
+// high word) and one LDS atomic per group and entry -- 64-bit LDS atomics
+// are slow, and lanes that hit one address in the same instruction are
+// served one at a time.
 template <class K>
 __device__ inline void flush_group(const K best[NB], uint32_t s2, uint32_t seg, uint64_t *acc) {
     const uint32_t lane = threadIdx.x & (kWave - 1);
 #pragma unroll
     for (int x = 0; x < NB; ++x) {
-        uint64_t b = Key<K>::bits(best[x]);           // unsigned order = key order
-        if (seg >= 2) { const uint64_t o = dpp_get64<0xB1>(b); b = o < b ? o : b; }    // quad_perm [1,0,3,2]
-        if (seg >= 4) { const uint64_t o = dpp_get64<0x4E>(b); b = o < b ? o : b; }    // quad_perm [2,3,0,1]
-        if (seg >= 8) { const uint64_t o = dpp_get64<0x141>(b); b = o < b ? o : b; }   // row_half_mirror
-        if ((lane & (seg - 1)) == 0 && b != Key<K>::bits(Key<K>::none()))
-            atomicMin((unsigned long long *)&acc[(s2 << CB) | x], (unsigned long long)b);
+        const uint64_t b = Key<K>::bits(best[x]);     // unsigned order = key order
+        const uint32_t hi = group_min32((uint32_t)(b >> 32), seg);
+        const uint32_t lo = group_min32((uint32_t)(b >> 32) == hi ? (uint32_t)b : 0xffffffffu, seg);
+        const uint64_t g = ((uint64_t)hi << 32) | lo;
+        if ((lane & (seg - 1)) == 0 && g != Key<K>::bits(Key<K>::none()))
+            atomicMin((unsigned long long *)&acc[(s2 << CB) | x], (unsigned long long)g);
     }
 }
 
@@ -1510,7 +1611,6 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
     const uint32_t sh = unrank_colex(r, h, m - L);
     const uint32_t lowh = sh & (0u - sh);
     const uint32_t rest = sh ^ lowh;
-    for (int e = threadIdx.x; e < ROW; e += THREADS) s.acc[e] = ~0ull;
     const uint32_t t0 = j * per_chunk;
     const uint32_t t1 = min(n_pairs, t0 + per_chunk);
     uint32_t ah = t0 < t1 ? (lowh | deposit(t0, rest)) : 0u;
@@ -1711,28 +1811,79 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
             if (t + 1 < t1) pair(std::integral_constant<int, 1>{}, t + 1);
         }
     }
+    // The lanes' best keys are combined through LDS: every lane stages its
+    // 16 keys (8 of block S2', 8 of S2'|E) as accumulator key bits (~0 for
+    // none) in the row buffers, and each quarter of a wave then takes the
+    // minimum over the lanes of its S2' for each of the S2''s 16 entries
+    // (the gather plan). The minimum of the packed keys is the (cost, A)
+    // order, so this equals one atomic minimum per lane and entry, without
+    // the atomics. Key q of lane i sits at 16 i + (q ^ (i & 15)): a lane's
+    // 16 stores and a quarter's 16 reads of one lane fall in distinct banks.
+    uint64_t *stage = reinterpret_cast<uint64_t *>(&s.r[0][0][0]);
+    static_assert(2 * NB * THREADS * sizeof(uint64_t) <= sizeof(s.r), "the staged keys fit the row buffers");
+    const uint32_t quarter = (threadIdx.x / 16u) & 3u, q16 = threadIdx.x & 15u;
+    const GatherSlot &slot = c_gather.s[threadIdx.x / kWave][quarter];
+    const uint4 gruns = *reinterpret_cast<const uint4 *>(slot.runs);   // loaded ahead of the barriers
+    const uint32_t gs2 = slot.s2;
+    lds_barrier();     // every wave is done with the rows
     if (has_item) {
         // the last pair's tracking; an odd number of pairs leaves the keys in
         // the second set
         // (a branch, not a pointer select, keeps both sets in registers)
-        auto flush_set = [&](const KI *f0, const KI *f1) {
-            if constexpr (NARROW) {
-                flush_narrow<K>(f0, bh0, s2, m, s.acc);
-                flush_narrow<K>(f1, bh1, s2 | E, m, s.acc);
-            } else {
-                flush<K>(f0, s2, s.acc);
-                flush<K>(f1, s2 | E, s.acc);
+        auto stage_set = [&](const KI *f0, const KI *f1) {
+            const int H = m - L;
+            uint64_t *own = stage + 16u * threadIdx.x;
+            const uint32_t sw = threadIdx.x & 15u;
+#pragma unroll
+            for (int q = 0; q < 2 * NB; ++q) {
+                const KI b = q < NB ? f0[q] : f1[q - NB];
+                uint64_t v;
+                if constexpr (NARROW) {
+                    const uint32_t h = q < NB ? bh0[q] : bh1[q - NB];
+                    const uint64_t key = ((uint64_t)(b >> L) << m) | ((uint64_t)(b & (ROW - 1u)) << H) | h;
+                    v = b == Key<uint32_t>::none() ? ~0ull : Key<K>::key_bits(key);
+                } else {
+                    v = b == Key<K>::none() ? ~0ull : Key<K>::bits(b);
+                }
+                own[(uint32_t)q ^ sw] = v;
             }
         };
         if (NARROW && ((t1 - t0) & 1u)) {
             track(bq0, bq1, bp0, bp1);
-            flush_set(bq0, bq1);
+            stage_set(bq0, bq1);
         } else {
             if (NARROW && t1 > t0) track(bp0, bp1, bq0, bq1);
-            flush_set(bp0, bp1);
+            stage_set(bp0, bp1);
         }
     }
     lds_barrier();
+    {
+        const uint32_t gw[4] = {gruns.x, gruns.y, gruns.z, gruns.w};
+        auto m2 = [](uint64_t a, uint64_t b) { return a < b ? a : b; };
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+            uint64_t v = ~0ull;
+#pragma unroll
+            for (int r = 0; r < kRuns; ++r) {
+                const uint32_t word = gw[jj] >> (16 * r);
+                const uint32_t first = word & 1023u, n = (word >> 10) & 63u;
+                // four reads in flight; a lane past the run repeats its last
+                for (uint32_t i = 0; i < n; i += 4) {
+                    auto at = [&](uint32_t k) {
+                        const uint32_t ln = first + min(i + k, n - 1u);
+                        return stage[16u * ln + (q16 ^ (ln & 15u))];
+                    };
+                    const uint64_t o0 = at(0), o1 = at(1), o2 = at(2), o3 = at(3);
+                    v = m2(v, m2(m2(o0, o1), m2(o2, o3)));
+                }
+            }
+            const uint32_t sp = (gs2 >> (8 * jj)) & 0xffu;
+            const uint32_t e = ((q16 < NB ? sp : (sp | E)) << CB) | (q16 & (NB - 1u));
+            if (fused) s.acc[e] = v;
+            else partial[(size_t)bid * ROW + e] = v;
+        }
+    }
+    lds_barrier();     // the staged keys are read before the buffers are reused
     if (fused) {
         if constexpr (NARROW) {
             copy_row(buf(0, 1), Pn, 0u);
@@ -1745,9 +1896,6 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
         lds_barrier();
         if constexpr (NARROW) finalize_row_narrow<K>(m, sh, s.acc, buf(0, 0), buf(0, 1), buf(1, 0), Wr, Pt, Tn, Pn, Sr);
         else finalize_row<K, NARROW>(m, sh, s, buf(0, 0), buf(0, 1), Wr, Tt, Pt, Tn, Pn, Sr);
-    } else {
-        uint64_t *dst = partial + (size_t)bid * ROW;
-        for (int e = threadIdx.x; e < ROW; e += THREADS) dst[e] = s.acc[e];
     }
 }
 
