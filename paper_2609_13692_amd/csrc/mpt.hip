@@ -1142,6 +1142,34 @@ __device__ inline void copy_row(void *dst, const E *__restrict__ tab, uint32_t x
         __builtin_amdgcn_global_load_lds(src + p0 + lane, (lds_void *)((char *)dst + p0 * 16), 16, 0, 0);
     }
 }
+// copy_row of a narrow row, with each direct copy issued through inline
+// assembly so that the compiler's wait insertion does not see it: while it
+// knows of a pending direct copy into LDS, it makes every LDS read wait for
+// all earlier LDS reads. These copies are retired explicitly (copies_done,
+// then a workgroup barrier) before their rows are read, and they add only
+// to the in-order count of vector loads, so the compiler's own waits stay
+// correct (at worst longer). M0, which carries the LDS address of a copy,
+// is saved and restored around it.
+__device__ inline void copy_row_quiet(void *dst, const uint32_t *__restrict__ tab, uint32_t xh) {
+    constexpr int PIECES = ROW * (int)sizeof(uint32_t) / 16;
+    constexpr int PER_WAVE = PIECES / (THREADS / kWave);
+    static_assert(PER_WAVE % kWave == 0, "whole wave copies");
+    const int w = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
+    const int lane = (int)(threadIdx.x & (kWave - 1));
+    const uint4 *src = reinterpret_cast<const uint4 *>(tab + ((size_t)xh << L));
+    typedef __attribute__((address_space(3))) char lds_c;
+    const uint32_t base = (uint32_t)(uintptr_t)(lds_c *)dst;
+#pragma unroll
+    for (int i = 0; i < PER_WAVE / kWave; ++i) {
+        const int p0 = w * PER_WAVE + i * kWave;
+        const uint32_t at = base + (uint32_t)p0 * 16u;     // the wave's 1 KiB of LDS
+        uint32_t saved;
+        asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %2, off\n\ts_nop 0\n\ts_mov_b32 m0, %0"
+                     : "=&s"(saved)
+                     : "s"(at), "v"(src + p0 + lane)
+                     : "memory");
+    }
+}
 // vmcnt(0), expcnt and lgkmcnt untouched (gfx9 encoding). The builtin, not
 // inline asm, so that the compiler's wait insertion sees the copies retire:
 // a pending direct-to-LDS copy (a flat-encoded instruction) makes it treat
@@ -1670,8 +1698,8 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
     };
     auto copy_pair = [&](int b, uint32_t a_h) {
         if constexpr (NARROW) {
-            copy_row(buf(b, 0), Tn, a_h);
-            copy_row(buf(b, 1), Pn, sh ^ a_h);
+            copy_row_quiet(buf(b, 0), Tn, a_h);
+            copy_row_quiet(buf(b, 1), Pn, sh ^ a_h);
         } else {
             copy_row(buf(b, 0), Tt, a_h);
             copy_row(buf(b, 1), Pt, sh ^ a_h);
@@ -1745,9 +1773,9 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
         // Narrow keys run the pairs in sets of two: the four narrow row pairs
         // fill the 128 KiB of row buffers (set 0 in slots 0, 1, set 1 in
         // slots 2, 3), so one barrier and one batch of copies serve two
-        // pairs; the copies of the next set are awaited after the first two
-        // steps of the set's first pair, and the rest runs with none in
-        // flight. Set 1 lies 64 KiB up, past the reads' 16-bit immediate
+        // pairs; the copies of the next set (unseen by the compiler's wait
+        // insertion) stay in flight for the whole set and are awaited when
+        // the next set starts. Set 1 lies 64 KiB up, past the reads' 16-bit immediate
         // offsets: its pairs add 64 KiB to the items' offset registers and
         // take set 0's immediates.
         auto adv = [&](uint32_t x) __attribute__((always_inline)) { return lowh | (((x | ~rest) + 1u) & rest); };
@@ -1773,7 +1801,6 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
                     cross_step<KI>(oa + (fa ^ low_off), ob + (fb ^ low_off), out0, out1, out0, out1);
                 };
                 two(0, in0, in1);
-                if constexpr (CUR == 0) copies_done();
                 if (cnt > 2) two(1, out0, out1);
                 if (cnt > 4) two(2, out0, out1);
                 if (cnt > 6) two(3, out0, out1);
