@@ -1274,62 +1274,17 @@ __device__ inline void run_item(uint32_t item, const K *rA, const K *rB, uint64_
     flush_group<K>(best, s2, chunks < 8u ? chunks : 8u, acc);
 }
 
-// run_item on narrow rows: rA is narrow row S_H (tagged), rB narrow row 0
-// (plain). Every candidate has A_H = S_H, so the 32-bit key order is the
-// (cost, A) order; the group minimum goes to the accumulator as the packed
-// key with A_H = S_H.
+// Complete row S_H (non-empty) on 64-bit keys (narrow rows have
+// finalize_row_narrow). s.acc holds the best cross-pair key bits (or ~0);
+// rS receives row S_H (tagged), r0 holds row 0 (plain), both in LDS. Writes
+// the row to the plain and the tagged table and its splits to Sr (row-major,
+// mask order inside a row).
 template <class K>
-__device__ inline void run_item_narrow(uint32_t item, const uint32_t *rA, const uint32_t *rB, uint64_t *acc,
-                                       uint32_t sh, int m) {
-    const uint32_t s2 = item & 0xffffu;
-    const int k = __popc(s2);
-    const int tb = (int)((item >> 28) & 7u);
-    const uint32_t cnt = 1u << tb;
-    const uint32_t slot_s2 = slot_of(s2);
-    uint32_t a2 = (item >> 16) & 0xfffu;
-    uint32_t best[NB];
-#pragma unroll
-    for (int x = 0; x < NB; ++x) best[x] = Key<uint32_t>::none();
-    for (uint32_t i = 0; i < cnt; ++i) {
-        if (a2 != s2) {
-            const uint32_t sa = slot_of(a2), sb = slot_s2 ^ sa;
-            uint32_t a[NB], b[NB];
-            load_blk(rA, sa, a);
-            load_blk(rB, sb, b);
-            conv_full<uint32_t>(a, b, best);
-        }
-        a2 = ((a2 | ~s2) + 1u) & s2;
-    }
-    const uint32_t chunks = 1u << (k - tb);
-    const uint32_t seg = chunks < 8u ? chunks : 8u;
-    const uint32_t lane = threadIdx.x & (kWave - 1);
-    const int H = m - L;
-#pragma unroll
-    for (int x = 0; x < NB; ++x) {
-        uint32_t b = best[x];
-        if (seg >= 2) { const uint32_t o = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)b, 0xB1, 0xF, 0xF, false); b = o < b ? o : b; }
-        if (seg >= 4) { const uint32_t o = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)b, 0x4E, 0xF, 0xF, false); b = o < b ? o : b; }
-        if (seg >= 8) { const uint32_t o = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)b, 0x141, 0xF, 0xF, false); b = o < b ? o : b; }
-        if ((lane & (seg - 1)) == 0 && b != Key<uint32_t>::none()) {
-            const uint64_t key = ((uint64_t)(b >> L) << m) | ((uint64_t)(b & (ROW - 1u)) << H) | sh;
-            atomicMin((unsigned long long *)&acc[(s2 << CB) | x], (unsigned long long)Key<K>::key_bits(key));
-        }
-    }
-}
-
-// Complete row S_H (non-empty). s.acc holds the best cross-pair key bits (or
-// ~0); rS receives row S_H (tagged), r0 holds row 0 (plain), both in LDS
-// and, with NARROW, both narrow. Writes the row to the plain table, to the
-// tagged one (NARROW: to the two narrow tables instead) and its splits to Sr
-// (row-major, mask order inside a row).
-template <class K, bool NARROW>
-__device__ __attribute__((always_inline)) inline void finalize_row(int m, uint32_t sh, Lds<K> &s, void *rS_,
-                                                                   const void *r0_,
+__device__ __attribute__((always_inline)) inline void finalize_row(int m, uint32_t sh, Lds<K> &s, K *rS,
+                                                                   const K *r0,
                                                                    const int64_t *__restrict__ Wr,
                                                                    uint64_t *__restrict__ Tt,
                                                                    uint64_t *__restrict__ Pt,
-                                                                   uint32_t *__restrict__ Tn,
-                                                                   uint32_t *__restrict__ Pn,
                                                                    uint32_t *__restrict__ Sr) {
     const int H = m - L;
     const uint32_t row = sh << L;
@@ -1345,15 +1300,10 @@ __device__ __attribute__((always_inline)) inline void finalize_row(int m, uint32
         return bi < c_blocks.end[k] ? (uint32_t)c_blocks.v[bi] | 0x10000u : 0u;
     };
     uint32_t item = level_item(0), blk = level_blk(0);
-    K *rS = (K *)rS_;
-    const K *r0 = (const K *)r0_;
-    uint32_t *rSn = (uint32_t *)rS_;
-    const uint32_t *r0n = (const uint32_t *)r0_;
     // block 0 of row 0, plain: C'(X1 << H) for every low part X1
     uint64_t b0[NB];
 #pragma unroll
-    for (int x = 0; x < NB; ++x)
-        b0[x] = NARROW ? (uint64_t)(r0n[npos(0u, x)] >> L) << m : Key<K>::entry_value(r0[lpos(0u, x)]);
+    for (int x = 0; x < NB; ++x) b0[x] = Key<K>::entry_value(r0[lpos(0u, x)]);
     for (int k = 0; k <= R2; ++k) {
         const uint32_t item_next = k < R2 ? level_item(k + 1) : 0u;
         const uint32_t blk_next = k < R2 ? level_blk(k + 1) : 0u;
@@ -1365,10 +1315,7 @@ __device__ __attribute__((always_inline)) inline void finalize_row(int m, uint32
             for (int x = 0; x < NB; ++x) wv[x] = wp[x];
         }
         // A2 a proper submask of S2
-        if (item) {
-            if constexpr (NARROW) run_item_narrow<K>(item, rSn, r0n, s.acc, sh, m);
-            else run_item<K>(item, rS, r0, s.acc);
-        }
+        if (item) run_item<K>(item, rS, r0, s.acc);
         lds_barrier();
         // A2 = S2: in-block pairs, one thread per block of this level; A =
         // (S_H, S2, A1) holds lowbit(S), B = (0, 0, S1 ^ A1) is in block 0
@@ -1409,28 +1356,10 @@ __device__ __attribute__((always_inline)) inline void finalize_row(int m, uint32
 #pragma unroll
             for (int x = 0; x < NB; ++x) {
                 const uint64_t tagged = out[x] | base | ((uint32_t)x << H);
-                if (!NARROW) {
-                    rS[lpos(sl, x)] = Key<K>::entry(tagged);
-                    Tt[row + lpos(sl, x)] = Key<K>::store(tagged);
-                }
+                rS[lpos(sl, x)] = Key<K>::entry(tagged);
+                Tt[row + lpos(sl, x)] = Key<K>::store(tagged);
                 Pt[row + lpos(sl, x)] = Key<K>::store(out[x]);
                 Sr[row | (s2 << CB) | (uint32_t)x] = sp[x];
-            }
-            if (NARROW) {
-                // C(X) << L, and tagged with X_L = S2 << CB | X1
-                uint32_t pn[NB];
-#pragma unroll
-                for (int x = 0; x < NB; ++x) pn[x] = (uint32_t)(out[x] >> m) << L;
-                const uint32_t tag = s2 << CB;
-#pragma unroll
-                for (int q = 0; q < NB / 4; ++q) {
-                    const uint32_t at = row + npos(sl, 4 * q);
-                    *reinterpret_cast<uint4 *>(Pn + at) = make_uint4(pn[4 * q], pn[4 * q + 1], pn[4 * q + 2], pn[4 * q + 3]);
-                    const uint4 tv = make_uint4(pn[4 * q] | tag | (4u * q), pn[4 * q + 1] | tag | (4u * q + 1u),
-                                                pn[4 * q + 2] | tag | (4u * q + 2u), pn[4 * q + 3] | tag | (4u * q + 3u));
-                    *reinterpret_cast<uint4 *>(Tn + at) = tv;
-                    *reinterpret_cast<uint4 *>(rSn + npos(sl, 4 * q)) = tv;
-                }
             }
         }
         lds_barrier();
@@ -1439,7 +1368,7 @@ __device__ __attribute__((always_inline)) inline void finalize_row(int m, uint32
     }
 }
 
-// One self-pair item (as run_item_narrow) whose group minimum goes to the
+// One self-pair item (as run_item, on narrow rows) whose group minimum goes to the
 // narrow self-pair minima sacc (32-bit LDS atomics): every candidate of the
 // self pair has A_H = S_H, so the 32-bit key order is the (cost, A) order.
 __device__ inline void run_item_self(uint32_t item, const uint32_t *rA, const uint32_t *rB, uint32_t *sacc) {
@@ -1922,7 +1851,7 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
         copies_done();
         lds_barrier();
         if constexpr (NARROW) finalize_row_narrow<K>(m, sh, s.acc, buf(0, 0), buf(0, 1), buf(1, 0), Wr, Pt, Tn, Pn, Sr);
-        else finalize_row<K, NARROW>(m, sh, s, buf(0, 0), buf(0, 1), Wr, Tt, Pt, Tn, Pn, Sr);
+        else finalize_row<K>(m, sh, s, s.r[0][0], s.r[0][1], Wr, Tt, Pt, Sr);
     }
 }
 
@@ -1968,7 +1897,7 @@ __global__ __launch_bounds__(THREADS) void k_rb_final(int m, int h, uint32_t chu
     copies_done();
     lds_barrier();
     if constexpr (NARROW) finalize_row_narrow<K>(m, sh, s.acc, nr, nr + ROW, nr + 2 * ROW, Wr, Pt, Tn, Pn, Sr);
-    else finalize_row<K, NARROW>(m, sh, s, s.r[0][0], s.r[0][1], Wr, Tt, Pt, Tn, Pn, Sr);
+    else finalize_row<K>(m, sh, s, s.r[0][0], s.r[0][1], Wr, Tt, Pt, Sr);
 }
 
 // the in-row masks grouped by popcount, for the row-0 DP
