@@ -1142,7 +1142,7 @@ __device__ inline void copy_row(void *dst, const E *__restrict__ tab, uint32_t x
         __builtin_amdgcn_global_load_lds(src + p0 + lane, (lds_void *)((char *)dst + p0 * 16), 16, 0, 0);
     }
 }
-// copy_row of a narrow row, with each direct copy issued through inline
+// copy_row, with each direct copy issued through inline
 // assembly so that the compiler's wait insertion does not see it: while it
 // knows of a pending direct copy into LDS, it makes every LDS read wait for
 // all earlier LDS reads. These copies are retired explicitly (copies_done,
@@ -1150,8 +1150,9 @@ __device__ inline void copy_row(void *dst, const E *__restrict__ tab, uint32_t x
 // to the in-order count of vector loads, so the compiler's own waits stay
 // correct (at worst longer). M0, which carries the LDS address of a copy,
 // is saved and restored around it.
-__device__ inline void copy_row_quiet(void *dst, const uint32_t *__restrict__ tab, uint32_t xh) {
-    constexpr int PIECES = ROW * (int)sizeof(uint32_t) / 16;
+template <class E>
+__device__ inline void copy_row_quiet(void *dst, const E *__restrict__ tab, uint32_t xh) {
+    constexpr int PIECES = ROW * (int)sizeof(E) / 16;
     constexpr int PER_WAVE = PIECES / (THREADS / kWave);
     static_assert(PER_WAVE % kWave == 0, "whole wave copies");
     const int w = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
@@ -1630,8 +1631,8 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
             copy_row_quiet(buf(b, 0), Tn, a_h);
             copy_row_quiet(buf(b, 1), Pn, sh ^ a_h);
         } else {
-            copy_row(buf(b, 0), Tt, a_h);
-            copy_row(buf(b, 1), Pt, sh ^ a_h);
+            copy_row_quiet(buf(b, 0), Tt, a_h);
+            copy_row_quiet(buf(b, 1), Pt, sh ^ a_h);
         }
     };
     // A_H tracking of a finished pair (narrow keys): a key the pair lowered
@@ -1683,11 +1684,10 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
                 cross_step<KI>(oa + fa, ob + fb, i0, i1, out0, out1);
                 cross_step<KI>(oa + (fa ^ low_off), ob + (fb ^ low_off), out0, out1, out0, out1);
             };
-            // the next pair's copies land while the first two steps run;
-            // retired before the rest, they leave the later LDS reads free to
-            // wait only for what each use needs
+            // (the next pair's copies, unseen by the compiler's wait
+            // insertion, land while this pair runs and are awaited when the
+            // next pair starts)
             two(0, in0, in1);
-            copies_done();
             if constexpr (NARROW) {
                 if (cnt > 2) two(1, out0, out1);
                 if (cnt > 4) two(2, out0, out1);
