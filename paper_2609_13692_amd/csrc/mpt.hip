@@ -1553,24 +1553,47 @@ __device__ __attribute__((always_inline)) inline void cross_step(uint32_t off_a,
     if (!std::is_same<KI, uint32_t>::value) __builtin_amdgcn_sched_barrier(0);
 }
 
-// cross pairs of one (S_H, chunk); fused = finish the row in place. NARROW:
-// the pairs run on the narrow tables (Tn tagged, Pn plain), two buffers of
-// 16 KiB rows at the start of the wide rows' space.
+// Cross pairs of one (S_H, chunk). The level's rows (colex ranks) come in
+// two parts: the first head_rows rows in chunks of per_chunk pairs (one
+// chunk, with fused set: the row is finished in place), then the other rows
+// in tail_chunks chunks of tail_per_chunk pairs, so that the level's last
+// round of workgroups is filled with short ones. The head's workgroups come
+// first in launch order. Chunk partials: head chunk b of the launch at slot
+// b, tail chunk b' at slot tail_base + b'. NARROW: the pairs run on the
+// narrow tables (Tn tagged, Pn plain), in the wide rows' space.
 template <class K, bool NARROW>
 __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_pairs, uint32_t chunks,
-                                                      uint32_t per_chunk, int fused, const int64_t *__restrict__ Wr,
+                                                      uint32_t per_chunk, int fused, uint32_t head_rows,
+                                                      uint32_t tail_chunks, uint32_t tail_per_chunk, uint32_t tail_base,
+                                                      const int64_t *__restrict__ Wr,
                                                       uint64_t *__restrict__ Tt, uint64_t *__restrict__ Pt,
                                                       uint32_t *__restrict__ Tn, uint32_t *__restrict__ Pn,
                                                       uint32_t *__restrict__ Sr, uint64_t *__restrict__ partial) {
     typedef typename std::conditional<NARROW, uint32_t, K>::type KI;
     __shared__ Lds<K> s;
-    const uint32_t bid = xcd_block(blockIdx.x, gridDim.x);
-    const uint32_t r = bid / chunks, j = bid % chunks;
+    const uint32_t head_wgs = head_rows * chunks;
+    uint32_t r, j, pc, slot;
+    bool fz;
+    if (blockIdx.x < head_wgs) {
+        const uint32_t b = xcd_block(blockIdx.x, head_wgs);
+        r = b / chunks;
+        j = b % chunks;
+        pc = per_chunk;
+        fz = fused != 0;
+        slot = b;
+    } else {
+        const uint32_t b = xcd_block(blockIdx.x - head_wgs, gridDim.x - head_wgs);
+        r = head_rows + b / tail_chunks;
+        j = b % tail_chunks;
+        pc = tail_per_chunk;
+        fz = false;
+        slot = tail_base + b;
+    }
     const uint32_t sh = unrank_colex(r, h, m - L);
     const uint32_t lowh = sh & (0u - sh);
     const uint32_t rest = sh ^ lowh;
-    const uint32_t t0 = j * per_chunk;
-    const uint32_t t1 = min(n_pairs, t0 + per_chunk);
+    const uint32_t t0 = j * pc;
+    const uint32_t t1 = min(n_pairs, t0 + pc);
     uint32_t ah = t0 < t1 ? (lowh | deposit(t0, rest)) : 0u;
     // this thread's item, its best keys for outputs S2' and S2'|E
     constexpr uint32_t E = 1u << RL;
@@ -1778,9 +1801,9 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
     uint64_t *stage = reinterpret_cast<uint64_t *>(&s.r[0][0][0]);
     static_assert(2 * NB * THREADS * sizeof(uint64_t) <= sizeof(s.r), "the staged keys fit the row buffers");
     const uint32_t quarter = (threadIdx.x / 16u) & 3u, q16 = threadIdx.x & 15u;
-    const GatherSlot &slot = c_gather.s[threadIdx.x / kWave][quarter];
-    const uint4 gruns = *reinterpret_cast<const uint4 *>(slot.runs);   // loaded ahead of the barriers
-    const uint32_t gs2 = slot.s2;
+    const GatherSlot &gslot = c_gather.s[threadIdx.x / kWave][quarter];
+    const uint4 gruns = *reinterpret_cast<const uint4 *>(gslot.runs);   // loaded ahead of the barriers
+    const uint32_t gs2 = gslot.s2;
     lds_barrier();     // every wave is done with the rows
     if (has_item) {
         // the last pair's tracking; an odd number of pairs leaves the keys in
@@ -1835,12 +1858,12 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
             }
             const uint32_t sp = (gs2 >> (8 * jj)) & 0xffu;
             const uint32_t e = ((q16 < NB ? sp : (sp | E)) << CB) | (q16 & (NB - 1u));
-            if (fused) s.acc[e] = v;
-            else partial[(size_t)bid * ROW + e] = v;
+            if (fz) s.acc[e] = v;
+            else partial[(size_t)slot * ROW + e] = v;
         }
     }
     lds_barrier();     // the staged keys are read before the buffers are reused
-    if (fused) {
+    if (fz) {
         if constexpr (NARROW) {
             copy_row(buf(0, 1), Pn, 0u);
             uint32_t *sacc = buf(1, 0);
@@ -1874,18 +1897,24 @@ __global__ __launch_bounds__(256) void k_rb_reduce(uint32_t chunks, uint32_t gro
     if (v != ~0ull) atomicMin((unsigned long long *)base, (unsigned long long)v);
 }
 
-// finish the rows of one level: acc from the reduced partials (chunks > 0)
-// or empty (level 1 has no cross pairs)
+// finish rows row_offset + blockIdx.x of one level: acc from the reduced
+// partials (the row's first chunk slot, as k_rb_cross lays them out: head
+// rows in chunks, the others in tail_chunks from tail_base) or empty (no
+// chunks: level 1 has no cross pairs)
 template <class K, bool NARROW>
-__global__ __launch_bounds__(THREADS) void k_rb_final(int m, int h, uint32_t chunks, const int64_t *__restrict__ Wr,
+__global__ __launch_bounds__(THREADS) void k_rb_final(int m, int h, uint32_t row_offset, uint32_t head_rows,
+                                                      uint32_t chunks, uint32_t tail_chunks, uint32_t tail_base,
+                                                      const int64_t *__restrict__ Wr,
                                                       uint64_t *__restrict__ Tt, uint64_t *__restrict__ Pt,
                                                       uint32_t *__restrict__ Tn, uint32_t *__restrict__ Pn,
                                                       uint32_t *__restrict__ Sr, const uint64_t *__restrict__ partial) {
     __shared__ Lds<K> s;
-    const uint32_t r = blockIdx.x;
+    const uint32_t r = row_offset + blockIdx.x;
     const uint32_t sh = unrank_colex(r, h, m - L);
-    const uint64_t *src = partial + (size_t)r * chunks * ROW;
-    for (int e = threadIdx.x; e < ROW; e += THREADS) s.acc[e] = chunks ? src[e] : ~0ull;
+    const uint32_t c = r < head_rows ? chunks : tail_chunks;
+    const size_t slot = r < head_rows ? (size_t)r * chunks : tail_base + (size_t)(r - head_rows) * tail_chunks;
+    const uint64_t *src = partial + slot * ROW;
+    for (int e = threadIdx.x; e < ROW; e += THREADS) s.acc[e] = c ? src[e] : ~0ull;
     // NARROW: the two narrow rows (16 KiB each) at the start of the row space
     uint32_t *nr = reinterpret_cast<uint32_t *>(&s.r[0][0][0]);
     if constexpr (NARROW) {
@@ -2166,7 +2195,15 @@ size_t dp_partial_entries(int m) {
 }
 
 // row-blocked DP: one entry per level h = |S_H| of the high part
-struct RbLevel { int h; uint32_t n_sets; uint32_t n_pairs; uint32_t chunks; uint32_t per_chunk; };
+// One level of the row-blocked DP: n_sets rows; the first n_sets - tail_rows
+// (the head) run their n_pairs cross pairs in `chunks` chunks of per_chunk
+// pairs (one chunk: finished in the same kernel), the other tail_rows in
+// tail_chunks chunks of tail_per_chunk.
+struct RbLevel {
+    int h;
+    uint32_t n_sets, n_pairs, chunks, per_chunk;
+    uint32_t tail_rows, tail_chunks, tail_per_chunk;
+};
 constexpr int kRbMinM = rb::L + 1;
 constexpr int kRbMaxLevels = MPT_MAX_M - rb::L + 1;
 constexpr uint32_t kRbMaxChunks = 4096;
@@ -2213,8 +2250,43 @@ RbPlan rb_plan(int m, int64_t chunk_pairs) {
                 if (e < best_cost - 1e-9) { best = c; best_cost = e; }
             }
             L.chunks = best;
+            // A tail: the rows whose workgroups would make up the last,
+            // partial round run in more, shorter chunks, which the CUs left
+            // free in that round (and then all CUs) take after the head's
+            // workgroups. Head workgroups take a, tail ones b: the head runs
+            // q full rounds and r more workgroups; the free CUs run tail
+            // workgroups while those r finish, all CUs the rest. The tail's
+            // rows are finished by a separate pass (fused head), and their
+            // partials take one more reduce launch.
+            constexpr double kLaunch = 1.0;
+            const uint32_t rem = (uint32_t)(((uint64_t)L.n_sets * best) % (uint64_t)slots);
+            const uint32_t nb = (rem + best - 1) / best;
+            if (rem != 0 && nb < L.n_sets && L.n_pairs >= 2) {
+                const double a = std::ceil((double)L.n_pairs / best) + kWgCost + (best == 1 ? kFinishCost : 0.0);
+                const double head = (double)(L.n_sets - nb) * best;
+                const double q = std::floor(head / slots), r = head - q * slots;
+                const double finals = best == 1 ? rounds(nb) * (kFinishCost + 0.3) + 2 * kLaunch
+                                                : rounds(L.n_sets) * (kFinishCost + 0.3) + kLaunch;
+                for (uint32_t c = 2; c <= std::min<uint32_t>(L.n_pairs, 64u); ++c) {
+                    const double b = std::ceil((double)L.n_pairs / c) + kWgCost;
+                    const double wb = (double)nb * c;
+                    double t;
+                    if (r == 0) {
+                        t = q * a + rounds(wb) * b;
+                    } else {
+                        const double f = slots - r, k = std::floor(a / b);
+                        t = wb <= f * k ? (q + 1) * a : (q + 1) * a + rounds(wb - f * k) * b;
+                    }
+                    if (t + finals < best_cost - 1e-9) {
+                        best_cost = t + finals;
+                        L.tail_rows = nb;
+                        L.tail_chunks = c;
+                    }
+                }
+            }
         }
         L.per_chunk = L.chunks ? (L.n_pairs + L.chunks - 1) / L.chunks : 0;
+        L.tail_per_chunk = L.tail_chunks ? (L.n_pairs + L.tail_chunks - 1) / L.tail_chunks : 0;
         plan.v[plan.n++] = L;
     }
     return plan;
@@ -2226,7 +2298,8 @@ size_t rb_partial_entries(int m, int64_t chunk_pairs) {
     const RbPlan plan = rb_plan(m, chunk_pairs);
     for (int i = 0; i < plan.n; ++i) {
         const RbLevel &L = plan.v[i];
-        if (L.chunks > 1) mx = std::max(mx, (size_t)L.n_sets * L.chunks * rb::ROW);
+        const size_t head = L.chunks > 1 ? (size_t)(L.n_sets - L.tail_rows) * L.chunks : 0;
+        mx = std::max(mx, (head + (size_t)L.tail_rows * L.tail_chunks) * rb::ROW);
     }
     return mx;
 }
@@ -2357,26 +2430,32 @@ int solve_rb(int m, const int64_t *W, int64_t *C, uint32_t *split, char *ws, con
         if (P.h == 0) continue;                               // row 0: done above
         if (P.n_pairs == 0) {
             LaunchScope ls("rb_final", pair_work * P.n_sets, s);
-            rb::k_rb_final<K, NARROW><<<P.n_sets, rb::THREADS, 0, s>>>(m, P.h, 0u, Wr, Tt, Pt, Tn, Pn, Sr, partial);
-        } else if (P.chunks == 1) {
-            LaunchScope ls(kCrossLabel, pair_work * (double)P.n_sets * (P.n_pairs + 1), s);
-            rb::k_rb_cross<K, NARROW><<<P.n_sets, rb::THREADS, 0, s>>>(m, P.h, P.n_pairs, 1u, P.n_pairs, 1, Wr, Tt,
-                                                                       Pt, Tn, Pn, Sr, partial);
+            rb::k_rb_final<K, NARROW><<<P.n_sets, rb::THREADS, 0, s>>>(m, P.h, 0u, P.n_sets, 0u, 0u, 0u, Wr, Tt, Pt,
+                                                                       Tn, Pn, Sr, partial);
         } else {
+            const uint32_t head = P.n_sets - P.tail_rows;
+            const uint32_t head_wgs = head * P.chunks, tail_wgs = P.tail_rows * P.tail_chunks;
+            const bool fused = P.chunks == 1;
+            const uint32_t tail_base = fused ? 0u : head_wgs;
             {
-                LaunchScope ls(kCrossLabel, pair_work * (double)P.n_sets * P.n_pairs, s);
-                rb::k_rb_cross<K, NARROW><<<P.n_sets * P.chunks, rb::THREADS, 0, s>>>(
-                    m, P.h, P.n_pairs, P.chunks, P.per_chunk, 0, Wr, Tt, Pt, Tn, Pn, Sr, partial);
+                // work: the row pairs, and a fused row's self pair
+                LaunchScope ls(kCrossLabel, pair_work * ((double)P.n_sets * P.n_pairs + (fused ? head : 0u)), s);
+                rb::k_rb_cross<K, NARROW><<<head_wgs + tail_wgs, rb::THREADS, 0, s>>>(
+                    m, P.h, P.n_pairs, P.chunks, P.per_chunk, fused ? 1 : 0, head, P.tail_chunks, P.tail_per_chunk,
+                    tail_base, Wr, Tt, Pt, Tn, Pn, Sr, partial);
             }
-            {
-                LaunchScope ls("rb_reduce", (double)P.n_sets * P.chunks * rb::ROW * 8.0, s);
-                const uint32_t groups = (P.chunks - 1 + rb::RED_CHUNKS_PER_BLOCK - 1) / rb::RED_CHUNKS_PER_BLOCK;
-                rb::k_rb_reduce<<<P.n_sets * (rb::ROW / 256) * groups, 256, 0, s>>>(P.chunks, groups, partial);
-            }
-            {
-                LaunchScope ls("rb_final", pair_work * P.n_sets, s);
-                rb::k_rb_final<K, NARROW><<<P.n_sets, rb::THREADS, 0, s>>>(m, P.h, P.chunks, Wr, Tt, Pt, Tn, Pn, Sr,
-                                                                        partial);
+            auto reduce = [&](uint32_t rows, uint32_t chunks, uint64_t *part) {
+                LaunchScope ls("rb_reduce", (double)rows * chunks * rb::ROW * 8.0, s);
+                const uint32_t groups = (chunks - 1 + rb::RED_CHUNKS_PER_BLOCK - 1) / rb::RED_CHUNKS_PER_BLOCK;
+                rb::k_rb_reduce<<<rows * (rb::ROW / 256) * groups, 256, 0, s>>>(chunks, groups, part);
+            };
+            if (!fused) reduce(head, P.chunks, partial);
+            if (P.tail_rows) reduce(P.tail_rows, P.tail_chunks, partial + (size_t)tail_base * rb::ROW);
+            if (!fused || P.tail_rows) {
+                const uint32_t first = fused ? head : 0u;
+                LaunchScope ls("rb_final", pair_work * (P.n_sets - first), s);
+                rb::k_rb_final<K, NARROW><<<P.n_sets - first, rb::THREADS, 0, s>>>(
+                    m, P.h, first, head, P.chunks, P.tail_chunks, tail_base, Wr, Tt, Pt, Tn, Pn, Sr, partial);
             }
         }
         MPT_HIP_TRY(hipGetLastError());
