@@ -150,6 +150,46 @@ def test_config5_sampled_sub_instances():
         assert got["C"][s] == oracle.solve(sub, with_orders=False)["opt"], members
 
 
+@pytest.mark.timeout(600)
+def test_m27_retrieval_sampled():
+    """A retrieval-shaped instance at m = 27 (the level plan runs tails of
+    shorter chunks in seven levels, three of them behind a split head;
+    2^27-entry tables): the split hierarchy's
+    Eq. (2) cost and the orders' trie cost equal OPT; C(S) equals the
+    oracle's optimum of the sub-instance for sampled S of up to 14 requests;
+    and at sampled S of up to 16 requests the tables satisfy the recurrence
+    under the tie rule, C(S) = C(A) + C(S \\ A) - W(S) for the stored A, which
+    is the least A (lowbit(S) in A, A a proper subset) reaching the minimum."""
+    inst = wl.gen_retrieval(m=27, u=10000, topics=100, k=50, seed=7)
+    got = gpu_run(inst)
+    W, C, split = got["W"], got["C"], got["split"]
+    opt = int(got["opt"])
+    assert oracle.hierarchy_cost(inst, split) == opt
+    assert oracle.trie_cost(inst, got["orders"][:inst.nnz]) == opt
+    sets = inst.requests()
+    rng = np.random.default_rng(27)
+    for trial in range(16):
+        k = int(rng.integers(1, 15))
+        members = sorted(rng.choice(inst.m, size=k, replace=False).tolist())
+        s_ = sum(1 << i for i in members)
+        sub = wl.from_sets([sets[i] for i in members], inst.weights, inst.n_chunks)
+        assert C[s_] == oracle.solve(sub, with_orders=False)["opt"], members
+    for trial in range(40):
+        k = int(rng.integers(2, 17))
+        members = rng.choice(inst.m, size=k, replace=False)
+        s_ = int(sum(1 << int(i) for i in members))
+        low = s_ & -s_
+        bits = [1 << int(i) for i in sorted(members)]
+        # every submask of S, as numpy integers: A = sum of the chosen bits
+        idx = np.arange(1 << k, dtype=np.int64)
+        subs = np.zeros(1 << k, dtype=np.int64)
+        for j, b in enumerate(bits):
+            subs |= ((idx >> j) & 1) * b
+        cand = subs[((subs & low) != 0) & (subs != s_)]
+        costs = C[cand] + C[s_ ^ cand] - W[s_]
+        best = costs.min()
+        assert C[s_] == best, members
+        assert int(split[s_]) == int(cand[costs == best].min()), members
 # --- sweeps over shapes and seeds ---------------------------------------------------
 
 SWEEP = [
