@@ -1126,13 +1126,13 @@ __device__ inline void load_blk(const uint32_t *row, uint32_t slot, uint32_t v[N
 }
 
 // row xh of a table of E-byte elements -> LDS dst, as direct global-to-LDS
-// copies of 16 bytes per lane (no registers held). Completion: this
-// thread's vmcnt, then a workgroup barrier.
+// copies of 16 bytes per lane (no registers held), by a workgroup of NT
+// threads. Completion: this thread's vmcnt, then a workgroup barrier.
 typedef __attribute__((address_space(3))) void lds_void;
-template <class E>
+template <class E, int NT = THREADS>
 __device__ inline void copy_row(void *dst, const E *__restrict__ tab, uint32_t xh) {
     constexpr int PIECES = ROW * (int)sizeof(E) / 16;    // 16-byte pieces per row
-    constexpr int PER_WAVE = PIECES / (THREADS / kWave);
+    constexpr int PER_WAVE = PIECES / (NT / kWave);
     static_assert(PER_WAVE % kWave == 0, "whole wave copies");
     const int w = (int)(threadIdx.x / kWave), lane = (int)(threadIdx.x & (kWave - 1));
     const uint4 *src = reinterpret_cast<const uint4 *>(tab + ((size_t)xh << L));
@@ -1416,24 +1416,31 @@ __device__ inline void run_item_self(uint32_t item, const uint32_t *rA, const ui
 // before the caller's barrier). Writes the row to the plain 64-bit table, to
 // both narrow tables and its splits to Sr (row-major, mask order inside a
 // row). The self pair's candidates (A_H = S_H) are kept as 32-bit keys up
-// to the comparison with the cross pairs' key of each entry.
-template <class K>
+// to the comparison with the cross pairs' key of each entry. NT threads: each
+// takes THREADS / NT items of a level (the item table is laid out for
+// THREADS; its lane groups stay aligned since NT is a multiple of the wave).
+template <class K, int NT = THREADS>
 __device__ __attribute__((always_inline)) inline void finalize_row_narrow(
         int m, uint32_t sh, const uint64_t *acc, uint32_t *rSn, const uint32_t *r0n, uint32_t *sacc,
         const int64_t *__restrict__ Wr, uint64_t *__restrict__ Pt, uint32_t *__restrict__ Tn,
         uint32_t *__restrict__ Pn, uint32_t *__restrict__ Sr) {
+    static_assert(THREADS % NT == 0 && NT % kWave == 0 && NT >= NS2 / 4, "items and blocks per thread");
+    constexpr int IPT = THREADS / NT;
     const int H = m - L;
     const uint32_t row = sh << L;
     const uint64_t mask = ((uint64_t)1 << m) - 1u;
-    auto level_item = [](int k) -> uint32_t {
-        const int it = c_items.begin[k] + (int)threadIdx.x;
+    auto level_item = [](int k, int i) -> uint32_t {
+        const int it = c_items.begin[k] + (int)threadIdx.x + i * NT;
         return it < c_items.end[k] ? c_items.v[it] : 0u;
     };
     auto level_blk = [](int k) -> uint32_t {
         const int bi = c_blocks.begin[k] + (int)threadIdx.x;
         return bi < c_blocks.end[k] ? (uint32_t)c_blocks.v[bi] | 0x10000u : 0u;
     };
-    uint32_t item = level_item(0), blk = level_blk(0);
+    uint32_t item[IPT];
+#pragma unroll
+    for (int i = 0; i < IPT; ++i) item[i] = level_item(0, i);
+    uint32_t blk = level_blk(0);
     // block 0 of row 0, plain narrow: C(X1 << H) << L for every low part X1
     uint32_t b0n[NB];
 #pragma unroll
@@ -1441,7 +1448,9 @@ __device__ __attribute__((always_inline)) inline void finalize_row_narrow(
     // S = (S_H, 0, 0) with one request in S_H is a leaf: C = W
     const bool single = (sh & (sh - 1u)) == 0;
     for (int k = 0; k <= R2; ++k) {
-        const uint32_t item_next = k < R2 ? level_item(k + 1) : 0u;
+        uint32_t item_next[IPT];
+#pragma unroll
+        for (int i = 0; i < IPT; ++i) item_next[i] = k < R2 ? level_item(k + 1, i) : 0u;
         const uint32_t blk_next = k < R2 ? level_blk(k + 1) : 0u;
         int64_t wv[NB];
         if (blk) {
@@ -1450,7 +1459,9 @@ __device__ __attribute__((always_inline)) inline void finalize_row_narrow(
             for (int x = 0; x < NB; ++x) wv[x] = wp[x];
         }
         // A2 a proper submask of S2
-        if (item) run_item_self(item, rSn, r0n, sacc);
+#pragma unroll
+        for (int i = 0; i < IPT; ++i)
+            if (item[i]) run_item_self(item[i], rSn, r0n, sacc);
         lds_barrier();
         // A2 = S2: in-block pairs, one thread per block of this level; A =
         // (S_H, S2, A1) holds lowbit(S), B = (0, 0, S1 ^ A1) is in block 0
@@ -1517,7 +1528,8 @@ __device__ __attribute__((always_inline)) inline void finalize_row_narrow(
             }
         }
         lds_barrier();
-        item = item_next;
+#pragma unroll
+        for (int i = 0; i < IPT; ++i) item[i] = item_next[i];
         blk = blk_next;
     }
 }
@@ -1897,16 +1909,16 @@ __global__ __launch_bounds__(256) void k_rb_reduce(uint32_t chunks, uint32_t gro
     if (v != ~0ull) atomicMin((unsigned long long *)base, (unsigned long long)v);
 }
 
-// finish rows row_offset + blockIdx.x of one level: acc from the reduced
-// partials (the row's first chunk slot, as k_rb_cross lays them out: head
-// rows in chunks, the others in tail_chunks from tail_base) or empty (no
-// chunks: level 1 has no cross pairs)
-template <class K, bool NARROW>
+// finish rows row_offset + blockIdx.x of one level on 64-bit keys (narrow
+// rows: k_rb_final_narrow): acc from the reduced partials (the row's first
+// chunk slot, as k_rb_cross lays them out: head rows in chunks, the others
+// in tail_chunks from tail_base) or empty (no chunks: level 1 has no cross
+// pairs)
+template <class K>
 __global__ __launch_bounds__(THREADS) void k_rb_final(int m, int h, uint32_t row_offset, uint32_t head_rows,
                                                       uint32_t chunks, uint32_t tail_chunks, uint32_t tail_base,
                                                       const int64_t *__restrict__ Wr,
                                                       uint64_t *__restrict__ Tt, uint64_t *__restrict__ Pt,
-                                                      uint32_t *__restrict__ Tn, uint32_t *__restrict__ Pn,
                                                       uint32_t *__restrict__ Sr, const uint64_t *__restrict__ partial) {
     __shared__ Lds<K> s;
     const uint32_t r = row_offset + blockIdx.x;
@@ -1915,18 +1927,44 @@ __global__ __launch_bounds__(THREADS) void k_rb_final(int m, int h, uint32_t row
     const size_t slot = r < head_rows ? (size_t)r * chunks : tail_base + (size_t)(r - head_rows) * tail_chunks;
     const uint64_t *src = partial + slot * ROW;
     for (int e = threadIdx.x; e < ROW; e += THREADS) s.acc[e] = c ? src[e] : ~0ull;
-    // NARROW: the two narrow rows (16 KiB each) at the start of the row space
-    uint32_t *nr = reinterpret_cast<uint32_t *>(&s.r[0][0][0]);
-    if constexpr (NARROW) {
-        copy_row(nr + ROW, Pn, 0u);
-        for (int e = threadIdx.x; e < ROW; e += THREADS) nr[2 * ROW + e] = Key<uint32_t>::none();
-    } else {
-        copy_row(s.r[0][1], Pt, 0u);
-    }
+    copy_row(s.r[0][1], Pt, 0u);
     copies_done();
     lds_barrier();
-    if constexpr (NARROW) finalize_row_narrow<K>(m, sh, s.acc, nr, nr + ROW, nr + 2 * ROW, Wr, Pt, Tn, Pn, Sr);
-    else finalize_row<K>(m, sh, s, s.r[0][0], s.r[0][1], Wr, Tt, Pt, Sr);
+    finalize_row<K>(m, sh, s, s.r[0][0], s.r[0][1], Wr, Tt, Pt, Sr);
+}
+
+// k_rb_final on narrow rows, in workgroups of half the threads and half
+// the CU's LDS (the accumulator row and three narrow rows), so that two rows
+// are finished on a CU at a time: the finishing's phases are bound by
+// latency, and the two workgroups' phases overlap.
+constexpr int FINAL_THREADS = THREADS / 2;
+struct alignas(16) LdsFinalNarrow {
+    uint64_t acc[ROW];
+    uint32_t nr[3 * ROW];      // row S_H (tagged), row 0 (plain), the self-pair minima
+};
+static_assert(2 * sizeof(LdsFinalNarrow) <= 160 * 1024, "two narrow finishing workgroups per CU");
+template <class K>
+__global__ __launch_bounds__(FINAL_THREADS) void k_rb_final_narrow(int m, int h, uint32_t row_offset,
+                                                                   uint32_t head_rows, uint32_t chunks,
+                                                                   uint32_t tail_chunks, uint32_t tail_base,
+                                                                   const int64_t *__restrict__ Wr,
+                                                                   uint64_t *__restrict__ Pt,
+                                                                   uint32_t *__restrict__ Tn,
+                                                                   uint32_t *__restrict__ Pn,
+                                                                   uint32_t *__restrict__ Sr,
+                                                                   const uint64_t *__restrict__ partial) {
+    __shared__ LdsFinalNarrow s;
+    const uint32_t r = row_offset + blockIdx.x;
+    const uint32_t sh = unrank_colex(r, h, m - L);
+    const uint32_t c = r < head_rows ? chunks : tail_chunks;
+    const size_t slot = r < head_rows ? (size_t)r * chunks : tail_base + (size_t)(r - head_rows) * tail_chunks;
+    const uint64_t *src = partial + slot * ROW;
+    for (int e = threadIdx.x; e < ROW; e += FINAL_THREADS) s.acc[e] = c ? src[e] : ~0ull;
+    copy_row<uint32_t, FINAL_THREADS>(s.nr + ROW, Pn, 0u);
+    for (int e = threadIdx.x; e < ROW; e += FINAL_THREADS) s.nr[2 * ROW + e] = Key<uint32_t>::none();
+    copies_done();
+    lds_barrier();
+    finalize_row_narrow<K, FINAL_THREADS>(m, sh, s.acc, s.nr, s.nr + ROW, s.nr + 2 * ROW, Wr, Pt, Tn, Pn, Sr);
 }
 
 // the in-row masks grouped by popcount, for the row-0 DP
@@ -2430,8 +2468,12 @@ int solve_rb(int m, const int64_t *W, int64_t *C, uint32_t *split, char *ws, con
         if (P.h == 0) continue;                               // row 0: done above
         if (P.n_pairs == 0) {
             LaunchScope ls("rb_final", pair_work * P.n_sets, s);
-            rb::k_rb_final<K, NARROW><<<P.n_sets, rb::THREADS, 0, s>>>(m, P.h, 0u, P.n_sets, 0u, 0u, 0u, Wr, Tt, Pt,
-                                                                       Tn, Pn, Sr, partial);
+            if constexpr (NARROW)
+                rb::k_rb_final_narrow<K><<<P.n_sets, rb::FINAL_THREADS, 0, s>>>(m, P.h, 0u, P.n_sets, 0u, 0u, 0u, Wr,
+                                                                              Pt, Tn, Pn, Sr, partial);
+            else
+                rb::k_rb_final<K><<<P.n_sets, rb::THREADS, 0, s>>>(m, P.h, 0u, P.n_sets, 0u, 0u, 0u, Wr, Tt, Pt, Sr,
+                                                                   partial);
         } else {
             const uint32_t head = P.n_sets - P.tail_rows;
             const uint32_t head_wgs = head * P.chunks, tail_wgs = P.tail_rows * P.tail_chunks;
@@ -2454,8 +2496,12 @@ int solve_rb(int m, const int64_t *W, int64_t *C, uint32_t *split, char *ws, con
             if (!fused || P.tail_rows) {
                 const uint32_t first = fused ? head : 0u;
                 LaunchScope ls("rb_final", pair_work * (P.n_sets - first), s);
-                rb::k_rb_final<K, NARROW><<<P.n_sets - first, rb::THREADS, 0, s>>>(
-                    m, P.h, first, head, P.chunks, P.tail_chunks, tail_base, Wr, Tt, Pt, Tn, Pn, Sr, partial);
+                if constexpr (NARROW)
+                    rb::k_rb_final_narrow<K><<<P.n_sets - first, rb::FINAL_THREADS, 0, s>>>(
+                        m, P.h, first, head, P.chunks, P.tail_chunks, tail_base, Wr, Pt, Tn, Pn, Sr, partial);
+                else
+                    rb::k_rb_final<K><<<P.n_sets - first, rb::THREADS, 0, s>>>(
+                        m, P.h, first, head, P.chunks, P.tail_chunks, tail_base, Wr, Tt, Pt, Sr, partial);
             }
         }
         MPT_HIP_TRY(hipGetLastError());
