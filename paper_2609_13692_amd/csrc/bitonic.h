@@ -29,7 +29,8 @@ static __global__ __launch_bounds__(kSortThreads) void k_sort_tile(uint64_t *key
     for (int k = 2; k <= kSortTile; k <<= 1)
         for (int j = k >> 1; j > 0; j >>= 1) {
             for (int p = threadIdx.x; p < kSortTile / 2; p += kSortThreads) {
-                const int i = ((p / j) * 2 * j) + (p % j), l = i + j;
+                // j is a power of two: the pair's lower index without a division
+                const int i = ((p & ~(j - 1)) << 1) | (p & (j - 1)), l = i + j;
                 cswap(t[i], t[l], ((base + i) & k) == 0);
             }
             __syncthreads();
@@ -40,7 +41,7 @@ static __global__ __launch_bounds__(kSortThreads) void k_sort_tile(uint64_t *key
 // one compare-exchange step of stage k with stride j >= kSortTile
 static __global__ void k_sort_global(uint64_t *keys, int64_t n, int64_t k, int64_t j) {
     for (int64_t p = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; p < n / 2; p += (int64_t)gridDim.x * blockDim.x) {
-        const int64_t i = ((p / j) * 2 * j) + (p % j), l = i + j;
+        const int64_t i = ((p & ~(j - 1)) << 1) | (p & (j - 1)), l = i + j;    // j: a power of two
         uint64_t a = keys[i], b = keys[l];
         cswap(a, b, (i & k) == 0);
         keys[i] = a; keys[l] = b;
@@ -56,7 +57,7 @@ static __global__ __launch_bounds__(kSortThreads) void k_sort_tile_merge(uint64_
     const bool up = (base & k) == 0;            // the tile lies inside one run of stage k
     for (int j = kSortTile >> 1; j > 0; j >>= 1) {
         for (int p = threadIdx.x; p < kSortTile / 2; p += kSortThreads) {
-            const int i = ((p / j) * 2 * j) + (p % j), l = i + j;
+            const int i = ((p & ~(j - 1)) << 1) | (p & (j - 1)), l = i + j;
             cswap(t[i], t[l], up);
         }
         __syncthreads();

@@ -100,7 +100,7 @@ static __global__ __launch_bounds__(256) void k_l_seq_sort_tile(int32_t *ord, co
     for (int k = 2; k <= kSeqSortTile; k <<= 1)
         for (int j = k >> 1; j > 0; j >>= 1) {
             for (int p = threadIdx.x; p < kSeqSortTile / 2; p += blockDim.x) {
-                const int i = ((p / j) * 2 * j) + (p % j), l = i + j;
+                const int i = ((p & ~(j - 1)) << 1) | (p & (j - 1)), l = i + j;    // j: a power of two
                 const bool up = ((base + i) & k) == 0;
                 const int x = T.t[i], y = T.t[l];
                 if (seq_less_slot(T, y, x, off, seqs) == up) { T.t[i] = y; T.t[l] = x; }
@@ -113,7 +113,7 @@ static __global__ __launch_bounds__(256) void k_l_seq_sort_tile(int32_t *ord, co
 static __global__ void k_l_seq_sort_global(int32_t *ord, int64_t n, int64_t k, int64_t j, const int64_t *off,
                                     const int32_t *seqs) {
     for (int64_t p = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; p < n / 2; p += (int64_t)gridDim.x * blockDim.x) {
-        const int64_t i = ((p / j) * 2 * j) + (p % j), l = i + j;
+        const int64_t i = ((p & ~(j - 1)) << 1) | (p & (j - 1)), l = i + j;    // j: a power of two
         const bool up = (i & k) == 0;
         const int a = ord[i], b = ord[l];
         if (seq_less(b, a, off, seqs) == up) { ord[i] = b; ord[l] = a; }
@@ -129,7 +129,7 @@ static __global__ __launch_bounds__(256) void k_l_seq_sort_tile_merge(int32_t *o
     const bool up = (base & k) == 0;
     for (int j = kSeqSortTile >> 1; j > 0; j >>= 1) {
         for (int p = threadIdx.x; p < kSeqSortTile / 2; p += blockDim.x) {
-            const int i = ((p / j) * 2 * j) + (p % j), l = i + j;
+            const int i = ((p & ~(j - 1)) << 1) | (p & (j - 1)), l = i + j;    // j: a power of two
             const int x = T.t[i], y = T.t[l];
             if (seq_less_slot(T, y, x, off, seqs) == up) { T.t[i] = y; T.t[l] = x; }
         }
