@@ -1410,64 +1410,84 @@ __device__ inline void run_item_self(uint32_t item, const uint32_t *rA, const ui
     }
 }
 
+// The block that thread t completes in finalize_row_narrow, and its W: the
+// t-th middle mask in order of popcount, so that the blocks of one level sit
+// in consecutive threads (threads past NS2 take none). Loaded before the
+// row's setup, whose waits then cover these loads too. Narrow keys hold
+// sum_i w(R_i) < 2^20, so every W fits 32 bits.
+struct OwnBlock {
+    uint32_t s2;
+    uint32_t w[NB];
+};
+__device__ inline void own_block_load(uint32_t sh, const int64_t *__restrict__ Wr, OwnBlock &o) {
+    const uint32_t t = threadIdx.x < (uint32_t)NS2 ? threadIdx.x : NS2 - 1u;
+    o.s2 = c_blocks.v[t];
+    const uint4 *wp = reinterpret_cast<const uint4 *>(Wr + ((sh << L) | (o.s2 << CB)));
+#pragma unroll
+    for (int q = 0; q < NB / 2; ++q) {
+        const uint4 v = wp[q];
+        o.w[2 * q] = v.x;
+        o.w[2 * q + 1] = v.z;
+    }
+}
+
 // Completes row S_H (non-empty) on narrow keys. In LDS: acc, the 64-bit
 // cross-pair keys of the row; rSn, row S_H (tagged, filled here); r0n, row 0
 // (plain); sacc, the narrow self-pair minima (4096 entries set to all ones
-// before the caller's barrier). Writes the row to the plain 64-bit table, to
-// both narrow tables and its splits to Sr (row-major, mask order inside a
-// row). The self pair's candidates (A_H = S_H) are kept as 32-bit keys up
-// to the comparison with the cross pairs' key of each entry. NT threads: each
-// takes THREADS / NT items of a level (the item table is laid out for
-// THREADS; its lane groups stay aligned since NT is a multiple of the wave).
+// before the caller's barrier). own: this thread's block (own_block_load).
+// Writes the row to the plain 64-bit table, to both narrow tables and its
+// splits to Sr (row-major, mask order inside a row). The self pair's
+// candidates (A_H = S_H) are kept as 32-bit keys up to the comparison with
+// the cross pairs' key of each entry. NT threads: each takes THREADS / NT
+// items of a level (the item table is laid out for THREADS; its lane groups
+// stay aligned since NT is a multiple of the wave).
+//
+// The levels issue no global stores: a finished block leaves its plain
+// entries in its (no longer needed) acc entries and its splits in its sacc
+// entries, and the whole row goes to HBM in coalesced pieces after the last
+// level. The only global loads inside the levels are the next level's item
+// entries, read unconditionally (clamped index, validity tested where they
+// are used) into the other of two register sets, so that no wait for them
+// comes before the next level: vector memory operations retire in order,
+// and a wait for an older load would wait for every newer one.
 template <class K, int NT = THREADS>
 __device__ __attribute__((always_inline)) inline void finalize_row_narrow(
-        int m, uint32_t sh, const uint64_t *acc, uint32_t *rSn, const uint32_t *r0n, uint32_t *sacc,
-        const int64_t *__restrict__ Wr, uint64_t *__restrict__ Pt, uint32_t *__restrict__ Tn,
-        uint32_t *__restrict__ Pn, uint32_t *__restrict__ Sr) {
+        int m, uint32_t sh, const OwnBlock &own, uint64_t *acc, uint32_t *rSn, const uint32_t *r0n,
+        uint32_t *sacc, uint64_t *__restrict__ Pt, uint32_t *__restrict__ Tn, uint32_t *__restrict__ Pn,
+        uint32_t *__restrict__ Sr) {
     static_assert(THREADS % NT == 0 && NT % kWave == 0 && NT >= NS2 / 4, "items and blocks per thread");
     constexpr int IPT = THREADS / NT;
     const int H = m - L;
     const uint32_t row = sh << L;
     const uint64_t mask = ((uint64_t)1 << m) - 1u;
-    auto level_item = [](int k, int i) -> uint32_t {
-        const int it = c_items.begin[k] + (int)threadIdx.x + i * NT;
-        return it < c_items.end[k] ? c_items.v[it] : 0u;
+    const int tid = (int)threadIdx.x;
+    // item entry i of level k (any valid entry past the level's end)
+    auto item_load = [tid](int k, int i) -> uint32_t {
+        constexpr int last = kItems.n - 1;
+        const int it = c_items.begin[k] + tid + i * NT;
+        return c_items.v[it < last ? it : last];
     };
-    auto level_blk = [](int k) -> uint32_t {
-        const int bi = c_blocks.begin[k] + (int)threadIdx.x;
-        return bi < c_blocks.end[k] ? (uint32_t)c_blocks.v[bi] | 0x10000u : 0u;
-    };
-    uint32_t item[IPT];
-#pragma unroll
-    for (int i = 0; i < IPT; ++i) item[i] = level_item(0, i);
-    uint32_t blk = level_blk(0);
     // block 0 of row 0, plain narrow: C(X1 << H) << L for every low part X1
     uint32_t b0n[NB];
 #pragma unroll
     for (int x = 0; x < NB; ++x) b0n[x] = r0n[npos(0u, x)];
     // S = (S_H, 0, 0) with one request in S_H is a leaf: C = W
     const bool single = (sh & (sh - 1u)) == 0;
-    for (int k = 0; k <= R2; ++k) {
-        uint32_t item_next[IPT];
+    auto level = [&](int k, const uint32_t (&cur)[IPT], uint32_t (&nxt)[IPT]) __attribute__((always_inline)) {
+        const int kn = k < R2 ? k + 1 : R2;     // (the last level reads entries it does not use)
 #pragma unroll
-        for (int i = 0; i < IPT; ++i) item_next[i] = k < R2 ? level_item(k + 1, i) : 0u;
-        const uint32_t blk_next = k < R2 ? level_blk(k + 1) : 0u;
-        int64_t wv[NB];
-        if (blk) {
-            const int64_t *wp = Wr + (row | ((blk & 0xffffu) << CB));
-#pragma unroll
-            for (int x = 0; x < NB; ++x) wv[x] = wp[x];
-        }
+        for (int i = 0; i < IPT; ++i) nxt[i] = item_load(kn, i);
         // A2 a proper submask of S2
+        const int n_items = c_items.end[k] - c_items.begin[k];
 #pragma unroll
         for (int i = 0; i < IPT; ++i)
-            if (item[i]) run_item_self(item[i], rSn, r0n, sacc);
+            if (tid + i * NT < n_items) run_item_self(cur[i], rSn, r0n, sacc);
         lds_barrier();
         // A2 = S2: in-block pairs, one thread per block of this level; A =
         // (S_H, S2, A1) holds lowbit(S), B = (0, 0, S1 ^ A1) is in block 0
         // of row 0
-        if (blk) {
-            const uint32_t s2 = blk & 0xffffu;
+        if (tid >= c_blocks.begin[k] && tid < c_blocks.end[k]) {
+            const uint32_t s2 = own.s2;
             const uint32_t tag = s2 << CB;                       // in-row part of (S2, X1 = 0)
             // the block's self-pair minima and cross-pair keys, read together
             uint32_t sself[NB];
@@ -1501,36 +1521,50 @@ __device__ __attribute__((always_inline)) inline void finalize_row_narrow(
                                             ? ~0ull
                                             : ((uint64_t)(nk >> L) << m) | ((uint64_t)(nk & (ROW - 1u)) << H) | sh;
                     const uint64_t kb = kacc[s1] < ks ? kacc[s1] : ks;
-                    const int64_t w = wv[s1];
+                    const uint64_t w = own.w[s1];
                     const bool leaf = s1 == 0 && leaf0;
-                    const uint64_t c = leaf ? (uint64_t)w : (kb >> m) - (uint64_t)w;
+                    const uint64_t c = leaf ? w : (kb >> m) - w;
                     sp[s1] = leaf ? 0u : (uint32_t)(kb & mask);
                     cm[s1] = c << m;
                     on[s1] = ((uint32_t)c << L) | tag | (uint32_t)s1;
                 }
             }
+            // the plain entries and the splits, over the entries just read
+#pragma unroll
+            for (int x = 0; x < NB; ++x) acc[tag | x] = Key<K>::store(cm[x]);
+            uint4 *sp4 = reinterpret_cast<uint4 *>(sacc + tag);
+            sp4[0] = make_uint4(sp[0], sp[1], sp[2], sp[3]);
+            sp4[1] = make_uint4(sp[4], sp[5], sp[6], sp[7]);
+            // C(X) << L, tagged with X_L = S2 << CB | X1
             const uint32_t sl = slot_of(s2);
 #pragma unroll
-            for (int x = 0; x < NB; ++x) {
-                Pt[row + lpos(sl, x)] = Key<K>::store(cm[x]);
-                Sr[row | tag | (uint32_t)x] = sp[x];
-            }
-            // C(X) << L, and tagged with X_L = S2 << CB | X1
-#pragma unroll
-            for (int q = 0; q < NB / 4; ++q) {
-                const uint32_t at = row + npos(sl, 4 * q);
-                const uint32_t lo = ~(ROW - 1u);
-                *reinterpret_cast<uint4 *>(Pn + at) =
-                    make_uint4(on[4 * q] & lo, on[4 * q + 1] & lo, on[4 * q + 2] & lo, on[4 * q + 3] & lo);
-                const uint4 tv = make_uint4(on[4 * q], on[4 * q + 1], on[4 * q + 2], on[4 * q + 3]);
-                *reinterpret_cast<uint4 *>(Tn + at) = tv;
-                *reinterpret_cast<uint4 *>(rSn + npos(sl, 4 * q)) = tv;
-            }
+            for (int q = 0; q < NB / 4; ++q)
+                *reinterpret_cast<uint4 *>(rSn + npos(sl, 4 * q)) =
+                    make_uint4(on[4 * q], on[4 * q + 1], on[4 * q + 2], on[4 * q + 3]);
         }
         lds_barrier();
+    };
+    uint32_t ia[IPT], ib[IPT];
 #pragma unroll
-        for (int i = 0; i < IPT; ++i) item[i] = item_next[i];
-        blk = blk_next;
+    for (int i = 0; i < IPT; ++i) ia[i] = item_load(0, i);
+    for (int k = 0; k <= R2; k += 2) {
+        level(k, ia, ib);
+        if (k + 1 <= R2) level(k + 1, ib, ia);
+    }
+    // the row to HBM: plain entries (the block at slot p, plane by plane),
+    // splits (mask order), and the tagged and plain narrow rows (the LDS
+    // layout is the table's)
+    for (int p = tid; p < NS2; p += NT) {
+        const uint4 *src = reinterpret_cast<const uint4 *>(acc + (slot_of((uint32_t)p) << CB));
+#pragma unroll
+        for (int q = 0; q < NB / 2; ++q) *reinterpret_cast<uint4 *>(Pt + row + lpos((uint32_t)p, 2 * q)) = src[q];
+    }
+    const uint32_t lo = ~(ROW - 1u);
+    for (int p = tid; p < ROW / 4; p += NT) {
+        reinterpret_cast<uint4 *>(Sr + row)[p] = reinterpret_cast<const uint4 *>(sacc)[p];
+        const uint4 tv = reinterpret_cast<const uint4 *>(rSn)[p];
+        reinterpret_cast<uint4 *>(Tn + row)[p] = tv;
+        reinterpret_cast<uint4 *>(Pn + row)[p] = make_uint4(tv.x & lo, tv.y & lo, tv.z & lo, tv.w & lo);
     }
 }
 
@@ -1876,7 +1910,9 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
     }
     lds_barrier();     // the staged keys are read before the buffers are reused
     if (fz) {
+        OwnBlock own;
         if constexpr (NARROW) {
+            own_block_load(sh, Wr, own);
             copy_row(buf(0, 1), Pn, 0u);
             uint32_t *sacc = buf(1, 0);
             for (int e = threadIdx.x; e < ROW; e += THREADS) sacc[e] = Key<uint32_t>::none();
@@ -1885,7 +1921,7 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
         }
         copies_done();
         lds_barrier();
-        if constexpr (NARROW) finalize_row_narrow<K>(m, sh, s.acc, buf(0, 0), buf(0, 1), buf(1, 0), Wr, Pt, Tn, Pn, Sr);
+        if constexpr (NARROW) finalize_row_narrow<K>(m, sh, own, s.acc, buf(0, 0), buf(0, 1), buf(1, 0), Pt, Tn, Pn, Sr);
         else finalize_row<K>(m, sh, s, s.r[0][0], s.r[0][1], Wr, Tt, Pt, Sr);
     }
 }
@@ -1958,13 +1994,18 @@ __global__ __launch_bounds__(FINAL_THREADS) void k_rb_final_narrow(int m, int h,
     const uint32_t sh = unrank_colex(r, h, m - L);
     const uint32_t c = r < head_rows ? chunks : tail_chunks;
     const size_t slot = r < head_rows ? (size_t)r * chunks : tail_base + (size_t)(r - head_rows) * tail_chunks;
-    const uint64_t *src = partial + slot * ROW;
-    for (int e = threadIdx.x; e < ROW; e += FINAL_THREADS) s.acc[e] = c ? src[e] : ~0ull;
+    OwnBlock own;
+    own_block_load(sh, Wr, own);
+    // the reduced cross-pair keys (direct copies, all in flight together),
+    // or none
+    if (c) copy_row<uint64_t, FINAL_THREADS>(s.acc, partial, (uint32_t)slot);
+    else
+        for (int e = threadIdx.x; e < ROW; e += FINAL_THREADS) s.acc[e] = ~0ull;
     copy_row<uint32_t, FINAL_THREADS>(s.nr + ROW, Pn, 0u);
     for (int e = threadIdx.x; e < ROW; e += FINAL_THREADS) s.nr[2 * ROW + e] = Key<uint32_t>::none();
     copies_done();
     lds_barrier();
-    finalize_row_narrow<K, FINAL_THREADS>(m, sh, s.acc, s.nr, s.nr + ROW, s.nr + 2 * ROW, Wr, Pt, Tn, Pn, Sr);
+    finalize_row_narrow<K, FINAL_THREADS>(m, sh, own, s.acc, s.nr, s.nr + ROW, s.nr + 2 * ROW, Pt, Tn, Pn, Sr);
 }
 
 // the in-row masks grouped by popcount, for the row-0 DP
