@@ -1275,64 +1275,90 @@ __device__ inline void run_item(uint32_t item, const K *rA, const K *rB, uint64_
     flush_group<K>(best, s2, chunks < 8u ? chunks : 8u, acc);
 }
 
+// The block that thread t completes when it finishes a row, and its W: the
+// t-th middle mask in order of popcount, so that the blocks of one level sit
+// in consecutive threads (threads past NS2 take none). Loaded before the
+// row's setup, whose waits then cover these loads too. WT: int64_t, or
+// uint32_t for narrow keys, which hold sum_i w(R_i) < 2^20 (every W fits 32
+// bits).
+template <class WT>
+struct OwnBlock {
+    uint32_t s2;
+    WT w[NB];
+};
+template <class WT>
+__device__ inline void own_block_load(uint32_t sh, const int64_t *__restrict__ Wr, OwnBlock<WT> &o) {
+    const uint32_t t = threadIdx.x < (uint32_t)NS2 ? threadIdx.x : NS2 - 1u;
+    o.s2 = c_blocks.v[t];
+    const uint4 *wp = reinterpret_cast<const uint4 *>(Wr + ((sh << L) | (o.s2 << CB)));
+#pragma unroll
+    for (int q = 0; q < NB / 2; ++q) {
+        const uint4 v = wp[q];
+        if constexpr (sizeof(WT) == 4) {
+            o.w[2 * q] = v.x;
+            o.w[2 * q + 1] = v.z;
+        } else {
+            o.w[2 * q] = (int64_t)(((uint64_t)v.y << 32) | v.x);
+            o.w[2 * q + 1] = (int64_t)(((uint64_t)v.w << 32) | v.z);
+        }
+    }
+}
+
+// A thread's self-pair item of level k (k at most R2): entry i of the
+// level's items, any valid entry past the level's end (validity is tested
+// where the entry is used, so that no wait for the load comes earlier).
+template <int NT>
+__device__ inline uint32_t item_load(int k, int i) {
+    constexpr int last = kItems.n - 1;
+    const int it = c_items.begin[k] + (int)threadIdx.x + i * NT;
+    return c_items.v[it < last ? it : last];
+}
+
 // Complete row S_H (non-empty) on 64-bit keys (narrow rows have
 // finalize_row_narrow). s.acc holds the best cross-pair key bits (or ~0);
-// rS receives row S_H (tagged), r0 holds row 0 (plain), both in LDS. Writes
-// the row to the plain and the tagged table and its splits to Sr (row-major,
-// mask order inside a row).
+// rS receives row S_H (tagged), r0 holds row 0 (plain), both in LDS; own:
+// this thread's block (own_block_load). Writes the row to the plain and the
+// tagged table and its splits to Sr (row-major, mask order inside a row).
+// As in finalize_row_narrow, the levels issue no global stores (a finished
+// block's plain entries go to its acc entries, its splits to s.r[1][0]) and
+// load only the next level's item entries, into the other of two registers.
 template <class K>
-__device__ __attribute__((always_inline)) inline void finalize_row(int m, uint32_t sh, Lds<K> &s, K *rS,
-                                                                   const K *r0,
-                                                                   const int64_t *__restrict__ Wr,
+__device__ __attribute__((always_inline)) inline void finalize_row(int m, uint32_t sh, const OwnBlock<int64_t> &own,
+                                                                   Lds<K> &s, K *rS, const K *r0,
                                                                    uint64_t *__restrict__ Tt,
                                                                    uint64_t *__restrict__ Pt,
                                                                    uint32_t *__restrict__ Sr) {
     const int H = m - L;
     const uint32_t row = sh << L;
     const uint64_t mask = ((uint64_t)1 << m) - 1u;
-    // this thread's item and block of a level (0: none), each read one
-    // level ahead so that the table lookups overlap the level before
-    auto level_item = [](int k) -> uint32_t {
-        const int it = c_items.begin[k] + (int)threadIdx.x;
-        return it < c_items.end[k] ? c_items.v[it] : 0u;
-    };
-    auto level_blk = [](int k) -> uint32_t {
-        const int bi = c_blocks.begin[k] + (int)threadIdx.x;
-        return bi < c_blocks.end[k] ? (uint32_t)c_blocks.v[bi] | 0x10000u : 0u;
-    };
-    uint32_t item = level_item(0), blk = level_blk(0);
+    const int tid = (int)threadIdx.x;
+    uint32_t *split = reinterpret_cast<uint32_t *>(s.r[1][0]);
     // block 0 of row 0, plain: C'(X1 << H) for every low part X1
     uint64_t b0[NB];
 #pragma unroll
     for (int x = 0; x < NB; ++x) b0[x] = Key<K>::entry_value(r0[lpos(0u, x)]);
-    for (int k = 0; k <= R2; ++k) {
-        const uint32_t item_next = k < R2 ? level_item(k + 1) : 0u;
-        const uint32_t blk_next = k < R2 ? level_blk(k + 1) : 0u;
-        // W of the block this thread finishes below, read ahead of phase 1
-        int64_t wv[NB];
-        if (blk) {
-            const int64_t *wp = Wr + (row | ((blk & 0xffffu) << CB));
-#pragma unroll
-            for (int x = 0; x < NB; ++x) wv[x] = wp[x];
-        }
+    // S = (S_H, 0, 0) with one request in S_H is a leaf: C = W
+    const bool single = (sh & (sh - 1u)) == 0;
+    auto level = [&](int k, const uint32_t &cur, uint32_t &nxt) __attribute__((always_inline)) {
+        nxt = item_load<THREADS>(k < R2 ? k + 1 : R2, 0);
         // A2 a proper submask of S2
-        if (item) run_item<K>(item, rS, r0, s.acc);
+        if (tid < c_items.end[k] - c_items.begin[k]) run_item<K>(cur, rS, r0, s.acc);
         lds_barrier();
         // A2 = S2: in-block pairs, one thread per block of this level; A =
         // (S_H, S2, A1) holds lowbit(S), B = (0, 0, S1 ^ A1) is in block 0
         // of row 0
-        if (blk) {
-            const uint32_t s2 = blk & 0xffffu;
-            const uint32_t base = sh | ((s2 << CB) << H);        // mask of (S_H, S2, X1 = 0)
+        if (tid >= c_blocks.begin[k] && tid < c_blocks.end[k]) {
+            const uint32_t s2 = own.s2;
+            const uint32_t tag = s2 << CB;
+            const uint32_t base = sh | (tag << H);               // mask of (S_H, S2, X1 = 0)
             uint64_t out[NB];
             uint32_t sp[NB];
             // the block's accumulated keys (cross pairs and this level's
             // items), read together before the dependent chain below
             uint64_t kacc[NB];
 #pragma unroll
-            for (int x = 0; x < NB; ++x) kacc[x] = Key<K>::key_value(s.acc[(s2 << CB) | x]);
-            // S = (S_H, 0, 0) with one request in S_H is a leaf: C = W
-            const bool leaf0 = s2 == 0 && (sh & (sh - 1u)) == 0;
+            for (int x = 0; x < NB; ++x) kacc[x] = Key<K>::key_value(s.acc[tag | x]);
+            const bool leaf0 = s2 == 0 && single;
             // S1 in order of popcount so that every A1 < S1 is ready; no
             // branches, so the reads above stay ahead of the chain
 #pragma unroll
@@ -1340,7 +1366,7 @@ __device__ __attribute__((always_inline)) inline void finalize_row(int m, uint32
 #pragma unroll
                 for (int s1 = 0; s1 < NB; ++s1) {
                     if (cpop(s1) != pc) continue;
-                    const int64_t w = wv[s1];
+                    const int64_t w = own.w[s1];
                     uint64_t kb = kacc[s1];
 #pragma unroll
                     for (int a1 = 0; a1 < NB; ++a1) {
@@ -1354,19 +1380,36 @@ __device__ __attribute__((always_inline)) inline void finalize_row(int m, uint32
                 }
             }
             const uint32_t sl = slot_of(s2);
+            // the tagged entries to the row, the plain ones and the splits
+            // over the entries just read
 #pragma unroll
             for (int x = 0; x < NB; ++x) {
-                const uint64_t tagged = out[x] | base | ((uint32_t)x << H);
-                rS[lpos(sl, x)] = Key<K>::entry(tagged);
-                Tt[row + lpos(sl, x)] = Key<K>::store(tagged);
-                Pt[row + lpos(sl, x)] = Key<K>::store(out[x]);
-                Sr[row | (s2 << CB) | (uint32_t)x] = sp[x];
+                rS[lpos(sl, x)] = Key<K>::entry(out[x] | base | ((uint32_t)x << H));
+                s.acc[tag | x] = Key<K>::store(out[x]);
             }
+            uint4 *sp4 = reinterpret_cast<uint4 *>(split + tag);
+            sp4[0] = make_uint4(sp[0], sp[1], sp[2], sp[3]);
+            sp4[1] = make_uint4(sp[4], sp[5], sp[6], sp[7]);
         }
         lds_barrier();
-        item = item_next;
-        blk = blk_next;
+    };
+    uint32_t ia = item_load<THREADS>(0, 0), ib;
+    for (int k = 0; k <= R2; k += 2) {
+        level(k, ia, ib);
+        if (k + 1 <= R2) level(k + 1, ib, ia);
     }
+    // the row to HBM: plain entries (the block at slot p, plane by plane),
+    // tagged entries (the LDS row's bits: an entry and its stored form are
+    // the same bits), splits (mask order)
+    for (int p = tid; p < NS2; p += THREADS) {
+        const uint4 *src = reinterpret_cast<const uint4 *>(s.acc + (slot_of((uint32_t)p) << CB));
+#pragma unroll
+        for (int q = 0; q < NB / 2; ++q) *reinterpret_cast<uint4 *>(Pt + row + lpos((uint32_t)p, 2 * q)) = src[q];
+    }
+    for (int p = tid; p < ROW / 2; p += THREADS)
+        reinterpret_cast<uint4 *>(Tt + row)[p] = reinterpret_cast<const uint4 *>(rS)[p];
+    for (int p = tid; p < ROW / 4; p += THREADS)
+        reinterpret_cast<uint4 *>(Sr + row)[p] = reinterpret_cast<const uint4 *>(split)[p];
 }
 
 // One self-pair item (as run_item, on narrow rows) whose group minimum goes to the
@@ -1410,27 +1453,6 @@ __device__ inline void run_item_self(uint32_t item, const uint32_t *rA, const ui
     }
 }
 
-// The block that thread t completes in finalize_row_narrow, and its W: the
-// t-th middle mask in order of popcount, so that the blocks of one level sit
-// in consecutive threads (threads past NS2 take none). Loaded before the
-// row's setup, whose waits then cover these loads too. Narrow keys hold
-// sum_i w(R_i) < 2^20, so every W fits 32 bits.
-struct OwnBlock {
-    uint32_t s2;
-    uint32_t w[NB];
-};
-__device__ inline void own_block_load(uint32_t sh, const int64_t *__restrict__ Wr, OwnBlock &o) {
-    const uint32_t t = threadIdx.x < (uint32_t)NS2 ? threadIdx.x : NS2 - 1u;
-    o.s2 = c_blocks.v[t];
-    const uint4 *wp = reinterpret_cast<const uint4 *>(Wr + ((sh << L) | (o.s2 << CB)));
-#pragma unroll
-    for (int q = 0; q < NB / 2; ++q) {
-        const uint4 v = wp[q];
-        o.w[2 * q] = v.x;
-        o.w[2 * q + 1] = v.z;
-    }
-}
-
 // Completes row S_H (non-empty) on narrow keys. In LDS: acc, the 64-bit
 // cross-pair keys of the row; rSn, row S_H (tagged, filled here); r0n, row 0
 // (plain); sacc, the narrow self-pair minima (4096 entries set to all ones
@@ -1452,7 +1474,7 @@ __device__ inline void own_block_load(uint32_t sh, const int64_t *__restrict__ W
 // and a wait for an older load would wait for every newer one.
 template <class K, int NT = THREADS>
 __device__ __attribute__((always_inline)) inline void finalize_row_narrow(
-        int m, uint32_t sh, const OwnBlock &own, uint64_t *acc, uint32_t *rSn, const uint32_t *r0n,
+        int m, uint32_t sh, const OwnBlock<uint32_t> &own, uint64_t *acc, uint32_t *rSn, const uint32_t *r0n,
         uint32_t *sacc, uint64_t *__restrict__ Pt, uint32_t *__restrict__ Tn, uint32_t *__restrict__ Pn,
         uint32_t *__restrict__ Sr) {
     static_assert(THREADS % NT == 0 && NT % kWave == 0 && NT >= NS2 / 4, "items and blocks per thread");
@@ -1461,12 +1483,6 @@ __device__ __attribute__((always_inline)) inline void finalize_row_narrow(
     const uint32_t row = sh << L;
     const uint64_t mask = ((uint64_t)1 << m) - 1u;
     const int tid = (int)threadIdx.x;
-    // item entry i of level k (any valid entry past the level's end)
-    auto item_load = [tid](int k, int i) -> uint32_t {
-        constexpr int last = kItems.n - 1;
-        const int it = c_items.begin[k] + tid + i * NT;
-        return c_items.v[it < last ? it : last];
-    };
     // block 0 of row 0, plain narrow: C(X1 << H) << L for every low part X1
     uint32_t b0n[NB];
 #pragma unroll
@@ -1476,7 +1492,7 @@ __device__ __attribute__((always_inline)) inline void finalize_row_narrow(
     auto level = [&](int k, const uint32_t (&cur)[IPT], uint32_t (&nxt)[IPT]) __attribute__((always_inline)) {
         const int kn = k < R2 ? k + 1 : R2;     // (the last level reads entries it does not use)
 #pragma unroll
-        for (int i = 0; i < IPT; ++i) nxt[i] = item_load(kn, i);
+        for (int i = 0; i < IPT; ++i) nxt[i] = item_load<NT>(kn, i);
         // A2 a proper submask of S2
         const int n_items = c_items.end[k] - c_items.begin[k];
 #pragma unroll
@@ -1546,7 +1562,7 @@ __device__ __attribute__((always_inline)) inline void finalize_row_narrow(
     };
     uint32_t ia[IPT], ib[IPT];
 #pragma unroll
-    for (int i = 0; i < IPT; ++i) ia[i] = item_load(0, i);
+    for (int i = 0; i < IPT; ++i) ia[i] = item_load<NT>(0, i);
     for (int k = 0; k <= R2; k += 2) {
         level(k, ia, ib);
         if (k + 1 <= R2) level(k + 1, ib, ia);
@@ -1910,9 +1926,9 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
     }
     lds_barrier();     // the staged keys are read before the buffers are reused
     if (fz) {
-        OwnBlock own;
+        OwnBlock<typename std::conditional<NARROW, uint32_t, int64_t>::type> own;
+        own_block_load(sh, Wr, own);
         if constexpr (NARROW) {
-            own_block_load(sh, Wr, own);
             copy_row(buf(0, 1), Pn, 0u);
             uint32_t *sacc = buf(1, 0);
             for (int e = threadIdx.x; e < ROW; e += THREADS) sacc[e] = Key<uint32_t>::none();
@@ -1922,7 +1938,7 @@ __global__ __launch_bounds__(THREADS) void k_rb_cross(int m, int h, uint32_t n_p
         copies_done();
         lds_barrier();
         if constexpr (NARROW) finalize_row_narrow<K>(m, sh, own, s.acc, buf(0, 0), buf(0, 1), buf(1, 0), Pt, Tn, Pn, Sr);
-        else finalize_row<K>(m, sh, s, s.r[0][0], s.r[0][1], Wr, Tt, Pt, Sr);
+        else finalize_row<K>(m, sh, own, s, s.r[0][0], s.r[0][1], Tt, Pt, Sr);
     }
 }
 
@@ -1961,12 +1977,17 @@ __global__ __launch_bounds__(THREADS) void k_rb_final(int m, int h, uint32_t row
     const uint32_t sh = unrank_colex(r, h, m - L);
     const uint32_t c = r < head_rows ? chunks : tail_chunks;
     const size_t slot = r < head_rows ? (size_t)r * chunks : tail_base + (size_t)(r - head_rows) * tail_chunks;
-    const uint64_t *src = partial + slot * ROW;
-    for (int e = threadIdx.x; e < ROW; e += THREADS) s.acc[e] = c ? src[e] : ~0ull;
+    OwnBlock<int64_t> own;
+    own_block_load(sh, Wr, own);
+    // the reduced cross-pair keys (direct copies, all in flight together),
+    // or none
+    if (c) copy_row<uint64_t>(s.acc, partial, (uint32_t)slot);
+    else
+        for (int e = threadIdx.x; e < ROW; e += THREADS) s.acc[e] = ~0ull;
     copy_row(s.r[0][1], Pt, 0u);
     copies_done();
     lds_barrier();
-    finalize_row<K>(m, sh, s, s.r[0][0], s.r[0][1], Wr, Tt, Pt, Sr);
+    finalize_row<K>(m, sh, own, s, s.r[0][0], s.r[0][1], Tt, Pt, Sr);
 }
 
 // k_rb_final on narrow rows, in workgroups of half the threads and half
@@ -1994,7 +2015,7 @@ __global__ __launch_bounds__(FINAL_THREADS) void k_rb_final_narrow(int m, int h,
     const uint32_t sh = unrank_colex(r, h, m - L);
     const uint32_t c = r < head_rows ? chunks : tail_chunks;
     const size_t slot = r < head_rows ? (size_t)r * chunks : tail_base + (size_t)(r - head_rows) * tail_chunks;
-    OwnBlock own;
+    OwnBlock<uint32_t> own;
     own_block_load(sh, Wr, own);
     // the reduced cross-pair keys (direct copies, all in flight together),
     // or none
