@@ -1513,9 +1513,24 @@ __device__ __attribute__((always_inline)) inline void finalize_row_narrow(
                 sself[0] = u0.x; sself[1] = u0.y; sself[2] = u0.z; sself[3] = u0.w;
                 sself[4] = u1.x; sself[5] = u1.y; sself[6] = u1.z; sself[7] = u1.w;
             }
-            uint64_t kacc[NB];
+            // The cross pairs' keys (cost << m | A_L << H | A_H) as narrow
+            // keys nacc = cost << L | A_L, and the least self-pair key that
+            // loses to them: the self pair's key (A_H = S_H) wins where
+            // nk < thr, with thr = nacc + 1 where S_H < A_H (equal narrow
+            // keys go to the smaller A_H); none stays all ones. The cost is
+            // below 2^20, so nacc + 1 does not overflow. The dependent chain
+            // below then runs on 32-bit keys alone.
+            uint32_t nacc[NB], thr[NB], aacc[NB];
+            const uint32_t hmask = (1u << H) - 1u;
 #pragma unroll
-            for (int x = 0; x < NB; ++x) kacc[x] = Key<K>::key_value(acc[tag | x]);
+            for (int x = 0; x < NB; ++x) {
+                const uint64_t ka = Key<K>::key_value(acc[tag | x]);
+                const bool none = ka == ~0ull;
+                const uint32_t n = ((uint32_t)(ka >> m) << L) | ((uint32_t)(ka >> H) & (ROW - 1u));
+                nacc[x] = none ? ~0u : n;
+                thr[x] = none ? ~0u : n + (sh < ((uint32_t)ka & hmask) ? 1u : 0u);
+                aacc[x] = (uint32_t)(ka & mask);
+            }
             const bool leaf0 = s2 == 0 && single;
             uint32_t on[NB], sp[NB];
             uint64_t cm[NB];
@@ -1532,17 +1547,16 @@ __device__ __attribute__((always_inline)) inline void finalize_row_narrow(
                         const uint32_t c = on[a1] + b0n[s1 ^ a1];
                         nk = c < nk ? c : nk;
                     }
-                    // as a 64-bit key: cost << m | A_L << H | A_H, A_H = S_H
-                    const uint64_t ks = nk == Key<uint32_t>::none()
-                                            ? ~0ull
-                                            : ((uint64_t)(nk >> L) << m) | ((uint64_t)(nk & (ROW - 1u)) << H) | sh;
-                    const uint64_t kb = kacc[s1] < ks ? kacc[s1] : ks;
-                    const uint64_t w = own.w[s1];
+                    const bool self = nk < thr[s1];
+                    const uint32_t best = self ? nk : nacc[s1];
+                    const uint32_t w = own.w[s1];
                     const bool leaf = s1 == 0 && leaf0;
-                    const uint64_t c = leaf ? w : (kb >> m) - w;
-                    sp[s1] = leaf ? 0u : (uint32_t)(kb & mask);
-                    cm[s1] = c << m;
-                    on[s1] = ((uint32_t)c << L) | tag | (uint32_t)s1;
+                    const uint32_t c = leaf ? w : (best >> L) - w;
+                    on[s1] = (c << L) | tag | (uint32_t)s1;
+                    // off the chain: the split A (A_L << H | A_H) and the
+                    // plain entry
+                    sp[s1] = leaf ? 0u : self ? ((nk & (ROW - 1u)) << H) | sh : aacc[s1];
+                    cm[s1] = (uint64_t)c << m;
                 }
             }
             // the plain entries and the splits, over the entries just read
