@@ -342,29 +342,39 @@ __global__ void k_rac_init(Rac R) {
     }
 }
 
-// mutual-best pairs of positive value
-__global__ void k_rac_pairs(Rac R) {
-    for (int a = blockIdx.x * blockDim.x + threadIdx.x; a < R.m; a += gridDim.x * blockDim.x) {
-        if (!R.act[a] || R.best_v[a] <= 0) continue;
-        const int32_t b = R.best_p[a];
-        if (b <= a || R.best_p[b] != a) continue;
-        const int i = atomicAdd(&R.h->n_rec, 1);
-        if (i >= R.m - 1) { atomicOr(&R.h->err, GERR_INVALID); continue; }   // cannot happen
-        R.ra[i] = a;
-        R.rb[i] = b;
-        R.rgain[i] = R.best_v[a];
-    }
-}
-
-// one wave per merge of the round: I(C) = I(A) ∩ I(B) in place of I(A),
-// D(B) = I(B) \ I(A) and D(A) = I(A) \ I(B) to the packed lists, and the
-// merges that formed A and B
-__global__ void k_rac_merge(Rac R, int round) {
+// One wave per row a: if a and its best partner b > a are mutual best with
+// positive value, a new merge record i (a, b, value) is taken, and the wave
+// merges: I(C) = I(A) ∩ I(B) in place of I(A), D(B) = I(B) \ I(A) and
+// D(A) = I(A) \ I(B) to the packed lists, and the merges that formed A and
+// B. The pair test reads only values that no merge of the round writes
+// (best values and partners; a partner b that a merge deactivates fails the
+// test b > best partner as well), so merging while other waves still test
+// finds the same pairs. Record numbers within a round follow the atomic
+// order; the sequence is recovered by sorting on the pair order.
+__global__ void k_rac_pairs_merge(Rac R, int round) {
     const int lane = threadIdx.x & (kWave - 1);
-    const int lo = R.h->lo, hi = min(R.h->n_rec, R.m - 1);
     const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) / kWave;
-    for (int64_t i = lo + (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) / kWave; i < hi; i += nwaves) {
-        const int32_t a = R.ra[i], b = R.rb[i];
+    for (int64_t a = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) / kWave; a < R.m; a += nwaves) {
+        int rec = -1;
+        int32_t b = -1;
+        if (lane == 0 && R.act[a] && R.best_v[a] > 0) {
+            b = R.best_p[a];
+            if (b > a && R.best_p[b] == (int32_t)a) {
+                const int i = atomicAdd(&R.h->n_rec, 1);
+                if (i >= R.m - 1) {
+                    atomicOr(&R.h->err, GERR_INVALID);   // cannot happen
+                } else {
+                    R.ra[i] = (int32_t)a;
+                    R.rb[i] = b;
+                    R.rgain[i] = R.best_v[a];
+                    rec = i;
+                }
+            }
+        }
+        rec = __shfl(rec, 0, kWave);
+        if (rec < 0) continue;
+        b = __shfl(b, 0, kWave);
+        const int64_t i = rec;
         int32_t *sa = R.sig + R.req_off[a];
         const int32_t *sb = R.sig + R.req_off[b];
         const int64_t na = R.sig_len[a], nb = R.sig_len[b];
@@ -867,19 +877,18 @@ extern "C" int mpt_greedy_hierarchy(int m, int64_t n_chunks, int64_t nnz, const 
     }
     // rounds in batches without host synchronisation; a round that finds
     // no pair changes nothing, so the batch's last round tells whether the
-    // rounds are over
+    // rounds are over. Batches of 8, 8, 16 and then 32 rounds: few
+    // synchronisations, at most 31 empty rounds (a few µs each) at the end.
     int n_rec = 0;
     {
         LaunchScope ls("g_rounds", (double)(m - 1), s);
-        const int g_rows = grid_for((int64_t)m, 256);
-        const int g_rec = std::max(1, std::min(4096, (m + 3) / 4));        // waves: one per record
+        const int g_rec = std::max(1, std::min(4096, (m + 3) / 4));        // waves: one per row
         const int g_cols = grid_for((int64_t)m * std::max(1, m / 2), 256, 2048);
         const int g_resc = std::max(1, std::min(m, 2048));                  // workgroups: one per marked row
-        constexpr int kBatch = 8;
         for (int round = 0;;) {
-            for (int k = 0; k < kBatch; ++k, ++round) {
-                k_rac_pairs<<<g_rows, 256, 0, s>>>(R);
-                k_rac_merge<<<g_rec, 4 * kWave, 0, s>>>(R, round);
+            const int batch = round < 16 ? 8 : round < 32 ? 16 : 32;
+            for (int k = 0; k < batch; ++k, ++round) {
+                k_rac_pairs_merge<<<g_rec, 4 * kWave, 0, s>>>(R, round);
                 k_rac_rows<<<g_cols, 256, 0, s>>>(R, round);
                 k_rac_rescan<<<g_resc, kRescThreads, 0, s>>>(R, round);
             }
@@ -890,7 +899,7 @@ extern "C" int mpt_greedy_hierarchy(int m, int64_t n_chunks, int64_t nnz, const 
             if (hh.err) return fail(MPT_E_INTERNAL, "greedy rounds left an inconsistent state");   // cannot happen
             n_rec = std::min(hh.n_rec, m - 1);
             if (hh.last_pairs == 0) break;
-            if (round > m + kBatch) return fail(MPT_E_INTERNAL, "greedy rounds do not end");   // cannot happen
+            if (round > m + 32) return fail(MPT_E_INTERNAL, "greedy rounds do not end");   // cannot happen
         }
     }
     {
