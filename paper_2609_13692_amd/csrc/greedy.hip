@@ -50,7 +50,7 @@ struct GHeader {
     int32_t lo;                  // first record of the current round
     int32_t n_resc[2];           // rows marked for a rescan, by round parity
     int32_t last_pairs;          // merges of the last finished round
-    int32_t pad1;
+    int32_t bv_done;             // spanning tree: 1 once one component is left
     unsigned long long dcursor;  // next free slot of the packed D lists
     int64_t pad[26];
 };
@@ -665,18 +665,28 @@ __device__ inline uint32_t edge_id(int u, int v) {
     return (lo << 14) | hi;                      // m <= 2^14
 }
 
-__global__ void k_bv_init(int m, int32_t *comp, unsigned long long *total) {
+// Borůvka's rounds after the last component has formed change nothing:
+// the hook kernel raises h->bv_done when a root finds no edge out of its
+// component (P is complete, so that root's component holds every vertex),
+// and the later rounds' kernels return at once.
+__global__ void k_bv_init(int m, int32_t *comp, GHeader *h) {
     for (int v = blockIdx.x * blockDim.x + threadIdx.x; v < m; v += gridDim.x * blockDim.x) comp[v] = v;
-    if (blockIdx.x == 0 && threadIdx.x == 0) *total = 0;
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        h->total = 0;
+        h->bv_done = 0;
+    }
 }
 
-__global__ void k_bv_reset(int m, int64_t *cw, uint32_t *ce) {
+__global__ void k_bv_reset(int m, int64_t *cw, uint32_t *ce, const GHeader *h) {
+    if (h->bv_done) return;
     for (int v = blockIdx.x * blockDim.x + threadIdx.x; v < m; v += gridDim.x * blockDim.x) { cw[v] = -1; ce[v] = ~0u; }
 }
 
 // best edge of every vertex to another component (one wave per vertex),
 // folded into its component's best weight
-__global__ void k_bv_vertex(int m, const int64_t *P, const int32_t *comp, int64_t *vw, uint32_t *ve, int64_t *cw) {
+__global__ void k_bv_vertex(int m, const int64_t *P, const int32_t *comp, int64_t *vw, uint32_t *ve, int64_t *cw,
+                            const GHeader *h) {
+    if (h->bv_done) return;
     const int lane = threadIdx.x & (kWave - 1);
     const int64_t u = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / kWave;
     if (u >= m) return;
@@ -703,7 +713,8 @@ __global__ void k_bv_vertex(int m, const int64_t *P, const int32_t *comp, int64_
 
 // among the vertices that reach their component's best weight, the smallest edge
 __global__ void k_bv_edge(int m, const int32_t *comp, const int64_t *vw, const uint32_t *ve, const int64_t *cw,
-                          uint32_t *ce) {
+                          uint32_t *ce, const GHeader *h) {
+    if (h->bv_done) return;
     for (int u = blockIdx.x * blockDim.x + threadIdx.x; u < m; u += gridDim.x * blockDim.x) {
         const int32_t cu = comp[u];
         if (vw[u] >= 0 && vw[u] == cw[cu]) atomicMin(&ce[cu], ve[u]);
@@ -712,21 +723,28 @@ __global__ void k_bv_edge(int m, const int32_t *comp, const int64_t *vw, const u
 
 // every component hooks onto the component across its best edge, except
 // the smaller one of a mutual pair; the hooking side adds the edge weight
+// (no early return here: a workgroup that saw bv_done raised by another
+// one of this launch would skip hooks; with one component there are none)
 __global__ void k_bv_hook(int m, const int32_t *comp, const int64_t *cw, const uint32_t *ce, int32_t *par,
-                          unsigned long long *total) {
+                          GHeader *h) {
     for (int c = blockIdx.x * blockDim.x + threadIdx.x; c < m; c += gridDim.x * blockDim.x) {
         par[c] = c;
-        if (comp[c] != c || ce[c] == ~0u) continue;
+        if (comp[c] != c) continue;
+        if (ce[c] == ~0u) {
+            h->bv_done = 1;
+            continue;
+        }
         const int lo = (int)(ce[c] >> 14), hi = (int)(ce[c] & 0x3fffu);
         const int32_t d = comp[lo] == c ? comp[hi] : comp[lo];
         if (ce[d] == ce[c] && c < d) continue;           // d hooks onto c
         par[c] = d;
-        atomicAdd(total, (unsigned long long)cw[c]);
+        atomicAdd(&h->total, (unsigned long long)cw[c]);
     }
 }
 
 // new component of every vertex: follow the hooks to a root
-__global__ void k_bv_jump(int m, int32_t *comp, const int32_t *par) {
+__global__ void k_bv_jump(int m, int32_t *comp, const int32_t *par, const GHeader *h) {
+    if (h->bv_done) return;
     for (int v = blockIdx.x * blockDim.x + threadIdx.x; v < m; v += gridDim.x * blockDim.x) {
         int32_t r = comp[v];
         for (int guard = 0; par[r] != r && guard < m; ++guard) r = par[r];
@@ -956,14 +974,14 @@ extern "C" int mpt_spanning_tree_bound(int m, const int64_t *P, int64_t *mst_wei
     int rounds = 0;
     while ((1 << rounds) < m) ++rounds;
     const int gv = grid_for(m, 256);
-    k_bv_init<<<gv, 256, 0, s>>>(m, comp, &h->total);
+    k_bv_init<<<gv, 256, 0, s>>>(m, comp, h);
     for (int r = 0; r < rounds; ++r) {
         LaunchScope ls("g_boruvka", 8.0 * (double)m * m, s);
-        k_bv_reset<<<gv, 256, 0, s>>>(m, cw, ce);
-        k_bv_vertex<<<(m + 3) / 4, 4 * kWave, 0, s>>>(m, P, comp, vw, ve, cw);
-        k_bv_edge<<<gv, 256, 0, s>>>(m, comp, vw, ve, cw, ce);
-        k_bv_hook<<<gv, 256, 0, s>>>(m, comp, cw, ce, par, &h->total);
-        k_bv_jump<<<gv, 256, 0, s>>>(m, comp, par);
+        k_bv_reset<<<gv, 256, 0, s>>>(m, cw, ce, h);
+        k_bv_vertex<<<(m + 3) / 4, 4 * kWave, 0, s>>>(m, P, comp, vw, ve, cw, h);
+        k_bv_edge<<<gv, 256, 0, s>>>(m, comp, vw, ve, cw, ce, h);
+        k_bv_hook<<<gv, 256, 0, s>>>(m, comp, cw, ce, par, h);
+        k_bv_jump<<<gv, 256, 0, s>>>(m, comp, par, h);
     }
     MPT_HIP_TRY(hipGetLastError());
     unsigned long long total = 0;
