@@ -641,7 +641,7 @@ int l_prepare(int m, int64_t n_chunks, int64_t nnz, const int64_t *w, const int6
     int64_t *base = (int64_t *)(ws + L.base);
     {
         LaunchScope ls("l_sort_requests", (double)m, s);
-        if ((rc = sort_requests(ord, m, L.mpad, off, seqs, s))) return rc;
+        if ((rc = sort_requests(ord, rank, m, L.mpad, off, seqs, s))) return rc;
     }
     {
         LaunchScope ls("l_lcp", (double)nnz, s);

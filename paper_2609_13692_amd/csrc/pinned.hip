@@ -288,7 +288,8 @@ extern "C" int mpt_pinned_split(int m, int64_t n_chunks, int64_t nnz, const int6
         k_p_keys<<<grid_for(L.kpad, 256), 256, 0, s>>>(m, t, nnz, L.kpad, req_off, req_chunks, keys);
         if ((rc = sort_keys(keys, L.kpad, s))) return rc;
         k_p_free_chunks<<<grid_for(std::max<int64_t>(nnz, 1), 256), 256, 0, s>>>(m, rf_off, keys, rf_chunks);
-        if ((rc = sort_requests(ord, m, L.mpad, rf_off, rf_chunks, s))) return rc;
+        // (gstart, written after the sort, is its scratch)
+        if ((rc = sort_requests(ord, gstart, m, L.mpad, rf_off, rf_chunks, s))) return rc;
         k_p_group_starts<<<grid_for(m, 256), 256, 0, s>>>(m, ord, rf_off, rf_chunks, gstart);
         k_p_max_scan<<<1, 1024, 0, s>>>(m, gstart);
         k_p_leaders<<<grid_for(m, 256), 256, 0, s>>>(m, ord, gstart, rf_off, lead, rep, roff);

@@ -202,3 +202,37 @@ def test_cache_simulation_at_m_8192():
     for k in (0, 3):
         W, C = windows[k], caps[k]
         assert got[k] == oracle.lru_cache_cost(inst, lay, oracle.window_schedule(inst, lay, W), C), (W, C)
+
+
+def order_edge_instance(m, seed):
+    """Requests whose sequences stress the lexicographic request order: a
+    common first 8 chunks with tails that differ late, prefixes at length
+    8 and below, duplicates (ordered by index), empty requests, and random
+    sequences over a small alphabet (long shared prefixes)."""
+    rng = np.random.default_rng(seed)
+    base = [int(x) for x in rng.permutation(40)[:8]]
+    fixed = [base + [50, 51, 52, 53], base + [50, 51, 52, 54], base + [50, 51], base, base[:7] + [60],
+             base + [50, 51, 52, 53], [], [3], [3, 1], [1], base[:3], base[:3] + [61], [], base]
+    sets = []
+    while len(sets) < m:
+        if rng.random() < 0.4:
+            sets.append(list(fixed[int(rng.integers(len(fixed)))]))
+        else:
+            n = int(rng.integers(0, 17))
+            head = base[:int(rng.integers(0, 9))] if rng.random() < 0.6 else []
+            rest = [int(x) for x in rng.permutation(np.arange(40, 64))[:max(0, n - len(head))]]
+            sets.append(head + rest)
+    return wl.from_sets(sets, [int(x) for x in rng.integers(1, 9, 64)], 64)
+
+
+@pytest.mark.parametrize("m", [300, 4096, 17000])
+def test_request_order_edge_cases(m):
+    """The request order behind the trie cost and the DFS order, on ties,
+    prefixes and sequences equal on their first 8 chunks: up to 16384
+    requests it comes from all-pairs ranks, above from the bitonic sort."""
+    inst = order_edge_instance(m, seed=m)
+    lay = np.asarray(inst.req_chunks, dtype=np.int32)
+    L = mpt.Layouts(inst)
+    say(f"[gpu layout] request order m={m}")
+    assert L.cost(L.seqs(lay)) == oracle.trie_cost(inst, lay)
+    assert np.array_equal(L.dfs.cpu().numpy(), oracle.dfs_schedule(inst, lay))
