@@ -67,6 +67,23 @@ static __global__ __launch_bounds__(kSortThreads) void k_sort_tile_merge(uint64_
 
 }  // namespace bitonic_detail
 
+// Short segments: the position of lane e's entry (key r, e < n <= 64) in
+// its wave's segment, ascending by key, ties by lane: the number of lanes f
+// < n with a smaller key, or an equal one and f < e. dup: some other lane
+// holds an equal key. One shuffle per lane of the segment.
+constexpr int kSegMax = 64;
+__device__ inline int seg_rank(uint32_t r, int n, bool &dup) {
+    const int e = (int)(threadIdx.x & 63u);
+    int pos = 0;
+    dup = false;
+    for (int f = 0; f < n; ++f) {
+        const uint32_t o = (uint32_t)__shfl((int)r, f, 64);
+        pos += (o < r || (o == r && f < e)) ? 1 : 0;
+        dup = dup || (o == r && f != e);
+    }
+    return pos;
+}
+
 // n must be a power of two and at least kSortTile
 inline int sort_keys(uint64_t *keys, int64_t n, hipStream_t s) {
     using namespace bitonic_detail;

@@ -34,7 +34,9 @@ using mptlib::align256;
 using mptlib::fail;
 using mptlib::grid_for;
 using mptlib::LaunchScope;
+using mptlib::kSegMax;
 using mptlib::kSortTile;
+using mptlib::seg_rank;
 using mptlib::sort_keys;
 
 constexpr int kWave = 64;
@@ -52,7 +54,8 @@ struct GHeader {
     int32_t last_pairs;          // merges of the last finished round
     int32_t bv_done;             // spanning tree: 1 once one component is left
     unsigned long long dcursor;  // next free slot of the packed D lists
-    int64_t pad[26];
+    int64_t max_len;             // longest request list
+    int64_t pad[25];
 };
 static_assert(sizeof(GHeader) == 256, "header is one 256-byte block");
 
@@ -151,14 +154,20 @@ __device__ inline int64_t find_sorted(const int32_t *a, int64_t n, int32_t x) {
 // validation and keys
 
 __global__ void k_g_header(GHeader *h) {
-    if (threadIdx.x == 0) { h->err = 0; h->total = 0; }
+    if (threadIdx.x == 0) { h->err = 0; h->total = 0; h->max_len = 0; }
 }
 
 __global__ void k_g_check_offsets(int m, int64_t nnz, const int64_t *req_off, GHeader *h) {
     bool ok = true;
-    for (int i = threadIdx.x; i < m; i += blockDim.x) ok = ok && req_off[i] <= req_off[i + 1];
+    int64_t mx = 0;
+    for (int i = threadIdx.x; i < m; i += blockDim.x) {
+        const int64_t len = req_off[i + 1] - req_off[i];
+        ok = ok && len >= 0;
+        mx = len > mx ? len : mx;
+    }
     if (threadIdx.x == 0) ok = ok && req_off[0] == 0 && req_off[m] == nnz;
     if (!ok) atomicOr(&h->err, GERR_INVALID);
+    if (mx > 0) atomicMax((long long *)&h->max_len, (long long)mx);
 }
 
 __global__ void k_g_check_weights(int64_t n_chunks, const int64_t *w, GHeader *h) {
@@ -195,16 +204,36 @@ __global__ void k_g_keys(int m, int64_t n_chunks, int64_t nnz, int64_t npad, con
 
 // sorted keys -> request lists (chunk ids ascending inside each request),
 // demand lists (request ids ascending inside each chunk); a repeated chunk
-// inside a request is two equal adjacent (request, chunk) keys
+// inside a request is two equal adjacent (request, chunk) keys. keys1 null:
+// the request lists are already in sig (k_g_sig_short).
 __global__ void k_g_lists(int m, int64_t nnz, const uint64_t *keys1, const uint64_t *keys2, int32_t *sig,
                           int32_t *sig_len, int32_t *dem, const int64_t *req_off, GHeader *h) {
     for (int64_t j = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; j < nnz; j += (int64_t)gridDim.x * blockDim.x) {
-        sig[j] = (int32_t)(keys1[j] & 0xffffffffu);
         dem[j] = (int32_t)(keys2[j] & 0xffffffffu);
+        if (!keys1) continue;
+        sig[j] = (int32_t)(keys1[j] & 0xffffffffu);
         if (j > 0 && keys1[j] == keys1[j - 1]) atomicOr(&h->err, GERR_DUP);
     }
     for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < m; i += (int64_t)gridDim.x * blockDim.x)
         sig_len[i] = (int32_t)(req_off[i + 1] - req_off[i]);
+}
+
+// request lists when every request has at most kSegMax chunks: one wave
+// per request ranks its chunks (chunk ids validated already)
+__global__ void k_g_sig_short(int m, const int64_t *req_off, const int32_t *req_chunks, int32_t *sig, GHeader *h) {
+    const int lane = (int)(threadIdx.x & (kWave - 1));
+    const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) / kWave;
+    for (int64_t i = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) / kWave; i < m; i += nwaves) {
+        const int64_t o = req_off[i];
+        const int n = (int)(req_off[i + 1] - o);
+        const uint32_t c = lane < n ? (uint32_t)req_chunks[o + lane] : 0u;
+        bool dup;
+        const int pos = seg_rank(c, n, dup);
+        if (lane < n) {
+            sig[o + pos] = (int32_t)c;
+            if (dup) atomicOr(&h->err, GERR_DUP);
+        }
+    }
 }
 
 // dem_off[x] = first slot of chunk x in the (chunk, request) order
@@ -769,7 +798,7 @@ int g_check_ws(const GLayout &L, void *ws, size_t bytes) {
     return MPT_OK;
 }
 
-int g_read_errors(GHeader *h, hipStream_t s, int64_t *request_total = nullptr) {
+int g_read_errors(GHeader *h, hipStream_t s, int64_t *request_total = nullptr, int64_t *max_len = nullptr) {
     GHeader hh;
     MPT_HIP_TRY(hipMemcpyAsync(&hh, h, sizeof hh, hipMemcpyDeviceToHost, s));
     MPT_HIP_TRY(hipStreamSynchronize(s));
@@ -779,6 +808,7 @@ int g_read_errors(GHeader *h, hipStream_t s, int64_t *request_total = nullptr) {
     if (hh.err & GERR_DUP) return fail(MPT_E_DUP, "a chunk is repeated inside one request");
     if (hh.total >= (1ull << 61)) return fail(MPT_E_OVERFLOW, "sum of request weights reaches 2^61");
     if (request_total) *request_total = (int64_t)hh.total;
+    if (max_len) *max_len = hh.max_len;
     return MPT_OK;
 }
 
@@ -798,16 +828,22 @@ int g_prepare(int m, int64_t n_chunks, int64_t nnz, const int64_t *chunk_w, cons
                                                       keys2, h);
     }
     MPT_HIP_TRY(hipGetLastError());
-    int rc = g_read_errors(h, s);
+    int64_t max_len = 0;
+    int rc = g_read_errors(h, s, nullptr, &max_len);
     if (rc) return rc;
-    {
-        LaunchScope ls("g_sort", 2.0 * (double)L.npad, s);
-        if ((rc = sort_keys(keys1, L.npad, s))) return rc;
-        if ((rc = sort_keys(keys2, L.npad, s))) return rc;
-    }
     int32_t *sig = (int32_t *)(ws + L.sig), *sig_len = (int32_t *)(ws + L.sig_len), *dem = (int32_t *)(ws + L.dem);
     int64_t *dem_off = (int64_t *)(ws + L.dem_off);
-    k_g_lists<<<grid_for(std::max<int64_t>(nnz, m), 256), 256, 0, s>>>(m, nnz, keys1, keys2, sig, sig_len, dem, req_off, h);
+    // short requests: the request lists by ranks inside each request, the
+    // (request, chunk) keys unsorted and unused
+    const bool short_lists = max_len <= kSegMax;
+    {
+        LaunchScope ls("g_sort", 2.0 * (double)L.npad, s);
+        if (short_lists) k_g_sig_short<<<std::max(1, (m + 3) / 4), 4 * kWave, 0, s>>>(m, req_off, req_chunks, sig, h);
+        else if ((rc = sort_keys(keys1, L.npad, s))) return rc;
+        if ((rc = sort_keys(keys2, L.npad, s))) return rc;
+    }
+    k_g_lists<<<grid_for(std::max<int64_t>(nnz, m), 256), 256, 0, s>>>(m, nnz, short_lists ? nullptr : keys1, keys2, sig,
+                                                                        sig_len, dem, req_off, h);
     k_g_dem_off<<<grid_for(n_chunks + 1, 256), 256, 0, s>>>(n_chunks, nnz, keys2, dem_off);
     MPT_HIP_TRY(hipGetLastError());
     if ((rc = g_read_errors(h, s, request_total))) return rc;

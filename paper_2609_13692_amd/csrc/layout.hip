@@ -41,8 +41,10 @@ namespace {
 using mptlib::align256;
 using mptlib::fail;
 using mptlib::grid_for;
+using mptlib::kSegMax;
 using mptlib::kSortTile;
 using mptlib::LaunchScope;
+using mptlib::seg_rank;
 using mptlib::sort_keys;
 using mptlib::kSeqSortTile;
 using mptlib::sort_requests;
@@ -56,7 +58,8 @@ struct LHeader {
     uint32_t pad0;
     unsigned long long total;   // sum of the sequence weights
     unsigned long long cost;    // trie cost
-    int64_t pad[29];
+    int64_t max_len;            // longest sequence
+    int64_t pad[28];
 };
 static_assert(sizeof(LHeader) == 256, "header is one 256-byte block");
 
@@ -114,14 +117,20 @@ LLayout l_layout(int m, int64_t n_chunks, int64_t nnz, int n_cfg) {
 // validation
 
 __global__ void k_l_header(LHeader *h) {
-    if (threadIdx.x == 0) { h->err = 0; h->total = 0; h->cost = 0; }
+    if (threadIdx.x == 0) { h->err = 0; h->total = 0; h->cost = 0; h->max_len = 0; }
 }
 
 __global__ void k_l_check_offsets(int m, int64_t nnz, const int64_t *off, LHeader *h) {
     bool ok = true;
-    for (int i = threadIdx.x; i < m; i += blockDim.x) ok = ok && off[i] <= off[i + 1];
+    int64_t mx = 0;
+    for (int i = threadIdx.x; i < m; i += blockDim.x) {
+        const int64_t len = off[i + 1] - off[i];
+        ok = ok && len >= 0;
+        mx = len > mx ? len : mx;
+    }
     if (threadIdx.x == 0) ok = ok && off[0] == 0 && off[m] == nnz;
     if (!ok) atomicOr(&h->err, LERR_INVALID);
+    if (mx > 0) atomicMax((long long *)&h->max_len, (long long)mx);
 }
 
 __global__ void k_l_check_chunks(int64_t nnz, int64_t n_chunks, const int32_t *seqs, const int64_t *w, LHeader *h) {
@@ -136,7 +145,7 @@ __global__ void k_l_check_chunks(int64_t nnz, int64_t n_chunks, const int32_t *s
     }
 }
 
-int l_read_errors(LHeader *h, hipStream_t s) {
+int l_read_errors(LHeader *h, hipStream_t s, int64_t *max_len = nullptr) {
     LHeader hh;
     MPT_HIP_TRY(hipMemcpyAsync(&hh, h, sizeof hh, hipMemcpyDeviceToHost, s));
     MPT_HIP_TRY(hipStreamSynchronize(s));
@@ -144,6 +153,7 @@ int l_read_errors(LHeader *h, hipStream_t s) {
     if (hh.err & LERR_RANGE) return fail(MPT_E_RANGE, "a chunk id is outside [0, n_chunks)");
     if (hh.err & LERR_WEIGHT) return fail(MPT_E_WEIGHT, "a chunk weight is <= 0 or > 2^32");
     if (hh.total >= (1ull << 61)) return fail(MPT_E_OVERFLOW, "sum of sequence weights reaches 2^61");
+    if (max_len) *max_len = hh.max_len;
     return MPT_OK;
 }
 
@@ -198,6 +208,24 @@ __global__ void k_l_layout_out(int64_t nnz, const uint64_t *keys, const int32_t 
     for (int64_t j = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; j < nnz; j += (int64_t)gridDim.x * blockDim.x) {
         const uint32_t r = (uint32_t)(keys[j] & 0xffffffffu);
         seqs[j] = kind == MPT_ORDER_ID ? (int32_t)r : inv[r];
+    }
+}
+
+// the layout when every request has at most kSegMax chunks: one wave per
+// request ranks its chunks by their position in the order (the id, or the
+// popularity rank), ties by slot
+__global__ void k_l_layout_short(int m, const int64_t *req_off, const int32_t *chunks, const int32_t *rank, int kind,
+                                 int32_t *seqs) {
+    const int lane = (int)(threadIdx.x & (kWave - 1));
+    const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) / kWave;
+    for (int64_t i = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) / kWave; i < m; i += nwaves) {
+        const int64_t o = req_off[i];
+        const int n = (int)(req_off[i + 1] - o);
+        const int32_t x = lane < n ? chunks[o + lane] : 0;
+        const uint32_t r = lane < n ? (kind == MPT_ORDER_ID ? (uint32_t)x : (uint32_t)rank[x]) : 0u;
+        bool dup;
+        const int pos = seg_rank(r, n, dup);
+        if (lane < n) seqs[o + pos] = x;
     }
 }
 
@@ -697,20 +725,28 @@ extern "C" int mpt_global_order_layout(int m, int64_t n_chunks, int64_t nnz, con
     k_l_check_offsets<<<1, 256, 0, s>>>(m, nnz, req_off, h);
     if (nnz > 0) k_l_check_chunks<<<grid_for(nnz, 256), 256, 0, s>>>(nnz, n_chunks, req_chunks, nullptr, h);
     MPT_HIP_TRY(hipGetLastError());
-    if ((rc = l_read_errors(h, s))) return rc;
+    int64_t max_len = 0;
+    if ((rc = l_read_errors(h, s, &max_len))) return rc;
     if (nnz == 0) return MPT_OK;
     uint64_t *keys = (uint64_t *)(ws + L.keys);
     int32_t *rank = (int32_t *)(ws + L.crank), *inv = (int32_t *)(ws + L.cinv);
     const int64_t kpad = L.kpad;
     LaunchScope ls("l_global_order", (double)nnz, s);
     if (order_kind == MPT_ORDER_POPULARITY) {
+        // (count, id) keys of the chunks, padded to a power of two
+        const int64_t cpad = std::max<int64_t>(pow2_at_least(n_chunks), kSortTile);
         k_l_fill_i32<<<grid_for(n_chunks, 256), 256, 0, s>>>(rank, n_chunks, 0);
         k_l_count<<<grid_for(nnz, 256), 256, 0, s>>>(nnz, req_chunks, rank);
-        k_l_fill_u64<<<grid_for(kpad, 256), 256, 0, s>>>(keys, kpad, ~0ull);
+        k_l_fill_u64<<<grid_for(cpad, 256), 256, 0, s>>>(keys, cpad, ~0ull);
         k_l_pop_keys<<<grid_for(n_chunks, 256), 256, 0, s>>>(n_chunks, rank, keys);
-        if ((rc = sort_keys(keys, kpad, s))) return rc;
+        if ((rc = sort_keys(keys, cpad, s))) return rc;
         k_l_pop_rank<<<grid_for(n_chunks, 256), 256, 0, s>>>(n_chunks, keys, rank);
-        k_l_inverse<<<grid_for(n_chunks, 256), 256, 0, s>>>(n_chunks, rank, inv);
+        if (max_len > kSegMax) k_l_inverse<<<grid_for(n_chunks, 256), 256, 0, s>>>(n_chunks, rank, inv);
+    }
+    if (max_len <= kSegMax) {
+        k_l_layout_short<<<std::max(1, (m + 3) / 4), 4 * kWave, 0, s>>>(m, req_off, req_chunks, rank, order_kind, seqs);
+        MPT_HIP_TRY(hipGetLastError());
+        return MPT_OK;
     }
     k_l_layout_keys<<<grid_for(kpad, 256), 256, 0, s>>>(m, nnz, kpad, req_off, req_chunks, rank, order_kind, keys);
     if ((rc = sort_keys(keys, kpad, s))) return rc;

@@ -250,3 +250,19 @@ def test_largest_m_properties():
     parent = got["parent"]
     assert parent.size == 2 * m - 1 and parent[-1] == -1
     assert np.all(np.bincount(parent[:-1], minlength=2 * m - 1)[m:] == 2)
+
+
+@pytest.mark.parametrize("n", [64, 65])
+def test_list_lengths_at_the_short_path_limit(n):
+    """Requests of up to 64 chunks have their lists ranked inside each
+    request, longer ones go through the key sort: both sides of the limit,
+    and a repeated chunk detected on each."""
+    rng = np.random.default_rng(n)
+    sets = [rng.permutation(n + 10)[:n].tolist() for _ in range(6)] + [list(range(3))]
+    inst = wl.from_sets(sets, rng.integers(1, 50, size=n + 10).tolist(), n + 10)
+    assert_same(inst, gpu_greedy(inst), oracle.greedy_solve(inst))
+    g = mpt.Greedy(inst)
+    g.req_chunks[1] = g.req_chunks[0]
+    with pytest.raises(mpt.MptError) as e:
+        g.hierarchy()
+    assert e.value.status == -3

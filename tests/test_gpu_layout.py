@@ -31,7 +31,11 @@ def max_request(inst):
 
 
 def test_global_orders_match_oracle():
+    # (requests of up to 64 chunks are ordered inside each request, longer
+    # ones by a key sort: both occur below)
     for inst in (wl.config(1), wl.gen_loo(9), wl.random_small(m=40, u=70, kmin=0, kmax=12, wmax=9, seed=3),
+                 wl.random_small(m=20, u=400, kmin=40, kmax=120, wmax=9, seed=4),
+                 wl.random_small(m=30, u=200, kmin=60, kmax=64, wmax=9, seed=6),
                  wl.trace_config("trace_512"), wl.trace_config("trace_4096")):
         say(f"[gpu layout] global orders {inst.name} m={inst.m}")
         L = mpt.Layouts(inst)
