@@ -2068,21 +2068,24 @@ __global__ __launch_bounds__(THREADS) void k_rb_row0(int m, const int64_t *__res
                                                      uint64_t *__restrict__ Pt, uint32_t *__restrict__ Pn,
                                                      uint32_t *__restrict__ Sr) {
     __shared__ uint64_t c[ROW];
+    __shared__ int64_t wrow[ROW];          // W of row 0, read once
     __shared__ uint32_t spl[ROW];
     const int H = m - L;
     const uint64_t mask = ((uint64_t)1 << m) - 1u;
     for (int e = threadIdx.x; e < ROW; e += THREADS) {
-        c[e] = __popc((uint32_t)e) == 1 ? (uint64_t)Wr[e] << m : 0u;     // C(empty) = 0 is never a part
+        const int64_t w = Wr[e];
+        wrow[e] = w;
+        c[e] = __popc((uint32_t)e) == 1 ? (uint64_t)w << m : 0u;         // C(empty) = 0 is never a part
         spl[e] = 0u;
     }
     __syncthreads();
     const int wv = (int)(threadIdx.x / kWave), lane = (int)(threadIdx.x & (kWave - 1));
     for (int p = 2; p <= L; ++p) {
-        // one thread per subset while a subset has at most 127 candidates
-        // (each level is then one round of the workgroup), a wave per subset
-        // above; lane li of a group takes candidates li, li + G, ..., its A'
-        // stepping by a masked add of G
-        const int G = p <= 8 ? 1 : kWave;
+        // one thread per subset while a subset has at most 63 candidates,
+        // two at |S| = 8 (each level is then one round of the workgroup), a
+        // wave per subset above; lane li of a group takes candidates li,
+        // li + G, ..., its A' stepping by a masked add of G
+        const int G = p <= 7 ? 1 : p == 8 ? 2 : kWave;
         const uint32_t n_sub = (uint32_t)(c_subsets.begin[p + 1] - c_subsets.begin[p]);
         const uint32_t per_wave = (uint32_t)(kWave / G);
         const uint32_t gl = (uint32_t)(lane / G), li = (uint32_t)(lane % G);
@@ -2108,7 +2111,7 @@ __global__ __launch_bounds__(THREADS) void k_rb_row0(int m, const int64_t *__res
                 kb = o < kb ? o : kb;
             }
             if (r < n_sub && li == 0) {
-                c[S] = ((kb >> m) - (uint64_t)Wr[S]) << m;
+                c[S] = ((kb >> m) - (uint64_t)wrow[S]) << m;
                 spl[S] = (uint32_t)(kb & mask);
             }
         }
