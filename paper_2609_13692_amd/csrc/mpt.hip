@@ -917,7 +917,6 @@ constexpr bool runs_cover(const ThreadItems &t, const ItemRuns &g) {
     return true;
 }
 static_assert(runs_cover(kTItems, kItemRuns), "every lane with an item is in one run of its S2'");
-__constant__ ItemRuns c_item_runs = kItemRuns;
 
 // The combining plan. Each 16-lane quarter of a wave takes four S2' in
 // turn, lane q the entry q of each (q < 8: entry q of block S2', else entry
