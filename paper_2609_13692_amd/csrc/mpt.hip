@@ -1974,11 +1974,44 @@ __global__ __launch_bounds__(256) void k_rb_reduce(uint32_t chunks, uint32_t gro
     if (v != ~0ull) atomicMin((unsigned long long *)base, (unsigned long long)v);
 }
 
+// A row's cross-pair keys into LDS acc from its c chunk slots (the first
+// at slot; as k_rb_cross lays them out: head rows in chunks, the others in
+// tail_chunks from tail_base), by NT threads: none without chunks (level 1
+// has no cross pairs); up to kFoldChunks chunks folded here, with every
+// thread's loads in flight together (16 bytes each); more chunks were
+// folded into the first slot by k_rb_reduce, which is then copied directly.
+// Completion: copies_done, then a workgroup barrier.
+constexpr uint32_t kFoldChunks = 16;
+template <int NT>
+__device__ inline void load_row_keys(uint64_t *acc, const uint64_t *__restrict__ partial, size_t slot, uint32_t c) {
+    if (c == 0) {
+        for (int e = threadIdx.x; e < ROW; e += NT) acc[e] = ~0ull;
+    } else if (c > kFoldChunks) {
+        copy_row<uint64_t, NT>(acc, partial, (uint32_t)slot);
+    } else {
+        const ulonglong2 *src = reinterpret_cast<const ulonglong2 *>(partial + slot * ROW);
+        constexpr int PER = ROW / 2 / NT;                       // 16-byte pieces per thread
+        ulonglong2 v[PER];
+#pragma unroll
+        for (int q = 0; q < PER; ++q) v[q] = src[threadIdx.x + q * NT];
+        for (uint32_t j = 1; j < c; ++j) {
+            ulonglong2 o[PER];
+#pragma unroll
+            for (int q = 0; q < PER; ++q) o[q] = src[(size_t)j * (ROW / 2) + threadIdx.x + q * NT];
+#pragma unroll
+            for (int q = 0; q < PER; ++q) {
+                v[q].x = o[q].x < v[q].x ? o[q].x : v[q].x;
+                v[q].y = o[q].y < v[q].y ? o[q].y : v[q].y;
+            }
+        }
+        ulonglong2 *dst = reinterpret_cast<ulonglong2 *>(acc);
+#pragma unroll
+        for (int q = 0; q < PER; ++q) dst[threadIdx.x + q * NT] = v[q];
+    }
+}
+
 // finish rows row_offset + blockIdx.x of one level on 64-bit keys (narrow
-// rows: k_rb_final_narrow): acc from the reduced partials (the row's first
-// chunk slot, as k_rb_cross lays them out: head rows in chunks, the others
-// in tail_chunks from tail_base) or empty (no chunks: level 1 has no cross
-// pairs)
+// rows: k_rb_final_narrow), acc from the row's chunk slots (load_row_keys)
 template <class K>
 __global__ __launch_bounds__(THREADS) void k_rb_final(int m, int h, uint32_t row_offset, uint32_t head_rows,
                                                       uint32_t chunks, uint32_t tail_chunks, uint32_t tail_base,
@@ -1992,11 +2025,7 @@ __global__ __launch_bounds__(THREADS) void k_rb_final(int m, int h, uint32_t row
     const size_t slot = r < head_rows ? (size_t)r * chunks : tail_base + (size_t)(r - head_rows) * tail_chunks;
     OwnBlock<int64_t> own;
     own_block_load(sh, Wr, own);
-    // the reduced cross-pair keys (direct copies, all in flight together),
-    // or none
-    if (c) copy_row<uint64_t>(s.acc, partial, (uint32_t)slot);
-    else
-        for (int e = threadIdx.x; e < ROW; e += THREADS) s.acc[e] = ~0ull;
+    load_row_keys<THREADS>(s.acc, partial, slot, c);
     copy_row(s.r[0][1], Pt, 0u);
     copies_done();
     lds_barrier();
@@ -2030,11 +2059,7 @@ __global__ __launch_bounds__(FINAL_THREADS) void k_rb_final_narrow(int m, int h,
     const size_t slot = r < head_rows ? (size_t)r * chunks : tail_base + (size_t)(r - head_rows) * tail_chunks;
     OwnBlock<uint32_t> own;
     own_block_load(sh, Wr, own);
-    // the reduced cross-pair keys (direct copies, all in flight together),
-    // or none
-    if (c) copy_row<uint64_t, FINAL_THREADS>(s.acc, partial, (uint32_t)slot);
-    else
-        for (int e = threadIdx.x; e < ROW; e += FINAL_THREADS) s.acc[e] = ~0ull;
+    load_row_keys<FINAL_THREADS>(s.acc, partial, slot, c);
     copy_row<uint32_t, FINAL_THREADS>(s.nr + ROW, Pn, 0u);
     for (int e = threadIdx.x; e < ROW; e += FINAL_THREADS) s.nr[2 * ROW + e] = Key<uint32_t>::none();
     copies_done();
@@ -2569,8 +2594,10 @@ int solve_rb(int m, const int64_t *W, int64_t *C, uint32_t *split, char *ws, con
                 const uint32_t groups = (chunks - 1 + rb::RED_CHUNKS_PER_BLOCK - 1) / rb::RED_CHUNKS_PER_BLOCK;
                 rb::k_rb_reduce<<<rows * (rb::ROW / 256) * groups, 256, 0, s>>>(chunks, groups, part);
             };
-            if (!fused) reduce(head, P.chunks, partial);
-            if (P.tail_rows) reduce(P.tail_rows, P.tail_chunks, partial + (size_t)tail_base * rb::ROW);
+            // (up to kFoldChunks chunks are folded by the finishing kernel)
+            if (!fused && P.chunks > rb::kFoldChunks) reduce(head, P.chunks, partial);
+            if (P.tail_rows && P.tail_chunks > rb::kFoldChunks)
+                reduce(P.tail_rows, P.tail_chunks, partial + (size_t)tail_base * rb::ROW);
             if (!fused || P.tail_rows) {
                 const uint32_t first = fused ? head : 0u;
                 LaunchScope ls("rb_final", pair_work * (P.n_sets - first), s);
