@@ -199,7 +199,7 @@ def greedy_bench(steps: int, warmup: int, cpu: bool) -> dict:
 
 def dense_w_bench(steps: int, warmup: int) -> dict:
     """The W table's dense route (scatter into a zeroed table, then the
-    superset zeta in read-write passes of up to 11 and 5 bits) on the long-
+    superset zeta in read-write passes of 11 bits and of up to 7) on the long-
     list instance (m = 25 requests of 90000 chunks over 2^20), inputs
     resident in HBM. One step = one mpt_ctx_build_weights (demand sets,
     compaction, W). `roofline` prices the route's own table traffic (the
@@ -229,7 +229,7 @@ def dense_w_bench(steps: int, warmup: int) -> dict:
     prof = mpt.profile_end()
     ctx.close()
     dense = prof.get("weights_dense")
-    passes = 1 + max(0, -(-(m - 11) // 5))
+    passes = 1 + max(0, -(-(m - 11) // 7))        # the low 11 bits, then high passes of at most 7 bits
     route_bytes = 8 * (1 << m) * (1 + 2 * passes)
     out = {
         "workload": f"long lists: m={m} requests of 90000 chunks drawn uniformly from u={inst.n_chunks}, "

@@ -520,7 +520,54 @@ __global__ __launch_bounds__(kDenseThreads) void k_dense_zeta_high(int m, int j,
     for (int r = 0; r + 1 < (1 << K); ++r) W[s + ((int64_t)r << j)] = v[r];   // the full-set value is unchanged
 }
 
+// bits j .. j + K - 1 for K of 6 or 7 (too many values for one thread's
+// registers), over the 2^K x 16 tile of the 16 consecutive low subsets
+// s0 .. s0 + 15 (16 x 8 bytes = one 128-byte line per row): thread (c, g)
+// loads rows 2^(K-4) g .. 2^(K-4) (g + 1) - 1 of column c and adds along
+// their K - 4 low row bits in registers; the tile goes through LDS once;
+// then a thread per column and low row part adds along the 4 high row bits
+// in registers and writes back: one HBM read and write of every value for K
+// bits, one barrier
+constexpr int kTileCols = 16;
+template <int K>
+__global__ __launch_bounds__(kDenseThreads) void k_dense_zeta_tile(int j, int64_t *W) {
+    constexpr int R = 1 << K, KR = K - 4, RB = 1 << KR;
+    static_assert(R * kTileCols == kDenseThreads * RB, "one thread per column and run of RB rows");
+    __shared__ int64_t t[R][kTileCols];
+    const int64_t g0 = (int64_t)blockIdx.x * kTileCols;          // first of the tile's low subsets
+    const int64_t s0 = ((g0 >> j) << (j + K)) | (g0 & (((int64_t)1 << j) - 1));
+    const int c = (int)threadIdx.x % kTileCols, g = (int)threadIdx.x / kTileCols;
+    int64_t v[RB];
+#pragma unroll
+    for (int i = 0; i < RB; ++i) v[i] = W[s0 + c + ((int64_t)(g * RB + i) << j)];
+    zeta_reg_bits<KR>(v);
+#pragma unroll
+    for (int i = 0; i < RB; ++i) t[g * RB + i][c] = v[i];
+    __syncthreads();
+    if ((int)threadIdx.x < RB * kTileCols) {
+        const int lo = g;                                          // rows lo + 2^KR h, h < 16
+        int64_t u[16];
+#pragma unroll
+        for (int h = 0; h < 16; ++h) u[h] = t[lo + (h << KR)][c];
+        zeta_reg_bits<4>(u);
+#pragma unroll
+        for (int h = 0; h < 16; ++h) {
+            const int r = lo + (h << KR);
+            if (r != R - 1) W[s0 + c + ((int64_t)r << j)] = u[h];     // the full-set row is unchanged
+        }
+    }
+}
+
+// the high bits 11 .. m - 1 in as few passes of at most 7 bits as they
+// need, their widths as even as possible (m = 25: 7 + 7)
+constexpr int kHighPassMax = 7;
 void dense_zeta_high(int m, int j, int K, int64_t *W, hipStream_t s) {
+    if (K > kLaneRegBits) {
+        const uint32_t blocks = (uint32_t)(((int64_t)1 << (m - K)) / kTileCols);
+        if (K == 6) k_dense_zeta_tile<6><<<blocks, kDenseThreads, 0, s>>>(j, W);
+        else k_dense_zeta_tile<7><<<blocks, kDenseThreads, 0, s>>>(j, W);
+        return;
+    }
     const uint32_t blocks = (uint32_t)((((int64_t)1 << (m - K)) + kDenseThreads - 1) / kDenseThreads);
     switch (K) {
     case 1: k_dense_zeta_high<1><<<blocks, kDenseThreads, 0, s>>>(m, j, W); break;
@@ -2701,7 +2748,14 @@ int build(int m, int64_t n_chunks, int64_t nnz, const int64_t *chunk_w, const in
                           kScatterThreads, 0, s>>>(cap, list_sig, list_w, h, W);
         const int64_t waves = (n + (1 << kLowPassBits) - 1) >> kLowPassBits;
         k_dense_zeta_low<<<(uint32_t)((waves * kWave + kDenseThreads - 1) / kDenseThreads), kDenseThreads, 0, s>>>(n, W);
-        for (int j = kLowPassBits; j < m; j += kLaneRegBits) dense_zeta_high(m, j, std::min(kLaneRegBits, m - j), W, s);
+        if (m > kLowPassBits) {
+            const int hb = m - kLowPassBits, passes = (hb + kHighPassMax - 1) / kHighPassMax;
+            for (int p = 0, j = kLowPassBits; p < passes; ++p) {
+                const int K = hb / passes + (p < hb % passes ? 1 : 0);
+                dense_zeta_high(m, j, K, W, s);
+                j += K;
+            }
+        }
     }
     k_check_total<<<1, 64, 0, s>>>(m, W, h);
     MPT_HIP_TRY(hipGetLastError());

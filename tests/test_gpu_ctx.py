@@ -143,9 +143,11 @@ def routed_W(inst, route):
     return W
 
 
-# m below the 11-bit low pass, at it, one past it, and the high passes of
-# 1 .. 5 bits (the last pass is m - 11 mod 5 bits wide)
-ROUTE_MS = [1, 4, 10, 11, 12, 13, 14, 15, 16, 17, 21, 22]
+# m below the 11-bit low pass, at it, one past it, and the high passes (the
+# m - 11 high bits in passes of at most 7, as even as possible): one pass of
+# 1 .. 5 bits in registers, of 6 or 7 bits through LDS tiles, and two passes
+# of each kind and mixed (19: 4 + 4, 21: 5 + 5, 22: 6 + 5, 23: 6 + 6)
+ROUTE_MS = [1, 4, 10, 11, 12, 13, 14, 15, 16, 17, 18, 19, 21, 22, 23]
 
 
 @pytest.mark.parametrize("m", ROUTE_MS)
