@@ -2079,18 +2079,20 @@ __global__ __launch_bounds__(THREADS) void k_rb_final(int m, int h, uint32_t row
     finalize_row<K>(m, sh, own, s, s.r[0][0], s.r[0][1], Tt, Pt, Sr);
 }
 
-// k_rb_final on narrow rows, in workgroups of half the threads and half
-// the CU's LDS (the accumulator row and three narrow rows), so that two rows
-// are finished on a CU at a time: the finishing's phases are bound by
-// latency, and the two workgroups' phases overlap.
+// k_rb_final on narrow rows, in NT threads and half the CU's LDS (the
+// accumulator row and three narrow rows). With NT = FINAL_THREADS, half the
+// threads of a CU, two rows are finished on a CU at a time: the finishing's
+// phases are bound by latency, and the two workgroups' phases overlap. A
+// launch of at most one row per CU takes NT = THREADS: every row then has
+// all of its CU's threads.
 constexpr int FINAL_THREADS = THREADS / 2;
 struct alignas(16) LdsFinalNarrow {
     uint64_t acc[ROW];
     uint32_t nr[3 * ROW];      // row S_H (tagged), row 0 (plain), the self-pair minima
 };
 static_assert(2 * sizeof(LdsFinalNarrow) <= 160 * 1024, "two narrow finishing workgroups per CU");
-template <class K>
-__global__ __launch_bounds__(FINAL_THREADS) void k_rb_final_narrow(int m, int h, uint32_t row_offset,
+template <class K, int NT>
+__global__ __launch_bounds__(NT) void k_rb_final_narrow(int m, int h, uint32_t row_offset,
                                                                    uint32_t head_rows, uint32_t chunks,
                                                                    uint32_t tail_chunks, uint32_t tail_base,
                                                                    const int64_t *__restrict__ Wr,
@@ -2106,12 +2108,12 @@ __global__ __launch_bounds__(FINAL_THREADS) void k_rb_final_narrow(int m, int h,
     const size_t slot = r < head_rows ? (size_t)r * chunks : tail_base + (size_t)(r - head_rows) * tail_chunks;
     OwnBlock<uint32_t> own;
     own_block_load(sh, Wr, own);
-    load_row_keys<FINAL_THREADS>(s.acc, partial, slot, c);
-    copy_row<uint32_t, FINAL_THREADS>(s.nr + ROW, Pn, 0u);
-    for (int e = threadIdx.x; e < ROW; e += FINAL_THREADS) s.nr[2 * ROW + e] = Key<uint32_t>::none();
+    load_row_keys<NT>(s.acc, partial, slot, c);
+    copy_row<uint32_t, NT>(s.nr + ROW, Pn, 0u);
+    for (int e = threadIdx.x; e < ROW; e += NT) s.nr[2 * ROW + e] = Key<uint32_t>::none();
     copies_done();
     lds_barrier();
-    finalize_row_narrow<K, FINAL_THREADS>(m, sh, own, s.acc, s.nr, s.nr + ROW, s.nr + 2 * ROW, Pt, Tn, Pn, Sr);
+    finalize_row_narrow<K, NT>(m, sh, own, s.acc, s.nr, s.nr + ROW, s.nr + 2 * ROW, Pt, Tn, Pn, Sr);
 }
 
 // the in-row masks grouped by popcount, for the row-0 DP
@@ -2616,11 +2618,21 @@ int solve_rb(int m, const int64_t *W, int64_t *C, uint32_t *split, char *ws, con
     for (int li = 0; li < plan.n; ++li) {
         const RbLevel &P = plan.v[li];
         if (P.h == 0) continue;                               // row 0: done above
+        // narrow finishing of rows first .. first + rows - 1: a whole CU per
+        // row when the rows fit one per CU, else two rows per CU
+        auto final_narrow = [&](uint32_t rows, uint32_t first, uint32_t head, uint32_t chunks, uint32_t tail_chunks,
+                                uint32_t tail_base) {
+            if (rows <= (uint32_t)rb::CUS)
+                rb::k_rb_final_narrow<K, rb::THREADS><<<rows, rb::THREADS, 0, s>>>(
+                    m, P.h, first, head, chunks, tail_chunks, tail_base, Wr, Pt, Tn, Pn, Sr, partial);
+            else
+                rb::k_rb_final_narrow<K, rb::FINAL_THREADS><<<rows, rb::FINAL_THREADS, 0, s>>>(
+                    m, P.h, first, head, chunks, tail_chunks, tail_base, Wr, Pt, Tn, Pn, Sr, partial);
+        };
         if (P.n_pairs == 0) {
             LaunchScope ls("rb_final", pair_work * P.n_sets, s);
             if constexpr (NARROW)
-                rb::k_rb_final_narrow<K><<<P.n_sets, rb::FINAL_THREADS, 0, s>>>(m, P.h, 0u, P.n_sets, 0u, 0u, 0u, Wr,
-                                                                              Pt, Tn, Pn, Sr, partial);
+                final_narrow(P.n_sets, 0u, P.n_sets, 0u, 0u, 0u);
             else
                 rb::k_rb_final<K><<<P.n_sets, rb::THREADS, 0, s>>>(m, P.h, 0u, P.n_sets, 0u, 0u, 0u, Wr, Tt, Pt, Sr,
                                                                    partial);
@@ -2649,8 +2661,7 @@ int solve_rb(int m, const int64_t *W, int64_t *C, uint32_t *split, char *ws, con
                 const uint32_t first = fused ? head : 0u;
                 LaunchScope ls("rb_final", pair_work * (P.n_sets - first), s);
                 if constexpr (NARROW)
-                    rb::k_rb_final_narrow<K><<<P.n_sets - first, rb::FINAL_THREADS, 0, s>>>(
-                        m, P.h, first, head, P.chunks, P.tail_chunks, tail_base, Wr, Pt, Tn, Pn, Sr, partial);
+                    final_narrow(P.n_sets - first, first, head, P.chunks, P.tail_chunks, tail_base);
                 else
                     rb::k_rb_final<K><<<P.n_sets - first, rb::THREADS, 0, s>>>(
                         m, P.h, first, head, P.chunks, P.tail_chunks, tail_base, Wr, Tt, Pt, Sr, partial);
